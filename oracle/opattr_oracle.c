@@ -1,0 +1,449 @@
+/*
+ * Oracle for the trace-attribution join (test infrastructure only; see the
+ * header). Plain single-threaded C: every stage is the paper's definition
+ * written out with sorting and stacks, no blocking, fusion or reordering.
+ *
+ *   match     -- invocation-order matching, Alg. 1 (Sec. 3.3)
+ *   dedup     -- positional inheritance from the class representative (Sec. 3.7)
+ *   enclose   -- innermost enclosing range at the query point (Alg. 2, Sec. 3.5)
+ *   aggregate -- per-operator SUM / duration-weighted mean (Eq. 1) / MAX
+ *                (Sec. 3.8.1 and the counter appendix table)
+ */
+#include "opattr_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ----------------------------------------------------------------------- */
+/* small helpers                                                            */
+/* ----------------------------------------------------------------------- */
+
+typedef struct {
+  uint64_t a, b, c; /* sort key, most significant first */
+  int64_t idx;      /* last tie-break: input index */
+} key3;
+
+static int cmp_key3(const void *x, const void *y) {
+  const key3 *p = (const key3 *)x, *q = (const key3 *)y;
+  if (p->a != q->a) return p->a < q->a ? -1 : 1;
+  if (p->b != q->b) return p->b < q->b ? -1 : 1;
+  if (p->c != q->c) return p->c < q->c ? -1 : 1;
+  if (p->idx != q->idx) return p->idx < q->idx ? -1 : 1;
+  return 0;
+}
+
+static void *xcalloc(size_t n, size_t sz) { return calloc(n ? n : 1, sz); }
+
+void oref_diag_clear(oref_diag *d) { memset(d, 0, sizeof(*d)); }
+
+void oref_diag_finish(oref_diag *d, int policy) {
+  uint32_t f = d->flags;
+  int32_t s = 0;
+  if (f & OREF_F_DATA) s = OREF_ERR_DATA;
+  else if (f & OREF_F_ORDER) s = OREF_ERR_ORDER;
+  else if (f & OREF_F_LIMIT) s = OREF_ERR_LIMIT;
+  else if (f & OREF_F_NOT_NESTED) s = OREF_ERR_NOT_NESTED;
+  else if (f & OREF_F_PARTITION) s = OREF_ERR_PARTITION;
+  else if (f & OREF_F_DEDUP) s = OREF_ERR_DEDUP;
+  else if ((f & OREF_F_COUNT) && policy == OREF_STRICT) s = OREF_ERR_COUNT_MISMATCH;
+  d->status = s;
+}
+
+/* a kernel takes part in matching and dedup only if its name and partition
+   ids are in range */
+static int kernel_ok(const oref_kernels *k, const oref_dims *d, int64_t i) {
+  if (k->name_id[i] >= d->n_names) return 0;
+  if (k->part_id && d->part_rep) {
+    int32_t p = k->part_id[i];
+    if (p < -1 || (p >= 0 && (uint32_t)p >= d->n_parts)) return 0;
+  }
+  return 1;
+}
+
+static int32_t part_of(const oref_kernels *k, const oref_dims *d, int64_t i) {
+  return (k->part_id && d->part_rep) ? k->part_id[i] : -1;
+}
+
+static int rep_ok(const oref_dims *d, int32_t p) {
+  int32_t r = d->part_rep[p];
+  return r >= 0 && (uint32_t)r < d->n_parts;
+}
+
+/* Eligibility for replay: kernels outside any partition, and kernels of a
+   class representative; structural duplicates are skipped in replay
+   (Sec. 3.7). */
+static int eligible(const oref_kernels *k, const oref_dims *d, int64_t i) {
+  if (!kernel_ok(k, d, i)) return 0;
+  int32_t p = part_of(k, d, i);
+  if (p < 0) return 1;
+  return rep_ok(d, p) && d->part_rep[p] == p;
+}
+
+/* ----------------------------------------------------------------------- */
+/* Stage 1: invocation-order matching (Alg. 1, Sec. 3.3)                    */
+/* ----------------------------------------------------------------------- */
+
+int oref_match(const oref_kernels *k, const oref_profiled *p, const oref_dims *d,
+               int policy, int32_t *match, uint32_t *name_counts, oref_diag *diag) {
+  if (!k || !p || !d || !match || !diag || k->n < 0 || p->n < 0) return OREF_ERR_ARG;
+  if (k->n > 0 && (!k->seq || !k->name_id)) return OREF_ERR_ARG;
+  if (p->n > 0 && !p->name_id) return OREF_ERR_ARG;
+  if (policy < 0 || policy > 2) return OREF_ERR_ARG;
+  const int64_t T = k->n, P = p->n;
+  const uint32_t NN = d->n_names;
+
+  /* bad records: ids out of range are counted and left out */
+  for (int64_t i = 0; i < T; ++i)
+    if (!kernel_ok(k, d, i)) diag->bad_records++;
+  for (int64_t j = 0; j < P; ++j)
+    if (p->name_id[j] >= NN) diag->bad_records++;
+  if (k->part_id && d->part_rep)
+    for (uint32_t q = 0; q < d->n_parts; ++q)
+      if (!rep_ok(d, (int32_t)q)) diag->bad_records++;
+
+  /* ncu_rows[name]: profiled rows of each name in replay order, which is the
+     per-name invocation index order required by Alg. 1 */
+  int64_t *pf_cnt = xcalloc(NN, sizeof(int64_t));
+  int64_t *pf_off = xcalloc((size_t)NN + 1, sizeof(int64_t));
+  for (int64_t j = 0; j < P; ++j)
+    if (p->name_id[j] < NN) pf_cnt[p->name_id[j]]++;
+  for (uint32_t n = 0; n < NN; ++n) pf_off[n + 1] = pf_off[n] + pf_cnt[n];
+  int64_t *rows = xcalloc((size_t)pf_off[NN], sizeof(int64_t));
+  int64_t *fill = xcalloc(NN, sizeof(int64_t));
+  for (int64_t j = 0; j < P; ++j) {
+    uint32_t n = p->name_id[j];
+    if (n < NN) rows[pf_off[n] + fill[n]++] = j;
+  }
+
+  /* timeline kernels eligible for replay, in launch (seq) order */
+  key3 *ord = xcalloc((size_t)T, sizeof(key3));
+  int64_t ne = 0;
+  for (int64_t i = 0; i < T; ++i) {
+    match[i] = -1;
+    if (eligible(k, d, i)) {
+      ord[ne].a = k->seq[i];
+      ord[ne].b = ord[ne].c = 0;
+      ord[ne].idx = i;
+      ne++;
+    }
+  }
+  qsort(ord, (size_t)ne, sizeof(key3), cmp_key3);
+  /* launch ordinals must be unique */
+  for (int64_t x = 1; x < ne; ++x)
+    if (ord[x].a == ord[x - 1].a) { diag->flags |= OREF_F_ORDER; break; }
+
+  /* Alg. 1: counter[name] = invocations seen so far; the i-th invocation of a
+     name takes the i-th profiled row of that name; once the rows run out the
+     kernel gets none (warn and continue, counter not advanced) */
+  int64_t *counter = xcalloc(NN, sizeof(int64_t));
+  int64_t *tl_cnt = xcalloc(NN, sizeof(int64_t));
+  for (int64_t x = 0; x < ne; ++x) {
+    int64_t i = ord[x].idx;
+    uint32_t n = k->name_id[i];
+    tl_cnt[n]++;
+    int64_t c = counter[n];
+    if (c >= pf_cnt[n]) continue; /* invocation count mismatch: skip */
+    match[i] = (int32_t)rows[pf_off[n] + c];
+    counter[n] = c + 1;
+  }
+
+  /* count validation (Sec. 3.3 text, limitations paragraph) */
+  for (uint32_t n = 0; n < NN; ++n) {
+    if (name_counts) {
+      name_counts[2 * (size_t)n] = (uint32_t)tl_cnt[n];
+      name_counts[2 * (size_t)n + 1] = (uint32_t)pf_cnt[n];
+    }
+    if (tl_cnt[n] != pf_cnt[n]) {
+      diag->names_mismatched++;
+      diag->flags |= OREF_F_COUNT;
+      if (tl_cnt[n] > pf_cnt[n]) diag->tl_unmatched += (uint64_t)(tl_cnt[n] - pf_cnt[n]);
+      else diag->pf_unmatched += (uint64_t)(pf_cnt[n] - tl_cnt[n]);
+    }
+  }
+  /* SKIP_NAME: a name whose counts disagree gets no assignment at all */
+  if (policy == OREF_SKIP_NAME)
+    for (int64_t x = 0; x < ne; ++x) {
+      int64_t i = ord[x].idx;
+      uint32_t n = k->name_id[i];
+      if (tl_cnt[n] != pf_cnt[n]) match[i] = -1;
+    }
+  if (diag->bad_records) diag->flags |= OREF_F_DATA;
+
+  free(pf_cnt); free(pf_off); free(rows); free(fill); free(ord); free(counter);
+  free(tl_cnt);
+  return 0;
+}
+
+/* ----------------------------------------------------------------------- */
+/* Stage 2: layer dedup, positional inheritance (Sec. 3.7)                  */
+/* ----------------------------------------------------------------------- */
+
+int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
+               oref_diag *diag) {
+  if (!k || !d || !match || !diag || k->n < 0) return OREF_ERR_ARG;
+  if (!k->part_id || !d->part_rep) return 0; /* no partitions: nothing to do */
+  const int64_t T = k->n;
+  const uint32_t NP = d->n_parts;
+
+  /* members[p]: the kernels of partition p in launch order */
+  int64_t *cnt = xcalloc(NP, sizeof(int64_t));
+  int64_t *off = xcalloc((size_t)NP + 1, sizeof(int64_t));
+  for (int64_t i = 0; i < T; ++i)
+    if (kernel_ok(k, d, i) && k->part_id[i] >= 0) cnt[k->part_id[i]]++;
+  for (uint32_t q = 0; q < NP; ++q) off[q + 1] = off[q] + cnt[q];
+  key3 *mem = xcalloc((size_t)off[NP], sizeof(key3));
+  int64_t *fill = xcalloc(NP, sizeof(int64_t));
+  for (int64_t i = 0; i < T; ++i) {
+    if (!kernel_ok(k, d, i) || k->part_id[i] < 0) continue;
+    int32_t q = k->part_id[i];
+    key3 *e = &mem[off[q] + fill[q]++];
+    e->a = (uint64_t)q;
+    e->b = k->seq[i];
+    e->c = 0;
+    e->idx = i;
+  }
+  qsort(mem, (size_t)off[NP], sizeof(key3), cmp_key3); /* by (partition, seq) */
+
+  /* a partition is the run of launches between its tags: its ordinals must
+     form one contiguous interval */
+  char *contig = xcalloc(NP, 1);
+  for (uint32_t q = 0; q < NP; ++q) {
+    if (cnt[q] == 0) { contig[q] = 1; continue; }
+    uint64_t lo = mem[off[q]].b, hi = mem[off[q + 1] - 1].b;
+    contig[q] = (hi - lo + 1 == (uint64_t)cnt[q]);
+    if (!contig[q]) diag->flags |= OREF_F_PARTITION;
+  }
+
+  /* every duplicate takes the match of the representative's kernel at the same
+     position of its partition; the position must exist and hold the same
+     kernel name, otherwise the duplicate stays unmatched */
+  for (uint32_t q = 0; q < NP; ++q) {
+    if (!rep_ok(d, (int32_t)q)) continue;
+    int32_t r = d->part_rep[q];
+    if (r == (int32_t)q) continue; /* representative itself */
+    int bad_class = !contig[q] || !rep_ok(d, r) || d->part_rep[r] != r || cnt[r] == 0 ||
+                    !contig[r];
+    for (int64_t pos = 0; pos < cnt[q]; ++pos) {
+      int64_t i = mem[off[q] + pos].idx;
+      int ok = !bad_class && pos < cnt[r];
+      if (ok) {
+        int64_t src = mem[off[r] + pos].idx;
+        ok = k->name_id[src] == k->name_id[i];
+        if (ok) match[i] = match[src];
+      }
+      if (!ok) { match[i] = -1; diag->dedup_errors++; }
+    }
+  }
+  if (diag->dedup_errors) diag->flags |= OREF_F_DEDUP;
+  free(cnt); free(off); free(mem); free(fill); free(contig);
+  return 0;
+}
+
+/* ----------------------------------------------------------------------- */
+/* Stage 3: enclosure (Alg. 2, Sec. 3.5)                                    */
+/* ----------------------------------------------------------------------- */
+
+static int range_ok(const oref_ranges *r, const oref_dims *d, int64_t x) {
+  return r->stream_id[x] < d->n_streams && r->op_id[x] < d->n_ops &&
+         r->start_ns[x] <= r->end_ns[x];
+}
+
+int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,
+                 int32_t *range_id, uint8_t *range_depth, oref_diag *diag) {
+  if (!k || !r || !d || !range_id || !diag || k->n < 0 || r->n < 0) return OREF_ERR_ARG;
+  if (k->n > 0 && (!k->stream_id || !(k->query_ns || k->start_ns))) return OREF_ERR_ARG;
+  const int64_t T = k->n, R = r->n;
+  const uint32_t NS = d->n_streams;
+  const uint64_t *q = k->query_ns ? k->query_ns : k->start_ns;
+
+  for (int64_t x = 0; x < R; ++x)
+    if (!range_ok(r, d, x)) diag->bad_records++;
+  for (int64_t i = 0; i < T; ++i)
+    if (k->stream_id[i] >= NS) diag->bad_records++;
+  if (diag->bad_records) diag->flags |= OREF_F_DATA;
+  if (range_depth)
+    for (int64_t x = 0; x < R; ++x) range_depth[x] = 0;
+
+  /* ranges in nesting order per stream: (stream, start asc, end desc, index
+     asc); an identical interval with a lower index is the outer one */
+  key3 *rs = xcalloc((size_t)R, sizeof(key3));
+  int64_t nr = 0;
+  for (int64_t x = 0; x < R; ++x) {
+    if (!range_ok(r, d, x)) continue;
+    rs[nr].a = r->stream_id[x];
+    rs[nr].b = r->start_ns[x];
+    rs[nr].c = UINT64_MAX - r->end_ns[x];
+    rs[nr].idx = x;
+    nr++;
+  }
+  qsort(rs, (size_t)nr, sizeof(key3), cmp_key3);
+  /* kernels per stream by query point */
+  key3 *ks = xcalloc((size_t)T, sizeof(key3));
+  int64_t nk = 0;
+  for (int64_t i = 0; i < T; ++i) {
+    range_id[i] = -1;
+    if (k->stream_id[i] >= NS) continue;
+    ks[nk].a = k->stream_id[i];
+    ks[nk].b = q[i];
+    ks[nk].c = 0;
+    ks[nk].idx = i;
+    nk++;
+  }
+  qsort(ks, (size_t)nk, sizeof(key3), cmp_key3);
+
+  int64_t *stack = xcalloc((size_t)nr + 1, sizeof(int64_t));
+  uint32_t *depth = xcalloc((size_t)R, sizeof(uint32_t));
+  int64_t a = 0, b = 0; /* cursors into rs and ks */
+  while (a < nr || b < nk) {
+    uint64_t s = a < nr ? rs[a].a : UINT64_MAX;
+    if (b < nk && ks[b].a < s) s = ks[b].a;
+    int64_t a_end = a, b_end = b;
+    while (a_end < nr && rs[a_end].a == s) a_end++;
+    while (b_end < nk && ks[b_end].a == s) b_end++;
+
+    /* depth: 1 + depth of the nearest earlier range (nesting order) whose end
+       is not before this one's end -- that range contains it */
+    int64_t top = 0;
+    for (int64_t x = a; x < a_end; ++x) {
+      int64_t id = rs[x].idx;
+      while (top > 0 && r->end_ns[stack[top - 1]] < r->end_ns[id]) top--;
+      depth[id] = top > 0 ? depth[stack[top - 1]] + 1 : 1;
+      if (depth[id] > 255) diag->flags |= OREF_F_LIMIT;
+      if (range_depth) range_depth[id] = (uint8_t)(depth[id] > 255 ? 255 : depth[id]);
+      stack[top++] = id;
+    }
+    /* proper nesting: no two ranges with s_A < s_B < e_A < e_B. Walking in
+       nesting order, after dropping ranges that end at or before s_B the top
+       has the smallest end of those still open at s_B; B crosses one of them
+       exactly when it crosses the top. */
+    top = 0;
+    int crossed = 0;
+    for (int64_t x = a; x < a_end; ++x) {
+      int64_t id = rs[x].idx;
+      while (top > 0 && r->end_ns[stack[top - 1]] <= r->start_ns[id]) top--;
+      if (top > 0 && r->end_ns[stack[top - 1]] < r->end_ns[id]) crossed = 1;
+      stack[top++] = id;
+    }
+    if (crossed) { diag->nesting_errors++; diag->flags |= OREF_F_NOT_NESTED; }
+
+    /* sweep: for each kernel in query order, push every range that has
+       started (s <= T), drop finished ones from the top (e < T); the top is
+       the last range in nesting order with s <= T <= e, i.e. the innermost
+       enclosing range */
+    top = 0;
+    int64_t x = a;
+    for (int64_t y = b; y < b_end; ++y) {
+      uint64_t t = ks[y].b;
+      while (x < a_end && rs[x].b <= t) stack[top++] = rs[x++].idx;
+      while (top > 0 && r->end_ns[stack[top - 1]] < t) top--;
+      range_id[ks[y].idx] = top > 0 ? (int32_t)stack[top - 1] : -1;
+    }
+    a = a_end;
+    b = b_end;
+  }
+  free(rs); free(ks); free(stack); free(depth);
+  return 0;
+}
+
+/* ----------------------------------------------------------------------- */
+/* Stage 4: per-operator aggregation (Eq. 1, Sec. 3.8.1)                    */
+/* ----------------------------------------------------------------------- */
+
+/* compensated (Neumaier) summation keeps the oracle's sum within a few ulps of
+   the exact sum at ten million terms */
+typedef struct { double s, c; } nsum;
+static void nadd(nsum *a, double x) {
+  double t = a->s + x;
+  if (fabs(a->s) >= fabs(x)) a->c += (a->s - t) + x;
+  else a->c += (x - t) + a->s;
+  a->s = t;
+}
+
+static const uint8_t DEFAULT_KIND[OREF_NC] = {
+    /* counter appendix table, rows 1..20 */
+    OREF_SUM, OREF_SUM, OREF_SUM, OREF_DWMEAN, OREF_DWMEAN, OREF_DWMEAN, OREF_DWMEAN,
+    OREF_DWMEAN, OREF_DWMEAN, OREF_DWMEAN, OREF_SUM, OREF_DWMEAN, OREF_DWMEAN,
+    OREF_DWMEAN, OREF_SUM, OREF_DWMEAN, OREF_DWMEAN, OREF_MAX, OREF_SUM, OREF_MAX};
+
+int oref_aggregate(const oref_kernels *k, const oref_profiled *p,
+                   const int32_t *match, const int32_t *range_id,
+                   const oref_ranges *r, const oref_dims *d, const uint8_t *agg_kind,
+                   oref_row *table, oref_summary *sum, oref_diag *diag) {
+  if (!k || !p || !match || !range_id || !r || !d || !table || !sum || !diag) return OREF_ERR_ARG;
+  if (k->n < 0 || (k->n > 0 && !k->dur_ns)) return OREF_ERR_ARG;
+  const uint8_t *kind = agg_kind ? agg_kind : DEFAULT_KIND;
+  for (int c = 0; c < OREF_NC; ++c)
+    if (kind[c] > OREF_MAX) return OREF_ERR_ARG;
+  const int64_t T = k->n;
+  const uint32_t G = d->n_ops + 1; /* row n_ops is UNATTRIBUTED */
+  nsum *acc = xcalloc((size_t)G * OREF_NC, sizeof(nsum));
+  double *mx = xcalloc((size_t)G * OREF_NC, sizeof(double));
+  for (size_t x = 0; x < (size_t)G * OREF_NC; ++x) mx[x] = -INFINITY;
+  memset(table, 0, sizeof(oref_row) * G);
+
+  for (int64_t i = 0; i < T; ++i) {
+    int32_t rid = range_id[i];
+    uint32_t g = d->n_ops;
+    if (rid >= 0 && rid < r->n && r->op_id[rid] < d->n_ops) g = r->op_id[rid];
+    else if (rid < -1 || rid >= r->n || (rid >= 0 && r->op_id[rid] >= d->n_ops))
+      diag->bad_records++;
+    oref_row *row = &table[g];
+    uint64_t dur = k->dur_ns[i];
+    row->kernel_count++;
+    row->total_ns += dur; /* nsys durations, not replay time (Sec. 3.2) */
+    int32_t m = match[i];
+    if (m < -1 || m >= p->n) { diag->bad_records++; continue; }
+    if (m < 0) continue; /* unmatched kernels carry no counters */
+    row->matched_count++;
+    row->matched_ns += dur;
+    for (int c = 0; c < OREF_NC; ++c) {
+      double v = (double)p->counters[(int64_t)m * p->row_stride + (int64_t)c * p->col_stride];
+      size_t x = (size_t)g * OREF_NC + c;
+      if (kind[c] == OREF_DWMEAN) nadd(&acc[x], v * (double)dur); /* m_i * d_i */
+      else if (kind[c] == OREF_SUM) nadd(&acc[x], v);
+      else if (isnan(v) || v > mx[x]) mx[x] = v;
+    }
+  }
+  if (diag->bad_records) diag->flags |= OREF_F_DATA;
+
+  memset(sum, 0, sizeof(*sum));
+  for (uint32_t g = 0; g < G; ++g) {
+    oref_row *row = &table[g];
+    for (int c = 0; c < OREF_NC; ++c) {
+      size_t x = (size_t)g * OREF_NC + c;
+      double v;
+      if (((p->absent_mask >> c) & 1u) || row->matched_count == 0) v = NAN;
+      else if (kind[c] == OREF_DWMEAN)
+        v = row->matched_ns ? (acc[x].s + acc[x].c) / (double)row->matched_ns : NAN;
+      else if (kind[c] == OREF_SUM) v = acc[x].s + acc[x].c;
+      else v = mx[x];
+      row->value[c] = v;
+    }
+    sum->total_ns += row->total_ns;
+    sum->matched_ns += row->matched_ns;
+    if (g < d->n_ops) sum->attributed_ns += row->total_ns;
+    else sum->unattributed_ns += row->total_ns;
+  }
+  sum->attributed_fraction =
+      sum->total_ns ? (double)sum->attributed_ns / (double)sum->total_ns : NAN;
+  free(acc); free(mx);
+  return 0;
+}
+
+int oref_attribute(const oref_kernels *k, const oref_profiled *p,
+                   const oref_ranges *r, const oref_dims *d, int policy,
+                   const uint8_t *agg_kind, int32_t *match, int32_t *range_id,
+                   uint8_t *range_depth, uint32_t *name_counts, oref_row *table,
+                   oref_summary *sum, oref_diag *diag) {
+  int rc = oref_match(k, p, d, policy, match, name_counts, diag);
+  if (rc) return rc;
+  rc = oref_dedup(k, d, match, diag);
+  if (rc) return rc;
+  rc = oref_enclose(k, r, d, range_id, range_depth, diag);
+  if (rc) return rc;
+  rc = oref_aggregate(k, p, match, range_id, r, d, agg_kind, table, sum, diag);
+  if (rc) return rc;
+  oref_diag_finish(diag, policy);
+  return 0;
+}

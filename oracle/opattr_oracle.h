@@ -1,0 +1,121 @@
+/*
+ * Oracle for the trace-attribution join: a plain, single-threaded CPU
+ * implementation of what the join computes, written from the paper
+ * ("Hardware-Attributed Operator Profiling for PyTorch").
+ *
+ * TEST INFRASTRUCTURE ONLY. Only the test-suite, the package smoke check and
+ * the benchmark's CPU-baseline leg may load this library. It shares no code,
+ * header, table or helper with the GPU library.
+ *
+ * All pointers are host pointers. Every array is indexed by input position.
+ * Functions return 0, or a negative value for an argument error.
+ */
+#ifndef OPATTR_ORACLE_H
+#define OPATTR_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OREF_NC 20 /* the 20-counter set of the counter appendix table */
+
+/* one timeline kernel record per index (nsys KernelRow, Alg. 1) */
+typedef struct {
+  int64_t n;
+  const uint32_t *seq;      /* launch ordinal (CUPTI correlation order)          */
+  const uint64_t *start_ns; /* GPU start time                                     */
+  const uint32_t *dur_ns;   /* duration, the weight d_i of Eq. 1                  */
+  const uint16_t *stream_id;
+  const uint32_t *name_id;
+  const int32_t *part_id;   /* layer partition instance, -1 none; NULL = none     */
+  const uint64_t *query_ns; /* enclosure query point; NULL = start_ns             */
+} oref_kernels;
+
+/* profiled counter rows (ncu NcuRow), in replay order */
+typedef struct {
+  int64_t n;
+  const uint32_t *name_id;
+  const float *counters; /* value of counter c of row j at counters[j*rs + c*cs] */
+  int64_t row_stride, col_stride;
+  uint32_t absent_mask;  /* bit c: counter c absent for the whole capture        */
+} oref_profiled;
+
+/* operator ranges: closed intervals [start, end] on a stream (Alg. 2) */
+typedef struct {
+  int64_t n;
+  const uint64_t *start_ns, *end_ns;
+  const uint16_t *stream_id;
+  const uint32_t *op_id;
+} oref_ranges;
+
+typedef struct {
+  uint32_t n_names, n_streams, n_ops, n_parts;
+  const int32_t *part_rep; /* class representative of each partition; NULL = no dedup */
+} oref_dims;
+
+typedef struct {
+  uint64_t kernel_count, total_ns, matched_count, matched_ns;
+  double value[OREF_NC];
+} oref_row;
+
+typedef struct {
+  uint64_t total_ns, attributed_ns, unattributed_ns, matched_ns;
+  double attributed_fraction;
+} oref_summary;
+
+/* error classes, as bits of oref_diag.flags */
+#define OREF_F_DATA 1u       /* an id out of range, or a range with start > end  */
+#define OREF_F_ORDER 2u      /* duplicate launch ordinal                          */
+#define OREF_F_LIMIT 4u      /* nesting deeper than 255                           */
+#define OREF_F_NOT_NESTED 8u /* two ranges of a stream cross                      */
+#define OREF_F_PARTITION 16u /* a partition is not one contiguous run of seq      */
+#define OREF_F_DEDUP 32u     /* positional inheritance failed for some duplicate  */
+#define OREF_F_COUNT 64u     /* per-name invocation counts differ                 */
+
+/* status codes (highest precedence first when several classes are flagged) */
+#define OREF_ERR_DATA (-9)
+#define OREF_ERR_ORDER (-8)
+#define OREF_ERR_LIMIT (-10)
+#define OREF_ERR_NOT_NESTED (-5)
+#define OREF_ERR_PARTITION (-7)
+#define OREF_ERR_DEDUP (-6)
+#define OREF_ERR_COUNT_MISMATCH (-4)
+#define OREF_ERR_ARG (-1)
+
+enum { OREF_PREFIX = 0, OREF_SKIP_NAME = 1, OREF_STRICT = 2 };
+enum { OREF_SUM = 0, OREF_DWMEAN = 1, OREF_MAX = 2 };
+
+typedef struct {
+  int32_t status;
+  uint32_t flags;
+  uint32_t names_mismatched;
+  uint32_t nesting_errors; /* streams whose ranges are not properly nested */
+  uint64_t tl_unmatched, pf_unmatched, dedup_errors, bad_records;
+} oref_diag;
+
+void oref_diag_clear(oref_diag *d);
+/* derive d->status from d->flags (STRICT makes COUNT an error) */
+void oref_diag_finish(oref_diag *d, int policy);
+
+int oref_match(const oref_kernels *k, const oref_profiled *p, const oref_dims *d,
+               int policy, int32_t *match, uint32_t *name_counts, oref_diag *diag);
+int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
+               oref_diag *diag);
+int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,
+                 int32_t *range_id, uint8_t *range_depth, oref_diag *diag);
+int oref_aggregate(const oref_kernels *k, const oref_profiled *p,
+                   const int32_t *match, const int32_t *range_id,
+                   const oref_ranges *r, const oref_dims *d, const uint8_t *agg_kind,
+                   oref_row *table, oref_summary *sum, oref_diag *diag);
+/* the four stages in order: match, dedup, enclose, aggregate */
+int oref_attribute(const oref_kernels *k, const oref_profiled *p,
+                   const oref_ranges *r, const oref_dims *d, int policy,
+                   const uint8_t *agg_kind, int32_t *match, int32_t *range_id,
+                   uint8_t *range_depth, uint32_t *name_counts, oref_row *table,
+                   oref_summary *sum, oref_diag *diag);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

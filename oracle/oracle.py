@@ -1,0 +1,222 @@
+"""Python wrapper of the C oracle (test infrastructure only).
+
+Only the test-suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this module. It loads ``oracle/_build/liboracle.so``,
+built from ``opattr_oracle.c`` by :func:`build` (plain gcc, one thread), and
+shares nothing with the GPU library.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "opattr_oracle.c")
+HDR = os.path.join(HERE, "opattr_oracle.h")
+OUT_DIR = os.path.join(HERE, "_build")
+LIB = os.path.join(OUT_DIR, "liboracle.so")
+
+NC = 20
+PREFIX, SKIP_NAME, STRICT = 0, 1, 2
+SUM, DWMEAN, MAX = 0, 1, 2
+# counter appendix table (rows 1..20): SUM for additive counts, duration-weighted
+# mean for rates and utilisations, MAX for per-kernel constants
+DEFAULT_KIND = np.array([SUM, SUM, SUM, DWMEAN, DWMEAN, DWMEAN, DWMEAN, DWMEAN, DWMEAN,
+                         DWMEAN, SUM, DWMEAN, DWMEAN, DWMEAN, SUM, DWMEAN, DWMEAN, MAX,
+                         SUM, MAX], dtype=np.uint8)
+
+F_DATA, F_ORDER, F_LIMIT, F_NOT_NESTED, F_PARTITION, F_DEDUP, F_COUNT = (
+    1, 2, 4, 8, 16, 32, 64)
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (single-threaded, no fast-math, no FMA
+    contraction, so every product is rounded once)."""
+    os.makedirs(OUT_DIR, exist_ok=True)
+    if not force and os.path.exists(LIB) and \
+            os.path.getmtime(LIB) >= max(os.path.getmtime(SRC), os.path.getmtime(HDR)):
+        return LIB
+    tmp = LIB + ".tmp"
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
+           "-fno-fast-math", "-Wall", "-Wextra", "-o", tmp, SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+class Kernels(C.Structure):
+    _fields_ = [("n", C.c_int64), ("seq", C.c_void_p), ("start_ns", C.c_void_p),
+                ("dur_ns", C.c_void_p), ("stream_id", C.c_void_p),
+                ("name_id", C.c_void_p), ("part_id", C.c_void_p),
+                ("query_ns", C.c_void_p)]
+
+
+class Profiled(C.Structure):
+    _fields_ = [("n", C.c_int64), ("name_id", C.c_void_p), ("counters", C.c_void_p),
+                ("row_stride", C.c_int64), ("col_stride", C.c_int64),
+                ("absent_mask", C.c_uint32)]
+
+
+class Ranges(C.Structure):
+    _fields_ = [("n", C.c_int64), ("start_ns", C.c_void_p), ("end_ns", C.c_void_p),
+                ("stream_id", C.c_void_p), ("op_id", C.c_void_p)]
+
+
+class Dims(C.Structure):
+    _fields_ = [("n_names", C.c_uint32), ("n_streams", C.c_uint32),
+                ("n_ops", C.c_uint32), ("n_parts", C.c_uint32), ("part_rep", C.c_void_p)]
+
+
+class Diag(C.Structure):
+    _fields_ = [("status", C.c_int32), ("flags", C.c_uint32),
+                ("names_mismatched", C.c_uint32), ("nesting_errors", C.c_uint32),
+                ("tl_unmatched", C.c_uint64), ("pf_unmatched", C.c_uint64),
+                ("dedup_errors", C.c_uint64), ("bad_records", C.c_uint64)]
+
+
+class Summary(C.Structure):
+    _fields_ = [("total_ns", C.c_uint64), ("attributed_ns", C.c_uint64),
+                ("unattributed_ns", C.c_uint64), ("matched_ns", C.c_uint64),
+                ("attributed_fraction", C.c_double)]
+
+
+ROW_DTYPE = np.dtype([("kernel_count", "<u8"), ("total_ns", "<u8"),
+                      ("matched_count", "<u8"), ("matched_ns", "<u8"),
+                      ("value", "<f8", (NC,))])
+
+_lib = None
+
+
+def load(path: str):
+    """Load an oracle library built from opattr_oracle.c and declare its
+    entry points."""
+    L = C.CDLL(path)
+    P = C.POINTER
+    L.oref_match.argtypes = [P(Kernels), P(Profiled), P(Dims), C.c_int, C.c_void_p,
+                             C.c_void_p, P(Diag)]
+    L.oref_dedup.argtypes = [P(Kernels), P(Dims), C.c_void_p, P(Diag)]
+    L.oref_enclose.argtypes = [P(Kernels), P(Ranges), P(Dims), C.c_void_p, C.c_void_p,
+                               P(Diag)]
+    L.oref_aggregate.argtypes = [P(Kernels), P(Profiled), C.c_void_p, C.c_void_p,
+                                 P(Ranges), P(Dims), C.c_void_p, C.c_void_p,
+                                 P(Summary), P(Diag)]
+    L.oref_diag_finish.argtypes = [P(Diag), C.c_int]
+    for f in ("oref_match", "oref_dedup", "oref_enclose", "oref_aggregate"):
+        getattr(L, f).restype = C.c_int
+    return L
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            build()
+        _lib = load(LIB)
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _c(a, dt):
+    return None if a is None else np.ascontiguousarray(a, dtype=dt)
+
+
+class _Inputs:
+    """Contiguous, correctly typed views of a trace dict, kept alive with the
+    ctypes structs that point into them."""
+
+    def __init__(self, tr, absent_mask=0):
+        self.seq = _c(tr["seq"], np.uint32)
+        self.start = _c(tr["start_ns"], np.uint64)
+        self.dur = _c(tr["dur_ns"], np.uint32)
+        self.stream = _c(tr["stream_id"], np.uint16)
+        self.name = _c(tr["name_id"], np.uint32)
+        self.part = _c(tr.get("part_id"), np.int32)
+        self.query = _c(tr.get("query_ns"), np.uint64)
+        self.pf_name = _c(tr["pf_name"], np.uint32)
+        cnt = tr["counters"]
+        if cnt.dtype != np.float32:
+            raise TypeError("counters must be float32")
+        self.counters = cnt  # arbitrary strides honoured
+        self.r_start = _c(tr["r_start"], np.uint64)
+        self.r_end = _c(tr["r_end"], np.uint64)
+        self.r_stream = _c(tr["r_stream"], np.uint16)
+        self.r_op = _c(tr["r_op"], np.uint32)
+        self.part_rep = _c(tr.get("part_rep"), np.int32)
+        T = self.seq.size
+        self.k = Kernels(T, _ptr(self.seq), _ptr(self.start), _ptr(self.dur),
+                         _ptr(self.stream), _ptr(self.name), _ptr(self.part),
+                         _ptr(self.query))
+        P = self.pf_name.size
+        rs = cnt.strides[0] // 4 if cnt.ndim == 2 and P > 0 else NC
+        cs = cnt.strides[1] // 4 if cnt.ndim == 2 and P > 0 else 1
+        self.p = Profiled(P, _ptr(self.pf_name), cnt.ctypes.data if P > 0 else None,
+                          rs, cs, absent_mask)
+        self.r = Ranges(self.r_start.size, _ptr(self.r_start), _ptr(self.r_end),
+                        _ptr(self.r_stream), _ptr(self.r_op))
+        self.d = Dims(tr["n_names"], tr["n_streams"], tr["n_ops"],
+                      tr.get("n_parts", 0) or 0, _ptr(self.part_rep))
+
+
+def diag_dict(dg: Diag) -> dict:
+    return {f: int(getattr(dg, f)) for f, _ in Diag._fields_}
+
+
+def attribute(tr, policy=PREFIX, agg_kind=None, absent_mask=0, stages=None, library=None):
+    """Run the oracle on a trace dict. ``stages`` (default all) is a subset of
+    {"match", "dedup", "enclose", "aggregate"}; stages not run leave their
+    outputs as provided in ``tr`` ("match", "range_id") or absent. ``library``
+    replaces the default build (used to load deliberately broken copies)."""
+    L = library if library is not None else lib()
+    x = _Inputs(tr, absent_mask)
+    stages = {"match", "dedup", "enclose", "aggregate"} if stages is None else set(stages)
+    T = x.seq.size
+    out = {}
+    dg = Diag()
+    if "match" in stages:
+        match = np.empty(T, dtype=np.int32)
+        nc = np.empty((tr["n_names"], 2), dtype=np.uint32)
+        rc = L.oref_match(C.byref(x.k), C.byref(x.p), C.byref(x.d), policy,
+                          _ptr(match), _ptr(nc), C.byref(dg))
+        if rc:
+            raise ValueError(f"oref_match: {rc}")
+        out["match_iom"] = match.copy()
+        out["name_counts"] = nc
+    else:
+        match = np.array(tr["match"], dtype=np.int32, copy=True)
+    if "dedup" in stages:
+        rc = L.oref_dedup(C.byref(x.k), C.byref(x.d), _ptr(match), C.byref(dg))
+        if rc:
+            raise ValueError(f"oref_dedup: {rc}")
+    out["match"] = match
+    if "enclose" in stages:
+        rid = np.empty(T, dtype=np.int32)
+        depth = np.empty(x.r_start.size, dtype=np.uint8)
+        rc = L.oref_enclose(C.byref(x.k), C.byref(x.r), C.byref(x.d), _ptr(rid),
+                            _ptr(depth), C.byref(dg))
+        if rc:
+            raise ValueError(f"oref_enclose: {rc}")
+        out["range_id"] = rid
+        out["range_depth"] = depth
+    else:
+        rid = np.array(tr["range_id"], dtype=np.int32, copy=True) if "range_id" in tr else None
+    if "aggregate" in stages:
+        rid_in = out.get("range_id", rid)
+        table = np.zeros(tr["n_ops"] + 1, dtype=ROW_DTYPE)
+        sm = Summary()
+        kind = None if agg_kind is None else np.ascontiguousarray(agg_kind, dtype=np.uint8)
+        rc = L.oref_aggregate(C.byref(x.k), C.byref(x.p), _ptr(match), _ptr(rid_in),
+                              C.byref(x.r), C.byref(x.d), _ptr(kind), _ptr(table),
+                              C.byref(sm), C.byref(dg))
+        if rc:
+            raise ValueError(f"oref_aggregate: {rc}")
+        out["table"] = table
+        out["summary"] = {f: getattr(sm, f) for f, _ in Summary._fields_}
+    L.oref_diag_finish(C.byref(dg), policy)
+    out["diag"] = diag_dict(dg)
+    return out

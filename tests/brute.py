@@ -1,0 +1,192 @@
+"""Brute-force restatements of the join's definitions, for tiny inputs only.
+
+Each function recomputes a stage from its definition by exhaustive search,
+without sorting tricks, stacks or sweeps, so that it shares no algorithm with
+the oracle it checks.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+NC = 20
+SUM, DWMEAN, MAX = 0, 1, 2
+DEFAULT_KIND = [SUM, SUM, SUM, DWMEAN, DWMEAN, DWMEAN, DWMEAN, DWMEAN, DWMEAN, DWMEAN,
+                SUM, DWMEAN, DWMEAN, DWMEAN, SUM, DWMEAN, DWMEAN, MAX, SUM, MAX]
+
+
+def eligible(tr, i):
+    part = tr.get("part_id")
+    if part is None or tr.get("part_rep") is None:
+        return True
+    p = int(part[i])
+    return p < 0 or int(tr["part_rep"][p]) == p
+
+
+def iom(tr, policy=0):
+    """match[i] = the profiled row of the same name whose replay ordinal equals
+    the number of earlier (by seq) eligible launches of that name."""
+    T = tr["seq"].size
+    name, seq, pf = tr["name_id"], tr["seq"], tr["pf_name"]
+    match = np.full(T, -1, dtype=np.int64)
+    tl = {}
+    pfc = {}
+    for n in pf.tolist():
+        pfc[n] = pfc.get(n, 0) + 1
+    for i in range(T):
+        if eligible(tr, i):
+            tl[int(name[i])] = tl.get(int(name[i]), 0) + 1
+    for i in range(T):
+        if not eligible(tr, i):
+            continue
+        n = int(name[i])
+        rank = sum(1 for j in range(T)
+                   if j != i and eligible(tr, j) and name[j] == n and seq[j] < seq[i])
+        rows = [j for j in range(pf.size) if pf[j] == n]
+        if rank < len(rows):
+            match[i] = rows[rank]
+        if policy == 1 and tl.get(n, 0) != pfc.get(n, 0):
+            match[i] = -1
+    return match
+
+
+def dedup(tr, match):
+    """Duplicates take the match of the representative's kernel at the same
+    launch-order position of their partition (name must agree)."""
+    part, rep = tr.get("part_id"), tr.get("part_rep")
+    out = match.copy()
+    errors = 0
+    if part is None or rep is None:
+        return out, errors
+    T = part.size
+    seq, name = tr["seq"], tr["name_id"]
+
+    def members(p):
+        return sorted([i for i in range(T) if part[i] == p], key=lambda i: int(seq[i]))
+
+    for i in range(T):
+        p = int(part[i])
+        if p < 0 or int(rep[p]) == p:
+            continue
+        r = int(rep[p])
+        mp, mr = members(p), members(r)
+        pos = mp.index(i)
+        if int(rep[r]) == r and pos < len(mr) and name[mr[pos]] == name[i]:
+            out[i] = match[mr[pos]]
+        else:
+            out[i] = -1
+            errors += 1
+    return out, errors
+
+
+def enclose(tr):
+    """range_id[i] = argmax over ranges r on kernel i's stream with
+    s_r <= q_i <= e_r of (s_r, -e_r, r); -1 if none."""
+    T = tr["seq"].size
+    q = tr.get("query_ns")
+    q = tr["start_ns"] if q is None else q
+    rs, re, rst = tr["r_start"], tr["r_end"], tr["r_stream"]
+    out = np.full(T, -1, dtype=np.int64)
+    for i in range(T):
+        best = None
+        for r in range(rs.size):
+            if rst[r] == tr["stream_id"][i] and rs[r] <= q[i] <= re[r]:
+                key = (int(rs[r]), -int(re[r]), r)
+                if best is None or key > best:
+                    best = key
+        if best is not None:
+            out[i] = best[2]
+    return out
+
+
+def nesting_before(tr, a, b):
+    """True if range a precedes range b in nesting order (start asc, end desc,
+    index asc)."""
+    ka = (int(tr["r_start"][a]), -int(tr["r_end"][a]), a)
+    kb = (int(tr["r_start"][b]), -int(tr["r_end"][b]), b)
+    return ka < kb
+
+
+def depth(tr):
+    """1 + depth of the nearest range earlier in nesting order on the same
+    stream whose end is not before this range's end (it contains this one)."""
+    R = tr["r_start"].size
+    order = sorted(range(R), key=lambda r: (int(tr["r_stream"][r]), int(tr["r_start"][r]),
+                                            -int(tr["r_end"][r]), r))
+    d = {}
+    for pos, r in enumerate(order):
+        par = None
+        for q in reversed(order[:pos]):
+            if tr["r_stream"][q] != tr["r_stream"][r]:
+                break
+            if tr["r_end"][q] >= tr["r_end"][r]:
+                par = q
+                break
+        d[r] = 1 if par is None else d[par] + 1
+    return np.array([d[r] for r in range(R)], dtype=np.int64)
+
+
+def containers(tr):
+    """Number of ranges containing each range (itself included), identical
+    intervals nesting in index order."""
+    R = tr["r_start"].size
+    out = np.zeros(R, dtype=np.int64)
+    for r in range(R):
+        for a in range(R):
+            if tr["r_stream"][a] != tr["r_stream"][r]:
+                continue
+            if tr["r_start"][a] <= tr["r_start"][r] and tr["r_end"][a] >= tr["r_end"][r] \
+                    and (a == r or nesting_before(tr, a, r)):
+                out[r] += 1
+    return out
+
+
+def crossing_streams(tr):
+    """Streams holding two ranges with s_A < s_B < e_A < e_B."""
+    R = tr["r_start"].size
+    bad = set()
+    s, e, st = tr["r_start"], tr["r_end"], tr["r_stream"]
+    for a in range(R):
+        for b in range(R):
+            if st[a] == st[b] and s[a] < s[b] < e[a] < e[b]:
+                bad.add(int(st[a]))
+    return bad
+
+
+def aggregate(tr, match, range_id, agg_kind=None, absent_mask=0):
+    """Per operator: counts and ns sums, and per counter the correctly rounded
+    (math.fsum) SUM, duration-weighted mean (Eq. 1) or MAX over matched
+    kernels."""
+    kind = DEFAULT_KIND if agg_kind is None else list(agg_kind)
+    G = tr["n_ops"] + 1
+    T = tr["seq"].size
+    groups = [[] for _ in range(G)]
+    for i in range(T):
+        r = int(range_id[i])
+        g = int(tr["r_op"][r]) if r >= 0 else tr["n_ops"]
+        groups[g].append(i)
+    rows = []
+    dur = tr["dur_ns"]
+    cnt = tr["counters"]
+    for g in range(G):
+        ks = groups[g]
+        mk = [i for i in ks if match[i] >= 0]
+        row = dict(kernel_count=len(ks), total_ns=sum(int(dur[i]) for i in ks),
+                   matched_count=len(mk), matched_ns=sum(int(dur[i]) for i in mk))
+        vals = []
+        for c in range(NC):
+            if (absent_mask >> c) & 1 or not mk:
+                vals.append(math.nan)
+                continue
+            ms = [float(cnt[match[i], c]) for i in mk]
+            if kind[c] == SUM:
+                vals.append(math.fsum(ms))
+            elif kind[c] == DWMEAN:
+                num = math.fsum(m * float(dur[i]) for m, i in zip(ms, mk))
+                vals.append(num / float(row["matched_ns"]) if row["matched_ns"] else math.nan)
+            else:
+                vals.append(max(ms))
+        row["value"] = vals
+        rows.append(row)
+    return rows

@@ -1,0 +1,459 @@
+"""Pins of the oracle against what the paper and mathematics fix.
+
+The oracle is checked against: brute-force restatements of each definition on
+tiny inputs (tests/brute.py), values printed in the paper (tests/golden/),
+closed forms, labels the generator planted by construction, and invariants.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import brute
+import cases
+from oracle import oracle as O
+from paper_2609_11938_amd import tracegen as tg
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    O.build(force=False)
+
+
+# --------------------------------------------------------------------------- #
+# invocation-order matching (Alg. 1)                                           #
+# --------------------------------------------------------------------------- #
+
+@pytest.mark.parametrize("seed", range(40))
+def test_iom_matches_brute_force(seed):
+    tr = cases.random_trace(seed, T=50, drop=0.15 if seed % 3 else 0.0,
+                            extra_pf=0.1 if seed % 4 == 1 else 0.0,
+                            dedup=seed % 5 == 2, seq_gaps=seed % 2 == 1)
+    for policy in (O.PREFIX, O.SKIP_NAME, O.STRICT):
+        got = O.attribute(tr, policy=policy, stages=["match"])
+        want = brute.iom(tr, policy=1 if policy == O.SKIP_NAME else 0)
+        np.testing.assert_array_equal(got["match_iom"], want)
+
+
+def test_iom_closed_form_identity():
+    """Profiled list = every launch in launch order: the k-th launch of a name
+    takes the k-th row of that name, which is row seq itself."""
+    for cfg in ("tiny", "sdpa"):
+        tr = tg.generate(cfg)
+        out = O.attribute(tr, stages=["match"])
+        np.testing.assert_array_equal(out["match"], tr["seq"].astype(np.int32))
+
+
+def test_iom_planted_source_rows():
+    """Without drops each profiled row matches the launch that produced it."""
+    tr = tg.generate("gpt2")
+    m = O.attribute(tr, stages=["match"])["match_iom"]
+    want = np.full(m.size, -1)
+    want[tr["pf_src"]] = np.arange(tr["pf_src"].size)
+    np.testing.assert_array_equal(m, want)
+
+
+def test_iom_prefix_with_drops_independent_path():
+    """With replay rows missing (LSTM-shaped trace, at a smaller size) each name
+    matches its first min(tl, pf) launches to its rows in order."""
+    tr = tg.generate("lstm", T=50_000, ranges=500)
+    out = O.attribute(tr, stages=["match"])
+    m = out["match_iom"]
+    order = np.argsort(tr["seq"], kind="stable")
+    want = np.full(m.size, -1)
+    for n in range(tr["n_names"]):
+        ks = order[tr["name_id"][order] == n]
+        rows = np.flatnonzero(tr["pf_name"] == n)
+        k = min(ks.size, rows.size)
+        want[ks[:k]] = rows[:k]
+    np.testing.assert_array_equal(m, want)
+    tl = np.bincount(tr["name_id"], minlength=tr["n_names"])
+    pf = np.bincount(tr["pf_name"], minlength=tr["n_names"])
+    d = out["diag"]
+    assert d["names_mismatched"] == int((tl != pf).sum()) > 0
+    assert d["tl_unmatched"] == int(np.maximum(tl - pf, 0).sum())
+    assert d["pf_unmatched"] == int(np.maximum(pf - tl, 0).sum())
+    np.testing.assert_array_equal(out["name_counts"][:, 0], tl)
+    np.testing.assert_array_equal(out["name_counts"][:, 1], pf)
+    assert d["status"] == 0
+    strict = O.attribute(tr, policy=O.STRICT, stages=["match"])
+    assert strict["diag"]["status"] == -4
+    np.testing.assert_array_equal(strict["match_iom"], m)
+
+
+def test_iom_invariants():
+    tr = tg.generate("lstm", T=40_000, ranges=400)
+    m = O.attribute(tr, stages=["match"])["match_iom"]
+    ok = m >= 0
+    # the matched row always carries the launch's name
+    np.testing.assert_array_equal(tr["pf_name"][m[ok]], tr["name_id"][ok])
+    # per name, matches = min(tl, pf)
+    tl = np.bincount(tr["name_id"], minlength=tr["n_names"])
+    pf = np.bincount(tr["pf_name"], minlength=tr["n_names"])
+    got = np.bincount(tr["name_id"][ok], minlength=tr["n_names"])
+    np.testing.assert_array_equal(got, np.minimum(tl, pf))
+    # injective, and increasing in launch order within a name
+    assert np.unique(m[ok]).size == ok.sum()
+    for n in range(tr["n_names"]):
+        sel = np.flatnonzero(ok & (tr["name_id"] == n))
+        o = np.argsort(tr["seq"][sel])
+        assert np.all(np.diff(m[sel][o]) > 0)
+
+
+def test_iom_timestamp_independence_figure():
+    """Figure 'fig:clockdomain': five launches of one kernel name whose replay
+    clock drifts. The nearest-timestamp join assigns K_D the row of K_C; IOM
+    pairs by name and position and is untouched by any timestamp change."""
+    fig = json.load(open(os.path.join(GOLD, "fig_clockdomain.json")))
+    nsys = np.array(fig["nsys_t"])
+    ncu = np.array(fig["ncu_t"])
+    nearest = np.abs(nsys[:, None] - ncu[None, :]).argmin(axis=1)
+    i_d = fig["kernels"].index(fig["timestamp_join_wrong"]["nsys"])
+    assert fig["kernels"][nearest[i_d]] == fig["timestamp_join_wrong"]["ncu"]
+    T = nsys.size
+    tr = dict(seq=np.arange(T, dtype=np.uint32), start_ns=(nsys * 1000).astype(np.uint64),
+              dur_ns=np.full(T, 10, np.uint32), stream_id=np.zeros(T, np.uint16),
+              name_id=np.zeros(T, np.uint32), part_id=None, pf_name=np.zeros(T, np.uint32),
+              counters=np.zeros((T, 20), np.float32), r_start=np.zeros(0, np.uint64),
+              r_end=np.zeros(0, np.uint64), r_stream=np.zeros(0, np.uint16),
+              r_op=np.zeros(0, np.uint32), part_rep=None, n_names=1, n_streams=1, n_ops=1)
+    m = O.attribute(tr, stages=["match"])["match"]
+    np.testing.assert_array_equal(m, np.arange(T))
+    tr["start_ns"] = (ncu * 1000).astype(np.uint64)[::-1].copy()
+    np.testing.assert_array_equal(O.attribute(tr, stages=["match"])["match"], np.arange(T))
+
+
+def test_iom_timestamps_irrelevant_on_generated_trace():
+    tr = tg.generate("lstm", T=20_000, ranges=200)
+    m0 = O.attribute(tr, stages=["match"])["match"]
+    rng = np.random.default_rng(7)
+    tr2 = dict(tr, start_ns=rng.integers(0, 2**40, size=tr["seq"].size).astype(np.uint64))
+    np.testing.assert_array_equal(O.attribute(tr2, stages=["match"])["match"], m0)
+
+
+def test_iom_duplicate_seq_is_order_error():
+    tr = cases.random_trace(3, T=30)
+    tr["seq"] = tr["seq"].copy()
+    tr["seq"][5] = tr["seq"][6]
+    d = O.attribute(tr)["diag"]
+    assert d["flags"] & O.F_ORDER and d["status"] == -8
+
+
+# --------------------------------------------------------------------------- #
+# layer dedup (Sec. 3.7)                                                       #
+# --------------------------------------------------------------------------- #
+
+@pytest.mark.parametrize("seed", range(30))
+def test_dedup_matches_brute_force(seed):
+    tr = cases.random_trace(100 + seed, T=60, dedup=True, drop=0.1 if seed % 2 else 0.0)
+    out = O.attribute(tr, stages=["match", "dedup"])
+    base = brute.iom(tr)
+    want, errs = brute.dedup(tr, base)
+    np.testing.assert_array_equal(out["match"], want)
+    assert out["diag"]["dedup_errors"] == errs
+
+
+def test_dedup_gpt2_profile_is_one_twelfth_and_planted():
+    tr = tg.generate("gpt2")
+    T, P = tr["seq"].size, tr["pf_name"].size
+    assert P * 12 == T  # N/K = 12 replay reduction
+    out = O.attribute(tr)
+    m = out["match"]
+    assert (m >= 0).all() and out["diag"]["dedup_errors"] == 0
+    # every launch inherits the row replayed for the same position of layer 0
+    # of its own iteration; the generator knows which launch produced each row
+    seq = tr["seq"].astype(np.int64)
+    per_layer, layers = 40, 12
+    it, pos = seq // (per_layer * layers), seq % per_layer
+    src_seq = it * per_layer * layers + pos
+    kernel_of_seq = np.empty(T, dtype=np.int64)
+    kernel_of_seq[seq] = np.arange(T)
+    row_of_kernel = np.full(T, -1)
+    row_of_kernel[tr["pf_src"]] = np.arange(P)
+    np.testing.assert_array_equal(m, row_of_kernel[kernel_of_seq[src_seq]])
+    np.testing.assert_array_equal(tr["pf_name"][m], tr["name_id"])
+
+
+def test_dedup_k_equals_n_reduces_to_no_dedup():
+    tr = cases.random_trace(11, T=80, dedup=True)
+    tr2 = dict(tr, part_rep=np.arange(tr["n_parts"], dtype=np.int32))
+    # with every partition its own class, every launch is replayed
+    order = np.argsort(tr2["seq"])
+    tr2["pf_name"] = tr2["name_id"][order]
+    tr2["counters"] = np.zeros((tr2["pf_name"].size, 20), np.float32)
+    a = O.attribute(tr2)["match"]
+    tr3 = dict(tr2, part_id=None, part_rep=None, n_parts=0)
+    b = O.attribute(tr3)["match"]
+    np.testing.assert_array_equal(a, b)
+
+
+def _dedup_case():
+    # launch order: [rep p0: names 1 2 3][dup p1: names 1 2 3][dup p2: 1 2 3]
+    T = 9
+    tr = dict(seq=np.arange(T, dtype=np.uint32), start_ns=np.arange(T, dtype=np.uint64) * 10,
+              dur_ns=np.ones(T, np.uint32), stream_id=np.zeros(T, np.uint16),
+              name_id=np.array([1, 2, 3] * 3, np.uint32),
+              part_id=np.repeat(np.arange(3), 3).astype(np.int32),
+              pf_name=np.array([1, 2, 3], np.uint32), counters=np.zeros((3, 20), np.float32),
+              r_start=np.zeros(0, np.uint64), r_end=np.zeros(0, np.uint64),
+              r_stream=np.zeros(0, np.uint16), r_op=np.zeros(0, np.uint32),
+              part_rep=np.zeros(3, np.int32), n_names=4, n_streams=1, n_ops=1, n_parts=3)
+    return tr
+
+
+def test_dedup_error_cases():
+    tr = _dedup_case()
+    out = O.attribute(tr)
+    np.testing.assert_array_equal(out["match"], [0, 1, 2] * 3)
+    assert out["diag"]["status"] == 0
+    # a duplicate whose name differs from the representative at its position
+    t2 = dict(tr, name_id=tr["name_id"].copy())
+    t2["name_id"][4] = 0
+    out = O.attribute(t2)
+    assert out["match"][4] == -1 and out["diag"]["dedup_errors"] == 1
+    assert out["diag"]["status"] == -6
+    # a duplicate partition longer than its representative
+    t3 = dict(tr, part_id=tr["part_id"].copy())
+    t3["part_id"][2] = 1  # rep p0 now has 2 kernels; p1 has 4
+    out = O.attribute(t3)
+    assert out["diag"]["dedup_errors"] >= 1
+    # a representative that is itself a duplicate (not a fixed point)
+    t4 = dict(tr, part_rep=np.array([0, 0, 1], np.int32))
+    out = O.attribute(t4)
+    np.testing.assert_array_equal(out["match"][6:], [-1, -1, -1])
+    assert out["diag"]["dedup_errors"] == 3
+    # a partition whose launches are not one contiguous run
+    t5 = dict(tr, part_id=np.array([0, 0, 0, 1, 2, 1, 2, 1, 2], np.int32))
+    out = O.attribute(t5)
+    assert out["diag"]["flags"] & O.F_PARTITION and out["diag"]["status"] == -7
+    np.testing.assert_array_equal(out["match"][3:], [-1] * 6)
+
+
+def test_bad_ids_are_data_errors():
+    tr = _dedup_case()
+    t = dict(tr, name_id=tr["name_id"].copy())
+    t["name_id"][0] = 99
+    out = O.attribute(t)
+    assert out["diag"]["bad_records"] == 1 and out["diag"]["status"] == -9
+    assert out["match"][0] == -1
+
+
+# --------------------------------------------------------------------------- #
+# enclosure (Alg. 2)                                                           #
+# --------------------------------------------------------------------------- #
+
+@pytest.mark.parametrize("seed", range(60))
+def test_enclose_matches_brute_force(seed):
+    tr = cases.random_trace(200 + seed, T=70, R=25, S=1 + seed % 3, t_max=40,
+                            nested=seed % 4 != 3)
+    out = O.attribute(tr, stages=["match", "enclose"])
+    np.testing.assert_array_equal(out["range_id"], brute.enclose(tr))
+    np.testing.assert_array_equal(out["range_depth"], np.minimum(brute.depth(tr), 255))
+    assert out["diag"]["nesting_errors"] == len(brute.crossing_streams(tr))
+
+
+def test_enclose_ties_and_edges():
+    # one stream; ranges: 0=[10,20] 1=[10,20] (identical: 1 is inner) 2=[20,30]
+    # (touches 0/1 at 20) 3=[25,25] (point) 4=[40,50]; kernels at 5 (before all),
+    # 10 (= s), 20 (touching point), 25 (point range), 30 (= e), 35 (gap), 60 (after)
+    q = np.array([5, 10, 20, 25, 30, 35, 60], np.uint64)
+    T = q.size
+    tr = dict(seq=np.arange(T, dtype=np.uint32), start_ns=q, dur_ns=np.ones(T, np.uint32),
+              stream_id=np.zeros(T, np.uint16), name_id=np.zeros(T, np.uint32), part_id=None,
+              pf_name=np.zeros(0, np.uint32), counters=np.zeros((0, 20), np.float32),
+              r_start=np.array([10, 10, 20, 25, 40], np.uint64),
+              r_end=np.array([20, 20, 30, 25, 50], np.uint64),
+              r_stream=np.zeros(5, np.uint16), r_op=np.arange(5, dtype=np.uint32),
+              part_rep=None, n_names=1, n_streams=1, n_ops=5)
+    out = O.attribute(tr)
+    np.testing.assert_array_equal(out["range_id"], [-1, 1, 2, 3, 2, -1, -1])
+    np.testing.assert_array_equal(out["range_id"], brute.enclose(tr))
+    np.testing.assert_array_equal(out["range_depth"], [1, 2, 1, 2, 1])
+    assert out["diag"]["nesting_errors"] == 0
+    # the query point, when given, replaces the start time
+    tr["query_ns"] = np.array([45] * T, np.uint64)
+    np.testing.assert_array_equal(O.attribute(tr)["range_id"], [4] * T)
+
+
+def test_enclose_crossing_ranges_flagged():
+    T = 3
+    tr = dict(seq=np.arange(T, dtype=np.uint32), start_ns=np.array([1, 4, 9], np.uint64),
+              dur_ns=np.ones(T, np.uint32), stream_id=np.zeros(T, np.uint16),
+              name_id=np.zeros(T, np.uint32), part_id=None, pf_name=np.zeros(0, np.uint32),
+              counters=np.zeros((0, 20), np.float32),
+              r_start=np.array([0, 3], np.uint64), r_end=np.array([5, 8], np.uint64),
+              r_stream=np.zeros(2, np.uint16), r_op=np.zeros(2, np.uint32), part_rep=None,
+              n_names=1, n_streams=1, n_ops=1)
+    out = O.attribute(tr)
+    assert out["diag"]["nesting_errors"] == 1 and out["diag"]["status"] == -5
+    np.testing.assert_array_equal(out["range_id"], brute.enclose(tr))
+
+
+@pytest.mark.parametrize("cfg", ["tiny", "gpt2", "sdpa", "lstm"])
+def test_enclose_planted_labels(cfg):
+    tr = tg.generate(cfg)
+    out = O.attribute(tr, stages=["match", "enclose"])
+    np.testing.assert_array_equal(out["range_id"], tr["planted_range"])
+    assert out["diag"]["nesting_errors"] == 0
+
+
+def test_enclose_invariants_and_depth():
+    tr = tg.generate("tiny")
+    out = O.attribute(tr, stages=["match", "enclose"])
+    rid, dep = out["range_id"], out["range_depth"].astype(np.int64)
+    q = tr["start_ns"]
+    ok = rid >= 0
+    # the chosen range holds the query point and lies on the kernel's stream
+    assert np.all(tr["r_start"][rid[ok]] <= q[ok]) and np.all(q[ok] <= tr["r_end"][rid[ok]])
+    assert np.all(tr["r_stream"][rid[ok]] == tr["stream_id"][ok])
+    # its depth is the maximum among all ranges containing the query point
+    for i in np.flatnonzero(ok)[::7]:
+        cont = (tr["r_stream"] == tr["stream_id"][i]) & (tr["r_start"] <= q[i]) & (q[i] <= tr["r_end"])
+        assert dep[rid[i]] == dep[cont].max()
+    # kernels before the first range of their stream fall through
+    first = tr["r_start"].min()
+    assert np.all(rid[q < first] == -1)
+    # depth = number of containing ranges (properly nested, no touching here)
+    small = cases.random_trace(5, T=10, R=40, S=2, t_max=200)
+    small_out = O.attribute(small, stages=["match", "enclose"])
+    np.testing.assert_array_equal(small_out["range_depth"], brute.depth(small))
+    assert out["range_depth"].min() >= 1 and out["range_depth"].max() <= 4
+
+
+def test_depth_equals_container_count_without_touching():
+    for seed in range(10):
+        tr = cases.random_trace(300 + seed, T=5, R=30, S=2, t_max=1000)
+        # drop ranges sharing an endpoint so containment is a tree
+        ends = np.concatenate([tr["r_start"], tr["r_end"]])
+        vals, cnt = np.unique(ends, return_counts=True)
+        dup = set(vals[cnt > 1].tolist())
+        keep = np.array([(a not in dup and b not in dup) for a, b in zip(tr["r_start"], tr["r_end"])],
+                        dtype=bool)
+        for k in ("r_start", "r_end", "r_stream", "r_op"):
+            tr[k] = tr[k][keep]
+        out = O.attribute(tr, stages=["match", "enclose"])
+        np.testing.assert_array_equal(out["range_depth"], brute.containers(tr))
+
+
+# --------------------------------------------------------------------------- #
+# aggregation (Eq. 1)                                                          #
+# --------------------------------------------------------------------------- #
+
+def _table_dicts(table):
+    return [dict(kernel_count=int(r["kernel_count"]), total_ns=int(r["total_ns"]),
+                 matched_count=int(r["matched_count"]), matched_ns=int(r["matched_ns"]),
+                 value=[float(v) for v in r["value"]]) for r in table]
+
+
+def _assert_rows(got, want, rtol):
+    for a, b in zip(got, want):
+        for f in ("kernel_count", "total_ns", "matched_count", "matched_ns"):
+            assert a[f] == b[f]
+        for x, y in zip(a["value"], b["value"]):
+            if math.isnan(y):
+                assert math.isnan(x)
+            else:
+                assert abs(x - y) <= rtol * max(abs(x), abs(y)), (x, y)
+
+
+def test_single_kernel_identity_from_profile_excerpt():
+    """The appendix excerpt: one kernel attributed to aten::mm_26 gives
+    kernel_count 1, total_duration_ns = its duration, and every aggregated
+    counter equal to that kernel's own value; the counter absent on the
+    capture's architecture is null."""
+    g = json.load(open(os.path.join(GOLD, "profile_excerpt.json")))
+    cnt = np.zeros((1, 20), np.float32)
+    for v in g["counters"].values():
+        cnt[0, v["index"]] = v["value"]
+    absent = 0
+    for v in g["absent"].values():
+        absent |= 1 << v["index"]
+    tr = dict(seq=np.zeros(1, np.uint32), start_ns=np.array([100], np.uint64),
+              dur_ns=np.array([g["duration_ns"]], np.uint32), stream_id=np.zeros(1, np.uint16),
+              name_id=np.zeros(1, np.uint32), part_id=None, pf_name=np.zeros(1, np.uint32),
+              counters=cnt, r_start=np.array([50], np.uint64), r_end=np.array([200], np.uint64),
+              r_stream=np.zeros(1, np.uint16), r_op=np.zeros(1, np.uint32), part_rep=None,
+              n_names=1, n_streams=1, n_ops=1)
+    out = O.attribute(tr, absent_mask=absent)
+    row = out["table"][0]
+    assert int(row["kernel_count"]) == g["kernel_count"]
+    assert int(row["total_ns"]) == g["total_duration_ns"]
+    for v in g["counters"].values():
+        assert row["value"][v["index"]] == float(np.float32(v["value"]))
+    for v in g["absent"].values():
+        assert math.isnan(row["value"][v["index"]])
+    assert out["summary"]["attributed_fraction"] == 1.0
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_aggregate_matches_fsum(seed):
+    tr = cases.random_trace(400 + seed, T=120, R=30, drop=0.2, dedup=seed % 2 == 0)
+    kind = None if seed % 3 else np.array([1] * 20, np.uint8)
+    absent = 0 if seed % 4 else (1 << 5) | (1 << 17)
+    out = O.attribute(tr, agg_kind=kind, absent_mask=absent)
+    want = brute.aggregate(tr, out["match"], out["range_id"], kind, absent)
+    _assert_rows(_table_dicts(out["table"]), want, 1e-13)
+
+
+@pytest.mark.parametrize("cfg", ["tiny", "gpt2"])
+def test_aggregate_matches_fsum_on_configs(cfg):
+    tr = tg.generate(cfg)
+    out = O.attribute(tr)
+    want = brute.aggregate(tr, out["match"], out["range_id"])
+    _assert_rows(_table_dicts(out["table"]), want, 1e-12)
+
+
+def test_aggregate_closed_forms():
+    tr = tg.generate("tiny")
+    # equal durations: the duration-weighted mean is the arithmetic mean
+    t = dict(tr, dur_ns=np.full(tr["seq"].size, 777, np.uint32))
+    t["counters"] = tr["counters"].copy()
+    t["counters"][:, 7] = np.float32(0.625)  # a constant counter: DW = constant
+    out = O.attribute(t)
+    for g, row in enumerate(out["table"]):
+        if row["matched_count"] == 0:
+            assert math.isnan(row["value"][3])
+            continue
+        sel = np.flatnonzero((np.where(out["range_id"] >= 0, t["r_op"][out["range_id"]],
+                                       t["n_ops"]) == g) & (out["match"] >= 0))
+        ms = t["counters"][out["match"][sel], 3].astype(np.float64)
+        assert abs(row["value"][3] - ms.mean()) <= 1e-12 * abs(ms.mean())
+        assert row["value"][7] == 0.625
+        # MAX is the plain maximum, exactly
+        assert row["value"][17] == t["counters"][out["match"][sel], 17].max()
+    # totals are exact and complete
+    tab, sm = out["table"], out["summary"]
+    assert int(tab["kernel_count"].sum()) == t["seq"].size
+    assert int(tab["total_ns"].sum(dtype=np.uint64)) == int(t["dur_ns"].sum(dtype=np.uint64))
+    assert sm["attributed_ns"] + sm["unattributed_ns"] == sm["total_ns"]
+    assert sm["unattributed_ns"] == int(tab["total_ns"][-1])
+
+
+def test_coverage_of_shaped_configs():
+    assert O.attribute(tg.generate("sdpa"))["summary"]["attributed_fraction"] == 1.0
+    tr = tg.generate("lstm", T=200_000, ranges=2_000)
+    f = O.attribute(tr)["summary"]["attributed_fraction"]
+    assert 0.10 < f < 0.20
+
+
+def test_emission_orders_agree():
+    base = None
+    for em in ("stream_major", "seq", "shuffled"):
+        tr = tg.generate("gpt2", emission=em)
+        out = O.attribute(tr)
+        # map outputs back to launch order and ranges to a canonical key
+        o = np.argsort(tr["seq"])
+        key = np.stack([tr["r_stream"].astype(np.uint64), tr["r_start"]], 1)
+        rid = out["range_id"][o]
+        rk = np.where(rid[:, None] >= 0, key[np.maximum(rid, 0)], -1)
+        res = (out["match"][o], rk, out["table"])
+        if base is None:
+            base = res
+            continue
+        np.testing.assert_array_equal(res[0], base[0])
+        np.testing.assert_array_equal(res[1], base[1])
+        _assert_rows(_table_dicts(res[2]), _table_dicts(base[2]), 1e-14)

@@ -1,0 +1,135 @@
+"""Plant one plausible mistake at a time in a copy of the oracle (on the CPU)
+and check that the pins catch it: an off-by-one, a reversed order, a dropped
+term, a wrong comparison. Every mutant must fail the pin battery; the
+unmodified source must pass it."""
+import math
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import brute
+import cases
+from oracle import oracle as O
+
+SRC = open(O.SRC).read()
+
+MUTANTS = {
+    "iom_descending_seq": ("ord[ne].a = k->seq[i];", "ord[ne].a = UINT32_MAX - k->seq[i];"),
+    "iom_counter_not_advanced": ("counter[n] = c + 1;", "counter[n] = c;"),
+    "iom_skip_name_ignored": ("if (tl_cnt[n] != pf_cnt[n]) match[i] = -1;",
+                              "if (0) match[i] = -1;"),
+    "dedup_reversed_position": ("int64_t src = mem[off[r] + pos].idx;",
+                                "int64_t src = mem[off[r] + cnt[r] - 1 - pos].idx;"),
+    "dedup_no_name_check": ("ok = k->name_id[src] == k->name_id[i];", "ok = 1;"),
+    "enclose_end_ascending": ("rs[nr].c = UINT64_MAX - r->end_ns[x];",
+                              "rs[nr].c = r->end_ns[x];"),
+    "enclose_open_at_start_excluded": ("while (x < a_end && rs[x].b <= t)",
+                                       "while (x < a_end && rs[x].b < t)"),
+    "enclose_closed_at_end_excluded": ("while (top > 0 && r->end_ns[stack[top - 1]] < t) top--;",
+                                       "while (top > 0 && r->end_ns[stack[top - 1]] <= t) top--;"),
+    "depth_root_zero": ("depth[id] = top > 0 ? depth[stack[top - 1]] + 1 : 1;",
+                        "depth[id] = top > 0 ? depth[stack[top - 1]] + 1 : 0;"),
+    "nesting_touch_is_cross": ("while (top > 0 && r->end_ns[stack[top - 1]] <= r->start_ns[id]) top--;",
+                               "while (top > 0 && r->end_ns[stack[top - 1]] < r->start_ns[id]) top--;"),
+    "dw_without_duration": ("nadd(&acc[x], v * (double)dur); /* m_i * d_i */",
+                            "nadd(&acc[x], v);"),
+    "max_is_min": ("else if (isnan(v) || v > mx[x]) mx[x] = v;",
+                   "else if (isnan(v) || v < mx[x] || isinf(mx[x])) mx[x] = v;"),
+    "absent_mask_ignored": ("if (((p->absent_mask >> c) & 1u) || row->matched_count == 0)",
+                            "if (row->matched_count == 0)"),
+    "unmatched_in_dw_denominator": ("if (m < 0) continue; /* unmatched kernels carry no counters */",
+                                    "if (m < 0) { row->matched_ns += dur; continue; }"),
+    "unattributed_dropped": ("row->kernel_count++;", "if (g < d->n_ops) row->kernel_count++;"),
+}
+
+
+def _build(tmp_path, name, src):
+    c = tmp_path / f"{name}.c"
+    so = tmp_path / f"{name}.so"
+    c.write_text(src)
+    subprocess.run(["gcc", "-O1", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
+                    "-I", os.path.dirname(O.SRC), "-o", str(so), str(c), "-lm"], check=True)
+    return O.load(str(so))
+
+
+def _edge_trace():
+    q = np.array([5, 10, 20, 25, 30, 35, 60], np.uint64)
+    T = q.size
+    return dict(seq=np.arange(T, dtype=np.uint32), start_ns=q, dur_ns=np.arange(1, T + 1, dtype=np.uint32),
+                stream_id=np.zeros(T, np.uint16), name_id=np.zeros(T, np.uint32), part_id=None,
+                pf_name=np.zeros(T, np.uint32),
+                counters=np.random.default_rng(0).random((T, 20), dtype=np.float32),
+                r_start=np.array([10, 10, 20, 25, 40], np.uint64),
+                r_end=np.array([20, 20, 30, 25, 50], np.uint64),
+                r_stream=np.zeros(5, np.uint16), r_op=np.arange(5, dtype=np.uint32),
+                part_rep=None, n_names=1, n_streams=1, n_ops=5)
+
+
+def _rows_close(out, want, rtol=1e-12):
+    for a, b in zip(out["table"], want):
+        for f in ("kernel_count", "total_ns", "matched_count", "matched_ns"):
+            if int(a[f]) != b[f]:
+                return False
+        for x, y in zip(a["value"], b["value"]):
+            if math.isnan(y) != math.isnan(float(x)):
+                return False
+            if not math.isnan(y) and abs(float(x) - y) > rtol * max(abs(float(x)), abs(y)):
+                return False
+    return True
+
+
+def battery(L) -> bool:
+    """True when every pin holds for library L."""
+    for seed in range(8):
+        tr = cases.random_trace(seed, T=40, drop=0.2 if seed % 2 else 0.0,
+                                dedup=seed % 3 == 0)
+        for pol in (O.PREFIX, O.SKIP_NAME):
+            got = O.attribute(tr, policy=pol, stages=["match"], library=L)["match_iom"]
+            if not np.array_equal(got, brute.iom(tr, policy=1 if pol == O.SKIP_NAME else 0)):
+                return False
+    for seed in range(8):
+        tr = cases.random_trace(100 + seed, T=60, dedup=True)
+        tr["name_id"] = tr["name_id"].copy()
+        if seed % 2:
+            tr["name_id"][int(np.argmax(tr["part_id"]))] ^= 1  # one foreign name
+        out = O.attribute(tr, stages=["match", "dedup"], library=L)
+        want, errs = brute.dedup(tr, brute.iom(tr))
+        if not np.array_equal(out["match"], want) or out["diag"]["dedup_errors"] != errs:
+            return False
+    for seed in range(12):
+        tr = cases.random_trace(200 + seed, T=60, R=25, S=2, t_max=30,
+                                nested=seed % 4 != 3)
+        out = O.attribute(tr, stages=["match", "enclose"], library=L)
+        if not np.array_equal(out["range_id"], brute.enclose(tr)):
+            return False
+        if not np.array_equal(out["range_depth"], np.minimum(brute.depth(tr), 255)):
+            return False
+        if out["diag"]["nesting_errors"] != len(brute.crossing_streams(tr)):
+            return False
+    tr = _edge_trace()
+    out = O.attribute(tr, library=L)
+    if not np.array_equal(out["range_id"], brute.enclose(tr)):
+        return False
+    if not _rows_close(out, brute.aggregate(tr, out["match"], out["range_id"])):
+        return False
+    for seed in range(6):
+        tr = cases.random_trace(400 + seed, T=80, R=20, drop=0.3)
+        absent = (1 << 4) if seed % 2 else 0
+        out = O.attribute(tr, absent_mask=absent, library=L)
+        if not _rows_close(out, brute.aggregate(tr, out["match"], out["range_id"], None, absent)):
+            return False
+    return True
+
+
+def test_unmodified_oracle_passes_battery(tmp_path):
+    assert battery(_build(tmp_path, "orig", SRC))
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(tmp_path, name):
+    old, new = MUTANTS[name]
+    assert SRC.count(old) == 1, f"mutation site for {name} not found exactly once"
+    L = _build(tmp_path, name, SRC.replace(old, new))
+    assert not battery(L), f"mutant {name} survived the pins"
