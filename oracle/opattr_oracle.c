@@ -35,6 +35,11 @@ static int cmp_key3(const void *x, const void *y) {
 
 static void *xcalloc(size_t n, size_t sz) { return calloc(n ? n : 1, sz); }
 
+static int cmp_u32(const void *x, const void *y) {
+  uint32_t a = *(const uint32_t *)x, b = *(const uint32_t *)y;
+  return a < b ? -1 : (a > b);
+}
+
 void oref_diag_clear(oref_diag *d) { memset(d, 0, sizeof(*d)); }
 
 void oref_diag_finish(oref_diag *d, int policy) {
@@ -52,9 +57,13 @@ void oref_diag_finish(oref_diag *d, int policy) {
 
 /* a kernel takes part in matching and dedup only if its name and partition
    ids are in range */
+static int dedup_on(const oref_kernels *k, const oref_dims *d) {
+  return k->part_id && d->part_rep && d->n_parts > 0;
+}
+
 static int kernel_ok(const oref_kernels *k, const oref_dims *d, int64_t i) {
   if (k->name_id[i] >= d->n_names) return 0;
-  if (k->part_id && d->part_rep) {
+  if (dedup_on(k, d)) {
     int32_t p = k->part_id[i];
     if (p < -1 || (p >= 0 && (uint32_t)p >= d->n_parts)) return 0;
   }
@@ -62,7 +71,7 @@ static int kernel_ok(const oref_kernels *k, const oref_dims *d, int64_t i) {
 }
 
 static int32_t part_of(const oref_kernels *k, const oref_dims *d, int64_t i) {
-  return (k->part_id && d->part_rep) ? k->part_id[i] : -1;
+  return dedup_on(k, d) ? k->part_id[i] : -1;
 }
 
 static int rep_ok(const oref_dims *d, int32_t p) {
@@ -98,7 +107,7 @@ int oref_match(const oref_kernels *k, const oref_profiled *p, const oref_dims *d
     if (!kernel_ok(k, d, i)) diag->bad_records++;
   for (int64_t j = 0; j < P; ++j)
     if (p->name_id[j] >= NN) diag->bad_records++;
-  if (k->part_id && d->part_rep)
+  if (dedup_on(k, d))
     for (uint32_t q = 0; q < d->n_parts; ++q)
       if (!rep_ok(d, (int32_t)q)) diag->bad_records++;
 
@@ -129,9 +138,15 @@ int oref_match(const oref_kernels *k, const oref_profiled *p, const oref_dims *d
     }
   }
   qsort(ord, (size_t)ne, sizeof(key3), cmp_key3);
-  /* launch ordinals must be unique */
-  for (int64_t x = 1; x < ne; ++x)
-    if (ord[x].a == ord[x - 1].a) { diag->flags |= OREF_F_ORDER; break; }
+  /* launch ordinals must be unique over the whole timeline */
+  {
+    uint32_t *all = xcalloc((size_t)T, sizeof(uint32_t));
+    for (int64_t i = 0; i < T; ++i) all[i] = k->seq[i];
+    qsort(all, (size_t)T, sizeof(uint32_t), cmp_u32);
+    for (int64_t x = 1; x < T; ++x)
+      if (all[x] == all[x - 1]) { diag->flags |= OREF_F_ORDER; break; }
+    free(all);
+  }
 
   /* Alg. 1: counter[name] = invocations seen so far; the i-th invocation of a
      name takes the i-th profiled row of that name; once the rows run out the
@@ -182,7 +197,7 @@ int oref_match(const oref_kernels *k, const oref_profiled *p, const oref_dims *d
 int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
                oref_diag *diag) {
   if (!k || !d || !match || !diag || k->n < 0) return OREF_ERR_ARG;
-  if (!k->part_id || !d->part_rep) return 0; /* no partitions: nothing to do */
+  if (!dedup_on(k, d)) return 0; /* no partitions: nothing to do */
   const int64_t T = k->n;
   const uint32_t NP = d->n_parts;
 
@@ -244,9 +259,10 @@ int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
 /* Stage 3: enclosure (Alg. 2, Sec. 3.5)                                    */
 /* ----------------------------------------------------------------------- */
 
+/* a range takes part only with in-range ids, start <= end and end < 2^63 */
 static int range_ok(const oref_ranges *r, const oref_dims *d, int64_t x) {
   return r->stream_id[x] < d->n_streams && r->op_id[x] < d->n_ops &&
-         r->start_ns[x] <= r->end_ns[x];
+         r->start_ns[x] <= r->end_ns[x] && r->end_ns[x] < (UINT64_C(1) << 63);
 }
 
 int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,

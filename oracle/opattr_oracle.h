@@ -65,8 +65,9 @@ typedef struct {
 } oref_summary;
 
 /* error classes, as bits of oref_diag.flags */
-#define OREF_F_DATA 1u       /* an id out of range, or a range with start > end  */
-#define OREF_F_ORDER 2u      /* duplicate launch ordinal                          */
+#define OREF_F_DATA 1u       /* an id out of range, or a range with start > end or
+                                end >= 2^63 (such records are left out)          */
+#define OREF_F_ORDER 2u      /* duplicate launch ordinal anywhere in the timeline */
 #define OREF_F_LIMIT 4u      /* nesting deeper than 255                           */
 #define OREF_F_NOT_NESTED 8u /* two ranges of a stream cross                      */
 #define OREF_F_PARTITION 16u /* a partition is not one contiguous run of seq      */
