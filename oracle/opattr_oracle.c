@@ -201,6 +201,19 @@ int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
   const int64_t T = k->n;
   const uint32_t NP = d->n_parts;
 
+  /* launch-order rank of every kernel: its position when the whole timeline is
+     sorted by seq (ties by input index) */
+  key3 *all = xcalloc((size_t)T, sizeof(key3));
+  for (int64_t i = 0; i < T; ++i) {
+    all[i].a = k->seq[i];
+    all[i].b = all[i].c = 0;
+    all[i].idx = i;
+  }
+  qsort(all, (size_t)T, sizeof(key3), cmp_key3);
+  int64_t *rank = xcalloc((size_t)T, sizeof(int64_t));
+  for (int64_t x = 0; x < T; ++x) rank[all[x].idx] = x;
+  free(all);
+
   /* members[p]: the kernels of partition p in launch order */
   int64_t *cnt = xcalloc(NP, sizeof(int64_t));
   int64_t *off = xcalloc((size_t)NP + 1, sizeof(int64_t));
@@ -214,14 +227,14 @@ int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
     int32_t q = k->part_id[i];
     key3 *e = &mem[off[q] + fill[q]++];
     e->a = (uint64_t)q;
-    e->b = k->seq[i];
+    e->b = (uint64_t)rank[i];
     e->c = 0;
     e->idx = i;
   }
-  qsort(mem, (size_t)off[NP], sizeof(key3), cmp_key3); /* by (partition, seq) */
+  qsort(mem, (size_t)off[NP], sizeof(key3), cmp_key3); /* by (partition, rank) */
 
-  /* a partition is the run of launches between its tags: its ordinals must
-     form one contiguous interval */
+  /* a partition is the run of launches between its tags: its launches must be
+     consecutive in launch order (no other launch between them) */
   char *contig = xcalloc(NP, 1);
   for (uint32_t q = 0; q < NP; ++q) {
     if (cnt[q] == 0) { contig[q] = 1; continue; }
@@ -251,7 +264,7 @@ int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
     }
   }
   if (diag->dedup_errors) diag->flags |= OREF_F_DEDUP;
-  free(cnt); free(off); free(mem); free(fill); free(contig);
+  free(cnt); free(off); free(mem); free(fill); free(contig); free(rank);
   return 0;
 }
 

@@ -149,7 +149,8 @@ def test_iom_duplicate_seq_is_order_error():
 
 @pytest.mark.parametrize("seed", range(30))
 def test_dedup_matches_brute_force(seed):
-    tr = cases.random_trace(100 + seed, T=60, dedup=True, drop=0.1 if seed % 2 else 0.0)
+    tr = cases.random_trace(100 + seed, T=60, dedup=True, drop=0.1 if seed % 2 else 0.0,
+                            seq_gaps=seed % 3 == 1)
     out = O.attribute(tr, stages=["match", "dedup"])
     base = brute.iom(tr)
     want, errs = brute.dedup(tr, base)
@@ -231,6 +232,30 @@ def test_dedup_error_cases():
     out = O.attribute(t5)
     assert out["diag"]["flags"] & O.F_PARTITION and out["diag"]["status"] == -7
     np.testing.assert_array_equal(out["match"][3:], [-1] * 6)
+
+
+def test_dedup_contiguity_is_in_launch_order():
+    """A partition is a window of launches (Sec. 3.7): with gaps between the
+    launch ordinals it is still contiguous when no other launch falls inside."""
+    tr = _dedup_case()
+    tr = dict(tr, seq=(np.arange(9) * 10 + 3).astype(np.uint32))
+    out = O.attribute(tr)
+    assert out["diag"]["status"] == 0
+    np.testing.assert_array_equal(out["match"], [0, 1, 2] * 3)
+    # an unpartitioned launch inside partition 1's window breaks it
+    t2 = dict(tr, seq=np.array([0, 10, 20, 30, 40, 55, 60, 70, 80], np.uint32),
+              part_id=np.array([0, 0, 0, 1, 1, 1, 2, 2, 2], np.int32))
+    t2["seq"] = t2["seq"].copy()
+    t2["part_id"] = np.concatenate([t2["part_id"], [-1]]).astype(np.int32)
+    t2["seq"] = np.concatenate([t2["seq"], [45]]).astype(np.uint32)
+    for key in ("start_ns", "dur_ns", "stream_id"):
+        t2[key] = np.concatenate([t2[key], t2[key][:1]])
+    t2["name_id"] = np.concatenate([t2["name_id"], [3]]).astype(np.uint32)
+    t2["pf_name"] = np.array([1, 2, 3, 3], np.uint32)
+    t2["counters"] = np.zeros((4, 20), np.float32)
+    out = O.attribute(t2)
+    assert out["diag"]["flags"] & O.F_PARTITION
+    assert (out["match"][3:6] == -1).all()
 
 
 def test_bad_ids_are_data_errors():

@@ -22,6 +22,7 @@ MUTANTS = {
                               "if (0) match[i] = -1;"),
     "dedup_reversed_position": ("int64_t src = mem[off[r] + pos].idx;",
                                 "int64_t src = mem[off[r] + cnt[r] - 1 - pos].idx;"),
+    "dedup_contiguity_on_seq_values": ("e->b = (uint64_t)rank[i];", "e->b = k->seq[i];"),
     "dedup_no_name_check": ("ok = k->name_id[src] == k->name_id[i];", "ok = 1;"),
     "enclose_end_ascending": ("rs[nr].c = UINT64_MAX - r->end_ns[x];",
                               "rs[nr].c = r->end_ns[x];"),
@@ -90,7 +91,7 @@ def battery(L) -> bool:
             if not np.array_equal(got, brute.iom(tr, policy=1 if pol == O.SKIP_NAME else 0)):
                 return False
     for seed in range(8):
-        tr = cases.random_trace(100 + seed, T=60, dedup=True)
+        tr = cases.random_trace(100 + seed, T=60, dedup=True, seq_gaps=seed % 2 == 0)
         tr["name_id"] = tr["name_id"].copy()
         if seed % 2:
             tr["name_id"][int(np.argmax(tr["part_id"]))] ^= 1  # one foreign name
