@@ -1,0 +1,230 @@
+/*
+ * opattr.h -- C ABI of the MI355X trace-attribution join.
+ *
+ * The library attributes GPU kernel records to operators in the three stages of
+ * the paper "Hardware-Attributed Operator Profiling for PyTorch":
+ *
+ *   opattr_match           invocation-order matching of profiled counter rows to
+ *                          timeline launches (Sec. 3.3, Alg. 1)
+ *   opattr_dedup_broadcast positional inheritance of counters from the profiled
+ *                          representative of a layer class (Sec. 3.7)
+ *   opattr_enclose         innermost operator range enclosing each launch on its
+ *                          own stream (Sec. 3.5, Alg. 2)
+ *   opattr_aggregate       per-operator SUM / duration-weighted mean (Eq. 1) / MAX
+ *                          of the 20-counter set, with an UNATTRIBUTED row
+ *                          (Sec. 3.8.1 and the counter appendix table)
+ *   opattr_attribute       all four stages in one call
+ *
+ * Conventions shared by every entry point:
+ *  - Array pointers inside the structs and all output arrays are DEVICE pointers
+ *    on the current HIP device, unless marked (host).
+ *  - Every call enqueues its work on `stream` (a hipStream_t; NULL = the null
+ *    stream) and returns without synchronising, except opattr_read_diag.
+ *  - The caller owns every buffer: inputs, outputs, the diag record and the
+ *    workspace. No entry point allocates or frees device memory. Calls are
+ *    stateless and reentrant on distinct workspaces.
+ *  - Return value: 0, or a negative OPATTR_ERR_* for an ARGUMENT error found on
+ *    the host (nothing is enqueued then). Errors that depend on the data are
+ *    recorded on the device in the opattr_diag record (flags, counts, status);
+ *    outputs are still written. Read them with opattr_read_diag.
+ *  - Sizes: every count is < 2^31. n_names <= 2^20 - 1, n_streams <= 65536.
+ *  - Records with an id out of range are left out and counted (bad_records):
+ *    launches with name_id >= n_names or part_id outside [-1, n_parts) take no
+ *    part in matching and dedup; launches with stream_id >= n_streams enclose
+ *    nothing; profiled rows with name_id >= n_names are never matched; ranges
+ *    with stream_id >= n_streams, op_id >= n_ops, start > end or end >= 2^63
+ *    enclose nothing. Partitions are used only when part_id, part_rep and
+ *    n_parts > 0 are all given.
+ *  - Ids: match[i] in [-1, P), range_id[i] in [-1, R); -1 means none.
+ */
+#ifndef OPATTR_H
+#define OPATTR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OPATTR_NUM_COUNTERS 20
+
+/* Timeline: one record per launched kernel (a KernelRow of Alg. 1), length n. */
+typedef struct {
+  int64_t n;
+  const uint32_t *seq;      /* launch ordinal, unique (CUPTI correlation order)      */
+  const uint64_t *start_ns; /* GPU start time                                         */
+  const uint32_t *dur_ns;   /* duration: the weight d_i of Eq. 1 (Sec. 3.2)           */
+  const uint16_t *stream_id;/* < n_streams                                            */
+  const uint32_t *name_id;  /* < n_names                                              */
+  const int32_t *part_id;   /* layer partition instance or -1; NULL = no partitions   */
+  const uint64_t *query_ns; /* enclosure query point (host launch time, Alg. 2);
+                               NULL = start_ns                                        */
+} opattr_kernels;
+
+/* Profiled counter rows in replay order (the NcuRow list of Alg. 1), length n.
+   Counter c of row j is counters[j*row_stride + c*col_stride] (float32). */
+typedef struct {
+  int64_t n;
+  const uint32_t *name_id;
+  const float *counters;
+  int64_t row_stride, col_stride;
+  uint32_t absent_mask; /* bit c set: counter c absent in this capture -> NaN   */
+} opattr_profiled;
+
+/* Operator ranges: closed intervals [start_ns, end_ns] on a stream (the NVTX
+   ranges of Sec. 3.5), length n. */
+typedef struct {
+  int64_t n;
+  const uint64_t *start_ns, *end_ns;
+  const uint16_t *stream_id;
+  const uint32_t *op_id; /* < n_ops: the aggregation key (row of the table)         */
+} opattr_ranges;
+
+/* Layout hints: each is a PROMISE about the inputs that lets the library skip a
+   reordering pass. A false promise gives unspecified outputs (never an
+   out-of-bounds access); with OPATTR_VALIDATE it is detected and reported as
+   OPATTR_ERR_ORDER. Without hints every input order is accepted. */
+#define OPATTR_KERNELS_STREAM_MAJOR 1u /* kernels sorted by (stream_id, seq), and
+                                          per stream the query point does not
+                                          decrease with seq                        */
+#define OPATTR_SEQ_DENSE 2u            /* seq is a permutation of [0, n)          */
+#define OPATTR_RANGES_NESTED 4u        /* ranges sorted by (stream_id, start asc,
+                                          end desc)                                */
+#define OPATTR_VALIDATE 8u             /* check the promised layouts on device    */
+
+typedef struct {
+  uint32_t n_names, n_streams, n_ops, n_parts;
+  const int32_t *part_rep; /* [n_parts] class representative of each partition
+                              (Sec. 3.7); NULL = no layer dedup                   */
+  uint32_t flags;          /* OPATTR_* layout hints                               */
+} opattr_dims;
+
+/* One row of the per-operator table (the "aggregated" block of profile.json).
+   Row n_ops is the UNATTRIBUTED bucket. value[c] is NaN when the row has no
+   matched kernel or counter c is absent. */
+typedef struct {
+  uint64_t kernel_count, total_ns, matched_count, matched_ns;
+  double value[OPATTR_NUM_COUNTERS];
+} opattr_op_row; /* 192 bytes */
+
+typedef struct {
+  uint64_t total_ns, attributed_ns, unattributed_ns, matched_ns;
+  double attributed_fraction; /* attributed_ns / total_ns, NaN if total is 0 */
+} opattr_summary;
+
+/* Error classes (bits of opattr_diag.flags) and status codes. */
+#define OPATTR_F_DATA 1u        /* an id out of range / a range with start > end */
+#define OPATTR_F_ORDER 2u       /* duplicate seq, or a promised layout is false   */
+#define OPATTR_F_LIMIT 4u       /* range nesting deeper than 255                  */
+#define OPATTR_F_NOT_NESTED 8u  /* two ranges of one stream cross                 */
+#define OPATTR_F_PARTITION 16u  /* a partition is not one contiguous seq run      */
+#define OPATTR_F_DEDUP 32u      /* positional inheritance failed for a duplicate  */
+#define OPATTR_F_COUNT 64u      /* per-name invocation counts differ              */
+
+#define OPATTR_OK 0
+#define OPATTR_ERR_INVALID_ARG (-1) /* host: NULL pointer, bad size or enum      */
+#define OPATTR_ERR_WORKSPACE (-2)   /* host: workspace smaller than required     */
+#define OPATTR_ERR_HIP (-3)         /* host: a HIP launch failed                 */
+#define OPATTR_ERR_COUNT_MISMATCH (-4) /* diag: STRICT policy and counts differ  */
+#define OPATTR_ERR_NOT_NESTED (-5)  /* diag */
+#define OPATTR_ERR_DEDUP (-6)       /* diag */
+#define OPATTR_ERR_PARTITION (-7)   /* diag */
+#define OPATTR_ERR_ORDER (-8)       /* diag */
+#define OPATTR_ERR_DATA (-9)        /* diag */
+#define OPATTR_ERR_LIMIT (-10)      /* diag */
+
+/* Device-resident error record. status is the highest-precedence flagged class
+   in the order DATA, ORDER, LIMIT, NOT_NESTED, PARTITION, DEDUP, COUNT (COUNT
+   only under OPATTR_MISMATCH_STRICT). Counters:
+     names_mismatched  names whose eligible-launch and profiled-row counts differ
+     nesting_errors    streams holding two crossing ranges
+     tl_unmatched      sum over names of max(0, launches - rows)
+     pf_unmatched      sum over names of max(0, rows - launches)
+     dedup_errors      duplicate launches left unmatched by a failed lookup
+     bad_records       records ignored because an id is out of range
+     order_violations  layout-promise violations found under OPATTR_VALIDATE */
+typedef struct {
+  int32_t status;
+  uint32_t flags;
+  uint32_t names_mismatched;
+  uint32_t nesting_errors;
+  uint64_t tl_unmatched, pf_unmatched, dedup_errors, bad_records;
+  uint64_t order_violations;
+  uint32_t strict; /* set by opattr_match under OPATTR_MISMATCH_STRICT */
+  uint32_t reserved;
+} opattr_diag;
+
+/* Count-mismatch policy of opattr_match (Sec. 3.3 and its limitations note):
+   PREFIX    Alg. 1 as printed: per name the first min(launches, rows) launches
+             take rows in order, the excess gets none;
+   SKIP_NAME a name whose counts differ gets no rows at all;
+   STRICT    PREFIX outputs, and status OPATTR_ERR_COUNT_MISMATCH. */
+enum { OPATTR_MISMATCH_PREFIX = 0, OPATTR_MISMATCH_SKIP_NAME = 1, OPATTR_MISMATCH_STRICT = 2 };
+
+/* Aggregation kind per counter (counter appendix table). */
+enum { OPATTR_AGG_SUM = 0, OPATTR_AGG_DWMEAN = 1, OPATTR_AGG_MAX = 2 };
+
+/* Workspace bytes every entry point needs for these sizes and hints (host,
+   pure, enqueues nothing). Pass NULL for an absent input set. */
+size_t opattr_workspace_bytes(const opattr_kernels *k, const opattr_profiled *p,
+                              const opattr_ranges *r, const opattr_dims *d);
+
+/* Zero the device diag record (enqueued on stream). Every entry point adds to
+   the record, so clear it before a fresh run. */
+int opattr_diag_clear(opattr_diag *diag, void *stream);
+
+/* Copy the device diag record to the host (synchronises the stream). */
+int opattr_read_diag(const opattr_diag *diag, opattr_diag *host_out, void *stream);
+
+/* Invocation-order matching (Alg. 1). For every launch eligible for replay (no
+   partition, or a partition that is its own class representative) in seq
+   order, the k-th launch of a name takes the k-th profiled row of that name.
+   Out: match[k->n] (all launches; ineligible ones get -1), name_counts
+   [n_names][2] = (eligible launches, profiled rows) or NULL. */
+int opattr_match(const opattr_kernels *k, const opattr_profiled *p, const opattr_dims *d,
+                 int policy, int32_t *match, uint32_t *name_counts, opattr_diag *diag,
+                 void *ws, size_t ws_bytes, void *stream);
+
+/* Layer dedup (Sec. 3.7). A launch of a duplicate partition q (part_rep[q] !=
+   q) at launch-order position x of q takes match[] of the launch at position x
+   of partition part_rep[q]; if that launch does not exist or has another name,
+   or either partition is not one contiguous seq run, it gets -1 and counts as a
+   dedup error. In/out: match[k->n]. */
+int opattr_dedup_broadcast(const opattr_kernels *k, const opattr_dims *d, int32_t *match,
+                           opattr_diag *diag, void *ws, size_t ws_bytes, void *stream);
+
+/* Enclosure (Alg. 2): range_id[i] = the range r on stream_id[i] with
+   start_r <= q_i <= end_r that is last in nesting order (start asc, end desc,
+   index asc) -- the innermost one -- or -1. q_i = query_ns[i] (or start_ns[i]).
+   range_depth[r] (or NULL) = 1 + depth of the nearest earlier range of the
+   stream in nesting order whose end is not before end_r (0 for a bad range). */
+int opattr_enclose(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,
+                   int32_t *range_id, uint8_t *range_depth, opattr_diag *diag, void *ws,
+                   size_t ws_bytes, void *stream);
+
+/* Aggregation (Eq. 1). Row g = op_id[range_id[i]] (or n_ops when range_id is
+   -1) collects kernel_count and total_ns of every launch, and over launches
+   with match >= 0: matched_count, matched_ns and, per counter c with
+   m = counters[match][c] widened to fp64, SUM m, DWMEAN (sum m*d)/matched_ns,
+   or MAX m. agg_kind (host, 20 entries) or NULL for the appendix table's kinds.
+   Out: table[n_ops + 1], sum (device). */
+int opattr_aggregate(const opattr_kernels *k, const opattr_profiled *p, const int32_t *match,
+                     const int32_t *range_id, const opattr_ranges *r, const opattr_dims *d,
+                     const uint8_t *agg_kind, opattr_op_row *table, opattr_summary *sum,
+                     opattr_diag *diag, void *ws, size_t ws_bytes, void *stream);
+
+/* All four stages: match, dedup, enclose, aggregate. */
+int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const opattr_ranges *r,
+                     const opattr_dims *d, int policy, const uint8_t *agg_kind, int32_t *match,
+                     int32_t *range_id, uint8_t *range_depth, uint32_t *name_counts,
+                     opattr_op_row *table, opattr_summary *sum, opattr_diag *diag, void *ws,
+                     size_t ws_bytes, void *stream);
+
+/* Human-readable name of a status code. */
+const char *opattr_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

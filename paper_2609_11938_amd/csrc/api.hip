@@ -1,0 +1,365 @@
+// C ABI entry points of libopattr: argument checks, workspace plan, stage
+// sequencing on the caller's stream.
+#include <string.h>
+
+#include "common.h"
+#include "impl.h"
+
+namespace opa {
+
+static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Bump {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + (bytes ? bytes : 1));
+    return o;
+  }
+};
+
+static bool has_dedup(const opattr_kernels *k, const opattr_dims *d) {
+  return k && k->part_id && d->part_rep && d->n_parts > 0;
+}
+
+Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_ranges *r,
+               const opattr_dims *d) {
+  Plan pl{};
+  pl.T = k ? k->n : 0;
+  pl.P = p ? p->n : 0;
+  pl.R = r ? r->n : 0;
+  pl.NN = d->n_names;
+  pl.NS = d->n_streams;
+  pl.G = d->n_ops + 1;
+  pl.NP = d->n_parts;
+  pl.seq_dense = (d->flags & OPATTR_SEQ_DENSE) != 0;
+  pl.ranges_nested = (d->flags & OPATTR_RANGES_NESTED) != 0;
+  pl.nt = (pl.T + OPA_TILE - 1) / OPA_TILE;
+  pl.ntp = (pl.P + OPA_TILE - 1) / OPA_TILE;
+  pl.ncht = (pl.nt + kColChunk - 1) / kColChunk;
+  pl.nchp = (pl.ntp + kColChunk - 1) / kColChunk;
+  pl.ntr_max = pl.R / kRangeTile + (int64_t)pl.NS + 1;
+  const bool dd = has_dedup(k, d);
+  const size_t T = (size_t)pl.T, P = (size_t)pl.P, R = (size_t)pl.R, NN = pl.NN;
+  Bump b;
+  pl.sv = b.take(T * 4);
+  pl.rk = b.take(pl.seq_dense ? 0 : T * 4);
+  pl.seqsort_k0 = b.take(pl.seq_dense ? 0 : T * 8);
+  pl.seqsort_k1 = b.take(pl.seq_dense ? 0 : T * 8);
+  pl.seqsort_v0 = b.take(pl.seq_dense ? 0 : T * 4);
+  pl.seqsort_v1 = b.take(pl.seq_dense ? 0 : T * 4);
+  pl.rs_hist = b.take(radix_hist_entries(pl.T > pl.R ? pl.T : pl.R) * 4);
+  pl.tlh = b.take((size_t)pl.nt * NN * 4);
+  pl.pfh = b.take((size_t)pl.ntp * NN * 4);
+  pl.tlch = b.take((size_t)pl.ncht * NN * 4);
+  pl.pfch = b.take((size_t)pl.nchp * NN * 4);
+  pl.tlc = b.take(NN * 4);
+  pl.pfc = b.take(NN * 4);
+  pl.off = b.take(NN * 4);
+  pl.slot = b.take(P * 4);
+  pl.pfirst = b.take(dd ? (size_t)pl.NP * 4 : 0);
+  pl.plast = b.take(dd ? (size_t)pl.NP * 4 : 0);
+  pl.pcnt = b.take(dd ? (size_t)pl.NP * 4 : 0);
+  pl.contig = b.take(dd ? (size_t)pl.NP : 0);
+  pl.mbs = b.take(dd ? T * 4 : 0);
+  pl.nbs = b.take(dd ? T * 4 : 0);
+  const bool rs = !pl.ranges_nested;
+  pl.rperm = b.take(rs ? R * 4 : 0);
+  pl.rs_c = b.take(rs ? R * 8 : 0);
+  pl.re_c = b.take(rs ? R * 8 : 0);
+  pl.rst_c = b.take(rs ? R * 2 : 0);
+  pl.rop_c = b.take(rs ? R * 4 : 0);
+  pl.rsort_k0 = b.take(rs ? R * 8 : 0);
+  pl.rsort_k1 = b.take(rs ? R * 8 : 0);
+  pl.rsort_v0 = b.take(rs ? R * 4 : 0);
+  pl.rsort_v1 = b.take(rs ? R * 4 : 0);
+  pl.ree = b.take(R * 8);
+  pl.npg = b.take(R * 4);
+  pl.mxv = b.take(R * 8);
+  pl.rblk = b.take(((size_t)pl.NS + 1) * 8);
+  pl.tbase = b.take(((size_t)pl.NS + 1) * 4);
+  const size_t ntr = (size_t)pl.ntr_max;
+  pl.tM = b.take(ntr * 8);
+  pl.tnpg = b.take(ntr * 4);
+  pl.tnpg2 = b.take(ntr * 4);
+  pl.tmx = b.take(ntr * 8);
+  pl.tmx2 = b.take(ntr * 8);
+  pl.tfirst = b.take(ntr * 4);
+  pl.tlast = b.take(ntr * 4);
+  pl.sflag = b.take(pl.NS);
+  pl.acc = b.take((size_t)pl.G * sizeof(AccRow));
+  pl.misc = b.take(256);
+  pl.total = b.off;
+  return pl;
+}
+
+// nesting_errors from the per-stream crossing flags; status from the flags
+__global__ void __launch_bounds__(256) k_finish(opattr_diag *diag, const uint8_t *sflag,
+                                                uint32_t ns) {
+  __shared__ uint32_t cnt;
+  if (threadIdx.x == 0) cnt = 0;
+  __syncthreads();
+  if (sflag) {
+    uint32_t c = 0;
+    for (uint32_t s = threadIdx.x; s < ns; s += 256) c += sflag[s] ? 1u : 0u;
+    if (c) atomicAdd(&cnt, c);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    if (sflag) diag->nesting_errors = cnt;
+    uint32_t f = diag->flags;
+    if (diag->nesting_errors) f |= OPATTR_F_NOT_NESTED;
+    if (diag->bad_records) f |= OPATTR_F_DATA;
+    if (diag->dedup_errors) f |= OPATTR_F_DEDUP;
+    diag->flags = f;
+    int32_t st = 0;
+    if (f & OPATTR_F_DATA) st = OPATTR_ERR_DATA;
+    else if (f & OPATTR_F_ORDER) st = OPATTR_ERR_ORDER;
+    else if (f & OPATTR_F_LIMIT) st = OPATTR_ERR_LIMIT;
+    else if (f & OPATTR_F_NOT_NESTED) st = OPATTR_ERR_NOT_NESTED;
+    else if (f & OPATTR_F_PARTITION) st = OPATTR_ERR_PARTITION;
+    else if (f & OPATTR_F_DEDUP) st = OPATTR_ERR_DEDUP;
+    else if ((f & OPATTR_F_COUNT) && diag->strict) st = OPATTR_ERR_COUNT_MISMATCH;
+    diag->status = st;
+  }
+}
+
+void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s) {
+  k_finish<<<1, 256, 0, s>>>(diag, sflag, ns);
+}
+
+static const uint8_t kDefaultKind[OPATTR_NUM_COUNTERS] = {
+    // counter appendix table, rows 1..20: SUM for additive counts, DW-mean for
+    // rates and utilisations, MAX for per-kernel constants
+    OPATTR_AGG_SUM,    OPATTR_AGG_SUM,    OPATTR_AGG_SUM,    OPATTR_AGG_DWMEAN,
+    OPATTR_AGG_DWMEAN, OPATTR_AGG_DWMEAN, OPATTR_AGG_DWMEAN, OPATTR_AGG_DWMEAN,
+    OPATTR_AGG_DWMEAN, OPATTR_AGG_DWMEAN, OPATTR_AGG_SUM,    OPATTR_AGG_DWMEAN,
+    OPATTR_AGG_DWMEAN, OPATTR_AGG_DWMEAN, OPATTR_AGG_SUM,    OPATTR_AGG_DWMEAN,
+    OPATTR_AGG_DWMEAN, OPATTR_AGG_MAX,    OPATTR_AGG_SUM,    OPATTR_AGG_MAX};
+
+static const int64_t kMaxN = (int64_t)1 << 31;
+
+static bool ok_n(int64_t n) { return n >= 0 && n < kMaxN; }
+
+static bool check_dims(const opattr_dims *d) {
+  if (!d) return false;
+  if (d->n_names > kMaxNames) return false;
+  if (d->n_streams > 65536u) return false;
+  if (d->n_ops >= 0x7FFFFFFFu || d->n_parts >= 0x7FFFFFFFu) return false;
+  if (d->flags & ~(OPATTR_KERNELS_STREAM_MAJOR | OPATTR_SEQ_DENSE | OPATTR_RANGES_NESTED |
+                   OPATTR_VALIDATE))
+    return false;
+  return true;
+}
+
+static bool check_kernels(const opattr_kernels *k, bool need_match, bool need_enc,
+                          bool need_agg) {
+  if (!k || !ok_n(k->n)) return false;
+  if (k->n == 0) return true;
+  if (need_match && (!k->seq || !k->name_id)) return false;
+  if (need_enc && (!k->stream_id || !(k->query_ns || k->start_ns))) return false;
+  if (need_agg && !k->dur_ns) return false;
+  return true;
+}
+
+static bool check_profiled(const opattr_profiled *p, bool need_names, bool need_counters) {
+  if (!p || !ok_n(p->n)) return false;
+  if (p->n == 0) return true;
+  if (need_names && !p->name_id) return false;
+  if (need_counters && (!p->counters || p->row_stride < 0 || p->col_stride < 0)) return false;
+  return true;
+}
+
+static bool check_ranges(const opattr_ranges *r) {
+  if (!r || !ok_n(r->n)) return false;
+  if (r->n == 0) return true;
+  return r->start_ns && r->end_ns && r->stream_id && r->op_id;
+}
+
+static int launch_status() {
+  const hipError_t launch = hipGetLastError();
+  const hipError_t first = g_hip_error;
+  g_hip_error = hipSuccess;
+  return (launch == hipSuccess && first == hipSuccess) ? OPATTR_OK : OPATTR_ERR_HIP;
+}
+
+}  // namespace opa
+
+using namespace opa;
+
+extern "C" {
+
+size_t opattr_workspace_bytes(const opattr_kernels *k, const opattr_profiled *p,
+                              const opattr_ranges *r, const opattr_dims *d) {
+  if (!d) return 0;
+  return make_plan(k, p, r, d).total;
+}
+
+int opattr_diag_clear(opattr_diag *diag, void *stream) {
+  if (!diag) return OPATTR_ERR_INVALID_ARG;
+  note(hipMemsetAsync(diag, 0, sizeof(opattr_diag), (hipStream_t)stream));
+  return launch_status();
+}
+
+int opattr_read_diag(const opattr_diag *diag, opattr_diag *host_out, void *stream) {
+  if (!diag || !host_out) return OPATTR_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  if (hipMemcpyAsync(host_out, diag, sizeof(opattr_diag), hipMemcpyDeviceToHost, s) != hipSuccess)
+    return OPATTR_ERR_HIP;
+  if (hipStreamSynchronize(s) != hipSuccess) return OPATTR_ERR_HIP;
+  return OPATTR_OK;
+}
+
+int opattr_match(const opattr_kernels *k, const opattr_profiled *p, const opattr_dims *d,
+                 int policy, int32_t *match, uint32_t *name_counts, opattr_diag *diag, void *ws,
+                 size_t ws_bytes, void *stream) {
+  if (!check_dims(d) || !check_kernels(k, true, false, false) || !check_profiled(p, true, false) ||
+      !diag || policy < 0 || policy > 2 || (k->n > 0 && !match))
+    return OPATTR_ERR_INVALID_ARG;
+  const Plan pl = make_plan(k, p, nullptr, d);
+  if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
+  build_seq_view(k, d, ws, pl, diag, validate, s);
+  IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, false, validate};
+  run_match(a, s);
+  launch_finish(diag, nullptr, 0, s);
+  return launch_status();
+}
+
+int opattr_dedup_broadcast(const opattr_kernels *k, const opattr_dims *d, int32_t *match,
+                           opattr_diag *diag, void *ws, size_t ws_bytes, void *stream) {
+  if (!check_dims(d) || !check_kernels(k, true, false, false) || !diag ||
+      (k->n > 0 && !match))
+    return OPATTR_ERR_INVALID_ARG;
+  const Plan pl = make_plan(k, nullptr, nullptr, d);
+  if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  if (has_dedup(k, d)) {
+    build_seq_view(k, d, ws, pl, diag, (d->flags & OPATTR_VALIDATE) != 0, s);
+    run_dedup(k, d, match, diag, ws, pl, false, s);
+  }
+  launch_finish(diag, nullptr, 0, s);
+  return launch_status();
+}
+
+int opattr_enclose(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,
+                   int32_t *range_id, uint8_t *range_depth, opattr_diag *diag, void *ws,
+                   size_t ws_bytes, void *stream) {
+  if (!check_dims(d) || !check_kernels(k, false, true, false) || !check_ranges(r) || !diag ||
+      (k->n > 0 && !range_id))
+    return OPATTR_ERR_INVALID_ARG;
+  const Plan pl = make_plan(k, nullptr, r, d);
+  if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
+  const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s);
+  resolve_ranges(cr, d, ws, pl, range_depth, diag, s);
+  EncArgs e{};
+  e.mode = kEncloseOnly;
+  e.k = k;
+  e.cr = cr;
+  e.d = d;
+  e.range_id = range_id;
+  e.diag = diag;
+  e.ws = ws;
+  e.pl = &pl;
+  run_enclose_aggregate(e, s);
+  launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s);
+  return launch_status();
+}
+
+static bool kinds_ok(const uint8_t *agg_kind) {
+  if (!agg_kind) return true;
+  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c)
+    if (agg_kind[c] > OPATTR_AGG_MAX) return false;
+  return true;
+}
+
+int opattr_aggregate(const opattr_kernels *k, const opattr_profiled *p, const int32_t *match,
+                     const int32_t *range_id, const opattr_ranges *r, const opattr_dims *d,
+                     const uint8_t *agg_kind, opattr_op_row *table, opattr_summary *sum,
+                     opattr_diag *diag, void *ws, size_t ws_bytes, void *stream) {
+  if (!check_dims(d) || !check_kernels(k, false, false, true) || !check_profiled(p, false, true) ||
+      !check_ranges(r) || !diag || !table || !sum || !kinds_ok(agg_kind) ||
+      (k->n > 0 && (!match || !range_id)))
+    return OPATTR_ERR_INVALID_ARG;
+  const Plan pl = make_plan(k, p, r, d);
+  if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  EncArgs e{};
+  e.mode = kAggregateOnly;
+  e.k = k;
+  e.p = p;
+  e.match = match;
+  e.r = r;
+  e.d = d;
+  e.range_id = const_cast<int32_t *>(range_id);
+  e.agg_kind = agg_kind ? agg_kind : kDefaultKind;
+  e.table = table;
+  e.sum = sum;
+  e.diag = diag;
+  e.ws = ws;
+  e.pl = &pl;
+  run_enclose_aggregate(e, s);
+  launch_finish(diag, nullptr, 0, s);
+  return launch_status();
+}
+
+int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const opattr_ranges *r,
+                     const opattr_dims *d, int policy, const uint8_t *agg_kind, int32_t *match,
+                     int32_t *range_id, uint8_t *range_depth, uint32_t *name_counts,
+                     opattr_op_row *table, opattr_summary *sum, opattr_diag *diag, void *ws,
+                     size_t ws_bytes, void *stream) {
+  if (!check_dims(d) || !check_kernels(k, true, true, true) || !check_profiled(p, true, true) ||
+      !check_ranges(r) || !diag || !table || !sum || policy < 0 || policy > 2 ||
+      !kinds_ok(agg_kind) || (k->n > 0 && (!match || !range_id)))
+    return OPATTR_ERR_INVALID_ARG;
+  const Plan pl = make_plan(k, p, r, d);
+  if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
+  build_seq_view(k, d, ws, pl, diag, validate, s);
+  IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, validate};
+  run_match(a, s);
+  run_dedup(k, d, match, diag, ws, pl, true, s);
+  const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s);
+  resolve_ranges(cr, d, ws, pl, range_depth, diag, s);
+  EncArgs e{};
+  e.mode = kEncloseAggregate;
+  e.k = k;
+  e.p = p;
+  e.match = match;
+  e.r = r;
+  e.cr = cr;
+  e.d = d;
+  e.range_id = range_id;
+  e.agg_kind = agg_kind ? agg_kind : kDefaultKind;
+  e.table = table;
+  e.sum = sum;
+  e.diag = diag;
+  e.ws = ws;
+  e.pl = &pl;
+  run_enclose_aggregate(e, s);
+  launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s);
+  return launch_status();
+}
+
+const char *opattr_strerror(int status) {
+  switch (status) {
+    case OPATTR_OK: return "ok";
+    case OPATTR_ERR_INVALID_ARG: return "invalid argument";
+    case OPATTR_ERR_WORKSPACE: return "workspace too small";
+    case OPATTR_ERR_HIP: return "HIP launch failed";
+    case OPATTR_ERR_COUNT_MISMATCH: return "per-name invocation counts differ (strict policy)";
+    case OPATTR_ERR_NOT_NESTED: return "ranges of a stream cross";
+    case OPATTR_ERR_DEDUP: return "positional dedup lookup failed";
+    case OPATTR_ERR_PARTITION: return "a partition is not one contiguous run of launches";
+    case OPATTR_ERR_ORDER: return "launch order violated (duplicate seq or false layout promise)";
+    case OPATTR_ERR_DATA: return "id out of range or malformed range";
+    case OPATTR_ERR_LIMIT: return "range nesting deeper than 255";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,181 @@
+// Device primitives shared by the opattr kernels (gfx950, wave64).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/opattr.h"
+
+#define OPA_WAVE 64
+#define OPA_TILE 4096          // elements per LDS tile (seq tiles, profiled tiles)
+#define OPA_TILE_THREADS 256   // 4 waves, 16 elements per thread
+#define OPA_TILE_CHUNKS (OPA_TILE / OPA_TILE_THREADS)
+#define OPA_SLOT_BITS 12       // log2(OPA_TILE)
+
+static_assert((1 << OPA_SLOT_BITS) == OPA_TILE, "tile size");
+
+namespace opa {
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (OPA_WAVE - 1)); }
+__device__ __forceinline__ int wave_id() { return (int)(threadIdx.x / OPA_WAVE); }
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  return (1ull << lane_id()) - 1ull;
+}
+
+// Lanes of the wave holding the same 8-bit digit (match-any built from one
+// ballot per bit: the published warp-multisplit peer-mask construction).
+__device__ __forceinline__ uint64_t peers8(uint32_t d) {
+  uint64_t m = ~0ull;
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const uint64_t v = __ballot((d >> b) & 1u);
+    m &= ((d >> b) & 1u) ? v : ~v;
+  }
+  return m;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_incl_scan_add(T x) {
+  const int l = lane_id();
+#pragma unroll
+  for (int o = 1; o < OPA_WAVE; o <<= 1) {
+    T y = __shfl_up(x, o, OPA_WAVE);
+    if (l >= o) x += y;
+  }
+  return x;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_incl_scan_max(T x) {
+  const int l = lane_id();
+#pragma unroll
+  for (int o = 1; o < OPA_WAVE; o <<= 1) {
+    T y = __shfl_up(x, o, OPA_WAVE);
+    if (l >= o) x = y > x ? y : x;
+  }
+  return x;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_reduce_add(T x) {
+#pragma unroll
+  for (int o = OPA_WAVE / 2; o > 0; o >>= 1) x += __shfl_xor(x, o, OPA_WAVE);
+  return x;
+}
+
+// Exclusive scan across a 256-thread block of one value per thread.
+// `sh` needs 4 entries. Returns the exclusive prefix; *total gets the sum.
+template <typename T>
+__device__ __forceinline__ T block_excl_scan_add(T x, T *sh, T *total) {
+  T inc = wave_incl_scan_add(x);
+  const int w = wave_id(), l = lane_id();
+  if (l == OPA_WAVE - 1) sh[w] = inc;
+  __syncthreads();
+  T base = 0, tot = 0;
+  for (int i = 0; i < (int)(blockDim.x / OPA_WAVE); ++i) {
+    if (i < w) base += sh[i];
+    tot += sh[i];
+  }
+  __syncthreads();
+  if (total) *total = tot;
+  return base + inc - x;
+}
+
+// Inclusive max-scan across the block; values per thread, block of 256.
+template <typename T>
+__device__ __forceinline__ T block_incl_scan_max(T x, T *sh) {
+  T inc = wave_incl_scan_max(x);
+  const int w = wave_id(), l = lane_id();
+  if (l == OPA_WAVE - 1) sh[w] = inc;
+  __syncthreads();
+  T base = inc;
+  for (int i = 0; i < w; ++i) base = sh[i] > base ? sh[i] : base;
+  __syncthreads();
+  return base;
+}
+
+// ---------------------------------------------------------------------------
+// Stable LDS radix sort of one tile of OPA_TILE 32-bit keys by bits
+// [lo_bit, lo_bit + nbits), 8 bits per pass, 256 threads. Element order is
+// index order (chunk c, thread t) -> index c*256 + t. `a` holds the keys and
+// receives the result; `b` is scratch of the same size; `cnt` needs
+// OPA_TILE_CHUNKS * 4 * 256 uint16 entries; `dbase` 256 + 4 uint32 entries.
+// ---------------------------------------------------------------------------
+struct TileSortSmem {
+  uint16_t cnt[OPA_TILE_CHUNKS][OPA_TILE_THREADS / OPA_WAVE][256];
+  uint32_t dbase[256];
+  uint32_t sh[8];
+};
+
+__device__ inline void tile_radix_sort(uint32_t *a, uint32_t *b, TileSortSmem &sm, int lo_bit,
+                                       int nbits) {
+  const int tid = threadIdx.x, w = wave_id();
+  for (int shift = lo_bit; shift < lo_bit + nbits; shift += 8) {
+    const int take = (lo_bit + nbits - shift) < 8 ? (lo_bit + nbits - shift) : 8;
+    const uint32_t mask = (1u << take) - 1u;
+    // per (chunk, wave) digit counts
+    for (int i = tid; i < OPA_TILE_CHUNKS * 4 * 256; i += OPA_TILE_THREADS)
+      (&sm.cnt[0][0][0])[i] = 0;
+    __syncthreads();
+    uint32_t lrank[OPA_TILE_CHUNKS];
+    uint32_t dig[OPA_TILE_CHUNKS];
+#pragma unroll
+    for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
+      const uint32_t k = a[c * OPA_TILE_THREADS + tid];
+      const uint32_t d = (k >> shift) & mask;
+      const uint64_t pm = peers8(d);
+      dig[c] = d;
+      lrank[c] = (uint32_t)__popcll(pm & lanemask_lt());
+      if ((pm & lanemask_lt()) == 0) sm.cnt[c][w][d] = (uint16_t)__popcll(pm);
+    }
+    __syncthreads();
+    // thread d scans its digit over (chunk, wave) in index order
+    {
+      const int d = tid;
+      uint32_t run = 0;
+      for (int c = 0; c < OPA_TILE_CHUNKS; ++c)
+        for (int ww = 0; ww < OPA_TILE_THREADS / OPA_WAVE; ++ww) {
+          const uint32_t v = sm.cnt[c][ww][d];
+          sm.cnt[c][ww][d] = (uint16_t)run;
+          run += v;
+        }
+      uint32_t tot;
+      const uint32_t base = block_excl_scan_add<uint32_t>(run, sm.sh, &tot);
+      sm.dbase[d] = base;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
+      const uint32_t d = dig[c];
+      const uint32_t dst = sm.dbase[d] + sm.cnt[c][w][d] + lrank[c];
+      b[dst] = a[c * OPA_TILE_THREADS + tid];
+    }
+    __syncthreads();
+    for (int i = tid; i < OPA_TILE; i += OPA_TILE_THREADS) a[i] = b[i];
+    __syncthreads();
+  }
+}
+
+__device__ __forceinline__ int bits_for(uint32_t v) {  // bits to hold values 0..v
+  return v == 0 ? 1 : 32 - __clz(v);
+}
+
+// first index in sorted LDS array a[0..n) with a[i] >= x
+__device__ __forceinline__ int lds_lower_bound(const uint32_t *a, int n, uint32_t x) {
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    int mid = (lo + hi) >> 1;
+    if (a[mid] < x) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Diag helpers: device-scope atomics on the caller's record.
+__device__ __forceinline__ void diag_flag(opattr_diag *d, uint32_t f) {
+  if (d) atomicOr(&d->flags, f);
+}
+__device__ __forceinline__ void diag_add(unsigned long long *p, unsigned long long v) {
+  if (v) atomicAdd(p, v);
+}
+
+}  // namespace opa

@@ -1,0 +1,134 @@
+// Internal interfaces of libopattr: workspace plan and kernel launchers.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/opattr.h"
+
+namespace opa {
+
+constexpr int kRangeTile = 1024;    // ranges per local-NPG tile
+constexpr int kColChunk = 64;       // rows per chunk of the column scans
+constexpr int kEncThreads = 256;    // kernels per enclose/aggregate block
+constexpr int kEncWindow = 1024;    // range starts staged in LDS per block
+constexpr int kMaxWalk = 300;       // bound on parent-chain walks (depth <= 255)
+constexpr uint32_t kMaxNames = (1u << 20) - 1;
+
+// Accumulator row of the aggregation (device scratch), one per operator.
+struct AccRow {
+  unsigned long long kc, tns, mc, mns;
+  double sum[OPATTR_NUM_COUNTERS];
+  uint32_t maxk[OPATTR_NUM_COUNTERS];  // order-preserving key of the fp32 max
+  uint32_t nanmask;                    // bit c: a NaN reached a MAX counter
+  uint32_t pad;
+};
+
+// Byte offsets of every scratch array inside the caller's workspace.
+struct Plan {
+  int64_t T, P, R;
+  uint32_t NN, NS, G, NP;
+  int64_t nt, ntp, ncht, nchp, ntr_max;
+  bool seq_dense, ranges_nested;
+  size_t total;
+  // IOM
+  size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist;
+  size_t tlh, pfh, tlch, pfch, tlc, pfc, off, slot;
+  size_t pfirst, plast, pcnt, contig, mbs, nbs;
+  // ranges
+  size_t rperm, rs_c, re_c, rst_c, rop_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
+  size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
+  // aggregation
+  size_t acc;
+  size_t misc;  // small device scalars
+};
+
+Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_ranges *r,
+               const opattr_dims *d);
+
+// First HIP error of the calling host thread since the last reset; entry
+// points report it as OPATTR_ERR_HIP.
+inline thread_local hipError_t g_hip_error = hipSuccess;
+inline void note(hipError_t e) {
+  if (e != hipSuccess && g_hip_error == hipSuccess) g_hip_error = e;
+}
+
+template <typename T>
+inline T *at(void *ws, size_t off) {
+  return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
+}
+
+// Core view of the ranges: nesting order per stream.
+struct CoreRanges {
+  int64_t n;
+  const uint64_t *s;
+  const uint64_t *e;
+  const uint16_t *st;
+  const uint32_t *op;
+  const int32_t *perm;  // core position -> input index; NULL = identity
+};
+
+// ---- radix sort (sort.hip) -------------------------------------------------
+// Stable LSD sort of (key, value) pairs over bits [begin_bit, end_bit).
+// Result ends in (k0, v0) when the pass count is even, else (k1, v1); returns
+// true when the result is in k1/v1.
+bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, int64_t n,
+                      int begin_bit, int end_bit, uint32_t *hist, hipStream_t s);
+size_t radix_hist_entries(int64_t n);
+void launch_iota(uint32_t *v, int64_t n, hipStream_t s);
+void launch_gather_key_u64(const uint64_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
+                           bool invert, hipStream_t s);
+void launch_gather_key_u16(const uint16_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
+                           hipStream_t s);
+void launch_gather_key_u32(const uint32_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
+                           hipStream_t s);
+
+// ---- IOM (iom.hip) -----------------------------------------------------------
+struct IomArgs {
+  const opattr_kernels *k;
+  const opattr_profiled *p;
+  const opattr_dims *d;
+  int policy;
+  int32_t *match;
+  uint32_t *name_counts;
+  opattr_diag *diag;
+  void *ws;
+  const Plan *pl;
+  bool want_dedup;  // also collect partition statistics and dedup sources
+  bool validate;
+};
+void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, const Plan &pl,
+                    opattr_diag *diag, bool validate, hipStream_t s);
+void run_match(const IomArgs &a, hipStream_t s);
+void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, opattr_diag *diag,
+               void *ws, const Plan &pl, bool stats_ready, hipStream_t s);
+
+// ---- ranges and enclosure (ranges.hip, enclose.hip) ----------------------------
+CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws, const Plan &pl,
+                          opattr_diag *diag, bool validate, hipStream_t s);
+void resolve_ranges(const CoreRanges &cr, const opattr_dims *d, void *ws, const Plan &pl,
+                    uint8_t *range_depth, opattr_diag *diag, hipStream_t s);
+
+enum EncMode { kEncloseOnly = 1, kAggregateOnly = 2, kEncloseAggregate = 3 };
+struct EncArgs {
+  EncMode mode;
+  const opattr_kernels *k;
+  const opattr_profiled *p;  // aggregation
+  const int32_t *match;      // aggregation
+  const opattr_ranges *r;    // input ranges (aggregate-only: op ids by input index)
+  CoreRanges cr;             // enclosure
+  const opattr_dims *d;
+  int32_t *range_id;         // out (enclose) or in (aggregate-only)
+  const uint8_t *agg_kind;   // host, 20 entries
+  opattr_op_row *table;
+  opattr_summary *sum;
+  opattr_diag *diag;
+  void *ws;
+  const Plan *pl;
+};
+void run_enclose_aggregate(const EncArgs &a, hipStream_t s);
+
+// ---- finish (api.hip) ---------------------------------------------------------
+void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s);
+
+}  // namespace opa

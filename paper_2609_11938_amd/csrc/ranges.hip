@@ -1,0 +1,377 @@
+// Range structure for the enclosure (Sec. 3.5, Alg. 2).
+//
+// The paper keeps a per-stream interval tree. Here the ranges of each stream
+// sit in nesting order (start asc, end desc, index asc) and every range gets
+// its parent: the nearest earlier range of the stream whose end is not before
+// its own (that range contains it). A launch's innermost range is then the last
+// range starting at or before its query point, or the first ancestor of that
+// range whose end is not before the query point.
+//
+// Parents are "nearest previous greater-or-equal" values, found without a
+// sequential stack: pointer jumping inside LDS tiles of 1024 ranges, the same
+// jumping over tile maxima, then one bounded walk for the ranges whose parent
+// lies in an earlier tile. While jumping, each range also records the largest
+// end it skipped; a skipped end beyond the range's start is a crossing.
+#include "common.h"
+#include "impl.h"
+
+namespace opa {
+
+constexpr uint64_t kEndLimit = 1ull << 63;  // valid ends stay below 2^63
+
+// validity, effective ends and stream blocks
+__global__ void k_rprep(CoreRanges cr, uint32_t NS, uint32_t NOPS, int64_t *ree, int32_t *npg,
+                        opattr_diag *diag) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  bool bad = false;
+  if (x < cr.n) {
+    const uint64_t s = cr.s[x], e = cr.e[x];
+    const bool ok = cr.st[x] < NS && cr.op[x] < NOPS && s <= e && e < kEndLimit;
+    ree[x] = ok ? (int64_t)e : -1;
+    npg[x] = -1;
+    bad = !ok;
+  }
+  const uint64_t m = __ballot(bad);
+  if (m && lane_id() == __ffsll((unsigned long long)m) - 1)
+    atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)__popcll(m));
+}
+
+// promised nesting order: (stream, start asc, end desc) never decreases
+__global__ void k_rcheck(CoreRanges cr, opattr_diag *diag) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  bool bad = false;
+  if (x > 0 && x < cr.n) {
+    const uint16_t a = cr.st[x - 1], b = cr.st[x];
+    bad = a > b || (a == b && (cr.s[x - 1] > cr.s[x] ||
+                               (cr.s[x - 1] == cr.s[x] && cr.e[x - 1] < cr.e[x])));
+  }
+  const uint64_t m = __ballot(bad);
+  if (m && lane_id() == __ffsll((unsigned long long)m) - 1) {
+    atomicAdd((unsigned long long *)&diag->order_violations, (unsigned long long)__popcll(m));
+    atomicOr(&diag->flags, OPATTR_F_ORDER);
+  }
+}
+
+// blk[s] = first core position with stream >= s, s = 0..NS
+__global__ void k_blocks16(const uint16_t *st, int64_t n, uint32_t NS, int64_t *blk) {
+  const uint32_t s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s > NS) return;
+  int64_t lo = 0, hi = n;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (st[mid] < s) lo = mid + 1;
+    else hi = mid;
+  }
+  blk[s] = lo;
+}
+
+// tbase[s] = first tile of stream s (tiles never straddle streams)
+__global__ void __launch_bounds__(1024) k_rtile_base(const int64_t *rblk, uint32_t NS,
+                                                     int32_t *tbase) {
+  __shared__ uint32_t sh[16];
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base < NS; base += 1024) {
+    const uint32_t s = base + threadIdx.x;
+    uint32_t c = 0;
+    if (s < NS) c = (uint32_t)((rblk[s + 1] - rblk[s] + kRangeTile - 1) / kRangeTile);
+    uint32_t tot;
+    const uint32_t pre = block_excl_scan_add<uint32_t>(c, sh, &tot);
+    if (s < NS) tbase[s] = (int32_t)(carry + pre);
+    carry += tot;
+  }
+  if (threadIdx.x == 0) tbase[NS] = (int32_t)carry;
+}
+
+__device__ __forceinline__ uint32_t stream_of_tile(const int32_t *tbase, uint32_t NS, int32_t t) {
+  uint32_t lo = 0, hi = NS;  // last s with tbase[s] <= t
+  while (lo + 1 < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (tbase[mid] <= t) lo = mid;
+    else hi = mid;
+  }
+  return lo;
+}
+
+struct RangeWork {
+  CoreRanges cr;
+  uint32_t NS;
+  const int64_t *rblk;
+  const int32_t *tbase;
+  int64_t *ree;
+  int32_t *npg;
+  int64_t *mxv;
+  int64_t *tM;
+  int32_t *tnpg, *tnpg2;
+  int64_t *tmx, *tmx2;
+  int32_t *tstr, *tlast;
+  uint8_t *sflag;
+  opattr_diag *diag;
+};
+
+// Local parents inside one tile by pointer jumping (Jacobi rounds): cand[i]
+// starts at i-1; while the candidate's end is before ours, jump to the
+// candidate's candidate. Every skipped range ends before ours, so cand stays a
+// valid candidate and converges to the nearest one with end >= ours, or -1 when
+// none is in the tile. mx[i] accumulates the largest end skipped.
+__global__ void __launch_bounds__(kRangeTile) k_rlocal(RangeWork w) {
+  __shared__ int64_t e[kRangeTile];
+  __shared__ int64_t mx[kRangeTile];
+  __shared__ int32_t cand[kRangeTile];
+  __shared__ int64_t red[kRangeTile / OPA_WAVE];
+  const int32_t t = blockIdx.x;
+  if (t >= w.tbase[w.NS]) return;
+  const uint32_t s = stream_of_tile(w.tbase, w.NS, t);
+  const int64_t x0 = w.rblk[s] + (int64_t)(t - w.tbase[s]) * kRangeTile;
+  const int64_t x1 = min(x0 + kRangeTile, w.rblk[s + 1]);
+  const int i = threadIdx.x;
+  const bool valid = x0 + i < x1;
+  e[i] = valid ? w.ree[x0 + i] : -1;
+  mx[i] = -1;
+  cand[i] = i - 1;
+  __syncthreads();
+  for (;;) {
+    const int c = cand[i];
+    int nc = c;
+    int64_t nm = mx[i];
+    if (valid && c >= 0 && e[c] < e[i]) {
+      nc = cand[c];
+      const int64_t v = e[c] > mx[c] ? e[c] : mx[c];
+      nm = v > nm ? v : nm;
+    }
+    __syncthreads();
+    cand[i] = nc;
+    mx[i] = nm;
+    if (!__syncthreads_or(nc != c)) break;
+  }
+  if (valid) {
+    const int64_t x = x0 + i;
+    const int c = cand[i];
+    w.npg[x] = c >= 0 ? (int32_t)(x0 + c) : -2;  // -2: parent lies before the tile
+    w.mxv[x] = mx[i];
+    if (c >= 0 && e[i] >= 0 && mx[i] > (int64_t)w.cr.s[x]) w.sflag[s] = 1;
+  }
+  // tile maximum
+  int64_t v = e[i];
+  for (int o = OPA_WAVE / 2; o > 0; o >>= 1) {
+    const int64_t y = __shfl_xor(v, o, OPA_WAVE);
+    v = y > v ? y : v;
+  }
+  if (lane_id() == 0) red[wave_id()] = v;
+  __syncthreads();
+  if (i == 0) {
+    int64_t m = -1;
+    for (int k = 0; k < kRangeTile / OPA_WAVE; ++k) m = red[k] > m ? red[k] : m;
+    w.tM[t] = m;
+    w.tstr[t] = (int32_t)s;
+    w.tlast[t] = (int32_t)(x1 - 1);
+  }
+}
+
+// The same jumping over tile maxima (one block, tiles in global memory).
+__global__ void __launch_bounds__(1024) k_rtiles(RangeWork w) {
+  const int32_t ntr = w.tbase[w.NS];
+  int32_t *cn = w.tnpg, *nn = w.tnpg2;
+  int64_t *cm = w.tmx, *nm = w.tmx2;
+  for (int32_t t = threadIdx.x; t < ntr; t += 1024) {
+    cn[t] = (t > 0 && w.tstr[t - 1] == w.tstr[t]) ? t - 1 : -1;
+    cm[t] = -1;
+  }
+  __threadfence_block();
+  __syncthreads();
+  for (;;) {
+    int changed = 0;
+    for (int32_t t = threadIdx.x; t < ntr; t += 1024) {
+      const int32_t c = cn[t];
+      int32_t n2 = c;
+      int64_t m2 = cm[t];
+      if (c >= 0 && w.tM[c] < w.tM[t]) {
+        n2 = cn[c];
+        const int64_t v = w.tM[c] > cm[c] ? w.tM[c] : cm[c];
+        m2 = v > m2 ? v : m2;
+      }
+      nn[t] = n2;
+      nm[t] = m2;
+      changed |= n2 != c;
+    }
+    __threadfence_block();
+    const int any = __syncthreads_or(changed);
+    int32_t *tn = cn;
+    cn = nn;
+    nn = tn;
+    int64_t *tm = cm;
+    cm = nm;
+    nm = tm;
+    if (!any) break;
+  }
+  if (cn != w.tnpg)
+    for (int32_t t = threadIdx.x; t < ntr; t += 1024) {
+      w.tnpg[t] = cn[t];
+      w.tmx[t] = cm[t];
+    }
+}
+
+// Parents of the ranges whose parent lies in an earlier tile: walk back over
+// tiles (tile parents skip tiles whose maximum end is below ours), then down
+// the local parents of the tile found, from its last range.
+__global__ void k_rresolve(RangeWork w) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= w.cr.n || w.npg[x] != -2) return;
+  const uint32_t s = w.cr.st[x];
+  const int64_t ex = w.ree[x];
+  const int32_t t = w.tbase[s] + (int32_t)((x - w.rblk[s]) / kRangeTile);
+  int64_t acc = w.mxv[x];
+  int32_t u = (t > w.tbase[s]) ? t - 1 : -1;
+  int steps = 0;
+  while (u >= 0 && w.tM[u] < ex && steps < (1 << 20)) {
+    const int64_t v = w.tM[u] > w.tmx[u] ? w.tM[u] : w.tmx[u];
+    acc = v > acc ? v : acc;
+    u = w.tnpg[u];
+    ++steps;
+  }
+  int32_t par = -1;
+  if (u >= 0) {
+    int32_t y = w.tlast[u];
+    steps = 0;
+    while (w.ree[y] < ex && steps < (1 << 20)) {
+      const int64_t v = w.ree[y] > w.mxv[y] ? w.ree[y] : w.mxv[y];
+      acc = v > acc ? v : acc;
+      y = w.npg[y];
+      ++steps;
+      if (y < 0) break;  // defensive: cannot happen, a tile maximum stops the walk
+    }
+    par = y;
+  }
+  w.npg[x] = par;
+  if (ex >= 0 && acc > (int64_t)w.cr.s[x]) w.sflag[s] = 1;
+}
+
+// depth = length of the parent chain (1 for a root, 0 for a bad range)
+__global__ void k_rdepth(RangeWork w, uint8_t *range_depth) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  bool lim = false;
+  if (x < w.cr.n) {
+    int d = 0;
+    int32_t y = (int32_t)x;
+    while (y >= 0 && d <= 255) {
+      ++d;
+      y = w.npg[y];
+    }
+    lim = y >= 0;
+    const bool ok = w.ree[x] >= 0 && w.cr.st[x] < w.NS;
+    if (range_depth) {
+      const int64_t o = w.cr.perm ? w.cr.perm[x] : x;
+      range_depth[o] = ok ? (uint8_t)(d > 255 ? 255 : d) : 0;
+    }
+    lim = lim && ok;
+  }
+  if (__ballot(lim) && lane_id() == 0) atomicOr(&w.diag->flags, OPATTR_F_LIMIT);
+}
+
+static RangeWork range_work(const CoreRanges &cr, const opattr_dims *d, void *ws, const Plan &pl,
+                            opattr_diag *diag) {
+  RangeWork w;
+  w.cr = cr;
+  w.NS = d->n_streams;
+  w.rblk = at<int64_t>(ws, pl.rblk);
+  w.tbase = at<int32_t>(ws, pl.tbase);
+  w.ree = at<int64_t>(ws, pl.ree);
+  w.npg = at<int32_t>(ws, pl.npg);
+  w.mxv = at<int64_t>(ws, pl.mxv);
+  w.tM = at<int64_t>(ws, pl.tM);
+  w.tnpg = at<int32_t>(ws, pl.tnpg);
+  w.tnpg2 = at<int32_t>(ws, pl.tnpg2);
+  w.tmx = at<int64_t>(ws, pl.tmx);
+  w.tmx2 = at<int64_t>(ws, pl.tmx2);
+  w.tstr = at<int32_t>(ws, pl.tfirst);
+  w.tlast = at<int32_t>(ws, pl.tlast);
+  w.sflag = at<uint8_t>(ws, pl.sflag);
+  w.diag = diag;
+  return w;
+}
+
+__global__ void k_gather_small(const uint16_t *st, const uint32_t *op, const uint32_t *perm,
+                               uint16_t *st_o, uint32_t *op_o, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) {
+    const uint32_t p = perm[i];
+    st_o[i] = st[p];
+    op_o[i] = op[p];
+  }
+}
+void launch_gather_small(const uint16_t *st, const uint32_t *op, const uint32_t *perm,
+                         uint16_t *st_o, uint32_t *op_o, int64_t n, hipStream_t s) {
+  if (n > 0) k_gather_small<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(st, op, perm, st_o, op_o, n);
+}
+
+CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws, const Plan &pl,
+                          opattr_diag *diag, bool validate, hipStream_t s) {
+  CoreRanges cr;
+  cr.n = pl.R;
+  const int64_t R = pl.R;
+  if (pl.ranges_nested) {
+    cr.s = r->start_ns;
+    cr.e = r->end_ns;
+    cr.st = r->stream_id;
+    cr.op = r->op_id;
+    cr.perm = nullptr;
+    if (validate && R > 1) k_rcheck<<<(unsigned)((R + 255) / 256), 256, 0, s>>>(cr, diag);
+  } else if (R > 0) {
+    // nesting order by three stable LSD sorts: end desc, then start asc, then
+    // stream; equal keys keep input order, so identical intervals nest by index
+    uint64_t *K[2] = {at<uint64_t>(ws, pl.rsort_k0), at<uint64_t>(ws, pl.rsort_k1)};
+    uint32_t *V[2] = {at<uint32_t>(ws, pl.rsort_v0), at<uint32_t>(ws, pl.rsort_v1)};
+    uint32_t *hist = at<uint32_t>(ws, pl.rs_hist);
+    int cur = 0;
+    launch_iota(V[0], R, s);
+    launch_gather_key_u64(r->end_ns, V[cur], K[cur], R, true, s);
+    cur ^= radix_sort_pairs(K[cur], V[cur], K[cur ^ 1], V[cur ^ 1], R, 0, 64, hist, s) ? 1 : 0;
+    launch_gather_key_u64(r->start_ns, V[cur], K[cur], R, false, s);
+    cur ^= radix_sort_pairs(K[cur], V[cur], K[cur ^ 1], V[cur ^ 1], R, 0, 64, hist, s) ? 1 : 0;
+    launch_gather_key_u16(r->stream_id, V[cur], K[cur], R, s);
+    cur ^= radix_sort_pairs(K[cur], V[cur], K[cur ^ 1], V[cur ^ 1], R, 0, 16, hist, s) ? 1 : 0;
+    const uint32_t *perm = V[cur];
+    uint64_t *sc = at<uint64_t>(ws, pl.rs_c), *ec = at<uint64_t>(ws, pl.re_c);
+    launch_gather_key_u64(r->start_ns, perm, sc, R, false, s);
+    launch_gather_key_u64(r->end_ns, perm, ec, R, false, s);
+    note(hipMemcpyAsync(at<uint32_t>(ws, pl.rperm), perm, (size_t)R * 4, hipMemcpyDeviceToDevice, s));
+    launch_gather_small(r->stream_id, r->op_id, at<uint32_t>(ws, pl.rperm),
+                        at<uint16_t>(ws, pl.rst_c), at<uint32_t>(ws, pl.rop_c), R, s);
+    cr.s = sc;
+    cr.e = ec;
+    cr.st = at<uint16_t>(ws, pl.rst_c);
+    cr.op = at<uint32_t>(ws, pl.rop_c);
+    cr.perm = reinterpret_cast<const int32_t *>(at<uint32_t>(ws, pl.rperm));
+  } else {
+    cr.s = cr.e = nullptr;
+    cr.st = nullptr;
+    cr.op = nullptr;
+    cr.perm = nullptr;
+  }
+  const uint32_t NS = d->n_streams;
+  int64_t *rblk = at<int64_t>(ws, pl.rblk);
+  if (R > 0)
+    k_rprep<<<(unsigned)((R + 255) / 256), 256, 0, s>>>(cr, NS, d->n_ops, at<int64_t>(ws, pl.ree),
+                                                        at<int32_t>(ws, pl.npg), diag);
+  if (R > 0) k_blocks16<<<(NS + 1 + 255) / 256, 256, 0, s>>>(cr.st, R, NS, rblk);
+  else note(hipMemsetAsync(rblk, 0, (size_t)(NS + 1) * 8, s));
+  return cr;
+}
+
+void resolve_ranges(const CoreRanges &cr, const opattr_dims *d, void *ws, const Plan &pl,
+                    uint8_t *range_depth, opattr_diag *diag, hipStream_t s) {
+  const uint32_t NS = d->n_streams;
+  note(hipMemsetAsync(at<uint8_t>(ws, pl.sflag), 0, NS ? NS : 1, s));
+  if (pl.R <= 0 || NS == 0) {
+    if (range_depth && pl.R > 0) note(hipMemsetAsync(range_depth, 0, (size_t)pl.R, s));
+    return;
+  }
+  RangeWork w = range_work(cr, d, ws, pl, diag);
+  k_rtile_base<<<1, 1024, 0, s>>>(w.rblk, NS, at<int32_t>(ws, pl.tbase));
+  k_rlocal<<<(unsigned)pl.ntr_max, kRangeTile, 0, s>>>(w);
+  k_rtiles<<<1, 1024, 0, s>>>(w);
+  const unsigned nb = (unsigned)((pl.R + 255) / 256);
+  k_rresolve<<<nb, 256, 0, s>>>(w);
+  k_rdepth<<<nb, 256, 0, s>>>(w, range_depth);
+}
+
+}  // namespace opa

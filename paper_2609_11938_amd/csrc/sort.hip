@@ -1,0 +1,156 @@
+// Stable LSD radix sort of (u64 key, u32 value) pairs, 8-bit digits.
+// Each pass: per-tile digit histograms -> one exclusive scan in digit-major
+// order -> a scatter that ranks equal digits stably inside the tile with
+// wave ballots (per-digit peer masks) and per-(chunk, wave) counts in LDS.
+#include "common.h"
+#include "impl.h"
+
+namespace opa {
+
+__global__ void __launch_bounds__(256) k_rs_hist(const uint64_t *__restrict__ keys, int64_t n,
+                                                 int shift, uint32_t *__restrict__ hist,
+                                                 int64_t ntiles) {
+  __shared__ uint32_t c[256];
+  c[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
+  for (int i = threadIdx.x; i < OPA_TILE; i += 256) {
+    const int64_t x = base + i;
+    if (x < n) atomicAdd(&c[(keys[x] >> shift) & 255u], 1u);
+  }
+  __syncthreads();
+  hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = c[threadIdx.x];
+}
+
+// Exclusive scan of a[0..n) in place by one block of 1024 threads.
+__global__ void __launch_bounds__(1024) k_scan_excl_u32(uint32_t *__restrict__ a, int64_t n) {
+  __shared__ uint32_t sh[16];
+  uint32_t carry = 0;
+  for (int64_t base = 0; base < n; base += 4096) {
+    uint32_t v[4];
+    uint32_t s = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t x = base + threadIdx.x * 4 + j;
+      v[j] = x < n ? a[x] : 0u;
+      s += v[j];
+    }
+    uint32_t tot;
+    uint32_t pre = block_excl_scan_add<uint32_t>(s, sh, &tot);
+    uint32_t run = carry + pre;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t x = base + threadIdx.x * 4 + j;
+      if (x < n) a[x] = run;
+      run += v[j];
+    }
+    carry += tot;
+  }
+}
+
+__global__ void __launch_bounds__(256) k_rs_scatter(const uint64_t *__restrict__ kin,
+                                                    const uint32_t *__restrict__ vin,
+                                                    uint64_t *__restrict__ kout,
+                                                    uint32_t *__restrict__ vout, int64_t n,
+                                                    int shift, const uint32_t *__restrict__ offs,
+                                                    int64_t ntiles) {
+  __shared__ uint16_t cnt[OPA_TILE_CHUNKS][4][256];
+  const int tid = threadIdx.x, w = wave_id();
+  const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
+  for (int i = tid; i < OPA_TILE_CHUNKS * 4 * 256; i += 256) (&cnt[0][0][0])[i] = 0;
+  __syncthreads();
+  uint32_t dig[OPA_TILE_CHUNKS], lr[OPA_TILE_CHUNKS];
+#pragma unroll
+  for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
+    const int64_t x = base + c * 256 + tid;
+    // elements past n sit after every valid one, so they never precede one
+    const uint32_t d = x < n ? (uint32_t)((kin[x] >> shift) & 255u) : 0u;
+    const uint64_t pm = peers8(d);
+    dig[c] = d;
+    lr[c] = (uint32_t)__popcll(pm & lanemask_lt());
+    if ((pm & lanemask_lt()) == 0) cnt[c][w][d] = (uint16_t)__popcll(pm);
+  }
+  __syncthreads();
+  {
+    uint32_t run = 0;
+    for (int c = 0; c < OPA_TILE_CHUNKS; ++c)
+      for (int ww = 0; ww < 4; ++ww) {
+        const uint32_t v = cnt[c][ww][tid];
+        cnt[c][ww][tid] = (uint16_t)run;
+        run += v;
+      }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
+    const int64_t x = base + c * 256 + tid;
+    if (x < n) {
+      const uint32_t d = dig[c];
+      const uint32_t dst = offs[(int64_t)d * ntiles + blockIdx.x] + cnt[c][w][d] + lr[c];
+      kout[dst] = kin[x];
+      vout[dst] = vin[x];
+    }
+  }
+}
+
+size_t radix_hist_entries(int64_t n) {
+  const int64_t nt = (n + OPA_TILE - 1) / OPA_TILE;
+  return (size_t)(nt > 0 ? nt : 1) * 256;
+}
+
+bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, int64_t n,
+                      int begin_bit, int end_bit, uint32_t *hist, hipStream_t s) {
+  if (n <= 0) return false;
+  const int64_t nt = (n + OPA_TILE - 1) / OPA_TILE;
+  bool in1 = false;
+  for (int sh = begin_bit; sh < end_bit; sh += 8) {
+    uint64_t *ki = in1 ? k1 : k0, *ko = in1 ? k0 : k1;
+    uint32_t *vi = in1 ? v1 : v0, *vo = in1 ? v0 : v1;
+    k_rs_hist<<<(unsigned)nt, 256, 0, s>>>(ki, n, sh, hist, nt);
+    k_scan_excl_u32<<<1, 1024, 0, s>>>(hist, nt * 256);
+    k_rs_scatter<<<(unsigned)nt, 256, 0, s>>>(ki, vi, ko, vo, n, sh, hist, nt);
+    in1 = !in1;
+  }
+  return in1;
+}
+
+__global__ void k_iota(uint32_t *v, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) v[i] = (uint32_t)i;
+}
+__global__ void k_gather_u64(const uint64_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
+                             bool invert) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) {
+    const uint64_t v = src[perm[i]];
+    dst[i] = invert ? ~v : v;
+  }
+}
+__global__ void k_gather_u16(const uint16_t *src, const uint32_t *perm, uint64_t *dst, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[perm[i]];
+}
+__global__ void k_gather_u32(const uint32_t *src, const uint32_t *perm, uint64_t *dst, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[perm[i]];
+}
+
+static unsigned blocks_for(int64_t n, int b) { return (unsigned)((n + b - 1) / b); }
+
+void launch_iota(uint32_t *v, int64_t n, hipStream_t s) {
+  if (n > 0) k_iota<<<blocks_for(n, 256), 256, 0, s>>>(v, n);
+}
+void launch_gather_key_u64(const uint64_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
+                           bool invert, hipStream_t s) {
+  if (n > 0) k_gather_u64<<<blocks_for(n, 256), 256, 0, s>>>(src, perm, dst, n, invert);
+}
+void launch_gather_key_u16(const uint16_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
+                           hipStream_t s) {
+  if (n > 0) k_gather_u16<<<blocks_for(n, 256), 256, 0, s>>>(src, perm, dst, n);
+}
+void launch_gather_key_u32(const uint32_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
+                           hipStream_t s) {
+  if (n > 0) k_gather_u32<<<blocks_for(n, 256), 256, 0, s>>>(src, perm, dst, n);
+}
+
+}  // namespace opa

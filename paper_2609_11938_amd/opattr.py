@@ -1,0 +1,351 @@
+"""Python binding of libopattr (the MI355X attribution join).
+
+Argument marshalling only: device tensors are handed to the C ABI declared in
+``include/opattr.h`` by pointer, every stage runs in the library's HIP kernels,
+and results come back as device tensors. PyTorch supplies device memory and the
+current HIP stream. There is no CPU fallback: a missing library raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "_build", "libopattr.so")
+
+NUM_COUNTERS = 20
+MISMATCH_PREFIX, MISMATCH_SKIP_NAME, MISMATCH_STRICT = 0, 1, 2
+AGG_SUM, AGG_DWMEAN, AGG_MAX = 0, 1, 2
+KERNELS_STREAM_MAJOR, SEQ_DENSE, RANGES_NESTED, VALIDATE = 1, 2, 4, 8
+F_DATA, F_ORDER, F_LIMIT, F_NOT_NESTED, F_PARTITION, F_DEDUP, F_COUNT = 1, 2, 4, 8, 16, 32, 64
+
+
+class InvocationCountMismatchError(RuntimeError):
+    """Per-name launch and profiled-row counts differ under the strict policy."""
+
+
+class opattr_kernels(C.Structure):
+    _fields_ = [("n", C.c_int64), ("seq", C.c_void_p), ("start_ns", C.c_void_p),
+                ("dur_ns", C.c_void_p), ("stream_id", C.c_void_p), ("name_id", C.c_void_p),
+                ("part_id", C.c_void_p), ("query_ns", C.c_void_p)]
+
+
+class opattr_profiled(C.Structure):
+    _fields_ = [("n", C.c_int64), ("name_id", C.c_void_p), ("counters", C.c_void_p),
+                ("row_stride", C.c_int64), ("col_stride", C.c_int64),
+                ("absent_mask", C.c_uint32)]
+
+
+class opattr_ranges(C.Structure):
+    _fields_ = [("n", C.c_int64), ("start_ns", C.c_void_p), ("end_ns", C.c_void_p),
+                ("stream_id", C.c_void_p), ("op_id", C.c_void_p)]
+
+
+class opattr_dims(C.Structure):
+    _fields_ = [("n_names", C.c_uint32), ("n_streams", C.c_uint32), ("n_ops", C.c_uint32),
+                ("n_parts", C.c_uint32), ("part_rep", C.c_void_p), ("flags", C.c_uint32)]
+
+
+class opattr_diag(C.Structure):
+    _fields_ = [("status", C.c_int32), ("flags", C.c_uint32), ("names_mismatched", C.c_uint32),
+                ("nesting_errors", C.c_uint32), ("tl_unmatched", C.c_uint64),
+                ("pf_unmatched", C.c_uint64), ("dedup_errors", C.c_uint64),
+                ("bad_records", C.c_uint64), ("order_violations", C.c_uint64),
+                ("strict", C.c_uint32), ("reserved", C.c_uint32)]
+
+
+OP_ROW_DTYPE = np.dtype([("kernel_count", "<u8"), ("total_ns", "<u8"),
+                         ("matched_count", "<u8"), ("matched_ns", "<u8"),
+                         ("value", "<f8", (NUM_COUNTERS,))])
+SUMMARY_DTYPE = np.dtype([("total_ns", "<u8"), ("attributed_ns", "<u8"),
+                          ("unattributed_ns", "<u8"), ("matched_ns", "<u8"),
+                          ("attributed_fraction", "<f8")])
+assert OP_ROW_DTYPE.itemsize == 192 and SUMMARY_DTYPE.itemsize == 40
+assert C.sizeof(opattr_diag) == 64
+
+EXPORTS = ("opattr_workspace_bytes", "opattr_diag_clear", "opattr_read_diag", "opattr_match",
+           "opattr_dedup_broadcast", "opattr_enclose", "opattr_aggregate", "opattr_attribute",
+           "opattr_strerror")
+
+_lib = None
+
+
+def library(path: str = LIB_PATH):
+    """Load libopattr.so and declare its entry points. Raises when it is not
+    built: this package has no CPU fallback."""
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libopattr is not built ({path}); run __graft_entry__.build()")
+    L = C.CDLL(path)
+    P = C.POINTER
+    vp, i, sz = C.c_void_p, C.c_int, C.c_size_t
+    L.opattr_workspace_bytes.argtypes = [P(opattr_kernels), P(opattr_profiled),
+                                         P(opattr_ranges), P(opattr_dims)]
+    L.opattr_workspace_bytes.restype = sz
+    L.opattr_diag_clear.argtypes = [vp, vp]
+    L.opattr_read_diag.argtypes = [vp, P(opattr_diag), vp]
+    L.opattr_match.argtypes = [P(opattr_kernels), P(opattr_profiled), P(opattr_dims), i, vp, vp,
+                               vp, vp, sz, vp]
+    L.opattr_dedup_broadcast.argtypes = [P(opattr_kernels), P(opattr_dims), vp, vp, vp, sz, vp]
+    L.opattr_enclose.argtypes = [P(opattr_kernels), P(opattr_ranges), P(opattr_dims), vp, vp,
+                                 vp, vp, sz, vp]
+    L.opattr_aggregate.argtypes = [P(opattr_kernels), P(opattr_profiled), vp, vp,
+                                   P(opattr_ranges), P(opattr_dims), vp, vp, vp, vp, vp, sz, vp]
+    L.opattr_attribute.argtypes = [P(opattr_kernels), P(opattr_profiled), P(opattr_ranges),
+                                   P(opattr_dims), i, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    for f in ("opattr_diag_clear", "opattr_read_diag", "opattr_match", "opattr_dedup_broadcast",
+              "opattr_enclose", "opattr_aggregate", "opattr_attribute"):
+        getattr(L, f).restype = C.c_int
+    L.opattr_strerror.argtypes = [i]
+    L.opattr_strerror.restype = C.c_char_p
+    if path == LIB_PATH:
+        _lib = L
+    return L
+
+
+def strerror(status: int) -> str:
+    return library().opattr_strerror(status).decode()
+
+
+# --------------------------------------------------------------------------- #
+# device trace                                                                #
+# --------------------------------------------------------------------------- #
+
+_KERNEL_FIELDS = {"seq": np.uint32, "start_ns": np.uint64, "dur_ns": np.uint32,
+                  "stream_id": np.uint16, "name_id": np.uint32, "part_id": np.int32,
+                  "query_ns": np.uint64}
+_RANGE_FIELDS = {"r_start": np.uint64, "r_end": np.uint64, "r_stream": np.uint16,
+                 "r_op": np.uint32}
+
+
+def to_device(tr: dict, device="cuda:0") -> dict:
+    """Copy a host trace (dict of numpy arrays, see tracegen.generate) to device
+    tensors. Dimension entries are kept as Python ints."""
+    import torch
+
+    out = {}
+    for k, dt in {**_KERNEL_FIELDS, **_RANGE_FIELDS, "pf_name": np.uint32,
+                  "part_rep": np.int32}.items():
+        a = tr.get(k)
+        out[k] = None if a is None else torch.from_numpy(
+            np.ascontiguousarray(a, dtype=dt)).to(device)
+    cnt = tr["counters"]
+    if cnt.dtype != np.float32 or cnt.ndim != 2:
+        raise TypeError("counters must be a 2-D float32 array")
+    out["counters"] = torch.from_numpy(np.ascontiguousarray(cnt)).to(device)
+    for k in ("n_names", "n_streams", "n_ops", "n_parts"):
+        out[k] = int(tr.get(k, 0) or 0)
+    return out
+
+
+def _p(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+class _Marshal:
+    """ctypes structs pointing at a device trace's tensors."""
+
+    def __init__(self, dt: dict, flags: int, absent_mask: int = 0):
+        T = 0 if dt["seq"] is None else int(dt["seq"].numel())
+        self.k = opattr_kernels(T, _p(dt["seq"]), _p(dt["start_ns"]), _p(dt["dur_ns"]),
+                                _p(dt["stream_id"]), _p(dt["name_id"]), _p(dt.get("part_id")),
+                                _p(dt.get("query_ns")))
+        cnt = dt["counters"]
+        P = int(dt["pf_name"].numel())
+        rs, cs = (cnt.stride(0), cnt.stride(1)) if cnt.dim() == 2 else (NUM_COUNTERS, 1)
+        self.p = opattr_profiled(P, _p(dt["pf_name"]), _p(cnt) if P else None, rs, cs,
+                                 absent_mask)
+        R = int(dt["r_start"].numel())
+        self.r = opattr_ranges(R, _p(dt["r_start"]), _p(dt["r_end"]), _p(dt["r_stream"]),
+                               _p(dt["r_op"]))
+        rep = dt.get("part_rep")
+        self.d = opattr_dims(dt["n_names"], dt["n_streams"], dt["n_ops"],
+                             dt.get("n_parts", 0) if rep is not None else 0, _p(rep), flags)
+        self.T, self.P, self.R = T, P, R
+
+
+class Workspace:
+    """Device scratch reused across calls (grown on demand)."""
+
+    def __init__(self, device="cuda:0"):
+        self.device = device
+        self.buf = None
+
+    def get(self, nbytes: int):
+        import torch
+
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=self.device)
+        return self.buf
+
+
+def _stream_handle(stream):
+    import torch
+
+    s = torch.cuda.current_stream() if stream is None else stream
+    return C.c_void_p(s.cuda_stream)
+
+
+def _check(rc: int, fn: str):
+    if rc != 0:
+        raise RuntimeError(f"{fn}: {strerror(rc)} ({rc})")
+
+
+def read_diag(diag_dev, stream=None) -> dict:
+    L = library()
+    h = opattr_diag()
+    _check(L.opattr_read_diag(_p(diag_dev), C.byref(h), _stream_handle(stream)),
+           "opattr_read_diag")
+    return {f: int(getattr(h, f)) for f, _ in opattr_diag._fields_}
+
+
+def _new_diag(device, stream):
+    import torch
+
+    d = torch.empty(C.sizeof(opattr_diag), dtype=torch.uint8, device=device)
+    _check(library().opattr_diag_clear(_p(d), _stream_handle(stream)), "opattr_diag_clear")
+    return d
+
+
+def workspace_bytes(dt: dict, flags: int = 0) -> int:
+    m = _Marshal(dt, flags)
+    return int(library().opattr_workspace_bytes(C.byref(m.k), C.byref(m.p), C.byref(m.r),
+                                                C.byref(m.d)))
+
+
+def _kinds(agg_kind):
+    if agg_kind is None:
+        return None, None
+    k = np.ascontiguousarray(agg_kind, dtype=np.uint8)
+    if k.size != NUM_COUNTERS:
+        raise ValueError("agg_kind needs 20 entries")
+    return k, C.c_void_p(k.ctypes.data)
+
+
+class Outputs(dict):
+    """Device outputs of a call plus host copies made on demand."""
+
+    def table_host(self):
+        return self["table"].cpu().numpy().view(OP_ROW_DTYPE).reshape(-1)
+
+    def summary_host(self):
+        a = self["summary"].cpu().numpy().view(SUMMARY_DTYPE)[0]
+        return {f: (float(a[f]) if f == "attributed_fraction" else int(a[f]))
+                for f in SUMMARY_DTYPE.names}
+
+
+def opattr_attribute(dt: dict, policy=MISMATCH_PREFIX, agg_kind=None, flags=0, absent_mask=0,
+                     want_depth=True, want_name_counts=True, ws: Workspace | None = None,
+                     stream=None, outputs: Outputs | None = None, raise_strict=True) -> Outputs:
+    """All four stages in one call (see opattr_attribute in include/opattr.h)."""
+    import torch
+
+    L = library()
+    m = _Marshal(dt, flags, absent_mask)
+    dev = dt["counters"].device
+    if outputs is None:
+        outputs = Outputs(
+            match=torch.empty(m.T, dtype=torch.int32, device=dev),
+            range_id=torch.empty(m.T, dtype=torch.int32, device=dev),
+            range_depth=torch.empty(m.R, dtype=torch.uint8, device=dev) if want_depth else None,
+            name_counts=torch.empty((dt["n_names"], 2), dtype=torch.int32, device=dev)
+            if want_name_counts else None,
+            table=torch.empty((dt["n_ops"] + 1) * 192, dtype=torch.uint8, device=dev),
+            summary=torch.empty(40, dtype=torch.uint8, device=dev),
+        )
+    outputs["diag"] = _new_diag(dev, stream)
+    ws = ws or Workspace(dev)
+    need = L.opattr_workspace_bytes(C.byref(m.k), C.byref(m.p), C.byref(m.r), C.byref(m.d))
+    buf = ws.get(need)
+    _, kp = _kinds(agg_kind)
+    k_keep = _kinds(agg_kind)[0]
+    rc = L.opattr_attribute(C.byref(m.k), C.byref(m.p), C.byref(m.r), C.byref(m.d), policy, kp,
+                            _p(outputs["match"]), _p(outputs["range_id"]),
+                            _p(outputs["range_depth"]), _p(outputs["name_counts"]),
+                            _p(outputs["table"]), _p(outputs["summary"]), _p(outputs["diag"]),
+                            _p(buf), C.c_size_t(buf.numel()), _stream_handle(stream))
+    del k_keep
+    _check(rc, "opattr_attribute")
+    if raise_strict and policy == MISMATCH_STRICT:
+        d = read_diag(outputs["diag"], stream)
+        if d["status"] == -4:
+            raise InvocationCountMismatchError(
+                f"{d['names_mismatched']} kernel names have different launch and profiled counts")
+    return outputs
+
+
+def opattr_match(dt: dict, policy=MISMATCH_PREFIX, flags=0, ws: Workspace | None = None,
+                 stream=None) -> Outputs:
+    import torch
+
+    L = library()
+    m = _Marshal(dt, flags)
+    dev = dt["counters"].device
+    out = Outputs(match=torch.empty(m.T, dtype=torch.int32, device=dev),
+                  name_counts=torch.empty((dt["n_names"], 2), dtype=torch.int32, device=dev),
+                  diag=_new_diag(dev, stream))
+    ws = ws or Workspace(dev)
+    buf = ws.get(L.opattr_workspace_bytes(C.byref(m.k), C.byref(m.p), C.byref(m.r), C.byref(m.d)))
+    _check(L.opattr_match(C.byref(m.k), C.byref(m.p), C.byref(m.d), policy, _p(out["match"]),
+                          _p(out["name_counts"]), _p(out["diag"]), _p(buf),
+                          C.c_size_t(buf.numel()), _stream_handle(stream)), "opattr_match")
+    return out
+
+
+def opattr_dedup_broadcast(dt: dict, match, flags=0, ws: Workspace | None = None,
+                           stream=None) -> Outputs:
+    L = library()
+    m = _Marshal(dt, flags)
+    dev = dt["counters"].device
+    out = Outputs(match=match, diag=_new_diag(dev, stream))
+    ws = ws or Workspace(dev)
+    buf = ws.get(L.opattr_workspace_bytes(C.byref(m.k), C.byref(m.p), C.byref(m.r), C.byref(m.d)))
+    _check(L.opattr_dedup_broadcast(C.byref(m.k), C.byref(m.d), _p(match), _p(out["diag"]),
+                                    _p(buf), C.c_size_t(buf.numel()), _stream_handle(stream)),
+           "opattr_dedup_broadcast")
+    return out
+
+
+def opattr_enclose(dt: dict, flags=0, want_depth=True, ws: Workspace | None = None,
+                   stream=None) -> Outputs:
+    import torch
+
+    L = library()
+    m = _Marshal(dt, flags)
+    dev = dt["counters"].device
+    out = Outputs(range_id=torch.empty(m.T, dtype=torch.int32, device=dev),
+                  range_depth=torch.empty(m.R, dtype=torch.uint8, device=dev)
+                  if want_depth else None,
+                  diag=_new_diag(dev, stream))
+    ws = ws or Workspace(dev)
+    buf = ws.get(L.opattr_workspace_bytes(C.byref(m.k), C.byref(m.p), C.byref(m.r), C.byref(m.d)))
+    _check(L.opattr_enclose(C.byref(m.k), C.byref(m.r), C.byref(m.d), _p(out["range_id"]),
+                            _p(out["range_depth"]), _p(out["diag"]), _p(buf),
+                            C.c_size_t(buf.numel()), _stream_handle(stream)), "opattr_enclose")
+    return out
+
+
+def opattr_aggregate(dt: dict, match, range_id, agg_kind=None, flags=0, absent_mask=0,
+                     ws: Workspace | None = None, stream=None) -> Outputs:
+    import torch
+
+    L = library()
+    m = _Marshal(dt, flags, absent_mask)
+    dev = dt["counters"].device
+    out = Outputs(table=torch.empty((dt["n_ops"] + 1) * 192, dtype=torch.uint8, device=dev),
+                  summary=torch.empty(40, dtype=torch.uint8, device=dev),
+                  diag=_new_diag(dev, stream))
+    ws = ws or Workspace(dev)
+    buf = ws.get(L.opattr_workspace_bytes(C.byref(m.k), C.byref(m.p), C.byref(m.r), C.byref(m.d)))
+    k_keep, kp = _kinds(agg_kind)
+    rc = L.opattr_aggregate(C.byref(m.k), C.byref(m.p), _p(match), _p(range_id), C.byref(m.r),
+                            C.byref(m.d), kp, _p(out["table"]), _p(out["summary"]),
+                            _p(out["diag"]), _p(buf), C.c_size_t(buf.numel()),
+                            _stream_handle(stream))
+    del k_keep
+    _check(rc, "opattr_aggregate")
+    return out
