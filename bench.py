@@ -1,0 +1,190 @@
+#!/usr/bin/env python
+"""Throughput of the trace-attribution join on one MI355X.
+
+One step = one opattr_attribute call (invocation-order matching, layer-dedup
+broadcast, enclosure, aggregation) over the large synthetic trace: 10M kernel
+launches on 16 streams, 500k nested ranges (depth <= 8), 1000 kernel names
+Zipf(1.1), layer dedup 48 layers / 3 classes, 1M profiled rows of 20 fp32
+counters. Inputs are resident in HBM before the timed region. Prints one JSON
+line: records/s, the dominant kernel against the HBM roofline (HIP probe events
+recorded by the library around its launches), and the oracle's rate on the
+host cores as a reported CPU baseline.
+"""
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "kernel records attributed/sec (match+enclose+aggregate); % of HBM peak"
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+
+
+def algorithmic_bytes(tr):
+    """Compulsory bytes: every input read once, every output written once, at
+    the ABI widths (duplicate counter rows reused by dedup count once)."""
+    T, P, R = tr["seq"].size, tr["pf_name"].size, tr["r_start"].size
+    part = 4 if tr.get("part_id") is not None else 0
+    G = tr["n_ops"] + 1
+    NP = tr.get("n_parts", 0) or 0
+    timeline = T * (4 + 8 + 4 + 2 + 4 + part)      # seq, start, dur, stream, name, part
+    profiled = P * (4 + 20 * 4)                     # name + 20 counters
+    ranges = R * (8 + 8 + 2 + 4)                    # start, end, stream, op
+    outputs = T * (4 + 4)                           # match, range_id
+    table = G * 192 + 4 * NP                        # op rows + class map
+    per_kernel = {
+        # enclosure + aggregation pass: stream, query, dur, match in; range_id
+        # out; each profiled row once; range starts/ends/parents/ops; op rows
+        "main_pass": T * (2 + 8 + 4 + 4 + 4) + P * 80 + R * (8 + 8 + 4 + 4) + G * 192,
+        # per-tile rank and join: seq view, name, part in; match out
+        "tl_match": T * (4 + 4 + part + 4),
+        # per-tile histograms: seq view, name, part in
+        "tl_hist": T * (4 + 4 + part),
+        "dedup": T * (4 + 4 + part) + T * 4,
+        "seq_view": T * (4 + 4),
+        "pf_hist": P * 4,
+        "pf_slot": P * (4 + 4),
+        "ranges": R * (8 + 8 + 2 + 4) + R * (8 + 4 + 8),
+    }
+    return timeline + profiled + ranges + outputs + table, per_kernel
+
+
+def cpu_baseline(tr, reps=2):
+    from oracle import oracle as O
+
+    O.build(force=False)
+    times = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        O.attribute(tr)
+        times.append(time.perf_counter() - t0)
+    med = statistics.median(times)
+    return {"value": tr["seq"].size / med, "unit": "records/s", "cores": 1, "kind": "oracle",
+            "sample": f"the full workload ({tr['seq'].size} launches), {reps} runs, median "
+                      f"{med:.2f} s, single-threaded C oracle"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="large")
+    ap.add_argument("--emission", default="stream_major",
+                    choices=["stream_major", "seq", "shuffled"])
+    ap.add_argument("--validate", action="store_true", help="also check the layout hints")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus > 1 or world > 1:
+        print("bench.py runs on one GPU only: the attribution join of one trace is "
+              "measured on a single MI355X (see DESIGN.md for how it would shard).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_11938_amd import opattr, tracegen
+
+    if not os.path.exists(opattr.LIB_PATH):
+        import __graft_entry__
+
+        __graft_entry__.build()
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    t0 = time.perf_counter()
+    tr = tracegen.generate(args.config, emission=args.emission)
+    gen_s = time.perf_counter() - t0
+    print(f"generated {args.config}/{args.emission}: {tracegen.summary(tr)} in {gen_s:.1f}s",
+          file=sys.stderr, flush=True)
+    dt = opattr.to_device(tr, dev)
+    flags = {"stream_major": opattr.KERNELS_STREAM_MAJOR | opattr.SEQ_DENSE |
+             opattr.RANGES_NESTED, "seq": opattr.SEQ_DENSE, "shuffled": 0}[args.emission]
+    if args.validate:
+        flags |= opattr.VALIDATE
+    ws = opattr.Workspace(dev)
+    T = tr["seq"].size
+    out = opattr.Outputs(
+        match=torch.empty(T, dtype=torch.int32, device=dev),
+        range_id=torch.empty(T, dtype=torch.int32, device=dev),
+        range_depth=None, name_counts=None,
+        table=torch.empty((tr["n_ops"] + 1) * 192, dtype=torch.uint8, device=dev),
+        summary=torch.empty(40, dtype=torch.uint8, device=dev))
+
+    def step():
+        opattr.opattr_attribute(dt, flags=flags, outputs=out, ws=ws, raise_strict=False)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    diag = opattr.read_diag(out["diag"])
+    if diag["status"] != 0:
+        raise SystemExit(f"attribution reported status {diag['status']}: {diag}")
+
+    # probe events: one start/stop pair per instrumented launch group per step
+    nprobe = len(opattr.PROBES)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * nprobe)]
+          for _ in range(args.steps)]
+    for row in ev:
+        for e in row:
+            e.record()  # materialise the HIP event before handing it over
+    torch.cuda.synchronize()
+
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        opattr.set_probe_events(ev[k])
+        step()
+    torch.cuda.synchronize()
+    t_end = time.perf_counter()
+    opattr.set_probe_events(None)
+
+    ms_per_step = (t_end - t_start) * 1e3 / args.steps
+    value = T / (ms_per_step * 1e-3)
+    probe_ms = {}
+    for p, name in enumerate(opattr.PROBES):
+        d = [ev[k][2 * p].elapsed_time(ev[k][2 * p + 1]) for k in range(args.steps)]
+        probe_ms[name] = statistics.mean(d)
+    total_bytes, kbytes = algorithmic_bytes(tr)
+    dominant = max((n for n in probe_ms if n in kbytes), key=lambda n: probe_ms[n])
+    dom_ms = probe_ms[dominant]
+    achieved = kbytes[dominant] / (dom_ms * 1e-3) / 1e9
+    pipe_gbps = total_bytes / (ms_per_step * 1e-3) / 1e9
+    print("probe ms/step: " + ", ".join(f"{n}={v:.4f}" for n, v in probe_ms.items()),
+          file=sys.stderr, flush=True)
+
+    line = {
+        "metric": METRIC, "value": value, "unit": "records/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int32+f64", "data": "synthetic",
+        "config": {"workload": f"{args.config}: {T} kernel launches, "
+                               f"{tr['n_streams']} streams, {tr['r_start'].size} ranges, "
+                               f"{tr['n_names']} names, {tr['pf_name'].size} profiled rows, "
+                               f"{tr['n_ops']} ops, emission {args.emission}",
+                   "kernels": int(T), "streams": tr["n_streams"],
+                   "ranges": int(tr["r_start"].size), "names": tr["n_names"],
+                   "profiled_rows": int(tr["pf_name"].size), "ops": tr["n_ops"],
+                   "partitions": tr["n_parts"], "emission": args.emission,
+                   "validate": bool(args.validate)},
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved,
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": None, "algorithmic_bytes": kbytes[dominant],
+                     "avg_ms": dom_ms},
+        "pipeline": {"algorithmic_bytes": total_bytes, "achieved_GBps": pipe_gbps,
+                     "frac_of_hbm_peak": pipe_gbps / HBM_PEAK_GBPS,
+                     "probe_ms": probe_ms},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(tr)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

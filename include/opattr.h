@@ -221,6 +221,26 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
                      opattr_op_row *table, opattr_summary *sum, opattr_diag *diag, void *ws,
                      size_t ws_bytes, void *stream);
 
+/* Probe events (diagnostics, per host thread). events is a host array of
+   2*n hipEvent_t values; while set, every later call on this thread records
+   events[2*i] on its stream right before the launches of probe i and
+   events[2*i+1] right after them, for the probes below that the call runs.
+   NULL (or n = 0) switches probing off. The events are the caller's. */
+enum {
+  OPATTR_PROBE_SEQ_VIEW = 0,   /* launch-order view of the timeline          */
+  OPATTR_PROBE_TL_HIST = 1,    /* per-tile name histograms of the timeline  */
+  OPATTR_PROBE_PF_HIST = 2,    /* per-tile name histograms of the rows      */
+  OPATTR_PROBE_COL_SCAN = 3,   /* column scans of both histogram tables     */
+  OPATTR_PROBE_PF_SLOT = 4,    /* profiled slot table                       */
+  OPATTR_PROBE_TL_MATCH = 5,   /* per-tile rank and join                    */
+  OPATTR_PROBE_DEDUP = 6,      /* dedup broadcast                           */
+  OPATTR_PROBE_RANGES = 7,     /* range order, parents and depths           */
+  OPATTR_PROBE_MAIN_PASS = 8,  /* enclosure + aggregation pass, operator rows */
+  OPATTR_PROBE_FINALIZE = 9,   /* status of the diag record                 */
+  OPATTR_NUM_PROBES = 10
+};
+int opattr_set_probe_events(void *const *events, int n);
+
 /* Human-readable name of a status code. */
 const char *opattr_strerror(int status);
 

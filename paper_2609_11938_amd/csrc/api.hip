@@ -125,7 +125,9 @@ __global__ void __launch_bounds__(256) k_finish(opattr_diag *diag, const uint8_t
 }
 
 void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s) {
+  probe_begin(OPATTR_PROBE_FINALIZE, s);
   k_finish<<<1, 256, 0, s>>>(diag, sflag, ns);
+  probe_end(OPATTR_PROBE_FINALIZE, s);
 }
 
 static const uint8_t kDefaultKind[OPATTR_NUM_COUNTERS] = {
@@ -323,8 +325,10 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, validate};
   run_match(a, s);
   run_dedup(k, d, match, diag, ws, pl, true, s);
+  probe_begin(OPATTR_PROBE_RANGES, s);
   const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s);
   resolve_ranges(cr, d, ws, pl, range_depth, diag, s);
+  probe_end(OPATTR_PROBE_RANGES, s);
   EncArgs e{};
   e.mode = kEncloseAggregate;
   e.k = k;
@@ -343,6 +347,14 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   run_enclose_aggregate(e, s);
   launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s);
   return launch_status();
+}
+
+int opattr_set_probe_events(void *const *events, int n) {
+  if (n < 0 || n > OPATTR_NUM_PROBES || (n > 0 && !events)) return OPATTR_ERR_INVALID_ARG;
+  g_probes.n = events ? n : 0;
+  for (int i = 0; i < 2 * OPATTR_NUM_PROBES; ++i)
+    g_probes.ev[i] = (events && i < 2 * n) ? (hipEvent_t)events[i] : nullptr;
+  return OPATTR_OK;
 }
 
 const char *opattr_strerror(int status) {

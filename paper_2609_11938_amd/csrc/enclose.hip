@@ -355,6 +355,7 @@ void run_enclose_aggregate(const EncArgs &x, hipStream_t s) {
     a.op_in = x.r ? x.r->op_id : nullptr;
   }
   const unsigned nb = (unsigned)((pl.T + kEncThreads - 1) / kEncThreads);
+  probe_begin(OPATTR_PROBE_MAIN_PASS, s);
   if (pl.T > 0) {
     if (x.mode == kEncloseOnly) k_enc<1><<<nb, kEncThreads, 0, s>>>(a);
     else if (x.mode == kAggregateOnly) k_enc<2><<<nb, kEncThreads, 0, s>>>(a);
@@ -363,6 +364,7 @@ void run_enclose_aggregate(const EncArgs &x, hipStream_t s) {
   if (x.mode & 2)
     k_agg_finalize<<<1, 1024, 0, s>>>(a.acc, G, a.NOPS, a.dwmask, a.summask, a.maxmask,
                                       x.p->absent_mask, x.table, x.sum);
+  probe_end(OPATTR_PROBE_MAIN_PASS, s);
 }
 
 }  // namespace opa

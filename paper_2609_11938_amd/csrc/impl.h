@@ -53,6 +53,20 @@ inline void note(hipError_t e) {
   if (e != hipSuccess && g_hip_error == hipSuccess) g_hip_error = e;
 }
 
+// Probe events of the calling host thread (opattr_set_probe_events).
+struct Probes {
+  hipEvent_t ev[2 * OPATTR_NUM_PROBES];
+  int n = 0;
+};
+inline thread_local Probes g_probes;
+inline void probe_begin(int id, hipStream_t s) {
+  if (id < g_probes.n && g_probes.ev[2 * id]) note(hipEventRecord(g_probes.ev[2 * id], s));
+}
+inline void probe_end(int id, hipStream_t s) {
+  if (id < g_probes.n && g_probes.ev[2 * id + 1])
+    note(hipEventRecord(g_probes.ev[2 * id + 1], s));
+}
+
 template <typename T>
 inline T *at(void *ws, size_t off) {
   return reinterpret_cast<T *>(static_cast<char *>(ws) + off);

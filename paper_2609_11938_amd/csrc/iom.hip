@@ -52,9 +52,11 @@ void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, con
   if (T <= 0) return;
   int32_t *sv = at<int32_t>(ws, pl.sv);
   const unsigned nb = (unsigned)((T + 255) / 256);
+  probe_begin(OPATTR_PROBE_SEQ_VIEW, s);
   if (pl.seq_dense) {
     note(hipMemsetAsync(sv, 0xFF, (size_t)T * 4, s));
     k_seqview_dense<<<nb, 256, 0, s>>>(k->seq, T, sv, diag, validate ? 1 : 0);
+    probe_end(OPATTR_PROBE_SEQ_VIEW, s);
     return;
   }
   uint64_t *k0 = at<uint64_t>(ws, pl.seqsort_k0), *k1 = at<uint64_t>(ws, pl.seqsort_k1);
@@ -64,6 +66,7 @@ void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, con
   const bool in1 = radix_sort_pairs(k0, v0, k1, v1, T, 0, 32, at<uint32_t>(ws, pl.rs_hist), s);
   k_seqview_sorted<<<nb, 256, 0, s>>>(in1 ? k1 : k0, in1 ? v1 : v0, T, sv,
                                        at<int32_t>(ws, pl.rk), diag);
+  probe_end(OPATTR_PROBE_SEQ_VIEW, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -454,18 +457,26 @@ void run_match(const IomArgs &x, hipStream_t s) {
   pa.name = x.p->name_id;
   pa.P = pl.P;
   pa.NN = NN;
+  probe_begin(OPATTR_PROBE_TL_HIST, s);
   if (pl.nt > 0)
     k_tl_hist<<<(unsigned)pl.nt, 256, 0, s>>>(ta, tlh, at<uint32_t>(ws, pl.pfirst),
                                               at<uint32_t>(ws, pl.plast),
                                               at<uint32_t>(ws, pl.pcnt), x.diag, parts ? 1 : 0);
+  probe_end(OPATTR_PROBE_TL_HIST, s);
+  probe_begin(OPATTR_PROBE_PF_HIST, s);
   if (pl.ntp > 0) k_pf_hist<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, x.diag);
+  probe_end(OPATTR_PROBE_PF_HIST, s);
+  probe_begin(OPATTR_PROBE_COL_SCAN, s);
   column_scan(tlh, pl.nt, NN, at<uint32_t>(ws, pl.tlch), tlc, s);
   column_scan(pfh, pl.ntp, NN, at<uint32_t>(ws, pl.pfch), pfc, s);
   if (NN)
     k_names<<<1, 1024, 0, s>>>(tlc, pfc, NN, off, x.name_counts, x.diag,
                                x.policy == OPATTR_MISMATCH_STRICT ? 1 : 0);
+  probe_end(OPATTR_PROBE_COL_SCAN, s);
+  probe_begin(OPATTR_PROBE_PF_SLOT, s);
   if (pl.ntp > 0)
     k_pf_slot<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
+  probe_end(OPATTR_PROBE_PF_SLOT, s);
   MatchArgs ma;
   ma.tlh = tlh;
   ma.tlc = tlc;
@@ -476,7 +487,9 @@ void run_match(const IomArgs &x, hipStream_t s) {
   ma.mbs = parts ? at<int32_t>(ws, pl.mbs) : nullptr;
   ma.nbs = parts ? at<uint32_t>(ws, pl.nbs) : nullptr;
   ma.skip_name = x.policy == OPATTR_MISMATCH_SKIP_NAME ? 1 : 0;
+  probe_begin(OPATTR_PROBE_TL_MATCH, s);
   if (pl.nt > 0) k_tl_match<<<(unsigned)pl.nt, 256, 0, s>>>(ta, ma);
+  probe_end(OPATTR_PROBE_TL_MATCH, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -595,6 +608,7 @@ void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, op
   a.match = match;
   a.diag = diag;
   const unsigned nb = (unsigned)((pl.T + 255) / 256);
+  probe_begin(OPATTR_PROBE_DEDUP, s);
   if (!stats_ready) {
     note(hipMemsetAsync(at<uint32_t>(ws, pl.pfirst), 0xFF, (size_t)pl.NP * 4, s));
     note(hipMemsetAsync(at<uint32_t>(ws, pl.plast), 0, (size_t)pl.NP * 4, s));
@@ -607,6 +621,7 @@ void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, op
   }
   k_part_check<<<(d->n_parts + 255) / 256, 256, 0, s>>>(a);
   k_dedup<<<nb, 256, 0, s>>>(a);
+  probe_end(OPATTR_PROBE_DEDUP, s);
 }
 
 }  // namespace opa

@@ -67,7 +67,9 @@ assert C.sizeof(opattr_diag) == 64
 
 EXPORTS = ("opattr_workspace_bytes", "opattr_diag_clear", "opattr_read_diag", "opattr_match",
            "opattr_dedup_broadcast", "opattr_enclose", "opattr_aggregate", "opattr_attribute",
-           "opattr_strerror")
+           "opattr_set_probe_events", "opattr_strerror")
+PROBES = ("seq_view", "tl_hist", "pf_hist", "col_scan", "pf_slot", "tl_match", "dedup",
+          "ranges", "main_pass", "finalize")
 
 _lib = None
 
@@ -100,11 +102,25 @@ def library(path: str = LIB_PATH):
     for f in ("opattr_diag_clear", "opattr_read_diag", "opattr_match", "opattr_dedup_broadcast",
               "opattr_enclose", "opattr_aggregate", "opattr_attribute"):
         getattr(L, f).restype = C.c_int
+    L.opattr_set_probe_events.argtypes = [vp, i]
+    L.opattr_set_probe_events.restype = C.c_int
     L.opattr_strerror.argtypes = [i]
     L.opattr_strerror.restype = C.c_char_p
     if path == LIB_PATH:
         _lib = L
     return L
+
+
+def set_probe_events(events) -> None:
+    """events: None, or a list of 2*n torch.cuda.Event (timing enabled, already
+    recorded once so that the HIP event exists), start/stop per probe in the
+    order of PROBES."""
+    L = library()
+    if not events:
+        _check(L.opattr_set_probe_events(None, 0), "opattr_set_probe_events")
+        return
+    arr = (C.c_void_p * len(events))(*[e.cuda_event for e in events])
+    _check(L.opattr_set_probe_events(arr, len(events) // 2), "opattr_set_probe_events")
 
 
 def strerror(status: int) -> str:
