@@ -38,9 +38,12 @@ def algorithmic_bytes(tr):
     outputs = T * (4 + 4)                           # match, range_id
     table = G * 192 + 4 * NP                        # op rows + class map
     per_kernel = {
-        # enclosure + aggregation pass: stream, query, dur, match in; range_id
-        # out; each profiled row once; range starts/ends/parents/ops; op rows
-        "main_pass": T * (2 + 8 + 4 + 4 + 4) + P * 80 + R * (8 + 8 + 4 + 4) + G * 192,
+        # enclosure pass: stream, query in, range_id out; range starts, ends,
+        # parents and ops
+        "main_pass": T * (2 + 8 + 4) + R * (8 + 8 + 4 + 4),
+        # aggregation: dur and match of every launch, each profiled row once,
+        # the operator rows out
+        "aggregate": T * (4 + 4) + P * 80 + G * 192,
         # per-tile rank and join: seq view, name, part in; match out
         "tl_match": T * (4 + 4 + part + 4),
         # per-tile histograms: seq view, name, part in

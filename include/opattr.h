@@ -27,7 +27,8 @@
  *    the host (nothing is enqueued then). Errors that depend on the data are
  *    recorded on the device in the opattr_diag record (flags, counts, status);
  *    outputs are still written. Read them with opattr_read_diag.
- *  - Sizes: every count is < 2^31. n_names <= 2^20 - 1, n_streams <= 65536.
+ *  - Sizes: every count is < 2^31. n_names <= 2^20 - 1, n_ops <= 2^20 - 2,
+ *    n_streams <= 65536.
  *  - Records with an id out of range are left out and counted (bad_records):
  *    launches with name_id >= n_names or part_id outside [-1, n_parts) take no
  *    part in matching and dedup; launches with stream_id >= n_streams enclose
@@ -235,9 +236,10 @@ enum {
   OPATTR_PROBE_TL_MATCH = 5,   /* per-tile rank and join                    */
   OPATTR_PROBE_DEDUP = 6,      /* dedup broadcast                           */
   OPATTR_PROBE_RANGES = 7,     /* range order, parents and depths           */
-  OPATTR_PROBE_MAIN_PASS = 8,  /* enclosure + aggregation pass, operator rows */
+  OPATTR_PROBE_MAIN_PASS = 8,  /* enclosure pass (range ids, operator runs) */
   OPATTR_PROBE_FINALIZE = 9,   /* status of the diag record                 */
-  OPATTR_NUM_PROBES = 10
+  OPATTR_PROBE_AGGREGATE = 10, /* run sort, reduction, operator rows        */
+  OPATTR_NUM_PROBES = 11
 };
 int opattr_set_probe_events(void *const *events, int n);
 

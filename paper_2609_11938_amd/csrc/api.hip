@@ -39,6 +39,9 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.ncht = (pl.nt + kColChunk - 1) / kColChunk;
   pl.nchp = (pl.ntp + kColChunk - 1) / kColChunk;
   pl.ntr_max = pl.R / kRangeTile + (int64_t)pl.NS + 1;
+  pl.nencb = (pl.T + kEncThreads - 1) / kEncThreads;
+  pl.ntrt = (pl.T + OPA_TILE - 1) / OPA_TILE;
+  pl.nchr = (pl.ntrt + kColChunk - 1) / kColChunk;
   const bool dd = has_dedup(k, d);
   const size_t T = (size_t)pl.T, P = (size_t)pl.P, R = (size_t)pl.R, NN = pl.NN;
   Bump b;
@@ -87,7 +90,24 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.tfirst = b.take(ntr * 4);
   pl.tlast = b.take(ntr * 4);
   pl.sflag = b.take(pl.NS);
-  pl.acc = b.take((size_t)pl.G * sizeof(AccRow));
+  const size_t NB = (size_t)pl.nencb, SL = NB * kEncThreads;
+  pl.slot_g = b.take(SL * 4);
+  pl.slot_kb = b.take(SL * 4);
+  pl.slot_len = b.take(SL * 4);
+  pl.nruns = b.take(NB * 4);
+  pl.roff = b.take(NB * 4);
+  pl.cg = b.take(SL * 4);
+  pl.ckb = b.take(SL * 4);
+  pl.clen = b.take(SL * 4);
+  pl.meta = b.take(4 * 8);
+  pl.rth = b.take((size_t)pl.ntrt * pl.G * 4);
+  pl.rtch = b.take((size_t)pl.nchr * pl.G * 4);
+  pl.gcnt = b.take((size_t)pl.G * 4);
+  pl.goff = b.take(((size_t)pl.G + 1) * 4);
+  pl.ioff = b.take(((size_t)pl.G + 1) * 4);
+  pl.skb = b.take(SL * 4);
+  pl.slen = b.take(SL * 4);
+  pl.part = b.take((size_t)max_agg_items(pl.T, pl.G) * sizeof(AccRow));
   pl.misc = b.take(256);
   pl.total = b.off;
   return pl;
@@ -147,7 +167,7 @@ static bool check_dims(const opattr_dims *d) {
   if (!d) return false;
   if (d->n_names > kMaxNames) return false;
   if (d->n_streams > 65536u) return false;
-  if (d->n_ops >= 0x7FFFFFFFu || d->n_parts >= 0x7FFFFFFFu) return false;
+  if (d->n_ops > kMaxOps || d->n_parts >= 0x7FFFFFFFu) return false;
   if (d->flags & ~(OPATTR_KERNELS_STREAM_MAJOR | OPATTR_SEQ_DENSE | OPATTR_RANGES_NESTED |
                    OPATTR_VALIDATE))
     return false;

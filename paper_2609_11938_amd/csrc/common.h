@@ -170,6 +170,23 @@ __device__ __forceinline__ int lds_lower_bound(const uint32_t *a, int n, uint32_
   return lo;
 }
 
+struct TileSmem {
+  uint32_t A[OPA_TILE];
+  uint32_t B[OPA_TILE];
+  TileSortSmem srt;
+  int32_t sh[16];
+  uint32_t bad;
+};
+
+// hist[tile][n] = eligible launches of name n in the tile (all n < NN)
+__device__ inline void write_hist_row(const uint32_t *A, uint32_t NN, uint32_t *row) {
+  for (uint32_t n = threadIdx.x; n < NN; n += OPA_TILE_THREADS) {
+    const int lo = lds_lower_bound(A, OPA_TILE, n << OPA_SLOT_BITS);
+    const int hi = lds_lower_bound(A, OPA_TILE, (n + 1) << OPA_SLOT_BITS);
+    row[n] = (uint32_t)(hi - lo);
+  }
+}
+
 // Diag helpers: device-scope atomics on the caller's record.
 __device__ __forceinline__ void diag_flag(opattr_diag *d, uint32_t f) {
   if (d) atomicOr(&d->flags, f);

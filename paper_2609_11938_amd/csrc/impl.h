@@ -13,9 +13,10 @@ constexpr int kColChunk = 64;       // rows per chunk of the column scans
 constexpr int kEncThreads = 256;    // kernels per enclose/aggregate block
 constexpr int kEncWindow = 1024;    // range starts staged in LDS per block
 constexpr int kMaxWalk = 300;       // bound on parent-chain walks (depth <= 255)
-constexpr uint32_t kMaxNames = (1u << 20) - 1;
+constexpr uint32_t kMaxNames = (1u << 20) - 1;  // names and rows are packed above a 12-bit slot
+constexpr uint32_t kMaxOps = (1u << 20) - 2;    // rows = n_ops + 1
 
-// Accumulator row of the aggregation (device scratch), one per operator.
+// Partial row of the aggregation (device scratch), one per reduction item.
 struct AccRow {
   unsigned long long kc, tns, mc, mns;
   double sum[OPATTR_NUM_COUNTERS];
@@ -28,7 +29,7 @@ struct AccRow {
 struct Plan {
   int64_t T, P, R;
   uint32_t NN, NS, G, NP;
-  int64_t nt, ntp, ncht, nchp, ntr_max;
+  int64_t nt, ntp, ncht, nchp, ntr_max, nencb, ntrt, nchr;
   bool seq_dense, ranges_nested;
   size_t total;
   // IOM
@@ -39,7 +40,8 @@ struct Plan {
   size_t rperm, rs_c, re_c, rst_c, rop_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
   // aggregation
-  size_t acc;
+  size_t slot_g, slot_kb, slot_len, nruns, roff, cg, ckb, clen, meta;
+  size_t rth, rtch, gcnt, goff, ioff, skb, slen, part;
   size_t misc;  // small device scalars
 };
 
@@ -86,6 +88,13 @@ struct CoreRanges {
 // Stable LSD sort of (key, value) pairs over bits [begin_bit, end_bit).
 // Result ends in (k0, v0) when the pass count is even, else (k1, v1); returns
 // true when the result is in k1/v1.
+// Exclusive scan of in[0..n) into out (one block); *total_out = the sum.
+void launch_scan_excl(const uint32_t *in, uint32_t *out, int64_t n, int64_t *total_out,
+                      hipStream_t s);
+// Exclusive prefix down each column of a [rows][cols] table in place, column
+// totals in totals; rows_dev (optional) holds the actual row count on device.
+void column_scan(uint32_t *tab, int64_t rows, uint32_t cols, uint32_t *chs, uint32_t *totals,
+                 hipStream_t s, const int64_t *rows_dev);
 bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, int64_t n,
                       int begin_bit, int end_bit, uint32_t *hist, hipStream_t s);
 size_t radix_hist_entries(int64_t n);
@@ -123,6 +132,14 @@ CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws
 void resolve_ranges(const CoreRanges &cr, const opattr_dims *d, void *ws, const Plan &pl,
                     uint8_t *range_depth, opattr_diag *diag, hipStream_t s);
 
+// Per enclosure block: runs of consecutive launches sharing an operator row.
+struct RunSlots {
+  uint32_t *g, *kb, *len;  // [block * 256 + r]
+  uint32_t *nruns;         // [block]
+};
+RunSlots run_slots(void *ws, const Plan &pl);
+int64_t max_agg_items(int64_t T, uint32_t G);
+
 enum EncMode { kEncloseOnly = 1, kAggregateOnly = 2, kEncloseAggregate = 3 };
 struct EncArgs {
   EncMode mode;
@@ -141,6 +158,7 @@ struct EncArgs {
   const Plan *pl;
 };
 void run_enclose_aggregate(const EncArgs &a, hipStream_t s);
+void run_aggregate(const EncArgs &a, hipStream_t s);
 
 // ---- finish (api.hip) ---------------------------------------------------------
 void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s);

@@ -142,23 +142,6 @@ __device__ inline void part_runs(const int32_t *lpart, int64_t base, uint32_t *p
   }
 }
 
-struct TileSmem {
-  uint32_t A[OPA_TILE];
-  uint32_t B[OPA_TILE];
-  TileSortSmem srt;
-  int32_t sh[16];
-  uint32_t bad;
-};
-
-// hist[tile][n] = eligible launches of name n in the tile (all n < NN)
-__device__ inline void write_hist_row(const uint32_t *A, uint32_t NN, uint32_t *row) {
-  for (uint32_t n = threadIdx.x; n < NN; n += OPA_TILE_THREADS) {
-    const int lo = lds_lower_bound(A, OPA_TILE, n << OPA_SLOT_BITS);
-    const int hi = lds_lower_bound(A, OPA_TILE, (n + 1) << OPA_SLOT_BITS);
-    row[n] = (uint32_t)(hi - lo);
-  }
-}
-
 __global__ void __launch_bounds__(256) k_tl_hist(TlArgs a, uint32_t *tlh, uint32_t *pfirst,
                                                  uint32_t *plast, uint32_t *pcnt,
                                                  opattr_diag *diag, int want_parts) {
@@ -220,12 +203,20 @@ __global__ void __launch_bounds__(256) k_pf_hist(PfArgs a, uint32_t *pfh, opattr
 // column scans of a [rows][cols] histogram table: exclusive prefix down each
 // column, in place, plus the column totals
 // ---------------------------------------------------------------------------
+// rows_dev (optional): the actual row count, known only on the device
+__device__ __forceinline__ int64_t rows_of(int64_t rows, const int64_t *rows_dev) {
+  return rows_dev ? (*rows_dev < rows ? *rows_dev : rows) : rows;
+}
+
 __global__ void __launch_bounds__(256) k_colsum(const uint32_t *__restrict__ tab, int64_t rows,
-                                                uint32_t cols, uint32_t *chs) {
+                                                uint32_t cols, uint32_t *chs,
+                                                const int64_t *rows_dev) {
   __shared__ uint32_t part[4][64];
+  rows = rows_of(rows, rows_dev);
   const int l = lane_id(), w = wave_id();
   const uint32_t col = blockIdx.x * 64 + l;
   const int64_t r0 = (int64_t)blockIdx.y * kColChunk + w * (kColChunk / 4);
+  if ((int64_t)blockIdx.y * kColChunk >= rows) return;
   uint32_t s = 0;
   if (col < cols)
     for (int i = 0; i < kColChunk / 4; ++i) {
@@ -238,9 +229,13 @@ __global__ void __launch_bounds__(256) k_colsum(const uint32_t *__restrict__ tab
     chs[(int64_t)blockIdx.y * cols + col] = part[0][l] + part[1][l] + part[2][l] + part[3][l];
 }
 
-__global__ void k_chunkscan(uint32_t *chs, int64_t nch, uint32_t cols, uint32_t *totals) {
+__global__ void k_chunkscan(uint32_t *chs, int64_t nch, uint32_t cols, uint32_t *totals,
+                            int64_t rows, const int64_t *rows_dev) {
   const uint32_t col = blockIdx.x * blockDim.x + threadIdx.x;
   if (col >= cols) return;
+  rows = rows_of(rows, rows_dev);
+  const int64_t nc = (rows + kColChunk - 1) / kColChunk;
+  if (nc < nch) nch = nc;
   uint32_t run = 0;
   for (int64_t c = 0; c < nch; ++c) {
     const uint32_t v = chs[c * cols + col];
@@ -251,8 +246,11 @@ __global__ void k_chunkscan(uint32_t *chs, int64_t nch, uint32_t cols, uint32_t 
 }
 
 __global__ void __launch_bounds__(256) k_colbase(uint32_t *tab, int64_t rows, uint32_t cols,
-                                                 const uint32_t *__restrict__ chs) {
+                                                 const uint32_t *__restrict__ chs,
+                                                 const int64_t *rows_dev) {
   __shared__ uint32_t part[4][64];
+  rows = rows_of(rows, rows_dev);
+  if ((int64_t)blockIdx.y * kColChunk >= rows) return;
   const int l = lane_id(), w = wave_id();
   const uint32_t col = blockIdx.x * 64 + l;
   const int64_t r0 = (int64_t)blockIdx.y * kColChunk + w * (kColChunk / 4);
@@ -277,14 +275,14 @@ __global__ void __launch_bounds__(256) k_colbase(uint32_t *tab, int64_t rows, ui
   }
 }
 
-static void column_scan(uint32_t *tab, int64_t rows, uint32_t cols, uint32_t *chs,
-                        uint32_t *totals, hipStream_t s) {
+void column_scan(uint32_t *tab, int64_t rows, uint32_t cols, uint32_t *chs, uint32_t *totals,
+                 hipStream_t s, const int64_t *rows_dev) {
   if (rows <= 0 || cols == 0) return;
   const int64_t nch = (rows + kColChunk - 1) / kColChunk;
   dim3 g((cols + 63) / 64, (unsigned)nch);
-  k_colsum<<<g, 256, 0, s>>>(tab, rows, cols, chs);
-  k_chunkscan<<<(cols + 255) / 256, 256, 0, s>>>(chs, nch, cols, totals);
-  k_colbase<<<g, 256, 0, s>>>(tab, rows, cols, chs);
+  k_colsum<<<g, 256, 0, s>>>(tab, rows, cols, chs, rows_dev);
+  k_chunkscan<<<(cols + 255) / 256, 256, 0, s>>>(chs, nch, cols, totals, rows, rows_dev);
+  k_colbase<<<g, 256, 0, s>>>(tab, rows, cols, chs, rows_dev);
 }
 
 // off[n] = rows of names before n; count validation (Sec. 3.3)
@@ -467,8 +465,8 @@ void run_match(const IomArgs &x, hipStream_t s) {
   if (pl.ntp > 0) k_pf_hist<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, x.diag);
   probe_end(OPATTR_PROBE_PF_HIST, s);
   probe_begin(OPATTR_PROBE_COL_SCAN, s);
-  column_scan(tlh, pl.nt, NN, at<uint32_t>(ws, pl.tlch), tlc, s);
-  column_scan(pfh, pl.ntp, NN, at<uint32_t>(ws, pl.pfch), pfc, s);
+  column_scan(tlh, pl.nt, NN, at<uint32_t>(ws, pl.tlch), tlc, s, nullptr);
+  column_scan(pfh, pl.ntp, NN, at<uint32_t>(ws, pl.pfch), pfc, s, nullptr);
   if (NN)
     k_names<<<1, 1024, 0, s>>>(tlc, pfc, NN, off, x.name_counts, x.diag,
                                x.policy == OPATTR_MISMATCH_STRICT ? 1 : 0);

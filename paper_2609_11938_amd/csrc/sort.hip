@@ -48,6 +48,40 @@ __global__ void __launch_bounds__(1024) k_scan_excl_u32(uint32_t *__restrict__ a
   }
 }
 
+// Exclusive scan of in[0..n) into out by one block of 1024 threads.
+__global__ void __launch_bounds__(1024) k_scan_excl_oop(const uint32_t *__restrict__ in,
+                                                        uint32_t *__restrict__ out, int64_t n,
+                                                        int64_t *total_out) {
+  __shared__ uint32_t sh[16];
+  uint32_t carry = 0;
+  for (int64_t base = 0; base < n; base += 4096) {
+    uint32_t v[4];
+    uint32_t s = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t x = base + threadIdx.x * 4 + j;
+      v[j] = x < n ? in[x] : 0u;
+      s += v[j];
+    }
+    uint32_t tot;
+    const uint32_t pre = block_excl_scan_add<uint32_t>(s, sh, &tot);
+    uint32_t run = carry + pre;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t x = base + threadIdx.x * 4 + j;
+      if (x < n) out[x] = run;
+      run += v[j];
+    }
+    carry += tot;
+  }
+  if (threadIdx.x == 0 && total_out) *total_out = carry;
+}
+
+void launch_scan_excl(const uint32_t *in, uint32_t *out, int64_t n, int64_t *total_out,
+                      hipStream_t s) {
+  k_scan_excl_oop<<<1, 1024, 0, s>>>(in, out, n, total_out);
+}
+
 __global__ void __launch_bounds__(256) k_rs_scatter(const uint64_t *__restrict__ kin,
                                                     const uint32_t *__restrict__ vin,
                                                     uint64_t *__restrict__ kout,

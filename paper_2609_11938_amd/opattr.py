@@ -69,15 +69,17 @@ EXPORTS = ("opattr_workspace_bytes", "opattr_diag_clear", "opattr_read_diag", "o
            "opattr_dedup_broadcast", "opattr_enclose", "opattr_aggregate", "opattr_attribute",
            "opattr_set_probe_events", "opattr_strerror")
 PROBES = ("seq_view", "tl_hist", "pf_hist", "col_scan", "pf_slot", "tl_match", "dedup",
-          "ranges", "main_pass", "finalize")
+          "ranges", "main_pass", "finalize", "aggregate")
 
 _lib = None
 
 
-def library(path: str = LIB_PATH):
-    """Load libopattr.so and declare its entry points. Raises when it is not
-    built: this package has no CPU fallback."""
+def library(path: str | None = None):
+    """Load libopattr.so (or the library at ``path``) and declare its entry
+    points. Raises when it is not built: this package has no CPU fallback."""
     global _lib
+    if path is None:
+        path = LIB_PATH
     if _lib is not None and path == LIB_PATH:
         return _lib
     if not os.path.exists(path):
