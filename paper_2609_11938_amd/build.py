@@ -13,8 +13,6 @@ ARCH = os.environ.get("OPATTR_ARCH", "gfx950")
 
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared", f"--offload-arch={ARCH}",
-    # hardware fp64 atomic add for the operator accumulators
-    "-munsafe-fp-atomics",
     # packed fp32 instructions are disabled for all device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",

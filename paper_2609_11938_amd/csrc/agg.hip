@@ -1,339 +1,255 @@
-// Per-operator aggregation (Eq. 1, Sec. 3.8.1) without atomics.
+// Per-operator aggregation (Eq. 1, Sec. 3.8.1), second and third levels.
 //
-// The enclosure pass leaves, per block of launches, runs of consecutive
-// launches that share an operator row. Here the runs are
-//   1. compacted in launch order,
-//   2. counting-sorted by row (tiles of 4096 runs sorted in LDS, per-tile row
-//      histograms scanned down the columns; stable, so each row keeps its runs
-//      in launch order),
-//   3. cut into items of at most 32 runs of one row, each reduced by one
-//      workgroup: every thread accumulates its launches in registers (u64
-//      counts and ns, fp64 sums of m or m*d, an order-preserving key for the
-//      fp32 maximum), then one block reduction writes the item's partial row,
-//   4. combined per row in item order by one wave, then finalised (duration-
-//      weighted means divided by the matched duration, NaN for absent
-//      counters and rows without matched launches).
+// The enclosure pass leaves, in launch order, items of one operator row each:
+// either a partial row (a run it reduced in place) or a reference to at most
+// 16 launches. Here the items are
+//   1. counting-sorted by row (per-tile row histograms scanned down the
+//      columns; stable, so each row keeps its items in launch order),
+//   2. cut into chunks of at most 64 items of one row, each reduced by one
+//      wave (a lane loads a partial row or accumulates its referenced
+//      launches, then a butterfly reduction),
+//   3. combined per row over its chunks by one wave and finalised
+//      (duration-weighted means divided by the matched duration, NaN for
+//      absent counters and rows without matched launches).
 // Every sum is taken in a fixed order, so results are reproducible.
+#include "accum.h"
 #include "common.h"
 #include "impl.h"
 
 namespace opa {
 
-constexpr int kRunsPerItem = 32;
+constexpr int kChunkItems = 64;
 
-RunSlots run_slots(void *ws, const Plan &pl) {
-  RunSlots r;
-  r.g = at<uint32_t>(ws, pl.slot_g);
-  r.kb = at<uint32_t>(ws, pl.slot_kb);
-  r.len = at<uint32_t>(ws, pl.slot_len);
-  r.nruns = at<uint32_t>(ws, pl.nruns);
-  return r;
+EmitOut emit_out(void *ws, const Plan &pl) {
+  EmitOut e;
+  e.state = at<unsigned long long>(ws, pl.lbs);
+  e.ctr = reinterpret_cast<uint32_t *>(e.state + pl.nencb);
+  e.ig = at<uint32_t>(ws, pl.ig);
+  e.ia = at<uint32_t>(ws, pl.ia);
+  e.ib = at<uint32_t>(ws, pl.ib);
+  e.rows = at<PartRow>(ws, pl.rows);
+  e.meta = at<int64_t>(ws, pl.meta);
+  e.nblocks = pl.nencb;
+  return e;
+}
+
+AggIn agg_inputs(const EncArgs &x) {
+  AggIn in{};
+  in.dur = x.k->dur_ns;
+  in.match = x.match;
+  in.P = x.p->n;
+  in.counters = x.p->counters;
+  in.rs = x.p->row_stride;
+  in.cs = x.p->col_stride;
+  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
+    if (x.agg_kind[c] == OPATTR_AGG_DWMEAN) in.dwmask |= 1u << c;
+    else if (x.agg_kind[c] == OPATTR_AGG_MAX) in.maxmask |= 1u << c;
+  }
+  in.vec4 = in.cs == 1 && (in.rs % 4) == 0 &&
+            (reinterpret_cast<uintptr_t>(in.counters) & 15) == 0;
+  return in;
 }
 
 struct AggWork {
-  int64_t T, nencb, ntrt;
-  uint32_t G, NOPS;
-  RunSlots slots;
-  const uint32_t *roff;
-  uint32_t *cg, *ckb, *clen;
-  int64_t *meta;  // [0] runs, [1] run tiles, [2] items
-  uint32_t *rth, *rtch, *gcnt, *goff, *ioff, *skb, *slen;
-  AccRow *part;
-  // inputs
-  const uint32_t *dur;
-  const int32_t *match;
-  int64_t P;
-  const float *counters;
-  int64_t rs, cs;
-  uint32_t dwmask, maxmask, absent;
+  uint32_t G, NOPS, absent;
+  AggIn in;
+  const uint32_t *ig, *ia, *ib;
+  const PartRow *rows;
+  int64_t *meta;  // [0] items, [1] partial rows, [2] item tiles, [3] chunks
+  uint32_t *ith, *gcnt, *goff, *coff, *cmap, *sidx;
+  PartRow *part;
   opattr_op_row *table;
   opattr_summary *sum;
 };
 
-// 1. compaction: one wave per enclosure block
-__global__ void __launch_bounds__(256) k_run_compact(AggWork w) {
-  const int64_t b = (int64_t)blockIdx.x * 4 + wave_id();
-  if (b == 0 && lane_id() == 0) {
-    const int64_t nr = w.meta[0];
-    w.meta[1] = (nr + OPA_TILE - 1) / OPA_TILE;
-  }
-  if (b >= w.nencb) return;
-  const uint32_t n = w.slots.nruns[b];
-  const uint32_t o = w.roff[b];
-  for (uint32_t r = lane_id(); r < n; r += OPA_WAVE) {
-    const int64_t src = b * kEncThreads + r;
-    w.cg[o + r] = w.slots.g[src];
-    w.ckb[o + r] = w.slots.kb[src];
-    w.clen[o + r] = w.slots.len[src];
+__device__ __forceinline__ int64_t item_x(int64_t tile, int c) {
+  return tile * OPA_TILE + wave_id() * (OPA_TILE / 4) + c * OPA_WAVE + lane_id();
+}
+
+// 1a. per-tile row histograms of the items (tile = 4096 items in launch order)
+__global__ void __launch_bounds__(256) k_item_hist_w(AggWork w) {
+  extern __shared__ __align__(16) unsigned char raw[];
+  uint16_t *cnt = reinterpret_cast<uint16_t *>(raw);
+  const int64_t n = w.meta[0];
+  const int64_t ntiles = (n + OPA_TILE - 1) / OPA_TILE;
+  if (blockIdx.x == 0 && threadIdx.x == 0) w.meta[2] = ntiles;
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < 4 * w.G; i += 256) cnt[i] = 0;
+    __syncthreads();
+    uint32_t key[16], rank[16];
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      const int64_t x = item_x(tile, c);
+      key[c] = x < n ? w.ig[x] : w.G;
+    }
+    wave_rank<16>(key, w.G, bits_for(w.G), cnt + wave_id() * w.G, rank);
+    block_rank_bases(cnt, w.G, w.ith + tile * w.G);
   }
 }
 
-__device__ inline void run_tile_keys(const AggWork &w, int64_t base, int64_t nr, uint32_t *A) {
-  for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
-    const int l = c * OPA_TILE_THREADS + threadIdx.x;
-    const int64_t x = base + l;
-    const uint32_t g = x < nr ? w.cg[x] : w.G;
-    A[l] = (g << OPA_SLOT_BITS) | (uint32_t)l;
-  }
-}
-
-// 2a. per-tile row histograms
-__global__ void __launch_bounds__(256) k_run_hist(AggWork w) {
+// 1a'. the same with an LDS radix sort per tile, for many rows
+__global__ void __launch_bounds__(256) k_item_hist_r(AggWork w) {
   __shared__ TileSmem sm;
-  const int64_t nr = w.meta[0];
-  const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
-  if (base >= nr) return;
-  run_tile_keys(w, base, nr, sm.A);
-  __syncthreads();
-  tile_radix_sort(sm.A, sm.B, sm.srt, OPA_SLOT_BITS, bits_for(w.G));
-  write_hist_row(sm.A, w.G, w.rth + (int64_t)blockIdx.x * w.G);
+  const int64_t n = w.meta[0];
+  const int64_t ntiles = (n + OPA_TILE - 1) / OPA_TILE;
+  if (blockIdx.x == 0 && threadIdx.x == 0) w.meta[2] = ntiles;
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    __syncthreads();
+    for (int l = threadIdx.x; l < OPA_TILE; l += 256) {
+      const int64_t x = tile * OPA_TILE + l;
+      const uint32_t g = x < n ? w.ig[x] : w.G;
+      sm.A[l] = (g << OPA_SLOT_BITS) | (uint32_t)l;
+    }
+    __syncthreads();
+    tile_radix_sort(sm.A, sm.B, sm.srt, OPA_SLOT_BITS, bits_for(w.G));
+    write_hist_row(sm.A, w.G, w.ith + tile * w.G);
+  }
 }
 
-// 2b. row offsets of the sorted runs and item offsets (one block)
+// 1b. row offsets of the sorted items and chunk offsets (one block)
 __global__ void __launch_bounds__(1024) k_row_offsets(AggWork w) {
   __shared__ uint32_t sh[16];
-  uint32_t carry = 0, icarry = 0;
+  uint32_t carry = 0, ccarry = 0;
   for (uint32_t base = 0; base < w.G; base += 1024) {
     const uint32_t g = base + threadIdx.x;
     const uint32_t c = g < w.G ? w.gcnt[g] : 0u;
-    const uint32_t it = (c + kRunsPerItem - 1) / kRunsPerItem;
-    uint32_t tot, itot;
+    const uint32_t ch = (c + kChunkItems - 1) / kChunkItems;
+    uint32_t tot, ctot;
     const uint32_t pre = block_excl_scan_add<uint32_t>(c, sh, &tot);
-    const uint32_t ipre = block_excl_scan_add<uint32_t>(it, sh, &itot);
+    const uint32_t cpre = block_excl_scan_add<uint32_t>(ch, sh, &ctot);
     if (g < w.G) {
       w.goff[g] = carry + pre;
-      w.ioff[g] = icarry + ipre;
+      w.coff[g] = ccarry + cpre;
     }
     carry += tot;
-    icarry += itot;
+    ccarry += ctot;
   }
   if (threadIdx.x == 0) {
     w.goff[w.G] = carry;
-    w.ioff[w.G] = icarry;
-    w.meta[2] = icarry;
+    w.coff[w.G] = ccarry;
+    w.meta[3] = ccarry;
   }
 }
 
-// 2c. stable scatter of the runs into row order
-__global__ void __launch_bounds__(256) k_run_scatter(AggWork w) {
+// 1c. stable scatter of the items into row order
+__global__ void __launch_bounds__(256) k_item_scatter_w(AggWork w) {
+  extern __shared__ __align__(16) unsigned char raw[];
+  uint16_t *cnt = reinterpret_cast<uint16_t *>(raw);
+  const int64_t n = w.meta[0];
+  const int64_t ntiles = (n + OPA_TILE - 1) / OPA_TILE;
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < 4 * w.G; i += 256) cnt[i] = 0;
+    __syncthreads();
+    uint32_t key[16], rank[16];
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      const int64_t x = item_x(tile, c);
+      key[c] = x < n ? w.ig[x] : w.G;
+    }
+    wave_rank<16>(key, w.G, bits_for(w.G), cnt + wave_id() * w.G, rank);
+    block_rank_bases(cnt, w.G, nullptr);
+    const uint32_t *row = w.ith + tile * w.G;
+    const uint16_t *wb = cnt + wave_id() * w.G;
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      const uint32_t g = key[c];
+      if (g >= w.G) continue;
+      w.sidx[w.goff[g] + row[g] + wb[g] + rank[c]] = (uint32_t)item_x(tile, c);
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256) k_item_scatter_r(AggWork w) {
   __shared__ TileSmem sm;
-  const int64_t nr = w.meta[0];
-  const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
-  if (base >= nr) return;
-  run_tile_keys(w, base, nr, sm.A);
-  __syncthreads();
-  tile_radix_sort(sm.A, sm.B, sm.srt, OPA_SLOT_BITS, bits_for(w.G));
-  const uint32_t *row = w.rth + (int64_t)blockIdx.x * w.G;
-  for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
-    const int p = c * OPA_TILE_THREADS + threadIdx.x;
-    const uint32_t key = sm.A[p];
-    const uint32_t g = key >> OPA_SLOT_BITS;
-    if (g >= w.G) continue;
-    const int lo = lds_lower_bound(sm.A, OPA_TILE, g << OPA_SLOT_BITS);
-    const uint32_t dst = w.goff[g] + row[g] + (uint32_t)(p - lo);
-    const int64_t x = base + (key & (OPA_TILE - 1));
-    w.skb[dst] = w.ckb[x];
-    w.slen[dst] = w.clen[x];
+  const int64_t n = w.meta[0];
+  const int64_t ntiles = (n + OPA_TILE - 1) / OPA_TILE;
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    __syncthreads();
+    for (int l = threadIdx.x; l < OPA_TILE; l += 256) {
+      const int64_t x = tile * OPA_TILE + l;
+      const uint32_t g = x < n ? w.ig[x] : w.G;
+      sm.A[l] = (g << OPA_SLOT_BITS) | (uint32_t)l;
+    }
+    __syncthreads();
+    tile_radix_sort(sm.A, sm.B, sm.srt, OPA_SLOT_BITS, bits_for(w.G));
+    const uint32_t *row = w.ith + tile * w.G;
+    for (int p = threadIdx.x; p < OPA_TILE; p += 256) {
+      const uint32_t key = sm.A[p];
+      const uint32_t g = key >> OPA_SLOT_BITS;
+      if (g >= w.G) continue;
+      const int lo = lds_lower_bound(sm.A, OPA_TILE, g << OPA_SLOT_BITS);
+      w.sidx[w.goff[g] + row[g] + (uint32_t)(p - lo)] =
+          (uint32_t)(tile * OPA_TILE + (key & (OPA_TILE - 1)));
+    }
   }
 }
 
-__device__ __forceinline__ uint32_t f2key(float f) {
-  const uint32_t b = __float_as_uint(f);
-  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
-}
-__device__ __forceinline__ float key2f(uint32_t k) {
-  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
-}
-
-// last index g in [0, n) with a[g] <= x (a non-decreasing, a[0] <= x)
-__device__ __forceinline__ uint32_t last_le(const uint32_t *a, uint32_t n, uint32_t x) {
-  uint32_t lo = 0, hi = n;
-  while (lo + 1 < hi) {
-    const uint32_t mid = (lo + hi) >> 1;
-    if (a[mid] <= x) lo = mid;
-    else hi = mid;
-  }
-  return lo;
+// 1d. chunk -> row map
+__global__ void k_chunk_map(AggWork w) {
+  const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= w.G) return;
+  for (uint32_t c = w.coff[g]; c < w.coff[g + 1]; ++c) w.cmap[c] = g;
 }
 
-// 3. one workgroup per item (grid-stride over items)
-__global__ void __launch_bounds__(256) k_reduce(AggWork w) {
-  __shared__ uint32_t kb[kRunsPerItem];
-  __shared__ uint32_t pre[kRunsPerItem + 1];
-  __shared__ unsigned long long ired[4][4];
-  __shared__ double fred[4][OPATTR_NUM_COUNTERS];
-  __shared__ uint32_t kred[4][OPATTR_NUM_COUNTERS + 1];
-  const int64_t nitems = w.meta[2];
-  const int tid = threadIdx.x, wv = wave_id(), ln = lane_id();
-  for (int64_t item = blockIdx.x; item < nitems; item += gridDim.x) {
-    const uint32_t g = last_le(w.ioff, w.G, (uint32_t)item);
-    const uint32_t first = w.goff[g] + ((uint32_t)item - w.ioff[g]) * kRunsPerItem;
-    const uint32_t end = w.goff[g + 1];
-    const int nrun = (int)min((uint32_t)kRunsPerItem, end - first);
-    if (wv == 0) {
-      const uint32_t len = ln < nrun ? w.slen[first + ln] : 0u;
-      if (ln < nrun) kb[ln] = w.skb[first + ln];
-      const uint32_t inc = wave_incl_scan_add(len);
-      if (ln < kRunsPerItem) pre[ln + 1] = inc;
-      if (ln == 0) pre[0] = 0;
-    }
-    __syncthreads();
-    const uint32_t K = pre[nrun];
-    unsigned long long kc = 0, tn = 0, mc = 0, mn = 0;
-    double f[OPATTR_NUM_COUNTERS];
-    uint32_t mk[OPATTR_NUM_COUNTERS];
-#pragma unroll
-    for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-      f[c] = 0.0;
-      mk[c] = 0u;
-    }
-    uint32_t nanb = 0;
-    for (uint32_t pos = tid; pos < K; pos += 256) {
-      int lo = 0, hi = nrun;  // run holding pos: last r with pre[r] <= pos
-      while (lo + 1 < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (pre[mid] <= pos) lo = mid;
-        else hi = mid;
-      }
-      const int64_t k = (int64_t)kb[lo] + (pos - pre[lo]);
-      const uint32_t d = w.dur[k];
-      const int32_t m = w.match[k];
-      kc += 1;
-      tn += d;
-      if (m >= 0 && m < w.P) {
-        mc += 1;
-        mn += d;
-        const float *row = w.counters + (int64_t)m * w.rs;
-        const double dd = (double)d;
-#pragma unroll
-        for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-          const float v = row[(int64_t)c * w.cs];
-          if ((w.maxmask >> c) & 1u) {
-            const uint32_t key = f2key(v);
-            mk[c] = key > mk[c] ? key : mk[c];
-            if (v != v) nanb |= 1u << c;
-          } else {
-            f[c] += ((w.dwmask >> c) & 1u) ? (double)v * dd : (double)v;  // m_i * d_i
-          }
-        }
-      }
-    }
-    // block reduction
-    kc = wave_reduce_add(kc);
-    tn = wave_reduce_add(tn);
-    mc = wave_reduce_add(mc);
-    mn = wave_reduce_add(mn);
-#pragma unroll
-    for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-      f[c] = wave_reduce_add(f[c]);
-      uint32_t x = mk[c];
-      for (int o = OPA_WAVE / 2; o > 0; o >>= 1) {
-        const uint32_t y = __shfl_xor(x, o, OPA_WAVE);
-        x = y > x ? y : x;
-      }
-      mk[c] = x;
-    }
-    for (int o = OPA_WAVE / 2; o > 0; o >>= 1) nanb |= __shfl_xor(nanb, o, OPA_WAVE);
-    if (ln == 0) {
-      ired[wv][0] = kc;
-      ired[wv][1] = tn;
-      ired[wv][2] = mc;
-      ired[wv][3] = mn;
-#pragma unroll
-      for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-        fred[wv][c] = f[c];
-        kred[wv][c] = mk[c];
-      }
-      kred[wv][OPATTR_NUM_COUNTERS] = nanb;
-    }
-    __syncthreads();
-    AccRow *out = w.part + item;
-    if (tid < 4) {
-      unsigned long long s = 0;
-      for (int k2 = 0; k2 < 4; ++k2) s += ired[k2][tid];
-      (&out->kc)[tid] = s;
-    } else if (tid >= 64 && tid < 64 + OPATTR_NUM_COUNTERS) {
-      const int c = tid - 64;
-      out->sum[c] = ((fred[0][c] + fred[1][c]) + fred[2][c]) + fred[3][c];
-    } else if (tid >= 128 && tid < 128 + OPATTR_NUM_COUNTERS + 1) {
-      const int c = tid - 128;
-      uint32_t x;
-      if (c < OPATTR_NUM_COUNTERS) {
-        x = kred[0][c];
-        for (int k2 = 1; k2 < 4; ++k2) x = kred[k2][c] > x ? kred[k2][c] : x;
-        out->maxk[c] = x;
+// 2. one wave per chunk of at most 64 items of one row
+__global__ void __launch_bounds__(256) k_chunk_reduce(AggWork w) {
+  const int64_t nch = w.meta[3];
+  const int ln = lane_id();
+  for (int64_t ch = (int64_t)blockIdx.x * 4 + wave_id(); ch < nch; ch += (int64_t)gridDim.x * 4) {
+    const uint32_t g = w.cmap[ch];
+    const uint32_t p = w.goff[g] + (uint32_t)(ch - w.coff[g]) * kChunkItems + (uint32_t)ln;
+    Acc acc;
+    acc_zero(acc);
+    if (p < w.goff[g + 1]) {
+      const uint32_t it = w.sidx[p];
+      const uint32_t a = w.ia[it], b = w.ib[it];
+      if (b == 0) {
+        acc_load(acc, w.rows + a);
       } else {
-        x = kred[0][c] | kred[1][c] | kred[2][c] | kred[3][c];
-        out->nanmask = x;
+        for (uint32_t k = 0; k < b; ++k) acc_launch(acc, w.in, w.in.match[a + k], w.in.dur[a + k]);
       }
     }
-    __syncthreads();
+    acc_wave_reduce(acc, w.in.maxmask);
+    if (ln == 0) acc_store(w.part + ch, acc, g);
   }
 }
 
-// 4. one wave per operator row: combine its items in order and finalise
+// 3. one wave per operator row: combine its chunks and finalise
 __global__ void __launch_bounds__(256) k_combine(AggWork w) {
   const uint32_t g = blockIdx.x * 4 + wave_id();
   if (g >= w.G) return;
   const int ln = lane_id();
-  const uint32_t i0 = w.ioff[g], i1 = w.ioff[g + 1];
-  unsigned long long kc = 0, tn = 0, mc = 0, mn = 0;
-  double f[OPATTR_NUM_COUNTERS];
-  uint32_t mk[OPATTR_NUM_COUNTERS];
-#pragma unroll
-  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-    f[c] = 0.0;
-    mk[c] = 0u;
+  const uint32_t c0 = w.coff[g], c1 = w.coff[g + 1];
+  Acc acc;
+  acc_zero(acc);
+  for (uint32_t c = c0 + ln; c < c1; c += OPA_WAVE) {
+    Acc b;
+    acc_load(b, w.part + c);
+    acc_merge(acc, b, w.in.maxmask);
   }
-  uint32_t nanb = 0;
-  for (uint32_t it = i0 + ln; it < i1; it += OPA_WAVE) {
-    const AccRow &p = w.part[it];
-    kc += p.kc;
-    tn += p.tns;
-    mc += p.mc;
-    mn += p.mns;
-#pragma unroll
-    for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-      f[c] += p.sum[c];
-      mk[c] = p.maxk[c] > mk[c] ? p.maxk[c] : mk[c];
-    }
-    nanb |= p.nanmask;
-  }
-  kc = wave_reduce_add(kc);
-  tn = wave_reduce_add(tn);
-  mc = wave_reduce_add(mc);
-  mn = wave_reduce_add(mn);
-  for (int o = OPA_WAVE / 2; o > 0; o >>= 1) nanb |= __shfl_xor(nanb, o, OPA_WAVE);
-  double mine = 0.0;
-  uint32_t mykey = 0;
-#pragma unroll
-  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-    const double s = wave_reduce_add(f[c]);
-    uint32_t x = mk[c];
-    for (int o = OPA_WAVE / 2; o > 0; o >>= 1) {
-      const uint32_t y = __shfl_xor(x, o, OPA_WAVE);
-      x = y > x ? y : x;
-    }
-    if (ln == c) {
-      mine = s;
-      mykey = x;
-    }
-  }
+  acc_wave_reduce(acc, w.in.maxmask);
   opattr_op_row *row = w.table + g;
   if (ln == 0) {
-    row->kernel_count = kc;
-    row->total_ns = tn;
-    row->matched_count = mc;
-    row->matched_ns = mn;
+    row->kernel_count = acc.kc;
+    row->total_ns = acc.tns;
+    row->matched_count = acc.mc;
+    row->matched_ns = acc.mns;
   }
   if (ln < OPATTR_NUM_COUNTERS) {
     const int c = ln;
+    unsigned long long mine = 0;
+#pragma unroll
+    for (int k = 0; k < OPATTR_NUM_COUNTERS; ++k)
+      if (k == c) mine = acc.v[k];
     const double qnan = __longlong_as_double(0x7FF8000000000000ll);
     double v;
-    if (((w.absent >> c) & 1u) || mc == 0) v = qnan;
-    else if ((w.maxmask >> c) & 1u) v = ((nanb >> c) & 1u) ? qnan : (double)key2f(mykey);
-    else if ((w.dwmask >> c) & 1u) v = mn ? mine / (double)mn : qnan;
-    else v = mine;
+    if (((w.absent >> c) & 1u) || acc.mc == 0) v = qnan;
+    else if ((w.in.maxmask >> c) & 1u)
+      v = ((acc.nan >> c) & 1u) ? qnan : (double)key2f((uint32_t)mine);
+    else if ((w.in.dwmask >> c) & 1u) v = acc.mns ? bits2d(mine) / (double)acc.mns : qnan;
+    else v = bits2d(mine);
     row->value[c] = v;
   }
 }
@@ -377,61 +293,48 @@ __global__ void __launch_bounds__(1024) k_summary(AggWork w) {
 void run_aggregate(const EncArgs &x, hipStream_t s) {
   const Plan &pl = *x.pl;
   AggWork w{};
-  w.T = pl.T;
-  w.nencb = pl.nencb;
-  w.ntrt = pl.ntrt;
   w.G = pl.G;
   w.NOPS = x.d->n_ops;
-  w.slots = run_slots(x.ws, pl);
-  w.roff = at<uint32_t>(x.ws, pl.roff);
-  w.cg = at<uint32_t>(x.ws, pl.cg);
-  w.ckb = at<uint32_t>(x.ws, pl.ckb);
-  w.clen = at<uint32_t>(x.ws, pl.clen);
+  w.absent = x.p->absent_mask;
+  w.in = agg_inputs(x);
+  w.ig = at<uint32_t>(x.ws, pl.ig);
+  w.ia = at<uint32_t>(x.ws, pl.ia);
+  w.ib = at<uint32_t>(x.ws, pl.ib);
+  w.rows = at<PartRow>(x.ws, pl.rows);
   w.meta = at<int64_t>(x.ws, pl.meta);
-  w.rth = at<uint32_t>(x.ws, pl.rth);
-  w.rtch = at<uint32_t>(x.ws, pl.rtch);
+  w.ith = at<uint32_t>(x.ws, pl.ith);
   w.gcnt = at<uint32_t>(x.ws, pl.gcnt);
   w.goff = at<uint32_t>(x.ws, pl.goff);
-  w.ioff = at<uint32_t>(x.ws, pl.ioff);
-  w.skb = at<uint32_t>(x.ws, pl.skb);
-  w.slen = at<uint32_t>(x.ws, pl.slen);
-  w.part = at<AccRow>(x.ws, pl.part);
-  w.dur = x.k->dur_ns;
-  w.match = x.match;
-  w.P = x.p->n;
-  w.counters = x.p->counters;
-  w.rs = x.p->row_stride;
-  w.cs = x.p->col_stride;
-  w.absent = x.p->absent_mask;
-  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-    if (x.agg_kind[c] == OPATTR_AGG_DWMEAN) w.dwmask |= 1u << c;
-    else if (x.agg_kind[c] == OPATTR_AGG_MAX) w.maxmask |= 1u << c;
-  }
+  w.coff = at<uint32_t>(x.ws, pl.coff);
+  w.cmap = at<uint32_t>(x.ws, pl.cmap);
+  w.sidx = at<uint32_t>(x.ws, pl.sidx);
+  w.part = at<PartRow>(x.ws, pl.part);
   w.table = x.table;
   w.sum = x.sum;
+  const bool fast = pl.G <= kFastKeys;
+  const size_t lds = (size_t)4 * pl.G * sizeof(uint16_t);
+  const unsigned tgrid = (unsigned)(pl.ntrt < 1024 ? (pl.ntrt > 0 ? pl.ntrt : 1) : 1024);
 
   probe_begin(OPATTR_PROBE_AGGREGATE, s);
-  note(hipMemsetAsync(w.gcnt, 0, (size_t)pl.G * 4, s));
+  fill_u32(w.gcnt, 0, pl.G, s);
   if (pl.T > 0) {
-    launch_scan_excl(w.slots.nruns, at<uint32_t>(x.ws, pl.roff), pl.nencb, w.meta, s);
-    k_run_compact<<<(unsigned)((pl.nencb + 3) / 4), 256, 0, s>>>(w);
-    k_run_hist<<<(unsigned)pl.ntrt, 256, 0, s>>>(w);
-    column_scan(w.rth, pl.ntrt, pl.G, w.rtch, w.gcnt, s, w.meta + 1);
+    if (fast) k_item_hist_w<<<tgrid, 256, lds, s>>>(w);
+    else k_item_hist_r<<<tgrid, 256, 0, s>>>(w);
+    column_scan(w.ith, pl.ntrt, pl.G, at<uint32_t>(x.ws, pl.itch), w.gcnt, s, w.meta + 2);
   } else {
-    note(hipMemsetAsync(w.meta, 0, 3 * sizeof(int64_t), s));
+    fill_u32(reinterpret_cast<uint32_t *>(w.meta), 0, 8, s);
   }
   k_row_offsets<<<1, 1024, 0, s>>>(w);
   if (pl.T > 0) {
-    k_run_scatter<<<(unsigned)pl.ntrt, 256, 0, s>>>(w);
-    const int64_t max_items = pl.T / kRunsPerItem + pl.G + 1;
-    const unsigned grid = (unsigned)(max_items < 16384 ? max_items : 16384);
-    k_reduce<<<grid, 256, 0, s>>>(w);
+    if (fast) k_item_scatter_w<<<tgrid, 256, lds, s>>>(w);
+    else k_item_scatter_r<<<tgrid, 256, 0, s>>>(w);
+    k_chunk_map<<<(pl.G + 255) / 256, 256, 0, s>>>(w);
+    const int64_t want = (pl.max_chunks + 3) / 4;
+    k_chunk_reduce<<<(unsigned)(want < 2048 ? want : 2048), 256, 0, s>>>(w);
   }
   k_combine<<<(pl.G + 3) / 4, 256, 0, s>>>(w);
   k_summary<<<1, 1024, 0, s>>>(w);
   probe_end(OPATTR_PROBE_AGGREGATE, s);
 }
-
-int64_t max_agg_items(int64_t T, uint32_t G) { return T / kRunsPerItem + G + 1; }
 
 }  // namespace opa

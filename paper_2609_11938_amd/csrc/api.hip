@@ -39,7 +39,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.ncht = (pl.nt + kColChunk - 1) / kColChunk;
   pl.nchp = (pl.ntp + kColChunk - 1) / kColChunk;
   pl.ntr_max = pl.R / kRangeTile + (int64_t)pl.NS + 1;
-  pl.nencb = (pl.T + kEncThreads - 1) / kEncThreads;
+  pl.nencb = (pl.T + kEncSpan - 1) / kEncSpan;
   pl.ntrt = (pl.T + OPA_TILE - 1) / OPA_TILE;
   pl.nchr = (pl.ntrt + kColChunk - 1) / kColChunk;
   const bool dd = has_dedup(k, d);
@@ -62,7 +62,6 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.slot = b.take(P * 4);
   pl.pfirst = b.take(dd ? (size_t)pl.NP * 4 : 0);
   pl.plast = b.take(dd ? (size_t)pl.NP * 4 : 0);
-  pl.pcnt = b.take(dd ? (size_t)pl.NP * 4 : 0);
   pl.contig = b.take(dd ? (size_t)pl.NP : 0);
   pl.mbs = b.take(dd ? T * 4 : 0);
   pl.nbs = b.take(dd ? T * 4 : 0);
@@ -90,24 +89,25 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.tfirst = b.take(ntr * 4);
   pl.tlast = b.take(ntr * 4);
   pl.sflag = b.take(pl.NS);
-  const size_t NB = (size_t)pl.nencb, SL = NB * kEncThreads;
-  pl.slot_g = b.take(SL * 4);
-  pl.slot_kb = b.take(SL * 4);
-  pl.slot_len = b.take(SL * 4);
-  pl.nruns = b.take(NB * 4);
-  pl.roff = b.take(NB * 4);
-  pl.cg = b.take(SL * 4);
-  pl.ckb = b.take(SL * 4);
-  pl.clen = b.take(SL * 4);
-  pl.meta = b.take(4 * 8);
-  pl.rth = b.take((size_t)pl.ntrt * pl.G * 4);
-  pl.rtch = b.take((size_t)pl.nchr * pl.G * 4);
+  // aggregation: items (at most one per launch), partial rows (at most
+  // kEncRowsPerWave per 64 * 8 launches), chunks of 64 items per row
+  pl.cap_items = pl.T;
+  pl.cap_rows = pl.nencb * (kEncThreads / OPA_WAVE) * kEncRowsPerWave;
+  pl.max_chunks = pl.T / 64 + pl.G + 1;
+  pl.lbs = b.take(((size_t)pl.nencb + 1) * 8);
+  pl.ig = b.take((size_t)pl.cap_items * 4);
+  pl.ia = b.take((size_t)pl.cap_items * 4);
+  pl.ib = b.take((size_t)pl.cap_items * 4);
+  pl.rows = b.take((size_t)pl.cap_rows * 200);
+  pl.meta = b.take(8 * 8);
+  pl.ith = b.take((size_t)pl.ntrt * pl.G * 4);
+  pl.itch = b.take((size_t)pl.nchr * pl.G * 4);
   pl.gcnt = b.take((size_t)pl.G * 4);
   pl.goff = b.take(((size_t)pl.G + 1) * 4);
-  pl.ioff = b.take(((size_t)pl.G + 1) * 4);
-  pl.skb = b.take(SL * 4);
-  pl.slen = b.take(SL * 4);
-  pl.part = b.take((size_t)max_agg_items(pl.T, pl.G) * sizeof(AccRow));
+  pl.coff = b.take(((size_t)pl.G + 1) * 4);
+  pl.cmap = b.take((size_t)pl.max_chunks * 4);
+  pl.sidx = b.take((size_t)pl.cap_items * 4);
+  pl.part = b.take((size_t)pl.max_chunks * 200);
   pl.misc = b.take(256);
   pl.total = b.off;
   return pl;
@@ -219,7 +219,7 @@ size_t opattr_workspace_bytes(const opattr_kernels *k, const opattr_profiled *p,
 
 int opattr_diag_clear(opattr_diag *diag, void *stream) {
   if (!diag) return OPATTR_ERR_INVALID_ARG;
-  note(hipMemsetAsync(diag, 0, sizeof(opattr_diag), (hipStream_t)stream));
+  fill_u32(reinterpret_cast<uint32_t *>(diag), 0, sizeof(opattr_diag) / 4, (hipStream_t)stream);
   return launch_status();
 }
 

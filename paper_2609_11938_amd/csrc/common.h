@@ -33,6 +33,58 @@ __device__ __forceinline__ uint64_t peers8(uint32_t d) {
   return m;
 }
 
+// Lanes whose keys agree on bits [0, nbits) (nbits uniform across the wave).
+__device__ __forceinline__ uint64_t match_any_bits(uint32_t key, int nbits) {
+  uint64_t m = ~0ull;
+  for (int b = 0; b < nbits; ++b) {
+    const uint32_t bit = (key >> b) & 1u;
+    const uint64_t v = __ballot(bit);
+    m &= bit ? v : ~v;
+  }
+  return m;
+}
+
+// Stable ranking with per-wave counters. The wave owns CH chunks of 64
+// elements, visited in order; key[c] is the lane's key in chunk c. On return
+// rank[c] = number of earlier elements of the wave with the same key, and
+// cnt[k] (this wave's counters in LDS, zeroed by the caller) has grown by the
+// wave's count of key k. Keys >= K are skipped; all of them must equal K and
+// K < 2^nbits.
+template <int CH>
+__device__ __forceinline__ void wave_rank(const uint32_t (&key)[CH], uint32_t K, int nbits,
+                                          uint16_t *cnt, uint32_t (&rank)[CH]) {
+  const uint64_t lt = lanemask_lt();
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    const uint32_t k = key[c];
+    const uint64_t pm = match_any_bits(k, nbits);
+    const uint32_t lr = (uint32_t)__popcll(pm & lt);
+    uint32_t r = 0;
+    if (k < K) {
+      const uint32_t c0 = cnt[k];
+      r = c0 + lr;
+      if (lr == 0) cnt[k] = (uint16_t)(c0 + (uint32_t)__popcll(pm));
+    }
+    rank[c] = r;
+  }
+}
+
+// After wave_rank over a 4-wave block: turn the per-wave counters cnt[w*K+n]
+// into the count of key n in earlier waves, and write the block totals to
+// total[n] (if given). Call from all threads; ends with a barrier.
+__device__ __forceinline__ void block_rank_bases(uint16_t *cnt, uint32_t K, uint32_t *total) {
+  __syncthreads();
+  for (uint32_t n = threadIdx.x; n < K; n += blockDim.x) {
+    const uint32_t a = cnt[n], b = cnt[K + n], c = cnt[2 * K + n], d = cnt[3 * K + n];
+    cnt[n] = 0;
+    cnt[K + n] = (uint16_t)a;
+    cnt[2 * K + n] = (uint16_t)(a + b);
+    cnt[3 * K + n] = (uint16_t)(a + b + c);
+    if (total) total[n] = a + b + c + d;
+  }
+  __syncthreads();
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_incl_scan_add(T x) {
   const int l = lane_id();

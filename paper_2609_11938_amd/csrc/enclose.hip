@@ -1,28 +1,41 @@
-// Enclosure (Alg. 2) in one pass over the timeline, emitting the operator
-// runs that the aggregation reduces.
+// Enclosure (Alg. 2) and the first level of the aggregation (Eq. 1) in one
+// pass over the launches, in storage order.
 //
-// Each block takes 256 consecutive launches. The range starts that can matter
-// for the block's main stream (those between the block's smallest and largest
-// query point) are staged in LDS; the two bounds are found by 64-ary searches
-// in which every lane of a wave probes one sample. A launch's innermost range
-// is the last range starting at or before its query point, lifted along the
-// parent chain while that range ends before the query point.
+// A block takes 2048 consecutive launches, eight consecutive ones per thread.
+// Enclosure: the range starts that can matter for the block's main stream
+// (between its smallest and largest query point) are staged in LDS; the two
+// bounds come from 64-ary searches in which every lane of a wave probes one
+// sample. A launch's innermost range is the last range starting at or before
+// its query point, lifted along the parent chain while that range ends before
+// the query point.
 //
-// For the aggregation the block then cuts its launches into runs of equal
-// operator row (consecutive launches of one range are one run) and writes one
-// (row, first launch, length) record per run into its own slot area; no
-// accumulation happens here.
+// Aggregation: each wave cuts its 512 launches into runs of one operator row.
+// With at most kRowCap runs the wave reduces them in place -- every thread
+// accumulates its launches in registers, a segmented scan over the lanes
+// carries runs across threads -- and writes one partial row per run. With
+// more runs it writes references (row, first launch, length <= 16) that the
+// per-row reduction resolves later. Partial rows and references land in
+// launch order at offsets found by a decoupled look-back over the blocks,
+// which take their positions from a counter in the order they start.
+#include "accum.h"
 #include "common.h"
 #include "impl.h"
 
 namespace opa {
 
+constexpr int kPer = 8;                         // launches per thread
+constexpr int kSpan = kEncThreads * kPer;       // launches per block
+constexpr int kRowCap = 32;                     // runs a wave reduces in place
+constexpr unsigned long long kLbAgg = 1ull << 62, kLbInc = 2ull << 62;
+constexpr long kLbSpinLimit = 1l << 26;
+
+static_assert(kSpan == kEncSpan, "block span");
+static_assert(kEncRowsPerWave == kRowCap, "row cap");
+
 struct EncParams {
   int64_t T;
   const uint64_t *q;  // query_ns or start_ns
   const uint16_t *stream;
-  const int32_t *match;
-  int64_t P;
   CoreRanges cr;
   const int64_t *rblk;
   const int64_t *ree;
@@ -31,7 +44,8 @@ struct EncParams {
   int64_t R_in;           // aggregate-only: input ranges
   const uint32_t *op_in;  // aggregate-only: op ids by input range index
   int32_t *range_id;
-  RunSlots runs;
+  AggIn ag;
+  EmitOut em;
   opattr_diag *diag;
 };
 
@@ -66,60 +80,151 @@ __device__ __forceinline__ int64_t thread_upper_bound(const uint64_t *a, int64_t
   return lo;
 }
 
+// kPer consecutive elements from p[i..), 16-byte vector loads when aligned
+template <typename T>
+__device__ __forceinline__ void load_run(const T *p, int64_t i, int nv, T (&o)[kPer]) {
+  static_assert(sizeof(T) * kPer % 16 == 0, "vector width");
+  if (nv == kPer && (reinterpret_cast<uintptr_t>(p + i) & 15) == 0) {
+    const uint4 *v = reinterpret_cast<const uint4 *>(p + i);
+#pragma unroll
+    for (int q = 0; q < (int)(sizeof(T) * kPer / 16); ++q) {
+      const uint4 t = v[q];
+      memcpy(reinterpret_cast<char *>(o) + 16 * q, &t, 16);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) o[k] = k < nv ? p[i + k] : T(0);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store_run(T *p, int64_t i, int nv, const T (&o)[kPer]) {
+  if (nv == kPer && (reinterpret_cast<uintptr_t>(p + i) & 15) == 0) {
+    uint4 *v = reinterpret_cast<uint4 *>(p + i);
+#pragma unroll
+    for (int q = 0; q < (int)(sizeof(T) * kPer / 16); ++q) {
+      uint4 t;
+      memcpy(&t, reinterpret_cast<const char *>(o) + 16 * q, 16);
+      v[q] = t;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < kPer; ++k)
+      if (k < nv) p[i + k] = o[k];
+  }
+}
+
+__device__ __forceinline__ unsigned long long lb_load(const unsigned long long *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void lb_store(unsigned long long *p, unsigned long long v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// state word: flag (2 bits) | items (31 bits) | rows (31 bits)
+__device__ __forceinline__ unsigned long long lb_pack(unsigned long long flag, uint32_t items,
+                                                      uint32_t rows) {
+  return flag | ((unsigned long long)items << 31) | rows;
+}
+
+// Exclusive prefix of (items, rows) over the blocks before bid; one wave.
+// Returns false if the wait bound ran out (reported as a limit error).
+__device__ inline bool lookback(const unsigned long long *state, int64_t bid, uint32_t &items,
+                                uint32_t &rows) {
+  const int ln = lane_id();
+  unsigned long long si = 0, sr = 0;
+  int64_t j = bid - 1;
+  long spins = 0;
+  while (j >= 0) {
+    const int64_t idx = j - ln;
+    unsigned long long st = idx >= 0 ? lb_load(state + idx) : kLbInc;
+    unsigned long long flag = st & (3ull << 62);
+    const unsigned long long inc = __ballot(flag == kLbInc);
+    // lanes up to and including the nearest inclusive predecessor matter
+    const int last = inc ? __ffsll(inc) - 1 : OPA_WAVE - 1;
+    const unsigned long long need = last == 63 ? ~0ull : ((2ull << last) - 1);
+    if (__ballot(flag == 0) & need) {
+      if (++spins > kLbSpinLimit) return false;
+      __builtin_amdgcn_s_sleep(1);
+      continue;
+    }
+    unsigned long long ci = ln <= last ? ((st >> 31) & 0x7FFFFFFFull) : 0;
+    unsigned long long cr = ln <= last ? (st & 0x7FFFFFFFull) : 0;
+    si += wave_reduce_add(ci);
+    sr += wave_reduce_add(cr);
+    if (inc) break;
+    j -= OPA_WAVE;
+  }
+  items = (uint32_t)si;
+  rows = (uint32_t)sr;
+  return true;
+}
+
 template <int MODE>
 __global__ void __launch_bounds__(kEncThreads) k_enc(EncParams a) {
   __shared__ uint64_t sS[kEncWindow];
   __shared__ uint64_t red[2][kEncThreads / OPA_WAVE];
   __shared__ int64_t win[3];
-  __shared__ uint32_t sg[kEncThreads];
-  __shared__ uint32_t rstart[kEncThreads];
-  __shared__ uint32_t sh[8];
-  __shared__ uint32_t sbad;
-  const int tid = threadIdx.x;
-  const int64_t i0 = (int64_t)blockIdx.x * kEncThreads;
-  const int64_t i = i0 + tid;
-  const bool valid = i < a.T;
-  if (tid == 0) sbad = 0;
+  __shared__ uint32_t wcnt[2][kEncThreads / OPA_WAVE];
+  __shared__ uint32_t spre[2];
+  __shared__ uint32_t sbid, sbad, sfail;
+  const int tid = threadIdx.x, w = wave_id(), ln = lane_id();
+  if (tid == 0) {
+    sbad = 0;
+    sfail = 0;
+    if (MODE & 2) sbid = atomicAdd(a.em.ctr, 1u);
+  }
+  __syncthreads();
+  const int64_t bid = (MODE & 2) ? (int64_t)sbid : (int64_t)blockIdx.x;
+  const int64_t i0 = bid * kSpan;
+  const int64_t ib = i0 + (int64_t)tid * kPer;
+  const int nv = (int)(a.T - ib < 0 ? 0 : (a.T - ib < kPer ? a.T - ib : kPer));
   uint32_t bad = 0;
-  uint32_t g = a.NOPS;
+  uint32_t g[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) g[k] = k < nv ? a.NOPS : 0xFFFFFFFFu;
 
   if (MODE & 1) {
-    const uint16_t st = valid ? a.stream[i] : (uint16_t)0xFFFF;
-    const uint64_t q = valid ? a.q[i] : 0;
+    uint16_t st[kPer];
+    uint64_t q[kPer];
+    load_run(a.stream, ib, nv, st);
+    load_run(a.q, ib, nv, q);
     const uint16_t s0 = a.stream[i0];
-    const bool in0 = valid && st == s0 && s0 < a.NS;
     // smallest and largest query point of the block's main stream
-    uint64_t mn = in0 ? q : ~0ull, mx = in0 ? q : 0ull;
+    uint64_t mn = ~0ull, mx = 0ull;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k)
+      if (k < nv && st[k] == s0) {
+        mn = q[k] < mn ? q[k] : mn;
+        mx = q[k] > mx ? q[k] : mx;
+      }
     for (int o = OPA_WAVE / 2; o > 0; o >>= 1) {
       const uint64_t y = __shfl_xor(mn, o, OPA_WAVE), z = __shfl_xor(mx, o, OPA_WAVE);
       mn = y < mn ? y : mn;
       mx = z > mx ? z : mx;
     }
-    if (lane_id() == 0) {
-      red[0][wave_id()] = mn;
-      red[1][wave_id()] = mx;
+    if (ln == 0) {
+      red[0][w] = mn;
+      red[1][w] = mx;
     }
     __syncthreads();
-    if (wave_id() == 0) {
+    if (w == 0) {
       uint64_t qa = ~0ull, qb = 0;
       for (int k = 0; k < kEncThreads / OPA_WAVE; ++k) {
         qa = red[0][k] < qa ? red[0][k] : qa;
         qb = red[1][k] > qb ? red[1][k] : qb;
       }
-      int64_t wlo = 0, wn = 0, lo = 0;
+      int64_t wlo = 0, wn = 0;
       if (s0 < a.NS && qa <= qb) {
-        lo = a.rblk[s0];
-        const int64_t hi = a.rblk[s0 + 1];
+        const int64_t lo = a.rblk[s0], hi = a.rblk[s0 + 1];
         const int64_t pa = wave_upper_bound(a.cr.s, lo, hi, qa) - 1;
         const int64_t pb = wave_upper_bound(a.cr.s, lo, hi, qb) - 1;
         wlo = pa > lo ? pa : lo;
         wn = pb - wlo + 1;
         if (wn < 0) wn = 0;
       }
-      if (lane_id() == 0) {
+      if (ln == 0) {
         win[0] = wlo;
         win[1] = wn;
-        win[2] = lo;
       }
     }
     __syncthreads();
@@ -129,70 +234,193 @@ __global__ void __launch_bounds__(kEncThreads) k_enc(EncParams a) {
       for (int k = tid; k < wn; k += kEncThreads) sS[k] = a.cr.s[wlo + k];
     __syncthreads();
 
-    int32_t rid = -1;
-    if (valid && st < a.NS && q < (1ull << 63)) {
-      const int64_t lo = a.rblk[st], hi = a.rblk[st + 1];
-      int64_t p;
-      if (in0 && wn == 0) {
-        p = lo - 1;  // no range of the stream starts at or before the block's queries
-      } else if (in0 && staged) {
-        int l2 = 0, h2 = (int)wn;
-        while (l2 < h2) {
-          const int mid = (l2 + h2) >> 1;
-          if (sS[mid] <= q) l2 = mid + 1;
-          else h2 = mid;
+    int32_t rout[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      int32_t rid = -1;
+      if (k < nv && st[k] < a.NS && q[k] < (1ull << 63)) {
+        const int64_t lo = a.rblk[st[k]], hi = a.rblk[st[k] + 1];
+        const bool in0 = st[k] == s0;
+        int64_t p;
+        if (in0 && wn == 0) {
+          p = lo - 1;  // no range of the stream starts at or before the block's queries
+        } else if (in0 && staged) {
+          int l2 = 0, h2 = (int)wn;
+          while (l2 < h2) {
+            const int mid = (l2 + h2) >> 1;
+            if (sS[mid] <= q[k]) l2 = mid + 1;
+            else h2 = mid;
+          }
+          p = wlo + l2 - 1;
+          if (p < lo) p = lo - 1;
+        } else {
+          p = thread_upper_bound(a.cr.s, lo, hi, q[k]) - 1;
         }
-        p = wlo + l2 - 1;
-        if (p < lo) p = lo - 1;
-      } else {
-        p = thread_upper_bound(a.cr.s, lo, hi, q) - 1;
+        int64_t j = p;
+        int steps = 0;
+        while (j >= lo && a.ree[j] < (int64_t)q[k] && steps < kMaxWalk) {
+          j = a.npg[j];
+          ++steps;
+        }
+        if (j >= lo && a.ree[j] >= (int64_t)q[k]) rid = (int32_t)j;
+      } else if (k < nv && st[k] >= a.NS) {
+        bad++;
       }
-      int64_t j = p;
-      int steps = 0;
-      while (j >= lo && a.ree[j] < (int64_t)q && steps < kMaxWalk) {
-        j = a.npg[j];
-        ++steps;
-      }
-      if (j >= lo && a.ree[j] >= (int64_t)q) rid = (int32_t)j;
-    } else if (valid && st >= a.NS) {
-      bad++;
+      rout[k] = rid >= 0 ? (a.cr.perm ? a.cr.perm[rid] : rid) : -1;
+      if (rid >= 0) g[k] = a.cr.op[rid];
     }
-    if (valid) a.range_id[i] = rid >= 0 ? (a.cr.perm ? a.cr.perm[rid] : rid) : -1;
-    if (rid >= 0) g = a.cr.op[rid];
-  } else if (valid) {
-    const int32_t r = a.range_id[i];
-    if (r >= 0 && r < a.R_in && a.op_in[r] < a.NOPS) g = a.op_in[r];
-    else if (r < -1 || r >= a.R_in || r >= 0) bad++;
+    store_run(a.range_id, ib, nv, rout);
+  } else {
+    int32_t rin[kPer];
+    load_run(a.range_id, ib, nv, rin);
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      if (k >= nv) continue;
+      const int32_t r = rin[k];
+      if (r >= 0 && r < a.R_in && a.op_in[r] < a.NOPS) g[k] = a.op_in[r];
+      else if (r < -1 || r >= a.R_in || r >= 0) bad++;
+    }
   }
 
   if (MODE & 2) {
-    // runs of equal operator row among the block's launches, in launch order
-    if (valid) {
-      const int32_t m = a.match[i];
-      if (m < -1 || m >= a.P) bad++;  // such a launch aggregates as unmatched
+    const AggIn &in = a.ag;
+    // ---- runs of one operator row inside the wave, in launch order
+    const uint32_t gl = __shfl_up(g[kPer - 1], 1, OPA_WAVE);
+    uint32_t hm = 0;  // bit k: launch k starts a run
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const uint32_t prev = k ? g[k - 1] : (ln ? gl : 0xFFFFFFFFu);
+      if (k < nv && g[k] != prev) hm |= 1u << k;
     }
-    sg[tid] = valid ? g : 0xFFFFFFFFu;
-    __syncthreads();
-    const bool head = valid && (tid == 0 || sg[tid - 1] != g);
-    uint32_t nr;
-    const uint32_t r = block_excl_scan_add<uint32_t>(head ? 1u : 0u, sh, &nr);
-    if (head) rstart[r] = (uint32_t)tid;
-    __syncthreads();
-    const bool tail = valid && (tid == kEncThreads - 1 || sg[tid + 1] != g);
-    if (tail) {
-      const uint32_t rr = r + (head ? 1u : 0u) - 1u;  // this launch's run
-      const uint32_t s0 = rstart[rr];
-      const int64_t slot = (int64_t)blockIdx.x * kEncThreads + rr;
-      a.runs.g[slot] = g;
-      a.runs.kb[slot] = (uint32_t)(i0 + s0);
-      a.runs.len[slot] = (uint32_t)(tid - s0 + 1);
+    // pieces for references: runs cut at every 16th launch as well
+    const uint32_t hp = hm | ((nv > 0 && (ln & 1) == 0) ? 1u : 0u);
+    const uint32_t nh = __popc(hm), nhp = __popc(hp);
+    const uint32_t hb = wave_incl_scan_add(nh) - nh;
+    const uint32_t hpb = wave_incl_scan_add(nhp) - nhp;
+    const uint32_t nr_w = __shfl(hb + nh, OPA_WAVE - 1, OPA_WAVE);
+    const uint32_t np_w = __shfl(hpb + nhp, OPA_WAVE - 1, OPA_WAVE);
+    const bool rowmode = nr_w <= (uint32_t)kRowCap;
+    if (ln == 0) {
+      wcnt[0][w] = rowmode ? nr_w : np_w;
+      wcnt[1][w] = rowmode ? nr_w : 0u;
     }
-    if (tid == 0) a.runs.nruns[blockIdx.x] = nr;
+    int32_t mt[kPer];
+    uint32_t du[kPer];
+    load_run(in.match, ib, nv, mt);
+    load_run(in.dur, ib, nv, du);
+#pragma unroll
+    for (int k = 0; k < kPer; ++k)
+      if (k < nv && (mt[k] < -1 || (int64_t)mt[k] >= in.P)) bad++;  // aggregates as unmatched
+    __syncthreads();
+    uint32_t bi = 0, br = 0, wi = 0, wr = 0;
+    for (int k = 0; k < kEncThreads / OPA_WAVE; ++k) {
+      if (k < w) {
+        wi += wcnt[0][k];
+        wr += wcnt[1][k];
+      }
+      bi += wcnt[0][k];
+      br += wcnt[1][k];
+    }
+    if (tid == 0) lb_store(a.em.state + bid, lb_pack(bid == 0 ? kLbInc : kLbAgg, bi, br));
+
+    // ---- in-place reduction (row mode): suffix of each thread, then a
+    // segmented scan over the lanes (a lane with a run start begins a segment)
+    Acc inc;
+    acc_zero(inc);
+    if (rowmode) {
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        if (k >= nv) continue;
+        if (k > 0 && ((hm >> k) & 1u)) acc_zero(inc);
+        acc_launch(inc, in, mt[k], du[k]);
+      }
+      const unsigned long long hl = __ballot(hm != 0) | 1ull;
+      const unsigned long long upto = ln == 63 ? ~0ull : ((2ull << ln) - 1);
+      const int sl = 63 - __clzll(hl & upto);
+#pragma unroll
+      for (int o = 1; o < OPA_WAVE; o <<= 1) {
+        const Acc y = acc_shfl_up(inc, o);
+        if (ln - o >= sl) {
+          Acc t = y;
+          acc_merge(t, inc, in.maxmask);
+          inc = t;
+        }
+      }
+    }
+
+    // ---- block offsets
+    if (w == 0) {
+      uint32_t pi = 0, pr = 0;
+      bool ok = true;
+      if (bid > 0) ok = lookback(a.em.state, bid, pi, pr);
+      if (ln == 0) {
+        if (bid > 0) lb_store(a.em.state + bid, lb_pack(kLbInc, pi + bi, pr + br));
+        spre[0] = pi;
+        spre[1] = pr;
+        if (!ok) sfail = 1;
+        if (bid == a.em.nblocks - 1) {
+          a.em.meta[0] = (int64_t)pi + bi;
+          a.em.meta[1] = (int64_t)pr + br;
+        }
+      }
+    }
+    __syncthreads();
+    const uint32_t ibase = spre[0] + wi, rbase = spre[1] + wr;
+
+    if (rowmode) {
+      const uint32_t nvn = __shfl_down((uint32_t)nv, 1, OPA_WAVE);
+      const uint32_t h0n = __shfl_down(hm & 1u, 1, OPA_WAVE);
+      // the run that enters this lane (for lanes whose first launch continues it)
+      Acc run = acc_shfl_up(inc, 1);
+      if ((hm & 1u) || ln == 0) acc_zero(run);
+      if (hm & 0xFEu) {
+        // runs that end inside the lane: recompute its launches before the
+        // last run start, emitting at every start
+        const int last = 31 - __clz(hm);
+        for (int k = 0; k < kPer; ++k) {
+          if (k > last) break;
+          if (k > 0 && ((hm >> k) & 1u)) {
+            const uint32_t idx = hb + __popc(hm & ((1u << k) - 1u)) - 1u;
+            acc_store(a.em.rows + rbase + idx, run, g[k - 1]);
+            a.em.ig[ibase + idx] = g[k - 1];
+            a.em.ia[ibase + idx] = rbase + idx;
+            a.em.ib[ibase + idx] = 0;
+            acc_zero(run);
+          }
+          if (k < last) acc_launch(run, in, mt[k], du[k]);
+        }
+      }
+      // the run through the lane's last launch ends here when the next lane
+      // starts a run or has no launches
+      if (nv > 0 && (ln == OPA_WAVE - 1 || nvn == 0 || h0n)) {
+        const uint32_t idx = hb + nh - 1u;
+        acc_store(a.em.rows + rbase + idx, inc, g[nv - 1]);
+        a.em.ig[ibase + idx] = g[nv - 1];
+        a.em.ia[ibase + idx] = rbase + idx;
+        a.em.ib[ibase + idx] = 0;
+      }
+    } else {
+      // references: every piece start writes (row, first launch, length)
+      const uint32_t hpn = __shfl_down(hp, 1, OPA_WAVE);
+      const uint32_t nvn = __shfl_down((uint32_t)nv, 1, OPA_WAVE);
+      const uint32_t spill = ln < OPA_WAVE - 1 ? (hpn ? (uint32_t)__ffs(hpn) - 1u : nvn) : 0u;
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        if (!((hp >> k) & 1u)) continue;
+        const uint32_t rest = hp >> (k + 1);
+        const uint32_t len = rest ? (uint32_t)__ffs(rest) : (uint32_t)(nv - k) + spill;
+        const uint32_t idx = hpb + __popc(hp & ((1u << k) - 1u));
+        a.em.ig[ibase + idx] = g[k];
+        a.em.ia[ibase + idx] = (uint32_t)(ib + k);
+        a.em.ib[ibase + idx] = len;
+      }
+    }
   }
   if (bad) atomicAdd(&sbad, bad);
   __syncthreads();
   if (tid == 0 && sbad)
     atomicAdd((unsigned long long *)&a.diag->bad_records, (unsigned long long)sbad);
+  if (tid == 0 && sfail) atomicOr(&a.diag->flags, OPATTR_F_LIMIT);
 }
 
 void run_enclose_aggregate(const EncArgs &x, hipStream_t s) {
@@ -202,8 +430,6 @@ void run_enclose_aggregate(const EncArgs &x, hipStream_t s) {
   a.T = pl.T;
   a.q = k->query_ns ? k->query_ns : k->start_ns;
   a.stream = k->stream_id;
-  a.match = x.match;
-  a.P = x.p ? x.p->n : 0;
   a.NS = x.d->n_streams;
   a.NOPS = x.d->n_ops;
   a.range_id = x.range_id;
@@ -212,10 +438,15 @@ void run_enclose_aggregate(const EncArgs &x, hipStream_t s) {
   a.rblk = at<int64_t>(x.ws, pl.rblk);
   a.ree = at<int64_t>(x.ws, pl.ree);
   a.npg = at<int32_t>(x.ws, pl.npg);
-  a.runs = run_slots(x.ws, pl);
   if (x.mode == kAggregateOnly) {
     a.R_in = x.r ? x.r->n : 0;
     a.op_in = x.r ? x.r->op_id : nullptr;
+  }
+  if (x.mode & 2) {
+    a.ag = agg_inputs(x);
+    a.em = emit_out(x.ws, pl);
+    // look-back states and the start counter, cleared by a kernel (graph-safe)
+    fill_u32(reinterpret_cast<uint32_t *>(a.em.state), 0, 2 * (pl.nencb + 1), s);
   }
   const unsigned nb = (unsigned)pl.nencb;
   probe_begin(OPATTR_PROBE_MAIN_PASS, s);

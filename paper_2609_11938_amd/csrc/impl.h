@@ -10,20 +10,17 @@ namespace opa {
 
 constexpr int kRangeTile = 1024;    // ranges per local-NPG tile
 constexpr int kColChunk = 64;       // rows per chunk of the column scans
-constexpr int kEncThreads = 256;    // kernels per enclose/aggregate block
-constexpr int kEncWindow = 1024;    // range starts staged in LDS per block
+constexpr int kEncThreads = 256;    // threads per enclose/aggregate block
+constexpr int kEncSpan = 2048;      // launches per enclose/aggregate block
+constexpr int kEncRowsPerWave = 32; // runs a wave of that block reduces in place
+constexpr int kEncWindow = 2048;    // range starts staged in LDS per block
+// Key counts ranked with per-wave LDS counters (8 bytes of LDS per key); the
+// seq-tile kernels also hold a 16 KB partition array, hence a lower limit.
+constexpr uint32_t kFastKeys = 6144;
+constexpr uint32_t kFastNames = 4096;
 constexpr int kMaxWalk = 300;       // bound on parent-chain walks (depth <= 255)
 constexpr uint32_t kMaxNames = (1u << 20) - 1;  // names and rows are packed above a 12-bit slot
 constexpr uint32_t kMaxOps = (1u << 20) - 2;    // rows = n_ops + 1
-
-// Partial row of the aggregation (device scratch), one per reduction item.
-struct AccRow {
-  unsigned long long kc, tns, mc, mns;
-  double sum[OPATTR_NUM_COUNTERS];
-  uint32_t maxk[OPATTR_NUM_COUNTERS];  // order-preserving key of the fp32 max
-  uint32_t nanmask;                    // bit c: a NaN reached a MAX counter
-  uint32_t pad;
-};
 
 // Byte offsets of every scratch array inside the caller's workspace.
 struct Plan {
@@ -35,13 +32,13 @@ struct Plan {
   // IOM
   size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist;
   size_t tlh, pfh, tlch, pfch, tlc, pfc, off, slot;
-  size_t pfirst, plast, pcnt, contig, mbs, nbs;
+  size_t pfirst, plast, contig, mbs, nbs;
   // ranges
   size_t rperm, rs_c, re_c, rst_c, rop_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
   // aggregation
-  size_t slot_g, slot_kb, slot_len, nruns, roff, cg, ckb, clen, meta;
-  size_t rth, rtch, gcnt, goff, ioff, skb, slen, part;
+  int64_t cap_items, cap_rows, max_chunks;
+  size_t lbs, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, coff, cmap, sidx, part;
   size_t misc;  // small device scalars
 };
 
@@ -98,6 +95,9 @@ void column_scan(uint32_t *tab, int64_t rows, uint32_t cols, uint32_t *chs, uint
 bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, int64_t n,
                       int begin_bit, int end_bit, uint32_t *hist, hipStream_t s);
 size_t radix_hist_entries(int64_t n);
+// Fill kernels (used instead of memset nodes, which misbehave under graph replay).
+void fill_u32(uint32_t *p, uint32_t v, int64_t n, hipStream_t s);
+void fill_u8(uint8_t *p, uint8_t v, int64_t n, hipStream_t s);
 void launch_iota(uint32_t *v, int64_t n, hipStream_t s);
 void launch_gather_key_u64(const uint64_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
                            bool invert, hipStream_t s);
@@ -132,13 +132,18 @@ CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws
 void resolve_ranges(const CoreRanges &cr, const opattr_dims *d, void *ws, const Plan &pl,
                     uint8_t *range_depth, opattr_diag *diag, hipStream_t s);
 
-// Per enclosure block: runs of consecutive launches sharing an operator row.
-struct RunSlots {
-  uint32_t *g, *kb, *len;  // [block * 256 + r]
-  uint32_t *nruns;         // [block]
+struct PartRow;
+struct AggIn;
+// Items left by the enclosure pass for the aggregation (see agg.hip).
+struct EmitOut {
+  unsigned long long *state;  // [blocks] look-back states
+  uint32_t *ctr;              // block start counter
+  uint32_t *ig, *ia, *ib;     // item: row, partial-row index or first launch, 0 or length
+  PartRow *rows;
+  int64_t *meta;
+  int64_t nblocks;
 };
-RunSlots run_slots(void *ws, const Plan &pl);
-int64_t max_agg_items(int64_t T, uint32_t G);
+EmitOut emit_out(void *ws, const Plan &pl);
 
 enum EncMode { kEncloseOnly = 1, kAggregateOnly = 2, kEncloseAggregate = 3 };
 struct EncArgs {
@@ -157,6 +162,7 @@ struct EncArgs {
   void *ws;
   const Plan *pl;
 };
+AggIn agg_inputs(const EncArgs &x);
 void run_enclose_aggregate(const EncArgs &a, hipStream_t s);
 void run_aggregate(const EncArgs &a, hipStream_t s);
 

@@ -54,7 +54,7 @@ void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, con
   const unsigned nb = (unsigned)((T + 255) / 256);
   probe_begin(OPATTR_PROBE_SEQ_VIEW, s);
   if (pl.seq_dense) {
-    note(hipMemsetAsync(sv, 0xFF, (size_t)T * 4, s));
+    fill_u32(reinterpret_cast<uint32_t *>(sv), 0xFFFFFFFFu, T, s);
     k_seqview_dense<<<nb, 256, 0, s>>>(k->seq, T, sv, diag, validate ? 1 : 0);
     probe_end(OPATTR_PROBE_SEQ_VIEW, s);
     return;
@@ -115,50 +115,134 @@ __device__ inline uint32_t tl_tile_keys(const TlArgs &a, int64_t base, uint32_t 
   return bad;
 }
 
-// Partition statistics over one seq tile: for every run of equal partition id
-// (launch order), fold its first rank, last rank and length into the
-// per-partition min / max / count.
-__device__ inline void part_runs(const int32_t *lpart, int64_t base, uint32_t *pfirst,
-                                 uint32_t *plast, uint32_t *pcnt, int32_t *sh) {
-  const int tid = threadIdx.x;
-  int32_t carry = -1;
-  for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
-    const int l = c * OPA_TILE_THREADS + tid;
-    const int32_t lp = lpart[l];
-    const bool head = lp >= 0 && (l == 0 || lpart[l - 1] != lp);
-    int32_t st = block_incl_scan_max<int32_t>(head ? l : -1, sh);
-    st = st > carry ? st : carry;
-    const bool tail = lp >= 0 && (l == OPA_TILE - 1 || lpart[l + 1] != lp);
-    if (tail) {
-      atomicMin(&pfirst[lp], (uint32_t)(base + st));
-      atomicMax(&plast[lp], (uint32_t)(base + l));
-      atomicAdd(&pcnt[lp], (uint32_t)(l - st + 1));
-    }
-    // the chunk's last thread publishes the running head for the next chunk
-    if (tid == OPA_TILE_THREADS - 1) sh[8] = st;
-    __syncthreads();
-    carry = sh[8];
-    __syncthreads();
-  }
-}
-
-__global__ void __launch_bounds__(256) k_tl_hist(TlArgs a, uint32_t *tlh, uint32_t *pfirst,
-                                                 uint32_t *plast, uint32_t *pcnt,
-                                                 opattr_diag *diag, int want_parts) {
+__global__ void __launch_bounds__(256) k_tl_hist(TlArgs a, uint32_t *tlh, opattr_diag *diag) {
   __shared__ TileSmem sm;
   const int64_t tile = blockIdx.x;
   const int64_t base = tile * OPA_TILE;
   if (threadIdx.x == 0) sm.bad = 0;
   __syncthreads();
-  int32_t *lpart = reinterpret_cast<int32_t *>(sm.B);
-  const uint32_t bad = tl_tile_keys(a, base, sm.A, want_parts ? lpart : nullptr, nullptr);
+  const uint32_t bad = tl_tile_keys(a, base, sm.A, nullptr, nullptr);
   if (bad) atomicAdd(&sm.bad, bad);
   __syncthreads();
-  if (want_parts) part_runs(lpart, base, pfirst, plast, pcnt, sm.sh);
   if (threadIdx.x == 0 && sm.bad)
     atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)sm.bad);
   tile_radix_sort(sm.A, sm.B, sm.srt, OPA_SLOT_BITS, bits_for(a.NN));
   write_hist_row(sm.A, a.NN, tlh + tile * a.NN);
+}
+
+// ---------------------------------------------------------------------------
+// Fast path for up to kFastKeys names: a tile of 4096 launches is owned by
+// four waves, each walking 16 chunks of 64 in seq order and ranking names
+// with its own LDS counters (wave_rank), so no in-LDS sort is needed.
+// Element e of a tile sits in wave e / 1024, chunk (e / 64) % 16, lane e % 64.
+// ---------------------------------------------------------------------------
+constexpr int kWaveChunks = OPA_TILE / OPA_TILE_THREADS;  // 16 chunks per wave
+
+__device__ __forceinline__ int tile_elem(int c) {
+  return wave_id() * (OPA_TILE / 4) + c * OPA_WAVE + lane_id();
+}
+
+// One launch of seq rank x: input index j (-1 for holes), ranking key (its
+// name if eligible for replay, else NN) and partition (-1 none, -2 hole or
+// bad id). Returns 1 if an id is out of range.
+__device__ __forceinline__ uint32_t tl_load(const TlArgs &a, int64_t x, uint32_t &key, int32_t &j,
+                                            int32_t &lp) {
+  j = (x >= 0 && x < a.T) ? a.sv[x] : -1;
+  key = a.NN;
+  lp = -2;
+  if (j < 0) return 0;
+  const uint32_t nm = a.name[j];
+  const int32_t pt = a.part ? a.part[j] : -1;
+  if (nm >= a.NN || pt < -1 || (pt >= 0 && (uint32_t)pt >= a.NP)) return 1;
+  if (pt < 0 || a.part_rep[pt] == pt) key = nm;
+  lp = pt;
+  return 0;
+}
+
+// Partition edges of a seq tile. A head (first launch of a maximal run of one
+// partition in seq order) stores its rank in pfirst, a tail in plast. With
+// verify set, heads and tails instead compare against what is stored: a
+// partition with two runs has two heads, only one of which can be stored, so
+// the other one marks it non-contiguous.
+__device__ inline uint32_t part_edges(const TlArgs &a, const int32_t *lpart, int64_t base,
+                                      uint32_t *pfirst, uint32_t *plast, uint8_t *contig,
+                                      bool verify) {
+  uint32_t nbad = 0;
+  for (int e = threadIdx.x; e < OPA_TILE; e += OPA_TILE_THREADS) {
+    const int32_t lp = lpart[e];
+    if (lp < 0) continue;
+    const int64_t x = base + e;
+    int32_t prev, next, jj;
+    uint32_t kk;
+    if (e > 0) prev = lpart[e - 1];
+    else tl_load(a, x - 1, kk, jj, prev);
+    if (e < OPA_TILE - 1) next = lpart[e + 1];
+    else tl_load(a, x + 1, kk, jj, next);
+    if (!verify) {
+      if (prev != lp) pfirst[lp] = (uint32_t)x;
+      if (next != lp) plast[lp] = (uint32_t)x;
+    } else {
+      const bool bad = (prev != lp && pfirst[lp] != (uint32_t)x) ||
+                       (next != lp && plast[lp] != (uint32_t)x);
+      if (bad) {
+        contig[lp] = 0;
+        nbad++;
+      }
+    }
+  }
+  return nbad;
+}
+
+#define OPA_DYN_LDS(T, name) extern __shared__ __align__(16) unsigned char name##_raw[]; \
+  T *name = reinterpret_cast<T *>(name##_raw)
+
+// Partition edges of every seq tile on their own (store, or verify).
+__global__ void __launch_bounds__(256) k_part_edges(TlArgs a, uint32_t *pfirst, uint32_t *plast,
+                                                    uint8_t *contig, opattr_diag *diag,
+                                                    int verify) {
+  __shared__ int32_t lpart[OPA_TILE];
+  __shared__ uint32_t snc;
+  const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
+  if (threadIdx.x == 0) snc = 0;
+  for (int e = threadIdx.x; e < OPA_TILE; e += OPA_TILE_THREADS) {
+    uint32_t k;
+    int32_t j, lp;
+    tl_load(a, base + e, k, j, lp);
+    lpart[e] = lp;
+  }
+  __syncthreads();
+  const uint32_t nb = part_edges(a, lpart, base, pfirst, plast, contig, verify != 0);
+  if (nb) atomicAdd(&snc, nb);
+  __syncthreads();
+  if (threadIdx.x == 0 && snc) atomicOr(&diag->flags, OPATTR_F_PARTITION);
+}
+
+__global__ void __launch_bounds__(256) k_tl_hist_w(TlArgs a, uint32_t *tlh, uint32_t *pfirst,
+                                                   uint32_t *plast, opattr_diag *diag,
+                                                   int want_parts) {
+  OPA_DYN_LDS(uint16_t, cnt);
+  __shared__ int32_t lpart[OPA_TILE];
+  __shared__ uint32_t sbad;
+  const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
+  const uint32_t NN = a.NN;
+  for (uint32_t i = threadIdx.x; i < 4 * NN; i += OPA_TILE_THREADS) cnt[i] = 0;
+  if (threadIdx.x == 0) sbad = 0;
+  __syncthreads();
+  uint32_t key[kWaveChunks], rank[kWaveChunks], bad = 0;
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const int e = tile_elem(c);
+    int32_t j, lp;
+    bad += tl_load(a, base + e, key[c], j, lp);
+    lpart[e] = lp;
+  }
+  wave_rank<kWaveChunks>(key, NN, bits_for(NN), cnt + wave_id() * NN, rank);
+  block_rank_bases(cnt, NN, tlh + tile * NN);
+  if (want_parts) part_edges(a, lpart, base, pfirst, plast, nullptr, false);
+  if (bad) atomicAdd(&sbad, bad);
+  __syncthreads();
+  if (threadIdx.x == 0 && sbad)
+    atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)sbad);
 }
 
 struct PfArgs {
@@ -361,6 +445,69 @@ __global__ void __launch_bounds__(256) k_pf_slot(PfArgs a, const uint32_t *__res
   }
 }
 
+__global__ void __launch_bounds__(256) k_pf_hist_w(PfArgs a, uint32_t *pfh, opattr_diag *diag) {
+  OPA_DYN_LDS(uint16_t, cnt);
+  __shared__ uint32_t sbad;
+  const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
+  const uint32_t NN = a.NN;
+  for (uint32_t i = threadIdx.x; i < 4 * NN; i += OPA_TILE_THREADS) cnt[i] = 0;
+  if (threadIdx.x == 0) sbad = 0;
+  __syncthreads();
+  uint32_t key[kWaveChunks], rank[kWaveChunks], bad = 0;
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const int64_t x = base + tile_elem(c);
+    uint32_t n = NN;
+    if (x < a.P) {
+      n = a.name[x];
+      if (n >= NN) {
+        bad++;
+        n = NN;
+      }
+    }
+    key[c] = n;
+  }
+  wave_rank<kWaveChunks>(key, NN, bits_for(NN), cnt + wave_id() * NN, rank);
+  block_rank_bases(cnt, NN, pfh + tile * NN);
+  if (bad) atomicAdd(&sbad, bad);
+  __syncthreads();
+  if (threadIdx.x == 0 && sbad)
+    atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)sbad);
+}
+
+__global__ void __launch_bounds__(256) k_pf_slot_w(PfArgs a, const uint32_t *__restrict__ pfh,
+                                                   const uint32_t *__restrict__ off,
+                                                   int32_t *slot) {
+  OPA_DYN_LDS(uint16_t, cnt);
+  const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
+  const uint32_t NN = a.NN;
+  for (uint32_t i = threadIdx.x; i < 4 * NN; i += OPA_TILE_THREADS) cnt[i] = 0;
+  __syncthreads();
+  uint32_t key[kWaveChunks], rank[kWaveChunks];
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const int64_t x = base + tile_elem(c);
+    uint32_t n = NN;
+    if (x < a.P) {
+      n = a.name[x];
+      if (n >= NN) n = NN;
+    }
+    key[c] = n;
+  }
+  wave_rank<kWaveChunks>(key, NN, bits_for(NN), cnt + wave_id() * NN, rank);
+  block_rank_bases(cnt, NN, nullptr);
+  const uint32_t *row = pfh + tile * NN;
+  const uint16_t *wb = cnt + wave_id() * NN;
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const uint32_t n = key[c];
+    if (n < NN) {
+      const int64_t x = base + tile_elem(c);
+      slot[off[n] + row[n] + wb[n] + rank[c]] = (int32_t)x;
+    }
+  }
+}
+
 struct MatchArgs {
   const uint32_t *tlh, *tlc, *pfc, *off;
   const int32_t *slot;
@@ -403,6 +550,58 @@ __global__ void __launch_bounds__(256) k_tl_match(TlArgs a, MatchArgs m) {
   }
 }
 
+__global__ void __launch_bounds__(256) k_tl_match_w(TlArgs a, MatchArgs m, const uint32_t *pfirst,
+                                                    const uint32_t *plast, uint8_t *contig,
+                                                    opattr_diag *diag, int want_parts) {
+  OPA_DYN_LDS(uint16_t, cnt);
+  __shared__ int32_t lpart[OPA_TILE];
+  __shared__ uint32_t snc;
+  const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
+  const uint32_t NN = a.NN;
+  for (uint32_t i = threadIdx.x; i < 4 * NN; i += OPA_TILE_THREADS) cnt[i] = 0;
+  if (threadIdx.x == 0) snc = 0;
+  __syncthreads();
+  uint32_t key[kWaveChunks], rank[kWaveChunks];
+  int32_t jj[kWaveChunks];
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const int e = tile_elem(c);
+    int32_t lp;
+    tl_load(a, base + e, key[c], jj[c], lp);
+    lpart[e] = lp;
+  }
+  wave_rank<kWaveChunks>(key, NN, bits_for(NN), cnt + wave_id() * NN, rank);
+  block_rank_bases(cnt, NN, nullptr);
+  const uint32_t *row = m.tlh + tile * NN;
+  const uint16_t *wb = cnt + wave_id() * NN;
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const int32_t j = jj[c];
+    if (j < 0) continue;
+    const uint32_t n = key[c];
+    int32_t mt = -1;
+    if (n < NN) {
+      const uint32_t r = row[n] + wb[n] + rank[c];
+      const uint32_t rows = m.pfc[n];
+      mt = r < rows ? m.slot[m.off[n] + r] : -1;
+      if (m.skip_name && m.tlc[n] != rows) mt = -1;
+      const int e = tile_elem(c);
+      if (m.mbs && lpart[e] >= 0) {
+        m.mbs[base + e] = mt;
+        m.nbs[base + e] = n;
+      }
+    }
+    m.match[j] = mt;
+  }
+  if (want_parts) {
+    const uint32_t nb = part_edges(a, lpart, base, const_cast<uint32_t *>(pfirst),
+                                   const_cast<uint32_t *>(plast), contig, true);
+    if (nb) atomicAdd(&snc, nb);
+    __syncthreads();
+    if (threadIdx.x == 0 && snc) atomicOr(&diag->flags, OPATTR_F_PARTITION);
+  }
+}
+
 // bad class-map entries are counted once, with the other bad ids of the match
 __global__ void k_rep_check(const int32_t *__restrict__ part_rep, uint32_t NP, opattr_diag *diag) {
   const uint32_t q = blockIdx.x * blockDim.x + threadIdx.x;
@@ -437,17 +636,19 @@ void run_match(const IomArgs &x, hipStream_t s) {
   const uint32_t NN = d->n_names;
   const bool dedup = has_dedup(k, d);
   const bool parts = dedup && x.want_dedup;
+  const bool fast = NN <= kFastNames, fast_pf = NN <= kFastKeys;
+  const size_t lds = (size_t)4 * NN * sizeof(uint16_t);
   uint32_t *tlh = at<uint32_t>(ws, pl.tlh), *pfh = at<uint32_t>(ws, pl.pfh);
   uint32_t *tlc = at<uint32_t>(ws, pl.tlc), *pfc = at<uint32_t>(ws, pl.pfc);
   uint32_t *off = at<uint32_t>(ws, pl.off);
-  if (NN) {
-    note(hipMemsetAsync(tlc, 0, (size_t)NN * 4, s));
-    note(hipMemsetAsync(pfc, 0, (size_t)NN * 4, s));
-  }
+  uint32_t *pfirst = at<uint32_t>(ws, pl.pfirst), *plast = at<uint32_t>(ws, pl.plast);
+  uint8_t *contig = at<uint8_t>(ws, pl.contig);
+  fill_u32(tlc, 0, NN, s);
+  fill_u32(pfc, 0, NN, s);
   if (parts) {
-    note(hipMemsetAsync(at<uint32_t>(ws, pl.pfirst), 0xFF, (size_t)pl.NP * 4, s));
-    note(hipMemsetAsync(at<uint32_t>(ws, pl.plast), 0, (size_t)pl.NP * 4, s));
-    note(hipMemsetAsync(at<uint32_t>(ws, pl.pcnt), 0, (size_t)pl.NP * 4, s));
+    fill_u32(pfirst, 0xFFFFFFFFu, pl.NP, s);
+    fill_u32(plast, 0xFFFFFFFFu, pl.NP, s);
+    fill_u8(contig, 1, pl.NP, s);
   }
   if (dedup) k_rep_check<<<(d->n_parts + 255) / 256, 256, 0, s>>>(d->part_rep, d->n_parts, x.diag);
   const TlArgs ta = tl_args(k, d, ws, pl, dedup);
@@ -456,13 +657,21 @@ void run_match(const IomArgs &x, hipStream_t s) {
   pa.P = pl.P;
   pa.NN = NN;
   probe_begin(OPATTR_PROBE_TL_HIST, s);
-  if (pl.nt > 0)
-    k_tl_hist<<<(unsigned)pl.nt, 256, 0, s>>>(ta, tlh, at<uint32_t>(ws, pl.pfirst),
-                                              at<uint32_t>(ws, pl.plast),
-                                              at<uint32_t>(ws, pl.pcnt), x.diag, parts ? 1 : 0);
+  if (pl.nt > 0) {
+    if (fast) {
+      k_tl_hist_w<<<(unsigned)pl.nt, 256, lds, s>>>(ta, tlh, pfirst, plast, x.diag, parts ? 1 : 0);
+    } else {
+      k_tl_hist<<<(unsigned)pl.nt, 256, 0, s>>>(ta, tlh, x.diag);
+      if (parts)
+        k_part_edges<<<(unsigned)pl.nt, 256, 0, s>>>(ta, pfirst, plast, contig, x.diag, 0);
+    }
+  }
   probe_end(OPATTR_PROBE_TL_HIST, s);
   probe_begin(OPATTR_PROBE_PF_HIST, s);
-  if (pl.ntp > 0) k_pf_hist<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, x.diag);
+  if (pl.ntp > 0) {
+    if (fast_pf) k_pf_hist_w<<<(unsigned)pl.ntp, 256, lds, s>>>(pa, pfh, x.diag);
+    else k_pf_hist<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, x.diag);
+  }
   probe_end(OPATTR_PROBE_PF_HIST, s);
   probe_begin(OPATTR_PROBE_COL_SCAN, s);
   column_scan(tlh, pl.nt, NN, at<uint32_t>(ws, pl.tlch), tlc, s, nullptr);
@@ -472,8 +681,10 @@ void run_match(const IomArgs &x, hipStream_t s) {
                                x.policy == OPATTR_MISMATCH_STRICT ? 1 : 0);
   probe_end(OPATTR_PROBE_COL_SCAN, s);
   probe_begin(OPATTR_PROBE_PF_SLOT, s);
-  if (pl.ntp > 0)
-    k_pf_slot<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
+  if (pl.ntp > 0) {
+    if (fast_pf) k_pf_slot_w<<<(unsigned)pl.ntp, 256, lds, s>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
+    else k_pf_slot<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
+  }
   probe_end(OPATTR_PROBE_PF_SLOT, s);
   MatchArgs ma;
   ma.tlh = tlh;
@@ -486,24 +697,22 @@ void run_match(const IomArgs &x, hipStream_t s) {
   ma.nbs = parts ? at<uint32_t>(ws, pl.nbs) : nullptr;
   ma.skip_name = x.policy == OPATTR_MISMATCH_SKIP_NAME ? 1 : 0;
   probe_begin(OPATTR_PROBE_TL_MATCH, s);
-  if (pl.nt > 0) k_tl_match<<<(unsigned)pl.nt, 256, 0, s>>>(ta, ma);
+  if (pl.nt > 0) {
+    if (fast) {
+      k_tl_match_w<<<(unsigned)pl.nt, 256, lds, s>>>(ta, ma, pfirst, plast, contig, x.diag,
+                                                     parts ? 1 : 0);
+    } else {
+      k_tl_match<<<(unsigned)pl.nt, 256, 0, s>>>(ta, ma);
+      if (parts)
+        k_part_edges<<<(unsigned)pl.nt, 256, 0, s>>>(ta, pfirst, plast, contig, x.diag, 1);
+    }
+  }
   probe_end(OPATTR_PROBE_TL_MATCH, s);
 }
 
 // ---------------------------------------------------------------------------
 // layer dedup
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) k_part_stats(TlArgs a, uint32_t *pfirst, uint32_t *plast,
-                                                    uint32_t *pcnt) {
-  __shared__ uint32_t A[OPA_TILE];
-  __shared__ int32_t lpart[OPA_TILE];
-  __shared__ int32_t sh[16];
-  const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
-  tl_tile_keys(a, base, A, lpart, nullptr);
-  __syncthreads();
-  part_runs(lpart, base, pfirst, plast, pcnt, sh);
-}
-
 struct DedupArgs {
   int64_t T;
   const uint32_t *seq;
@@ -512,7 +721,7 @@ struct DedupArgs {
   const int32_t *part;
   const int32_t *part_rep;
   uint32_t NN, NP;
-  const uint32_t *pfirst, *plast, *pcnt;
+  const uint32_t *pfirst, *plast;
   const uint8_t *contig;
   int32_t *mbs;
   uint32_t *nbs;
@@ -539,18 +748,6 @@ __global__ void k_src_fill(DedupArgs a) {
   a.nbs[r] = nm;
 }
 
-__global__ void k_part_check(DedupArgs a) {
-  const uint32_t q = blockIdx.x * blockDim.x + threadIdx.x;
-  bool nc = false;
-  if (q < a.NP) {
-    const uint32_t c = a.pcnt[q];
-    const bool ok = c == 0 || (a.plast[q] - a.pfirst[q] + 1u == c);
-    const_cast<uint8_t *>(a.contig)[q] = ok ? 1 : 0;
-    nc = !ok;
-  }
-  if (__ballot(nc) && lane_id() == 0) atomicOr(&a.diag->flags, OPATTR_F_PARTITION);
-}
-
 __global__ void k_dedup(DedupArgs a) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   bool err = false;
@@ -562,15 +759,16 @@ __global__ void k_dedup(DedupArgs a) {
       if (r >= 0 && (uint32_t)r < a.NP && r != pt) {
         // a duplicate: inherit from the representative's launch at the same
         // position of its partition
-        bool ok = a.contig[pt] && a.part_rep[r] == r && a.pcnt[r] > 0 && a.contig[r];
+        const uint32_t f = a.pfirst[r];
+        bool ok = a.contig[pt] && a.part_rep[r] == r && f != 0xFFFFFFFFu && a.contig[r];
         const int64_t rk = rank_of(a, i);
         ok = ok && rk >= 0;
         int32_t mt = -1;
         if (ok) {
           const uint32_t pos = (uint32_t)(rk - (int64_t)a.pfirst[pt]);
-          ok = pos < a.pcnt[r];
+          ok = pos < a.plast[r] - f + 1u;
           if (ok) {
-            const uint32_t src = a.pfirst[r] + pos;
+            const uint32_t src = f + pos;
             ok = a.nbs[src] == nm;
             if (ok) mt = a.mbs[src];
           }
@@ -597,10 +795,11 @@ void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, op
   a.part_rep = d->part_rep;
   a.NN = d->n_names;
   a.NP = d->n_parts;
-  a.pfirst = at<uint32_t>(ws, pl.pfirst);
-  a.plast = at<uint32_t>(ws, pl.plast);
-  a.pcnt = at<uint32_t>(ws, pl.pcnt);
-  a.contig = at<uint8_t>(ws, pl.contig);
+  uint32_t *pfirst = at<uint32_t>(ws, pl.pfirst), *plast = at<uint32_t>(ws, pl.plast);
+  uint8_t *contig = at<uint8_t>(ws, pl.contig);
+  a.pfirst = pfirst;
+  a.plast = plast;
+  a.contig = contig;
   a.mbs = at<int32_t>(ws, pl.mbs);
   a.nbs = at<uint32_t>(ws, pl.nbs);
   a.match = match;
@@ -608,16 +807,14 @@ void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, op
   const unsigned nb = (unsigned)((pl.T + 255) / 256);
   probe_begin(OPATTR_PROBE_DEDUP, s);
   if (!stats_ready) {
-    note(hipMemsetAsync(at<uint32_t>(ws, pl.pfirst), 0xFF, (size_t)pl.NP * 4, s));
-    note(hipMemsetAsync(at<uint32_t>(ws, pl.plast), 0, (size_t)pl.NP * 4, s));
-    note(hipMemsetAsync(at<uint32_t>(ws, pl.pcnt), 0, (size_t)pl.NP * 4, s));
-    k_part_stats<<<(unsigned)pl.nt, 256, 0, s>>>(tl_args(k, d, ws, pl, true),
-                                                 at<uint32_t>(ws, pl.pfirst),
-                                                 at<uint32_t>(ws, pl.plast),
-                                                 at<uint32_t>(ws, pl.pcnt));
+    const TlArgs ta = tl_args(k, d, ws, pl, true);
+    fill_u32(pfirst, 0xFFFFFFFFu, pl.NP, s);
+    fill_u32(plast, 0xFFFFFFFFu, pl.NP, s);
+    fill_u8(contig, 1, pl.NP, s);
+    k_part_edges<<<(unsigned)pl.nt, 256, 0, s>>>(ta, pfirst, plast, contig, diag, 0);
+    k_part_edges<<<(unsigned)pl.nt, 256, 0, s>>>(ta, pfirst, plast, contig, diag, 1);
     k_src_fill<<<nb, 256, 0, s>>>(a);
   }
-  k_part_check<<<(d->n_parts + 255) / 256, 256, 0, s>>>(a);
   k_dedup<<<nb, 256, 0, s>>>(a);
   probe_end(OPATTR_PROBE_DEDUP, s);
 }

@@ -353,16 +353,16 @@ CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws
     k_rprep<<<(unsigned)((R + 255) / 256), 256, 0, s>>>(cr, NS, d->n_ops, at<int64_t>(ws, pl.ree),
                                                         at<int32_t>(ws, pl.npg), diag);
   if (R > 0) k_blocks16<<<(NS + 1 + 255) / 256, 256, 0, s>>>(cr.st, R, NS, rblk);
-  else note(hipMemsetAsync(rblk, 0, (size_t)(NS + 1) * 8, s));
+  else fill_u32(reinterpret_cast<uint32_t *>(rblk), 0, 2 * ((int64_t)NS + 1), s);
   return cr;
 }
 
 void resolve_ranges(const CoreRanges &cr, const opattr_dims *d, void *ws, const Plan &pl,
                     uint8_t *range_depth, opattr_diag *diag, hipStream_t s) {
   const uint32_t NS = d->n_streams;
-  note(hipMemsetAsync(at<uint8_t>(ws, pl.sflag), 0, NS ? NS : 1, s));
+  fill_u8(at<uint8_t>(ws, pl.sflag), 0, NS ? NS : 1, s);
   if (pl.R <= 0 || NS == 0) {
-    if (range_depth && pl.R > 0) note(hipMemsetAsync(range_depth, 0, (size_t)pl.R, s));
+    if (range_depth && pl.R > 0) fill_u8(range_depth, 0, pl.R, s);
     return;
   }
   RangeWork w = range_work(cr, d, ws, pl, diag);

@@ -169,8 +169,23 @@ __global__ void k_gather_u32(const uint32_t *src, const uint32_t *perm, uint64_t
   if (i < n) dst[i] = src[perm[i]];
 }
 
+__global__ void k_fill_u32(uint32_t *p, uint32_t v, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+__global__ void k_fill_u8(uint8_t *p, uint8_t v, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
 static unsigned blocks_for(int64_t n, int b) { return (unsigned)((n + b - 1) / b); }
 
+void fill_u32(uint32_t *p, uint32_t v, int64_t n, hipStream_t s) {
+  if (n > 0) k_fill_u32<<<blocks_for(n, 256), 256, 0, s>>>(p, v, n);
+}
+void fill_u8(uint8_t *p, uint8_t v, int64_t n, hipStream_t s) {
+  if (n > 0) k_fill_u8<<<blocks_for(n, 256), 256, 0, s>>>(p, v, n);
+}
 void launch_iota(uint32_t *v, int64_t n, hipStream_t s) {
   if (n > 0) k_iota<<<blocks_for(n, 256), 256, 0, s>>>(v, n);
 }

@@ -95,6 +95,21 @@ def test_random_traces_with_ties(seed):
         parity.assert_attribute(out2, want2, diag2)
 
 
+@pytest.mark.parametrize("n_names,n_ops", [(5000, 50), (7000, 7000)])
+def test_many_names_and_rows(n_names, n_ops):
+    """Name and operator-row counts past the LDS-counter limits take the
+    tile radix sort instead; both must agree with the oracle."""
+    tr = cases.random_trace(4242 + n_names, T=40_000, S=4, n_names=n_names, R=6_000,
+                            n_ops=n_ops, t_max=400_000, max_depth=5, dedup=True)
+    print(f"case many names={n_names} ops={n_ops} T={tr['seq'].size}", flush=True)
+    want = O.attribute(tr)
+    out, diag = _run(tr)
+    parity.assert_attribute(out, want, diag)
+    sm, _, _ = cases.stream_major(tr)
+    out2, diag2 = _run(sm, flags=HINTS)
+    parity.assert_attribute(out2, O.attribute(sm), diag2)
+
+
 @pytest.mark.parametrize("policy", [opattr.MISMATCH_SKIP_NAME, opattr.MISMATCH_STRICT])
 def test_mismatch_policies(policy):
     tr = tg.generate("lstm", T=300_000, ranges=3_000, emission="stream_major")
