@@ -236,10 +236,11 @@ enum {
   OPATTR_PROBE_TL_MATCH = 5,   /* per-tile rank and join                    */
   OPATTR_PROBE_DEDUP = 6,      /* dedup broadcast                           */
   OPATTR_PROBE_RANGES = 7,     /* range order, parents and depths           */
-  OPATTR_PROBE_MAIN_PASS = 8,  /* enclosure pass (range ids, operator runs) */
+  OPATTR_PROBE_MAIN_PASS = 8,  /* enclosure pass (range ids)                */
   OPATTR_PROBE_FINALIZE = 9,   /* status of the diag record                 */
-  OPATTR_PROBE_AGGREGATE = 10, /* run sort, reduction, operator rows        */
-  OPATTR_NUM_PROBES = 11
+  OPATTR_PROBE_AGGREGATE = 10, /* item sort, per-row reduction, table       */
+  OPATTR_PROBE_AGG_RUNS = 11,  /* in-place run reduction over the launches  */
+  OPATTR_NUM_PROBES = 12
 };
 int opattr_set_probe_events(void *const *events, int n);
 

@@ -4,6 +4,7 @@
 // in-place reduction of the enclosure pass and by the per-row reduction.
 #pragma once
 #include "common.h"
+#include "impl.h"
 
 namespace opa {
 
@@ -52,7 +53,10 @@ __device__ __forceinline__ void acc_zero(Acc &a) {
 }
 
 // One launch with duration d and profiled row m (m outside [0, P): unmatched).
-__device__ __forceinline__ void acc_launch(Acc &a, const AggIn &in, int32_t m, uint32_t d) {
+// mx / dw: MAX and DW-mean counters (compile-time constants in the kernels
+// specialised for the default kinds, so the per-counter tests fold away).
+__device__ __forceinline__ void acc_launch(Acc &a, const AggIn &in, int32_t m, uint32_t d,
+                                           uint32_t mx, uint32_t dw) {
   a.kc += 1;
   a.tns += d;
   if (m < 0 || (int64_t)m >= in.P) return;
@@ -77,12 +81,12 @@ __device__ __forceinline__ void acc_launch(Acc &a, const AggIn &in, int32_t m, u
   const double dd = (double)d;
 #pragma unroll
   for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-    if ((in.maxmask >> c) & 1u) {
+    if ((mx >> c) & 1u) {
       const unsigned long long k = f2key(v[c]);
       a.v[c] = k > a.v[c] ? k : a.v[c];
       if (v[c] != v[c]) a.nan |= 1u << c;
     } else {
-      const double x = ((in.dwmask >> c) & 1u) ? (double)v[c] * dd : (double)v[c];  // m_i * d_i
+      const double x = ((dw >> c) & 1u) ? (double)v[c] * dd : (double)v[c];  // m_i * d_i
       a.v[c] = d2bits(bits2d(a.v[c]) + x);
     }
   }
@@ -102,24 +106,29 @@ __device__ __forceinline__ void acc_merge(Acc &a, const Acc &b, uint32_t maxmask
   a.nan |= b.nan;
 }
 
-template <typename F>
-__device__ __forceinline__ Acc acc_map(const Acc &a, F f) {
-  Acc r;
-  r.kc = f(a.kc);
-  r.tns = f(a.tns);
-  r.mc = f(a.mc);
-  r.mns = f(a.mns);
+// One step of a segmented inclusive scan over the lanes, field by field so
+// that no second accumulator is held: a += value of lane (lane - o) if take.
+__device__ __forceinline__ void acc_scan_step(Acc &a, int o, bool take, uint32_t maxmask) {
+#define OPA_SCAN_U64(f)                                                  \
+  {                                                                      \
+    const unsigned long long y = __shfl_up(a.f, (unsigned)o, OPA_WAVE); \
+    if (take) a.f += y;                                                  \
+  }
+  OPA_SCAN_U64(kc)
+  OPA_SCAN_U64(tns)
+  OPA_SCAN_U64(mc)
+  OPA_SCAN_U64(mns)
+#undef OPA_SCAN_U64
 #pragma unroll
-  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) r.v[c] = f(a.v[c]);
-  r.nan = (uint32_t)f((unsigned long long)a.nan);
-  return r;
-}
-
-__device__ __forceinline__ Acc acc_shfl_up(const Acc &a, int o) {
-  return acc_map(a, [o](unsigned long long x) { return __shfl_up(x, (unsigned)o, OPA_WAVE); });
-}
-__device__ __forceinline__ Acc acc_shfl_xor(const Acc &a, int o) {
-  return acc_map(a, [o](unsigned long long x) { return __shfl_xor(x, o, OPA_WAVE); });
+  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
+    const unsigned long long y = __shfl_up(a.v[c], (unsigned)o, OPA_WAVE);
+    if (take) {
+      if ((maxmask >> c) & 1u) a.v[c] = y > a.v[c] ? y : a.v[c];
+      else a.v[c] = d2bits(bits2d(a.v[c]) + bits2d(y));
+    }
+  }
+  const uint32_t yn = __shfl_up(a.nan, (unsigned)o, OPA_WAVE);
+  if (take) a.nan |= yn;
 }
 
 // Butterfly reduction over the wave; every lane ends with the total. Each
@@ -128,8 +137,17 @@ __device__ __forceinline__ Acc acc_shfl_xor(const Acc &a, int o) {
 __device__ __forceinline__ void acc_wave_reduce(Acc &a, uint32_t maxmask) {
 #pragma unroll
   for (int o = 1; o < OPA_WAVE; o <<= 1) {
-    const Acc b = acc_shfl_xor(a, o);
-    acc_merge(a, b, maxmask);
+    a.kc += __shfl_xor(a.kc, o, OPA_WAVE);
+    a.tns += __shfl_xor(a.tns, o, OPA_WAVE);
+    a.mc += __shfl_xor(a.mc, o, OPA_WAVE);
+    a.mns += __shfl_xor(a.mns, o, OPA_WAVE);
+#pragma unroll
+    for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
+      const unsigned long long y = __shfl_xor(a.v[c], o, OPA_WAVE);
+      if ((maxmask >> c) & 1u) a.v[c] = y > a.v[c] ? y : a.v[c];
+      else a.v[c] = d2bits(bits2d(a.v[c]) + bits2d(y));
+    }
+    a.nan |= __shfl_xor(a.nan, o, OPA_WAVE);
   }
 }
 

@@ -190,11 +190,14 @@ __global__ void __launch_bounds__(256) k_item_scatter_r(AggWork w) {
 __global__ void k_chunk_map(AggWork w) {
   const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
   if (g >= w.G) return;
-  for (uint32_t c = w.coff[g]; c < w.coff[g + 1]; ++c) w.cmap[c] = g;
+  const uint32_t c0 = w.coff[g], c1 = w.coff[g + 1];  // read once: cmap may alias
+  for (uint32_t c = c0; c < c1; ++c) w.cmap[c] = g;
 }
 
 // 2. one wave per chunk of at most 64 items of one row
+template <bool DEF>
 __global__ void __launch_bounds__(256) k_chunk_reduce(AggWork w) {
+  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
   const int64_t nch = w.meta[3];
   const int ln = lane_id();
   for (int64_t ch = (int64_t)blockIdx.x * 4 + wave_id(); ch < nch; ch += (int64_t)gridDim.x * 4) {
@@ -208,16 +211,19 @@ __global__ void __launch_bounds__(256) k_chunk_reduce(AggWork w) {
       if (b == 0) {
         acc_load(acc, w.rows + a);
       } else {
-        for (uint32_t k = 0; k < b; ++k) acc_launch(acc, w.in, w.in.match[a + k], w.in.dur[a + k]);
+        for (uint32_t k = 0; k < b; ++k)
+          acc_launch(acc, w.in, w.in.match[a + k], w.in.dur[a + k], mx, dw);
       }
     }
-    acc_wave_reduce(acc, w.in.maxmask);
+    acc_wave_reduce(acc, mx);
     if (ln == 0) acc_store(w.part + ch, acc, g);
   }
 }
 
 // 3. one wave per operator row: combine its chunks and finalise
+template <bool DEF>
 __global__ void __launch_bounds__(256) k_combine(AggWork w) {
+  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
   const uint32_t g = blockIdx.x * 4 + wave_id();
   if (g >= w.G) return;
   const int ln = lane_id();
@@ -227,9 +233,9 @@ __global__ void __launch_bounds__(256) k_combine(AggWork w) {
   for (uint32_t c = c0 + ln; c < c1; c += OPA_WAVE) {
     Acc b;
     acc_load(b, w.part + c);
-    acc_merge(acc, b, w.in.maxmask);
+    acc_merge(acc, b, mx);
   }
-  acc_wave_reduce(acc, w.in.maxmask);
+  acc_wave_reduce(acc, mx);
   opattr_op_row *row = w.table + g;
   if (ln == 0) {
     row->kernel_count = acc.kc;
@@ -246,9 +252,9 @@ __global__ void __launch_bounds__(256) k_combine(AggWork w) {
     const double qnan = __longlong_as_double(0x7FF8000000000000ll);
     double v;
     if (((w.absent >> c) & 1u) || acc.mc == 0) v = qnan;
-    else if ((w.in.maxmask >> c) & 1u)
+    else if ((mx >> c) & 1u)
       v = ((acc.nan >> c) & 1u) ? qnan : (double)key2f((uint32_t)mine);
-    else if ((w.in.dwmask >> c) & 1u) v = acc.mns ? bits2d(mine) / (double)acc.mns : qnan;
+    else if ((dw >> c) & 1u) v = acc.mns ? bits2d(mine) / (double)acc.mns : qnan;
     else v = bits2d(mine);
     row->value[c] = v;
   }
@@ -312,6 +318,7 @@ void run_aggregate(const EncArgs &x, hipStream_t s) {
   w.table = x.table;
   w.sum = x.sum;
   const bool fast = pl.G <= kFastKeys;
+  const bool def = w.in.maxmask == kDefMaxMask && w.in.dwmask == kDefDwMask;
   const size_t lds = (size_t)4 * pl.G * sizeof(uint16_t);
   const unsigned tgrid = (unsigned)(pl.ntrt < 1024 ? (pl.ntrt > 0 ? pl.ntrt : 1) : 1024);
 
@@ -330,9 +337,12 @@ void run_aggregate(const EncArgs &x, hipStream_t s) {
     else k_item_scatter_r<<<tgrid, 256, 0, s>>>(w);
     k_chunk_map<<<(pl.G + 255) / 256, 256, 0, s>>>(w);
     const int64_t want = (pl.max_chunks + 3) / 4;
-    k_chunk_reduce<<<(unsigned)(want < 2048 ? want : 2048), 256, 0, s>>>(w);
+    const unsigned cgrid = (unsigned)(want < 2048 ? want : 2048);
+    if (def) k_chunk_reduce<true><<<cgrid, 256, 0, s>>>(w);
+    else k_chunk_reduce<false><<<cgrid, 256, 0, s>>>(w);
   }
-  k_combine<<<(pl.G + 3) / 4, 256, 0, s>>>(w);
+  if (def) k_combine<true><<<(pl.G + 3) / 4, 256, 0, s>>>(w);
+  else k_combine<false><<<(pl.G + 3) / 4, 256, 0, s>>>(w);
   k_summary<<<1, 1024, 0, s>>>(w);
   probe_end(OPATTR_PROBE_AGGREGATE, s);
 }

@@ -150,7 +150,7 @@ void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStre
   probe_end(OPATTR_PROBE_FINALIZE, s);
 }
 
-static const uint8_t kDefaultKind[OPATTR_NUM_COUNTERS] = {
+static constexpr uint8_t kDefaultKind[OPATTR_NUM_COUNTERS] = {
     // counter appendix table, rows 1..20: SUM for additive counts, DW-mean for
     // rates and utilisations, MAX for per-kernel constants
     OPATTR_AGG_SUM,    OPATTR_AGG_SUM,    OPATTR_AGG_SUM,    OPATTR_AGG_DWMEAN,
@@ -158,6 +158,15 @@ static const uint8_t kDefaultKind[OPATTR_NUM_COUNTERS] = {
     OPATTR_AGG_DWMEAN, OPATTR_AGG_DWMEAN, OPATTR_AGG_SUM,    OPATTR_AGG_DWMEAN,
     OPATTR_AGG_DWMEAN, OPATTR_AGG_DWMEAN, OPATTR_AGG_SUM,    OPATTR_AGG_DWMEAN,
     OPATTR_AGG_DWMEAN, OPATTR_AGG_MAX,    OPATTR_AGG_SUM,    OPATTR_AGG_MAX};
+
+constexpr uint32_t kind_mask(uint8_t kind) {
+  uint32_t m = 0;
+  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c)
+    if (kDefaultKind[c] == kind) m |= 1u << c;
+  return m;
+}
+static_assert(kind_mask(OPATTR_AGG_MAX) == kDefMaxMask && kind_mask(OPATTR_AGG_DWMEAN) == kDefDwMask,
+              "default kinds and their masks disagree");
 
 static const int64_t kMaxN = (int64_t)1 << 31;
 

@@ -1,5 +1,5 @@
-// Enclosure (Alg. 2) and the first level of the aggregation (Eq. 1) in one
-// pass over the launches, in storage order.
+// Enclosure (Alg. 2) and the first level of the aggregation (Eq. 1), two
+// passes over the launches in storage order.
 //
 // A block takes 2048 consecutive launches, eight consecutive ones per thread.
 // Enclosure: the range starts that can matter for the block's main stream
@@ -10,10 +10,11 @@
 // the query point.
 //
 // Aggregation: each wave cuts its 512 launches into runs of one operator row.
-// With at most kRowCap runs the wave reduces them in place -- every thread
-// accumulates its launches in registers, a segmented scan over the lanes
-// carries runs across threads -- and writes one partial row per run. With
-// more runs it writes references (row, first launch, length <= 16) that the
+// With at most kRowCap runs the wave reduces them in place: every thread
+// accumulates its launches in registers, leaving each run that ends inside it
+// in an LDS row, and a segmented scan over the lanes carries the runs that
+// cross threads. The rows then go out with coalesced stores. With more runs
+// the wave writes references (row, first launch, length <= 16) that the
 // per-row reduction resolves later. Partial rows and references land in
 // launch order at offsets found by a decoupled look-back over the blocks,
 // which take their positions from a counter in the order they start.
@@ -114,6 +115,15 @@ __device__ __forceinline__ void store_run(T *p, int64_t i, int nv, const T (&o)[
   }
 }
 
+// g[k] for a run-time k without indexing the register array
+__device__ __forceinline__ uint32_t pick(const uint32_t (&g)[kPer], int k) {
+  uint32_t r = g[0];
+#pragma unroll
+  for (int j = 1; j < kPer; ++j)
+    if (j == k) r = g[j];
+  return r;
+}
+
 __device__ __forceinline__ unsigned long long lb_load(const unsigned long long *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -159,261 +169,271 @@ __device__ inline bool lookback(const unsigned long long *state, int64_t bid, ui
   return true;
 }
 
-template <int MODE>
-__global__ void __launch_bounds__(kEncThreads) k_enc(EncParams a) {
+__global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
   __shared__ uint64_t sS[kEncWindow];
   __shared__ uint64_t red[2][kEncThreads / OPA_WAVE];
-  __shared__ int64_t win[3];
+  __shared__ int64_t win[2];
+  __shared__ uint32_t sbad;
+  const int tid = threadIdx.x, w = wave_id(), ln = lane_id();
+  if (tid == 0) sbad = 0;
+  const int64_t i0 = (int64_t)blockIdx.x * kSpan;
+  const int64_t ib = i0 + (int64_t)tid * kPer;
+  const int nv = (int)(a.T - ib < 0 ? 0 : (a.T - ib < kPer ? a.T - ib : kPer));
+  uint32_t bad = 0;
+  uint16_t st[kPer];
+  uint64_t q[kPer];
+  load_run(a.stream, ib, nv, st);
+  load_run(a.q, ib, nv, q);
+  const uint16_t s0 = a.stream[i0];
+  // smallest and largest query point of the block's main stream
+  uint64_t mn = ~0ull, mx = 0ull;
+#pragma unroll
+  for (int k = 0; k < kPer; ++k)
+    if (k < nv && st[k] == s0) {
+      mn = q[k] < mn ? q[k] : mn;
+      mx = q[k] > mx ? q[k] : mx;
+    }
+  for (int o = OPA_WAVE / 2; o > 0; o >>= 1) {
+    const uint64_t y = __shfl_xor(mn, o, OPA_WAVE), z = __shfl_xor(mx, o, OPA_WAVE);
+    mn = y < mn ? y : mn;
+    mx = z > mx ? z : mx;
+  }
+  if (ln == 0) {
+    red[0][w] = mn;
+    red[1][w] = mx;
+  }
+  __syncthreads();
+  // wave 0 finds the window start, wave 1 its end
+  if (w < 2) {
+    uint64_t qa = ~0ull, qb = 0;
+    for (int k = 0; k < kEncThreads / OPA_WAVE; ++k) {
+      qa = red[0][k] < qa ? red[0][k] : qa;
+      qb = red[1][k] > qb ? red[1][k] : qb;
+    }
+    int64_t p = -1;
+    if (s0 < a.NS && qa <= qb) {
+      const int64_t lo = a.rblk[s0], hi = a.rblk[s0 + 1];
+      p = wave_upper_bound(a.cr.s, lo, hi, w == 0 ? qa : qb) - 1;
+      if (w == 0 && p < lo) p = lo;
+    }
+    if (ln == 0) win[w] = p;
+  }
+  __syncthreads();
+  const int64_t wlo = win[0];
+  int64_t wn = (s0 < a.NS) ? win[1] - wlo + 1 : 0;
+  if (wn < 0) wn = 0;
+  const bool staged = wn > 0 && wn <= kEncWindow;
+  if (staged)
+    for (int k = tid; k < wn; k += kEncThreads) sS[k] = a.cr.s[wlo + k];
+  __syncthreads();
+
+  int32_t rout[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    int32_t rid = -1;
+    if (k < nv && st[k] < a.NS && q[k] < (1ull << 63)) {
+      const int64_t lo = a.rblk[st[k]], hi = a.rblk[st[k] + 1];
+      const bool in0 = st[k] == s0;
+      int64_t p;
+      if (in0 && wn == 0) {
+        p = lo - 1;  // no range of the stream starts at or before the block's queries
+      } else if (in0 && staged) {
+        int l2 = 0, h2 = (int)wn;
+        while (l2 < h2) {
+          const int mid = (l2 + h2) >> 1;
+          if (sS[mid] <= q[k]) l2 = mid + 1;
+          else h2 = mid;
+        }
+        p = wlo + l2 - 1;
+        if (p < lo) p = lo - 1;
+      } else {
+        p = thread_upper_bound(a.cr.s, lo, hi, q[k]) - 1;
+      }
+      int64_t j = p;
+      int steps = 0;
+      while (j >= lo && a.ree[j] < (int64_t)q[k] && steps < kMaxWalk) {
+        j = a.npg[j];
+        ++steps;
+      }
+      if (j >= lo && a.ree[j] >= (int64_t)q[k]) rid = (int32_t)j;
+    } else if (k < nv && st[k] >= a.NS) {
+      bad++;
+    }
+    rout[k] = rid >= 0 ? (a.cr.perm ? a.cr.perm[rid] : rid) : -1;
+  }
+  store_run(a.range_id, ib, nv, rout);
+  if (bad) atomicAdd(&sbad, bad);
+  __syncthreads();
+  if (tid == 0 && sbad)
+    atomicAdd((unsigned long long *)&a.diag->bad_records, (unsigned long long)sbad);
+}
+
+// a += b, field by field (rows staged in LDS)
+__device__ __forceinline__ void row_add(PartRow *r, const Acc &b, uint32_t maxmask) {
+  r->kc += b.kc;
+  r->tns += b.tns;
+  r->mc += b.mc;
+  r->mns += b.mns;
+#pragma unroll
+  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
+    const unsigned long long x = r->v[c];
+    if ((maxmask >> c) & 1u) r->v[c] = b.v[c] > x ? b.v[c] : x;
+    else r->v[c] = d2bits(bits2d(x) + bits2d(b.v[c]));
+  }
+  r->nan |= b.nan;
+}
+
+template <bool DEF>  // DEF: the default aggregation kinds
+__global__ void __launch_bounds__(kEncThreads) __attribute__((amdgpu_waves_per_eu(4)))
+k_agg_runs(EncParams a) {
+  __shared__ PartRow stage[kEncThreads / OPA_WAVE][kRowCap];
   __shared__ uint32_t wcnt[2][kEncThreads / OPA_WAVE];
   __shared__ uint32_t spre[2];
   __shared__ uint32_t sbid, sbad, sfail;
   const int tid = threadIdx.x, w = wave_id(), ln = lane_id();
+  const AggIn &in = a.ag;
+  const uint32_t mx = DEF ? kDefMaxMask : in.maxmask, dw = DEF ? kDefDwMask : in.dwmask;
   if (tid == 0) {
     sbad = 0;
     sfail = 0;
-    if (MODE & 2) sbid = atomicAdd(a.em.ctr, 1u);
+    sbid = atomicAdd(a.em.ctr, 1u);
   }
   __syncthreads();
-  const int64_t bid = (MODE & 2) ? (int64_t)sbid : (int64_t)blockIdx.x;
-  const int64_t i0 = bid * kSpan;
-  const int64_t ib = i0 + (int64_t)tid * kPer;
+  const int64_t bid = sbid;
+  const int64_t ib = bid * kSpan + (int64_t)tid * kPer;
   const int nv = (int)(a.T - ib < 0 ? 0 : (a.T - ib < kPer ? a.T - ib : kPer));
   uint32_t bad = 0;
   uint32_t g[kPer];
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) g[k] = k < nv ? a.NOPS : 0xFFFFFFFFu;
-
-  if (MODE & 1) {
-    uint16_t st[kPer];
-    uint64_t q[kPer];
-    load_run(a.stream, ib, nv, st);
-    load_run(a.q, ib, nv, q);
-    const uint16_t s0 = a.stream[i0];
-    // smallest and largest query point of the block's main stream
-    uint64_t mn = ~0ull, mx = 0ull;
-#pragma unroll
-    for (int k = 0; k < kPer; ++k)
-      if (k < nv && st[k] == s0) {
-        mn = q[k] < mn ? q[k] : mn;
-        mx = q[k] > mx ? q[k] : mx;
-      }
-    for (int o = OPA_WAVE / 2; o > 0; o >>= 1) {
-      const uint64_t y = __shfl_xor(mn, o, OPA_WAVE), z = __shfl_xor(mx, o, OPA_WAVE);
-      mn = y < mn ? y : mn;
-      mx = z > mx ? z : mx;
-    }
-    if (ln == 0) {
-      red[0][w] = mn;
-      red[1][w] = mx;
-    }
-    __syncthreads();
-    if (w == 0) {
-      uint64_t qa = ~0ull, qb = 0;
-      for (int k = 0; k < kEncThreads / OPA_WAVE; ++k) {
-        qa = red[0][k] < qa ? red[0][k] : qa;
-        qb = red[1][k] > qb ? red[1][k] : qb;
-      }
-      int64_t wlo = 0, wn = 0;
-      if (s0 < a.NS && qa <= qb) {
-        const int64_t lo = a.rblk[s0], hi = a.rblk[s0 + 1];
-        const int64_t pa = wave_upper_bound(a.cr.s, lo, hi, qa) - 1;
-        const int64_t pb = wave_upper_bound(a.cr.s, lo, hi, qb) - 1;
-        wlo = pa > lo ? pa : lo;
-        wn = pb - wlo + 1;
-        if (wn < 0) wn = 0;
-      }
-      if (ln == 0) {
-        win[0] = wlo;
-        win[1] = wn;
-      }
-    }
-    __syncthreads();
-    const int64_t wlo = win[0], wn = win[1];
-    const bool staged = wn > 0 && wn <= kEncWindow;
-    if (staged)
-      for (int k = tid; k < wn; k += kEncThreads) sS[k] = a.cr.s[wlo + k];
-    __syncthreads();
-
-    int32_t rout[kPer];
-#pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-      int32_t rid = -1;
-      if (k < nv && st[k] < a.NS && q[k] < (1ull << 63)) {
-        const int64_t lo = a.rblk[st[k]], hi = a.rblk[st[k] + 1];
-        const bool in0 = st[k] == s0;
-        int64_t p;
-        if (in0 && wn == 0) {
-          p = lo - 1;  // no range of the stream starts at or before the block's queries
-        } else if (in0 && staged) {
-          int l2 = 0, h2 = (int)wn;
-          while (l2 < h2) {
-            const int mid = (l2 + h2) >> 1;
-            if (sS[mid] <= q[k]) l2 = mid + 1;
-            else h2 = mid;
-          }
-          p = wlo + l2 - 1;
-          if (p < lo) p = lo - 1;
-        } else {
-          p = thread_upper_bound(a.cr.s, lo, hi, q[k]) - 1;
-        }
-        int64_t j = p;
-        int steps = 0;
-        while (j >= lo && a.ree[j] < (int64_t)q[k] && steps < kMaxWalk) {
-          j = a.npg[j];
-          ++steps;
-        }
-        if (j >= lo && a.ree[j] >= (int64_t)q[k]) rid = (int32_t)j;
-      } else if (k < nv && st[k] >= a.NS) {
-        bad++;
-      }
-      rout[k] = rid >= 0 ? (a.cr.perm ? a.cr.perm[rid] : rid) : -1;
-      if (rid >= 0) g[k] = a.cr.op[rid];
-    }
-    store_run(a.range_id, ib, nv, rout);
-  } else {
+  int32_t mt[kPer];
+  uint32_t du[kPer];
+  {
     int32_t rin[kPer];
     load_run(a.range_id, ib, nv, rin);
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
+      g[k] = k < nv ? a.NOPS : 0xFFFFFFFFu;
       if (k >= nv) continue;
       const int32_t r = rin[k];
       if (r >= 0 && r < a.R_in && a.op_in[r] < a.NOPS) g[k] = a.op_in[r];
       else if (r < -1 || r >= a.R_in || r >= 0) bad++;
     }
   }
+  load_run(in.match, ib, nv, mt);
+  load_run(in.dur, ib, nv, du);
+#pragma unroll
+  for (int k = 0; k < kPer; ++k)
+    if (k < nv && (mt[k] < -1 || (int64_t)mt[k] >= in.P)) bad++;  // aggregates as unmatched
 
-  if (MODE & 2) {
-    const AggIn &in = a.ag;
-    // ---- runs of one operator row inside the wave, in launch order
-    const uint32_t gl = __shfl_up(g[kPer - 1], 1, OPA_WAVE);
-    uint32_t hm = 0;  // bit k: launch k starts a run
+  // ---- runs of one operator row inside the wave, in launch order
+  const uint32_t gl = __shfl_up(g[kPer - 1], 1, OPA_WAVE);
+  uint32_t hm = 0;  // bit k: launch k starts a run
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const uint32_t prev = k ? g[k - 1] : (ln ? gl : 0xFFFFFFFFu);
+    if (k < nv && g[k] != prev) hm |= 1u << k;
+  }
+  // pieces for references: runs cut at every 16th launch as well
+  const uint32_t hp = hm | ((nv > 0 && (ln & 1) == 0) ? 1u : 0u);
+  const uint32_t nh = __popc(hm), nhp = __popc(hp);
+  const uint32_t hb = wave_incl_scan_add(nh) - nh;
+  const uint32_t hpb = wave_incl_scan_add(nhp) - nhp;
+  const uint32_t nr_w = __shfl(hb + nh, OPA_WAVE - 1, OPA_WAVE);
+  const uint32_t np_w = __shfl(hpb + nhp, OPA_WAVE - 1, OPA_WAVE);
+  const bool rowmode = nr_w <= (uint32_t)kRowCap;
+  if (ln == 0) {
+    wcnt[0][w] = rowmode ? nr_w : np_w;
+    wcnt[1][w] = rowmode ? nr_w : 0u;
+  }
+  __syncthreads();
+  uint32_t bi = 0, br = 0, wi = 0, wr = 0;
+  for (int k = 0; k < kEncThreads / OPA_WAVE; ++k) {
+    if (k < w) {
+      wi += wcnt[0][k];
+      wr += wcnt[1][k];
+    }
+    bi += wcnt[0][k];
+    br += wcnt[1][k];
+  }
+  if (tid == 0) lb_store(a.em.state + bid, lb_pack(bid == 0 ? kLbInc : kLbAgg, bi, br));
+
+  // ---- in-place reduction (row mode). Each thread accumulates its launches;
+  // a run that ends inside the thread goes to its LDS row (the first one of
+  // them still lacks the part from earlier threads, added after the scan).
+  // The thread's last run is scanned across the lanes.
+  PartRow *wst = stage[w];
+  Acc inc;
+  acc_zero(inc);
+  if (rowmode) {
+    uint32_t gk = g[0];
+#pragma unroll 1
+    for (int k = 0; k < nv; ++k) {
+      if (k > 0 && ((hm >> k) & 1u)) {
+        acc_store(wst + hb + __popc(hm & ((1u << k) - 1u)) - 1u, inc, gk);
+        acc_zero(inc);
+      }
+      acc_launch(inc, in, in.match[ib + k], in.dur[ib + k], mx, dw);
+      gk = pick(g, k);
+    }
+    const unsigned long long hl = __ballot(hm != 0) | 1ull;
+    const unsigned long long upto = ln == 63 ? ~0ull : ((2ull << ln) - 1);
+    const int sl = 63 - __clzll(hl & upto);
+#pragma unroll
+    for (int o = 1; o < OPA_WAVE; o <<= 1) acc_scan_step(inc, o, ln - o >= sl, mx);
+    // the lane's last run: ends here, or continues into the next lane and
+    // (if it ends inside that lane) completes the row that lane left
+    const uint32_t nvn = __shfl_down((uint32_t)nv, 1, OPA_WAVE);
+    const uint32_t hmn = __shfl_down(hm, 1, OPA_WAVE);
+    if (nv > 0) {
+      PartRow *r = wst + hb + nh - 1u;
+      if (ln == OPA_WAVE - 1 || nvn == 0 || (hmn & 1u)) acc_store(r, inc, g[nv - 1]);
+      else if (hmn & 0xFEu) row_add(r, inc, mx);
+    }
+  }
+
+  // ---- block offsets
+  if (w == 0) {
+    uint32_t pi = 0, pr = 0;
+    bool ok = true;
+    if (bid > 0) ok = lookback(a.em.state, bid, pi, pr);
+    if (ln == 0) {
+      if (bid > 0) lb_store(a.em.state + bid, lb_pack(kLbInc, pi + bi, pr + br));
+      spre[0] = pi;
+      spre[1] = pr;
+      if (!ok) sfail = 1;
+      if (bid == a.em.nblocks - 1) {
+        a.em.meta[0] = (int64_t)pi + bi;
+        a.em.meta[1] = (int64_t)pr + br;
+      }
+    }
+  }
+  __syncthreads();
+  const uint32_t ibase = spre[0] + wi, rbase = spre[1] + wr;
+
+  if (rowmode) {
+    // coalesced copy of the wave's rows, then one item per row
+    const unsigned long long *src = reinterpret_cast<const unsigned long long *>(wst);
+    unsigned long long *dst = reinterpret_cast<unsigned long long *>(a.em.rows + rbase);
+    const uint32_t nw = nr_w * (uint32_t)(sizeof(PartRow) / 8);
+    for (uint32_t x = ln; x < nw; x += OPA_WAVE) dst[x] = src[x];
+    if ((uint32_t)ln < nr_w) {
+      a.em.ig[ibase + ln] = wst[ln].g;
+      a.em.ia[ibase + ln] = rbase + ln;
+      a.em.ib[ibase + ln] = 0;
+    }
+  } else {
+    // references: every piece start writes (row, first launch, length)
+    const uint32_t hpn = __shfl_down(hp, 1, OPA_WAVE);
+    const uint32_t nvn = __shfl_down((uint32_t)nv, 1, OPA_WAVE);
+    const uint32_t spill = ln < OPA_WAVE - 1 ? (hpn ? (uint32_t)__ffs(hpn) - 1u : nvn) : 0u;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
-      const uint32_t prev = k ? g[k - 1] : (ln ? gl : 0xFFFFFFFFu);
-      if (k < nv && g[k] != prev) hm |= 1u << k;
-    }
-    // pieces for references: runs cut at every 16th launch as well
-    const uint32_t hp = hm | ((nv > 0 && (ln & 1) == 0) ? 1u : 0u);
-    const uint32_t nh = __popc(hm), nhp = __popc(hp);
-    const uint32_t hb = wave_incl_scan_add(nh) - nh;
-    const uint32_t hpb = wave_incl_scan_add(nhp) - nhp;
-    const uint32_t nr_w = __shfl(hb + nh, OPA_WAVE - 1, OPA_WAVE);
-    const uint32_t np_w = __shfl(hpb + nhp, OPA_WAVE - 1, OPA_WAVE);
-    const bool rowmode = nr_w <= (uint32_t)kRowCap;
-    if (ln == 0) {
-      wcnt[0][w] = rowmode ? nr_w : np_w;
-      wcnt[1][w] = rowmode ? nr_w : 0u;
-    }
-    int32_t mt[kPer];
-    uint32_t du[kPer];
-    load_run(in.match, ib, nv, mt);
-    load_run(in.dur, ib, nv, du);
-#pragma unroll
-    for (int k = 0; k < kPer; ++k)
-      if (k < nv && (mt[k] < -1 || (int64_t)mt[k] >= in.P)) bad++;  // aggregates as unmatched
-    __syncthreads();
-    uint32_t bi = 0, br = 0, wi = 0, wr = 0;
-    for (int k = 0; k < kEncThreads / OPA_WAVE; ++k) {
-      if (k < w) {
-        wi += wcnt[0][k];
-        wr += wcnt[1][k];
-      }
-      bi += wcnt[0][k];
-      br += wcnt[1][k];
-    }
-    if (tid == 0) lb_store(a.em.state + bid, lb_pack(bid == 0 ? kLbInc : kLbAgg, bi, br));
-
-    // ---- in-place reduction (row mode): suffix of each thread, then a
-    // segmented scan over the lanes (a lane with a run start begins a segment)
-    Acc inc;
-    acc_zero(inc);
-    if (rowmode) {
-#pragma unroll
-      for (int k = 0; k < kPer; ++k) {
-        if (k >= nv) continue;
-        if (k > 0 && ((hm >> k) & 1u)) acc_zero(inc);
-        acc_launch(inc, in, mt[k], du[k]);
-      }
-      const unsigned long long hl = __ballot(hm != 0) | 1ull;
-      const unsigned long long upto = ln == 63 ? ~0ull : ((2ull << ln) - 1);
-      const int sl = 63 - __clzll(hl & upto);
-#pragma unroll
-      for (int o = 1; o < OPA_WAVE; o <<= 1) {
-        const Acc y = acc_shfl_up(inc, o);
-        if (ln - o >= sl) {
-          Acc t = y;
-          acc_merge(t, inc, in.maxmask);
-          inc = t;
-        }
-      }
-    }
-
-    // ---- block offsets
-    if (w == 0) {
-      uint32_t pi = 0, pr = 0;
-      bool ok = true;
-      if (bid > 0) ok = lookback(a.em.state, bid, pi, pr);
-      if (ln == 0) {
-        if (bid > 0) lb_store(a.em.state + bid, lb_pack(kLbInc, pi + bi, pr + br));
-        spre[0] = pi;
-        spre[1] = pr;
-        if (!ok) sfail = 1;
-        if (bid == a.em.nblocks - 1) {
-          a.em.meta[0] = (int64_t)pi + bi;
-          a.em.meta[1] = (int64_t)pr + br;
-        }
-      }
-    }
-    __syncthreads();
-    const uint32_t ibase = spre[0] + wi, rbase = spre[1] + wr;
-
-    if (rowmode) {
-      const uint32_t nvn = __shfl_down((uint32_t)nv, 1, OPA_WAVE);
-      const uint32_t h0n = __shfl_down(hm & 1u, 1, OPA_WAVE);
-      // the run that enters this lane (for lanes whose first launch continues it)
-      Acc run = acc_shfl_up(inc, 1);
-      if ((hm & 1u) || ln == 0) acc_zero(run);
-      if (hm & 0xFEu) {
-        // runs that end inside the lane: recompute its launches before the
-        // last run start, emitting at every start
-        const int last = 31 - __clz(hm);
-        for (int k = 0; k < kPer; ++k) {
-          if (k > last) break;
-          if (k > 0 && ((hm >> k) & 1u)) {
-            const uint32_t idx = hb + __popc(hm & ((1u << k) - 1u)) - 1u;
-            acc_store(a.em.rows + rbase + idx, run, g[k - 1]);
-            a.em.ig[ibase + idx] = g[k - 1];
-            a.em.ia[ibase + idx] = rbase + idx;
-            a.em.ib[ibase + idx] = 0;
-            acc_zero(run);
-          }
-          if (k < last) acc_launch(run, in, mt[k], du[k]);
-        }
-      }
-      // the run through the lane's last launch ends here when the next lane
-      // starts a run or has no launches
-      if (nv > 0 && (ln == OPA_WAVE - 1 || nvn == 0 || h0n)) {
-        const uint32_t idx = hb + nh - 1u;
-        acc_store(a.em.rows + rbase + idx, inc, g[nv - 1]);
-        a.em.ig[ibase + idx] = g[nv - 1];
-        a.em.ia[ibase + idx] = rbase + idx;
-        a.em.ib[ibase + idx] = 0;
-      }
-    } else {
-      // references: every piece start writes (row, first launch, length)
-      const uint32_t hpn = __shfl_down(hp, 1, OPA_WAVE);
-      const uint32_t nvn = __shfl_down((uint32_t)nv, 1, OPA_WAVE);
-      const uint32_t spill = ln < OPA_WAVE - 1 ? (hpn ? (uint32_t)__ffs(hpn) - 1u : nvn) : 0u;
-#pragma unroll
-      for (int k = 0; k < kPer; ++k) {
-        if (!((hp >> k) & 1u)) continue;
-        const uint32_t rest = hp >> (k + 1);
-        const uint32_t len = rest ? (uint32_t)__ffs(rest) : (uint32_t)(nv - k) + spill;
-        const uint32_t idx = hpb + __popc(hp & ((1u << k) - 1u));
-        a.em.ig[ibase + idx] = g[k];
-        a.em.ia[ibase + idx] = (uint32_t)(ib + k);
-        a.em.ib[ibase + idx] = len;
-      }
+      if (!((hp >> k) & 1u)) continue;
+      const uint32_t rest = hp >> (k + 1);
+      const uint32_t len = rest ? (uint32_t)__ffs(rest) : (uint32_t)(nv - k) + spill;
+      const uint32_t idx = hpb + __popc(hp & ((1u << k) - 1u));
+      a.em.ig[ibase + idx] = g[k];
+      a.em.ia[ibase + idx] = (uint32_t)(ib + k);
+      a.em.ib[ibase + idx] = len;
     }
   }
   if (bad) atomicAdd(&sbad, bad);
@@ -438,25 +458,30 @@ void run_enclose_aggregate(const EncArgs &x, hipStream_t s) {
   a.rblk = at<int64_t>(x.ws, pl.rblk);
   a.ree = at<int64_t>(x.ws, pl.ree);
   a.npg = at<int32_t>(x.ws, pl.npg);
-  if (x.mode == kAggregateOnly) {
-    a.R_in = x.r ? x.r->n : 0;
-    a.op_in = x.r ? x.r->op_id : nullptr;
+  // the aggregation reads range ids by input range index
+  a.R_in = x.r ? x.r->n : 0;
+  a.op_in = x.r ? x.r->op_id : nullptr;
+  const unsigned nb = (unsigned)pl.nencb;
+  if (x.mode & 1) {
+    probe_begin(OPATTR_PROBE_MAIN_PASS, s);
+    if (pl.T > 0) k_enclose<<<nb, kEncThreads, 0, s>>>(a);
+    probe_end(OPATTR_PROBE_MAIN_PASS, s);
   }
   if (x.mode & 2) {
     a.ag = agg_inputs(x);
     a.em = emit_out(x.ws, pl);
     // look-back states and the start counter, cleared by a kernel (graph-safe)
     fill_u32(reinterpret_cast<uint32_t *>(a.em.state), 0, 2 * (pl.nencb + 1), s);
+    probe_begin(OPATTR_PROBE_AGG_RUNS, s);
+    if (pl.T > 0) {
+      if (a.ag.maxmask == kDefMaxMask && a.ag.dwmask == kDefDwMask)
+        k_agg_runs<true><<<nb, kEncThreads, 0, s>>>(a);
+      else
+        k_agg_runs<false><<<nb, kEncThreads, 0, s>>>(a);
+    }
+    probe_end(OPATTR_PROBE_AGG_RUNS, s);
+    run_aggregate(x, s);
   }
-  const unsigned nb = (unsigned)pl.nencb;
-  probe_begin(OPATTR_PROBE_MAIN_PASS, s);
-  if (pl.T > 0) {
-    if (x.mode == kEncloseOnly) k_enc<1><<<nb, kEncThreads, 0, s>>>(a);
-    else if (x.mode == kAggregateOnly) k_enc<2><<<nb, kEncThreads, 0, s>>>(a);
-    else k_enc<3><<<nb, kEncThreads, 0, s>>>(a);
-  }
-  probe_end(OPATTR_PROBE_MAIN_PASS, s);
-  if (x.mode & 2) run_aggregate(x, s);
 }
 
 }  // namespace opa

@@ -14,6 +14,11 @@ constexpr int kEncThreads = 256;    // threads per enclose/aggregate block
 constexpr int kEncSpan = 2048;      // launches per enclose/aggregate block
 constexpr int kEncRowsPerWave = 32; // runs a wave of that block reduces in place
 constexpr int kEncWindow = 2048;    // range starts staged in LDS per block
+// Default aggregation kinds (counter appendix table) as bit masks over the
+// counters: MAX for the two per-kernel constants, SUM for the six additive
+// counts (neither mask), DW-mean otherwise.
+constexpr uint32_t kDefMaxMask = (1u << 17) | (1u << 19);
+constexpr uint32_t kDefDwMask = 0x1BBF8u;
 // Key counts ranked with per-wave LDS counters (8 bytes of LDS per key); the
 // seq-tile kernels also hold a 16 KB partition array, hence a lower limit.
 constexpr uint32_t kFastKeys = 6144;

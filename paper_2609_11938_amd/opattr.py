@@ -69,7 +69,7 @@ EXPORTS = ("opattr_workspace_bytes", "opattr_diag_clear", "opattr_read_diag", "o
            "opattr_dedup_broadcast", "opattr_enclose", "opattr_aggregate", "opattr_attribute",
            "opattr_set_probe_events", "opattr_strerror")
 PROBES = ("seq_view", "tl_hist", "pf_hist", "col_scan", "pf_slot", "tl_match", "dedup",
-          "ranges", "main_pass", "finalize", "aggregate")
+          "ranges", "main_pass", "finalize", "aggregate", "agg_runs")
 
 _lib = None
 
