@@ -27,7 +27,8 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
 
 def algorithmic_bytes(tr):
     """Compulsory bytes: every input read once, every output written once, at
-    the ABI widths (duplicate counter rows reused by dedup count once)."""
+    the ABI widths (duplicate counter rows reused by dedup count once).
+    Returns the step total and, per single-kernel probe, that kernel's bytes."""
     T, P, R = tr["seq"].size, tr["pf_name"].size, tr["r_start"].size
     part = 4 if tr.get("part_id") is not None else 0
     G = tr["n_ops"] + 1
@@ -38,23 +39,82 @@ def algorithmic_bytes(tr):
     outputs = T * (4 + 4)                           # match, range_id
     table = G * 192 + 4 * NP                        # op rows + class map
     per_kernel = {
-        # enclosure pass: stream, query in, range_id out; range starts, ends,
-        # parents and ops
-        "main_pass": T * (2 + 8 + 4) + R * (8 + 8 + 4 + 4),
-        # aggregation: dur and match of every launch, each profiled row once,
-        # the operator rows out
-        "aggregate": T * (4 + 4) + P * 80 + G * 192,
-        # per-tile rank and join: seq view, name, part in; match out
-        "tl_match": T * (4 + 4 + part + 4),
-        # per-tile histograms: seq view, name, part in
-        "tl_hist": T * (4 + 4 + part),
-        "dedup": T * (4 + 4 + part) + T * 4,
+        # k_seqview_dense: seq in, launch-order view out
         "seq_view": T * (4 + 4),
+        # k_tl_hist_w: view, name, partition in
+        "tl_hist": T * (4 + 4 + part),
+        # k_pf_hist_w: row names in
         "pf_hist": P * 4,
+        # k_pf_slot_w: row names in, slot table out
         "pf_slot": P * (4 + 4),
-        "ranges": R * (8 + 8 + 2 + 4) + R * (8 + 4 + 8),
+        # k_tl_match_w: view, name, partition in; match out
+        "tl_match": T * (4 + 4 + part + 4),
+        # k_dedup: partition, name, seq in; match out
+        "dedup": T * (4 + 4 + 4 + 4),
+        # k_enclose: stream, query point in, range id out; range starts, ends
+        # and parents
+        "main_pass": T * (2 + 8 + 4) + R * (8 + 8 + 4),
+        # k_agg_runs: range id, match, duration of every launch, each range's
+        # op id and each profiled counter row once
+        "agg_runs": T * (4 + 4 + 4) + R * 4 + P * 80,
     }
     return timeline + profiled + ranges + outputs + table, per_kernel
+
+
+# kernel behind each single-kernel probe (for the rocprofv3 cross-check)
+PROBE_KERNEL = {"seq_view": "k_seqview_dense", "tl_hist": "k_tl_hist_w",
+                "pf_hist": "k_pf_hist_w", "pf_slot": "k_pf_slot_w",
+                "tl_match": "k_tl_match_w", "dedup": "k_dedup",
+                "main_pass": "k_enclose", "agg_runs": "k_agg_runs"}
+
+
+def source_hash():
+    """Hash of the HIP sources: stored traffic counters are valid only for the
+    kernels they were taken on."""
+    import glob
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2609_11938_amd", "csrc", "*"))) + \
+            [os.path.join(ROOT, "include", "opattr.h")]:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(kernel, config, emission):
+    """HBM bytes per launch of `kernel` from profiles/traffic_<kernel>_<config>_<emission>.txt
+    (two rocprofv3 --pmc passes, FETCH_SIZE then WRITE_SIZE, scaled by a plain
+    copy of known size), or None when absent or taken on other sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{config}_{emission}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_hash") != source_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(mb, reps):
+    """A plain device-to-device copy of `mb` MiB, `reps` times: the reference
+    the FETCH_SIZE / WRITE_SIZE counters are scaled by."""
+    import torch
+
+    n = mb * (1 << 20) // 4
+    a = torch.arange(n, dtype=torch.int32, device="cuda:0")
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n * 4, "reps": reps}), flush=True)
 
 
 def cpu_baseline(tr, reps=2):
@@ -82,6 +142,8 @@ def main():
                     choices=["stream_major", "seq", "shuffled"])
     ap.add_argument("--validate", action="store_true", help="also check the layout hints")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
@@ -90,10 +152,13 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     from paper_2609_11938_amd import opattr, tracegen
+
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration, max(1, args.steps))
+        return
 
     if not os.path.exists(opattr.LIB_PATH):
         import __graft_entry__
@@ -155,10 +220,13 @@ def main():
         d = [ev[k][2 * p].elapsed_time(ev[k][2 * p + 1]) for k in range(args.steps)]
         probe_ms[name] = statistics.mean(d)
     total_bytes, kbytes = algorithmic_bytes(tr)
-    dominant = max((n for n in probe_ms if n in kbytes), key=lambda n: probe_ms[n])
+    # the dominant single-kernel probe sets the roofline line
+    dominant = max(kbytes, key=lambda n: probe_ms[n])
     dom_ms = probe_ms[dominant]
     achieved = kbytes[dominant] / (dom_ms * 1e-3) / 1e9
     pipe_gbps = total_bytes / (ms_per_step * 1e-3) / 1e9
+    per_launch = stored_traffic(PROBE_KERNEL[dominant], args.config, args.emission)
+    traffic = per_launch * T if per_launch is not None else None
     print("probe ms/step: " + ", ".join(f"{n}={v:.4f}" for n, v in probe_ms.items()),
           file=sys.stderr, flush=True)
 
@@ -176,9 +244,9 @@ def main():
                    "profiled_rows": int(tr["pf_name"].size), "ops": tr["n_ops"],
                    "partitions": tr["n_parts"], "emission": args.emission,
                    "validate": bool(args.validate)},
-        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved,
+        "roofline": {"bound": "hbm", "kernel": PROBE_KERNEL[dominant], "achieved": achieved,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": None, "algorithmic_bytes": kbytes[dominant],
+                     "traffic": traffic, "algorithmic_bytes": kbytes[dominant],
                      "avg_ms": dom_ms},
         "pipeline": {"algorithmic_bytes": total_bytes, "achieved_GBps": pipe_gbps,
                      "frac_of_hbm_peak": pipe_gbps / HBM_PEAK_GBPS,

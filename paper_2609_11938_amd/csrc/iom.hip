@@ -52,13 +52,14 @@ void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, con
   if (T <= 0) return;
   int32_t *sv = at<int32_t>(ws, pl.sv);
   const unsigned nb = (unsigned)((T + 255) / 256);
-  probe_begin(OPATTR_PROBE_SEQ_VIEW, s);
   if (pl.seq_dense) {
     fill_u32(reinterpret_cast<uint32_t *>(sv), 0xFFFFFFFFu, T, s);
+    probe_begin(OPATTR_PROBE_SEQ_VIEW, s);
     k_seqview_dense<<<nb, 256, 0, s>>>(k->seq, T, sv, diag, validate ? 1 : 0);
     probe_end(OPATTR_PROBE_SEQ_VIEW, s);
     return;
   }
+  probe_begin(OPATTR_PROBE_SEQ_VIEW, s);
   uint64_t *k0 = at<uint64_t>(ws, pl.seqsort_k0), *k1 = at<uint64_t>(ws, pl.seqsort_k1);
   uint32_t *v0 = at<uint32_t>(ws, pl.seqsort_v0), *v1 = at<uint32_t>(ws, pl.seqsort_v1);
   launch_iota(v0, T, s);
