@@ -86,9 +86,10 @@ typedef struct {
    reordering pass. A false promise gives unspecified outputs (never an
    out-of-bounds access); with OPATTR_VALIDATE it is detected and reported as
    OPATTR_ERR_ORDER. Without hints every input order is accepted. */
-#define OPATTR_KERNELS_STREAM_MAJOR 1u /* kernels sorted by (stream_id, seq), and
-                                          per stream the query point does not
-                                          decrease with seq                        */
+#define OPATTR_KERNELS_STREAM_MAJOR 1u /* kernels sorted by (stream_id, seq), every
+                                          stream_id < n_streams, and per stream
+                                          the query point does not decrease with
+                                          seq                                      */
 #define OPATTR_SEQ_DENSE 2u            /* seq is a permutation of [0, n)          */
 #define OPATTR_RANGES_NESTED 4u        /* ranges sorted by (stream_id, start asc,
                                           end desc)                                */

@@ -34,6 +34,12 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.NP = d->n_parts;
   pl.seq_dense = (d->flags & OPATTR_SEQ_DENSE) != 0;
   pl.ranges_nested = (d->flags & OPATTR_RANGES_NESTED) != 0;
+  // seq tiles straight from per-stream segments: needs both kernel promises,
+  // a matching stage (profiled rows given) and few streams and names; under
+  // OPATTR_VALIDATE the general path runs (it checks what it relies on)
+  pl.seg = (d->flags & OPATTR_KERNELS_STREAM_MAJOR) && pl.seq_dense &&
+           !(d->flags & OPATTR_VALIDATE) && p != nullptr && pl.NS >= 1 &&
+           pl.NS <= 64 && pl.NN <= kFastNames;
   pl.nt = (pl.T + OPA_TILE - 1) / OPA_TILE;
   pl.ntp = (pl.P + OPA_TILE - 1) / OPA_TILE;
   pl.ncht = (pl.nt + kColChunk - 1) / kColChunk;
@@ -45,7 +51,9 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   const bool dd = has_dedup(k, d);
   const size_t T = (size_t)pl.T, P = (size_t)pl.P, R = (size_t)pl.R, NN = pl.NN;
   Bump b;
-  pl.sv = b.take(T * 4);
+  pl.sv = b.take(pl.seg ? 0 : T * 4);
+  pl.kblk = b.take(pl.seg ? ((size_t)pl.NS + 2) * 8 : 0);
+  pl.tbnd = b.take(pl.seg ? ((size_t)pl.nt + 1) * pl.NS * 4 : 0);
   pl.rk = b.take(pl.seq_dense ? 0 : T * 4);
   pl.seqsort_k0 = b.take(pl.seq_dense ? 0 : T * 8);
   pl.seqsort_k1 = b.take(pl.seq_dense ? 0 : T * 8);
@@ -62,9 +70,10 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.slot = b.take(P * 4);
   pl.pfirst = b.take(dd ? (size_t)pl.NP * 4 : 0);
   pl.plast = b.take(dd ? (size_t)pl.NP * 4 : 0);
-  pl.contig = b.take(dd ? (size_t)pl.NP : 0);
+  pl.pheads = b.take(dd ? (size_t)pl.NP * 4 : 0);
   pl.mbs = b.take(dd ? T * 4 : 0);
-  pl.nbs = b.take(dd ? T * 4 : 0);
+  pl.nbs = b.take(T * 4);  // dedup source names, or the fast path's keys by seq rank
+  pl.rit = b.take(T * 2);  // fast path: in-tile rank by seq rank
   const bool rs = !pl.ranges_nested;
   pl.rperm = b.take(rs ? R * 4 : 0);
   pl.rs_c = b.take(rs ? R * 8 : 0);
@@ -250,6 +259,7 @@ int opattr_match(const opattr_kernels *k, const opattr_profiled *p, const opattr
   const Plan pl = make_plan(k, p, nullptr, d);
   if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
+  check_kernel_layout(k, d, diag, s);
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
   build_seq_view(k, d, ws, pl, diag, validate, s);
   IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, false, validate};
@@ -266,9 +276,10 @@ int opattr_dedup_broadcast(const opattr_kernels *k, const opattr_dims *d, int32_
   const Plan pl = make_plan(k, nullptr, nullptr, d);
   if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
+  check_kernel_layout(k, d, diag, s);
   if (has_dedup(k, d)) {
     build_seq_view(k, d, ws, pl, diag, (d->flags & OPATTR_VALIDATE) != 0, s);
-    run_dedup(k, d, match, diag, ws, pl, false, s);
+    run_dedup(k, d, match, diag, ws, pl, s);
   }
   launch_finish(diag, nullptr, 0, s);
   return launch_status();
@@ -283,6 +294,7 @@ int opattr_enclose(const opattr_kernels *k, const opattr_ranges *r, const opattr
   const Plan pl = make_plan(k, nullptr, r, d);
   if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
+  check_kernel_layout(k, d, diag, s);
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
   const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s);
   resolve_ranges(cr, d, ws, pl, range_depth, diag, s);
@@ -318,6 +330,7 @@ int opattr_aggregate(const opattr_kernels *k, const opattr_profiled *p, const in
   const Plan pl = make_plan(k, p, r, d);
   if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
+  check_kernel_layout(k, d, diag, s);
   EncArgs e{};
   e.mode = kAggregateOnly;
   e.k = k;
@@ -349,11 +362,11 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   const Plan pl = make_plan(k, p, r, d);
   if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
+  check_kernel_layout(k, d, diag, s);
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
   build_seq_view(k, d, ws, pl, diag, validate, s);
   IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, validate};
   run_match(a, s);
-  run_dedup(k, d, match, diag, ws, pl, true, s);
   probe_begin(OPATTR_PROBE_RANGES, s);
   const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s);
   resolve_ranges(cr, d, ws, pl, range_depth, diag, s);

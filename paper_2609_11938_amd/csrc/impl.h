@@ -33,11 +33,12 @@ struct Plan {
   uint32_t NN, NS, G, NP;
   int64_t nt, ntp, ncht, nchp, ntr_max, nencb, ntrt, nchr;
   bool seq_dense, ranges_nested;
+  bool seg;  // seq tiles read from per-stream segments (kernels stream-major, seq dense)
   size_t total;
   // IOM
-  size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist;
+  size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist, kblk, tbnd;
   size_t tlh, pfh, tlch, pfch, tlc, pfc, off, slot;
-  size_t pfirst, plast, contig, mbs, nbs;
+  size_t pfirst, plast, pheads, mbs, nbs, rit;
   // ranges
   size_t rperm, rs_c, re_c, rst_c, rop_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
@@ -128,8 +129,16 @@ struct IomArgs {
 void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, const Plan &pl,
                     opattr_diag *diag, bool validate, hipStream_t s);
 void run_match(const IomArgs &a, hipStream_t s);
+// OPATTR_VALIDATE: check the kernels' stream-major promise (if given)
+void check_kernel_layout(const opattr_kernels *k, const opattr_dims *d, opattr_diag *diag,
+                         hipStream_t s);
+// blk[s] = first index with st[i] >= s, s in [0, NS] (st sorted)
+void launch_stream_blocks(const uint16_t *st, int64_t n, uint32_t NS, int64_t *blk,
+                          hipStream_t s);
+// Standalone dedup broadcast over a given match array (run_match already
+// broadcasts when IomArgs::want_dedup is set).
 void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, opattr_diag *diag,
-               void *ws, const Plan &pl, bool stats_ready, hipStream_t s);
+               void *ws, const Plan &pl, hipStream_t s);
 
 // ---- ranges and enclosure (ranges.hip, enclose.hip) ----------------------------
 CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws, const Plan &pl,

@@ -4,18 +4,31 @@
 // i-th profiled row of that name. Written data-parallel: the rank of a launch
 // among the eligible launches of its name (in seq order) is
 //     rank = (launches of the name in earlier seq tiles) + (rank inside the tile)
-// and the row is slot[off[name] + rank] when rank < rows(name). Tiles of 4096
-// launches in seq order are sorted by name in LDS (stable, so the in-tile rank
-// is the distance to the start of the name's run); per-tile name histograms
-// are scanned down the columns for the cross-tile part. The profiled side is
-// ranked the same way (tiles in replay order) to build the slot table.
+// and the row is slot[off[name] + rank] when rank < rows(name). Seq tiles hold
+// 4096 launches; per-tile name histograms are scanned down the columns for the
+// cross-tile part. The profiled side is ranked the same way (tiles in replay
+// order) to build the slot table.
+//
+// Fast path (at most 4096 names): a histogram kernel ranks every tile once
+// with per-wave LDS counters and leaves each launch's in-tile rank and key by
+// seq position; a lookup kernel then gives eligible launches their row and
+// duplicates the row of the representative's launch at the same position of
+// the representative partition. With more names an LDS radix sort ranks the
+// tiles and a separate kernel broadcasts to duplicates.
+//
+// Seq tiles are read through a launch-order view (sv[seq] = input index), or,
+// when the kernels are promised stream-major with dense seq, straight from one
+// storage segment per stream (no view is built).
 #include "common.h"
 #include "impl.h"
 
 namespace opa {
 
+constexpr int kWaveChunks = OPA_TILE / OPA_TILE_THREADS;  // 16 chunks of 64 per wave
+constexpr int kMaxSegStreams = OPA_WAVE;
+
 // ---------------------------------------------------------------------------
-// seq view: sv[rank] = input index of the launch with that rank in seq order
+// launch-order view: sv[rank] = input index of the launch with that rank
 // ---------------------------------------------------------------------------
 __global__ void k_seqview_dense(const uint32_t *__restrict__ seq, int64_t T, int32_t *sv,
                                 opattr_diag *diag, int validate) {
@@ -49,7 +62,7 @@ __global__ void k_seqview_sorted(const uint64_t *__restrict__ keys, const uint32
 void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, const Plan &pl,
                     opattr_diag *diag, bool validate, hipStream_t s) {
   const int64_t T = pl.T;
-  if (T <= 0) return;
+  if (T <= 0 || pl.seg) return;  // the segment path reads tiles without the view
   int32_t *sv = at<int32_t>(ws, pl.sv);
   const unsigned nb = (unsigned)((T + 255) / 256);
   if (pl.seq_dense) {
@@ -71,7 +84,7 @@ void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, con
 }
 
 // ---------------------------------------------------------------------------
-// tile loading
+// tile elements
 // ---------------------------------------------------------------------------
 struct TlArgs {
   const int32_t *sv;
@@ -80,37 +93,416 @@ struct TlArgs {
   const int32_t *part;      // NULL when dedup is off
   const int32_t *part_rep;  // NULL when dedup is off
   uint32_t NN, NP;
+  // segment path
+  const uint32_t *seq;
+  const uint32_t *bnd;  // [tiles + 1][NS]
+  const int64_t *kblk;  // [NS + 1]
+  uint32_t NS;
 };
 
-// Fill A[l] with (name << 12 | l) for launches eligible for replay, and
-// (NN << 12 | l) otherwise, for the launches of seq ranks base..base+4095.
-// lpart[l]: partition of a valid launch (-1 none), -2 for holes and bad ids.
-// Returns the number of launches with an id out of range.
-__device__ inline uint32_t tl_tile_keys(const TlArgs &a, int64_t base, uint32_t *A, int32_t *lpart,
-                                        int32_t *jidx) {
+// Element e of a tile sits in wave e / 1024, chunk (e / 64) % 16, lane e % 64.
+__device__ __forceinline__ int tile_elem(int c) {
+  return wave_id() * (OPA_TILE / 4) + c * OPA_WAVE + lane_id();
+}
+
+// Ranking key of launch j (its name if eligible for replay -- no partition,
+// or a partition that is its own class representative -- else NN) and
+// partition (-1 none, -2 bad id). Returns 1 if an id is out of range.
+__device__ __forceinline__ uint32_t tl_classify(const TlArgs &a, int64_t j, uint32_t &key,
+                                                int32_t &lp) {
+  key = a.NN;
+  lp = -2;
+  const uint32_t nm = a.name[j];
+  const int32_t pt = a.part ? a.part[j] : -1;
+  if (nm >= a.NN || pt < -1 || (pt >= 0 && (uint32_t)pt >= a.NP)) return 1;
+  if (pt < 0 || a.part_rep[pt] == pt) key = nm;
+  lp = pt;
+  return 0;
+}
+
+// The launch of seq rank x through the view: input index j (-1 for holes),
+// key and partition as above (NN and -2 for holes).
+__device__ __forceinline__ uint32_t tl_load(const TlArgs &a, int64_t x, uint32_t &key, int32_t &j,
+                                            int32_t &lp) {
+  j = (x >= 0 && x < a.T) ? a.sv[x] : -1;
+  key = a.NN;
+  lp = -2;
+  if (j < 0) return 0;
+  return tl_classify(a, j, key, lp);
+}
+
+__device__ __forceinline__ int32_t tl_lp(const TlArgs &a, int64_t x) {
+  uint32_t k;
+  int32_t j, lp;
+  tl_load(a, x, k, j, lp);
+  return lp;
+}
+
+// Segment table of a seq tile (segment path) and the partitions of the
+// launches just before and after the tile.
+struct SegTable {
+  uint32_t lo[kMaxSegStreams], pre[kMaxSegStreams + 1];
+  int32_t edge[2];
+};
+
+// One seq tile in LDS, by position in the tile.
+struct TileData {
+  uint16_t key[OPA_TILE];  // ranking key (NN: not eligible, or no launch)
+  int32_t lp[OPA_TILE];    // partition (-1 none, -2 no launch or bad id)
+  SegTable sg;
+  uint32_t bad;
+};
+
+// Fill TileData for seq tile t through the view. Ends with a barrier;
+// returns this thread's bad-id count.
+__device__ inline uint32_t view_tile(const TlArgs &a, int64_t t, TileData &sm) {
+  const int64_t base = t * OPA_TILE;
+  uint32_t bad = 0;
+#pragma unroll 4
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const int e = c * OPA_TILE_THREADS + threadIdx.x;
+    uint32_t key;
+    int32_t j, lp;
+    bad += tl_load(a, base + e, key, j, lp);
+    sm.key[e] = (uint16_t)key;
+    sm.lp[e] = lp;
+  }
+  if (threadIdx.x == 0) {
+    sm.sg.edge[0] = tl_lp(a, base - 1);
+    sm.sg.edge[1] = tl_lp(a, base + OPA_TILE);
+  }
+  __syncthreads();
+  return bad;
+}
+
+// ---------------------------------------------------------------------------
+// Segment path (kernels stream-major, seq dense): seq tile t holds, for every
+// stream s, the storage range [bnd[t][s], bnd[t+1][s]) -- the launches of s
+// whose seq falls in the tile -- so a tile is read with coalesced loads and no
+// launch-order view is built. Every bound is clamped, so a broken promise
+// gives wrong tiles, never an access out of bounds.
+// ---------------------------------------------------------------------------
+
+// bnd[t * NS + s] = first launch of stream s with seq >= t * 4096, t in [0, nt]
+__global__ void k_tile_bounds(const uint32_t *__restrict__ seq, const int64_t *__restrict__ kblk,
+                              uint32_t NS, int64_t nt, uint32_t *bnd) {
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= (nt + 1) * NS) return;
+  const int64_t t = id / NS;
+  const uint32_t s = (uint32_t)(id - t * NS);
+  int64_t lo = kblk[s], hi = kblk[s + 1];
+  const uint64_t x = (uint64_t)t * OPA_TILE;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if ((uint64_t)seq[mid] < x) lo = mid + 1;
+    else hi = mid;
+  }
+  bnd[id] = (uint32_t)lo;
+}
+
+// Segment table of tile t in sm.lo / sm.pre (wave 0) and, with edges set,
+// the partitions of the launches with seq base - 1 (wave 1) and base + 4096
+// (wave 2). The caller synchronises.
+__device__ inline void seg_table(const TlArgs &a, int64_t t, SegTable &sm, bool edges) {
+  const int ln = lane_id(), w = wave_id();
+  const int64_t base = t * OPA_TILE;
+  const uint64_t T = (uint64_t)a.T;
+  if (w == 0) {
+    uint32_t lo = 0, len = 0;
+    if ((uint32_t)ln < a.NS) {
+      uint64_t l = a.bnd[t * a.NS + ln], h = a.bnd[(t + 1) * a.NS + ln];
+      l = l < T ? l : T;
+      h = h < T ? h : T;
+      lo = (uint32_t)l;
+      len = h > l ? (uint32_t)(h - l) : 0u;
+      len = len < OPA_TILE ? len : OPA_TILE;
+    }
+    const uint32_t inc = wave_incl_scan_add(len);
+    sm.lo[ln] = lo;
+    sm.pre[ln] = inc - len;
+    if (ln == OPA_WAVE - 1) sm.pre[OPA_WAVE] = inc;
+  } else if (edges && (w == 1 || w == 2)) {
+    // the launch with seq base - 1 is the last one before some stream's
+    // segment; the one with base + 4096 the first one after
+    const int side = w - 1;
+    const uint64_t want = side ? (uint64_t)base + OPA_TILE : (uint64_t)base - 1;
+    int64_t c = -1;
+    if ((uint32_t)ln < a.NS && (side ? want < T : base > 0)) {
+      const int64_t b = a.bnd[(t + side) * a.NS + ln];
+      const int64_t s0 = a.kblk[ln], s1 = a.kblk[ln + 1];
+      c = side ? b : b - 1;
+      if (c < s0 || c >= s1 || c < 0 || (uint64_t)c >= T || (uint64_t)a.seq[c] != want) c = -1;
+    }
+    const uint64_t m = __ballot(c >= 0);
+    const int src = m ? __ffsll((unsigned long long)m) - 1 : 0;
+    const int64_t cj = __shfl(c, src, OPA_WAVE);
+    int32_t lp = -2;
+    if (cj >= 0) {
+      uint32_t k;
+      tl_classify(a, cj, k, lp);
+    }
+    if (ln == 0) sm.edge[side] = lp;
+  }
+}
+
+// Input index of the launch at position e of tile t's segment order (or -1).
+__device__ __forceinline__ int64_t seg_elem(const SegTable &sm, uint32_t e, int64_t T) {
+  const uint32_t total = sm.pre[OPA_WAVE] < OPA_TILE ? sm.pre[OPA_WAVE] : OPA_TILE;
+  if (e >= total) return -1;
+  int lo = 0, hi = OPA_WAVE;  // last segment with pre <= e
+#pragma unroll
+  for (int st = 0; st < 6; ++st) {
+    const int mid = (lo + hi) >> 1;
+    if (sm.pre[mid] <= e) lo = mid;
+    else hi = mid;
+  }
+  const int64_t i = (int64_t)sm.lo[lo] + (e - sm.pre[lo]);
+  return i < T ? i : -1;
+}
+
+// Fill TileData for seq tile t from its segments. Ends with a barrier.
+__device__ inline uint32_t seg_tile(const TlArgs &a, int64_t t, TileData &sm) {
+  const int tid = threadIdx.x;
+  const int64_t base = t * OPA_TILE;
+  for (int x = tid; x < OPA_TILE; x += OPA_TILE_THREADS) {
+    sm.key[x] = (uint16_t)a.NN;
+    sm.lp[x] = -2;
+  }
+  seg_table(a, t, sm.sg, true);
+  __syncthreads();
+  // element e = c * 256 + tid: a fixed, unrolled count so that the loads of
+  // all chunks are in flight together
+  int64_t ii[kWaveChunks];
+  uint32_t sq[kWaveChunks];
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c)
+    ii[c] = seg_elem(sm.sg, (uint32_t)(c * OPA_TILE_THREADS + tid), a.T);
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) sq[c] = ii[c] >= 0 ? a.seq[ii[c]] : 0u;
+  uint32_t bad = 0;
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    if (ii[c] < 0) continue;
+    const int64_t x = (int64_t)sq[c] - base;
+    if (x < 0 || x >= OPA_TILE || base + x >= a.T) continue;  // a broken promise: left out
+    uint32_t key;
+    int32_t lp;
+    bad += tl_classify(a, ii[c], key, lp);
+    sm.key[x] = (uint16_t)key;
+    sm.lp[x] = lp;
+  }
+  __syncthreads();
+  return bad;
+}
+
+// ---------------------------------------------------------------------------
+// Partition edges. A head (first launch of a maximal run of one partition in
+// seq order) stores its rank in pfirst and counts itself in pheads, a tail
+// stores its rank in plast. A partition is one contiguous run exactly when it
+// has one head, and then [pfirst, plast] is that run.
+// ---------------------------------------------------------------------------
+__device__ inline void part_edges(const int32_t *lpart, int64_t base, int32_t lp_before,
+                                  int32_t lp_after, uint32_t *pfirst, uint32_t *plast,
+                                  uint32_t *pheads) {
+  for (int e = threadIdx.x; e < OPA_TILE; e += OPA_TILE_THREADS) {
+    const int32_t lp = lpart[e];
+    if (lp < 0) continue;
+    const int64_t x = base + e;
+    const int32_t prev = e > 0 ? lpart[e - 1] : lp_before;
+    const int32_t next = e < OPA_TILE - 1 ? lpart[e + 1] : lp_after;
+    if (prev != lp) {
+      pfirst[lp] = (uint32_t)x;
+      atomicAdd(&pheads[lp], 1u);
+    }
+    if (next != lp) plast[lp] = (uint32_t)x;
+  }
+}
+
+// partition edges of every seq tile on their own (view path)
+__global__ void __launch_bounds__(256) k_part_edges(TlArgs a, uint32_t *pfirst, uint32_t *plast,
+                                                    uint32_t *pheads) {
+  __shared__ TileData sm;
+  const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
+  view_tile(a, blockIdx.x, sm);
+  part_edges(sm.lp, base, sm.sg.edge[0], sm.sg.edge[1], pfirst, plast, pheads);
+}
+
+// PARTITION error for every partition seen in more than one run
+__global__ void k_part_flags(const uint32_t *__restrict__ pheads, uint32_t NP, opattr_diag *diag) {
+  const uint32_t q = blockIdx.x * blockDim.x + threadIdx.x;
+  const bool nc = q < NP && pheads[q] > 1;
+  if (__ballot(nc) && lane_id() == 0) atomicOr(&diag->flags, OPATTR_F_PARTITION);
+}
+
+// bad class-map entries are counted once, with the other bad ids of the match
+__global__ void k_rep_check(const int32_t *__restrict__ part_rep, uint32_t NP, opattr_diag *diag) {
+  const uint32_t q = blockIdx.x * blockDim.x + threadIdx.x;
+  const bool bad = q < NP && (part_rep[q] < 0 || (uint32_t)part_rep[q] >= NP);
+  const uint64_t m = __ballot(bad);
+  if (m && lane_id() == __ffsll((unsigned long long)m) - 1)
+    atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)__popcll(m));
+}
+
+#define OPA_DYN_LDS(T, name) extern __shared__ __align__(16) unsigned char name##_raw[]; \
+  T *name = reinterpret_cast<T *>(name##_raw)
+
+// ---------------------------------------------------------------------------
+// Fast path, histogram kernel: per seq tile, the per-name counts of eligible
+// launches (tlh row), each launch's in-tile rank (rit) and key (kbs) by seq
+// position, and the partition edges.
+// ---------------------------------------------------------------------------
+struct HistOut {
+  uint32_t *tlh;
+  uint16_t *rit;
+  uint32_t *kbs;
+  uint32_t *pfirst, *plast, *pheads;  // pheads NULL: no partitions
+  opattr_diag *diag;
+};
+
+template <bool SEG>
+__global__ void __launch_bounds__(256) k_tl_hist_w(TlArgs a, HistOut o) {
+  OPA_DYN_LDS(uint16_t, cnt);
+  __shared__ TileData sm;
+  const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
+  const uint32_t NN = a.NN;
+  for (uint32_t i = threadIdx.x; i < 4 * NN; i += OPA_TILE_THREADS) cnt[i] = 0;
+  if (threadIdx.x == 0) sm.bad = 0;
+  const uint32_t bad = SEG ? seg_tile(a, tile, sm) : view_tile(a, tile, sm);
+  uint32_t key[kWaveChunks], rank[kWaveChunks];
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) key[c] = sm.key[tile_elem(c)];
+  wave_rank<kWaveChunks>(key, NN, bits_for(NN), cnt + wave_id() * NN, rank);
+  block_rank_bases(cnt, NN, o.tlh + tile * NN);
+  const uint16_t *wb = cnt + wave_id() * NN;
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const int e = tile_elem(c);
+    if (base + e >= a.T) continue;
+    o.rit[base + e] = key[c] < NN ? (uint16_t)(wb[key[c]] + rank[c]) : (uint16_t)0;
+    o.kbs[base + e] = key[c];
+  }
+  if (o.pheads) part_edges(sm.lp, base, sm.sg.edge[0], sm.sg.edge[1], o.pfirst, o.plast, o.pheads);
+  if (bad) atomicAdd(&sm.bad, bad);
+  __syncthreads();
+  if (threadIdx.x == 0 && sm.bad)
+    atomicAdd((unsigned long long *)&o.diag->bad_records, (unsigned long long)sm.bad);
+}
+
+// ---------------------------------------------------------------------------
+// Fast path, lookup kernel: every launch of a seq tile gets its match.
+// Eligible: slot[off[n] + rank] with rank = (tile prefix) + (in-tile rank).
+// Duplicate (partition p with class representative r != p): the launch at
+// the same position of r, if both partitions are one run each and the names
+// agree, lends its rank (the rank decides the row, so the source's match need
+// not exist yet); otherwise -1 and a dedup error.
+// ---------------------------------------------------------------------------
+struct LookArgs {
+  const uint32_t *tlh;  // exclusive prefix of each name down the tiles
+  const uint32_t *tlc, *pfc, *off;
+  const int32_t *slot;
+  const uint16_t *rit;
+  const uint32_t *kbs;
+  const uint32_t *pfirst, *plast, *pheads;  // pheads NULL: no dedup broadcast
+  int32_t *match;
+  int skip_name;
+  opattr_diag *diag;
+};
+
+__device__ __forceinline__ int32_t row_of(const LookArgs &m, uint32_t NN, uint32_t n, uint32_t x) {
+  const uint32_t r = m.tlh[(int64_t)(x >> OPA_SLOT_BITS) * NN + n] + m.rit[x];
+  const uint32_t rows = m.pfc[n];
+  int32_t mt = r < rows ? m.slot[m.off[n] + r] : -1;
+  if (m.skip_name && m.tlc[n] != rows) mt = -1;
+  return mt;
+}
+
+template <bool SEG>
+__global__ void __launch_bounds__(256) k_tl_look(TlArgs a, LookArgs m) {
+  __shared__ SegTable sm;
+  __shared__ unsigned long long serr;
+  const int tid = threadIdx.x;
+  const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
+  const uint32_t NN = a.NN;
+  if (tid == 0) serr = 0;
+  if (SEG) seg_table(a, tile, sm, false);
+  __syncthreads();
+  // phase 1: input index and seq rank of each element
+  int64_t ii[kWaveChunks];
+  uint32_t xs[kWaveChunks];
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const uint32_t e = (uint32_t)(c * OPA_TILE_THREADS + tid);
+    if (SEG) ii[c] = seg_elem(sm, e, a.T);
+    else ii[c] = base + e < a.T ? a.sv[base + e] : -1;
+  }
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const uint32_t e = (uint32_t)(c * OPA_TILE_THREADS + tid);
+    xs[c] = SEG ? (ii[c] >= 0 ? a.seq[ii[c]] : 0u) : (uint32_t)(base + e);
+    if (SEG && (int64_t)xs[c] >= a.T) ii[c] = -1;  // a broken promise: left out
+  }
+  // phase 2: ids, class representative
+  uint32_t nm[kWaveChunks];
+  int32_t pt[kWaveChunks], rp[kWaveChunks];
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    nm[c] = ii[c] >= 0 ? a.name[ii[c]] : NN;
+    pt[c] = (ii[c] >= 0 && a.part) ? a.part[ii[c]] : -1;
+  }
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const bool good = nm[c] < NN && pt[c] >= -1 && (pt[c] < 0 || (uint32_t)pt[c] < a.NP);
+    rp[c] = -2;  // -2: neither eligible nor a duplicate
+    if (good) rp[c] = pt[c] < 0 ? pt[c] : a.part_rep[pt[c]];
+  }
+  // phase 3: the position whose rank gives the row (own, or the
+  // representative's launch at the same position)
+  uint32_t src[kWaveChunks];
+  uint32_t err = 0;
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    src[c] = 0xFFFFFFFFu;
+    if (ii[c] < 0 || rp[c] == -2) continue;
+    if (pt[c] < 0 || rp[c] == pt[c]) {
+      src[c] = xs[c];  // eligible
+    } else if (m.pheads && rp[c] >= 0 && (uint32_t)rp[c] < a.NP) {
+      const int32_t r = rp[c], p = pt[c];
+      const uint32_t f = m.pfirst[r];
+      bool ok = m.pheads[p] == 1u && m.pheads[r] == 1u && a.part_rep[r] == r && f != 0xFFFFFFFFu;
+      const uint32_t pos = xs[c] - m.pfirst[p];
+      ok = ok && pos < m.plast[r] - f + 1u;
+      ok = ok && m.kbs[f + pos] == nm[c];
+      if (ok) src[c] = f + pos;
+      else err++;
+    }
+  }
+  // phase 4: rows
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    if (ii[c] < 0) continue;
+    m.match[ii[c]] = src[c] != 0xFFFFFFFFu ? row_of(m, NN, nm[c], src[c]) : -1;
+  }
+  const unsigned long long e = wave_reduce_add((unsigned long long)err);
+  if (lane_id() == 0 && e) atomicAdd(&serr, e);
+  __syncthreads();
+  if (tid == 0 && serr) atomicAdd((unsigned long long *)&m.diag->dedup_errors, serr);
+}
+
+// ---------------------------------------------------------------------------
+// Radix path (more names than the LDS counters hold)
+// ---------------------------------------------------------------------------
+// A[l] = (key << 12 | l) for the launches of seq ranks base..base+4095
+// through the view; jidx[l] = input index (-1 holes). Returns bad-id count.
+__device__ inline uint32_t tl_tile_keys(const TlArgs &a, int64_t base, uint32_t *A, int32_t *jidx) {
   const int tid = threadIdx.x;
   uint32_t bad = 0;
 #pragma unroll 4
   for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
     const int l = c * OPA_TILE_THREADS + tid;
-    const int64_t x = base + l;
-    const int32_t j = x < a.T ? a.sv[x] : -1;
-    uint32_t key = (a.NN << OPA_SLOT_BITS) | (uint32_t)l;
-    int32_t lp = -2;
-    if (j >= 0) {
-      const uint32_t nm = a.name[j];
-      const int32_t pt = a.part ? a.part[j] : -1;
-      const bool good = nm < a.NN && pt >= -1 && (pt < 0 || (uint32_t)pt < a.NP);
-      if (!good) {
-        bad++;
-      } else {
-        const bool elig = pt < 0 || a.part_rep[pt] == pt;
-        if (elig) key = (nm << OPA_SLOT_BITS) | (uint32_t)l;
-        lp = pt;
-      }
-    }
-    A[l] = key;
-    if (lpart) lpart[l] = lp;
+    uint32_t key;
+    int32_t j, lp;
+    bad += tl_load(a, base + l, key, j, lp);
+    A[l] = (key << OPA_SLOT_BITS) | (uint32_t)l;
     if (jidx) jidx[l] = j;
   }
   return bad;
@@ -122,7 +514,7 @@ __global__ void __launch_bounds__(256) k_tl_hist(TlArgs a, uint32_t *tlh, opattr
   const int64_t base = tile * OPA_TILE;
   if (threadIdx.x == 0) sm.bad = 0;
   __syncthreads();
-  const uint32_t bad = tl_tile_keys(a, base, sm.A, nullptr, nullptr);
+  const uint32_t bad = tl_tile_keys(a, base, sm.A, nullptr);
   if (bad) atomicAdd(&sm.bad, bad);
   __syncthreads();
   if (threadIdx.x == 0 && sm.bad)
@@ -131,98 +523,59 @@ __global__ void __launch_bounds__(256) k_tl_hist(TlArgs a, uint32_t *tlh, opattr
   write_hist_row(sm.A, a.NN, tlh + tile * a.NN);
 }
 
-// ---------------------------------------------------------------------------
-// Fast path for up to kFastKeys names: a tile of 4096 launches is owned by
-// four waves, each walking 16 chunks of 64 in seq order and ranking names
-// with its own LDS counters (wave_rank), so no in-LDS sort is needed.
-// Element e of a tile sits in wave e / 1024, chunk (e / 64) % 16, lane e % 64.
-// ---------------------------------------------------------------------------
-constexpr int kWaveChunks = OPA_TILE / OPA_TILE_THREADS;  // 16 chunks per wave
+struct MatchArgs {
+  const uint32_t *tlh, *tlc, *pfc, *off;
+  const int32_t *slot;
+  int32_t *match;
+  int32_t *mbs;   // match of dedup-source launches by seq rank (NULL: off)
+  uint32_t *nbs;  // their names
+  int skip_name;
+};
 
-__device__ __forceinline__ int tile_elem(int c) {
-  return wave_id() * (OPA_TILE / 4) + c * OPA_WAVE + lane_id();
-}
-
-// One launch of seq rank x: input index j (-1 for holes), ranking key (its
-// name if eligible for replay, else NN) and partition (-1 none, -2 hole or
-// bad id). Returns 1 if an id is out of range.
-__device__ __forceinline__ uint32_t tl_load(const TlArgs &a, int64_t x, uint32_t &key, int32_t &j,
-                                            int32_t &lp) {
-  j = (x >= 0 && x < a.T) ? a.sv[x] : -1;
-  key = a.NN;
-  lp = -2;
-  if (j < 0) return 0;
-  const uint32_t nm = a.name[j];
-  const int32_t pt = a.part ? a.part[j] : -1;
-  if (nm >= a.NN || pt < -1 || (pt >= 0 && (uint32_t)pt >= a.NP)) return 1;
-  if (pt < 0 || a.part_rep[pt] == pt) key = nm;
-  lp = pt;
-  return 0;
-}
-
-// Partition edges of a seq tile. A head (first launch of a maximal run of one
-// partition in seq order) stores its rank in pfirst, a tail in plast. With
-// verify set, heads and tails instead compare against what is stored: a
-// partition with two runs has two heads, only one of which can be stored, so
-// the other one marks it non-contiguous.
-__device__ inline uint32_t part_edges(const TlArgs &a, const int32_t *lpart, int64_t base,
-                                      uint32_t *pfirst, uint32_t *plast, uint8_t *contig,
-                                      bool verify) {
-  uint32_t nbad = 0;
-  for (int e = threadIdx.x; e < OPA_TILE; e += OPA_TILE_THREADS) {
-    const int32_t lp = lpart[e];
-    if (lp < 0) continue;
-    const int64_t x = base + e;
-    int32_t prev, next, jj;
-    uint32_t kk;
-    if (e > 0) prev = lpart[e - 1];
-    else tl_load(a, x - 1, kk, jj, prev);
-    if (e < OPA_TILE - 1) next = lpart[e + 1];
-    else tl_load(a, x + 1, kk, jj, next);
-    if (!verify) {
-      if (prev != lp) pfirst[lp] = (uint32_t)x;
-      if (next != lp) plast[lp] = (uint32_t)x;
-    } else {
-      const bool bad = (prev != lp && pfirst[lp] != (uint32_t)x) ||
-                       (next != lp && plast[lp] != (uint32_t)x);
-      if (bad) {
-        contig[lp] = 0;
-        nbad++;
+__global__ void __launch_bounds__(256) k_tl_match(TlArgs a, MatchArgs m) {
+  __shared__ TileSmem sm;
+  __shared__ int32_t jidx[OPA_TILE];
+  const int64_t tile = blockIdx.x;
+  const int64_t base = tile * OPA_TILE;
+  tl_tile_keys(a, base, sm.A, jidx);
+  __syncthreads();
+  tile_radix_sort(sm.A, sm.B, sm.srt, OPA_SLOT_BITS, bits_for(a.NN));
+  const uint32_t *row = m.tlh + tile * a.NN;
+  for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
+    const int p = c * OPA_TILE_THREADS + threadIdx.x;
+    const uint32_t key = sm.A[p];
+    const uint32_t n = key >> OPA_SLOT_BITS;
+    const int l = (int)(key & (OPA_TILE - 1));
+    const int32_t j = jidx[l];
+    if (j < 0) continue;
+    if (n < a.NN) {
+      const int lo = lds_lower_bound(sm.A, OPA_TILE, n << OPA_SLOT_BITS);
+      const uint32_t rank = row[n] + (uint32_t)(p - lo);
+      const uint32_t rows = m.pfc[n];
+      int32_t mt = rank < rows ? m.slot[m.off[n] + rank] : -1;
+      if (m.skip_name && m.tlc[n] != rows) mt = -1;
+      m.match[j] = mt;
+      if (m.mbs && a.part[j] >= 0) {
+        m.mbs[base + l] = mt;
+        m.nbs[base + l] = n;
       }
+    } else {
+      m.match[j] = -1;
     }
   }
-  return nbad;
 }
 
-#define OPA_DYN_LDS(T, name) extern __shared__ __align__(16) unsigned char name##_raw[]; \
-  T *name = reinterpret_cast<T *>(name##_raw)
+// ---------------------------------------------------------------------------
+// profiled rows: per-tile name histograms and the slot table
+// ---------------------------------------------------------------------------
+struct PfArgs {
+  const uint32_t *name;
+  int64_t P;
+  uint32_t NN;
+};
 
-// Partition edges of every seq tile on their own (store, or verify).
-__global__ void __launch_bounds__(256) k_part_edges(TlArgs a, uint32_t *pfirst, uint32_t *plast,
-                                                    uint8_t *contig, opattr_diag *diag,
-                                                    int verify) {
-  __shared__ int32_t lpart[OPA_TILE];
-  __shared__ uint32_t snc;
-  const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
-  if (threadIdx.x == 0) snc = 0;
-  for (int e = threadIdx.x; e < OPA_TILE; e += OPA_TILE_THREADS) {
-    uint32_t k;
-    int32_t j, lp;
-    tl_load(a, base + e, k, j, lp);
-    lpart[e] = lp;
-  }
-  __syncthreads();
-  const uint32_t nb = part_edges(a, lpart, base, pfirst, plast, contig, verify != 0);
-  if (nb) atomicAdd(&snc, nb);
-  __syncthreads();
-  if (threadIdx.x == 0 && snc) atomicOr(&diag->flags, OPATTR_F_PARTITION);
-}
-
-__global__ void __launch_bounds__(256) k_tl_hist_w(TlArgs a, uint32_t *tlh, uint32_t *pfirst,
-                                                   uint32_t *plast, opattr_diag *diag,
-                                                   int want_parts) {
+__global__ void __launch_bounds__(256) k_pf_hist_w(PfArgs a, uint32_t *pfh, opattr_diag *diag) {
   OPA_DYN_LDS(uint16_t, cnt);
-  __shared__ int32_t lpart[OPA_TILE];
   __shared__ uint32_t sbad;
   const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
   const uint32_t NN = a.NN;
@@ -232,25 +585,54 @@ __global__ void __launch_bounds__(256) k_tl_hist_w(TlArgs a, uint32_t *tlh, uint
   uint32_t key[kWaveChunks], rank[kWaveChunks], bad = 0;
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
-    const int e = tile_elem(c);
-    int32_t j, lp;
-    bad += tl_load(a, base + e, key[c], j, lp);
-    lpart[e] = lp;
+    const int64_t x = base + tile_elem(c);
+    uint32_t n = NN;
+    if (x < a.P) {
+      n = a.name[x];
+      if (n >= NN) {
+        bad++;
+        n = NN;
+      }
+    }
+    key[c] = n;
   }
   wave_rank<kWaveChunks>(key, NN, bits_for(NN), cnt + wave_id() * NN, rank);
-  block_rank_bases(cnt, NN, tlh + tile * NN);
-  if (want_parts) part_edges(a, lpart, base, pfirst, plast, nullptr, false);
+  block_rank_bases(cnt, NN, pfh + tile * NN);
   if (bad) atomicAdd(&sbad, bad);
   __syncthreads();
   if (threadIdx.x == 0 && sbad)
     atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)sbad);
 }
 
-struct PfArgs {
-  const uint32_t *name;
-  int64_t P;
-  uint32_t NN;
-};
+__global__ void __launch_bounds__(256) k_pf_slot_w(PfArgs a, const uint32_t *__restrict__ pfh,
+                                                   const uint32_t *__restrict__ off,
+                                                   int32_t *slot) {
+  OPA_DYN_LDS(uint16_t, cnt);
+  const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
+  const uint32_t NN = a.NN;
+  for (uint32_t i = threadIdx.x; i < 4 * NN; i += OPA_TILE_THREADS) cnt[i] = 0;
+  __syncthreads();
+  uint32_t key[kWaveChunks], rank[kWaveChunks];
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const int64_t x = base + tile_elem(c);
+    uint32_t n = NN;
+    if (x < a.P) {
+      n = a.name[x];
+      if (n >= NN) n = NN;
+    }
+    key[c] = n;
+  }
+  wave_rank<kWaveChunks>(key, NN, bits_for(NN), cnt + wave_id() * NN, rank);
+  block_rank_bases(cnt, NN, nullptr);
+  const uint32_t *row = pfh + tile * NN;
+  const uint16_t *wb = cnt + wave_id() * NN;
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const uint32_t n = key[c];
+    if (n < NN) slot[off[n] + row[n] + wb[n] + rank[c]] = (int32_t)(base + tile_elem(c));
+  }
+}
 
 __device__ inline uint32_t pf_tile_keys(const PfArgs &a, int64_t base, uint32_t *A) {
   uint32_t bad = 0;
@@ -282,6 +664,28 @@ __global__ void __launch_bounds__(256) k_pf_hist(PfArgs a, uint32_t *pfh, opattr
     atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)sm.bad);
   tile_radix_sort(sm.A, sm.B, sm.srt, OPA_SLOT_BITS, bits_for(a.NN));
   write_hist_row(sm.A, a.NN, pfh + tile * a.NN);
+}
+
+// slot[off[n] + r] = index of the r-th profiled row of name n
+__global__ void __launch_bounds__(256) k_pf_slot(PfArgs a, const uint32_t *__restrict__ pfh,
+                                                 const uint32_t *__restrict__ off, int32_t *slot) {
+  __shared__ TileSmem sm;
+  const int64_t tile = blockIdx.x;
+  const int64_t base = tile * OPA_TILE;
+  pf_tile_keys(a, base, sm.A);
+  __syncthreads();
+  tile_radix_sort(sm.A, sm.B, sm.srt, OPA_SLOT_BITS, bits_for(a.NN));
+  const uint32_t *row = pfh + tile * a.NN;
+  for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
+    const int p = c * OPA_TILE_THREADS + threadIdx.x;
+    const uint32_t key = sm.A[p];
+    const uint32_t n = key >> OPA_SLOT_BITS;
+    if (n < a.NN) {
+      const int lo = lds_lower_bound(sm.A, OPA_TILE, n << OPA_SLOT_BITS);
+      const uint32_t rank = row[n] + (uint32_t)(p - lo);
+      slot[off[n] + rank] = (int32_t)(base + (key & (OPA_TILE - 1)));
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -424,295 +828,38 @@ __global__ void __launch_bounds__(1024) k_names(const uint32_t *__restrict__ tlc
   }
 }
 
-// slot[off[n] + r] = index of the r-th profiled row of name n
-__global__ void __launch_bounds__(256) k_pf_slot(PfArgs a, const uint32_t *__restrict__ pfh,
-                                                 const uint32_t *__restrict__ off, int32_t *slot) {
-  __shared__ TileSmem sm;
-  const int64_t tile = blockIdx.x;
-  const int64_t base = tile * OPA_TILE;
-  pf_tile_keys(a, base, sm.A);
-  __syncthreads();
-  tile_radix_sort(sm.A, sm.B, sm.srt, OPA_SLOT_BITS, bits_for(a.NN));
-  const uint32_t *row = pfh + tile * a.NN;
-  for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
-    const int p = c * OPA_TILE_THREADS + threadIdx.x;
-    const uint32_t key = sm.A[p];
-    const uint32_t n = key >> OPA_SLOT_BITS;
-    if (n < a.NN) {
-      const int lo = lds_lower_bound(sm.A, OPA_TILE, n << OPA_SLOT_BITS);
-      const uint32_t rank = row[n] + (uint32_t)(p - lo);
-      slot[off[n] + rank] = (int32_t)(base + (key & (OPA_TILE - 1)));
+// Layout promise of the kernels (checked under OPATTR_VALIDATE): sorted by
+// (stream, seq) with seq unique, streams below n_streams, query points not
+// decreasing along a stream.
+__global__ void k_check_stream_major(const uint16_t *st, const uint32_t *seq, const uint64_t *q,
+                                     int64_t T, uint32_t NS, opattr_diag *diag) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  bool bad = false;
+  if (i < T) {
+    bad = st[i] >= NS;
+    if (i > 0) {
+      const uint16_t a = st[i - 1], b = st[i];
+      bad = bad || a > b || (a == b && (seq[i - 1] >= seq[i] || q[i - 1] > q[i]));
     }
   }
-}
-
-__global__ void __launch_bounds__(256) k_pf_hist_w(PfArgs a, uint32_t *pfh, opattr_diag *diag) {
-  OPA_DYN_LDS(uint16_t, cnt);
-  __shared__ uint32_t sbad;
-  const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
-  const uint32_t NN = a.NN;
-  for (uint32_t i = threadIdx.x; i < 4 * NN; i += OPA_TILE_THREADS) cnt[i] = 0;
-  if (threadIdx.x == 0) sbad = 0;
-  __syncthreads();
-  uint32_t key[kWaveChunks], rank[kWaveChunks], bad = 0;
-#pragma unroll
-  for (int c = 0; c < kWaveChunks; ++c) {
-    const int64_t x = base + tile_elem(c);
-    uint32_t n = NN;
-    if (x < a.P) {
-      n = a.name[x];
-      if (n >= NN) {
-        bad++;
-        n = NN;
-      }
-    }
-    key[c] = n;
-  }
-  wave_rank<kWaveChunks>(key, NN, bits_for(NN), cnt + wave_id() * NN, rank);
-  block_rank_bases(cnt, NN, pfh + tile * NN);
-  if (bad) atomicAdd(&sbad, bad);
-  __syncthreads();
-  if (threadIdx.x == 0 && sbad)
-    atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)sbad);
-}
-
-__global__ void __launch_bounds__(256) k_pf_slot_w(PfArgs a, const uint32_t *__restrict__ pfh,
-                                                   const uint32_t *__restrict__ off,
-                                                   int32_t *slot) {
-  OPA_DYN_LDS(uint16_t, cnt);
-  const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
-  const uint32_t NN = a.NN;
-  for (uint32_t i = threadIdx.x; i < 4 * NN; i += OPA_TILE_THREADS) cnt[i] = 0;
-  __syncthreads();
-  uint32_t key[kWaveChunks], rank[kWaveChunks];
-#pragma unroll
-  for (int c = 0; c < kWaveChunks; ++c) {
-    const int64_t x = base + tile_elem(c);
-    uint32_t n = NN;
-    if (x < a.P) {
-      n = a.name[x];
-      if (n >= NN) n = NN;
-    }
-    key[c] = n;
-  }
-  wave_rank<kWaveChunks>(key, NN, bits_for(NN), cnt + wave_id() * NN, rank);
-  block_rank_bases(cnt, NN, nullptr);
-  const uint32_t *row = pfh + tile * NN;
-  const uint16_t *wb = cnt + wave_id() * NN;
-#pragma unroll
-  for (int c = 0; c < kWaveChunks; ++c) {
-    const uint32_t n = key[c];
-    if (n < NN) {
-      const int64_t x = base + tile_elem(c);
-      slot[off[n] + row[n] + wb[n] + rank[c]] = (int32_t)x;
-    }
-  }
-}
-
-struct MatchArgs {
-  const uint32_t *tlh, *tlc, *pfc, *off;
-  const int32_t *slot;
-  int32_t *match;
-  int32_t *mbs;   // match of dedup-source launches by seq rank (NULL: off)
-  uint32_t *nbs;  // their names
-  int skip_name;
-};
-
-__global__ void __launch_bounds__(256) k_tl_match(TlArgs a, MatchArgs m) {
-  __shared__ TileSmem sm;
-  __shared__ int32_t jidx[OPA_TILE];
-  const int64_t tile = blockIdx.x;
-  const int64_t base = tile * OPA_TILE;
-  tl_tile_keys(a, base, sm.A, nullptr, jidx);
-  __syncthreads();
-  tile_radix_sort(sm.A, sm.B, sm.srt, OPA_SLOT_BITS, bits_for(a.NN));
-  const uint32_t *row = m.tlh + tile * a.NN;
-  for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
-    const int p = c * OPA_TILE_THREADS + threadIdx.x;
-    const uint32_t key = sm.A[p];
-    const uint32_t n = key >> OPA_SLOT_BITS;
-    const int l = (int)(key & (OPA_TILE - 1));
-    const int32_t j = jidx[l];
-    if (j < 0) continue;
-    if (n < a.NN) {
-      const int lo = lds_lower_bound(sm.A, OPA_TILE, n << OPA_SLOT_BITS);
-      const uint32_t rank = row[n] + (uint32_t)(p - lo);
-      const uint32_t rows = m.pfc[n];
-      int32_t mt = rank < rows ? m.slot[m.off[n] + rank] : -1;
-      if (m.skip_name && m.tlc[n] != rows) mt = -1;
-      m.match[j] = mt;
-      if (m.mbs && a.part[j] >= 0) {
-        m.mbs[base + l] = mt;
-        m.nbs[base + l] = n;
-      }
-    } else {
-      m.match[j] = -1;
-    }
-  }
-}
-
-__global__ void __launch_bounds__(256) k_tl_match_w(TlArgs a, MatchArgs m, const uint32_t *pfirst,
-                                                    const uint32_t *plast, uint8_t *contig,
-                                                    opattr_diag *diag, int want_parts) {
-  OPA_DYN_LDS(uint16_t, cnt);
-  __shared__ int32_t lpart[OPA_TILE];
-  __shared__ uint32_t snc;
-  const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
-  const uint32_t NN = a.NN;
-  for (uint32_t i = threadIdx.x; i < 4 * NN; i += OPA_TILE_THREADS) cnt[i] = 0;
-  if (threadIdx.x == 0) snc = 0;
-  __syncthreads();
-  uint32_t key[kWaveChunks], rank[kWaveChunks];
-  int32_t jj[kWaveChunks];
-#pragma unroll
-  for (int c = 0; c < kWaveChunks; ++c) {
-    const int e = tile_elem(c);
-    int32_t lp;
-    tl_load(a, base + e, key[c], jj[c], lp);
-    lpart[e] = lp;
-  }
-  wave_rank<kWaveChunks>(key, NN, bits_for(NN), cnt + wave_id() * NN, rank);
-  block_rank_bases(cnt, NN, nullptr);
-  const uint32_t *row = m.tlh + tile * NN;
-  const uint16_t *wb = cnt + wave_id() * NN;
-#pragma unroll
-  for (int c = 0; c < kWaveChunks; ++c) {
-    const int32_t j = jj[c];
-    if (j < 0) continue;
-    const uint32_t n = key[c];
-    int32_t mt = -1;
-    if (n < NN) {
-      const uint32_t r = row[n] + wb[n] + rank[c];
-      const uint32_t rows = m.pfc[n];
-      mt = r < rows ? m.slot[m.off[n] + r] : -1;
-      if (m.skip_name && m.tlc[n] != rows) mt = -1;
-      const int e = tile_elem(c);
-      if (m.mbs && lpart[e] >= 0) {
-        m.mbs[base + e] = mt;
-        m.nbs[base + e] = n;
-      }
-    }
-    m.match[j] = mt;
-  }
-  if (want_parts) {
-    const uint32_t nb = part_edges(a, lpart, base, const_cast<uint32_t *>(pfirst),
-                                   const_cast<uint32_t *>(plast), contig, true);
-    if (nb) atomicAdd(&snc, nb);
-    __syncthreads();
-    if (threadIdx.x == 0 && snc) atomicOr(&diag->flags, OPATTR_F_PARTITION);
-  }
-}
-
-// bad class-map entries are counted once, with the other bad ids of the match
-__global__ void k_rep_check(const int32_t *__restrict__ part_rep, uint32_t NP, opattr_diag *diag) {
-  const uint32_t q = blockIdx.x * blockDim.x + threadIdx.x;
-  const bool bad = q < NP && (part_rep[q] < 0 || (uint32_t)part_rep[q] >= NP);
   const uint64_t m = __ballot(bad);
-  if (m && lane_id() == __ffsll((unsigned long long)m) - 1)
-    atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)__popcll(m));
+  if (m && lane_id() == __ffsll((unsigned long long)m) - 1) {
+    atomicAdd((unsigned long long *)&diag->order_violations, (unsigned long long)__popcll(m));
+    atomicOr(&diag->flags, OPATTR_F_ORDER);
+  }
 }
 
-static TlArgs tl_args(const opattr_kernels *k, const opattr_dims *d, void *ws, const Plan &pl,
-                      bool dedup) {
-  TlArgs a;
-  a.sv = at<int32_t>(ws, pl.sv);
-  a.T = pl.T;
-  a.name = k->name_id;
-  a.part = dedup ? k->part_id : nullptr;
-  a.part_rep = dedup ? d->part_rep : nullptr;
-  a.NN = d->n_names;
-  a.NP = dedup ? d->n_parts : 0;
-  return a;
-}
-
-static bool has_dedup(const opattr_kernels *k, const opattr_dims *d) {
-  return k->part_id && d->part_rep && d->n_parts > 0;
-}
-
-void run_match(const IomArgs &x, hipStream_t s) {
-  const Plan &pl = *x.pl;
-  const opattr_kernels *k = x.k;
-  const opattr_dims *d = x.d;
-  void *ws = x.ws;
-  const uint32_t NN = d->n_names;
-  const bool dedup = has_dedup(k, d);
-  const bool parts = dedup && x.want_dedup;
-  const bool fast = NN <= kFastNames, fast_pf = NN <= kFastKeys;
-  const size_t lds = (size_t)4 * NN * sizeof(uint16_t);
-  uint32_t *tlh = at<uint32_t>(ws, pl.tlh), *pfh = at<uint32_t>(ws, pl.pfh);
-  uint32_t *tlc = at<uint32_t>(ws, pl.tlc), *pfc = at<uint32_t>(ws, pl.pfc);
-  uint32_t *off = at<uint32_t>(ws, pl.off);
-  uint32_t *pfirst = at<uint32_t>(ws, pl.pfirst), *plast = at<uint32_t>(ws, pl.plast);
-  uint8_t *contig = at<uint8_t>(ws, pl.contig);
-  fill_u32(tlc, 0, NN, s);
-  fill_u32(pfc, 0, NN, s);
-  if (parts) {
-    fill_u32(pfirst, 0xFFFFFFFFu, pl.NP, s);
-    fill_u32(plast, 0xFFFFFFFFu, pl.NP, s);
-    fill_u8(contig, 1, pl.NP, s);
-  }
-  if (dedup) k_rep_check<<<(d->n_parts + 255) / 256, 256, 0, s>>>(d->part_rep, d->n_parts, x.diag);
-  const TlArgs ta = tl_args(k, d, ws, pl, dedup);
-  PfArgs pa;
-  pa.name = x.p->name_id;
-  pa.P = pl.P;
-  pa.NN = NN;
-  probe_begin(OPATTR_PROBE_TL_HIST, s);
-  if (pl.nt > 0) {
-    if (fast) {
-      k_tl_hist_w<<<(unsigned)pl.nt, 256, lds, s>>>(ta, tlh, pfirst, plast, x.diag, parts ? 1 : 0);
-    } else {
-      k_tl_hist<<<(unsigned)pl.nt, 256, 0, s>>>(ta, tlh, x.diag);
-      if (parts)
-        k_part_edges<<<(unsigned)pl.nt, 256, 0, s>>>(ta, pfirst, plast, contig, x.diag, 0);
-    }
-  }
-  probe_end(OPATTR_PROBE_TL_HIST, s);
-  probe_begin(OPATTR_PROBE_PF_HIST, s);
-  if (pl.ntp > 0) {
-    if (fast_pf) k_pf_hist_w<<<(unsigned)pl.ntp, 256, lds, s>>>(pa, pfh, x.diag);
-    else k_pf_hist<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, x.diag);
-  }
-  probe_end(OPATTR_PROBE_PF_HIST, s);
-  probe_begin(OPATTR_PROBE_COL_SCAN, s);
-  column_scan(tlh, pl.nt, NN, at<uint32_t>(ws, pl.tlch), tlc, s, nullptr);
-  column_scan(pfh, pl.ntp, NN, at<uint32_t>(ws, pl.pfch), pfc, s, nullptr);
-  if (NN)
-    k_names<<<1, 1024, 0, s>>>(tlc, pfc, NN, off, x.name_counts, x.diag,
-                               x.policy == OPATTR_MISMATCH_STRICT ? 1 : 0);
-  probe_end(OPATTR_PROBE_COL_SCAN, s);
-  probe_begin(OPATTR_PROBE_PF_SLOT, s);
-  if (pl.ntp > 0) {
-    if (fast_pf) k_pf_slot_w<<<(unsigned)pl.ntp, 256, lds, s>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
-    else k_pf_slot<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
-  }
-  probe_end(OPATTR_PROBE_PF_SLOT, s);
-  MatchArgs ma;
-  ma.tlh = tlh;
-  ma.tlc = tlc;
-  ma.pfc = pfc;
-  ma.off = off;
-  ma.slot = at<int32_t>(ws, pl.slot);
-  ma.match = x.match;
-  ma.mbs = parts ? at<int32_t>(ws, pl.mbs) : nullptr;
-  ma.nbs = parts ? at<uint32_t>(ws, pl.nbs) : nullptr;
-  ma.skip_name = x.policy == OPATTR_MISMATCH_SKIP_NAME ? 1 : 0;
-  probe_begin(OPATTR_PROBE_TL_MATCH, s);
-  if (pl.nt > 0) {
-    if (fast) {
-      k_tl_match_w<<<(unsigned)pl.nt, 256, lds, s>>>(ta, ma, pfirst, plast, contig, x.diag,
-                                                     parts ? 1 : 0);
-    } else {
-      k_tl_match<<<(unsigned)pl.nt, 256, 0, s>>>(ta, ma);
-      if (parts)
-        k_part_edges<<<(unsigned)pl.nt, 256, 0, s>>>(ta, pfirst, plast, contig, x.diag, 1);
-    }
-  }
-  probe_end(OPATTR_PROBE_TL_MATCH, s);
+void check_kernel_layout(const opattr_kernels *k, const opattr_dims *d, opattr_diag *diag,
+                         hipStream_t s) {
+  if (!(d->flags & OPATTR_KERNELS_STREAM_MAJOR) || !(d->flags & OPATTR_VALIDATE) || k->n <= 0 ||
+      !k->seq || !k->stream_id || !(k->query_ns || k->start_ns))
+    return;
+  k_check_stream_major<<<(unsigned)((k->n + 255) / 256), 256, 0, s>>>(
+      k->stream_id, k->seq, k->query_ns ? k->query_ns : k->start_ns, k->n, d->n_streams, diag);
 }
 
 // ---------------------------------------------------------------------------
-// layer dedup
+// layer dedup as its own pass (radix path and the standalone broadcast)
 // ---------------------------------------------------------------------------
 struct DedupArgs {
   int64_t T;
@@ -722,8 +869,7 @@ struct DedupArgs {
   const int32_t *part;
   const int32_t *part_rep;
   uint32_t NN, NP;
-  const uint32_t *pfirst, *plast;
-  const uint8_t *contig;
+  const uint32_t *pfirst, *plast, *pheads;
   int32_t *mbs;
   uint32_t *nbs;
   int32_t *match;
@@ -761,7 +907,8 @@ __global__ void k_dedup(DedupArgs a) {
         // a duplicate: inherit from the representative's launch at the same
         // position of its partition
         const uint32_t f = a.pfirst[r];
-        bool ok = a.contig[pt] && a.part_rep[r] == r && f != 0xFFFFFFFFu && a.contig[r];
+        bool ok = a.pheads[pt] == 1u && a.part_rep[r] == r && f != 0xFFFFFFFFu &&
+                  a.pheads[r] == 1u;
         const int64_t rk = rank_of(a, i);
         ok = ok && rk >= 0;
         int32_t mt = -1;
@@ -784,9 +931,32 @@ __global__ void k_dedup(DedupArgs a) {
     atomicAdd((unsigned long long *)&a.diag->dedup_errors, (unsigned long long)__popcll(m));
 }
 
-void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, opattr_diag *diag,
-               void *ws, const Plan &pl, bool stats_ready, hipStream_t s) {
-  if (!has_dedup(k, d) || pl.T <= 0) return;
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+static bool has_dedup(const opattr_kernels *k, const opattr_dims *d) {
+  return k->part_id && d->part_rep && d->n_parts > 0;
+}
+
+static TlArgs tl_args(const opattr_kernels *k, const opattr_dims *d, void *ws, const Plan &pl,
+                      bool dedup) {
+  TlArgs a;
+  a.sv = at<int32_t>(ws, pl.sv);
+  a.T = pl.T;
+  a.name = k->name_id;
+  a.part = dedup ? k->part_id : nullptr;
+  a.part_rep = dedup ? d->part_rep : nullptr;
+  a.NN = d->n_names;
+  a.NP = dedup ? d->n_parts : 0;
+  a.seq = k->seq;
+  a.bnd = at<uint32_t>(ws, pl.tbnd);
+  a.kblk = at<int64_t>(ws, pl.kblk);
+  a.NS = d->n_streams;
+  return a;
+}
+
+static DedupArgs dedup_args(const opattr_kernels *k, const opattr_dims *d, int32_t *match,
+                            opattr_diag *diag, void *ws, const Plan &pl) {
   DedupArgs a;
   a.T = pl.T;
   a.seq = k->seq;
@@ -796,26 +966,152 @@ void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, op
   a.part_rep = d->part_rep;
   a.NN = d->n_names;
   a.NP = d->n_parts;
-  uint32_t *pfirst = at<uint32_t>(ws, pl.pfirst), *plast = at<uint32_t>(ws, pl.plast);
-  uint8_t *contig = at<uint8_t>(ws, pl.contig);
-  a.pfirst = pfirst;
-  a.plast = plast;
-  a.contig = contig;
+  a.pfirst = at<uint32_t>(ws, pl.pfirst);
+  a.plast = at<uint32_t>(ws, pl.plast);
+  a.pheads = at<uint32_t>(ws, pl.pheads);
   a.mbs = at<int32_t>(ws, pl.mbs);
   a.nbs = at<uint32_t>(ws, pl.nbs);
   a.match = match;
   a.diag = diag;
+  return a;
+}
+
+static void clear_partitions(void *ws, const Plan &pl, hipStream_t s) {
+  fill_u32(at<uint32_t>(ws, pl.pfirst), 0xFFFFFFFFu, pl.NP, s);
+  fill_u32(at<uint32_t>(ws, pl.plast), 0xFFFFFFFFu, pl.NP, s);
+  fill_u32(at<uint32_t>(ws, pl.pheads), 0u, pl.NP, s);
+}
+
+void run_match(const IomArgs &x, hipStream_t s) {
+  const Plan &pl = *x.pl;
+  const opattr_kernels *k = x.k;
+  const opattr_dims *d = x.d;
+  void *ws = x.ws;
+  const uint32_t NN = d->n_names;
+  const bool dedup = has_dedup(k, d);
+  const bool parts = dedup && x.want_dedup;
+  const bool seg = pl.seg;  // implies the fast path
+  const bool fast = NN <= kFastNames, fast_pf = NN <= kFastKeys;
+  const size_t lds = (size_t)4 * NN * sizeof(uint16_t);
+  uint32_t *tlh = at<uint32_t>(ws, pl.tlh), *pfh = at<uint32_t>(ws, pl.pfh);
+  uint32_t *tlc = at<uint32_t>(ws, pl.tlc), *pfc = at<uint32_t>(ws, pl.pfc);
+  uint32_t *off = at<uint32_t>(ws, pl.off);
+  uint32_t *pfirst = at<uint32_t>(ws, pl.pfirst), *plast = at<uint32_t>(ws, pl.plast);
+  uint32_t *pheads = at<uint32_t>(ws, pl.pheads);
+  fill_u32(tlc, 0, NN, s);
+  fill_u32(pfc, 0, NN, s);
+  if (parts) clear_partitions(ws, pl, s);
+  if (dedup) k_rep_check<<<(d->n_parts + 255) / 256, 256, 0, s>>>(d->part_rep, d->n_parts, x.diag);
+  const TlArgs ta = tl_args(k, d, ws, pl, dedup);
+  PfArgs pa;
+  pa.name = x.p->name_id;
+  pa.P = pl.P;
+  pa.NN = NN;
+  if (seg && pl.nt > 0) {
+    launch_stream_blocks(k->stream_id, pl.T, pl.NS, at<int64_t>(ws, pl.kblk), s);
+    const int64_t nb = (pl.nt + 1) * pl.NS;
+    k_tile_bounds<<<(unsigned)((nb + 255) / 256), 256, 0, s>>>(k->seq, at<int64_t>(ws, pl.kblk),
+                                                             pl.NS, pl.nt, at<uint32_t>(ws, pl.tbnd));
+  }
+  HistOut ho;
+  ho.tlh = tlh;
+  ho.rit = at<uint16_t>(ws, pl.rit);
+  ho.kbs = at<uint32_t>(ws, pl.nbs);
+  ho.pfirst = pfirst;
+  ho.plast = plast;
+  ho.pheads = parts ? pheads : nullptr;
+  ho.diag = x.diag;
+  probe_begin(OPATTR_PROBE_TL_HIST, s);
+  if (pl.nt > 0) {
+    if (seg) {
+      k_tl_hist_w<true><<<(unsigned)pl.nt, 256, lds, s>>>(ta, ho);
+    } else if (fast) {
+      k_tl_hist_w<false><<<(unsigned)pl.nt, 256, lds, s>>>(ta, ho);
+    } else {
+      k_tl_hist<<<(unsigned)pl.nt, 256, 0, s>>>(ta, tlh, x.diag);
+      if (parts) k_part_edges<<<(unsigned)pl.nt, 256, 0, s>>>(ta, pfirst, plast, pheads);
+    }
+  }
+  probe_end(OPATTR_PROBE_TL_HIST, s);
+  if (parts && pl.nt > 0)
+    k_part_flags<<<(unsigned)((pl.NP + 255) / 256), 256, 0, s>>>(pheads, pl.NP, x.diag);
+  probe_begin(OPATTR_PROBE_PF_HIST, s);
+  if (pl.ntp > 0) {
+    if (fast_pf) k_pf_hist_w<<<(unsigned)pl.ntp, 256, lds, s>>>(pa, pfh, x.diag);
+    else k_pf_hist<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, x.diag);
+  }
+  probe_end(OPATTR_PROBE_PF_HIST, s);
+  probe_begin(OPATTR_PROBE_COL_SCAN, s);
+  column_scan(tlh, pl.nt, NN, at<uint32_t>(ws, pl.tlch), tlc, s, nullptr);
+  column_scan(pfh, pl.ntp, NN, at<uint32_t>(ws, pl.pfch), pfc, s, nullptr);
+  if (NN)
+    k_names<<<1, 1024, 0, s>>>(tlc, pfc, NN, off, x.name_counts, x.diag,
+                               x.policy == OPATTR_MISMATCH_STRICT ? 1 : 0);
+  probe_end(OPATTR_PROBE_COL_SCAN, s);
+  probe_begin(OPATTR_PROBE_PF_SLOT, s);
+  if (pl.ntp > 0) {
+    if (fast_pf) k_pf_slot_w<<<(unsigned)pl.ntp, 256, lds, s>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
+    else k_pf_slot<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
+  }
+  probe_end(OPATTR_PROBE_PF_SLOT, s);
+  probe_begin(OPATTR_PROBE_TL_MATCH, s);
+  if (pl.nt > 0) {
+    if (fast) {
+      LookArgs m;
+      m.tlh = tlh;
+      m.tlc = tlc;
+      m.pfc = pfc;
+      m.off = off;
+      m.slot = at<int32_t>(ws, pl.slot);
+      m.rit = ho.rit;
+      m.kbs = ho.kbs;
+      m.pfirst = pfirst;
+      m.plast = plast;
+      m.pheads = parts ? pheads : nullptr;
+      m.match = x.match;
+      m.skip_name = x.policy == OPATTR_MISMATCH_SKIP_NAME ? 1 : 0;
+      m.diag = x.diag;
+      if (seg) k_tl_look<true><<<(unsigned)pl.nt, 256, 0, s>>>(ta, m);
+      else k_tl_look<false><<<(unsigned)pl.nt, 256, 0, s>>>(ta, m);
+    } else {
+      MatchArgs ma;
+      ma.tlh = tlh;
+      ma.tlc = tlc;
+      ma.pfc = pfc;
+      ma.off = off;
+      ma.slot = at<int32_t>(ws, pl.slot);
+      ma.match = x.match;
+      ma.mbs = parts ? at<int32_t>(ws, pl.mbs) : nullptr;
+      ma.nbs = parts ? at<uint32_t>(ws, pl.nbs) : nullptr;
+      ma.skip_name = x.policy == OPATTR_MISMATCH_SKIP_NAME ? 1 : 0;
+      k_tl_match<<<(unsigned)pl.nt, 256, 0, s>>>(ta, ma);
+    }
+  }
+  probe_end(OPATTR_PROBE_TL_MATCH, s);
+  // the radix path broadcasts to duplicates in a pass of its own
+  if (parts && !fast && pl.T > 0) {
+    const DedupArgs da = dedup_args(k, d, x.match, x.diag, ws, pl);
+    probe_begin(OPATTR_PROBE_DEDUP, s);
+    k_dedup<<<(unsigned)((pl.T + 255) / 256), 256, 0, s>>>(da);
+    probe_end(OPATTR_PROBE_DEDUP, s);
+  }
+}
+
+// standalone broadcast over a given match array
+void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, opattr_diag *diag,
+               void *ws, const Plan &pl, hipStream_t s) {
+  if (!has_dedup(k, d) || pl.T <= 0) return;
+  const DedupArgs a = dedup_args(k, d, match, diag, ws, pl);
+  const TlArgs ta = tl_args(k, d, ws, pl, true);
   const unsigned nb = (unsigned)((pl.T + 255) / 256);
   probe_begin(OPATTR_PROBE_DEDUP, s);
-  if (!stats_ready) {
-    const TlArgs ta = tl_args(k, d, ws, pl, true);
-    fill_u32(pfirst, 0xFFFFFFFFu, pl.NP, s);
-    fill_u32(plast, 0xFFFFFFFFu, pl.NP, s);
-    fill_u8(contig, 1, pl.NP, s);
-    k_part_edges<<<(unsigned)pl.nt, 256, 0, s>>>(ta, pfirst, plast, contig, diag, 0);
-    k_part_edges<<<(unsigned)pl.nt, 256, 0, s>>>(ta, pfirst, plast, contig, diag, 1);
-    k_src_fill<<<nb, 256, 0, s>>>(a);
-  }
+  clear_partitions(ws, pl, s);
+  k_part_edges<<<(unsigned)pl.nt, 256, 0, s>>>(ta, at<uint32_t>(ws, pl.pfirst),
+                                               at<uint32_t>(ws, pl.plast),
+                                               at<uint32_t>(ws, pl.pheads));
+  k_part_flags<<<(unsigned)((pl.NP + 255) / 256), 256, 0, s>>>(at<uint32_t>(ws, pl.pheads), pl.NP,
+                                                              diag);
+  k_src_fill<<<nb, 256, 0, s>>>(a);
   k_dedup<<<nb, 256, 0, s>>>(a);
   probe_end(OPATTR_PROBE_DEDUP, s);
 }

@@ -65,6 +65,11 @@ __global__ void k_blocks16(const uint16_t *st, int64_t n, uint32_t NS, int64_t *
   blk[s] = lo;
 }
 
+void launch_stream_blocks(const uint16_t *st, int64_t n, uint32_t NS, int64_t *blk,
+                          hipStream_t s) {
+  k_blocks16<<<(NS + 1 + 255) / 256, 256, 0, s>>>(st, n, NS, blk);
+}
+
 // tbase[s] = first tile of stream s (tiles never straddle streams)
 __global__ void __launch_bounds__(1024) k_rtile_base(const int64_t *rblk, uint32_t NS,
                                                      int32_t *tbase) {

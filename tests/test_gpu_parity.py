@@ -110,6 +110,19 @@ def test_many_names_and_rows(n_names, n_ops):
     parity.assert_attribute(out2, O.attribute(sm), diag2)
 
 
+def test_layout_promises_validated():
+    """Under VALIDATE a kept promise changes nothing and a broken kernel
+    layout promise is reported as an order error."""
+    tr = _trace("gpt2", "stream_major")
+    want = _oracle("gpt2", "stream_major")
+    out, diag = _run(tr, flags=HINTS | opattr.VALIDATE)
+    assert diag["status"] == 0 and diag["order_violations"] == 0
+    parity.assert_attribute(out, want, diag)
+    bad = _trace("gpt2", "shuffled")
+    _, diag2 = _run(bad, flags=HINTS | opattr.VALIDATE)
+    assert diag2["status"] == -8 and diag2["order_violations"] > 0
+
+
 @pytest.mark.parametrize("policy", [opattr.MISMATCH_SKIP_NAME, opattr.MISMATCH_STRICT])
 def test_mismatch_policies(policy):
     tr = tg.generate("lstm", T=300_000, ranges=3_000, emission="stream_major")
