@@ -20,6 +20,11 @@
  *    on the current HIP device, unless marked (host).
  *  - Every call enqueues its work on `stream` (a hipStream_t; NULL = the null
  *    stream) and returns without synchronising, except opattr_read_diag.
+ *    opattr_attribute forks independent stages onto an internal stream of the
+ *    current device (one per calling host thread, created on first use, default
+ *    priority) with events recorded on `stream`, and joins it back on `stream`
+ *    before its last kernels: completion is observed on `stream` alone, and a
+ *    capture of `stream` records both branches.
  *  - The caller owns every buffer: inputs, outputs, the diag record and the
  *    workspace. No entry point allocates or frees device memory. Calls are
  *    stateless and reentrant on distinct workspaces.

@@ -322,14 +322,13 @@ void run_aggregate(const EncArgs &x, hipStream_t s) {
   const size_t lds = (size_t)4 * pl.G * sizeof(uint16_t);
   const unsigned tgrid = (unsigned)(pl.ntrt < 1024 ? (pl.ntrt > 0 ? pl.ntrt : 1) : 1024);
 
+  // gcnt (and meta when there are no launches) were cleared with the
+  // look-back states
   probe_begin(OPATTR_PROBE_AGGREGATE, s);
-  fill_u32(w.gcnt, 0, pl.G, s);
   if (pl.T > 0) {
     if (fast) k_item_hist_w<<<tgrid, 256, lds, s>>>(w);
     else k_item_hist_r<<<tgrid, 256, 0, s>>>(w);
     column_scan(w.ith, pl.ntrt, pl.G, at<uint32_t>(x.ws, pl.itch), w.gcnt, s, w.meta + 2);
-  } else {
-    fill_u32(reinterpret_cast<uint32_t *>(w.meta), 0, 8, s);
   }
   k_row_offsets<<<1, 1024, 0, s>>>(w);
   if (pl.T > 0) {

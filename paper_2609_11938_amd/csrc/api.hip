@@ -59,7 +59,10 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.seqsort_k1 = b.take(pl.seq_dense ? 0 : T * 8);
   pl.seqsort_v0 = b.take(pl.seq_dense ? 0 : T * 4);
   pl.seqsort_v1 = b.take(pl.seq_dense ? 0 : T * 4);
-  pl.rs_hist = b.take(radix_hist_entries(pl.T > pl.R ? pl.T : pl.R) * 4);
+  // radix histograms: one for the seq sort, one for the range sort (the two
+  // run concurrently in opattr_attribute)
+  pl.rs_hist = b.take(radix_hist_entries(pl.seq_dense ? 0 : pl.T) * 4);
+  pl.rs_hist_r = b.take(radix_hist_entries(pl.ranges_nested ? 0 : pl.R) * 4);
   pl.tlh = b.take((size_t)pl.nt * NN * 4);
   pl.pfh = b.take((size_t)pl.ntp * NN * 4);
   pl.tlch = b.take((size_t)pl.ncht * NN * 4);
@@ -216,6 +219,37 @@ static bool check_ranges(const opattr_ranges *r) {
   return r->start_ns && r->end_ns && r->stream_id && r->op_id;
 }
 
+// A side stream per device and calling thread (default priority), with the
+// two events that fork work onto it from the caller's stream and join it
+// back. NULL when it cannot be created; the caller's stream is used alone.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+constexpr int kMaxDevices = 64;
+inline thread_local SideStream g_side[kMaxDevices];
+
+static SideStream *side_stream() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  SideStream &ss = g_side[dev];
+  if (!ss.s) {
+    hipStream_t st = nullptr;
+    hipEvent_t a = nullptr, b = nullptr;
+    if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&a, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&b, hipEventDisableTiming) != hipSuccess) {
+      if (a) (void)hipEventDestroy(a);
+      (void)hipStreamDestroy(st);
+      return nullptr;
+    }
+    ss.s = st;
+    ss.fork = a;
+    ss.join = b;
+  }
+  return &ss;
+}
+
 static int launch_status() {
   const hipError_t launch = hipGetLastError();
   const hipError_t first = g_hip_error;
@@ -299,7 +333,6 @@ int opattr_enclose(const opattr_kernels *k, const opattr_ranges *r, const opattr
   const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s);
   resolve_ranges(cr, d, ws, pl, range_depth, diag, s);
   EncArgs e{};
-  e.mode = kEncloseOnly;
   e.k = k;
   e.cr = cr;
   e.d = d;
@@ -307,7 +340,7 @@ int opattr_enclose(const opattr_kernels *k, const opattr_ranges *r, const opattr
   e.diag = diag;
   e.ws = ws;
   e.pl = &pl;
-  run_enclose_aggregate(e, s);
+  run_enclose(e, s);
   launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s);
   return launch_status();
 }
@@ -332,7 +365,6 @@ int opattr_aggregate(const opattr_kernels *k, const opattr_profiled *p, const in
   hipStream_t s = (hipStream_t)stream;
   check_kernel_layout(k, d, diag, s);
   EncArgs e{};
-  e.mode = kAggregateOnly;
   e.k = k;
   e.p = p;
   e.match = match;
@@ -345,7 +377,7 @@ int opattr_aggregate(const opattr_kernels *k, const opattr_profiled *p, const in
   e.diag = diag;
   e.ws = ws;
   e.pl = &pl;
-  run_enclose_aggregate(e, s);
+  run_aggregate_all(e, s);
   launch_finish(diag, nullptr, 0, s);
   return launch_status();
 }
@@ -364,15 +396,19 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   hipStream_t s = (hipStream_t)stream;
   check_kernel_layout(k, d, diag, s);
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
-  build_seq_view(k, d, ws, pl, diag, validate, s);
-  IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, validate};
-  run_match(a, s);
-  probe_begin(OPATTR_PROBE_RANGES, s);
-  const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s);
-  resolve_ranges(cr, d, ws, pl, range_depth, diag, s);
-  probe_end(OPATTR_PROBE_RANGES, s);
+  // the ranges and the enclosure do not depend on the matching: they run on
+  // a side stream of this device, joined back before the aggregation
+  SideStream *ss = side_stream();
+  const hipStream_t s2 = ss ? ss->s : s;
+  if (ss) {
+    note(hipEventRecord(ss->fork, s));
+    note(hipStreamWaitEvent(s2, ss->fork, 0));
+  }
+  probe_begin(OPATTR_PROBE_RANGES, s2);
+  const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s2);
+  resolve_ranges(cr, d, ws, pl, range_depth, diag, s2);
+  probe_end(OPATTR_PROBE_RANGES, s2);
   EncArgs e{};
-  e.mode = kEncloseAggregate;
   e.k = k;
   e.p = p;
   e.match = match;
@@ -386,7 +422,13 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   e.diag = diag;
   e.ws = ws;
   e.pl = &pl;
-  run_enclose_aggregate(e, s);
+  run_enclose(e, s2);
+  if (ss) note(hipEventRecord(ss->join, s2));
+  build_seq_view(k, d, ws, pl, diag, validate, s);
+  IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, validate};
+  run_match(a, s);
+  if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
+  run_aggregate_all(e, s);
   launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s);
   return launch_status();
 }

@@ -57,6 +57,10 @@ __device__ __forceinline__ void wave_rank(const uint32_t (&key)[CH], uint32_t K,
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
     const uint32_t k = key[c];
+    if (__ballot(k < K) == 0) {  // nothing to rank in this chunk
+      rank[c] = 0;
+      continue;
+    }
     const uint64_t pm = match_any_bits(k, nbits);
     const uint32_t lr = (uint32_t)__popcll(pm & lt);
     uint32_t r = 0;

@@ -443,7 +443,7 @@ k_agg_runs(EncParams a) {
   if (tid == 0 && sfail) atomicOr(&a.diag->flags, OPATTR_F_LIMIT);
 }
 
-void run_enclose_aggregate(const EncArgs &x, hipStream_t s) {
+static EncParams enc_params(const EncArgs &x) {
   const Plan &pl = *x.pl;
   const opattr_kernels *k = x.k;
   EncParams a{};
@@ -461,27 +461,39 @@ void run_enclose_aggregate(const EncArgs &x, hipStream_t s) {
   // the aggregation reads range ids by input range index
   a.R_in = x.r ? x.r->n : 0;
   a.op_in = x.r ? x.r->op_id : nullptr;
-  const unsigned nb = (unsigned)pl.nencb;
-  if (x.mode & 1) {
-    probe_begin(OPATTR_PROBE_MAIN_PASS, s);
-    if (pl.T > 0) k_enclose<<<nb, kEncThreads, 0, s>>>(a);
-    probe_end(OPATTR_PROBE_MAIN_PASS, s);
+  return a;
+}
+
+void run_enclose(const EncArgs &x, hipStream_t s) {
+  const Plan &pl = *x.pl;
+  const EncParams a = enc_params(x);
+  probe_begin(OPATTR_PROBE_MAIN_PASS, s);
+  if (pl.T > 0) k_enclose<<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
+  probe_end(OPATTR_PROBE_MAIN_PASS, s);
+}
+
+void run_aggregate_all(const EncArgs &x, hipStream_t s) {
+  const Plan &pl = *x.pl;
+  EncParams a = enc_params(x);
+  a.ag = agg_inputs(x);
+  a.em = emit_out(x.ws, pl);
+  // look-back states, the start counter, the per-row item counts (and with
+  // no launches the item totals), cleared by one kernel (graph-safe)
+  FillJobs clr;
+  clr.add(a.em.state, 0, 2 * (pl.nencb + 1));
+  clr.add(at<uint32_t>(x.ws, pl.gcnt), 0, pl.G);
+  if (pl.T <= 0) clr.add(a.em.meta, 0, 8);
+  fill_many(clr, s);
+  probe_begin(OPATTR_PROBE_AGG_RUNS, s);
+  if (pl.T > 0) {
+    const unsigned nb = (unsigned)pl.nencb;
+    if (a.ag.maxmask == kDefMaxMask && a.ag.dwmask == kDefDwMask)
+      k_agg_runs<true><<<nb, kEncThreads, 0, s>>>(a);
+    else
+      k_agg_runs<false><<<nb, kEncThreads, 0, s>>>(a);
   }
-  if (x.mode & 2) {
-    a.ag = agg_inputs(x);
-    a.em = emit_out(x.ws, pl);
-    // look-back states and the start counter, cleared by a kernel (graph-safe)
-    fill_u32(reinterpret_cast<uint32_t *>(a.em.state), 0, 2 * (pl.nencb + 1), s);
-    probe_begin(OPATTR_PROBE_AGG_RUNS, s);
-    if (pl.T > 0) {
-      if (a.ag.maxmask == kDefMaxMask && a.ag.dwmask == kDefDwMask)
-        k_agg_runs<true><<<nb, kEncThreads, 0, s>>>(a);
-      else
-        k_agg_runs<false><<<nb, kEncThreads, 0, s>>>(a);
-    }
-    probe_end(OPATTR_PROBE_AGG_RUNS, s);
-    run_aggregate(x, s);
-  }
+  probe_end(OPATTR_PROBE_AGG_RUNS, s);
+  run_aggregate(x, s);
 }
 
 }  // namespace opa

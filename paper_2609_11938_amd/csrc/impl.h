@@ -36,7 +36,7 @@ struct Plan {
   bool seg;  // seq tiles read from per-stream segments (kernels stream-major, seq dense)
   size_t total;
   // IOM
-  size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist, kblk, tbnd;
+  size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist, rs_hist_r, kblk, tbnd;
   size_t tlh, pfh, tlch, pfch, tlc, pfc, off, slot;
   size_t pfirst, plast, pheads, mbs, nbs, rit;
   // ranges
@@ -101,6 +101,15 @@ void column_scan(uint32_t *tab, int64_t rows, uint32_t cols, uint32_t *chs, uint
 bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, int64_t n,
                       int begin_bit, int end_bit, uint32_t *hist, hipStream_t s);
 size_t radix_hist_entries(int64_t n);
+// Several 32-bit fills in one launch (up to 8 arrays).
+struct FillJobs {
+  uint32_t *p[8];
+  uint32_t v[8];
+  int64_t n[8];
+  int count = 0;
+  void add(void *ptr, uint32_t value, int64_t words);
+};
+void fill_many(const FillJobs &j, hipStream_t s);
 // Fill kernels (used instead of memset nodes, which misbehave under graph replay).
 void fill_u32(uint32_t *p, uint32_t v, int64_t n, hipStream_t s);
 void fill_u8(uint8_t *p, uint8_t v, int64_t n, hipStream_t s);
@@ -159,9 +168,7 @@ struct EmitOut {
 };
 EmitOut emit_out(void *ws, const Plan &pl);
 
-enum EncMode { kEncloseOnly = 1, kAggregateOnly = 2, kEncloseAggregate = 3 };
 struct EncArgs {
-  EncMode mode;
   const opattr_kernels *k;
   const opattr_profiled *p;  // aggregation
   const int32_t *match;      // aggregation
@@ -177,7 +184,10 @@ struct EncArgs {
   const Plan *pl;
 };
 AggIn agg_inputs(const EncArgs &x);
-void run_enclose_aggregate(const EncArgs &a, hipStream_t s);
+// range_id of every launch (Alg. 2)
+void run_enclose(const EncArgs &a, hipStream_t s);
+// operator table from range_id and match: run reduction, item sort, rows
+void run_aggregate_all(const EncArgs &a, hipStream_t s);
 void run_aggregate(const EncArgs &a, hipStream_t s);
 
 // ---- finish (api.hip) ---------------------------------------------------------

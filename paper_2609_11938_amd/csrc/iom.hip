@@ -976,10 +976,10 @@ static DedupArgs dedup_args(const opattr_kernels *k, const opattr_dims *d, int32
   return a;
 }
 
-static void clear_partitions(void *ws, const Plan &pl, hipStream_t s) {
-  fill_u32(at<uint32_t>(ws, pl.pfirst), 0xFFFFFFFFu, pl.NP, s);
-  fill_u32(at<uint32_t>(ws, pl.plast), 0xFFFFFFFFu, pl.NP, s);
-  fill_u32(at<uint32_t>(ws, pl.pheads), 0u, pl.NP, s);
+static void clear_partitions(FillJobs &f, void *ws, const Plan &pl) {
+  f.add(at<uint32_t>(ws, pl.pfirst), 0xFFFFFFFFu, pl.NP);
+  f.add(at<uint32_t>(ws, pl.plast), 0xFFFFFFFFu, pl.NP);
+  f.add(at<uint32_t>(ws, pl.pheads), 0u, pl.NP);
 }
 
 void run_match(const IomArgs &x, hipStream_t s) {
@@ -998,9 +998,11 @@ void run_match(const IomArgs &x, hipStream_t s) {
   uint32_t *off = at<uint32_t>(ws, pl.off);
   uint32_t *pfirst = at<uint32_t>(ws, pl.pfirst), *plast = at<uint32_t>(ws, pl.plast);
   uint32_t *pheads = at<uint32_t>(ws, pl.pheads);
-  fill_u32(tlc, 0, NN, s);
-  fill_u32(pfc, 0, NN, s);
-  if (parts) clear_partitions(ws, pl, s);
+  FillJobs clr;
+  clr.add(tlc, 0, NN);
+  clr.add(pfc, 0, NN);
+  if (parts) clear_partitions(clr, ws, pl);
+  fill_many(clr, s);
   if (dedup) k_rep_check<<<(d->n_parts + 255) / 256, 256, 0, s>>>(d->part_rep, d->n_parts, x.diag);
   const TlArgs ta = tl_args(k, d, ws, pl, dedup);
   PfArgs pa;
@@ -1105,7 +1107,9 @@ void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, op
   const TlArgs ta = tl_args(k, d, ws, pl, true);
   const unsigned nb = (unsigned)((pl.T + 255) / 256);
   probe_begin(OPATTR_PROBE_DEDUP, s);
-  clear_partitions(ws, pl, s);
+  FillJobs clr;
+  clear_partitions(clr, ws, pl);
+  fill_many(clr, s);
   k_part_edges<<<(unsigned)pl.nt, 256, 0, s>>>(ta, at<uint32_t>(ws, pl.pfirst),
                                                at<uint32_t>(ws, pl.plast),
                                                at<uint32_t>(ws, pl.pheads));

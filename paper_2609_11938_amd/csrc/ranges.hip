@@ -325,7 +325,7 @@ CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws
     // stream; equal keys keep input order, so identical intervals nest by index
     uint64_t *K[2] = {at<uint64_t>(ws, pl.rsort_k0), at<uint64_t>(ws, pl.rsort_k1)};
     uint32_t *V[2] = {at<uint32_t>(ws, pl.rsort_v0), at<uint32_t>(ws, pl.rsort_v1)};
-    uint32_t *hist = at<uint32_t>(ws, pl.rs_hist);
+    uint32_t *hist = at<uint32_t>(ws, pl.rs_hist_r);
     int cur = 0;
     launch_iota(V[0], R, s);
     launch_gather_key_u64(r->end_ns, V[cur], K[cur], R, true, s);

@@ -180,6 +180,30 @@ __global__ void k_fill_u8(uint8_t *p, uint8_t v, int64_t n) {
 
 static unsigned blocks_for(int64_t n, int b) { return (unsigned)((n + b - 1) / b); }
 
+__global__ void k_fill_many(FillJobs j) {
+  const int q = blockIdx.y;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < j.n[q]; i += stride)
+    j.p[q][i] = j.v[q];
+}
+
+void FillJobs::add(void *ptr, uint32_t value, int64_t words) {
+  if (words <= 0) return;
+  p[count] = static_cast<uint32_t *>(ptr);
+  v[count] = value;
+  n[count] = words;
+  ++count;
+}
+
+void fill_many(const FillJobs &j, hipStream_t s) {
+  if (j.count == 0) return;
+  int64_t mx = 0;
+  for (int q = 0; q < j.count; ++q) mx = j.n[q] > mx ? j.n[q] : mx;
+  int64_t bx = (mx + 255) / 256;
+  if (bx > 1024) bx = 1024;
+  k_fill_many<<<dim3((unsigned)bx, (unsigned)j.count), 256, 0, s>>>(j);
+}
+
 void fill_u32(uint32_t *p, uint32_t v, int64_t n, hipStream_t s) {
   if (n > 0) k_fill_u32<<<blocks_for(n, 256), 256, 0, s>>>(p, v, n);
 }

@@ -123,6 +123,50 @@ def test_layout_promises_validated():
     assert diag2["status"] == -8 and diag2["order_violations"] > 0
 
 
+def test_graph_replay_matches_eager():
+    """A captured opattr_attribute (both stream branches) replays to the eager
+    outputs bit for bit, replay after replay, with eager work in between."""
+    import torch
+
+    tr = _trace("gpt2", "stream_major")
+    dt = opattr.to_device(tr, DEV)
+    ws = opattr.Workspace(DEV)
+    T, R = tr["seq"].size, tr["r_start"].size
+
+    def outs():
+        return opattr.Outputs(
+            match=torch.empty(T, dtype=torch.int32, device=DEV),
+            range_id=torch.empty(T, dtype=torch.int32, device=DEV),
+            range_depth=torch.empty(R, dtype=torch.uint8, device=DEV),
+            name_counts=torch.empty((tr["n_names"], 2), dtype=torch.int32, device=DEV),
+            table=torch.empty((tr["n_ops"] + 1) * 192, dtype=torch.uint8, device=DEV),
+            summary=torch.empty(40, dtype=torch.uint8, device=DEV))
+
+    eager = opattr.opattr_attribute(dt, flags=HINTS, ws=ws, outputs=outs(), raise_strict=False)
+    torch.cuda.synchronize()
+    ref = {k: v.clone() for k, v in eager.items() if v is not None}
+    o = outs()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):  # warm-up on the capture stream
+        opattr.opattr_attribute(dt, flags=HINTS, ws=ws, outputs=o, raise_strict=False)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        opattr.opattr_attribute(dt, flags=HINTS, ws=ws, outputs=o, raise_strict=False)
+    for rep in range(4):
+        for k in ("match", "range_id", "table", "summary", "range_depth", "name_counts"):
+            o[k].fill_(0x5A if o[k].dtype == torch.uint8 else -7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        print(f"case graph replay {rep}", flush=True)
+        for k, v in ref.items():
+            if k == "diag":
+                continue
+            assert torch.equal(o[k], v), (rep, k)
+        assert opattr.read_diag(o["diag"])["status"] == 0
+
+
 @pytest.mark.parametrize("policy", [opattr.MISMATCH_SKIP_NAME, opattr.MISMATCH_STRICT])
 def test_mismatch_policies(policy):
     tr = tg.generate("lstm", T=300_000, ranges=3_000, emission="stream_major")
