@@ -74,6 +74,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.pfirst = b.take(dd ? (size_t)pl.NP * 4 : 0);
   pl.plast = b.take(dd ? (size_t)pl.NP * 4 : 0);
   pl.pheads = b.take(dd ? (size_t)pl.NP * 4 : 0);
+  pl.prec = b.take(dd ? (size_t)pl.NP * 8 : 0);
   pl.mbs = b.take(dd ? T * 4 : 0);
   pl.nbs = b.take(T * 4);  // dedup source names, or the fast path's keys by seq rank
   pl.rit = b.take(T * 2);  // fast path: in-tile rank by seq rank
@@ -223,8 +224,8 @@ static bool check_ranges(const opattr_ranges *r) {
 // two events that fork work onto it from the caller's stream and join it
 // back. NULL when it cannot be created; the caller's stream is used alone.
 struct SideStream {
-  hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
+  hipStream_t s = nullptr, s2 = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr, fork2 = nullptr, join2 = nullptr;
 };
 constexpr int kMaxDevices = 64;
 inline thread_local SideStream g_side[kMaxDevices];
@@ -234,18 +235,19 @@ static SideStream *side_stream() {
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
   SideStream &ss = g_side[dev];
   if (!ss.s) {
-    hipStream_t st = nullptr;
-    hipEvent_t a = nullptr, b = nullptr;
-    if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return nullptr;
-    if (hipEventCreateWithFlags(&a, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&b, hipEventDisableTiming) != hipSuccess) {
-      if (a) (void)hipEventDestroy(a);
-      (void)hipStreamDestroy(st);
+    SideStream n;
+    bool ok = hipStreamCreateWithFlags(&n.s, hipStreamNonBlocking) == hipSuccess &&
+              hipStreamCreateWithFlags(&n.s2, hipStreamNonBlocking) == hipSuccess;
+    for (hipEvent_t *e : {&n.fork, &n.join, &n.fork2, &n.join2})
+      ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
+    if (!ok) {
+      for (hipEvent_t e : {n.fork, n.join, n.fork2, n.join2})
+        if (e) (void)hipEventDestroy(e);
+      for (hipStream_t t : {n.s, n.s2})
+        if (t) (void)hipStreamDestroy(t);
       return nullptr;
     }
-    ss.s = st;
-    ss.fork = a;
-    ss.join = b;
+    ss = n;
   }
   return &ss;
 }
@@ -426,6 +428,11 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   if (ss) note(hipEventRecord(ss->join, s2));
   build_seq_view(k, d, ws, pl, diag, validate, s);
   IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, validate};
+  if (ss) {
+    a.pf_stream = ss->s2;
+    a.pf_fork = ss->fork2;
+    a.pf_join = ss->join2;
+  }
   run_match(a, s);
   if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
   run_aggregate_all(e, s);

@@ -38,7 +38,7 @@ struct Plan {
   // IOM
   size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist, rs_hist_r, kblk, tbnd;
   size_t tlh, pfh, tlch, pfch, tlc, pfc, off, slot;
-  size_t pfirst, plast, pheads, mbs, nbs, rit;
+  size_t pfirst, plast, pheads, prec, mbs, nbs, rit;
   // ranges
   size_t rperm, rs_c, re_c, rst_c, rop_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
@@ -132,8 +132,12 @@ struct IomArgs {
   opattr_diag *diag;
   void *ws;
   const Plan *pl;
-  bool want_dedup;  // also collect partition statistics and dedup sources
+  bool want_dedup;  // also broadcast to duplicate partitions
   bool validate;
+  // optional second stream for the profiled side, with the events that fork
+  // it from and join it back to the main stream
+  hipStream_t pf_stream = nullptr;
+  hipEvent_t pf_fork = nullptr, pf_join = nullptr;
 };
 void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, const Plan &pl,
                     opattr_diag *diag, bool validate, hipStream_t s);

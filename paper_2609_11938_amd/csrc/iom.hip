@@ -167,10 +167,8 @@ __device__ inline uint32_t view_tile(const TlArgs &a, int64_t t, TileData &sm) {
     sm.key[e] = (uint16_t)key;
     sm.lp[e] = lp;
   }
-  if (threadIdx.x == 0) {
-    sm.sg.edge[0] = tl_lp(a, base - 1);
-    sm.sg.edge[1] = tl_lp(a, base + OPA_TILE);
-  }
+  if (threadIdx.x == 0) sm.sg.edge[0] = tl_lp(a, base - 1);
+  if (threadIdx.x == OPA_WAVE) sm.sg.edge[1] = tl_lp(a, base + OPA_TILE);
   __syncthreads();
   return bad;
 }
@@ -200,49 +198,53 @@ __global__ void k_tile_bounds(const uint32_t *__restrict__ seq, const int64_t *_
   bnd[id] = (uint32_t)lo;
 }
 
-// Segment table of tile t in sm.lo / sm.pre (wave 0) and, with edges set,
-// the partitions of the launches with seq base - 1 (wave 1) and base + 4096
-// (wave 2). The caller synchronises.
-__device__ inline void seg_table(const TlArgs &a, int64_t t, SegTable &sm, bool edges) {
+// Segment table of tile t in sm.lo / sm.pre (wave 0; the caller
+// synchronises).
+__device__ inline void seg_table(const TlArgs &a, int64_t t, SegTable &sm) {
+  const int ln = lane_id();
+  const uint64_t T = (uint64_t)a.T;
+  if (wave_id() != 0) return;
+  uint32_t lo = 0, len = 0;
+  if ((uint32_t)ln < a.NS) {
+    uint64_t l = a.bnd[t * a.NS + ln], h = a.bnd[(t + 1) * a.NS + ln];
+    l = l < T ? l : T;
+    h = h < T ? h : T;
+    lo = (uint32_t)l;
+    len = h > l ? (uint32_t)(h - l) : 0u;
+    len = len < OPA_TILE ? len : OPA_TILE;
+  }
+  const uint32_t inc = wave_incl_scan_add(len);
+  sm.lo[ln] = lo;
+  sm.pre[ln] = inc - len;
+  if (ln == OPA_WAVE - 1) sm.pre[OPA_WAVE] = inc;
+}
+
+// Partitions of the launches with seq base - 1 (wave 1) and base + 4096
+// (wave 2) in sm.edge: the last launch before, or the first launch of, some
+// stream's segment (the caller synchronises).
+__device__ inline void seg_edges(const TlArgs &a, int64_t t, SegTable &sm) {
   const int ln = lane_id(), w = wave_id();
+  if (w != 1 && w != 2) return;
   const int64_t base = t * OPA_TILE;
   const uint64_t T = (uint64_t)a.T;
-  if (w == 0) {
-    uint32_t lo = 0, len = 0;
-    if ((uint32_t)ln < a.NS) {
-      uint64_t l = a.bnd[t * a.NS + ln], h = a.bnd[(t + 1) * a.NS + ln];
-      l = l < T ? l : T;
-      h = h < T ? h : T;
-      lo = (uint32_t)l;
-      len = h > l ? (uint32_t)(h - l) : 0u;
-      len = len < OPA_TILE ? len : OPA_TILE;
-    }
-    const uint32_t inc = wave_incl_scan_add(len);
-    sm.lo[ln] = lo;
-    sm.pre[ln] = inc - len;
-    if (ln == OPA_WAVE - 1) sm.pre[OPA_WAVE] = inc;
-  } else if (edges && (w == 1 || w == 2)) {
-    // the launch with seq base - 1 is the last one before some stream's
-    // segment; the one with base + 4096 the first one after
-    const int side = w - 1;
-    const uint64_t want = side ? (uint64_t)base + OPA_TILE : (uint64_t)base - 1;
-    int64_t c = -1;
-    if ((uint32_t)ln < a.NS && (side ? want < T : base > 0)) {
-      const int64_t b = a.bnd[(t + side) * a.NS + ln];
-      const int64_t s0 = a.kblk[ln], s1 = a.kblk[ln + 1];
-      c = side ? b : b - 1;
-      if (c < s0 || c >= s1 || c < 0 || (uint64_t)c >= T || (uint64_t)a.seq[c] != want) c = -1;
-    }
-    const uint64_t m = __ballot(c >= 0);
-    const int src = m ? __ffsll((unsigned long long)m) - 1 : 0;
-    const int64_t cj = __shfl(c, src, OPA_WAVE);
-    int32_t lp = -2;
-    if (cj >= 0) {
-      uint32_t k;
-      tl_classify(a, cj, k, lp);
-    }
-    if (ln == 0) sm.edge[side] = lp;
+  const int side = w - 1;
+  const uint64_t want = side ? (uint64_t)base + OPA_TILE : (uint64_t)base - 1;
+  int64_t c = -1;
+  if ((uint32_t)ln < a.NS && (side ? want < T : base > 0)) {
+    const int64_t b = a.bnd[(t + side) * a.NS + ln];
+    const int64_t s0 = a.kblk[ln], s1 = a.kblk[ln + 1];
+    c = side ? b : b - 1;
+    if (c < s0 || c >= s1 || c < 0 || (uint64_t)c >= T || (uint64_t)a.seq[c] != want) c = -1;
   }
+  const uint64_t m = __ballot(c >= 0);
+  const int src = m ? __ffsll((unsigned long long)m) - 1 : 0;
+  const int64_t cj = __shfl(c, src, OPA_WAVE);
+  int32_t lp = -2;
+  if (cj >= 0) {
+    uint32_t k;
+    tl_classify(a, cj, k, lp);
+  }
+  if (ln == 0) sm.edge[side] = lp;
 }
 
 // Input index of the launch at position e of tile t's segment order (or -1).
@@ -268,7 +270,7 @@ __device__ inline uint32_t seg_tile(const TlArgs &a, int64_t t, TileData &sm) {
     sm.key[x] = (uint16_t)a.NN;
     sm.lp[x] = -2;
   }
-  seg_table(a, t, sm.sg, true);
+  seg_table(a, t, sm.sg);
   __syncthreads();
   // element e = c * 256 + tid: a fixed, unrolled count so that the loads of
   // all chunks are in flight together
@@ -291,6 +293,7 @@ __device__ inline uint32_t seg_tile(const TlArgs &a, int64_t t, TileData &sm) {
     sm.key[x] = (uint16_t)key;
     sm.lp[x] = lp;
   }
+  seg_edges(a, t, sm.sg);  // needed only at the end, so after the tile's loads
   __syncthreads();
   return bad;
 }
@@ -327,10 +330,46 @@ __global__ void __launch_bounds__(256) k_part_edges(TlArgs a, uint32_t *pfirst, 
   part_edges(sm.lp, base, sm.sg.edge[0], sm.sg.edge[1], pfirst, plast, pheads);
 }
 
-// PARTITION error for every partition seen in more than one run
-__global__ void k_part_flags(const uint32_t *__restrict__ pheads, uint32_t NP, opattr_diag *diag) {
-  const uint32_t q = blockIdx.x * blockDim.x + threadIdx.x;
-  const bool nc = q < NP && pheads[q] > 1;
+// Per partition p, how its launches find their row (fast path lookup):
+//   hi == kRecEligible  p is its own class representative: its launches rank
+//                       themselves;
+//   hi == kRecNone      p has no valid representative: no row, no dedup error;
+//   otherwise           a duplicate: the launch at seq rank x takes the rank of
+//                       the launch at x + delta when x < hi (the representative
+//                       partition is shorter otherwise), else a dedup error;
+//                       hi == 0 when either partition is not one run.
+// Also raises PARTITION for every partition seen in more than one run.
+struct PartRec {
+  int32_t delta;
+  uint32_t hi;
+};
+constexpr uint32_t kRecEligible = 0xFFFFFFFFu, kRecNone = 0xFFFFFFFEu;
+
+__global__ void k_part_prep(const int32_t *__restrict__ part_rep, uint32_t NP,
+                            const uint32_t *__restrict__ pfirst, const uint32_t *__restrict__ plast,
+                            const uint32_t *__restrict__ pheads, PartRec *prec,
+                            opattr_diag *diag) {
+  const uint32_t p = blockIdx.x * blockDim.x + threadIdx.x;
+  bool nc = false;
+  if (p < NP) {
+    nc = pheads[p] > 1;
+    if (prec) {
+      const int32_t r = part_rep[p];
+      PartRec q{0, kRecNone};
+      if (r == (int32_t)p) {
+        q.hi = kRecEligible;
+      } else if (r >= 0 && (uint32_t)r < NP) {
+        q.hi = 0;
+        const uint32_t f = pfirst[r];
+        if (pheads[p] == 1u && pheads[r] == 1u && part_rep[r] == r && f != 0xFFFFFFFFu) {
+          q.delta = (int32_t)(f - pfirst[p]);
+          const uint64_t hi = (uint64_t)pfirst[p] + (plast[r] - f + 1u);
+          q.hi = (uint32_t)(hi < 0x7FFFFFFFull ? hi : 0x7FFFFFFFull);  // seq ranks are < 2^31
+        }
+      }
+      prec[p] = q;
+    }
+  }
   if (__ballot(nc) && lane_id() == 0) atomicOr(&diag->flags, OPATTR_F_PARTITION);
 }
 
@@ -402,7 +441,7 @@ struct LookArgs {
   const int32_t *slot;
   const uint16_t *rit;
   const uint32_t *kbs;
-  const uint32_t *pfirst, *plast, *pheads;  // pheads NULL: no dedup broadcast
+  const PartRec *prec;  // NULL: no dedup broadcast (duplicates get -1)
   int32_t *match;
   int skip_name;
   opattr_diag *diag;
@@ -424,7 +463,7 @@ __global__ void __launch_bounds__(256) k_tl_look(TlArgs a, LookArgs m) {
   const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
   const uint32_t NN = a.NN;
   if (tid == 0) serr = 0;
-  if (SEG) seg_table(a, tile, sm, false);
+  if (SEG) seg_table(a, tile, sm);
   __syncthreads();
   // phase 1: input index and seq rank of each element
   int64_t ii[kWaveChunks];
@@ -441,38 +480,37 @@ __global__ void __launch_bounds__(256) k_tl_look(TlArgs a, LookArgs m) {
     xs[c] = SEG ? (ii[c] >= 0 ? a.seq[ii[c]] : 0u) : (uint32_t)(base + e);
     if (SEG && (int64_t)xs[c] >= a.T) ii[c] = -1;  // a broken promise: left out
   }
-  // phase 2: ids, class representative
+  // phase 2: ids, then how each launch finds its row
   uint32_t nm[kWaveChunks];
-  int32_t pt[kWaveChunks], rp[kWaveChunks];
+  int32_t pt[kWaveChunks];
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
     nm[c] = ii[c] >= 0 ? a.name[ii[c]] : NN;
     pt[c] = (ii[c] >= 0 && a.part) ? a.part[ii[c]] : -1;
   }
+  PartRec rc[kWaveChunks];
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
     const bool good = nm[c] < NN && pt[c] >= -1 && (pt[c] < 0 || (uint32_t)pt[c] < a.NP);
-    rp[c] = -2;  // -2: neither eligible nor a duplicate
-    if (good) rp[c] = pt[c] < 0 ? pt[c] : a.part_rep[pt[c]];
+    rc[c] = PartRec{0, kRecNone};
+    if (!good || ii[c] < 0) continue;
+    if (pt[c] < 0) rc[c].hi = kRecEligible;
+    else if (m.prec) rc[c] = m.prec[pt[c]];
+    else if (a.part_rep[pt[c]] == pt[c]) rc[c].hi = kRecEligible;
   }
-  // phase 3: the position whose rank gives the row (own, or the
-  // representative's launch at the same position)
+  // phase 3: the seq rank whose rank gives the row (own, or the launch at the
+  // same position of the representative partition, if it has this name)
   uint32_t src[kWaveChunks];
   uint32_t err = 0;
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
     src[c] = 0xFFFFFFFFu;
-    if (ii[c] < 0 || rp[c] == -2) continue;
-    if (pt[c] < 0 || rp[c] == pt[c]) {
-      src[c] = xs[c];  // eligible
-    } else if (m.pheads && rp[c] >= 0 && (uint32_t)rp[c] < a.NP) {
-      const int32_t r = rp[c], p = pt[c];
-      const uint32_t f = m.pfirst[r];
-      bool ok = m.pheads[p] == 1u && m.pheads[r] == 1u && a.part_rep[r] == r && f != 0xFFFFFFFFu;
-      const uint32_t pos = xs[c] - m.pfirst[p];
-      ok = ok && pos < m.plast[r] - f + 1u;
-      ok = ok && m.kbs[f + pos] == nm[c];
-      if (ok) src[c] = f + pos;
+    const uint32_t hi = rc[c].hi;
+    if (hi == kRecEligible) {
+      src[c] = xs[c];
+    } else if (hi != kRecNone) {
+      const uint32_t y = xs[c] + (uint32_t)rc[c].delta;
+      if (xs[c] < hi && m.kbs[y] == nm[c]) src[c] = y;
       else err++;
     }
   }
@@ -774,33 +812,39 @@ void column_scan(uint32_t *tab, int64_t rows, uint32_t cols, uint32_t *chs, uint
   k_colbase<<<g, 256, 0, s>>>(tab, rows, cols, chs, rows_dev);
 }
 
-// off[n] = rows of names before n; count validation (Sec. 3.3)
-__global__ void __launch_bounds__(1024) k_names(const uint32_t *__restrict__ tlc,
-                                                const uint32_t *__restrict__ pfc, uint32_t NN,
-                                                uint32_t *off, uint32_t *name_counts,
-                                                opattr_diag *diag, int strict) {
+// off[n] = rows of names before n (one block)
+__global__ void __launch_bounds__(1024) k_pf_off(const uint32_t *__restrict__ pfc, uint32_t NN,
+                                                 uint32_t *off) {
   __shared__ uint32_t sh[16];
-  __shared__ unsigned long long red[3][16];
   uint32_t carry = 0;
-  unsigned long long mism = 0, tlu = 0, pfu = 0;
   for (uint32_t base = 0; base < NN; base += 1024) {
     const uint32_t n = base + threadIdx.x;
-    const uint32_t tl = n < NN ? tlc[n] : 0u, pf = n < NN ? pfc[n] : 0u;
+    const uint32_t pf = n < NN ? pfc[n] : 0u;
     uint32_t tot;
     const uint32_t pre = block_excl_scan_add<uint32_t>(pf, sh, &tot);
-    if (n < NN) {
-      off[n] = carry + pre;
-      if (name_counts) {
-        name_counts[2 * (size_t)n] = tl;
-        name_counts[2 * (size_t)n + 1] = pf;
-      }
-      if (tl != pf) {
-        mism++;
-        if (tl > pf) tlu += tl - pf;
-        else pfu += pf - tl;
-      }
-    }
+    if (n < NN) off[n] = carry + pre;
     carry += tot;
+  }
+}
+
+// count validation (Sec. 3.3): per name, eligible launches against rows
+__global__ void __launch_bounds__(1024) k_names(const uint32_t *__restrict__ tlc,
+                                                const uint32_t *__restrict__ pfc, uint32_t NN,
+                                                uint32_t *name_counts, opattr_diag *diag,
+                                                int strict) {
+  __shared__ unsigned long long red[3][16];
+  unsigned long long mism = 0, tlu = 0, pfu = 0;
+  for (uint32_t n = threadIdx.x; n < NN; n += 1024) {
+    const uint32_t tl = tlc[n], pf = pfc[n];
+    if (name_counts) {
+      name_counts[2 * (size_t)n] = tl;
+      name_counts[2 * (size_t)n + 1] = pf;
+    }
+    if (tl != pf) {
+      mism++;
+      if (tl > pf) tlu += tl - pf;
+      else pfu += pf - tl;
+    }
   }
   mism = wave_reduce_add(mism);
   tlu = wave_reduce_add(tlu);
@@ -1009,6 +1053,30 @@ void run_match(const IomArgs &x, hipStream_t s) {
   pa.name = x.p->name_id;
   pa.P = pl.P;
   pa.NN = NN;
+  // the profiled side depends only on the row names: it runs on its own
+  // stream when one is given, joined back before the lookups
+  const hipStream_t sp = x.pf_stream ? x.pf_stream : s;
+  if (sp != s) {
+    note(hipEventRecord(x.pf_fork, s));
+    note(hipStreamWaitEvent(sp, x.pf_fork, 0));
+  }
+  probe_begin(OPATTR_PROBE_PF_HIST, sp);
+  if (pl.ntp > 0) {
+    if (fast_pf) k_pf_hist_w<<<(unsigned)pl.ntp, 256, lds, sp>>>(pa, pfh, x.diag);
+    else k_pf_hist<<<(unsigned)pl.ntp, 256, 0, sp>>>(pa, pfh, x.diag);
+  }
+  probe_end(OPATTR_PROBE_PF_HIST, sp);
+  column_scan(pfh, pl.ntp, NN, at<uint32_t>(ws, pl.pfch), pfc, sp, nullptr);
+  if (NN) k_pf_off<<<1, 1024, 0, sp>>>(pfc, NN, off);
+  probe_begin(OPATTR_PROBE_PF_SLOT, sp);
+  if (pl.ntp > 0) {
+    if (fast_pf) k_pf_slot_w<<<(unsigned)pl.ntp, 256, lds, sp>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
+    else k_pf_slot<<<(unsigned)pl.ntp, 256, 0, sp>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
+  }
+  probe_end(OPATTR_PROBE_PF_SLOT, sp);
+  if (sp != s) note(hipEventRecord(x.pf_join, sp));
+
+  // the timeline side
   if (seg && pl.nt > 0) {
     launch_stream_blocks(k->stream_id, pl.T, pl.NS, at<int64_t>(ws, pl.kblk), s);
     const int64_t nb = (pl.nt + 1) * pl.NS;
@@ -1035,27 +1103,17 @@ void run_match(const IomArgs &x, hipStream_t s) {
     }
   }
   probe_end(OPATTR_PROBE_TL_HIST, s);
+  PartRec *prec = (parts && fast) ? at<PartRec>(ws, pl.prec) : nullptr;
   if (parts && pl.nt > 0)
-    k_part_flags<<<(unsigned)((pl.NP + 255) / 256), 256, 0, s>>>(pheads, pl.NP, x.diag);
-  probe_begin(OPATTR_PROBE_PF_HIST, s);
-  if (pl.ntp > 0) {
-    if (fast_pf) k_pf_hist_w<<<(unsigned)pl.ntp, 256, lds, s>>>(pa, pfh, x.diag);
-    else k_pf_hist<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, x.diag);
-  }
-  probe_end(OPATTR_PROBE_PF_HIST, s);
+    k_part_prep<<<(unsigned)((pl.NP + 255) / 256), 256, 0, s>>>(d->part_rep, pl.NP, pfirst, plast,
+                                                                pheads, prec, x.diag);
   probe_begin(OPATTR_PROBE_COL_SCAN, s);
   column_scan(tlh, pl.nt, NN, at<uint32_t>(ws, pl.tlch), tlc, s, nullptr);
-  column_scan(pfh, pl.ntp, NN, at<uint32_t>(ws, pl.pfch), pfc, s, nullptr);
-  if (NN)
-    k_names<<<1, 1024, 0, s>>>(tlc, pfc, NN, off, x.name_counts, x.diag,
-                               x.policy == OPATTR_MISMATCH_STRICT ? 1 : 0);
   probe_end(OPATTR_PROBE_COL_SCAN, s);
-  probe_begin(OPATTR_PROBE_PF_SLOT, s);
-  if (pl.ntp > 0) {
-    if (fast_pf) k_pf_slot_w<<<(unsigned)pl.ntp, 256, lds, s>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
-    else k_pf_slot<<<(unsigned)pl.ntp, 256, 0, s>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
-  }
-  probe_end(OPATTR_PROBE_PF_SLOT, s);
+  if (sp != s) note(hipStreamWaitEvent(s, x.pf_join, 0));
+  if (NN)
+    k_names<<<1, 1024, 0, s>>>(tlc, pfc, NN, x.name_counts, x.diag,
+                               x.policy == OPATTR_MISMATCH_STRICT ? 1 : 0);
   probe_begin(OPATTR_PROBE_TL_MATCH, s);
   if (pl.nt > 0) {
     if (fast) {
@@ -1067,9 +1125,7 @@ void run_match(const IomArgs &x, hipStream_t s) {
       m.slot = at<int32_t>(ws, pl.slot);
       m.rit = ho.rit;
       m.kbs = ho.kbs;
-      m.pfirst = pfirst;
-      m.plast = plast;
-      m.pheads = parts ? pheads : nullptr;
+      m.prec = prec;
       m.match = x.match;
       m.skip_name = x.policy == OPATTR_MISMATCH_SKIP_NAME ? 1 : 0;
       m.diag = x.diag;
@@ -1113,8 +1169,9 @@ void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, op
   k_part_edges<<<(unsigned)pl.nt, 256, 0, s>>>(ta, at<uint32_t>(ws, pl.pfirst),
                                                at<uint32_t>(ws, pl.plast),
                                                at<uint32_t>(ws, pl.pheads));
-  k_part_flags<<<(unsigned)((pl.NP + 255) / 256), 256, 0, s>>>(at<uint32_t>(ws, pl.pheads), pl.NP,
-                                                              diag);
+  k_part_prep<<<(unsigned)((pl.NP + 255) / 256), 256, 0, s>>>(
+      d->part_rep, pl.NP, at<uint32_t>(ws, pl.pfirst), at<uint32_t>(ws, pl.plast),
+      at<uint32_t>(ws, pl.pheads), nullptr, diag);
   k_src_fill<<<nb, 256, 0, s>>>(a);
   k_dedup<<<nb, 256, 0, s>>>(a);
   probe_end(OPATTR_PROBE_DEDUP, s);
