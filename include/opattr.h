@@ -231,7 +231,8 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
 /* Probe events (diagnostics, per host thread). events is a host array of
    2*n hipEvent_t values; while set, every later call on this thread records
    events[2*i] on its stream right before the launches of probe i and
-   events[2*i+1] right after them, for the probes below that the call runs.
+   events[2*i+1] right after them, for the probes below that the call runs;
+   a NULL entry is not recorded (each recorded event is a stream barrier).
    NULL (or n = 0) switches probing off. The events are the caller's. */
 enum {
   OPATTR_PROBE_SEQ_VIEW = 0,   /* launch-order view of the timeline          */
@@ -242,11 +243,12 @@ enum {
   OPATTR_PROBE_TL_MATCH = 5,   /* per-tile rank and join                    */
   OPATTR_PROBE_DEDUP = 6,      /* dedup broadcast                           */
   OPATTR_PROBE_RANGES = 7,     /* range order, parents and depths           */
-  OPATTR_PROBE_MAIN_PASS = 8,  /* enclosure pass (range ids)                */
+  OPATTR_PROBE_MAIN_PASS = 8,  /* enclosure pass (range ids, item plan)     */
   OPATTR_PROBE_FINALIZE = 9,   /* status of the diag record                 */
-  OPATTR_PROBE_AGGREGATE = 10, /* item sort, per-row reduction, table       */
+  OPATTR_PROBE_AGGREGATE = 10, /* per-row reduction of the items, table    */
   OPATTR_PROBE_AGG_RUNS = 11,  /* in-place run reduction over the launches  */
-  OPATTR_NUM_PROBES = 12
+  OPATTR_PROBE_ITEM_SORT = 12, /* sort of the planned items by operator row */
+  OPATTR_NUM_PROBES = 13
 };
 int opattr_set_probe_events(void *const *events, int n);
 

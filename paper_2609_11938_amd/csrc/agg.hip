@@ -1,10 +1,11 @@
 // Per-operator aggregation (Eq. 1, Sec. 3.8.1), second and third levels.
 //
-// The enclosure pass leaves, in launch order, items of one operator row each:
-// either a partial row (a run it reduced in place) or a reference to at most
-// 16 launches. Here the items are
+// The enclosure pass plans, in launch order, items of one operator row each:
+// either a partial row (a run reduced in place once the matches are known)
+// or a reference to at most 16 launches. Here the items are
 //   1. counting-sorted by row (per-tile row histograms scanned down the
-//      columns; stable, so each row keeps its items in launch order),
+//      columns; stable, so each row keeps its items in launch order); this
+//      needs only the rows, so it runs beside the matching,
 //   2. cut into chunks of at most 64 items of one row, each reduced by one
 //      wave (a lane loads a partial row or accumulates its referenced
 //      launches, then a butterfly reduction),
@@ -22,14 +23,13 @@ constexpr int kChunkItems = 64;
 
 EmitOut emit_out(void *ws, const Plan &pl) {
   EmitOut e;
-  e.state = at<unsigned long long>(ws, pl.lbs);
-  e.ctr = reinterpret_cast<uint32_t *>(e.state + pl.nencb);
+  e.wi = at<uint32_t>(ws, pl.wi);
+  e.wr = at<uint32_t>(ws, pl.wr);
   e.ig = at<uint32_t>(ws, pl.ig);
   e.ia = at<uint32_t>(ws, pl.ia);
   e.ib = at<uint32_t>(ws, pl.ib);
   e.rows = at<PartRow>(ws, pl.rows);
   e.meta = at<int64_t>(ws, pl.meta);
-  e.nblocks = pl.nencb;
   return e;
 }
 
@@ -56,7 +56,8 @@ struct AggWork {
   const uint32_t *ig, *ia, *ib;
   const PartRow *rows;
   int64_t *meta;  // [0] items, [1] partial rows, [2] item tiles, [3] chunks
-  uint32_t *ith, *gcnt, *goff, *coff, *cmap, *sidx;
+  uint32_t *ith, *gcnt, *goff, *coff, *cmap;
+  unsigned long long *sit;  // sorted items: partial-row index or first launch | length << 32
   PartRow *part;
   opattr_op_row *table;
   opattr_summary *sum;
@@ -156,7 +157,8 @@ __global__ void __launch_bounds__(256) k_item_scatter_w(AggWork w) {
     for (int c = 0; c < 16; ++c) {
       const uint32_t g = key[c];
       if (g >= w.G) continue;
-      w.sidx[w.goff[g] + row[g] + wb[g] + rank[c]] = (uint32_t)item_x(tile, c);
+      const int64_t x = item_x(tile, c);
+      w.sit[w.goff[g] + row[g] + wb[g] + rank[c]] = w.ia[x] | ((unsigned long long)w.ib[x] << 32);
     }
   }
 }
@@ -180,8 +182,9 @@ __global__ void __launch_bounds__(256) k_item_scatter_r(AggWork w) {
       const uint32_t g = key >> OPA_SLOT_BITS;
       if (g >= w.G) continue;
       const int lo = lds_lower_bound(sm.A, OPA_TILE, g << OPA_SLOT_BITS);
-      w.sidx[w.goff[g] + row[g] + (uint32_t)(p - lo)] =
-          (uint32_t)(tile * OPA_TILE + (key & (OPA_TILE - 1)));
+      const int64_t x = tile * OPA_TILE + (key & (OPA_TILE - 1));
+      w.sit[w.goff[g] + row[g] + (uint32_t)(p - lo)] =
+          w.ia[x] | ((unsigned long long)w.ib[x] << 32);
     }
   }
 }
@@ -206,8 +209,8 @@ __global__ void __launch_bounds__(256) k_chunk_reduce(AggWork w) {
     Acc acc;
     acc_zero(acc);
     if (p < w.goff[g + 1]) {
-      const uint32_t it = w.sidx[p];
-      const uint32_t a = w.ia[it], b = w.ib[it];
+      const unsigned long long it = w.sit[p];
+      const uint32_t a = (uint32_t)it, b = (uint32_t)(it >> 32);
       if (b == 0) {
         acc_load(acc, w.rows + a);
       } else {
@@ -296,7 +299,7 @@ __global__ void __launch_bounds__(1024) k_summary(AggWork w) {
   }
 }
 
-void run_aggregate(const EncArgs &x, hipStream_t s) {
+static AggWork agg_work(const EncArgs &x) {
   const Plan &pl = *x.pl;
   AggWork w{};
   w.G = pl.G;
@@ -313,18 +316,22 @@ void run_aggregate(const EncArgs &x, hipStream_t s) {
   w.goff = at<uint32_t>(x.ws, pl.goff);
   w.coff = at<uint32_t>(x.ws, pl.coff);
   w.cmap = at<uint32_t>(x.ws, pl.cmap);
-  w.sidx = at<uint32_t>(x.ws, pl.sidx);
+  w.sit = at<unsigned long long>(x.ws, pl.sit);
   w.part = at<PartRow>(x.ws, pl.part);
   w.table = x.table;
   w.sum = x.sum;
+  return w;
+}
+
+void plan_items(const EncArgs &x, hipStream_t s) {
+  const Plan &pl = *x.pl;
+  AggWork w = agg_work(x);
   const bool fast = pl.G <= kFastKeys;
-  const bool def = w.in.maxmask == kDefMaxMask && w.in.dwmask == kDefDwMask;
   const size_t lds = (size_t)4 * pl.G * sizeof(uint16_t);
   const unsigned tgrid = (unsigned)(pl.ntrt < 1024 ? (pl.ntrt > 0 ? pl.ntrt : 1) : 1024);
-
   // gcnt (and meta when there are no launches) were cleared with the
   // look-back states
-  probe_begin(OPATTR_PROBE_AGGREGATE, s);
+  probe_begin(OPATTR_PROBE_ITEM_SORT, s);
   if (pl.T > 0) {
     if (fast) k_item_hist_w<<<tgrid, 256, lds, s>>>(w);
     else k_item_hist_r<<<tgrid, 256, 0, s>>>(w);
@@ -335,6 +342,16 @@ void run_aggregate(const EncArgs &x, hipStream_t s) {
     if (fast) k_item_scatter_w<<<tgrid, 256, lds, s>>>(w);
     else k_item_scatter_r<<<tgrid, 256, 0, s>>>(w);
     k_chunk_map<<<(pl.G + 255) / 256, 256, 0, s>>>(w);
+  }
+  probe_end(OPATTR_PROBE_ITEM_SORT, s);
+}
+
+void reduce_items(const EncArgs &x, hipStream_t s) {
+  const Plan &pl = *x.pl;
+  AggWork w = agg_work(x);
+  const bool def = w.in.maxmask == kDefMaxMask && w.in.dwmask == kDefDwMask;
+  probe_begin(OPATTR_PROBE_AGGREGATE, s);
+  if (pl.T > 0) {
     const int64_t want = (pl.max_chunks + 3) / 4;
     const unsigned cgrid = (unsigned)(want < 2048 ? want : 2048);
     if (def) k_chunk_reduce<true><<<cgrid, 256, 0, s>>>(w);

@@ -107,7 +107,8 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.cap_items = pl.T;
   pl.cap_rows = pl.nencb * (kEncThreads / OPA_WAVE) * kEncRowsPerWave;
   pl.max_chunks = pl.T / 64 + pl.G + 1;
-  pl.lbs = b.take(((size_t)pl.nencb + 1) * 8);
+  pl.wi = b.take((size_t)pl.nencb * (kEncThreads / OPA_WAVE) * 4);
+  pl.wr = b.take((size_t)pl.nencb * (kEncThreads / OPA_WAVE) * 4);
   pl.ig = b.take((size_t)pl.cap_items * 4);
   pl.ia = b.take((size_t)pl.cap_items * 4);
   pl.ib = b.take((size_t)pl.cap_items * 4);
@@ -119,7 +120,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.goff = b.take(((size_t)pl.G + 1) * 4);
   pl.coff = b.take(((size_t)pl.G + 1) * 4);
   pl.cmap = b.take((size_t)pl.max_chunks * 4);
-  pl.sidx = b.take((size_t)pl.cap_items * 4);
+  pl.sit = b.take((size_t)pl.cap_items * 8);
   pl.part = b.take((size_t)pl.max_chunks * 200);
   pl.misc = b.take(256);
   pl.total = b.off;
@@ -398,8 +399,9 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   hipStream_t s = (hipStream_t)stream;
   check_kernel_layout(k, d, diag, s);
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
-  // the ranges and the enclosure do not depend on the matching: they run on
-  // a side stream of this device, joined back before the aggregation
+  // the ranges, the enclosure and the aggregation plan do not depend on the
+  // matching: they run on a side stream of this device, joined back before
+  // the reduction
   SideStream *ss = side_stream();
   const hipStream_t s2 = ss ? ss->s : s;
   if (ss) {
@@ -424,7 +426,7 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   e.diag = diag;
   e.ws = ws;
   e.pl = &pl;
-  run_enclose(e, s2);
+  run_enclose_plan(e, s2);
   if (ss) note(hipEventRecord(ss->join, s2));
   build_seq_view(k, d, ws, pl, diag, validate, s);
   IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, validate};
@@ -435,7 +437,7 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   }
   run_match(a, s);
   if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
-  run_aggregate_all(e, s);
+  run_reduce(e, s);
   launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s);
   return launch_status();
 }

@@ -1,5 +1,7 @@
 // Enclosure (Alg. 2) and the first level of the aggregation (Eq. 1), two
-// passes over the launches in storage order.
+// passes over the launches in storage order: the enclosure, which also plans
+// the aggregation's items (it needs only the operator row of each launch),
+// and the in-place reduction of the runs (which needs the matches).
 //
 // A block takes 2048 consecutive launches, eight consecutive ones per thread.
 // Enclosure: the range starts that can matter for the block's main stream
@@ -10,14 +12,15 @@
 // the query point.
 //
 // Aggregation: each wave cuts its 512 launches into runs of one operator row.
-// With at most kRowCap runs the wave reduces them in place: every thread
-// accumulates its launches in registers, leaving each run that ends inside it
-// in an LDS row, and a segmented scan over the lanes carries the runs that
-// cross threads. The rows then go out with coalesced stores. With more runs
-// the wave writes references (row, first launch, length <= 16) that the
-// per-row reduction resolves later. Partial rows and references land in
-// launch order at offsets found by a decoupled look-back over the blocks,
-// which take their positions from a counter in the order they start.
+// Plan: a wave with at most kRowCap runs will reduce them in place and emits
+// one item (row, partial-row index) per run; a wave with more runs emits
+// references (row, first launch, length <= 16) that the per-row reduction
+// resolves later. The enclosure pass counts each wave's items and partial
+// rows, a scan over the waves turns the counts into bases, and an emission
+// pass writes the items in launch order. Reduction: every thread accumulates
+// its launches in registers, leaving each run that ends inside it in an LDS
+// row, and a segmented scan over the lanes carries the runs that cross
+// threads; the rows then go out with coalesced stores at the planned indices.
 #include "accum.h"
 #include "common.h"
 #include "impl.h"
@@ -27,8 +30,6 @@ namespace opa {
 constexpr int kPer = 8;                         // launches per thread
 constexpr int kSpan = kEncThreads * kPer;       // launches per block
 constexpr int kRowCap = 32;                     // runs a wave reduces in place
-constexpr unsigned long long kLbAgg = 1ull << 62, kLbInc = 2ull << 62;
-constexpr long kLbSpinLimit = 1l << 26;
 
 static_assert(kSpan == kEncSpan, "block span");
 static_assert(kEncRowsPerWave == kRowCap, "row cap");
@@ -124,148 +125,235 @@ __device__ __forceinline__ uint32_t pick(const uint32_t (&g)[kPer], int k) {
   return r;
 }
 
-__device__ __forceinline__ unsigned long long lb_load(const unsigned long long *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void lb_store(unsigned long long *p, unsigned long long v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// state word: flag (2 bits) | items (31 bits) | rows (31 bits)
-__device__ __forceinline__ unsigned long long lb_pack(unsigned long long flag, uint32_t items,
-                                                      uint32_t rows) {
-  return flag | ((unsigned long long)items << 31) | rows;
-}
-
-// Exclusive prefix of (items, rows) over the blocks before bid; one wave.
-// Returns false if the wait bound ran out (reported as a limit error).
-__device__ inline bool lookback(const unsigned long long *state, int64_t bid, uint32_t &items,
-                                uint32_t &rows) {
-  const int ln = lane_id();
-  unsigned long long si = 0, sr = 0;
-  int64_t j = bid - 1;
-  long spins = 0;
-  while (j >= 0) {
-    const int64_t idx = j - ln;
-    unsigned long long st = idx >= 0 ? lb_load(state + idx) : kLbInc;
-    unsigned long long flag = st & (3ull << 62);
-    const unsigned long long inc = __ballot(flag == kLbInc);
-    // lanes up to and including the nearest inclusive predecessor matter
-    const int last = inc ? __ffsll(inc) - 1 : OPA_WAVE - 1;
-    const unsigned long long need = last == 63 ? ~0ull : ((2ull << last) - 1);
-    if (__ballot(flag == 0) & need) {
-      if (++spins > kLbSpinLimit) return false;
-      __builtin_amdgcn_s_sleep(1);
-      continue;
-    }
-    unsigned long long ci = ln <= last ? ((st >> 31) & 0x7FFFFFFFull) : 0;
-    unsigned long long cr = ln <= last ? (st & 0x7FFFFFFFull) : 0;
-    si += wave_reduce_add(ci);
-    sr += wave_reduce_add(cr);
-    if (inc) break;
-    j -= OPA_WAVE;
+// The operator rows of a thread's launches from input range ids (plan from a
+// given range_id array, and the reduction). Counts malformed range ids.
+__device__ __forceinline__ uint32_t rows_from_ids(const EncParams &a, int64_t ib, int nv,
+                                                  uint32_t (&g)[kPer]) {
+  int32_t rin[kPer];
+  load_run(a.range_id, ib, nv, rin);
+  uint32_t bad = 0;
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    g[k] = k < nv ? a.NOPS : 0xFFFFFFFFu;
+    if (k >= nv) continue;
+    const int32_t r = rin[k];
+    if (r >= 0 && r < a.R_in && a.op_in[r] < a.NOPS) g[k] = a.op_in[r];
+    else if (r < -1 || r >= a.R_in || r >= 0) bad++;
   }
-  items = (uint32_t)si;
-  rows = (uint32_t)sr;
-  return true;
+  return bad;
 }
 
+// Run starts of a thread's launches inside its wave (bit k: launch k starts
+// a run; the wave's first launch always does), and the references' piece
+// starts (runs cut at every 16th launch as well).
+__device__ __forceinline__ void run_heads(const uint32_t (&g)[kPer], int nv, uint32_t &hm,
+                                          uint32_t &hp) {
+  const int ln = lane_id();
+  const uint32_t gl = __shfl_up(g[kPer - 1], 1, OPA_WAVE);
+  hm = 0;
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const uint32_t prev = k ? g[k - 1] : (ln ? gl : 0xFFFFFFFFu);
+    if (k < nv && g[k] != prev) hm |= 1u << k;
+  }
+  hp = hm | ((nv > 0 && (ln & 1) == 0) ? 1u : 0u);
+}
+
+// Items and partial rows of the calling wave (all lanes get them).
+__device__ __forceinline__ void wave_counts(uint32_t hm, uint32_t hp, uint32_t &items,
+                                            uint32_t &rows) {
+  const uint32_t nr = wave_reduce_add((uint32_t)__popc(hm));
+  const uint32_t np = wave_reduce_add((uint32_t)__popc(hp));
+  const bool rowmode = nr <= (uint32_t)kRowCap;
+  items = rowmode ? nr : np;
+  rows = rowmode ? nr : 0u;
+}
+
+// MODE 1: range ids; MODE 3: range ids and the per-wave item and row counts;
+// MODE 2: the counts from a given range_id array.
+template <int MODE>
 __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
-  __shared__ uint64_t sS[kEncWindow];
+  __shared__ uint64_t sS[(MODE & 1) ? kEncWindow : 1];
   __shared__ uint64_t red[2][kEncThreads / OPA_WAVE];
   __shared__ int64_t win[2];
   __shared__ uint32_t sbad;
   const int tid = threadIdx.x, w = wave_id(), ln = lane_id();
   if (tid == 0) sbad = 0;
-  const int64_t i0 = (int64_t)blockIdx.x * kSpan;
+  if (MODE == 2) __syncthreads();
+  const int64_t bid = blockIdx.x;
+  const int64_t i0 = bid * kSpan;
   const int64_t ib = i0 + (int64_t)tid * kPer;
   const int nv = (int)(a.T - ib < 0 ? 0 : (a.T - ib < kPer ? a.T - ib : kPer));
   uint32_t bad = 0;
-  uint16_t st[kPer];
-  uint64_t q[kPer];
-  load_run(a.stream, ib, nv, st);
-  load_run(a.q, ib, nv, q);
-  const uint16_t s0 = a.stream[i0];
-  // smallest and largest query point of the block's main stream
-  uint64_t mn = ~0ull, mx = 0ull;
+  uint32_t g[kPer];
+  if (MODE & 1) {
+    uint16_t st[kPer];
+    uint64_t q[kPer];
+    load_run(a.stream, ib, nv, st);
+    load_run(a.q, ib, nv, q);
+    const uint16_t s0 = a.stream[i0];
+    // smallest and largest query point of the block's main stream
+    uint64_t mn = ~0ull, mx = 0ull;
 #pragma unroll
-  for (int k = 0; k < kPer; ++k)
-    if (k < nv && st[k] == s0) {
-      mn = q[k] < mn ? q[k] : mn;
-      mx = q[k] > mx ? q[k] : mx;
+    for (int k = 0; k < kPer; ++k)
+      if (k < nv && st[k] == s0) {
+        mn = q[k] < mn ? q[k] : mn;
+        mx = q[k] > mx ? q[k] : mx;
+      }
+    for (int o = OPA_WAVE / 2; o > 0; o >>= 1) {
+      const uint64_t y = __shfl_xor(mn, o, OPA_WAVE), z = __shfl_xor(mx, o, OPA_WAVE);
+      mn = y < mn ? y : mn;
+      mx = z > mx ? z : mx;
     }
-  for (int o = OPA_WAVE / 2; o > 0; o >>= 1) {
-    const uint64_t y = __shfl_xor(mn, o, OPA_WAVE), z = __shfl_xor(mx, o, OPA_WAVE);
-    mn = y < mn ? y : mn;
-    mx = z > mx ? z : mx;
-  }
-  if (ln == 0) {
-    red[0][w] = mn;
-    red[1][w] = mx;
-  }
-  __syncthreads();
-  // wave 0 finds the window start, wave 1 its end
-  if (w < 2) {
-    uint64_t qa = ~0ull, qb = 0;
-    for (int k = 0; k < kEncThreads / OPA_WAVE; ++k) {
-      qa = red[0][k] < qa ? red[0][k] : qa;
-      qb = red[1][k] > qb ? red[1][k] : qb;
+    if (ln == 0) {
+      red[0][w] = mn;
+      red[1][w] = mx;
     }
-    int64_t p = -1;
-    if (s0 < a.NS && qa <= qb) {
-      const int64_t lo = a.rblk[s0], hi = a.rblk[s0 + 1];
-      p = wave_upper_bound(a.cr.s, lo, hi, w == 0 ? qa : qb) - 1;
-      if (w == 0 && p < lo) p = lo;
+    __syncthreads();
+    // wave 0 finds the window start, wave 1 its end
+    if (w < 2) {
+      uint64_t qa = ~0ull, qb = 0;
+      for (int k = 0; k < kEncThreads / OPA_WAVE; ++k) {
+        qa = red[0][k] < qa ? red[0][k] : qa;
+        qb = red[1][k] > qb ? red[1][k] : qb;
+      }
+      int64_t p = -1;
+      if (s0 < a.NS && qa <= qb) {
+        const int64_t lo = a.rblk[s0], hi = a.rblk[s0 + 1];
+        p = wave_upper_bound(a.cr.s, lo, hi, w == 0 ? qa : qb) - 1;
+        if (w == 0 && p < lo) p = lo;
+      }
+      if (ln == 0) win[w] = p;
     }
-    if (ln == 0) win[w] = p;
-  }
-  __syncthreads();
-  const int64_t wlo = win[0];
-  int64_t wn = (s0 < a.NS) ? win[1] - wlo + 1 : 0;
-  if (wn < 0) wn = 0;
-  const bool staged = wn > 0 && wn <= kEncWindow;
-  if (staged)
-    for (int k = tid; k < wn; k += kEncThreads) sS[k] = a.cr.s[wlo + k];
-  __syncthreads();
+    __syncthreads();
+    const int64_t wlo = win[0];
+    int64_t wn = (s0 < a.NS) ? win[1] - wlo + 1 : 0;
+    if (wn < 0) wn = 0;
+    const bool staged = wn > 0 && wn <= kEncWindow;
+    if (staged)
+      for (int k = tid; k < wn; k += kEncThreads) sS[k] = a.cr.s[wlo + k];
+    __syncthreads();
 
-  int32_t rout[kPer];
+    int32_t rout[kPer];
 #pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    int32_t rid = -1;
-    if (k < nv && st[k] < a.NS && q[k] < (1ull << 63)) {
-      const int64_t lo = a.rblk[st[k]], hi = a.rblk[st[k] + 1];
-      const bool in0 = st[k] == s0;
-      int64_t p;
-      if (in0 && wn == 0) {
-        p = lo - 1;  // no range of the stream starts at or before the block's queries
-      } else if (in0 && staged) {
-        int l2 = 0, h2 = (int)wn;
-        while (l2 < h2) {
-          const int mid = (l2 + h2) >> 1;
-          if (sS[mid] <= q[k]) l2 = mid + 1;
-          else h2 = mid;
+    for (int k = 0; k < kPer; ++k) {
+      int32_t rid = -1;
+      if (k < nv && st[k] < a.NS && q[k] < (1ull << 63)) {
+        const int64_t lo = a.rblk[st[k]], hi = a.rblk[st[k] + 1];
+        const bool in0 = st[k] == s0;
+        int64_t p;
+        if (in0 && wn == 0) {
+          p = lo - 1;  // no range of the stream starts at or before the block's queries
+        } else if (in0 && staged) {
+          int l2 = 0, h2 = (int)wn;
+          while (l2 < h2) {
+            const int mid = (l2 + h2) >> 1;
+            if (sS[mid] <= q[k]) l2 = mid + 1;
+            else h2 = mid;
+          }
+          p = wlo + l2 - 1;
+          if (p < lo) p = lo - 1;
+        } else {
+          p = thread_upper_bound(a.cr.s, lo, hi, q[k]) - 1;
         }
-        p = wlo + l2 - 1;
-        if (p < lo) p = lo - 1;
-      } else {
-        p = thread_upper_bound(a.cr.s, lo, hi, q[k]) - 1;
+        int64_t j = p;
+        int steps = 0;
+        while (j >= lo && a.ree[j] < (int64_t)q[k] && steps < kMaxWalk) {
+          j = a.npg[j];
+          ++steps;
+        }
+        if (j >= lo && a.ree[j] >= (int64_t)q[k]) rid = (int32_t)j;
+      } else if (k < nv && st[k] >= a.NS) {
+        bad++;
       }
-      int64_t j = p;
-      int steps = 0;
-      while (j >= lo && a.ree[j] < (int64_t)q[k] && steps < kMaxWalk) {
-        j = a.npg[j];
-        ++steps;
-      }
-      if (j >= lo && a.ree[j] >= (int64_t)q[k]) rid = (int32_t)j;
-    } else if (k < nv && st[k] >= a.NS) {
-      bad++;
+      rout[k] = rid >= 0 ? (a.cr.perm ? a.cr.perm[rid] : rid) : -1;
+      g[k] = k < nv ? (rid >= 0 ? a.cr.op[rid] : a.NOPS) : 0xFFFFFFFFu;
     }
-    rout[k] = rid >= 0 ? (a.cr.perm ? a.cr.perm[rid] : rid) : -1;
+    store_run(a.range_id, ib, nv, rout);
+  } else {
+    bad += rows_from_ids(a, ib, nv, g);
   }
-  store_run(a.range_id, ib, nv, rout);
+  if (MODE & 2) {
+    uint32_t hm, hp, items, rows;
+    run_heads(g, nv, hm, hp);
+    wave_counts(hm, hp, items, rows);
+    if (ln == 0) {
+      a.em.wi[bid * (kEncThreads / OPA_WAVE) + w] = items;
+      a.em.wr[bid * (kEncThreads / OPA_WAVE) + w] = rows;
+    }
+  }
   if (bad) atomicAdd(&sbad, bad);
   __syncthreads();
   if (tid == 0 && sbad)
     atomicAdd((unsigned long long *)&a.diag->bad_records, (unsigned long long)sbad);
+}
+
+// Exclusive scans of the per-wave item and row counts, in place (one block);
+// meta[0] / meta[1] get the totals.
+__global__ void __launch_bounds__(1024) k_wave_scan(EmitOut e, int64_t nwaves) {
+  __shared__ uint32_t sh[16];
+  uint32_t ci = 0, cr = 0;
+  for (int64_t base = 0; base < nwaves; base += 1024) {
+    const int64_t x = base + threadIdx.x;
+    const uint32_t vi = x < nwaves ? e.wi[x] : 0u, vr = x < nwaves ? e.wr[x] : 0u;
+    uint32_t ti, tr;
+    const uint32_t pi = block_excl_scan_add<uint32_t>(vi, sh, &ti);
+    const uint32_t pr = block_excl_scan_add<uint32_t>(vr, sh, &tr);
+    if (x < nwaves) {
+      e.wi[x] = ci + pi;
+      e.wr[x] = cr + pr;
+    }
+    ci += ti;
+    cr += tr;
+  }
+  if (threadIdx.x == 0) {
+    e.meta[0] = ci;
+    e.meta[1] = cr;
+  }
+}
+
+// Items of every wave at its scanned bases, in launch order.
+__global__ void __launch_bounds__(kEncThreads) k_emit(EncParams a) {
+  const int w = wave_id(), ln = lane_id();
+  const int64_t wave = (int64_t)blockIdx.x * (kEncThreads / OPA_WAVE) + w;
+  const int64_t ib = (int64_t)blockIdx.x * kSpan + (int64_t)threadIdx.x * kPer;
+  const int nv = (int)(a.T - ib < 0 ? 0 : (a.T - ib < kPer ? a.T - ib : kPer));
+  uint32_t g[kPer];
+  rows_from_ids(a, ib, nv, g);  // malformed ids were counted with the counts
+  uint32_t hm, hp;
+  run_heads(g, nv, hm, hp);
+  const uint32_t nh = __popc(hm), nhp = __popc(hp);
+  const uint32_t hb = wave_incl_scan_add(nh) - nh;
+  const uint32_t hpb = wave_incl_scan_add(nhp) - nhp;
+  const uint32_t nr_w = __shfl(hb + nh, OPA_WAVE - 1, OPA_WAVE);
+  const uint32_t ibase = a.em.wi[wave];
+  if (nr_w <= (uint32_t)kRowCap) {
+    // one item per run, written by the launch that starts it
+    const uint32_t rbase = a.em.wr[wave];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      if (!((hm >> k) & 1u)) continue;
+      const uint32_t idx = hb + __popc(hm & ((1u << k) - 1u));
+      a.em.ig[ibase + idx] = g[k];
+      a.em.ia[ibase + idx] = rbase + idx;
+      a.em.ib[ibase + idx] = 0;
+    }
+  } else {
+    // references: every piece start writes (row, first launch, length)
+    const uint32_t hpn = __shfl_down(hp, 1, OPA_WAVE);
+    const uint32_t nvn = __shfl_down((uint32_t)nv, 1, OPA_WAVE);
+    const uint32_t spill = ln < OPA_WAVE - 1 ? (hpn ? (uint32_t)__ffs(hpn) - 1u : nvn) : 0u;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      if (!((hp >> k) & 1u)) continue;
+      const uint32_t rest = hp >> (k + 1);
+      const uint32_t len = rest ? (uint32_t)__ffs(rest) : (uint32_t)(nv - k) + spill;
+      const uint32_t idx = hpb + __popc(hp & ((1u << k) - 1u));
+      a.em.ig[ibase + idx] = g[k];
+      a.em.ia[ibase + idx] = (uint32_t)(ib + k);
+      a.em.ib[ibase + idx] = len;
+    }
+  }
 }
 
 // a += b, field by field (rows staged in LDS)
@@ -283,87 +371,44 @@ __device__ __forceinline__ void row_add(PartRow *r, const Acc &b, uint32_t maxma
   r->nan |= b.nan;
 }
 
+// In-place reduction of the planned runs (waves in row mode); the matches of
+// every launch are checked here.
 template <bool DEF>  // DEF: the default aggregation kinds
 __global__ void __launch_bounds__(kEncThreads) __attribute__((amdgpu_waves_per_eu(4)))
-k_agg_runs(EncParams a) {
+k_agg_rows(EncParams a) {
   __shared__ PartRow stage[kEncThreads / OPA_WAVE][kRowCap];
-  __shared__ uint32_t wcnt[2][kEncThreads / OPA_WAVE];
-  __shared__ uint32_t spre[2];
-  __shared__ uint32_t sbid, sbad, sfail;
+  __shared__ uint32_t sbad;
   const int tid = threadIdx.x, w = wave_id(), ln = lane_id();
   const AggIn &in = a.ag;
   const uint32_t mx = DEF ? kDefMaxMask : in.maxmask, dw = DEF ? kDefDwMask : in.dwmask;
-  if (tid == 0) {
-    sbad = 0;
-    sfail = 0;
-    sbid = atomicAdd(a.em.ctr, 1u);
-  }
+  if (tid == 0) sbad = 0;
   __syncthreads();
-  const int64_t bid = sbid;
+  const int64_t bid = blockIdx.x;
   const int64_t ib = bid * kSpan + (int64_t)tid * kPer;
   const int nv = (int)(a.T - ib < 0 ? 0 : (a.T - ib < kPer ? a.T - ib : kPer));
-  uint32_t bad = 0;
   uint32_t g[kPer];
+  rows_from_ids(a, ib, nv, g);  // malformed ids were counted by the plan
   int32_t mt[kPer];
   uint32_t du[kPer];
-  {
-    int32_t rin[kPer];
-    load_run(a.range_id, ib, nv, rin);
-#pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-      g[k] = k < nv ? a.NOPS : 0xFFFFFFFFu;
-      if (k >= nv) continue;
-      const int32_t r = rin[k];
-      if (r >= 0 && r < a.R_in && a.op_in[r] < a.NOPS) g[k] = a.op_in[r];
-      else if (r < -1 || r >= a.R_in || r >= 0) bad++;
-    }
-  }
   load_run(in.match, ib, nv, mt);
   load_run(in.dur, ib, nv, du);
+  uint32_t bad = 0;
 #pragma unroll
   for (int k = 0; k < kPer; ++k)
     if (k < nv && (mt[k] < -1 || (int64_t)mt[k] >= in.P)) bad++;  // aggregates as unmatched
-
-  // ---- runs of one operator row inside the wave, in launch order
-  const uint32_t gl = __shfl_up(g[kPer - 1], 1, OPA_WAVE);
-  uint32_t hm = 0;  // bit k: launch k starts a run
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    const uint32_t prev = k ? g[k - 1] : (ln ? gl : 0xFFFFFFFFu);
-    if (k < nv && g[k] != prev) hm |= 1u << k;
-  }
-  // pieces for references: runs cut at every 16th launch as well
-  const uint32_t hp = hm | ((nv > 0 && (ln & 1) == 0) ? 1u : 0u);
-  const uint32_t nh = __popc(hm), nhp = __popc(hp);
+  uint32_t hm, hp;
+  run_heads(g, nv, hm, hp);
+  const uint32_t nh = __popc(hm);
   const uint32_t hb = wave_incl_scan_add(nh) - nh;
-  const uint32_t hpb = wave_incl_scan_add(nhp) - nhp;
   const uint32_t nr_w = __shfl(hb + nh, OPA_WAVE - 1, OPA_WAVE);
-  const uint32_t np_w = __shfl(hpb + nhp, OPA_WAVE - 1, OPA_WAVE);
-  const bool rowmode = nr_w <= (uint32_t)kRowCap;
-  if (ln == 0) {
-    wcnt[0][w] = rowmode ? nr_w : np_w;
-    wcnt[1][w] = rowmode ? nr_w : 0u;
-  }
-  __syncthreads();
-  uint32_t bi = 0, br = 0, wi = 0, wr = 0;
-  for (int k = 0; k < kEncThreads / OPA_WAVE; ++k) {
-    if (k < w) {
-      wi += wcnt[0][k];
-      wr += wcnt[1][k];
-    }
-    bi += wcnt[0][k];
-    br += wcnt[1][k];
-  }
-  if (tid == 0) lb_store(a.em.state + bid, lb_pack(bid == 0 ? kLbInc : kLbAgg, bi, br));
-
-  // ---- in-place reduction (row mode). Each thread accumulates its launches;
-  // a run that ends inside the thread goes to its LDS row (the first one of
-  // them still lacks the part from earlier threads, added after the scan).
-  // The thread's last run is scanned across the lanes.
-  PartRow *wst = stage[w];
-  Acc inc;
-  acc_zero(inc);
-  if (rowmode) {
+  if (nr_w <= (uint32_t)kRowCap) {
+    // Each thread accumulates its launches; a run that ends inside the thread
+    // goes to its LDS row (the first one of them still lacks the part from
+    // earlier threads, added after the scan). The thread's last run is
+    // scanned across the lanes.
+    PartRow *wst = stage[w];
+    Acc inc;
+    acc_zero(inc);
     uint32_t gk = g[0];
 #pragma unroll 1
     for (int k = 0; k < nv; ++k) {
@@ -388,59 +433,17 @@ k_agg_runs(EncParams a) {
       if (ln == OPA_WAVE - 1 || nvn == 0 || (hmn & 1u)) acc_store(r, inc, g[nv - 1]);
       else if (hmn & 0xFEu) row_add(r, inc, mx);
     }
-  }
-
-  // ---- block offsets
-  if (w == 0) {
-    uint32_t pi = 0, pr = 0;
-    bool ok = true;
-    if (bid > 0) ok = lookback(a.em.state, bid, pi, pr);
-    if (ln == 0) {
-      if (bid > 0) lb_store(a.em.state + bid, lb_pack(kLbInc, pi + bi, pr + br));
-      spre[0] = pi;
-      spre[1] = pr;
-      if (!ok) sfail = 1;
-      if (bid == a.em.nblocks - 1) {
-        a.em.meta[0] = (int64_t)pi + bi;
-        a.em.meta[1] = (int64_t)pr + br;
-      }
-    }
-  }
-  __syncthreads();
-  const uint32_t ibase = spre[0] + wi, rbase = spre[1] + wr;
-
-  if (rowmode) {
-    // coalesced copy of the wave's rows, then one item per row
+    // coalesced copy of the wave's rows to the planned indices
+    const uint32_t rbase = a.em.wr[bid * (kEncThreads / OPA_WAVE) + w];
     const unsigned long long *src = reinterpret_cast<const unsigned long long *>(wst);
     unsigned long long *dst = reinterpret_cast<unsigned long long *>(a.em.rows + rbase);
     const uint32_t nw = nr_w * (uint32_t)(sizeof(PartRow) / 8);
     for (uint32_t x = ln; x < nw; x += OPA_WAVE) dst[x] = src[x];
-    if ((uint32_t)ln < nr_w) {
-      a.em.ig[ibase + ln] = wst[ln].g;
-      a.em.ia[ibase + ln] = rbase + ln;
-      a.em.ib[ibase + ln] = 0;
-    }
-  } else {
-    // references: every piece start writes (row, first launch, length)
-    const uint32_t hpn = __shfl_down(hp, 1, OPA_WAVE);
-    const uint32_t nvn = __shfl_down((uint32_t)nv, 1, OPA_WAVE);
-    const uint32_t spill = ln < OPA_WAVE - 1 ? (hpn ? (uint32_t)__ffs(hpn) - 1u : nvn) : 0u;
-#pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-      if (!((hp >> k) & 1u)) continue;
-      const uint32_t rest = hp >> (k + 1);
-      const uint32_t len = rest ? (uint32_t)__ffs(rest) : (uint32_t)(nv - k) + spill;
-      const uint32_t idx = hpb + __popc(hp & ((1u << k) - 1u));
-      a.em.ig[ibase + idx] = g[k];
-      a.em.ia[ibase + idx] = (uint32_t)(ib + k);
-      a.em.ib[ibase + idx] = len;
-    }
   }
   if (bad) atomicAdd(&sbad, bad);
   __syncthreads();
   if (tid == 0 && sbad)
     atomicAdd((unsigned long long *)&a.diag->bad_records, (unsigned long long)sbad);
-  if (tid == 0 && sfail) atomicOr(&a.diag->flags, OPATTR_F_LIMIT);
 }
 
 static EncParams enc_params(const EncArgs &x) {
@@ -461,39 +464,61 @@ static EncParams enc_params(const EncArgs &x) {
   // the aggregation reads range ids by input range index
   a.R_in = x.r ? x.r->n : 0;
   a.op_in = x.r ? x.r->op_id : nullptr;
+  a.em = emit_out(x.ws, pl);
   return a;
+}
+
+// the aggregation plan: per-wave counts (with the enclosure when enclose is
+// set), their scan, the items, and the items sorted by operator row
+static void run_plan(const EncArgs &x, bool enclose, hipStream_t s) {
+  const Plan &pl = *x.pl;
+  const EncParams a = enc_params(x);
+  FillJobs clr;
+  clr.add(at<uint32_t>(x.ws, pl.gcnt), 0, pl.G);
+  if (pl.T <= 0) clr.add(a.em.meta, 0, 8);
+  fill_many(clr, s);
+  probe_begin(OPATTR_PROBE_MAIN_PASS, s);
+  if (pl.T > 0) {
+    if (enclose) k_enclose<3><<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
+    else k_enclose<2><<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
+  }
+  probe_end(OPATTR_PROBE_MAIN_PASS, s);
+  if (pl.T > 0) {
+    k_wave_scan<<<1, 1024, 0, s>>>(a.em, pl.nencb * (kEncThreads / OPA_WAVE));
+    k_emit<<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
+  }
+  plan_items(x, s);
 }
 
 void run_enclose(const EncArgs &x, hipStream_t s) {
   const Plan &pl = *x.pl;
   const EncParams a = enc_params(x);
   probe_begin(OPATTR_PROBE_MAIN_PASS, s);
-  if (pl.T > 0) k_enclose<<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
+  if (pl.T > 0) k_enclose<1><<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
   probe_end(OPATTR_PROBE_MAIN_PASS, s);
 }
 
-void run_aggregate_all(const EncArgs &x, hipStream_t s) {
+void run_enclose_plan(const EncArgs &x, hipStream_t s) { run_plan(x, true, s); }
+
+void run_reduce(const EncArgs &x, hipStream_t s) {
   const Plan &pl = *x.pl;
   EncParams a = enc_params(x);
   a.ag = agg_inputs(x);
-  a.em = emit_out(x.ws, pl);
-  // look-back states, the start counter, the per-row item counts (and with
-  // no launches the item totals), cleared by one kernel (graph-safe)
-  FillJobs clr;
-  clr.add(a.em.state, 0, 2 * (pl.nencb + 1));
-  clr.add(at<uint32_t>(x.ws, pl.gcnt), 0, pl.G);
-  if (pl.T <= 0) clr.add(a.em.meta, 0, 8);
-  fill_many(clr, s);
   probe_begin(OPATTR_PROBE_AGG_RUNS, s);
   if (pl.T > 0) {
     const unsigned nb = (unsigned)pl.nencb;
     if (a.ag.maxmask == kDefMaxMask && a.ag.dwmask == kDefDwMask)
-      k_agg_runs<true><<<nb, kEncThreads, 0, s>>>(a);
+      k_agg_rows<true><<<nb, kEncThreads, 0, s>>>(a);
     else
-      k_agg_runs<false><<<nb, kEncThreads, 0, s>>>(a);
+      k_agg_rows<false><<<nb, kEncThreads, 0, s>>>(a);
   }
   probe_end(OPATTR_PROBE_AGG_RUNS, s);
-  run_aggregate(x, s);
+  reduce_items(x, s);
+}
+
+void run_aggregate_all(const EncArgs &x, hipStream_t s) {
+  run_plan(x, false, s);
+  run_reduce(x, s);
 }
 
 }  // namespace opa

@@ -44,7 +44,7 @@ struct Plan {
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
   // aggregation
   int64_t cap_items, cap_rows, max_chunks;
-  size_t lbs, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, coff, cmap, sidx, part;
+  size_t wi, wr, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, coff, cmap, sit, part;
   size_t misc;  // small device scalars
 };
 
@@ -161,14 +161,12 @@ void resolve_ranges(const CoreRanges &cr, const opattr_dims *d, void *ws, const 
 
 struct PartRow;
 struct AggIn;
-// Items left by the enclosure pass for the aggregation (see agg.hip).
+// Items planned by the enclosure pass for the aggregation (see agg.hip).
 struct EmitOut {
-  unsigned long long *state;  // [blocks] look-back states
-  uint32_t *ctr;              // block start counter
+  uint32_t *wi, *wr;          // [waves] item / partial-row counts, then bases
   uint32_t *ig, *ia, *ib;     // item: row, partial-row index or first launch, 0 or length
   PartRow *rows;
   int64_t *meta;
-  int64_t nblocks;
 };
 EmitOut emit_out(void *ws, const Plan &pl);
 
@@ -190,9 +188,16 @@ struct EncArgs {
 AggIn agg_inputs(const EncArgs &x);
 // range_id of every launch (Alg. 2)
 void run_enclose(const EncArgs &a, hipStream_t s);
-// operator table from range_id and match: run reduction, item sort, rows
+// range_id of every launch and the aggregation plan: items and their sort
+// by operator row (no matches needed)
+void run_enclose_plan(const EncArgs &a, hipStream_t s);
+// operator table from a planned aggregation and match: run reduction, rows
+void run_reduce(const EncArgs &a, hipStream_t s);
+// operator table from range_id and match: plan, then reduce
 void run_aggregate_all(const EncArgs &a, hipStream_t s);
-void run_aggregate(const EncArgs &a, hipStream_t s);
+// item sort by row (agg.hip), and the per-row reduction of the sorted items
+void plan_items(const EncArgs &a, hipStream_t s);
+void reduce_items(const EncArgs &a, hipStream_t s);
 
 // ---- finish (api.hip) ---------------------------------------------------------
 void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s);

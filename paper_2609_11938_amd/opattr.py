@@ -69,7 +69,7 @@ EXPORTS = ("opattr_workspace_bytes", "opattr_diag_clear", "opattr_read_diag", "o
            "opattr_dedup_broadcast", "opattr_enclose", "opattr_aggregate", "opattr_attribute",
            "opattr_set_probe_events", "opattr_strerror")
 PROBES = ("seq_view", "tl_hist", "pf_hist", "col_scan", "pf_slot", "tl_match", "dedup",
-          "ranges", "main_pass", "finalize", "aggregate", "agg_runs")
+          "ranges", "main_pass", "finalize", "aggregate", "agg_runs", "item_sort")
 
 _lib = None
 
@@ -116,12 +116,13 @@ def library(path: str | None = None):
 def set_probe_events(events) -> None:
     """events: None, or a list of 2*n torch.cuda.Event (timing enabled, already
     recorded once so that the HIP event exists), start/stop per probe in the
-    order of PROBES."""
+    order of PROBES; a None entry leaves that event unrecorded."""
     L = library()
     if not events:
         _check(L.opattr_set_probe_events(None, 0), "opattr_set_probe_events")
         return
-    arr = (C.c_void_p * len(events))(*[e.cuda_event for e in events])
+    arr = (C.c_void_p * len(events))(*[e.cuda_event if e is not None else None
+                                       for e in events])
     _check(L.opattr_set_probe_events(arr, len(events) // 2), "opattr_set_probe_events")
 
 
