@@ -13,7 +13,7 @@ struct PartRow {
   unsigned long long kc, tns, mc, mns;
   unsigned long long v[OPATTR_NUM_COUNTERS];  // fp64 bits of a sum, or a MAX key
   uint32_t nan;                               // bit c: a NaN reached MAX counter c
-  uint32_t g;                                 // operator row
+  uint32_t pad;
 };
 static_assert(sizeof(PartRow) == 200, "PartRow layout");
 
@@ -151,7 +151,7 @@ __device__ __forceinline__ void acc_wave_reduce(Acc &a, uint32_t maxmask) {
   }
 }
 
-__device__ __forceinline__ void acc_store(PartRow *p, const Acc &a, uint32_t g) {
+__device__ __forceinline__ void acc_store(PartRow *p, const Acc &a) {
   p->kc = a.kc;
   p->tns = a.tns;
   p->mc = a.mc;
@@ -159,7 +159,6 @@ __device__ __forceinline__ void acc_store(PartRow *p, const Acc &a, uint32_t g) 
 #pragma unroll
   for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) p->v[c] = a.v[c];
   p->nan = a.nan;
-  p->g = g;
 }
 
 __device__ __forceinline__ void acc_load(Acc &a, const PartRow *p) {

@@ -219,7 +219,7 @@ __global__ void __launch_bounds__(256) k_chunk_reduce(AggWork w) {
       }
     }
     acc_wave_reduce(acc, mx);
-    if (ln == 0) acc_store(w.part + ch, acc, g);
+    if (ln == 0) acc_store(w.part + ch, acc);
   }
 }
 

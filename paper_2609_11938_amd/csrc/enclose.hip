@@ -116,15 +116,6 @@ __device__ __forceinline__ void store_run(T *p, int64_t i, int nv, const T (&o)[
   }
 }
 
-// g[k] for a run-time k without indexing the register array
-__device__ __forceinline__ uint32_t pick(const uint32_t (&g)[kPer], int k) {
-  uint32_t r = g[0];
-#pragma unroll
-  for (int j = 1; j < kPer; ++j)
-    if (j == k) r = g[j];
-  return r;
-}
-
 // The operator rows of a thread's launches from input range ids (plan from a
 // given range_id array, and the reduction). Counts malformed range ids.
 __device__ __forceinline__ uint32_t rows_from_ids(const EncParams &a, int64_t ib, int nv,
@@ -388,14 +379,15 @@ k_agg_rows(EncParams a) {
   const int nv = (int)(a.T - ib < 0 ? 0 : (a.T - ib < kPer ? a.T - ib : kPer));
   uint32_t g[kPer];
   rows_from_ids(a, ib, nv, g);  // malformed ids were counted by the plan
-  int32_t mt[kPer];
+  uint32_t mt[kPer];  // profiled row indices (as stored, -1 = unmatched)
   uint32_t du[kPer];
-  load_run(in.match, ib, nv, mt);
+  load_run(reinterpret_cast<const uint32_t *>(in.match), ib, nv, mt);
   load_run(in.dur, ib, nv, du);
   uint32_t bad = 0;
 #pragma unroll
   for (int k = 0; k < kPer; ++k)
-    if (k < nv && (mt[k] < -1 || (int64_t)mt[k] >= in.P)) bad++;  // aggregates as unmatched
+    if (k < nv && ((int32_t)mt[k] < -1 || (int64_t)(int32_t)mt[k] >= in.P))
+      bad++;  // aggregates as unmatched
   uint32_t hm, hp;
   run_heads(g, nv, hm, hp);
   const uint32_t nh = __popc(hm);
@@ -409,15 +401,20 @@ k_agg_rows(EncParams a) {
     PartRow *wst = stage[w];
     Acc inc;
     acc_zero(inc);
-    uint32_t gk = g[0];
+    // launch k is always at position 0 of mt / du: the arrays shift by one
+    // per step (a run-time index would move them to scratch memory)
 #pragma unroll 1
     for (int k = 0; k < nv; ++k) {
       if (k > 0 && ((hm >> k) & 1u)) {
-        acc_store(wst + hb + __popc(hm & ((1u << k) - 1u)) - 1u, inc, gk);
+        acc_store(wst + hb + __popc(hm & ((1u << k) - 1u)) - 1u, inc);
         acc_zero(inc);
       }
-      acc_launch(inc, in, in.match[ib + k], in.dur[ib + k], mx, dw);
-      gk = pick(g, k);
+      acc_launch(inc, in, (int32_t)mt[0], du[0], mx, dw);
+#pragma unroll
+      for (int j = 0; j + 1 < kPer; ++j) {
+        mt[j] = mt[j + 1];
+        du[j] = du[j + 1];
+      }
     }
     const unsigned long long hl = __ballot(hm != 0) | 1ull;
     const unsigned long long upto = ln == 63 ? ~0ull : ((2ull << ln) - 1);
@@ -430,7 +427,7 @@ k_agg_rows(EncParams a) {
     const uint32_t hmn = __shfl_down(hm, 1, OPA_WAVE);
     if (nv > 0) {
       PartRow *r = wst + hb + nh - 1u;
-      if (ln == OPA_WAVE - 1 || nvn == 0 || (hmn & 1u)) acc_store(r, inc, g[nv - 1]);
+      if (ln == OPA_WAVE - 1 || nvn == 0 || (hmn & 1u)) acc_store(r, inc);
       else if (hmn & 0xFEu) row_add(r, inc, mx);
     }
     // coalesced copy of the wave's rows to the planned indices
