@@ -108,28 +108,33 @@ __global__ void __launch_bounds__(256) k_item_hist_r(AggWork w) {
   }
 }
 
-// 1b. row offsets of the sorted items and chunk offsets (one block)
+// 1b. row offsets of the sorted items and chunk offsets (one block; each
+// thread scans a contiguous run of rows)
 __global__ void __launch_bounds__(1024) k_row_offsets(AggWork w) {
   __shared__ uint32_t sh[16];
-  uint32_t carry = 0, ccarry = 0;
-  for (uint32_t base = 0; base < w.G; base += 1024) {
-    const uint32_t g = base + threadIdx.x;
-    const uint32_t c = g < w.G ? w.gcnt[g] : 0u;
-    const uint32_t ch = (c + kChunkItems - 1) / kChunkItems;
-    uint32_t tot, ctot;
-    const uint32_t pre = block_excl_scan_add<uint32_t>(c, sh, &tot);
-    const uint32_t cpre = block_excl_scan_add<uint32_t>(ch, sh, &ctot);
-    if (g < w.G) {
-      w.goff[g] = carry + pre;
-      w.coff[g] = ccarry + cpre;
-    }
-    carry += tot;
-    ccarry += ctot;
+  const uint32_t ch = (w.G + blockDim.x - 1) / blockDim.x;
+  const uint32_t lo = threadIdx.x * ch;
+  const uint32_t hi = lo + ch < w.G ? lo + ch : w.G;
+  uint32_t c = 0, cc = 0;
+  for (uint32_t g = lo; g < hi; ++g) {
+    const uint32_t n = w.gcnt[g];
+    c += n;
+    cc += (n + kChunkItems - 1) / kChunkItems;
+  }
+  uint32_t tot, ctot;
+  uint32_t run = block_excl_scan_add<uint32_t>(c, sh, &tot);
+  uint32_t crun = block_excl_scan_add<uint32_t>(cc, sh, &ctot);
+  for (uint32_t g = lo; g < hi; ++g) {
+    const uint32_t n = w.gcnt[g];
+    w.goff[g] = run;
+    w.coff[g] = crun;
+    run += n;
+    crun += (n + kChunkItems - 1) / kChunkItems;
   }
   if (threadIdx.x == 0) {
-    w.goff[w.G] = carry;
-    w.coff[w.G] = ccarry;
-    w.meta[3] = ccarry;
+    w.goff[w.G] = tot;
+    w.coff[w.G] = ctot;
+    w.meta[3] = ctot;
   }
 }
 

@@ -136,6 +136,25 @@ __device__ __forceinline__ T block_excl_scan_add(T x, T *sh, T *total) {
   return base + inc - x;
 }
 
+// Exclusive scan of a[0, n) in place by one block: each thread takes a
+// contiguous chunk, so the block synchronises for one scan only. sh needs
+// blockDim.x / 64 entries. Returns the total.
+__device__ inline uint32_t block_scan_chunked(uint32_t *a, int64_t n, uint32_t *sh) {
+  const int64_t ch = (n + blockDim.x - 1) / blockDim.x;
+  const int64_t lo = (int64_t)threadIdx.x * ch;
+  const int64_t hi = lo + ch < n ? lo + ch : n;
+  uint32_t sum = 0;
+  for (int64_t i = lo; i < hi; ++i) sum += a[i];
+  uint32_t tot;
+  uint32_t run = block_excl_scan_add<uint32_t>(sum, sh, &tot);
+  for (int64_t i = lo; i < hi; ++i) {
+    const uint32_t v = a[i];
+    a[i] = run;
+    run += v;
+  }
+  return tot;
+}
+
 // Inclusive max-scan across the block; values per thread, block of 256.
 template <typename T>
 __device__ __forceinline__ T block_incl_scan_max(T x, T *sh) {

@@ -225,37 +225,68 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
       for (int k = tid; k < wn; k += kEncThreads) sS[k] = a.cr.s[wlo + k];
     __syncthreads();
 
+    // Consecutive launches of one stream with non-decreasing query points
+    // (the common case) continue from the previous launch: the last range
+    // starting at or before the query only moves forward, and while it stays
+    // the same, the parent walk resumes where the previous one stopped (the
+    // ranges it skipped end before the earlier query point, hence before this
+    // one too), with the same step budget.
     int32_t rout[kPer];
+    bool have = false;  // the previous launch was searched
+    uint16_t sprev = 0;
+    uint64_t qprev = 0;
+    int64_t pprev = 0, jprev = -1;
+    int sprevsteps = 0;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
       int32_t rid = -1;
       if (k < nv && st[k] < a.NS && q[k] < (1ull << 63)) {
         const int64_t lo = a.rblk[st[k]], hi = a.rblk[st[k] + 1];
-        const bool in0 = st[k] == s0;
-        int64_t p;
-        if (in0 && wn == 0) {
-          p = lo - 1;  // no range of the stream starts at or before the block's queries
-        } else if (in0 && staged) {
-          int l2 = 0, h2 = (int)wn;
-          while (l2 < h2) {
-            const int mid = (l2 + h2) >> 1;
-            if (sS[mid] <= q[k]) l2 = mid + 1;
-            else h2 = mid;
-          }
-          p = wlo + l2 - 1;
-          if (p < lo) p = lo - 1;
-        } else {
-          p = thread_upper_bound(a.cr.s, lo, hi, q[k]) - 1;
-        }
-        int64_t j = p;
+        int64_t j;
         int steps = 0;
+        if (have && st[k] == sprev && q[k] >= qprev) {
+          int64_t p = pprev;
+          while (p + 1 < hi && a.cr.s[p + 1] <= q[k]) ++p;
+          if (p == pprev) {
+            j = jprev;
+            steps = sprevsteps;
+          } else {
+            j = p;
+          }
+          pprev = p;
+        } else {
+          const bool in0 = st[k] == s0;
+          int64_t p;
+          if (in0 && wn == 0) {
+            p = lo - 1;  // no range of the stream starts at or before the block's queries
+          } else if (in0 && staged) {
+            int l2 = 0, h2 = (int)wn;
+            while (l2 < h2) {
+              const int mid = (l2 + h2) >> 1;
+              if (sS[mid] <= q[k]) l2 = mid + 1;
+              else h2 = mid;
+            }
+            p = wlo + l2 - 1;
+            if (p < lo) p = lo - 1;
+          } else {
+            p = thread_upper_bound(a.cr.s, lo, hi, q[k]) - 1;
+          }
+          j = p;
+          pprev = p;
+        }
         while (j >= lo && a.ree[j] < (int64_t)q[k] && steps < kMaxWalk) {
           j = a.npg[j];
           ++steps;
         }
         if (j >= lo && a.ree[j] >= (int64_t)q[k]) rid = (int32_t)j;
-      } else if (k < nv && st[k] >= a.NS) {
-        bad++;
+        have = true;
+        sprev = st[k];
+        qprev = q[k];
+        jprev = j;
+        sprevsteps = steps;
+      } else {
+        if (k < nv && st[k] >= a.NS) bad++;
+        have = false;
       }
       rout[k] = rid >= 0 ? (a.cr.perm ? a.cr.perm[rid] : rid) : -1;
       g[k] = k < nv ? (rid >= 0 ? a.cr.op[rid] : a.NOPS) : 0xFFFFFFFFu;
@@ -283,23 +314,11 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
 // meta[0] / meta[1] get the totals.
 __global__ void __launch_bounds__(1024) k_wave_scan(EmitOut e, int64_t nwaves) {
   __shared__ uint32_t sh[16];
-  uint32_t ci = 0, cr = 0;
-  for (int64_t base = 0; base < nwaves; base += 1024) {
-    const int64_t x = base + threadIdx.x;
-    const uint32_t vi = x < nwaves ? e.wi[x] : 0u, vr = x < nwaves ? e.wr[x] : 0u;
-    uint32_t ti, tr;
-    const uint32_t pi = block_excl_scan_add<uint32_t>(vi, sh, &ti);
-    const uint32_t pr = block_excl_scan_add<uint32_t>(vr, sh, &tr);
-    if (x < nwaves) {
-      e.wi[x] = ci + pi;
-      e.wr[x] = cr + pr;
-    }
-    ci += ti;
-    cr += tr;
-  }
+  const uint32_t ti = block_scan_chunked(e.wi, nwaves, sh);
+  const uint32_t tr = block_scan_chunked(e.wr, nwaves, sh);
   if (threadIdx.x == 0) {
-    e.meta[0] = ci;
-    e.meta[1] = cr;
+    e.meta[0] = ti;
+    e.meta[1] = tr;
   }
 }
 
