@@ -27,7 +27,9 @@
  *    capture of `stream` records both branches.
  *  - The caller owns every buffer: inputs, outputs, the diag record and the
  *    workspace. No entry point allocates or frees device memory. Calls are
- *    stateless and reentrant on distinct workspaces.
+ *    stateless and reentrant on distinct workspaces. The workspace starts on a
+ *    256-byte boundary (as hipMalloc returns it); otherwise, or when it is
+ *    smaller than opattr_workspace_bytes, the call returns OPATTR_ERR_WORKSPACE.
  *  - Return value: 0, or a negative OPATTR_ERR_* for an ARGUMENT error found on
  *    the host (nothing is enqueued then). Errors that depend on the data are
  *    recorded on the device in the opattr_diag record (flags, counts, status);

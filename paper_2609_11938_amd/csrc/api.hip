@@ -127,6 +127,11 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   return pl;
 }
 
+// the workspace regions are 256-byte aligned offsets from ws (vector loads)
+static bool ws_ok(const void *ws, size_t ws_bytes, const Plan &pl) {
+  return ws && (reinterpret_cast<uintptr_t>(ws) & 255) == 0 && ws_bytes >= pl.total;
+}
+
 // nesting_errors from the per-stream crossing flags; status from the flags
 __global__ void __launch_bounds__(256) k_finish(opattr_diag *diag, const uint8_t *sflag,
                                                 uint32_t ns) {
@@ -294,7 +299,7 @@ int opattr_match(const opattr_kernels *k, const opattr_profiled *p, const opattr
       !diag || policy < 0 || policy > 2 || (k->n > 0 && !match))
     return OPATTR_ERR_INVALID_ARG;
   const Plan pl = make_plan(k, p, nullptr, d);
-  if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
+  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   check_kernel_layout(k, d, diag, s);
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
@@ -311,7 +316,7 @@ int opattr_dedup_broadcast(const opattr_kernels *k, const opattr_dims *d, int32_
       (k->n > 0 && !match))
     return OPATTR_ERR_INVALID_ARG;
   const Plan pl = make_plan(k, nullptr, nullptr, d);
-  if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
+  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   check_kernel_layout(k, d, diag, s);
   if (has_dedup(k, d)) {
@@ -329,7 +334,7 @@ int opattr_enclose(const opattr_kernels *k, const opattr_ranges *r, const opattr
       (k->n > 0 && !range_id))
     return OPATTR_ERR_INVALID_ARG;
   const Plan pl = make_plan(k, nullptr, r, d);
-  if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
+  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   check_kernel_layout(k, d, diag, s);
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
@@ -364,7 +369,7 @@ int opattr_aggregate(const opattr_kernels *k, const opattr_profiled *p, const in
       (k->n > 0 && (!match || !range_id)))
     return OPATTR_ERR_INVALID_ARG;
   const Plan pl = make_plan(k, p, r, d);
-  if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
+  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   check_kernel_layout(k, d, diag, s);
   EncArgs e{};
@@ -395,7 +400,7 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
       !kinds_ok(agg_kind) || (k->n > 0 && (!match || !range_id)))
     return OPATTR_ERR_INVALID_ARG;
   const Plan pl = make_plan(k, p, r, d);
-  if (!ws || ws_bytes < pl.total) return OPATTR_ERR_WORKSPACE;
+  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   check_kernel_layout(k, d, diag, s);
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;

@@ -311,11 +311,64 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
 }
 
 // Exclusive scans of the per-wave item and row counts, in place (one block);
-// meta[0] / meta[1] get the totals.
-__global__ void __launch_bounds__(1024) k_wave_scan(EmitOut e, int64_t nwaves) {
+// meta[0] / meta[1] get the totals. Each thread takes a contiguous run of
+// enclosure blocks (four waves each, one 16-byte load per array) and loads
+// them four blocks at a time, so the loads of a batch are in flight
+// together.
+__global__ void __launch_bounds__(1024) k_wave_scan(EmitOut e, int64_t nblocks) {
+  constexpr int kW = kEncThreads / OPA_WAVE;
+  static_assert(kW == 4, "one 16-byte load per block");
+  constexpr int kBatch = 4;
   __shared__ uint32_t sh[16];
-  const uint32_t ti = block_scan_chunked(e.wi, nwaves, sh);
-  const uint32_t tr = block_scan_chunked(e.wr, nwaves, sh);
+  const uint4 *wi4 = reinterpret_cast<const uint4 *>(e.wi);
+  const uint4 *wr4 = reinterpret_cast<const uint4 *>(e.wr);
+  const int64_t ch = (nblocks + blockDim.x - 1) / blockDim.x;
+  const int64_t lo = (int64_t)threadIdx.x * ch;
+  const int64_t hi = lo + ch < nblocks ? lo + ch : nblocks;
+  uint32_t si = 0, sr = 0;
+  for (int64_t b0 = lo; b0 < hi; b0 += kBatch) {
+    uint4 vi[kBatch], vr[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      vi[j] = b0 + j < hi ? wi4[b0 + j] : make_uint4(0, 0, 0, 0);
+      vr[j] = b0 + j < hi ? wr4[b0 + j] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      si += vi[j].x + vi[j].y + vi[j].z + vi[j].w;
+      sr += vr[j].x + vr[j].y + vr[j].z + vr[j].w;
+    }
+  }
+  uint32_t ti, tr;
+  uint32_t ri = block_excl_scan_add<uint32_t>(si, sh, &ti);
+  uint32_t rr = block_excl_scan_add<uint32_t>(sr, sh, &tr);
+  uint4 *oi = reinterpret_cast<uint4 *>(e.wi);
+  uint4 *orr = reinterpret_cast<uint4 *>(e.wr);
+  for (int64_t b0 = lo; b0 < hi; b0 += kBatch) {
+    uint4 vi[kBatch], vr[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      vi[j] = b0 + j < hi ? wi4[b0 + j] : make_uint4(0, 0, 0, 0);
+      vr[j] = b0 + j < hi ? wr4[b0 + j] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      if (b0 + j >= hi) break;
+      uint4 bi, br;
+      bi.x = ri;
+      bi.y = bi.x + vi[j].x;
+      bi.z = bi.y + vi[j].y;
+      bi.w = bi.z + vi[j].z;
+      ri = bi.w + vi[j].w;
+      br.x = rr;
+      br.y = br.x + vr[j].x;
+      br.z = br.y + vr[j].y;
+      br.w = br.z + vr[j].z;
+      rr = br.w + vr[j].w;
+      oi[b0 + j] = bi;
+      orr[b0 + j] = br;
+    }
+  }
   if (threadIdx.x == 0) {
     e.meta[0] = ti;
     e.meta[1] = tr;
@@ -500,7 +553,7 @@ static void run_plan(const EncArgs &x, bool enclose, hipStream_t s) {
   }
   probe_end(OPATTR_PROBE_MAIN_PASS, s);
   if (pl.T > 0) {
-    k_wave_scan<<<1, 1024, 0, s>>>(a.em, pl.nencb * (kEncThreads / OPA_WAVE));
+    k_wave_scan<<<1, 1024, 0, s>>>(a.em, pl.nencb);
     k_emit<<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
   }
   plan_items(x, s);

@@ -121,6 +121,10 @@ def test_argument_errors_return_before_any_device_work(lib):
     assert lib.opattr_attribute(C.byref(k), C.byref(p), C.byref(r), C.byref(d), 0, None, fake,
                                 fake, None, None, fake, fake, fake, ws, C.c_size_t(need - 1),
                                 None) == WORKSPACE
+    # workspace off a 256-byte boundary
+    assert lib.opattr_attribute(C.byref(k), C.byref(p), C.byref(r), C.byref(d), 0, None, fake,
+                                fake, None, None, fake, fake, fake, C.c_void_p(0x2010),
+                                C.c_size_t(need + 256), None) == WORKSPACE
     assert lib.opattr_diag_clear(None, None) == INVALID
     assert lib.opattr_read_diag(None, None, None) == INVALID
 
