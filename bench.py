@@ -47,7 +47,8 @@ def algorithmic_bytes(tr):
         "pf_hist": P * 4,
         # k_pf_slot_w: row names in, slot table out
         "pf_slot": P * (4 + 4),
-        # k_tl_match_w: view, name, partition in; match out
+        # k_tl_look (per-tile rank, join and dedup lookup): seq, name,
+        # partition in; match out
         "tl_match": T * (4 + 4 + part + 4),
         # k_dedup: partition, name, seq in; match out
         "dedup": T * (4 + 4 + 4 + 4),
@@ -64,7 +65,7 @@ def algorithmic_bytes(tr):
 # kernel behind each single-kernel probe (for the rocprofv3 cross-check)
 PROBE_KERNEL = {"seq_view": "k_seqview_dense", "tl_hist": "k_tl_hist_w",
                 "pf_hist": "k_pf_hist_w", "pf_slot": "k_pf_slot_w",
-                "tl_match": "k_tl_match_w", "dedup": "k_dedup",
+                "tl_match": "k_tl_look", "dedup": "k_dedup",
                 "main_pass": "k_enclose", "agg_runs": "k_agg_rows"}
 
 

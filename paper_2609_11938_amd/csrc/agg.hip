@@ -25,6 +25,7 @@ EmitOut emit_out(void *ws, const Plan &pl) {
   EmitOut e;
   e.wi = at<uint32_t>(ws, pl.wi);
   e.wr = at<uint32_t>(ws, pl.wr);
+  e.hmb = at<uint8_t>(ws, pl.hmb);
   e.ig = at<uint32_t>(ws, pl.ig);
   e.ia = at<uint32_t>(ws, pl.ia);
   e.ib = at<uint32_t>(ws, pl.ib);

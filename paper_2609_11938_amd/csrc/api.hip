@@ -109,6 +109,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.max_chunks = pl.T / 64 + pl.G + 1;
   pl.wi = b.take((size_t)pl.nencb * (kEncThreads / OPA_WAVE) * 4);
   pl.wr = b.take((size_t)pl.nencb * (kEncThreads / OPA_WAVE) * 4);
+  pl.hmb = b.take((size_t)pl.nencb * kEncThreads);
   pl.ig = b.take((size_t)pl.cap_items * 4);
   pl.ia = b.take((size_t)pl.cap_items * 4);
   pl.ib = b.take((size_t)pl.cap_items * 4);

@@ -134,6 +134,17 @@ __device__ __forceinline__ uint32_t rows_from_ids(const EncParams &a, int64_t ib
   return bad;
 }
 
+// Piece starts of the references: run starts, and every 16th launch.
+__device__ __forceinline__ uint32_t piece_heads(uint32_t hm, int nv) {
+  return hm | ((nv > 0 && (lane_id() & 1) == 0) ? 1u : 0u);
+}
+
+// The operator row of launch x (an item's row) from its input range id.
+__device__ __forceinline__ uint32_t row_of_launch(const EncParams &a, int64_t x) {
+  const int32_t r = a.range_id[x];
+  return (r >= 0 && r < a.R_in && a.op_in[r] < a.NOPS) ? a.op_in[r] : a.NOPS;
+}
+
 // Run starts of a thread's launches inside its wave (bit k: launch k starts
 // a run; the wave's first launch always does), and the references' piece
 // starts (runs cut at every 16th launch as well).
@@ -147,7 +158,7 @@ __device__ __forceinline__ void run_heads(const uint32_t (&g)[kPer], int nv, uin
     const uint32_t prev = k ? g[k - 1] : (ln ? gl : 0xFFFFFFFFu);
     if (k < nv && g[k] != prev) hm |= 1u << k;
   }
-  hp = hm | ((nv > 0 && (ln & 1) == 0) ? 1u : 0u);
+  hp = piece_heads(hm, nv);
 }
 
 // Items and partial rows of the calling wave (all lanes get them).
@@ -299,6 +310,7 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
     uint32_t hm, hp, items, rows;
     run_heads(g, nv, hm, hp);
     wave_counts(hm, hp, items, rows);
+    a.em.hmb[bid * kEncThreads + tid] = (uint8_t)hm;
     if (ln == 0) {
       a.em.wi[bid * (kEncThreads / OPA_WAVE) + w] = items;
       a.em.wr[bid * (kEncThreads / OPA_WAVE) + w] = rows;
@@ -381,10 +393,8 @@ __global__ void __launch_bounds__(kEncThreads) k_emit(EncParams a) {
   const int64_t wave = (int64_t)blockIdx.x * (kEncThreads / OPA_WAVE) + w;
   const int64_t ib = (int64_t)blockIdx.x * kSpan + (int64_t)threadIdx.x * kPer;
   const int nv = (int)(a.T - ib < 0 ? 0 : (a.T - ib < kPer ? a.T - ib : kPer));
-  uint32_t g[kPer];
-  rows_from_ids(a, ib, nv, g);  // malformed ids were counted with the counts
-  uint32_t hm, hp;
-  run_heads(g, nv, hm, hp);
+  const uint32_t hm = a.em.hmb[(int64_t)blockIdx.x * kEncThreads + threadIdx.x];
+  const uint32_t hp = piece_heads(hm, nv);
   const uint32_t nh = __popc(hm), nhp = __popc(hp);
   const uint32_t hb = wave_incl_scan_add(nh) - nh;
   const uint32_t hpb = wave_incl_scan_add(nhp) - nhp;
@@ -397,7 +407,7 @@ __global__ void __launch_bounds__(kEncThreads) k_emit(EncParams a) {
     for (int k = 0; k < kPer; ++k) {
       if (!((hm >> k) & 1u)) continue;
       const uint32_t idx = hb + __popc(hm & ((1u << k) - 1u));
-      a.em.ig[ibase + idx] = g[k];
+      a.em.ig[ibase + idx] = row_of_launch(a, ib + k);
       a.em.ia[ibase + idx] = rbase + idx;
       a.em.ib[ibase + idx] = 0;
     }
@@ -412,7 +422,7 @@ __global__ void __launch_bounds__(kEncThreads) k_emit(EncParams a) {
       const uint32_t rest = hp >> (k + 1);
       const uint32_t len = rest ? (uint32_t)__ffs(rest) : (uint32_t)(nv - k) + spill;
       const uint32_t idx = hpb + __popc(hp & ((1u << k) - 1u));
-      a.em.ig[ibase + idx] = g[k];
+      a.em.ig[ibase + idx] = row_of_launch(a, ib + k);
       a.em.ia[ibase + idx] = (uint32_t)(ib + k);
       a.em.ib[ibase + idx] = len;
     }
@@ -449,8 +459,7 @@ k_agg_rows(EncParams a) {
   const int64_t bid = blockIdx.x;
   const int64_t ib = bid * kSpan + (int64_t)tid * kPer;
   const int nv = (int)(a.T - ib < 0 ? 0 : (a.T - ib < kPer ? a.T - ib : kPer));
-  uint32_t g[kPer];
-  rows_from_ids(a, ib, nv, g);  // malformed ids were counted by the plan
+  const uint32_t hm = a.em.hmb[bid * kEncThreads + tid];
   uint32_t mt[kPer];  // profiled row indices (as stored, -1 = unmatched)
   uint32_t du[kPer];
   load_run(reinterpret_cast<const uint32_t *>(in.match), ib, nv, mt);
@@ -460,8 +469,6 @@ k_agg_rows(EncParams a) {
   for (int k = 0; k < kPer; ++k)
     if (k < nv && ((int32_t)mt[k] < -1 || (int64_t)(int32_t)mt[k] >= in.P))
       bad++;  // aggregates as unmatched
-  uint32_t hm, hp;
-  run_heads(g, nv, hm, hp);
   const uint32_t nh = __popc(hm);
   const uint32_t hb = wave_incl_scan_add(nh) - nh;
   const uint32_t nr_w = __shfl(hb + nh, OPA_WAVE - 1, OPA_WAVE);

@@ -44,7 +44,7 @@ struct Plan {
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
   // aggregation
   int64_t cap_items, cap_rows, max_chunks;
-  size_t wi, wr, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, coff, cmap, sit, part;
+  size_t wi, wr, hmb, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, coff, cmap, sit, part;
   size_t misc;  // small device scalars
 };
 
@@ -164,6 +164,7 @@ struct AggIn;
 // Items planned by the enclosure pass for the aggregation (see agg.hip).
 struct EmitOut {
   uint32_t *wi, *wr;          // [waves] item / partial-row counts, then bases
+  uint8_t *hmb;               // [blocks * threads] run starts among a thread's launches
   uint32_t *ig, *ia, *ib;     // item: row, partial-row index or first launch, 0 or length
   PartRow *rows;
   int64_t *meta;
