@@ -9,9 +9,11 @@
 //   2. cut into chunks of at most 64 items of one row, each reduced by one
 //      wave (a lane loads a partial row or accumulates its referenced
 //      launches, then a butterfly reduction),
-//   3. combined per row over its chunks by one wave and finalised
-//      (duration-weighted means divided by the matched duration, NaN for
-//      absent counters and rows without matched launches).
+//   3. finalised (duration-weighted means divided by the matched duration,
+//      NaN for absent counters and rows without matched launches): a row of
+//      one chunk by the wave that reduced it, a row of several chunks by one
+//      wave that combines them in chunk order in a second pass. The summary
+//      over the table is taken by the finishing kernel.
 // Every sum is taken in a fixed order, so results are reproducible.
 #include "accum.h"
 #include "common.h"
@@ -203,48 +205,10 @@ __global__ void k_chunk_map(AggWork w) {
   for (uint32_t c = c0; c < c1; ++c) w.cmap[c] = g;
 }
 
-// 2. one wave per chunk of at most 64 items of one row
-template <bool DEF>
-__global__ void __launch_bounds__(256) k_chunk_reduce(AggWork w) {
-  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
-  const int64_t nch = w.meta[3];
+// the row's table entry from its combined partial (lane c writes counter c)
+__device__ __forceinline__ void write_row(const AggWork &w, uint32_t g, const Acc &acc,
+                                          uint32_t mx, uint32_t dw) {
   const int ln = lane_id();
-  for (int64_t ch = (int64_t)blockIdx.x * 4 + wave_id(); ch < nch; ch += (int64_t)gridDim.x * 4) {
-    const uint32_t g = w.cmap[ch];
-    const uint32_t p = w.goff[g] + (uint32_t)(ch - w.coff[g]) * kChunkItems + (uint32_t)ln;
-    Acc acc;
-    acc_zero(acc);
-    if (p < w.goff[g + 1]) {
-      const unsigned long long it = w.sit[p];
-      const uint32_t a = (uint32_t)it, b = (uint32_t)(it >> 32);
-      if (b == 0) {
-        acc_load(acc, w.rows + a);
-      } else {
-        for (uint32_t k = 0; k < b; ++k)
-          acc_launch(acc, w.in, w.in.match[a + k], w.in.dur[a + k], mx, dw);
-      }
-    }
-    acc_wave_reduce(acc, mx);
-    if (ln == 0) acc_store(w.part + ch, acc);
-  }
-}
-
-// 3. one wave per operator row: combine its chunks and finalise
-template <bool DEF>
-__global__ void __launch_bounds__(256) k_combine(AggWork w) {
-  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
-  const uint32_t g = blockIdx.x * 4 + wave_id();
-  if (g >= w.G) return;
-  const int ln = lane_id();
-  const uint32_t c0 = w.coff[g], c1 = w.coff[g + 1];
-  Acc acc;
-  acc_zero(acc);
-  for (uint32_t c = c0 + ln; c < c1; c += OPA_WAVE) {
-    Acc b;
-    acc_load(b, w.part + c);
-    acc_merge(acc, b, mx);
-  }
-  acc_wave_reduce(acc, mx);
   opattr_op_row *row = w.table + g;
   if (ln == 0) {
     row->kernel_count = acc.kc;
@@ -269,40 +233,53 @@ __global__ void __launch_bounds__(256) k_combine(AggWork w) {
   }
 }
 
-// summary over the finished rows (one block)
-__global__ void __launch_bounds__(1024) k_summary(AggWork w) {
-  __shared__ unsigned long long red[4][16];
-  unsigned long long at_ = 0, un = 0, tot = 0, mt = 0;
-  for (uint32_t g = threadIdx.x; g < w.G; g += 1024) {
-    const unsigned long long t = w.table[g].total_ns;
-    tot += t;
-    mt += w.table[g].matched_ns;
-    if (g < w.NOPS) at_ += t;
-    else un += t;
-  }
-  at_ = wave_reduce_add(at_);
-  un = wave_reduce_add(un);
-  tot = wave_reduce_add(tot);
-  mt = wave_reduce_add(mt);
-  if (lane_id() == 0) {
-    red[0][wave_id()] = at_;
-    red[1][wave_id()] = un;
-    red[2][wave_id()] = tot;
-    red[3][wave_id()] = mt;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    opattr_summary s{};
-    for (int k = 0; k < 16; ++k) {
-      s.attributed_ns += red[0][k];
-      s.unattributed_ns += red[1][k];
-      s.total_ns += red[2][k];
-      s.matched_ns += red[3][k];
+// 2. one wave per chunk of at most 64 items of one row; a row's only chunk
+// is finalised right away
+template <bool DEF>
+__global__ void __launch_bounds__(256) k_chunk_reduce(AggWork w) {
+  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
+  const int64_t nch = w.meta[3];
+  const int ln = lane_id();
+  for (int64_t ch = (int64_t)blockIdx.x * 4 + wave_id(); ch < nch; ch += (int64_t)gridDim.x * 4) {
+    const uint32_t g = w.cmap[ch];
+    const uint32_t c0 = w.coff[g];
+    const uint32_t p = w.goff[g] + (uint32_t)(ch - c0) * kChunkItems + (uint32_t)ln;
+    Acc acc;
+    acc_zero(acc);
+    if (p < w.goff[g + 1]) {
+      const unsigned long long it = w.sit[p];
+      const uint32_t a = (uint32_t)it, b = (uint32_t)(it >> 32);
+      if (b == 0) {
+        acc_load(acc, w.rows + a);
+      } else {
+        for (uint32_t k = 0; k < b; ++k)
+          acc_launch(acc, w.in, w.in.match[a + k], w.in.dur[a + k], mx, dw);
+      }
     }
-    s.attributed_fraction = s.total_ns ? (double)s.attributed_ns / (double)s.total_ns
-                                       : __longlong_as_double(0x7FF8000000000000ll);
-    *w.sum = s;
+    acc_wave_reduce(acc, mx);
+    if (w.coff[g + 1] - c0 == 1) write_row(w, g, acc, mx, dw);
+    else if (ln == 0) acc_store(w.part + ch, acc);
   }
+}
+
+// 3. one wave per operator row with no or several chunks
+template <bool DEF>
+__global__ void __launch_bounds__(256) k_combine(AggWork w) {
+  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
+  const uint32_t g = blockIdx.x * 4 + wave_id();
+  if (g >= w.G) return;
+  const int ln = lane_id();
+  const uint32_t c0 = w.coff[g], c1 = w.coff[g + 1];
+  if (c1 - c0 == 1) return;  // finalised with its chunk
+  Acc acc;
+  acc_zero(acc);
+  for (uint32_t c = c0 + ln; c < c1; c += OPA_WAVE) {
+    Acc b;
+    acc_load(b, w.part + c);
+    acc_merge(acc, b, mx);
+  }
+  acc_wave_reduce(acc, mx);
+  write_row(w, g, acc, mx, dw);
 }
 
 static AggWork agg_work(const EncArgs &x) {
@@ -365,7 +342,6 @@ void reduce_items(const EncArgs &x, hipStream_t s) {
   }
   if (def) k_combine<true><<<(pl.G + 3) / 4, 256, 0, s>>>(w);
   else k_combine<false><<<(pl.G + 3) / 4, 256, 0, s>>>(w);
-  k_summary<<<1, 1024, 0, s>>>(w);
   probe_end(OPATTR_PROBE_AGGREGATE, s);
 }
 

@@ -133,18 +133,54 @@ static bool ws_ok(const void *ws, size_t ws_bytes, const Plan &pl) {
   return ws && (reinterpret_cast<uintptr_t>(ws) & 255) == 0 && ws_bytes >= pl.total;
 }
 
-// nesting_errors from the per-stream crossing flags; status from the flags
-__global__ void __launch_bounds__(256) k_finish(opattr_diag *diag, const uint8_t *sflag,
-                                                uint32_t ns) {
+// nesting_errors from the per-stream crossing flags; status from the flags;
+// with a table, the summary over its rows (one block)
+__global__ void __launch_bounds__(1024) k_finish(opattr_diag *diag, const uint8_t *sflag,
+                                                 uint32_t ns, const opattr_op_row *table,
+                                                 opattr_summary *sum, uint32_t G,
+                                                 uint32_t NOPS) {
   __shared__ uint32_t cnt;
+  __shared__ unsigned long long red[4][16];
   if (threadIdx.x == 0) cnt = 0;
   __syncthreads();
   if (sflag) {
     uint32_t c = 0;
-    for (uint32_t s = threadIdx.x; s < ns; s += 256) c += sflag[s] ? 1u : 0u;
+    for (uint32_t s = threadIdx.x; s < ns; s += blockDim.x) c += sflag[s] ? 1u : 0u;
     if (c) atomicAdd(&cnt, c);
   }
+  if (table) {
+    unsigned long long at_ = 0, un = 0, tot = 0, mt = 0;
+    for (uint32_t g = threadIdx.x; g < G; g += blockDim.x) {
+      const unsigned long long t = table[g].total_ns;
+      tot += t;
+      mt += table[g].matched_ns;
+      if (g < NOPS) at_ += t;
+      else un += t;
+    }
+    at_ = wave_reduce_add(at_);
+    un = wave_reduce_add(un);
+    tot = wave_reduce_add(tot);
+    mt = wave_reduce_add(mt);
+    if (lane_id() == 0) {
+      red[0][wave_id()] = at_;
+      red[1][wave_id()] = un;
+      red[2][wave_id()] = tot;
+      red[3][wave_id()] = mt;
+    }
+  }
   __syncthreads();
+  if (threadIdx.x == 0 && table) {
+    opattr_summary s{};
+    for (uint32_t k = 0; k < blockDim.x / OPA_WAVE; ++k) {
+      s.attributed_ns += red[0][k];
+      s.unattributed_ns += red[1][k];
+      s.total_ns += red[2][k];
+      s.matched_ns += red[3][k];
+    }
+    s.attributed_fraction = s.total_ns ? (double)s.attributed_ns / (double)s.total_ns
+                                       : __longlong_as_double(0x7FF8000000000000ll);
+    *sum = s;
+  }
   if (threadIdx.x == 0) {
     if (sflag) diag->nesting_errors = cnt;
     uint32_t f = diag->flags;
@@ -164,9 +200,10 @@ __global__ void __launch_bounds__(256) k_finish(opattr_diag *diag, const uint8_t
   }
 }
 
-void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s) {
+void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s,
+                   const opattr_op_row *table, opattr_summary *sum, uint32_t G, uint32_t NOPS) {
   probe_begin(OPATTR_PROBE_FINALIZE, s);
-  k_finish<<<1, 256, 0, s>>>(diag, sflag, ns);
+  k_finish<<<1, 1024, 0, s>>>(diag, sflag, ns, table, sum, G, NOPS);
   probe_end(OPATTR_PROBE_FINALIZE, s);
 }
 
@@ -387,7 +424,7 @@ int opattr_aggregate(const opattr_kernels *k, const opattr_profiled *p, const in
   e.ws = ws;
   e.pl = &pl;
   run_aggregate_all(e, s);
-  launch_finish(diag, nullptr, 0, s);
+  launch_finish(diag, nullptr, 0, s, table, sum, pl.G, d->n_ops);
   return launch_status();
 }
 
@@ -444,7 +481,7 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   run_match(a, s);
   if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
   run_reduce(e, s);
-  launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s);
+  launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s, table, sum, pl.G, d->n_ops);
   return launch_status();
 }
 

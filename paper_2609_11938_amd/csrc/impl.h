@@ -201,6 +201,10 @@ void plan_items(const EncArgs &a, hipStream_t s);
 void reduce_items(const EncArgs &a, hipStream_t s);
 
 // ---- finish (api.hip) ---------------------------------------------------------
-void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s);
+// status of the diag record; with a table, also the summary over its G rows
+// (rows below NOPS attributed)
+void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s,
+                   const opattr_op_row *table = nullptr, opattr_summary *sum = nullptr,
+                   uint32_t G = 0, uint32_t NOPS = 0);
 
 }  // namespace opa
