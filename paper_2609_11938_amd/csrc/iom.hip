@@ -219,12 +219,14 @@ __device__ inline void seg_table(const TlArgs &a, int64_t t, SegTable &sm) {
   if (ln == OPA_WAVE - 1) sm.pre[OPA_WAVE] = inc;
 }
 
-// Partitions of the launches with seq base - 1 (wave 1) and base + 4096
-// (wave 2) in sm.edge: the last launch before, or the first launch of, some
-// stream's segment (the caller synchronises).
-__device__ inline void seg_edges(const TlArgs &a, int64_t t, SegTable &sm) {
+// The launches with seq base - 1 (wave 1) and base + 4096 (wave 2) are the
+// last launch before, or the first launch of, some stream's segment. Lane s
+// of those waves holds its stream's candidate (or -1); the caller loads the
+// candidate's ids with the tile's own loads and keeps the first candidate
+// whose seq matches.
+__device__ __forceinline__ int64_t edge_candidate(const TlArgs &a, int64_t t) {
   const int ln = lane_id(), w = wave_id();
-  if (w != 1 && w != 2) return;
+  if (w != 1 && w != 2) return -1;
   const int64_t base = t * OPA_TILE;
   const uint64_t T = (uint64_t)a.T;
   const int side = w - 1;
@@ -234,21 +236,13 @@ __device__ inline void seg_edges(const TlArgs &a, int64_t t, SegTable &sm) {
     const int64_t b = a.bnd[(t + side) * a.NS + ln];
     const int64_t s0 = a.kblk[ln], s1 = a.kblk[ln + 1];
     c = side ? b : b - 1;
-    if (c < s0 || c >= s1 || c < 0 || (uint64_t)c >= T || (uint64_t)a.seq[c] != want) c = -1;
+    if (c < s0 || c >= s1 || c < 0 || (uint64_t)c >= T) c = -1;
   }
-  const uint64_t m = __ballot(c >= 0);
-  const int src = m ? __ffsll((unsigned long long)m) - 1 : 0;
-  const int64_t cj = __shfl(c, src, OPA_WAVE);
-  int32_t lp = -2;
-  if (cj >= 0) {
-    uint32_t k;
-    tl_classify(a, cj, k, lp);
-  }
-  if (ln == 0) sm.edge[side] = lp;
+  return c;
 }
 
 // Input index of the launch at position e of tile t's segment order (or -1).
-__device__ __forceinline__ int64_t seg_elem(const SegTable &sm, uint32_t e, int64_t T) {
+__device__ __forceinline__ int32_t seg_elem(const SegTable &sm, uint32_t e, int64_t T) {
   const uint32_t total = sm.pre[OPA_WAVE] < OPA_TILE ? sm.pre[OPA_WAVE] : OPA_TILE;
   if (e >= total) return -1;
   int lo = 0, hi = OPA_WAVE;  // last segment with pre <= e
@@ -259,10 +253,12 @@ __device__ __forceinline__ int64_t seg_elem(const SegTable &sm, uint32_t e, int6
     else hi = mid;
   }
   const int64_t i = (int64_t)sm.lo[lo] + (e - sm.pre[lo]);
-  return i < T ? i : -1;
+  return i < T ? (int32_t)i : -1;
 }
 
-// Fill TileData for seq tile t from its segments. Ends with a barrier.
+// Fill TileData for seq tile t from its segments. Ends with a barrier. The
+// loads come in two batches for all elements at once: seq rank, name and
+// partition; then the partitions' class representatives.
 __device__ inline uint32_t seg_tile(const TlArgs &a, int64_t t, TileData &sm) {
   const int tid = threadIdx.x;
   const int64_t base = t * OPA_TILE;
@@ -271,29 +267,61 @@ __device__ inline uint32_t seg_tile(const TlArgs &a, int64_t t, TileData &sm) {
     sm.lp[x] = -2;
   }
   seg_table(a, t, sm.sg);
+  const int64_t ec = edge_candidate(a, t);
   __syncthreads();
-  // element e = c * 256 + tid: a fixed, unrolled count so that the loads of
-  // all chunks are in flight together
-  int64_t ii[kWaveChunks];
-  uint32_t sq[kWaveChunks];
+  int32_t ii[kWaveChunks];
+  uint32_t sq[kWaveChunks], nm[kWaveChunks];
+  int32_t pt[kWaveChunks];
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c)
     ii[c] = seg_elem(sm.sg, (uint32_t)(c * OPA_TILE_THREADS + tid), a.T);
 #pragma unroll
-  for (int c = 0; c < kWaveChunks; ++c) sq[c] = ii[c] >= 0 ? a.seq[ii[c]] : 0u;
+  for (int c = 0; c < kWaveChunks; ++c) {
+    sq[c] = ii[c] >= 0 ? a.seq[ii[c]] : 0u;
+    nm[c] = ii[c] >= 0 ? a.name[ii[c]] : a.NN;
+    pt[c] = (ii[c] >= 0 && a.part) ? a.part[ii[c]] : -1;
+  }
+  uint64_t esq = 0;
+  uint32_t enm = a.NN;
+  int32_t ept = -2;
+  if (ec >= 0) {
+    esq = a.seq[ec];
+    enm = a.name[ec];
+    ept = a.part ? a.part[ec] : -1;
+  }
+  // class representatives, and the key / partition of every element
   uint32_t bad = 0;
+  int32_t rp[kWaveChunks];
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const bool ok = nm[c] < a.NN && pt[c] >= -1 && (pt[c] < 0 || (uint32_t)pt[c] < a.NP);
+    rp[c] = (ii[c] >= 0 && ok && pt[c] >= 0) ? a.part_rep[pt[c]] : -1;
+  }
+  const bool eok = enm < a.NN && ept >= -1 && (ept < 0 || (uint32_t)ept < a.NP);
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
     if (ii[c] < 0) continue;
     const int64_t x = (int64_t)sq[c] - base;
     if (x < 0 || x >= OPA_TILE || base + x >= a.T) continue;  // a broken promise: left out
-    uint32_t key;
-    int32_t lp;
-    bad += tl_classify(a, ii[c], key, lp);
-    sm.key[x] = (uint16_t)key;
-    sm.lp[x] = lp;
+    const bool ok = nm[c] < a.NN && pt[c] >= -1 && (pt[c] < 0 || (uint32_t)pt[c] < a.NP);
+    if (!ok) {
+      bad++;
+      continue;
+    }
+    sm.key[x] = (uint16_t)((pt[c] < 0 || rp[c] == pt[c]) ? nm[c] : a.NN);
+    sm.lp[x] = pt[c];
   }
-  seg_edges(a, t, sm.sg);  // needed only at the end, so after the tile's loads
+  // edges: the first stream whose candidate has the wanted seq rank
+  const int w = wave_id();
+  if (w == 1 || w == 2) {
+    const int side = w - 1;
+    const uint64_t want = side ? (uint64_t)base + OPA_TILE : (uint64_t)base - 1;
+    const uint64_t m = __ballot(ec >= 0 && esq == want);
+    const int src = m ? __ffsll((unsigned long long)m) - 1 : 0;
+    const int32_t lp = eok ? ept : -2;
+    const int32_t got = __shfl(lp, src, OPA_WAVE);
+    if (lane_id() == 0) sm.sg.edge[side] = m ? got : -2;
+  }
   __syncthreads();
   return bad;
 }

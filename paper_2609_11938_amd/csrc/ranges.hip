@@ -52,22 +52,42 @@ __global__ void k_rcheck(CoreRanges cr, opattr_diag *diag) {
   }
 }
 
-// blk[s] = first core position with stream >= s, s = 0..NS
-__global__ void k_blocks16(const uint16_t *st, int64_t n, uint32_t NS, int64_t *blk) {
-  const uint32_t s = blockIdx.x * blockDim.x + threadIdx.x;
+// blk[s] = first position with stream >= s, s = 0..NS (the array is sorted
+// by stream). One wave per s: each round, the 64 lanes probe 64 evenly spaced
+// positions and the range shrinks to the gap where the answer lies.
+__global__ void __launch_bounds__(256) k_blocks16(const uint16_t *st, int64_t n, uint32_t NS,
+                                                  int64_t *blk) {
+  const uint32_t s = blockIdx.x * (blockDim.x / OPA_WAVE) + wave_id();
   if (s > NS) return;
-  int64_t lo = 0, hi = n;
-  while (lo < hi) {
-    const int64_t mid = (lo + hi) >> 1;
-    if (st[mid] < s) lo = mid + 1;
-    else hi = mid;
+  const int ln = lane_id();
+  int64_t lo = 0, hi = n;  // answer in [lo, hi]
+  while (hi - lo > OPA_WAVE) {
+    const int64_t step = (hi - lo + OPA_WAVE - 1) / OPA_WAVE;
+    int64_t p = lo + (int64_t)(ln + 1) * step - 1;
+    if (p > hi - 1) p = hi - 1;
+    const uint64_t m = __ballot(st[p] >= s);
+    if (m == 0) {
+      lo = hi;
+      break;
+    }
+    const int f = __ffsll((unsigned long long)m) - 1;  // first probe at or past s
+    int64_t pf = lo + (int64_t)(f + 1) * step - 1;
+    if (pf > hi - 1) pf = hi - 1;
+    lo = f == 0 ? lo : lo + (int64_t)f * step;
+    hi = pf;  // st[pf] >= s
   }
-  blk[s] = lo;
+  if (hi - lo <= OPA_WAVE && lo < hi) {
+    const int64_t p = lo + ln;
+    const uint64_t m = __ballot(p < hi && st[p] >= s);
+    lo = m ? lo + __ffsll((unsigned long long)m) - 1 : hi;
+  }
+  if (ln == 0) blk[s] = lo;
 }
 
 void launch_stream_blocks(const uint16_t *st, int64_t n, uint32_t NS, int64_t *blk,
                           hipStream_t s) {
-  k_blocks16<<<(NS + 1 + 255) / 256, 256, 0, s>>>(st, n, NS, blk);
+  const uint32_t waves = NS + 1;
+  k_blocks16<<<(waves + 3) / 4, 256, 0, s>>>(st, n, NS, blk);
 }
 
 // tbase[s] = first tile of stream s (tiles never straddle streams)
@@ -357,7 +377,7 @@ CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws
   if (R > 0)
     k_rprep<<<(unsigned)((R + 255) / 256), 256, 0, s>>>(cr, NS, d->n_ops, at<int64_t>(ws, pl.ree),
                                                         at<int32_t>(ws, pl.npg), diag);
-  if (R > 0) k_blocks16<<<(NS + 1 + 255) / 256, 256, 0, s>>>(cr.st, R, NS, rblk);
+  if (R > 0) launch_stream_blocks(cr.st, R, NS, rblk, s);
   else fill_u32(reinterpret_cast<uint32_t *>(rblk), 0, 2 * ((int64_t)NS + 1), s);
   return cr;
 }
