@@ -415,13 +415,12 @@ __global__ void k_rep_check(const int32_t *__restrict__ part_rep, uint32_t NP, o
 
 // ---------------------------------------------------------------------------
 // Fast path, histogram kernel: per seq tile, the per-name counts of eligible
-// launches (tlh row), each launch's in-tile rank (rit) and key (kbs) by seq
-// position, and the partition edges.
+// launches (tlh row), each launch's key and in-tile rank by seq position
+// (kr = key << 16 | rank), and the partition edges.
 // ---------------------------------------------------------------------------
 struct HistOut {
   uint32_t *tlh;
-  uint16_t *rit;
-  uint32_t *kbs;
+  uint32_t *kr;
   uint32_t *pfirst, *plast, *pheads;  // pheads NULL: no partitions
   opattr_diag *diag;
 };
@@ -445,8 +444,8 @@ __global__ void __launch_bounds__(256) k_tl_hist_w(TlArgs a, HistOut o) {
   for (int c = 0; c < kWaveChunks; ++c) {
     const int e = tile_elem(c);
     if (base + e >= a.T) continue;
-    o.rit[base + e] = key[c] < NN ? (uint16_t)(wb[key[c]] + rank[c]) : (uint16_t)0;
-    o.kbs[base + e] = key[c];
+    const uint32_t r = key[c] < NN ? (uint32_t)(wb[key[c]] + rank[c]) : 0u;
+    o.kr[base + e] = (key[c] << 16) | r;
   }
   if (o.pheads) part_edges(sm.lp, base, sm.sg.edge[0], sm.sg.edge[1], o.pfirst, o.plast, o.pheads);
   if (bad) atomicAdd(&sm.bad, bad);
@@ -467,35 +466,33 @@ struct LookArgs {
   const uint32_t *tlh;  // exclusive prefix of each name down the tiles
   const uint32_t *tlc, *pfc, *off;
   const int32_t *slot;
-  const uint16_t *rit;
-  const uint32_t *kbs;
+  const uint32_t *kr;   // key << 16 | in-tile rank, by seq rank
   const PartRec *prec;  // NULL: no dedup broadcast (duplicates get -1)
   int32_t *match;
   int skip_name;
   opattr_diag *diag;
 };
 
-__device__ __forceinline__ int32_t row_of(const LookArgs &m, uint32_t NN, uint32_t n, uint32_t x) {
-  const uint32_t r = m.tlh[(int64_t)(x >> OPA_SLOT_BITS) * NN + n] + m.rit[x];
-  const uint32_t rows = m.pfc[n];
-  int32_t mt = r < rows ? m.slot[m.off[n] + r] : -1;
-  if (m.skip_name && m.tlc[n] != rows) mt = -1;
-  return mt;
-}
-
+// Loads come in batches for all of a thread's elements at once: ids; the
+// partition record; the source launch's key and in-tile rank, the name's
+// prefix in the source tile and the name's rows; the row itself.
 template <bool SEG>
-__global__ void __launch_bounds__(256) k_tl_look(TlArgs a, LookArgs m) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
+k_tl_look(TlArgs a, LookArgs m) {
   __shared__ SegTable sm;
+  __shared__ int32_t sii[OPA_TILE];  // input index of each element (kept out of registers)
   __shared__ unsigned long long serr;
   const int tid = threadIdx.x;
   const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
   const uint32_t NN = a.NN;
+  constexpr uint32_t kNone = 0xFFFFFFFFu;
   if (tid == 0) serr = 0;
   if (SEG) seg_table(a, tile, sm);
   __syncthreads();
-  // phase 1: input index and seq rank of each element
-  int64_t ii[kWaveChunks];
-  uint32_t xs[kWaveChunks];
+  // batch 1: input index, seq rank, name and partition of each element
+  int32_t ii[kWaveChunks];
+  uint32_t xs[kWaveChunks], nm[kWaveChunks];
+  int32_t pt[kWaveChunks];
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
     const uint32_t e = (uint32_t)(c * OPA_TILE_THREADS + tid);
@@ -506,19 +503,15 @@ __global__ void __launch_bounds__(256) k_tl_look(TlArgs a, LookArgs m) {
   for (int c = 0; c < kWaveChunks; ++c) {
     const uint32_t e = (uint32_t)(c * OPA_TILE_THREADS + tid);
     xs[c] = SEG ? (ii[c] >= 0 ? a.seq[ii[c]] : 0u) : (uint32_t)(base + e);
-    if (SEG && (int64_t)xs[c] >= a.T) ii[c] = -1;  // a broken promise: left out
-  }
-  // phase 2: ids, then how each launch finds its row
-  uint32_t nm[kWaveChunks];
-  int32_t pt[kWaveChunks];
-#pragma unroll
-  for (int c = 0; c < kWaveChunks; ++c) {
     nm[c] = ii[c] >= 0 ? a.name[ii[c]] : NN;
     pt[c] = (ii[c] >= 0 && a.part) ? a.part[ii[c]] : -1;
   }
+  // batch 2: how each launch finds its row
   PartRec rc[kWaveChunks];
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
+    if (SEG && (int64_t)xs[c] >= a.T) ii[c] = -1;  // a broken promise: left out
+    sii[c * OPA_TILE_THREADS + tid] = ii[c];
     const bool good = nm[c] < NN && pt[c] >= -1 && (pt[c] < 0 || (uint32_t)pt[c] < a.NP);
     rc[c] = PartRec{0, kRecNone};
     if (!good || ii[c] < 0) continue;
@@ -526,27 +519,51 @@ __global__ void __launch_bounds__(256) k_tl_look(TlArgs a, LookArgs m) {
     else if (m.prec) rc[c] = m.prec[pt[c]];
     else if (a.part_rep[pt[c]] == pt[c]) rc[c].hi = kRecEligible;
   }
-  // phase 3: the seq rank whose rank gives the row (own, or the launch at the
-  // same position of the representative partition, if it has this name)
-  uint32_t src[kWaveChunks];
-  uint32_t err = 0;
+  // batch 3: the seq rank whose rank gives the row (own, or the launch at the
+  // same position of the representative partition), its key and in-tile
+  // rank, the name's prefix in that tile, and the name's rows
+  uint32_t kr[kWaveChunks], pre[kWaveChunks], rows[kWaveChunks], ro[kWaveChunks];
+  uint32_t dup = 0, err = 0;  // bit c: element c is a duplicate
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
-    src[c] = 0xFFFFFFFFu;
+    uint32_t src = kNone;
     const uint32_t hi = rc[c].hi;
     if (hi == kRecEligible) {
-      src[c] = xs[c];
+      src = xs[c];
     } else if (hi != kRecNone) {
-      const uint32_t y = xs[c] + (uint32_t)rc[c].delta;
-      if (xs[c] < hi && m.kbs[y] == nm[c]) src[c] = y;
-      else err++;
+      if (xs[c] < hi) {
+        src = xs[c] + (uint32_t)rc[c].delta;
+        dup |= 1u << c;
+      } else {
+        err++;
+      }
+    }
+    kr[c] = kNone;
+    pre[c] = rows[c] = ro[c] = 0;
+    if (src != kNone) {
+      kr[c] = m.kr[src];
+      pre[c] = m.tlh[(int64_t)(src >> OPA_SLOT_BITS) * NN + nm[c]];
+      rows[c] = m.pfc[nm[c]];
+      ro[c] = m.off[nm[c]];
+      if (m.skip_name && m.tlc[nm[c]] != rows[c]) rows[c] = 0;  // the name is left out
     }
   }
-  // phase 4: rows
+  // batch 4: rows; a duplicate needs the representative's launch at its
+  // position to have the same name
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
-    if (ii[c] < 0) continue;
-    m.match[ii[c]] = src[c] != 0xFFFFFFFFu ? row_of(m, NN, nm[c], src[c]) : -1;
+    const int32_t i = sii[c * OPA_TILE_THREADS + tid];
+    if (i < 0) continue;
+    int32_t mt = -1;
+    if (kr[c] != kNone) {
+      if (((dup >> c) & 1u) && (kr[c] >> 16) != nm[c]) {
+        err++;
+      } else {
+        const uint32_t r = pre[c] + (kr[c] & 0xFFFFu);
+        if (r < rows[c]) mt = m.slot[ro[c] + r];
+      }
+    }
+    m.match[i] = mt;
   }
   const unsigned long long e = wave_reduce_add((unsigned long long)err);
   if (lane_id() == 0 && e) atomicAdd(&serr, e);
@@ -1113,8 +1130,7 @@ void run_match(const IomArgs &x, hipStream_t s) {
   }
   HistOut ho;
   ho.tlh = tlh;
-  ho.rit = at<uint16_t>(ws, pl.rit);
-  ho.kbs = at<uint32_t>(ws, pl.nbs);
+  ho.kr = at<uint32_t>(ws, pl.nbs);
   ho.pfirst = pfirst;
   ho.plast = plast;
   ho.pheads = parts ? pheads : nullptr;
@@ -1151,8 +1167,7 @@ void run_match(const IomArgs &x, hipStream_t s) {
       m.pfc = pfc;
       m.off = off;
       m.slot = at<int32_t>(ws, pl.slot);
-      m.rit = ho.rit;
-      m.kbs = ho.kbs;
+      m.kr = ho.kr;
       m.prec = prec;
       m.match = x.match;
       m.skip_name = x.policy == OPATTR_MISMATCH_SKIP_NAME ? 1 : 0;
