@@ -76,8 +76,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.pheads = b.take(dd ? (size_t)pl.NP * 4 : 0);
   pl.prec = b.take(dd ? (size_t)pl.NP * 8 : 0);
   pl.mbs = b.take(dd ? T * 4 : 0);
-  pl.nbs = b.take(T * 4);  // dedup source names, or the fast path's keys by seq rank
-  pl.rit = b.take(T * 2);  // fast path: in-tile rank by seq rank
+  pl.nbs = b.take(T * 4);  // dedup source names, or the fast path's key and in-tile rank
   const bool rs = !pl.ranges_nested;
   pl.rperm = b.take(rs ? R * 4 : 0);
   pl.rs_c = b.take(rs ? R * 8 : 0);

@@ -38,7 +38,7 @@ struct Plan {
   // IOM
   size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist, rs_hist_r, kblk, tbnd;
   size_t tlh, pfh, tlch, pfch, tlc, pfc, off, slot;
-  size_t pfirst, plast, pheads, prec, mbs, nbs, rit;
+  size_t pfirst, plast, pheads, prec, mbs, nbs;
   // ranges
   size_t rperm, rs_c, re_c, rst_c, rop_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
