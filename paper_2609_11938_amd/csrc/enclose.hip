@@ -246,21 +246,32 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
     bool have = false;  // the previous launch was searched
     uint16_t sprev = 0;
     uint64_t qprev = 0;
-    int64_t pprev = 0, jprev = -1;
+    int64_t pprev = 0, jprev = -1, eprev = 0;  // eprev = ree[jprev] when jprev is a range
     int sprevsteps = 0;
+    int32_t rlast = -1, olast = -1;  // the last range found, its output id and row
+    uint32_t glast = 0;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
       int32_t rid = -1;
       if (k < nv && st[k] < a.NS && q[k] < (1ull << 63)) {
         const int64_t lo = a.rblk[st[k]], hi = a.rblk[st[k] + 1];
-        int64_t j;
+        const bool win = staged && st[k] == s0;  // the staged starts belong to this stream
+        int64_t j, ej = 0;
         int steps = 0;
+        bool fresh = true;
         if (have && st[k] == sprev && q[k] >= qprev) {
           int64_t p = pprev;
-          while (p + 1 < hi && a.cr.s[p + 1] <= q[k]) ++p;
+          while (p + 1 < hi) {
+            const int64_t x = p + 1 - wlo;
+            const uint64_t sx = (win && x >= 0 && x < wn) ? sS[x] : a.cr.s[p + 1];
+            if (sx > q[k]) break;
+            ++p;
+          }
           if (p == pprev) {
             j = jprev;
             steps = sprevsteps;
+            ej = eprev;
+            fresh = false;
           } else {
             j = p;
           }
@@ -270,7 +281,7 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
           int64_t p;
           if (in0 && wn == 0) {
             p = lo - 1;  // no range of the stream starts at or before the block's queries
-          } else if (in0 && staged) {
+          } else if (win) {
             int l2 = 0, h2 = (int)wn;
             while (l2 < h2) {
               const int mid = (l2 + h2) >> 1;
@@ -285,22 +296,30 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
           j = p;
           pprev = p;
         }
-        while (j >= lo && a.ree[j] < (int64_t)q[k] && steps < kMaxWalk) {
+        if (fresh && j >= lo) ej = a.ree[j];
+        while (j >= lo && ej < (int64_t)q[k] && steps < kMaxWalk) {
           j = a.npg[j];
           ++steps;
+          if (j >= lo) ej = a.ree[j];
         }
-        if (j >= lo && a.ree[j] >= (int64_t)q[k]) rid = (int32_t)j;
+        if (j >= lo && ej >= (int64_t)q[k]) rid = (int32_t)j;
         have = true;
         sprev = st[k];
         qprev = q[k];
         jprev = j;
+        eprev = ej;
         sprevsteps = steps;
       } else {
         if (k < nv && st[k] >= a.NS) bad++;
         have = false;
       }
-      rout[k] = rid >= 0 ? (a.cr.perm ? a.cr.perm[rid] : rid) : -1;
-      g[k] = k < nv ? (rid >= 0 ? a.cr.op[rid] : a.NOPS) : 0xFFFFFFFFu;
+      if (rid >= 0 && rid != rlast) {
+        rlast = rid;
+        olast = a.cr.perm ? a.cr.perm[rid] : rid;
+        glast = a.cr.op[rid];
+      }
+      rout[k] = rid >= 0 ? olast : -1;
+      g[k] = k < nv ? (rid >= 0 ? glast : a.NOPS) : 0xFFFFFFFFu;
     }
     store_run(a.range_id, ib, nv, rout);
   } else {
