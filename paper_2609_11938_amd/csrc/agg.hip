@@ -55,6 +55,7 @@ AggIn agg_inputs(const EncArgs &x) {
 
 struct AggWork {
   uint32_t G, NOPS, absent;
+  int64_t tcap;  // item tiles of 4096 the histogram table holds
   AggIn in;
   const uint32_t *ig, *ia, *ib;
   const PartRow *rows;
@@ -66,30 +67,47 @@ struct AggWork {
   opattr_summary *sum;
 };
 
+// Item tiles hold 1024 items (4 per thread) when the items fit the
+// histogram table that way, else 4096 (16 per thread): small tiles give
+// more blocks for the usual item counts, and the table is sized for the
+// worst case (one item per launch) in 4096-item tiles.
+template <int PER>
 __device__ __forceinline__ int64_t item_x(int64_t tile, int c) {
-  return tile * OPA_TILE + wave_id() * (OPA_TILE / 4) + c * OPA_WAVE + lane_id();
+  constexpr int kTile = 256 * PER;
+  return tile * kTile + wave_id() * (kTile / 4) + c * OPA_WAVE + lane_id();
 }
 
-// 1a. per-tile row histograms of the items (tile = 4096 items in launch order)
-__global__ void __launch_bounds__(256) k_item_hist_w(AggWork w) {
-  extern __shared__ __align__(16) unsigned char raw[];
-  uint16_t *cnt = reinterpret_cast<uint16_t *>(raw);
-  const int64_t n = w.meta[0];
-  const int64_t ntiles = (n + OPA_TILE - 1) / OPA_TILE;
+__device__ __forceinline__ bool small_item_tiles(const AggWork &w, int64_t n) {
+  return n <= w.tcap * 1024;
+}
+
+// 1a. per-tile row histograms of the items (tiles in launch order)
+template <int PER>
+__device__ inline void item_hist(const AggWork &w, int64_t n, uint16_t *cnt) {
+  constexpr int kTile = 256 * PER;
+  const int64_t ntiles = (n + kTile - 1) / kTile;
   if (blockIdx.x == 0 && threadIdx.x == 0) w.meta[2] = ntiles;
   for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     __syncthreads();
     for (uint32_t i = threadIdx.x; i < 4 * w.G; i += 256) cnt[i] = 0;
     __syncthreads();
-    uint32_t key[16], rank[16];
+    uint32_t key[PER], rank[PER];
 #pragma unroll
-    for (int c = 0; c < 16; ++c) {
-      const int64_t x = item_x(tile, c);
+    for (int c = 0; c < PER; ++c) {
+      const int64_t x = item_x<PER>(tile, c);
       key[c] = x < n ? w.ig[x] : w.G;
     }
-    wave_rank<16>(key, w.G, bits_for(w.G), cnt + wave_id() * w.G, rank);
+    wave_rank<PER>(key, w.G, bits_for(w.G), cnt + wave_id() * w.G, rank);
     block_rank_bases(cnt, w.G, w.ith + tile * w.G);
   }
+}
+
+__global__ void __launch_bounds__(256) k_item_hist_w(AggWork w) {
+  extern __shared__ __align__(16) unsigned char raw[];
+  uint16_t *cnt = reinterpret_cast<uint16_t *>(raw);
+  const int64_t n = w.meta[0];
+  if (small_item_tiles(w, n)) item_hist<4>(w, n, cnt);
+  else item_hist<16>(w, n, cnt);
 }
 
 // 1a'. the same with an LDS radix sort per tile, for many rows
@@ -142,33 +160,40 @@ __global__ void __launch_bounds__(1024) k_row_offsets(AggWork w) {
 }
 
 // 1c. stable scatter of the items into row order
-__global__ void __launch_bounds__(256) k_item_scatter_w(AggWork w) {
-  extern __shared__ __align__(16) unsigned char raw[];
-  uint16_t *cnt = reinterpret_cast<uint16_t *>(raw);
-  const int64_t n = w.meta[0];
-  const int64_t ntiles = (n + OPA_TILE - 1) / OPA_TILE;
+template <int PER>
+__device__ inline void item_scatter(const AggWork &w, int64_t n, uint16_t *cnt) {
+  constexpr int kTile = 256 * PER;
+  const int64_t ntiles = (n + kTile - 1) / kTile;
   for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     __syncthreads();
     for (uint32_t i = threadIdx.x; i < 4 * w.G; i += 256) cnt[i] = 0;
     __syncthreads();
-    uint32_t key[16], rank[16];
+    uint32_t key[PER], rank[PER];
 #pragma unroll
-    for (int c = 0; c < 16; ++c) {
-      const int64_t x = item_x(tile, c);
+    for (int c = 0; c < PER; ++c) {
+      const int64_t x = item_x<PER>(tile, c);
       key[c] = x < n ? w.ig[x] : w.G;
     }
-    wave_rank<16>(key, w.G, bits_for(w.G), cnt + wave_id() * w.G, rank);
+    wave_rank<PER>(key, w.G, bits_for(w.G), cnt + wave_id() * w.G, rank);
     block_rank_bases(cnt, w.G, nullptr);
     const uint32_t *row = w.ith + tile * w.G;
     const uint16_t *wb = cnt + wave_id() * w.G;
 #pragma unroll
-    for (int c = 0; c < 16; ++c) {
+    for (int c = 0; c < PER; ++c) {
       const uint32_t g = key[c];
       if (g >= w.G) continue;
-      const int64_t x = item_x(tile, c);
+      const int64_t x = item_x<PER>(tile, c);
       w.sit[w.goff[g] + row[g] + wb[g] + rank[c]] = w.ia[x] | ((unsigned long long)w.ib[x] << 32);
     }
   }
+}
+
+__global__ void __launch_bounds__(256) k_item_scatter_w(AggWork w) {
+  extern __shared__ __align__(16) unsigned char raw[];
+  uint16_t *cnt = reinterpret_cast<uint16_t *>(raw);
+  const int64_t n = w.meta[0];
+  if (small_item_tiles(w, n)) item_scatter<4>(w, n, cnt);
+  else item_scatter<16>(w, n, cnt);
 }
 
 __global__ void __launch_bounds__(256) k_item_scatter_r(AggWork w) {
@@ -286,6 +311,7 @@ static AggWork agg_work(const EncArgs &x) {
   const Plan &pl = *x.pl;
   AggWork w{};
   w.G = pl.G;
+  w.tcap = pl.ntrt;
   w.NOPS = x.d->n_ops;
   w.absent = x.p->absent_mask;
   w.in = agg_inputs(x);
