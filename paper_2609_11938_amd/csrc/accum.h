@@ -106,29 +106,59 @@ __device__ __forceinline__ void acc_merge(Acc &a, const Acc &b, uint32_t maxmask
   a.nan |= b.nan;
 }
 
-// One step of a segmented inclusive scan over the lanes, field by field so
-// that no second accumulator is held: a += value of lane (lane - o) if take.
-__device__ __forceinline__ void acc_scan_step(Acc &a, int o, bool take, uint32_t maxmask) {
-#define OPA_SCAN_U64(f)                                                  \
-  {                                                                      \
-    const unsigned long long y = __shfl_up(a.f, (unsigned)o, OPA_WAVE); \
-    if (take) a.f += y;                                                  \
+// Lane shift of a 64-bit value by a DPP move of each half (register to
+// register, no LDS round trip); lanes without a source get 0.
+template <int CTRL, int ROWMASK, int BANKMASK>
+__device__ __forceinline__ unsigned long long dpp64(unsigned long long v) {
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  const uint32_t l2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)lo, CTRL, ROWMASK, BANKMASK, false);
+  const uint32_t h2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)hi, CTRL, ROWMASK, BANKMASK, false);
+  return ((unsigned long long)h2 << 32) | l2;
+}
+
+// One step of the segmented scan, field by field so that no second
+// accumulator is held: a += the shifted value if take.
+template <int CTRL, int ROWMASK, int BANKMASK>
+__device__ __forceinline__ void acc_scan_dpp(Acc &a, bool take, uint32_t maxmask) {
+  {
+    const unsigned long long y = dpp64<CTRL, ROWMASK, BANKMASK>(a.kc);
+    if (take) a.kc += y;
   }
-  OPA_SCAN_U64(kc)
-  OPA_SCAN_U64(tns)
-  OPA_SCAN_U64(mc)
-  OPA_SCAN_U64(mns)
-#undef OPA_SCAN_U64
+  {
+    const unsigned long long y = dpp64<CTRL, ROWMASK, BANKMASK>(a.tns);
+    if (take) a.tns += y;
+  }
+  {
+    const unsigned long long y = dpp64<CTRL, ROWMASK, BANKMASK>(a.mc);
+    if (take) a.mc += y;
+  }
+  {
+    const unsigned long long y = dpp64<CTRL, ROWMASK, BANKMASK>(a.mns);
+    if (take) a.mns += y;
+  }
 #pragma unroll
   for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-    const unsigned long long y = __shfl_up(a.v[c], (unsigned)o, OPA_WAVE);
+    const unsigned long long y = dpp64<CTRL, ROWMASK, BANKMASK>(a.v[c]);
     if (take) {
       if ((maxmask >> c) & 1u) a.v[c] = y > a.v[c] ? y : a.v[c];
       else a.v[c] = d2bits(bits2d(a.v[c]) + bits2d(y));
     }
   }
-  const uint32_t yn = __shfl_up(a.nan, (unsigned)o, OPA_WAVE);
+  const uint32_t yn = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)a.nan, CTRL, ROWMASK, BANKMASK, false);
   if (take) a.nan |= yn;
+}
+
+// Segmented inclusive scan over the wave (segment of lane l starts at lane
+// sl): shifts by 1, 2, 4, 8 inside rows of 16 lanes, then the row totals
+// broadcast from lane 15 to rows 1 and 3 and from lane 31 to rows 2 and 3.
+__device__ __forceinline__ void acc_seg_scan(Acc &a, int sl, uint32_t maxmask) {
+  const int ln = lane_id(), p = ln & 15, row = ln >> 4;
+  acc_scan_dpp<0x111, 0xF, 0xF>(a, p >= 1 && ln - 1 >= sl, maxmask);
+  acc_scan_dpp<0x112, 0xF, 0xF>(a, p >= 2 && ln - 2 >= sl, maxmask);
+  acc_scan_dpp<0x114, 0xF, 0xF>(a, p >= 4 && ln - 4 >= sl, maxmask);
+  acc_scan_dpp<0x118, 0xF, 0xF>(a, p >= 8 && ln - 8 >= sl, maxmask);
+  acc_scan_dpp<0x142, 0xA, 0xF>(a, (row == 1 || row == 3) && sl <= row * 16 - 1, maxmask);
+  acc_scan_dpp<0x143, 0xC, 0xF>(a, row >= 2 && sl <= 31, maxmask);
 }
 
 // Butterfly reduction over the wave; every lane ends with the total. Each

@@ -517,8 +517,7 @@ k_agg_rows(EncParams a) {
     const unsigned long long hl = __ballot(hm != 0) | 1ull;
     const unsigned long long upto = ln == 63 ? ~0ull : ((2ull << ln) - 1);
     const int sl = 63 - __clzll(hl & upto);
-#pragma unroll
-    for (int o = 1; o < OPA_WAVE; o <<= 1) acc_scan_step(inc, o, ln - o >= sl, mx);
+    acc_seg_scan(inc, sl, mx);
     // the lane's last run: ends here, or continues into the next lane and
     // (if it ends inside that lane) completes the row that lane left
     const uint32_t nvn = __shfl_down((uint32_t)nv, 1, OPA_WAVE);
