@@ -161,24 +161,25 @@ __device__ __forceinline__ void acc_seg_scan(Acc &a, int sl, uint32_t maxmask) {
   acc_scan_dpp<0x143, 0xC, 0xF>(a, row >= 2 && sl <= 31, maxmask);
 }
 
-// Butterfly reduction over the wave; every lane ends with the total. Each
-// step adds two partials (addition is commutative), so the result does not
-// depend on scheduling.
+// Reduction over the wave; every lane ends with the total: an inclusive
+// scan in a fixed lane order (DPP moves, as above), then lane 63's value is
+// read into every lane. The order of the additions does not depend on
+// scheduling.
+__device__ __forceinline__ unsigned long long lane63(unsigned long long v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 63);
+  return ((unsigned long long)hi << 32) | lo;
+}
+
 __device__ __forceinline__ void acc_wave_reduce(Acc &a, uint32_t maxmask) {
+  acc_seg_scan(a, 0, maxmask);
+  a.kc = lane63(a.kc);
+  a.tns = lane63(a.tns);
+  a.mc = lane63(a.mc);
+  a.mns = lane63(a.mns);
 #pragma unroll
-  for (int o = 1; o < OPA_WAVE; o <<= 1) {
-    a.kc += __shfl_xor(a.kc, o, OPA_WAVE);
-    a.tns += __shfl_xor(a.tns, o, OPA_WAVE);
-    a.mc += __shfl_xor(a.mc, o, OPA_WAVE);
-    a.mns += __shfl_xor(a.mns, o, OPA_WAVE);
-#pragma unroll
-    for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-      const unsigned long long y = __shfl_xor(a.v[c], o, OPA_WAVE);
-      if ((maxmask >> c) & 1u) a.v[c] = y > a.v[c] ? y : a.v[c];
-      else a.v[c] = d2bits(bits2d(a.v[c]) + bits2d(y));
-    }
-    a.nan |= __shfl_xor(a.nan, o, OPA_WAVE);
-  }
+  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) a.v[c] = lane63(a.v[c]);
+  a.nan = (uint32_t)__builtin_amdgcn_readlane((int)a.nan, 63);
 }
 
 __device__ __forceinline__ void acc_store(PartRow *p, const Acc &a) {
