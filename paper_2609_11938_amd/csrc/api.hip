@@ -268,7 +268,8 @@ static bool check_ranges(const opattr_ranges *r) {
 // back. NULL when it cannot be created; the caller's stream is used alone.
 struct SideStream {
   hipStream_t s = nullptr, s2 = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr, fork2 = nullptr, join2 = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr, fork2 = nullptr, join2 = nullptr,
+             join3 = nullptr;
 };
 constexpr int kMaxDevices = 64;
 inline thread_local SideStream g_side[kMaxDevices];
@@ -281,10 +282,10 @@ static SideStream *side_stream() {
     SideStream n;
     bool ok = hipStreamCreateWithFlags(&n.s, hipStreamNonBlocking) == hipSuccess &&
               hipStreamCreateWithFlags(&n.s2, hipStreamNonBlocking) == hipSuccess;
-    for (hipEvent_t *e : {&n.fork, &n.join, &n.fork2, &n.join2})
+    for (hipEvent_t *e : {&n.fork, &n.join, &n.fork2, &n.join2, &n.join3})
       ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
     if (!ok) {
-      for (hipEvent_t e : {n.fork, n.join, n.fork2, n.join2})
+      for (hipEvent_t e : {n.fork, n.join, n.fork2, n.join2, n.join3})
         if (e) (void)hipEventDestroy(e);
       for (hipStream_t t : {n.s, n.s2})
         if (t) (void)hipStreamDestroy(t);
@@ -443,7 +444,7 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
   // the ranges, the enclosure and the aggregation plan do not depend on the
   // matching: they run on a side stream of this device, joined back before
-  // the reduction
+  // the run reduction (counts) and the per-row reduction (items)
   SideStream *ss = side_stream();
   const hipStream_t s2 = ss ? ss->s : s;
   if (ss) {
@@ -468,8 +469,12 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   e.diag = diag;
   e.ws = ws;
   e.pl = &pl;
-  run_enclose_plan(e, s2);
+  // the run reduction needs only the counts; the items and their sort
+  // continue on the side stream beside the matching and the run reduction
+  plan_counts(e, true, s2);
   if (ss) note(hipEventRecord(ss->join, s2));
+  plan_emit(e, s2);
+  if (ss) note(hipEventRecord(ss->join3, s2));
   build_seq_view(k, d, ws, pl, diag, validate, s);
   IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, validate};
   if (ss) {
@@ -479,7 +484,9 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   }
   run_match(a, s);
   if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
-  run_reduce(e, s);
+  reduce_runs(e, s);
+  if (ss) note(hipStreamWaitEvent(s, ss->join3, 0));
+  reduce_items(e, s);
   launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s, table, sum, pl.G, d->n_ops);
   return launch_status();
 }

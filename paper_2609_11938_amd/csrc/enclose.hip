@@ -562,9 +562,9 @@ static EncParams enc_params(const EncArgs &x) {
   return a;
 }
 
-// the aggregation plan: per-wave counts (with the enclosure when enclose is
-// set), their scan, the items, and the items sorted by operator row
-static void run_plan(const EncArgs &x, bool enclose, hipStream_t s) {
+// per-wave item and row counts (with the enclosure when enclose is set) and
+// their scan: all the run reduction needs besides the matches
+void plan_counts(const EncArgs &x, bool enclose, hipStream_t s) {
   const Plan &pl = *x.pl;
   const EncParams a = enc_params(x);
   FillJobs clr;
@@ -577,10 +577,14 @@ static void run_plan(const EncArgs &x, bool enclose, hipStream_t s) {
     else k_enclose<2><<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
   }
   probe_end(OPATTR_PROBE_MAIN_PASS, s);
-  if (pl.T > 0) {
-    k_wave_scan<<<1, 1024, 0, s>>>(a.em, pl.nencb);
-    k_emit<<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
-  }
+  if (pl.T > 0) k_wave_scan<<<1, 1024, 0, s>>>(a.em, pl.nencb);
+}
+
+// the items and their sort by operator row
+void plan_emit(const EncArgs &x, hipStream_t s) {
+  const Plan &pl = *x.pl;
+  const EncParams a = enc_params(x);
+  if (pl.T > 0) k_emit<<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
   plan_items(x, s);
 }
 
@@ -592,9 +596,7 @@ void run_enclose(const EncArgs &x, hipStream_t s) {
   probe_end(OPATTR_PROBE_MAIN_PASS, s);
 }
 
-void run_enclose_plan(const EncArgs &x, hipStream_t s) { run_plan(x, true, s); }
-
-void run_reduce(const EncArgs &x, hipStream_t s) {
+void reduce_runs(const EncArgs &x, hipStream_t s) {
   const Plan &pl = *x.pl;
   EncParams a = enc_params(x);
   a.ag = agg_inputs(x);
@@ -607,12 +609,13 @@ void run_reduce(const EncArgs &x, hipStream_t s) {
       k_agg_rows<false><<<nb, kEncThreads, 0, s>>>(a);
   }
   probe_end(OPATTR_PROBE_AGG_RUNS, s);
-  reduce_items(x, s);
 }
 
 void run_aggregate_all(const EncArgs &x, hipStream_t s) {
-  run_plan(x, false, s);
-  run_reduce(x, s);
+  plan_counts(x, false, s);
+  plan_emit(x, s);
+  reduce_runs(x, s);
+  reduce_items(x, s);
 }
 
 }  // namespace opa

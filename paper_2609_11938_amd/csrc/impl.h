@@ -189,12 +189,15 @@ struct EncArgs {
 AggIn agg_inputs(const EncArgs &x);
 // range_id of every launch (Alg. 2)
 void run_enclose(const EncArgs &a, hipStream_t s);
-// range_id of every launch and the aggregation plan: items and their sort
-// by operator row (no matches needed)
-void run_enclose_plan(const EncArgs &a, hipStream_t s);
-// operator table from a planned aggregation and match: run reduction, rows
-void run_reduce(const EncArgs &a, hipStream_t s);
-// operator table from range_id and match: plan, then reduce
+// The aggregation in four parts. Plan (no matches needed): per-wave item and
+// row counts and their scan (with the enclosure when enclose is set), then
+// the items and their sort by operator row. Reduction: the runs in place
+// (needs the counts and the matches), then the per-row reduction of the
+// sorted items (needs the runs and the sort).
+void plan_counts(const EncArgs &a, bool enclose, hipStream_t s);
+void plan_emit(const EncArgs &a, hipStream_t s);
+void reduce_runs(const EncArgs &a, hipStream_t s);
+// operator table from range_id and match: all four parts on one stream
 void run_aggregate_all(const EncArgs &a, hipStream_t s);
 // item sort by row (agg.hip), and the per-row reduction of the sorted items
 void plan_items(const EncArgs &a, hipStream_t s);
