@@ -847,14 +847,66 @@ __global__ void __launch_bounds__(256) k_colbase(uint32_t *tab, int64_t rows, ui
   }
 }
 
+// With few chunks, each block sums the chunk totals before its own (at most
+// kFewChunks - 1 per column) instead of a separate scan over the chunks;
+// the blocks of the last chunk write the column totals.
+constexpr int64_t kFewChunks = 64;
+
+__global__ void __launch_bounds__(256) k_colbase_few(uint32_t *tab, int64_t rows, uint32_t cols,
+                                                     const uint32_t *__restrict__ chs,
+                                                     uint32_t *totals, const int64_t *rows_dev) {
+  __shared__ uint32_t part[4][64];
+  rows = rows_of(rows, rows_dev);
+  if ((int64_t)blockIdx.y * kColChunk >= rows) return;
+  const int l = lane_id(), w = wave_id();
+  const uint32_t col = blockIdx.x * 64 + l;
+  const int64_t r0 = (int64_t)blockIdx.y * kColChunk + w * (kColChunk / 4);
+  uint32_t v[kColChunk / 4];
+  uint32_t s = 0;
+#pragma unroll
+  for (int i = 0; i < kColChunk / 4; ++i) {
+    const int64_t r = r0 + i;
+    v[i] = (col < cols && r < rows) ? tab[r * cols + col] : 0u;
+    s += v[i];
+  }
+  part[w][l] = s;
+  uint32_t base = 0;
+  if (col < cols) {
+    const int64_t nb = blockIdx.y;  // chunks before this one
+    for (int64_t c0 = 0; c0 < nb; c0 += 8) {
+      uint32_t t[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) t[j] = c0 + j < nb ? chs[(c0 + j) * cols + col] : 0u;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) base += t[j];
+    }
+  }
+  __syncthreads();
+  if (col >= cols) return;
+  uint32_t run = base;
+  for (int ww = 0; ww < w; ++ww) run += part[ww][l];
+#pragma unroll
+  for (int i = 0; i < kColChunk / 4; ++i) {
+    const int64_t r = r0 + i;
+    if (r < rows) tab[r * cols + col] = run;
+    run += v[i];
+  }
+  const int64_t nc = (rows + kColChunk - 1) / kColChunk;
+  if (w == 3 && (int64_t)blockIdx.y == nc - 1) totals[col] = run;
+}
+
 void column_scan(uint32_t *tab, int64_t rows, uint32_t cols, uint32_t *chs, uint32_t *totals,
                  hipStream_t s, const int64_t *rows_dev) {
   if (rows <= 0 || cols == 0) return;
   const int64_t nch = (rows + kColChunk - 1) / kColChunk;
   dim3 g((cols + 63) / 64, (unsigned)nch);
   k_colsum<<<g, 256, 0, s>>>(tab, rows, cols, chs, rows_dev);
-  k_chunkscan<<<(cols + 255) / 256, 256, 0, s>>>(chs, nch, cols, totals, rows, rows_dev);
-  k_colbase<<<g, 256, 0, s>>>(tab, rows, cols, chs, rows_dev);
+  if (nch <= kFewChunks) {
+    k_colbase_few<<<g, 256, 0, s>>>(tab, rows, cols, chs, totals, rows_dev);
+  } else {
+    k_chunkscan<<<(cols + 255) / 256, 256, 0, s>>>(chs, nch, cols, totals, rows, rows_dev);
+    k_colbase<<<g, 256, 0, s>>>(tab, rows, cols, chs, rows_dev);
+  }
 }
 
 // off[n] = rows of names before n (one block)
