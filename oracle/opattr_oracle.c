@@ -272,14 +272,22 @@ int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
 /* Stage 3: enclosure (Alg. 2, Sec. 3.5)                                    */
 /* ----------------------------------------------------------------------- */
 
-/* a range takes part only with in-range ids, start <= end and end < 2^63 */
+/* a range takes part only with in-range ids and kind, start <= end and
+   end < 2^63 */
 static int range_ok(const oref_ranges *r, const oref_dims *d, int64_t x) {
   return r->stream_id[x] < d->n_streams && r->op_id[x] < d->n_ops &&
-         r->start_ns[x] <= r->end_ns[x] && r->end_ns[x] < (UINT64_C(1) << 63);
+         r->start_ns[x] <= r->end_ns[x] && r->end_ns[x] < (UINT64_C(1) << 63) &&
+         (!r->kind || r->kind[x] <= OREF_KIND_SKIP);
 }
 
 int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,
                  int32_t *range_id, uint8_t *range_depth, oref_diag *diag) {
+  return oref_enclose_walk(k, r, d, range_id, NULL, NULL, NULL, range_depth, diag);
+}
+
+int oref_enclose_walk(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,
+                      int32_t *range_id, uint8_t *fused, int32_t *range_any,
+                      int32_t *range_parent, uint8_t *range_depth, oref_diag *diag) {
   if (!k || !r || !d || !range_id || !diag || k->n < 0 || r->n < 0) return OREF_ERR_ARG;
   if (k->n > 0 && (!k->stream_id || !(k->query_ns || k->start_ns))) return OREF_ERR_ARG;
   const int64_t T = k->n, R = r->n;
@@ -293,6 +301,8 @@ int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d
   if (diag->bad_records) diag->flags |= OREF_F_DATA;
   if (range_depth)
     for (int64_t x = 0; x < R; ++x) range_depth[x] = 0;
+  if (range_parent)
+    for (int64_t x = 0; x < R; ++x) range_parent[x] = -1;
 
   /* ranges in nesting order per stream: (stream, start asc, end desc, index
      asc); an identical interval with a lower index is the outer one */
@@ -312,6 +322,8 @@ int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d
   int64_t nk = 0;
   for (int64_t i = 0; i < T; ++i) {
     range_id[i] = -1;
+    if (fused) fused[i] = 0;
+    if (range_any) range_any[i] = -1;
     if (k->stream_id[i] >= NS) continue;
     ks[nk].a = k->stream_id[i];
     ks[nk].b = q[i];
@@ -338,6 +350,7 @@ int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d
       int64_t id = rs[x].idx;
       while (top > 0 && r->end_ns[stack[top - 1]] < r->end_ns[id]) top--;
       depth[id] = top > 0 ? depth[stack[top - 1]] + 1 : 1;
+      if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[top - 1] : -1;
       if (depth[id] > 255) diag->flags |= OREF_F_LIMIT;
       if (range_depth) range_depth[id] = (uint8_t)(depth[id] > 255 ? 255 : depth[id]);
       stack[top++] = id;
@@ -359,14 +372,31 @@ int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d
     /* sweep: for each kernel in query order, push every range that has
        started (s <= T), drop finished ones from the top (e < T); the top is
        the last range in nesting order with s <= T <= e, i.e. the innermost
-       enclosing range */
+       enclosing range, and (properly nested) the stack below it holds the
+       other enclosing ranges, outward. The walk of Alg. 2 goes down the
+       stack: ops are collected, skipped kinds passed over, a boundary ends
+       it. */
     top = 0;
     int64_t x = a;
     for (int64_t y = b; y < b_end; ++y) {
       uint64_t t = ks[y].b;
       while (x < a_end && rs[x].b <= t) stack[top++] = rs[x++].idx;
       while (top > 0 && r->end_ns[stack[top - 1]] < t) top--;
-      range_id[ks[y].idx] = top > 0 ? (int32_t)stack[top - 1] : -1;
+      const int64_t i = ks[y].idx;
+      if (range_any) range_any[i] = top > 0 ? (int32_t)stack[top - 1] : -1;
+      int32_t first = -1;
+      int nops = 0;
+      for (int64_t u = top - 1; u >= 0; --u) {
+        const int64_t id = stack[u];
+        if (r->end_ns[id] < t) continue; /* only under broken nesting */
+        const uint8_t kd = r->kind ? r->kind[id] : OREF_KIND_OP;
+        if (kd == OREF_KIND_BOUNDARY) break;
+        if (kd == OREF_KIND_SKIP) continue;
+        if (first < 0) first = (int32_t)id;
+        nops++;
+      }
+      range_id[i] = first;
+      if (fused) fused[i] = nops > 1 ? 1 : 0;
     }
     a = a_end;
     b = b_end;

@@ -47,7 +47,15 @@ typedef struct {
   const uint64_t *start_ns, *end_ns;
   const uint16_t *stream_id;
   const uint32_t *op_id;
+  const uint8_t *kind; /* OREF_KIND_*; NULL = every range is an attributed op */
 } oref_ranges;
+
+/* Range kinds of the enclosure walk (Alg. 2): an attributed operator (an
+   aten::, quantized:: or custom op range), a structural boundary (a range
+   whose text has no namespace, e.g. a profiler step: the walk stops there),
+   or a namespaced range that launches no kernel of its own (prims::,
+   torch::: skipped). Other values make the range a bad record. */
+enum { OREF_KIND_OP = 0, OREF_KIND_BOUNDARY = 1, OREF_KIND_SKIP = 2 };
 
 typedef struct {
   uint32_t n_names, n_streams, n_ops, n_parts;
@@ -105,6 +113,18 @@ int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
                oref_diag *diag);
 int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,
                  int32_t *range_id, uint8_t *range_depth, oref_diag *diag);
+/* The full walk of Alg. 2. For each kernel, the ranges of its stream that
+   contain its query point, innermost first, are walked outward: attributed
+   ops are collected, skipped kinds passed over, and the walk stops at the
+   first structural boundary. range_id = the first op collected (-1 none);
+   fused = 1 when more than one op was collected; range_any = the innermost
+   enclosing range of any kind (-1 none), from which range_parent (per range:
+   the innermost range that contains it, -1 for a root or a bad range)
+   leads through all enclosing ranges. Optional outputs may be NULL. Defined
+   for properly nested ranges (NOT_NESTED is flagged otherwise). */
+int oref_enclose_walk(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,
+                      int32_t *range_id, uint8_t *fused, int32_t *range_any,
+                      int32_t *range_parent, uint8_t *range_depth, oref_diag *diag);
 int oref_aggregate(const oref_kernels *k, const oref_profiled *p,
                    const int32_t *match, const int32_t *range_id,
                    const oref_ranges *r, const oref_dims *d, const uint8_t *agg_kind,

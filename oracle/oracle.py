@@ -62,7 +62,11 @@ class Profiled(C.Structure):
 
 class Ranges(C.Structure):
     _fields_ = [("n", C.c_int64), ("start_ns", C.c_void_p), ("end_ns", C.c_void_p),
-                ("stream_id", C.c_void_p), ("op_id", C.c_void_p)]
+                ("stream_id", C.c_void_p), ("op_id", C.c_void_p), ("kind", C.c_void_p)]
+
+
+# range kinds of the enclosure walk (Alg. 2)
+KIND_OP, KIND_BOUNDARY, KIND_SKIP = 0, 1, 2
 
 
 class Dims(C.Structure):
@@ -103,8 +107,10 @@ def load(path: str):
     L.oref_aggregate.argtypes = [P(Kernels), P(Profiled), C.c_void_p, C.c_void_p,
                                  P(Ranges), P(Dims), C.c_void_p, C.c_void_p,
                                  P(Summary), P(Diag)]
+    L.oref_enclose_walk.argtypes = [P(Kernels), P(Ranges), P(Dims), C.c_void_p, C.c_void_p,
+                                    C.c_void_p, C.c_void_p, C.c_void_p, P(Diag)]
     L.oref_diag_finish.argtypes = [P(Diag), C.c_int]
-    for f in ("oref_match", "oref_dedup", "oref_enclose", "oref_aggregate"):
+    for f in ("oref_match", "oref_dedup", "oref_enclose", "oref_enclose_walk", "oref_aggregate"):
         getattr(L, f).restype = C.c_int
     return L
 
@@ -147,6 +153,7 @@ class _Inputs:
         self.r_end = _c(tr["r_end"], np.uint64)
         self.r_stream = _c(tr["r_stream"], np.uint16)
         self.r_op = _c(tr["r_op"], np.uint32)
+        self.r_kind = _c(tr.get("r_kind"), np.uint8)
         self.part_rep = _c(tr.get("part_rep"), np.int32)
         T = self.seq.size
         self.k = Kernels(T, _ptr(self.seq), _ptr(self.start), _ptr(self.dur),
@@ -158,7 +165,7 @@ class _Inputs:
         self.p = Profiled(P, _ptr(self.pf_name), cnt.ctypes.data if P > 0 else None,
                           rs, cs, absent_mask)
         self.r = Ranges(self.r_start.size, _ptr(self.r_start), _ptr(self.r_end),
-                        _ptr(self.r_stream), _ptr(self.r_op))
+                        _ptr(self.r_stream), _ptr(self.r_op), _ptr(self.r_kind))
         self.d = Dims(tr["n_names"], tr["n_streams"], tr["n_ops"],
                       tr.get("n_parts", 0) or 0, _ptr(self.part_rep))
 
@@ -220,3 +227,27 @@ def attribute(tr, policy=PREFIX, agg_kind=None, absent_mask=0, stages=None, libr
     L.oref_diag_finish(C.byref(dg), policy)
     out["diag"] = diag_dict(dg)
     return out
+
+
+def enclose_walk(tr, library=None):
+    """The full enclosure walk of Alg. 2 (range kinds from ``tr["r_kind"]``,
+    absent = every range an attributed op): per kernel ``range_id`` (innermost
+    attributed op before a structural boundary), ``fused`` and ``range_any``
+    (innermost enclosing range of any kind); per range ``range_parent`` and
+    ``range_depth``."""
+    L = library if library is not None else lib()
+    x = _Inputs(tr)
+    T, R = x.seq.size, x.r_start.size
+    dg = Diag()
+    rid = np.empty(T, dtype=np.int32)
+    fused = np.empty(T, dtype=np.uint8)
+    rany = np.empty(T, dtype=np.int32)
+    par = np.empty(R, dtype=np.int32)
+    depth = np.empty(R, dtype=np.uint8)
+    rc = L.oref_enclose_walk(C.byref(x.k), C.byref(x.r), C.byref(x.d), _ptr(rid), _ptr(fused),
+                             _ptr(rany), _ptr(par), _ptr(depth), C.byref(dg))
+    if rc:
+        raise ValueError(f"oref_enclose_walk: {rc}")
+    L.oref_diag_finish(C.byref(dg), PREFIX)
+    return {"range_id": rid, "fused": fused, "range_any": rany, "range_parent": par,
+            "range_depth": depth, "diag": diag_dict(dg)}

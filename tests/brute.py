@@ -100,6 +100,62 @@ def enclose(tr):
     return out
 
 
+def _range_valid(tr, r):
+    kind = tr.get("r_kind")
+    return (int(tr["r_stream"][r]) < tr["n_streams"] and int(tr["r_op"][r]) < tr["n_ops"]
+            and int(tr["r_start"][r]) <= int(tr["r_end"][r]) < 2 ** 63
+            and (kind is None or int(kind[r]) <= 2))
+
+
+def enclose_walk(tr):
+    """Alg. 2 written out per kernel: the valid ranges of its stream that
+    contain its query point, outermost first in nesting order, are walked
+    from the innermost outward; kind 0 (op) ranges are collected, kind 2 is
+    passed over, kind 1 ends the walk. Returns range_id (first op collected),
+    fused (more than one collected), range_any (innermost of any kind) and,
+    per range, range_parent (innermost valid range of the same stream that
+    contains it and precedes it in nesting order)."""
+    T, R = tr["seq"].size, tr["r_start"].size
+    q = tr.get("query_ns")
+    q = tr["start_ns"] if q is None else q
+    kind = tr.get("r_kind")
+    rs, re, rst = tr["r_start"], tr["r_end"], tr["r_stream"]
+    rid = np.full(T, -1, dtype=np.int64)
+    fused = np.zeros(T, dtype=np.int64)
+    rany = np.full(T, -1, dtype=np.int64)
+    for i in range(T):
+        enc = [r for r in range(R) if _range_valid(tr, r) and rst[r] == tr["stream_id"][i]
+               and int(rs[r]) <= int(q[i]) <= int(re[r])]
+        enc.sort(key=lambda r: (int(rs[r]), -int(re[r]), r))  # outermost first
+        if enc:
+            rany[i] = enc[-1]
+        ops = []
+        for r in reversed(enc):
+            k = 0 if kind is None else int(kind[r])
+            if k == 0:
+                ops.append(r)
+            elif k == 1:
+                break
+        if ops:
+            rid[i] = ops[0]
+            fused[i] = 1 if len(ops) > 1 else 0
+    par = np.full(R, -1, dtype=np.int64)
+    for x in range(R):
+        if not _range_valid(tr, x):
+            continue
+        best = None
+        for y in range(R):
+            if (y != x and _range_valid(tr, y) and rst[y] == rst[x]
+                    and int(rs[y]) <= int(rs[x]) and int(re[x]) <= int(re[y])
+                    and nesting_before(tr, y, x)):
+                key = (int(rs[y]), -int(re[y]), y)
+                if best is None or key > best:
+                    best = key
+        if best is not None:
+            par[x] = best[2]
+    return rid, fused, rany, par
+
+
 def nesting_before(tr, a, b):
     """True if range a precedes range b in nesting order (start asc, end desc,
     index asc)."""

@@ -318,6 +318,82 @@ def test_enclose_crossing_ranges_flagged():
     np.testing.assert_array_equal(out["range_id"], brute.enclose(tr))
 
 
+def _with_kinds(tr, seed, p_boundary=0.2, p_skip=0.25, p_bad=0.0):
+    rng = np.random.default_rng(seed)
+    R = tr["r_start"].size
+    u = rng.random(R)
+    kind = np.where(u < p_boundary, 1, np.where(u < p_boundary + p_skip, 2, 0)).astype(np.uint8)
+    if p_bad:
+        kind[rng.random(R) < p_bad] = 3
+    tr = dict(tr)
+    tr["r_kind"] = kind
+    return tr
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_enclose_walk_matches_brute_force(seed):
+    """Alg. 2's walk with range kinds (op / structural boundary / skipped
+    namespace) against its definition written out per kernel."""
+    tr = cases.random_trace(700 + seed, T=70, R=30, S=1 + seed % 3, t_max=40, max_depth=5)
+    tr = _with_kinds(tr, seed, p_bad=0.05 if seed % 4 == 3 else 0.0)
+    out = O.enclose_walk(tr)
+    rid, fused, rany, par = brute.enclose_walk(tr)
+    np.testing.assert_array_equal(out["range_id"], rid)
+    np.testing.assert_array_equal(out["fused"], fused)
+    np.testing.assert_array_equal(out["range_any"], rany)
+    np.testing.assert_array_equal(out["range_parent"], par)
+    assert out["diag"]["nesting_errors"] == 0
+
+
+def test_enclose_walk_all_ops_is_innermost():
+    """Without kinds every range is an op: the walk returns the innermost
+    enclosing range, and a kernel is fused exactly when that range has a
+    parent (a second op encloses it)."""
+    tr = tg.generate("tiny")
+    out = O.enclose_walk(tr)
+    np.testing.assert_array_equal(out["range_id"], tr["planted_range"])
+    np.testing.assert_array_equal(out["range_any"], out["range_id"])
+    has = out["range_any"] >= 0
+    want = np.zeros_like(out["fused"])
+    want[has] = out["range_parent"][out["range_any"][has]] >= 0
+    np.testing.assert_array_equal(out["fused"], want)
+    # parents are one level up
+    d = out["range_depth"].astype(np.int64)
+    ok = out["range_parent"] >= 0
+    np.testing.assert_array_equal(d[ok], d[out["range_parent"][ok]] + 1)
+    assert (d[~ok] <= 1).all()
+
+
+def test_enclose_walk_hand_shaped():
+    """A profiler step (structural boundary) encloses aten::linear (op), which
+    encloses prims::view (skipped) enclosing aten::addmm (op); a second step
+    holds aten::relu directly. Kernels: inside addmm (op addmm, fused: linear
+    is also collected), inside view only (op linear, not fused), inside linear
+    only, inside the step only (no op: the walk stops at the boundary), inside
+    relu, and outside everything."""
+    #          0=step1   1=linear  2=view    3=addmm   4=step2   5=relu
+    rs = np.array([0, 10, 20, 30, 100, 110], np.uint64)
+    re = np.array([90, 80, 70, 40, 190, 120], np.uint64)
+    kind = np.array([1, 0, 2, 0, 1, 0], np.uint8)
+    q = np.array([35, 50, 75, 5, 115, 95], np.uint64)
+    T = q.size
+    tr = dict(seq=np.arange(T, dtype=np.uint32), start_ns=q, dur_ns=np.ones(T, np.uint32),
+              stream_id=np.zeros(T, np.uint16), name_id=np.zeros(T, np.uint32), part_id=None,
+              pf_name=np.zeros(0, np.uint32), counters=np.zeros((0, 20), np.float32),
+              r_start=rs, r_end=re, r_stream=np.zeros(6, np.uint16),
+              r_op=np.arange(6, dtype=np.uint32), r_kind=kind, part_rep=None,
+              n_names=1, n_streams=1, n_ops=6)
+    out = O.enclose_walk(tr)
+    np.testing.assert_array_equal(out["range_id"], [3, 1, 1, -1, 5, -1])
+    np.testing.assert_array_equal(out["fused"], [1, 0, 0, 0, 0, 0])
+    np.testing.assert_array_equal(out["range_any"], [3, 2, 1, 0, 5, -1])
+    np.testing.assert_array_equal(out["range_parent"], [-1, 0, 1, 2, -1, 4])
+    # the aggregation follows the walk: the step's own kernel is unattributed
+    agg = O.attribute(tr, stages=["match", "enclose", "aggregate"])
+    np.testing.assert_array_equal(agg["range_id"], out["range_id"])
+    assert agg["table"]["kernel_count"][6] == 2
+
+
 @pytest.mark.parametrize("cfg", ["tiny", "gpt2", "sdpa", "lstm"])
 def test_enclose_planted_labels(cfg):
     tr = tg.generate(cfg)

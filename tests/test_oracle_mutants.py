@@ -43,6 +43,15 @@ MUTANTS = {
     "unmatched_in_dw_denominator": ("if (m < 0) continue; /* unmatched kernels carry no counters */",
                                     "if (m < 0) { row->matched_ns += dur; continue; }"),
     "unattributed_dropped": ("row->kernel_count++;", "if (g < d->n_ops) row->kernel_count++;"),
+    "walk_skip_ends_walk": ("if (kd == OREF_KIND_SKIP) continue;",
+                            "if (kd == OREF_KIND_SKIP) break;"),
+    "walk_boundary_passed": ("if (kd == OREF_KIND_BOUNDARY) break;",
+                             "if (kd == OREF_KIND_BOUNDARY) continue;"),
+    "walk_outermost_op_kept": ("if (first < 0) first = (int32_t)id;", "first = (int32_t)id;"),
+    "fused_counts_every_range": ("if (fused) fused[i] = nops > 1 ? 1 : 0;",
+                                 "if (fused) fused[i] = top > 1 ? 1 : 0;"),
+    "parent_is_root": ("if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[top - 1] : -1;",
+                       "if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[0] : -1;"),
 }
 
 
@@ -109,6 +118,17 @@ def battery(L) -> bool:
             return False
         if out["diag"]["nesting_errors"] != len(brute.crossing_streams(tr)):
             return False
+    for seed in range(6):
+        tr = cases.random_trace(700 + seed, T=60, R=30, S=2, t_max=40, max_depth=5)
+        rng = np.random.default_rng(seed)
+        u = rng.random(tr["r_start"].size)
+        tr["r_kind"] = np.where(u < 0.2, 1, np.where(u < 0.45, 2, 0)).astype(np.uint8)
+        out = O.enclose_walk(tr, library=L)
+        rid, fused, rany, par = brute.enclose_walk(tr)
+        for got, want in ((out["range_id"], rid), (out["fused"], fused),
+                          (out["range_any"], rany), (out["range_parent"], par)):
+            if not np.array_equal(got, want):
+                return False
     tr = _edge_trace()
     out = O.attribute(tr, library=L)
     if not np.array_equal(out["range_id"], brute.enclose(tr)):
