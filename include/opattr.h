@@ -87,7 +87,15 @@ typedef struct {
   const uint64_t *start_ns, *end_ns;
   const uint16_t *stream_id;
   const uint32_t *op_id; /* < n_ops: the aggregation key (row of the table)         */
+  const uint8_t *kind;   /* OPATTR_KIND_* of each range; NULL = every range an op   */
 } opattr_ranges;
+
+/* Range kinds of the enclosure walk (Alg. 2): an attributed operator range
+   (aten::, quantized:: or a custom op), a structural boundary (a range whose
+   text has no namespace, e.g. a profiler step; the walk stops there), or a
+   namespaced range that launches no kernel of its own (prims::, torch::;
+   passed over). A kind above 2 makes the range a bad record. */
+enum { OPATTR_KIND_OP = 0, OPATTR_KIND_BOUNDARY = 1, OPATTR_KIND_SKIP = 2 };
 
 /* Layout hints: each is a PROMISE about the inputs that lets the library skip a
    reordering pass. A false promise gives unspecified outputs (never an
@@ -203,14 +211,32 @@ int opattr_match(const opattr_kernels *k, const opattr_profiled *p, const opattr
 int opattr_dedup_broadcast(const opattr_kernels *k, const opattr_dims *d, int32_t *match,
                            opattr_diag *diag, void *ws, size_t ws_bytes, void *stream);
 
-/* Enclosure (Alg. 2): range_id[i] = the range r on stream_id[i] with
-   start_r <= q_i <= end_r that is last in nesting order (start asc, end desc,
-   index asc) -- the innermost one -- or -1. q_i = query_ns[i] (or start_ns[i]).
-   range_depth[r] (or NULL) = 1 + depth of the nearest earlier range of the
-   stream in nesting order whose end is not before end_r (0 for a bad range). */
+/* Enclosure (Alg. 2). The ranges on stream_id[i] with start_r <= q_i <= end_r
+   (q_i = query_ns[i], or start_ns[i]) are walked from the innermost (the one
+   last in nesting order: start asc, end desc, index asc) outward: op ranges
+   are collected, SKIP ranges passed over, and a BOUNDARY range ends the walk.
+   range_id[i] = the first op collected, or -1 (without kinds: the innermost
+   enclosing range). range_depth[r] (or NULL) = 1 + depth of the nearest
+   earlier range of the stream in nesting order whose end is not before end_r
+   (0 for a bad range). */
 int opattr_enclose(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,
                    int32_t *range_id, uint8_t *range_depth, opattr_diag *diag, void *ws,
                    size_t ws_bytes, void *stream);
+
+/* The enclosure walk of Alg. 2 with all of its outputs, as opattr_enclose plus:
+   fused[i] = 1 when the walk collected more than one op range (a kernel
+   spanning several attributed operators), else 0; range_any[i] = the
+   innermost enclosing range of any kind, or -1; range_parent[r] = the
+   innermost range that contains range r (the nearest earlier range of its
+   stream in nesting order whose end is not before end_r), or -1 for a root
+   or a bad range. range_any and range_parent together give every range
+   enclosing a kernel, innermost first. fused, range_any, range_parent and
+   range_depth may be NULL. Defined for properly nested ranges (crossing
+   ranges are reported as NOT_NESTED). */
+int opattr_enclose_walk(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,
+                        int32_t *range_id, uint8_t *fused, int32_t *range_any,
+                        int32_t *range_parent, uint8_t *range_depth, opattr_diag *diag,
+                        void *ws, size_t ws_bytes, void *stream);
 
 /* Aggregation (Eq. 1). Row g = op_id[range_id[i]] (or n_ops when range_id is
    -1) collects kernel_count and total_ns of every launch, and over launches

@@ -51,7 +51,10 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   const bool dd = has_dedup(k, d);
   const size_t T = (size_t)pl.T, P = (size_t)pl.P, R = (size_t)pl.R, NN = pl.NN;
   Bump b;
-  pl.sv = b.take(pl.seg ? 0 : T * 4);
+  // the launch-order view: unused on the segment path, but the standalone
+  // dedup (no profiled rows, so never the segment path) needs it, and the
+  // size for all inputs must cover every entry point
+  pl.sv = b.take(T * 4);
   pl.kblk = b.take(pl.seg ? ((size_t)pl.NS + 2) * 8 : 0);
   pl.tbnd = b.take(pl.seg ? ((size_t)pl.nt + 1) * pl.NS * 4 : 0);
   pl.rk = b.take(pl.seq_dense ? 0 : T * 4);
@@ -83,6 +86,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.re_c = b.take(rs ? R * 8 : 0);
   pl.rst_c = b.take(rs ? R * 2 : 0);
   pl.rop_c = b.take(rs ? R * 4 : 0);
+  pl.rkd_c = b.take(rs && r && r->kind ? R : 0);
   pl.rsort_k0 = b.take(rs ? R * 8 : 0);
   pl.rsort_k1 = b.take(rs ? R * 8 : 0);
   pl.rsort_v0 = b.take(rs ? R * 4 : 0);
@@ -365,9 +369,10 @@ int opattr_dedup_broadcast(const opattr_kernels *k, const opattr_dims *d, int32_
   return launch_status();
 }
 
-int opattr_enclose(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,
-                   int32_t *range_id, uint8_t *range_depth, opattr_diag *diag, void *ws,
-                   size_t ws_bytes, void *stream) {
+int opattr_enclose_walk(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,
+                        int32_t *range_id, uint8_t *fused, int32_t *range_any,
+                        int32_t *range_parent, uint8_t *range_depth, opattr_diag *diag,
+                        void *ws, size_t ws_bytes, void *stream) {
   if (!check_dims(d) || !check_kernels(k, false, true, false) || !check_ranges(r) || !diag ||
       (k->n > 0 && !range_id))
     return OPATTR_ERR_INVALID_ARG;
@@ -378,17 +383,27 @@ int opattr_enclose(const opattr_kernels *k, const opattr_ranges *r, const opattr
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
   const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s);
   resolve_ranges(cr, d, ws, pl, range_depth, diag, s);
+  write_range_parents(cr, ws, pl, range_parent, s);
   EncArgs e{};
   e.k = k;
   e.cr = cr;
   e.d = d;
   e.range_id = range_id;
+  e.fused = fused;
+  e.range_any = range_any;
   e.diag = diag;
   e.ws = ws;
   e.pl = &pl;
   run_enclose(e, s);
   launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s);
   return launch_status();
+}
+
+int opattr_enclose(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,
+                   int32_t *range_id, uint8_t *range_depth, opattr_diag *diag, void *ws,
+                   size_t ws_bytes, void *stream) {
+  return opattr_enclose_walk(k, r, d, range_id, nullptr, nullptr, nullptr, range_depth, diag, ws,
+                             ws_bytes, stream);
 }
 
 static bool kinds_ok(const uint8_t *agg_kind) {

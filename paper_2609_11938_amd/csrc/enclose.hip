@@ -46,6 +46,8 @@ struct EncParams {
   int64_t R_in;           // aggregate-only: input ranges
   const uint32_t *op_in;  // aggregate-only: op ids by input range index
   int32_t *range_id;
+  uint8_t *fused;      // optional walk outputs
+  int32_t *range_any;
   AggIn ag;
   EmitOut em;
   opattr_diag *diag;
@@ -248,8 +250,11 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
     uint64_t qprev = 0;
     int64_t pprev = 0, jprev = -1, eprev = 0;  // eprev = ree[jprev] when jprev is a range
     int sprevsteps = 0;
-    int32_t rlast = -1, olast = -1;  // the last range found, its output id and row
+    // the last innermost range found, and what the walk made of it: the op
+    // range (output id and row), the innermost range's output id, fused
+    int32_t rlast = -1, olast = -1, alast = -1;
     uint32_t glast = 0;
+    uint8_t flast = 0;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
       int32_t rid = -1;
@@ -315,11 +320,32 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
       }
       if (rid >= 0 && rid != rlast) {
         rlast = rid;
-        olast = a.cr.perm ? a.cr.perm[rid] : rid;
-        glast = a.cr.op[rid];
+        // Alg. 2's walk outward from the innermost range: ops collected,
+        // skipped kinds passed over, a boundary ends it
+        int32_t first = rid;
+        flast = 0;
+        if (a.cr.kind) {
+          first = -1;
+          int nops = 0, hops = 0;
+          for (int32_t j = rid; j >= 0 && hops < kMaxWalk; j = a.npg[j], ++hops) {
+            const uint8_t kd = a.cr.kind[j];
+            if (kd == OPATTR_KIND_BOUNDARY) break;
+            if (kd != OPATTR_KIND_OP) continue;
+            if (first < 0) first = j;
+            ++nops;
+          }
+          flast = nops > 1 ? 1 : 0;
+        } else if (a.fused) {
+          flast = a.npg[rid] >= 0 ? 1 : 0;  // every enclosing range is an op
+        }
+        olast = first >= 0 ? (a.cr.perm ? a.cr.perm[first] : first) : -1;
+        glast = first >= 0 ? a.cr.op[first] : a.NOPS;
+        alast = a.cr.perm ? a.cr.perm[rid] : rid;
       }
       rout[k] = rid >= 0 ? olast : -1;
       g[k] = k < nv ? (rid >= 0 ? glast : a.NOPS) : 0xFFFFFFFFu;
+      if (k < nv && a.range_any) a.range_any[ib + k] = rid >= 0 ? alast : -1;
+      if (k < nv && a.fused) a.fused[ib + k] = rid >= 0 ? flast : 0;
     }
     store_run(a.range_id, ib, nv, rout);
   } else {
@@ -550,6 +576,8 @@ static EncParams enc_params(const EncArgs &x) {
   a.NS = x.d->n_streams;
   a.NOPS = x.d->n_ops;
   a.range_id = x.range_id;
+  a.fused = x.fused;
+  a.range_any = x.range_any;
   a.diag = x.diag;
   a.cr = x.cr;
   a.rblk = at<int64_t>(x.ws, pl.rblk);

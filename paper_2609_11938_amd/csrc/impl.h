@@ -40,7 +40,7 @@ struct Plan {
   size_t tlh, pfh, tlch, pfch, tlc, pfc, off, slot;
   size_t pfirst, plast, pheads, prec, mbs, nbs;
   // ranges
-  size_t rperm, rs_c, re_c, rst_c, rop_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
+  size_t rperm, rs_c, re_c, rst_c, rop_c, rkd_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
   // aggregation
   int64_t cap_items, cap_rows, max_chunks;
@@ -84,6 +84,7 @@ struct CoreRanges {
   const uint64_t *e;
   const uint16_t *st;
   const uint32_t *op;
+  const uint8_t *kind;  // range kinds of the walk; NULL = every range an op
   const int32_t *perm;  // core position -> input index; NULL = identity
 };
 
@@ -158,6 +159,9 @@ CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws
                           opattr_diag *diag, bool validate, hipStream_t s);
 void resolve_ranges(const CoreRanges &cr, const opattr_dims *d, void *ws, const Plan &pl,
                     uint8_t *range_depth, opattr_diag *diag, hipStream_t s);
+// range_parent[input index] = input index of the range's parent, -1 root / bad
+void write_range_parents(const CoreRanges &cr, void *ws, const Plan &pl, int32_t *range_parent,
+                         hipStream_t s);
 
 struct PartRow;
 struct AggIn;
@@ -172,6 +176,8 @@ struct EmitOut {
 EmitOut emit_out(void *ws, const Plan &pl);
 
 struct EncArgs {
+  uint8_t *fused = nullptr;      // walk outputs (enclosure), optional
+  int32_t *range_any = nullptr;
   const opattr_kernels *k;
   const opattr_profiled *p;  // aggregation
   const int32_t *match;      // aggregation

@@ -26,7 +26,8 @@ __global__ void k_rprep(CoreRanges cr, uint32_t NS, uint32_t NOPS, int64_t *ree,
   bool bad = false;
   if (x < cr.n) {
     const uint64_t s = cr.s[x], e = cr.e[x];
-    const bool ok = cr.st[x] < NS && cr.op[x] < NOPS && s <= e && e < kEndLimit;
+    const bool ok = cr.st[x] < NS && cr.op[x] < NOPS && s <= e && e < kEndLimit &&
+                    (!cr.kind || cr.kind[x] <= OPATTR_KIND_SKIP);
     ree[x] = ok ? (int64_t)e : -1;
     npg[x] = -1;
     bad = !ok;
@@ -314,18 +315,40 @@ static RangeWork range_work(const CoreRanges &cr, const opattr_dims *d, void *ws
   return w;
 }
 
-__global__ void k_gather_small(const uint16_t *st, const uint32_t *op, const uint32_t *perm,
-                               uint16_t *st_o, uint32_t *op_o, int64_t n) {
+__global__ void k_gather_small(const uint16_t *st, const uint32_t *op, const uint8_t *kd,
+                               const uint32_t *perm, uint16_t *st_o, uint32_t *op_o,
+                               uint8_t *kd_o, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) {
     const uint32_t p = perm[i];
     st_o[i] = st[p];
     op_o[i] = op[p];
+    if (kd) kd_o[i] = kd[p];
   }
 }
-void launch_gather_small(const uint16_t *st, const uint32_t *op, const uint32_t *perm,
-                         uint16_t *st_o, uint32_t *op_o, int64_t n, hipStream_t s) {
-  if (n > 0) k_gather_small<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(st, op, perm, st_o, op_o, n);
+void launch_gather_small(const uint16_t *st, const uint32_t *op, const uint8_t *kd,
+                         const uint32_t *perm, uint16_t *st_o, uint32_t *op_o, uint8_t *kd_o,
+                         int64_t n, hipStream_t s) {
+  if (n > 0)
+    k_gather_small<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(st, op, kd, perm, st_o, op_o, kd_o,
+                                                               n);
+}
+
+// range_parent[perm(x)] = perm(parent of x) for valid ranges, else -1
+__global__ void k_range_parent(CoreRanges cr, const int64_t *ree, const int32_t *npg,
+                               int32_t *range_parent) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= cr.n) return;
+  const int32_t par = ree[x] >= 0 ? npg[x] : -1;
+  const int64_t o = cr.perm ? cr.perm[x] : x;
+  range_parent[o] = par >= 0 ? (cr.perm ? cr.perm[par] : par) : -1;
+}
+
+void write_range_parents(const CoreRanges &cr, void *ws, const Plan &pl, int32_t *range_parent,
+                         hipStream_t s) {
+  if (range_parent && cr.n > 0)
+    k_range_parent<<<(unsigned)((cr.n + 255) / 256), 256, 0, s>>>(
+        cr, at<int64_t>(ws, pl.ree), at<int32_t>(ws, pl.npg), range_parent);
 }
 
 CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws, const Plan &pl,
@@ -338,6 +361,7 @@ CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws
     cr.e = r->end_ns;
     cr.st = r->stream_id;
     cr.op = r->op_id;
+    cr.kind = r->kind;
     cr.perm = nullptr;
     if (validate && R > 1) k_rcheck<<<(unsigned)((R + 255) / 256), 256, 0, s>>>(cr, diag);
   } else if (R > 0) {
@@ -359,17 +383,20 @@ CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws
     launch_gather_key_u64(r->start_ns, perm, sc, R, false, s);
     launch_gather_key_u64(r->end_ns, perm, ec, R, false, s);
     note(hipMemcpyAsync(at<uint32_t>(ws, pl.rperm), perm, (size_t)R * 4, hipMemcpyDeviceToDevice, s));
-    launch_gather_small(r->stream_id, r->op_id, at<uint32_t>(ws, pl.rperm),
-                        at<uint16_t>(ws, pl.rst_c), at<uint32_t>(ws, pl.rop_c), R, s);
+    launch_gather_small(r->stream_id, r->op_id, r->kind, at<uint32_t>(ws, pl.rperm),
+                        at<uint16_t>(ws, pl.rst_c), at<uint32_t>(ws, pl.rop_c),
+                        at<uint8_t>(ws, pl.rkd_c), R, s);
     cr.s = sc;
     cr.e = ec;
     cr.st = at<uint16_t>(ws, pl.rst_c);
     cr.op = at<uint32_t>(ws, pl.rop_c);
+    cr.kind = r->kind ? at<uint8_t>(ws, pl.rkd_c) : nullptr;
     cr.perm = reinterpret_cast<const int32_t *>(at<uint32_t>(ws, pl.rperm));
   } else {
     cr.s = cr.e = nullptr;
     cr.st = nullptr;
     cr.op = nullptr;
+    cr.kind = nullptr;
     cr.perm = nullptr;
   }
   const uint32_t NS = d->n_streams;

@@ -40,7 +40,11 @@ class opattr_profiled(C.Structure):
 
 class opattr_ranges(C.Structure):
     _fields_ = [("n", C.c_int64), ("start_ns", C.c_void_p), ("end_ns", C.c_void_p),
-                ("stream_id", C.c_void_p), ("op_id", C.c_void_p)]
+                ("stream_id", C.c_void_p), ("op_id", C.c_void_p), ("kind", C.c_void_p)]
+
+
+# range kinds of the enclosure walk (Alg. 2)
+KIND_OP, KIND_BOUNDARY, KIND_SKIP = 0, 1, 2
 
 
 class opattr_dims(C.Structure):
@@ -66,8 +70,8 @@ assert OP_ROW_DTYPE.itemsize == 192 and SUMMARY_DTYPE.itemsize == 40
 assert C.sizeof(opattr_diag) == 64
 
 EXPORTS = ("opattr_workspace_bytes", "opattr_diag_clear", "opattr_read_diag", "opattr_match",
-           "opattr_dedup_broadcast", "opattr_enclose", "opattr_aggregate", "opattr_attribute",
-           "opattr_set_probe_events", "opattr_strerror")
+           "opattr_dedup_broadcast", "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate",
+           "opattr_attribute", "opattr_set_probe_events", "opattr_strerror")
 PROBES = ("seq_view", "tl_hist", "pf_hist", "col_scan", "pf_slot", "tl_match", "dedup",
           "ranges", "main_pass", "finalize", "aggregate", "agg_runs", "item_sort")
 
@@ -97,12 +101,14 @@ def library(path: str | None = None):
     L.opattr_dedup_broadcast.argtypes = [P(opattr_kernels), P(opattr_dims), vp, vp, vp, sz, vp]
     L.opattr_enclose.argtypes = [P(opattr_kernels), P(opattr_ranges), P(opattr_dims), vp, vp,
                                  vp, vp, sz, vp]
+    L.opattr_enclose_walk.argtypes = [P(opattr_kernels), P(opattr_ranges), P(opattr_dims), vp,
+                                      vp, vp, vp, vp, vp, vp, sz, vp]
     L.opattr_aggregate.argtypes = [P(opattr_kernels), P(opattr_profiled), vp, vp,
                                    P(opattr_ranges), P(opattr_dims), vp, vp, vp, vp, vp, sz, vp]
     L.opattr_attribute.argtypes = [P(opattr_kernels), P(opattr_profiled), P(opattr_ranges),
                                    P(opattr_dims), i, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     for f in ("opattr_diag_clear", "opattr_read_diag", "opattr_match", "opattr_dedup_broadcast",
-              "opattr_enclose", "opattr_aggregate", "opattr_attribute"):
+              "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate", "opattr_attribute"):
         getattr(L, f).restype = C.c_int
     L.opattr_set_probe_events.argtypes = [vp, i]
     L.opattr_set_probe_events.restype = C.c_int
@@ -138,7 +144,7 @@ _KERNEL_FIELDS = {"seq": np.uint32, "start_ns": np.uint64, "dur_ns": np.uint32,
                   "stream_id": np.uint16, "name_id": np.uint32, "part_id": np.int32,
                   "query_ns": np.uint64}
 _RANGE_FIELDS = {"r_start": np.uint64, "r_end": np.uint64, "r_stream": np.uint16,
-                 "r_op": np.uint32}
+                 "r_op": np.uint32, "r_kind": np.uint8}
 
 
 def to_device(tr: dict, device="cuda:0") -> dict:
@@ -180,7 +186,7 @@ class _Marshal:
                                  absent_mask)
         R = int(dt["r_start"].numel())
         self.r = opattr_ranges(R, _p(dt["r_start"]), _p(dt["r_end"]), _p(dt["r_stream"]),
-                               _p(dt["r_op"]))
+                               _p(dt["r_op"]), _p(dt.get("r_kind")))
         rep = dt.get("part_rep")
         self.d = opattr_dims(dt["n_names"], dt["n_streams"], dt["n_ops"],
                              dt.get("n_parts", 0) if rep is not None else 0, _p(rep), flags)
@@ -345,6 +351,31 @@ def opattr_enclose(dt: dict, flags=0, want_depth=True, ws: Workspace | None = No
     _check(L.opattr_enclose(C.byref(m.k), C.byref(m.r), C.byref(m.d), _p(out["range_id"]),
                             _p(out["range_depth"]), _p(out["diag"]), _p(buf),
                             C.c_size_t(buf.numel()), _stream_handle(stream)), "opattr_enclose")
+    return out
+
+
+def opattr_enclose_walk(dt: dict, flags=0, ws: Workspace | None = None, stream=None) -> Outputs:
+    """The full enclosure walk of Alg. 2 (range kinds from ``dt["r_kind"]``):
+    range_id, fused and range_any per launch; range_parent and range_depth
+    per range."""
+    import torch
+
+    L = library()
+    m = _Marshal(dt, flags)
+    dev = dt["counters"].device
+    out = Outputs(range_id=torch.empty(m.T, dtype=torch.int32, device=dev),
+                  fused=torch.empty(m.T, dtype=torch.uint8, device=dev),
+                  range_any=torch.empty(m.T, dtype=torch.int32, device=dev),
+                  range_parent=torch.empty(m.R, dtype=torch.int32, device=dev),
+                  range_depth=torch.empty(m.R, dtype=torch.uint8, device=dev),
+                  diag=_new_diag(dev, stream))
+    ws = ws or Workspace(dev)
+    buf = ws.get(L.opattr_workspace_bytes(C.byref(m.k), C.byref(m.p), C.byref(m.r), C.byref(m.d)))
+    _check(L.opattr_enclose_walk(C.byref(m.k), C.byref(m.r), C.byref(m.d), _p(out["range_id"]),
+                                 _p(out["fused"]), _p(out["range_any"]), _p(out["range_parent"]),
+                                 _p(out["range_depth"]), _p(out["diag"]), _p(buf),
+                                 C.c_size_t(buf.numel()), _stream_handle(stream)),
+           "opattr_enclose_walk")
     return out
 
 

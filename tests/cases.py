@@ -135,6 +135,31 @@ def stream_major(tr):
     for k in ("seq", "start_ns", "dur_ns", "stream_id", "name_id", "part_id", "query_ns"):
         if out.get(k) is not None:
             out[k] = np.ascontiguousarray(out[k][korder])
-    for k in ("r_start", "r_end", "r_stream", "r_op"):
-        out[k] = np.ascontiguousarray(out[k][rorder])
+    for k in ("r_start", "r_end", "r_stream", "r_op", "r_kind"):
+        if out.get(k) is not None:
+            out[k] = np.ascontiguousarray(out[k][rorder])
     return out, korder, rorder
+
+
+def with_kinds(tr, seed, p_boundary=0.2, p_skip=0.25, p_bad=0.0, roots_boundary=False):
+    """A copy of tr whose ranges carry enclosure-walk kinds (0 op, 1 boundary,
+    2 skip; p_bad of them an invalid kind 3). With roots_boundary, ranges
+    that no other range contains become boundaries (profiler steps)."""
+    rng = np.random.default_rng(seed)
+    R = tr["r_start"].size
+    u = rng.random(R)
+    kind = np.where(u < p_boundary, 1, np.where(u < p_boundary + p_skip, 2, 0)).astype(np.uint8)
+    if roots_boundary and R:
+        rs, re, st = tr["r_start"], tr["r_end"], tr["r_stream"]
+        order = np.lexsort((np.arange(R), -re.astype(np.int64), rs, st))
+        top_end = {}
+        for x in order:
+            s = int(st[x])
+            if s not in top_end or int(re[x]) > top_end[s]:
+                kind[x] = 1
+                top_end[s] = int(re[x])
+    if p_bad:
+        kind[rng.random(R) < p_bad] = 3
+    out = dict(tr)
+    out["r_kind"] = kind
+    return out

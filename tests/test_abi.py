@@ -43,20 +43,37 @@ def test_library_exports_every_declared_symbol(lib):
         assert hasattr(lib, f)
 
 
-def test_struct_layouts_match_header():
-    assert C.sizeof(opattr.opattr_kernels) == 64
-    assert C.sizeof(opattr.opattr_profiled) == 48
-    assert C.sizeof(opattr.opattr_ranges) == 40
-    assert C.sizeof(opattr.opattr_dims) == 32
-    assert C.sizeof(opattr.opattr_diag) == 64
-    assert opattr.OP_ROW_DTYPE.itemsize == 192
+def test_struct_layouts_match_header(tmp_path):
+    """Sizes and field offsets of the binding's structs, against a C program
+    compiled from the header."""
+    structs = {"opattr_kernels": opattr.opattr_kernels, "opattr_profiled": opattr.opattr_profiled,
+               "opattr_ranges": opattr.opattr_ranges, "opattr_dims": opattr.opattr_dims,
+               "opattr_diag": opattr.opattr_diag}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "opattr.h"', "int main(void) {"]
+    for name, cls in structs.items():
+        lines.append(f'  printf("{name} %zu\\n", sizeof({name}));')
+        for f, _ in cls._fields_:
+            lines.append(f'  printf("{name}.{f} %zu\\n", offsetof({name}, {f}));')
+    lines += ['  printf("opattr_op_row %zu\\n", sizeof(opattr_op_row));', "  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c11", "-I", os.path.dirname(HEADER), "-o", str(exe), str(src)],
+                   check=True)
+    got = dict(line.split() for line in subprocess.run([str(exe)], check=True, capture_output=True,
+                                                       text=True).stdout.splitlines())
+    for name, cls in structs.items():
+        assert int(got[name]) == C.sizeof(cls), name
+        for f, _ in cls._fields_:
+            assert int(got[f"{name}.{f}"]) == getattr(cls, f).offset, f"{name}.{f}"
+    assert int(got["opattr_op_row"]) == opattr.OP_ROW_DTYPE.itemsize == 192
 
 
 def _structs(T=100, P=50, R=10, NN=8, NS=2, NOPS=4, flags=0):
     fake = C.c_void_p(0x1000)  # never dereferenced on the host
     k = opattr.opattr_kernels(T, fake, fake, fake, fake, fake, None, None)
     p = opattr.opattr_profiled(P, fake, fake, 20, 1, 0)
-    r = opattr.opattr_ranges(R, fake, fake, fake, fake)
+    r = opattr.opattr_ranges(R, fake, fake, fake, fake, None)
     d = opattr.opattr_dims(NN, NS, NOPS, 0, None, flags)
     return k, p, r, d
 
@@ -75,6 +92,21 @@ def test_workspace_size_is_pure_and_monotone(lib):
     hinted = lib.opattr_workspace_bytes(C.byref(k), C.byref(p), C.byref(r), C.byref(d))
     assert hinted < full
     assert lib.opattr_workspace_bytes(C.byref(k), C.byref(p), C.byref(r), None) == 0
+
+
+def test_workspace_for_all_inputs_covers_every_entry_point(lib):
+    """The header's contract: the size computed with every input covers each
+    entry point, whose own plan leaves out the inputs it does not take."""
+    for flags in (0, opattr.SEQ_DENSE, opattr.KERNELS_STREAM_MAJOR | opattr.SEQ_DENSE |
+                  opattr.RANGES_NESTED):
+        k, p, r, d = _structs(T=100_000, P=20_000, R=5_000, NN=300, NS=8, NOPS=64, flags=flags)
+        d.n_parts, d.part_rep = 16, C.c_void_p(0x3000)
+        k.part_id = C.c_void_p(0x4000)
+        full = lib.opattr_workspace_bytes(C.byref(k), C.byref(p), C.byref(r), C.byref(d))
+        for pp, rr in ((None, None), (None, r), (p, None), (p, r)):
+            part = lib.opattr_workspace_bytes(C.byref(k), C.byref(pp) if pp else None,
+                                              C.byref(rr) if rr else None, C.byref(d))
+            assert part <= full, (flags, pp is None, rr is None)
 
 
 def test_argument_errors_return_before_any_device_work(lib):

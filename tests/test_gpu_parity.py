@@ -308,6 +308,64 @@ def test_error_classes_match_oracle():
             parity.assert_attribute(out, want, diag)
 
 
+def _walk_gpu(tr, flags=0):
+    import torch
+
+    dt = opattr.to_device(tr, DEV)
+    out = opattr.opattr_enclose_walk(dt, flags=flags)
+    torch.cuda.synchronize()
+    return out, opattr.read_diag(out["diag"])
+
+
+def _assert_walk(out, want, diag):
+    for f in ("range_id", "fused", "range_any", "range_parent", "range_depth"):
+        np.testing.assert_array_equal(parity.host(out[f]), want[f], err_msg=f)
+    parity.assert_diag(diag, want["diag"])
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_enclose_walk_parity(seed):
+    """Alg. 2's walk with range kinds: every output of the walk entry point
+    against the oracle, on random nested traces (some with invalid kinds),
+    in every emission order."""
+    emission = ("stream_major", "seq", "shuffled")[seed % 3]
+    print(f"case walk seed={seed} emission={emission}", flush=True)
+    tr = cases.random_trace(900 + seed, T=400, R=120, S=1 + seed % 4, t_max=300, max_depth=6)
+    tr = cases.with_kinds(tr, seed, p_bad=0.05 if seed % 5 == 4 else 0.0,
+                          roots_boundary=seed % 2 == 0)
+    flags = 0
+    if emission == "stream_major":
+        tr = cases.stream_major(tr)[0]
+        flags = opattr.KERNELS_STREAM_MAJOR | opattr.RANGES_NESTED
+    want = O.enclose_walk(tr)
+    out, diag = _walk_gpu(tr, flags)
+    _assert_walk(out, want, diag)
+
+
+def test_enclose_walk_large_with_kinds():
+    """The 10M-launch trace with profiler-step roots (boundaries) and skipped
+    namespaces: the walk outputs, and the whole attribution following the
+    walk (operator rows from the innermost op before a boundary)."""
+    print("case walk large", flush=True)
+    tr = cases.with_kinds(_trace("large", "stream_major"), 5, p_boundary=0.0, p_skip=0.2,
+                          roots_boundary=True)
+    want = O.enclose_walk(tr)
+    out, diag = _walk_gpu(tr, HINTS)
+    _assert_walk(out, want, diag)
+    want_all = O.attribute(tr)
+    got, gdiag = _run(tr, flags=HINTS)
+    parity.assert_attribute(got, want_all, gdiag)
+
+
+def test_enclose_walk_without_kinds_is_innermost():
+    print("case walk no kinds", flush=True)
+    tr = _trace("gpt2", "stream_major")
+    want = O.enclose_walk(tr)
+    out, diag = _walk_gpu(tr, HINTS)
+    _assert_walk(out, want, diag)
+    np.testing.assert_array_equal(parity.host(out["range_id"]), tr["planted_range"])
+
+
 def test_deep_nesting_limit():
     T, depth = 8, 300
     r_start = np.arange(depth, dtype=np.uint64)

@@ -318,16 +318,8 @@ def test_enclose_crossing_ranges_flagged():
     np.testing.assert_array_equal(out["range_id"], brute.enclose(tr))
 
 
-def _with_kinds(tr, seed, p_boundary=0.2, p_skip=0.25, p_bad=0.0):
-    rng = np.random.default_rng(seed)
-    R = tr["r_start"].size
-    u = rng.random(R)
-    kind = np.where(u < p_boundary, 1, np.where(u < p_boundary + p_skip, 2, 0)).astype(np.uint8)
-    if p_bad:
-        kind[rng.random(R) < p_bad] = 3
-    tr = dict(tr)
-    tr["r_kind"] = kind
-    return tr
+def _with_kinds(tr, seed, p_bad=0.0):
+    return cases.with_kinds(tr, seed, p_bad=p_bad)
 
 
 @pytest.mark.parametrize("seed", range(12))
