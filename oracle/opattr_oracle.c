@@ -269,6 +269,125 @@ int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
 }
 
 /* ----------------------------------------------------------------------- */
+/* Dedup class discovery (Sec. 3.7)                                         */
+/* ----------------------------------------------------------------------- */
+
+/* the sequences being compared by qsort (file-scope: qsort takes no context) */
+static const oref_kernels *cls_k;
+static const int64_t *cls_cnt, *cls_off;
+static const key3 *cls_mem;
+static const char *cls_contig;
+
+/* partitions ordered by their (name, stream) sequence in launch order:
+   non-consecutive partitions last, then by length, then element by element;
+   ties by partition number */
+static int cmp_part_seq(const void *x, const void *y) {
+  const int64_t p = *(const int64_t *)x, q = *(const int64_t *)y;
+  if (cls_contig[p] != cls_contig[q]) return cls_contig[p] ? -1 : 1;
+  if (cls_contig[p]) {
+    if (cls_cnt[p] != cls_cnt[q]) return cls_cnt[p] < cls_cnt[q] ? -1 : 1;
+    for (int64_t j = 0; j < cls_cnt[p]; ++j) {
+      const int64_t a = cls_mem[cls_off[p] + j].idx, b = cls_mem[cls_off[q] + j].idx;
+      if (cls_k->name_id[a] != cls_k->name_id[b])
+        return cls_k->name_id[a] < cls_k->name_id[b] ? -1 : 1;
+      if (cls_k->stream_id[a] != cls_k->stream_id[b])
+        return cls_k->stream_id[a] < cls_k->stream_id[b] ? -1 : 1;
+    }
+  }
+  return p < q ? -1 : (p > q ? 1 : 0);
+}
+
+int oref_dedup_classes(const oref_kernels *k, const oref_dims *d, int32_t *part_rep,
+                       oref_diag *diag) {
+  if (!k || !d || !diag || k->n < 0 || (d->n_parts > 0 && !part_rep)) return OREF_ERR_ARG;
+  if (k->n > 0 && (!k->seq || !k->name_id || !k->stream_id)) return OREF_ERR_ARG;
+  const int64_t T = k->n;
+  const uint32_t NP = d->n_parts;
+  if (NP == 0) return 0;
+  for (uint32_t q = 0; q < NP; ++q) part_rep[q] = (int32_t)q;
+  if (!k->part_id) return 0;
+
+  /* a launch takes part with an in-range name and partition */
+  for (int64_t i = 0; i < T; ++i) {
+    const int32_t p = k->part_id[i];
+    if (k->name_id[i] >= d->n_names || p < -1 || (p >= 0 && (uint32_t)p >= NP))
+      diag->bad_records++;
+  }
+  if (diag->bad_records) diag->flags |= OREF_F_DATA;
+
+  /* launch-order rank of every launch (seq, ties by input index) */
+  key3 *all = xcalloc((size_t)T, sizeof(key3));
+  for (int64_t i = 0; i < T; ++i) {
+    all[i].a = k->seq[i];
+    all[i].b = all[i].c = 0;
+    all[i].idx = i;
+  }
+  qsort(all, (size_t)T, sizeof(key3), cmp_key3);
+  int64_t *rank = xcalloc((size_t)T, sizeof(int64_t));
+  for (int64_t x = 0; x < T; ++x) rank[all[x].idx] = x;
+  free(all);
+
+  /* members of each partition in launch order */
+  int64_t *cnt = xcalloc(NP, sizeof(int64_t));
+  int64_t *off = xcalloc((size_t)NP + 1, sizeof(int64_t));
+  for (int64_t i = 0; i < T; ++i) {
+    const int32_t p = k->part_id[i];
+    if (k->name_id[i] < d->n_names && p >= 0 && (uint32_t)p < NP) cnt[p]++;
+  }
+  for (uint32_t q = 0; q < NP; ++q) off[q + 1] = off[q] + cnt[q];
+  key3 *mem = xcalloc((size_t)off[NP], sizeof(key3));
+  int64_t *fill = xcalloc(NP, sizeof(int64_t));
+  for (int64_t i = 0; i < T; ++i) {
+    const int32_t p = k->part_id[i];
+    if (k->name_id[i] >= d->n_names || p < 0 || (uint32_t)p >= NP) continue;
+    key3 *e = &mem[off[p] + fill[p]++];
+    e->a = (uint64_t)p;
+    e->b = (uint64_t)rank[i];
+    e->c = 0;
+    e->idx = i;
+  }
+  qsort(mem, (size_t)off[NP], sizeof(key3), cmp_key3);
+
+  /* consecutive in launch order (as for the dedup broadcast) */
+  char *contig = xcalloc(NP, 1);
+  for (uint32_t q = 0; q < NP; ++q) {
+    if (cnt[q] == 0) { contig[q] = 1; continue; }
+    const uint64_t lo = mem[off[q]].b, hi = mem[off[q + 1] - 1].b;
+    contig[q] = (hi - lo + 1 == (uint64_t)cnt[q]);
+    if (!contig[q]) diag->flags |= OREF_F_PARTITION;
+  }
+
+  /* sort partitions by sequence; each run of equal sequences is a class,
+     represented by its first (lowest-numbered) partition */
+  int64_t *ord = xcalloc(NP, sizeof(int64_t));
+  for (uint32_t q = 0; q < NP; ++q) ord[q] = q;
+  cls_k = k;
+  cls_cnt = cnt;
+  cls_off = off;
+  cls_mem = mem;
+  cls_contig = contig;
+  qsort(ord, NP, sizeof(int64_t), cmp_part_seq);
+  int64_t head = -1;
+  for (uint32_t j = 0; j < NP; ++j) {
+    const int64_t q = ord[j];
+    if (!contig[q]) { part_rep[q] = (int32_t)q; continue; }
+    /* same class as the current head: the same sequence, element by element */
+    int eq = 0;
+    if (head >= 0 && cnt[head] == cnt[q]) {
+      eq = 1;
+      for (int64_t t = 0; t < cnt[q] && eq; ++t) {
+        const int64_t a = mem[off[head] + t].idx, b = mem[off[q] + t].idx;
+        eq = k->name_id[a] == k->name_id[b] && k->stream_id[a] == k->stream_id[b];
+      }
+    }
+    if (!eq) head = q;
+    part_rep[q] = (int32_t)head;
+  }
+  free(ord); free(cnt); free(off); free(mem); free(fill); free(contig); free(rank);
+  return 0;
+}
+
+/* ----------------------------------------------------------------------- */
 /* Stage 3: enclosure (Alg. 2, Sec. 3.5)                                    */
 /* ----------------------------------------------------------------------- */
 

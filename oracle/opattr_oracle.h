@@ -129,6 +129,16 @@ int oref_aggregate(const oref_kernels *k, const oref_profiled *p,
                    const int32_t *match, const int32_t *range_id,
                    const oref_ranges *r, const oref_dims *d, const uint8_t *agg_kind,
                    oref_row *table, oref_summary *sum, oref_diag *diag);
+/* Dedup class discovery (Sec. 3.7): partitions whose launches form the same
+   sequence of (name, stream) in launch order are structural duplicates; each
+   gets as representative the lowest-numbered partition of its class
+   (part_rep[q], n_parts entries; d->part_rep is not read). Launches with a
+   name or partition out of range take no part. A partition whose launches
+   are not consecutive in launch order is its own class and raises
+   PARTITION. */
+int oref_dedup_classes(const oref_kernels *k, const oref_dims *d, int32_t *part_rep,
+                       oref_diag *diag);
+
 /* the four stages in order: match, dedup, enclose, aggregate */
 int oref_attribute(const oref_kernels *k, const oref_profiled *p,
                    const oref_ranges *r, const oref_dims *d, int policy,

@@ -109,8 +109,10 @@ def load(path: str):
                                  P(Summary), P(Diag)]
     L.oref_enclose_walk.argtypes = [P(Kernels), P(Ranges), P(Dims), C.c_void_p, C.c_void_p,
                                     C.c_void_p, C.c_void_p, C.c_void_p, P(Diag)]
+    L.oref_dedup_classes.argtypes = [P(Kernels), P(Dims), C.c_void_p, P(Diag)]
     L.oref_diag_finish.argtypes = [P(Diag), C.c_int]
-    for f in ("oref_match", "oref_dedup", "oref_enclose", "oref_enclose_walk", "oref_aggregate"):
+    for f in ("oref_match", "oref_dedup", "oref_enclose", "oref_enclose_walk", "oref_aggregate",
+              "oref_dedup_classes"):
         getattr(L, f).restype = C.c_int
     return L
 
@@ -251,3 +253,22 @@ def enclose_walk(tr, library=None):
     L.oref_diag_finish(C.byref(dg), PREFIX)
     return {"range_id": rid, "fused": fused, "range_any": rany, "range_parent": par,
             "range_depth": depth, "diag": diag_dict(dg)}
+
+
+def dedup_classes(tr, library=None):
+    """Dedup class discovery (Sec. 3.7): the class representative of every
+    partition (``tr["part_id"]``, ``tr["n_parts"]``; ``tr["part_rep"]`` is not
+    read) from the partitions' (name, stream) sequences in launch order."""
+    L = library if library is not None else lib()
+    tr = dict(tr)
+    tr["part_rep"] = None
+    x = _Inputs(tr)
+    NP = int(tr.get("n_parts", 0) or 0)
+    x.d.n_parts = NP
+    dg = Diag()
+    rep = np.empty(NP, dtype=np.int32)
+    rc = L.oref_dedup_classes(C.byref(x.k), C.byref(x.d), _ptr(rep), C.byref(dg))
+    if rc:
+        raise ValueError(f"oref_dedup_classes: {rc}")
+    L.oref_diag_finish(C.byref(dg), PREFIX)
+    return {"part_rep": rep, "diag": diag_dict(dg)}

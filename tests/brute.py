@@ -100,6 +100,34 @@ def enclose(tr):
     return out
 
 
+def dedup_classes(tr):
+    """Per partition: the lowest-numbered partition whose launches (valid
+    name and partition) form the same (name, stream) sequence in launch
+    order; a partition whose launches are not consecutive in launch order
+    (among all launches, by seq then index) is its own class."""
+    NP = int(tr.get("n_parts", 0) or 0)
+    part, seq, name, st = tr["part_id"], tr["seq"], tr["name_id"], tr["stream_id"]
+    T = seq.size
+    order = sorted(range(T), key=lambda i: (int(seq[i]), i))
+    rank = {i: x for x, i in enumerate(order)}
+    members = [[] for _ in range(NP)]
+    for i in order:
+        p = int(part[i])
+        if 0 <= p < NP and int(name[i]) < tr["n_names"]:
+            members[p].append(i)
+    contig = [not m or rank[m[-1]] - rank[m[0]] + 1 == len(m) for m in members]
+    seqs = [[(int(name[i]), int(st[i])) for i in m] for m in members]
+    rep = list(range(NP))
+    for q in range(NP):
+        if not contig[q]:
+            continue
+        for r in range(q):
+            if contig[r] and seqs[r] == seqs[q]:
+                rep[q] = r
+                break
+    return np.array(rep, dtype=np.int64), any(not c for c in contig)
+
+
 def _range_valid(tr, r):
     kind = tr.get("r_kind")
     return (int(tr["r_stream"][r]) < tr["n_streams"] and int(tr["r_op"][r]) < tr["n_ops"]

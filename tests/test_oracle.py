@@ -386,6 +386,68 @@ def test_enclose_walk_hand_shaped():
     assert agg["table"]["kernel_count"][6] == 2
 
 
+def _class_trace(seed, T=90, n_parts=9, noncontig=False, bad=False):
+    """Partitions as consecutive launch-order runs; some copy the (name,
+    stream) sequence of an earlier one, some differ in one stream or name."""
+    rng = np.random.default_rng(seed)
+    tr = cases.random_trace(seed, T=T, S=3, n_names=4, seq_gaps=seed % 2 == 0)
+    order = np.argsort(tr["seq"], kind="stable")
+    L = T // (n_parts + 1)
+    part_seq = np.full(T, -1, np.int32)
+    name_seq = tr["name_id"][order].copy()
+    st_seq = tr["stream_id"][order].copy()
+    for p in range(n_parts):
+        a = p * L + 2
+        part_seq[a:a + L] = p
+        src = int(rng.integers(0, p + 1))
+        if src < p and rng.random() < 0.7:
+            b = src * L + 2
+            name_seq[a:a + L] = name_seq[b:b + L]
+            st_seq[a:a + L] = st_seq[b:b + L]
+            if rng.random() < 0.3:  # a near copy: one stream differs
+                st_seq[a + int(rng.integers(0, L))] ^= 1
+    if noncontig:
+        part_seq[2 * L + 2 + L // 2] = -1  # a hole in partition 2
+    if bad:
+        name_seq[5 * L + 3] = tr["n_names"] + 1  # a launch with a bad name
+    tr["part_id"] = np.empty(T, np.int32)
+    tr["part_id"][order] = part_seq
+    tr["name_id"] = tr["name_id"].copy()
+    tr["name_id"][order] = name_seq
+    tr["stream_id"] = tr["stream_id"].copy()
+    tr["stream_id"][order] = st_seq
+    tr["n_parts"] = n_parts
+    tr["part_rep"] = None
+    return tr
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_dedup_classes_match_brute_force(seed):
+    """Class discovery against its definition: pairwise comparison of the
+    partitions' (name, stream) sequences in launch order."""
+    tr = _class_trace(seed, noncontig=seed % 3 == 1, bad=seed % 4 == 3)
+    out = O.dedup_classes(tr)
+    rep, has_noncontig = brute.dedup_classes(tr)
+    np.testing.assert_array_equal(out["part_rep"], rep)
+    assert bool(out["diag"]["flags"] & 16) == has_noncontig
+
+
+@pytest.mark.parametrize("cfg", ["gpt2", "large"])
+def test_dedup_classes_recover_the_generated_templates(cfg):
+    """The generator copies class templates into every layer instance: GPT-2
+    has one class (every layer is the same 40-kernel template), the large
+    trace three (layer l of every iteration belongs to class l mod 3), so
+    discovery finds the first instances as representatives. The planted
+    per-iteration representatives are members of those classes."""
+    tr = tg.generate(cfg)
+    out = O.dedup_classes(tr)
+    q = np.arange(tr["n_parts"])
+    want = np.zeros_like(q) if cfg == "gpt2" else (q % 48) % 3
+    np.testing.assert_array_equal(out["part_rep"], want)
+    np.testing.assert_array_equal(out["part_rep"][tr["part_rep"]], out["part_rep"])
+    assert out["diag"]["status"] == 0
+
+
 @pytest.mark.parametrize("cfg", ["tiny", "gpt2", "sdpa", "lstm"])
 def test_enclose_planted_labels(cfg):
     tr = tg.generate(cfg)

@@ -22,7 +22,10 @@ MUTANTS = {
                               "if (0) match[i] = -1;"),
     "dedup_reversed_position": ("int64_t src = mem[off[r] + pos].idx;",
                                 "int64_t src = mem[off[r] + cnt[r] - 1 - pos].idx;"),
-    "dedup_contiguity_on_seq_values": ("e->b = (uint64_t)rank[i];", "e->b = k->seq[i];"),
+    "dedup_contiguity_on_seq_values": ("e->a = (uint64_t)q;\n    e->b = (uint64_t)rank[i];",
+                                       "e->a = (uint64_t)q;\n    e->b = k->seq[i];"),
+    "classes_contiguity_on_seq_values": ("e->a = (uint64_t)p;\n    e->b = (uint64_t)rank[i];",
+                                         "e->a = (uint64_t)p;\n    e->b = k->seq[i];"),
     "dedup_no_name_check": ("ok = k->name_id[src] == k->name_id[i];", "ok = 1;"),
     "enclose_end_ascending": ("rs[nr].c = UINT64_MAX - r->end_ns[x];",
                               "rs[nr].c = r->end_ns[x];"),
@@ -50,6 +53,11 @@ MUTANTS = {
     "walk_outermost_op_kept": ("if (first < 0) first = (int32_t)id;", "first = (int32_t)id;"),
     "fused_counts_every_range": ("if (fused) fused[i] = nops > 1 ? 1 : 0;",
                                  "if (fused) fused[i] = top > 1 ? 1 : 0;"),
+    "classes_names_only": ("eq = k->name_id[a] == k->name_id[b] && k->stream_id[a] == k->stream_id[b];",
+                           "eq = k->name_id[a] == k->name_id[b];"),
+    "classes_contiguity_ignored": ("contig[q] = (hi - lo + 1 == (uint64_t)cnt[q]);\n    if (!contig[q]) diag->flags |= OREF_F_PARTITION;\n  }\n\n  /* sort partitions",
+                                   "contig[q] = 1;\n  }\n\n  /* sort partitions"),
+    "classes_never_grouped": ("part_rep[q] = (int32_t)head;", "part_rep[q] = (int32_t)q;"),
     "parent_is_root": ("if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[top - 1] : -1;",
                        "if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[0] : -1;"),
 }
@@ -129,6 +137,13 @@ def battery(L) -> bool:
                           (out["range_any"], rany), (out["range_parent"], par)):
             if not np.array_equal(got, want):
                 return False
+    import test_oracle
+    for seed in range(8):
+        tr = test_oracle._class_trace(seed, noncontig=seed % 3 == 1, bad=seed % 4 == 3)
+        out = O.dedup_classes(tr, library=L)
+        rep, has_nc = brute.dedup_classes(tr)
+        if not np.array_equal(out["part_rep"], rep) or bool(out["diag"]["flags"] & 16) != has_nc:
+            return False
     tr = _edge_trace()
     out = O.attribute(tr, library=L)
     if not np.array_equal(out["range_id"], brute.enclose(tr)):
