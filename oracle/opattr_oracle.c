@@ -194,15 +194,11 @@ int oref_match(const oref_kernels *k, const oref_profiled *p, const oref_dims *d
 /* Stage 2: layer dedup, positional inheritance (Sec. 3.7)                  */
 /* ----------------------------------------------------------------------- */
 
-int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
-               oref_diag *diag) {
-  if (!k || !d || !match || !diag || k->n < 0) return OREF_ERR_ARG;
-  if (!dedup_on(k, d)) return 0; /* no partitions: nothing to do */
+/* Launch-order rank of every kernel: its position when the whole timeline is
+   sorted by seq (ties by input index). Launch ordinals are unique over the
+   timeline, as for the matching: equal seq values raise ORDER. */
+static int64_t *launch_ranks(const oref_kernels *k, oref_diag *diag) {
   const int64_t T = k->n;
-  const uint32_t NP = d->n_parts;
-
-  /* launch-order rank of every kernel: its position when the whole timeline is
-     sorted by seq (ties by input index) */
   key3 *all = xcalloc((size_t)T, sizeof(key3));
   for (int64_t i = 0; i < T; ++i) {
     all[i].a = k->seq[i];
@@ -212,7 +208,20 @@ int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
   qsort(all, (size_t)T, sizeof(key3), cmp_key3);
   int64_t *rank = xcalloc((size_t)T, sizeof(int64_t));
   for (int64_t x = 0; x < T; ++x) rank[all[x].idx] = x;
+  for (int64_t x = 1; x < T; ++x)
+    if (all[x].a == all[x - 1].a) { diag->flags |= OREF_F_ORDER; break; }
   free(all);
+  return rank;
+}
+
+int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
+               oref_diag *diag) {
+  if (!k || !d || !match || !diag || k->n < 0) return OREF_ERR_ARG;
+  if (!dedup_on(k, d)) return 0; /* no partitions: nothing to do */
+  const int64_t T = k->n;
+  const uint32_t NP = d->n_parts;
+
+  int64_t *rank = launch_ranks(k, diag);
 
   /* members[p]: the kernels of partition p in launch order */
   int64_t *cnt = xcalloc(NP, sizeof(int64_t));
@@ -315,17 +324,7 @@ int oref_dedup_classes(const oref_kernels *k, const oref_dims *d, int32_t *part_
   }
   if (diag->bad_records) diag->flags |= OREF_F_DATA;
 
-  /* launch-order rank of every launch (seq, ties by input index) */
-  key3 *all = xcalloc((size_t)T, sizeof(key3));
-  for (int64_t i = 0; i < T; ++i) {
-    all[i].a = k->seq[i];
-    all[i].b = all[i].c = 0;
-    all[i].idx = i;
-  }
-  qsort(all, (size_t)T, sizeof(key3), cmp_key3);
-  int64_t *rank = xcalloc((size_t)T, sizeof(int64_t));
-  for (int64_t x = 0; x < T; ++x) rank[all[x].idx] = x;
-  free(all);
+  int64_t *rank = launch_ranks(k, diag);
 
   /* members of each partition in launch order */
   int64_t *cnt = xcalloc(NP, sizeof(int64_t));

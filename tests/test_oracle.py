@@ -432,6 +432,25 @@ def test_dedup_classes_match_brute_force(seed):
     assert bool(out["diag"]["flags"] & 16) == has_noncontig
 
 
+def test_dedup_classes_duplicate_seq_ties_by_index():
+    """Equal seq values rank by input index (as in the matching) and raise
+    ORDER: launches 0 and 1 share seq 5, so partition 0 = (a, b) in index
+    order and partition 1 = (a, b) too; swapping the indices of partition 1's
+    launches would reverse it."""
+    tr = cases.random_trace(0, T=4, S=1, n_names=2)
+    tr.update(seq=np.array([5, 5, 7, 8], np.uint32), name_id=np.array([0, 1, 0, 1], np.uint32),
+              stream_id=np.zeros(4, np.uint16), part_id=np.array([0, 0, 1, 1], np.int32),
+              n_parts=2, part_rep=None)
+    out = O.dedup_classes(tr)
+    np.testing.assert_array_equal(out["part_rep"], [0, 0])
+    assert out["diag"]["flags"] & 2 and out["diag"]["status"] == -8
+    tr["name_id"] = np.array([1, 0, 0, 1], np.uint32)
+    np.testing.assert_array_equal(O.dedup_classes(tr)["part_rep"], [0, 1])
+    np.testing.assert_array_equal(brute.dedup_classes(tr)[0], [0, 1])
+    tr["seq"] = np.array([5, 6, 7, 8], np.uint32)
+    assert not O.dedup_classes(tr)["diag"]["flags"] & 2
+
+
 @pytest.mark.parametrize("cfg", ["gpt2", "large"])
 def test_dedup_classes_recover_the_generated_templates(cfg):
     """The generator copies class templates into every layer instance: GPT-2

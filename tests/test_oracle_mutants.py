@@ -57,6 +57,8 @@ MUTANTS = {
                            "eq = k->name_id[a] == k->name_id[b];"),
     "classes_contiguity_ignored": ("contig[q] = (hi - lo + 1 == (uint64_t)cnt[q]);\n    if (!contig[q]) diag->flags |= OREF_F_PARTITION;\n  }\n\n  /* sort partitions",
                                    "contig[q] = 1;\n  }\n\n  /* sort partitions"),
+    "ranks_order_unchecked": ("if (all[x].a == all[x - 1].a) { diag->flags |= OREF_F_ORDER; break; }",
+                              "if (0) break;"),
     "classes_never_grouped": ("part_rep[q] = (int32_t)head;", "part_rep[q] = (int32_t)q;"),
     "parent_is_root": ("if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[top - 1] : -1;",
                        "if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[0] : -1;"),
@@ -140,9 +142,14 @@ def battery(L) -> bool:
     import test_oracle
     for seed in range(8):
         tr = test_oracle._class_trace(seed, noncontig=seed % 3 == 1, bad=seed % 4 == 3)
+        if seed % 4 == 2:  # two launches share a seq value
+            tr["seq"] = tr["seq"].copy()
+            tr["seq"][7] = tr["seq"][3]
         out = O.dedup_classes(tr, library=L)
         rep, has_nc = brute.dedup_classes(tr)
         if not np.array_equal(out["part_rep"], rep) or bool(out["diag"]["flags"] & 16) != has_nc:
+            return False
+        if bool(out["diag"]["flags"] & 2) != (np.unique(tr["seq"]).size < tr["seq"].size):
             return False
     tr = _edge_trace()
     out = O.attribute(tr, library=L)
