@@ -8,6 +8,8 @@
  *                          timeline launches (Sec. 3.3, Alg. 1)
  *   opattr_dedup_broadcast positional inheritance of counters from the profiled
  *                          representative of a layer class (Sec. 3.7)
+ *   opattr_dedup_classes   discovery of those classes from the timeline alone
+ *                          (Sec. 3.7)
  *   opattr_enclose         innermost operator range enclosing each launch on its
  *                          own stream (Sec. 3.5, Alg. 2)
  *   opattr_aggregate       per-operator SUM / duration-weighted mean (Eq. 1) / MAX
@@ -211,6 +213,25 @@ int opattr_match(const opattr_kernels *k, const opattr_profiled *p, const opattr
 int opattr_dedup_broadcast(const opattr_kernels *k, const opattr_dims *d, int32_t *match,
                            opattr_diag *diag, void *ws, size_t ws_bytes, void *stream);
 
+/* Layer class discovery (Sec. 3.7: structurally identical layers share one
+   profiled representative). Two partitions are one class when the launches
+   of each (valid name_id and part_id) form the same sequence of (name_id,
+   stream_id) in launch order (seq, ties by input index); every partition
+   gets as representative the lowest-numbered partition of its class.
+   Partitions without launches share the empty sequence. A partition whose
+   launches are not consecutive in launch order is its own class and raises
+   PARTITION; equal seq values raise ORDER (checked unless OPATTR_SEQ_DENSE is
+   promised without OPATTR_VALIDATE). Launches with an id out of range count
+   as bad_records.
+   In: k->seq, name_id, stream_id, part_id (required when k->n > 0), and
+   d->n_names, d->n_parts (d->part_rep is not read). Out: part_rep[d->n_parts]
+   (device), a class map that opattr_dedup_broadcast and opattr_attribute
+   accept as d->part_rep. Exact: a 64-bit sequence hash proposes the
+   representative and an element-wise comparison confirms it. Workspace:
+   opattr_workspace_bytes(k, NULL, NULL, d) with d->n_parts set. */
+int opattr_dedup_classes(const opattr_kernels *k, const opattr_dims *d, int32_t *part_rep,
+                         opattr_diag *diag, void *ws, size_t ws_bytes, void *stream);
+
 /* Enclosure (Alg. 2). The ranges on stream_id[i] with start_r <= q_i <= end_r
    (q_i = query_ns[i], or start_ns[i]) are walked from the innermost (the one
    last in nesting order: start asc, end desc, index asc) outward: op ranges
@@ -279,6 +300,12 @@ enum {
   OPATTR_NUM_PROBES = 13
 };
 int opattr_set_probe_events(void *const *events, int n);
+
+/* Test support for opattr_dedup_classes, per calling host thread: keep only
+   the low `bits` (1..64, default 64) bits of each partition's sequence key,
+   so that partitions with different sequences share keys and the exact
+   element-wise search decides. Results are unchanged; only time grows. */
+int opattr_set_class_key_bits(int bits);
 
 /* Human-readable name of a status code. */
 const char *opattr_strerror(int status);

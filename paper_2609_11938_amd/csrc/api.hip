@@ -126,6 +126,19 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.cmap = b.take((size_t)pl.max_chunks * 4);
   pl.sit = b.take((size_t)pl.cap_items * 8);
   pl.part = b.take((size_t)pl.max_chunks * 200);
+  // class discovery: per partition, and the key table
+  const size_t NPc = d->n_parts, TS = (size_t)class_table_slots(d->n_parts);
+  pl.c_cnt = b.take(NPc * 4);
+  pl.c_lo = b.take(NPc * 4);
+  pl.c_hi = b.take(NPc * 4);
+  pl.c_cc = b.take(NPc * 4);
+  pl.c_off = b.take(NPc * 4);
+  pl.c_key = b.take(NPc * 8);
+  pl.c_cand = b.take(NPc * 4);
+  pl.c_fail = b.take(NPc * 4);
+  pl.c_list = b.take(NPc * 4);
+  pl.c_tkey = b.take(TS * 8);
+  pl.c_tmin = b.take(TS * 4);
   pl.misc = b.take(256);
   pl.total = b.off;
   return pl;
@@ -369,6 +382,26 @@ int opattr_dedup_broadcast(const opattr_kernels *k, const opattr_dims *d, int32_
   return launch_status();
 }
 
+int opattr_dedup_classes(const opattr_kernels *k, const opattr_dims *d, int32_t *part_rep,
+                         opattr_diag *diag, void *ws, size_t ws_bytes, void *stream) {
+  if (!check_dims(d) || !k || !ok_n(k->n) || !diag || (d->n_parts > 0 && !part_rep) ||
+      (k->n > 0 && (!k->seq || !k->name_id || !k->stream_id || !k->part_id)))
+    return OPATTR_ERR_INVALID_ARG;
+  const Plan pl = make_plan(k, nullptr, nullptr, d);
+  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  check_kernel_layout(k, d, diag, s);
+  if (d->n_parts > 0) {
+    // launch-order ranks: sorted when seq is not promised dense; a dense seq
+    // is checked only under OPATTR_VALIDATE
+    const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
+    if (!pl.seq_dense || validate) build_seq_view(k, d, ws, pl, diag, validate, s);
+    run_classes(k, d, part_rep, diag, ws, pl, s);
+  }
+  launch_finish(diag, nullptr, 0, s);
+  return launch_status();
+}
+
 int opattr_enclose_walk(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,
                         int32_t *range_id, uint8_t *fused, int32_t *range_any,
                         int32_t *range_parent, uint8_t *range_depth, opattr_diag *diag,
@@ -504,6 +537,12 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   reduce_items(e, s);
   launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s, table, sum, pl.G, d->n_ops);
   return launch_status();
+}
+
+int opattr_set_class_key_bits(int bits) {
+  if (bits < 1 || bits > 64) return OPATTR_ERR_INVALID_ARG;
+  g_class_key_bits = bits;
+  return OPATTR_OK;
 }
 
 int opattr_set_probe_events(void *const *events, int n) {

@@ -70,8 +70,9 @@ assert OP_ROW_DTYPE.itemsize == 192 and SUMMARY_DTYPE.itemsize == 40
 assert C.sizeof(opattr_diag) == 64
 
 EXPORTS = ("opattr_workspace_bytes", "opattr_diag_clear", "opattr_read_diag", "opattr_match",
-           "opattr_dedup_broadcast", "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate",
-           "opattr_attribute", "opattr_set_probe_events", "opattr_strerror")
+           "opattr_dedup_broadcast", "opattr_dedup_classes", "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate",
+           "opattr_attribute", "opattr_set_probe_events", "opattr_set_class_key_bits",
+           "opattr_strerror")
 PROBES = ("seq_view", "tl_hist", "pf_hist", "col_scan", "pf_slot", "tl_match", "dedup",
           "ranges", "main_pass", "finalize", "aggregate", "agg_runs", "item_sort")
 
@@ -99,6 +100,7 @@ def library(path: str | None = None):
     L.opattr_match.argtypes = [P(opattr_kernels), P(opattr_profiled), P(opattr_dims), i, vp, vp,
                                vp, vp, sz, vp]
     L.opattr_dedup_broadcast.argtypes = [P(opattr_kernels), P(opattr_dims), vp, vp, vp, sz, vp]
+    L.opattr_dedup_classes.argtypes = [P(opattr_kernels), P(opattr_dims), vp, vp, vp, sz, vp]
     L.opattr_enclose.argtypes = [P(opattr_kernels), P(opattr_ranges), P(opattr_dims), vp, vp,
                                  vp, vp, sz, vp]
     L.opattr_enclose_walk.argtypes = [P(opattr_kernels), P(opattr_ranges), P(opattr_dims), vp,
@@ -110,6 +112,8 @@ def library(path: str | None = None):
     for f in ("opattr_diag_clear", "opattr_read_diag", "opattr_match", "opattr_dedup_broadcast",
               "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate", "opattr_attribute"):
         getattr(L, f).restype = C.c_int
+    L.opattr_set_class_key_bits.argtypes = [i]
+    L.opattr_set_class_key_bits.restype = C.c_int
     L.opattr_set_probe_events.argtypes = [vp, i]
     L.opattr_set_probe_events.restype = C.c_int
     L.opattr_strerror.argtypes = [i]
@@ -333,6 +337,35 @@ def opattr_dedup_broadcast(dt: dict, match, flags=0, ws: Workspace | None = None
                                     _p(buf), C.c_size_t(buf.numel()), _stream_handle(stream)),
            "opattr_dedup_broadcast")
     return out
+
+
+def opattr_dedup_classes(dt: dict, flags=0, ws: Workspace | None = None,
+                         stream=None) -> Outputs:
+    """Layer class discovery (Sec. 3.7): part_rep for ``dt["n_parts"]``
+    partitions from the launches' (name, stream) sequences; ``dt["part_rep"]``
+    is not read."""
+    import torch
+
+    L = library()
+    m = _Marshal(dt, flags)
+    NP = int(dt.get("n_parts", 0) or 0)
+    m.d.n_parts = NP
+    m.d.part_rep = None
+    dev = dt["seq"].device
+    out = Outputs(part_rep=torch.empty(NP, dtype=torch.int32, device=dev),
+                  diag=_new_diag(dev, stream))
+    ws = ws or Workspace(dev)
+    buf = ws.get(L.opattr_workspace_bytes(C.byref(m.k), None, None, C.byref(m.d)))
+    _check(L.opattr_dedup_classes(C.byref(m.k), C.byref(m.d), _p(out["part_rep"]),
+                                  _p(out["diag"]), _p(buf), C.c_size_t(buf.numel()),
+                                  _stream_handle(stream)), "opattr_dedup_classes")
+    return out
+
+
+def set_class_key_bits(bits: int = 64):
+    """Test support: keep only ``bits`` bits of the class keys on this thread
+    (see opattr_set_class_key_bits)."""
+    _check(library().opattr_set_class_key_bits(int(bits)), "opattr_set_class_key_bits")
 
 
 def opattr_enclose(dt: dict, flags=0, want_depth=True, ws: Workspace | None = None,

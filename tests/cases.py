@@ -163,3 +163,41 @@ def with_kinds(tr, seed, p_boundary=0.2, p_skip=0.25, p_bad=0.0, roots_boundary=
     out = dict(tr)
     out["r_kind"] = kind
     return out
+
+
+def class_trace(seed, T=90, n_parts=9, noncontig=False, bad=False, S=3, n_names=4,
+                seq_gaps=None):
+    """Partitions as consecutive launch-order runs; some copy the (name,
+    stream) sequence of an earlier one, some differ in one stream or name."""
+    rng = np.random.default_rng(seed)
+    if seq_gaps is None:
+        seq_gaps = seed % 2 == 0
+    tr = random_trace(seed, T=T, S=S, n_names=n_names, R=4, seq_gaps=seq_gaps)
+    order = np.argsort(tr["seq"], kind="stable")
+    L = T // (n_parts + 1)
+    part_seq = np.full(T, -1, np.int32)
+    name_seq = tr["name_id"][order].copy()
+    st_seq = tr["stream_id"][order].copy()
+    for p in range(n_parts):
+        a = p * L + 2
+        part_seq[a:a + L] = p
+        src = int(rng.integers(0, p + 1))
+        if src < p and rng.random() < 0.7:
+            b = src * L + 2
+            name_seq[a:a + L] = name_seq[b:b + L]
+            st_seq[a:a + L] = st_seq[b:b + L]
+            if rng.random() < 0.3:  # a near copy: one stream differs
+                st_seq[a + int(rng.integers(0, L))] ^= 1
+    if noncontig:
+        part_seq[2 * L + 2 + L // 2] = -1  # a hole in partition 2
+    if bad:
+        name_seq[5 * L + 3] = tr["n_names"] + 1  # a launch with a bad name
+    tr["part_id"] = np.empty(T, np.int32)
+    tr["part_id"][order] = part_seq
+    tr["name_id"] = tr["name_id"].copy()
+    tr["name_id"][order] = name_seq
+    tr["stream_id"] = tr["stream_id"].copy()
+    tr["stream_id"][order] = st_seq
+    tr["n_parts"] = n_parts
+    tr["part_rep"] = None
+    return tr

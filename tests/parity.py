@@ -13,6 +13,20 @@ DIAG_FIELDS = ("status", "names_mismatched", "nesting_errors", "tl_unmatched", "
 COMMON_FLAGS = 0x7F
 
 
+_TRACES = {}
+
+
+def trace(cfg, emission):
+    """A generated trace, made once per process (the 10M-launch one takes a
+    while) and shared by the GPU test modules."""
+    from paper_2609_11938_amd import tracegen
+
+    key = (cfg, emission)
+    if key not in _TRACES:
+        _TRACES[key] = tracegen.generate(cfg, emission=emission)
+    return _TRACES[key]
+
+
 def host(t):
     return None if t is None else t.cpu().numpy()
 

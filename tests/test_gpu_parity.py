@@ -32,10 +32,7 @@ _CACHE = {}
 
 
 def _trace(cfg, emission):
-    key = ("trace", cfg, emission)
-    if key not in _CACHE:
-        _CACHE[key] = tg.generate(cfg, emission=emission)
-    return _CACHE[key]
+    return parity.trace(cfg, emission)
 
 
 def _oracle(cfg, emission):

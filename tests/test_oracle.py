@@ -387,38 +387,7 @@ def test_enclose_walk_hand_shaped():
 
 
 def _class_trace(seed, T=90, n_parts=9, noncontig=False, bad=False):
-    """Partitions as consecutive launch-order runs; some copy the (name,
-    stream) sequence of an earlier one, some differ in one stream or name."""
-    rng = np.random.default_rng(seed)
-    tr = cases.random_trace(seed, T=T, S=3, n_names=4, seq_gaps=seed % 2 == 0)
-    order = np.argsort(tr["seq"], kind="stable")
-    L = T // (n_parts + 1)
-    part_seq = np.full(T, -1, np.int32)
-    name_seq = tr["name_id"][order].copy()
-    st_seq = tr["stream_id"][order].copy()
-    for p in range(n_parts):
-        a = p * L + 2
-        part_seq[a:a + L] = p
-        src = int(rng.integers(0, p + 1))
-        if src < p and rng.random() < 0.7:
-            b = src * L + 2
-            name_seq[a:a + L] = name_seq[b:b + L]
-            st_seq[a:a + L] = st_seq[b:b + L]
-            if rng.random() < 0.3:  # a near copy: one stream differs
-                st_seq[a + int(rng.integers(0, L))] ^= 1
-    if noncontig:
-        part_seq[2 * L + 2 + L // 2] = -1  # a hole in partition 2
-    if bad:
-        name_seq[5 * L + 3] = tr["n_names"] + 1  # a launch with a bad name
-    tr["part_id"] = np.empty(T, np.int32)
-    tr["part_id"][order] = part_seq
-    tr["name_id"] = tr["name_id"].copy()
-    tr["name_id"][order] = name_seq
-    tr["stream_id"] = tr["stream_id"].copy()
-    tr["stream_id"][order] = st_seq
-    tr["n_parts"] = n_parts
-    tr["part_rep"] = None
-    return tr
+    return cases.class_trace(seed, T=T, n_parts=n_parts, noncontig=noncontig, bad=bad)
 
 
 @pytest.mark.parametrize("seed", range(10))
@@ -430,6 +399,21 @@ def test_dedup_classes_match_brute_force(seed):
     rep, has_noncontig = brute.dedup_classes(tr)
     np.testing.assert_array_equal(out["part_rep"], rep)
     assert bool(out["diag"]["flags"] & 16) == has_noncontig
+
+
+def test_dedup_classes_empty_partitions_form_one_class():
+    """Partitions without launches all have the empty sequence."""
+    tr = _class_trace(4)
+    part = tr["part_id"].copy()
+    part[(part == 3) | (part == 5)] = -1
+    tr["part_id"] = part
+    out = O.dedup_classes(tr)
+    rep, _ = brute.dedup_classes(tr)
+    np.testing.assert_array_equal(out["part_rep"], rep)
+    assert out["part_rep"][5] == 3 and out["part_rep"][3] == 3
+    empty = cases.random_trace(0, T=0, S=1, n_names=2)
+    empty.update(part_id=np.zeros(0, np.int32), n_parts=3, part_rep=None)
+    np.testing.assert_array_equal(O.dedup_classes(empty)["part_rep"], [0, 0, 0])
 
 
 def test_dedup_classes_duplicate_seq_ties_by_index():
