@@ -309,12 +309,10 @@ static int cmp_part_seq(const void *x, const void *y) {
 int oref_dedup_classes(const oref_kernels *k, const oref_dims *d, int32_t *part_rep,
                        oref_diag *diag) {
   if (!k || !d || !diag || k->n < 0 || (d->n_parts > 0 && !part_rep)) return OREF_ERR_ARG;
-  if (k->n > 0 && (!k->seq || !k->name_id || !k->stream_id)) return OREF_ERR_ARG;
+  if (k->n > 0 && (!k->seq || !k->name_id || !k->stream_id || !k->part_id)) return OREF_ERR_ARG;
   const int64_t T = k->n;
   const uint32_t NP = d->n_parts;
   if (NP == 0) return 0;
-  for (uint32_t q = 0; q < NP; ++q) part_rep[q] = (int32_t)q;
-  if (!k->part_id) return 0;
 
   /* a launch takes part with an in-range name and partition */
   for (int64_t i = 0; i < T; ++i) {

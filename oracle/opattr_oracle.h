@@ -135,7 +135,9 @@ int oref_aggregate(const oref_kernels *k, const oref_profiled *p,
    (part_rep[q], n_parts entries; d->part_rep is not read). Launches with a
    name or partition out of range take no part. A partition whose launches
    are not consecutive in launch order is its own class and raises
-   PARTITION; equal seq values raise ORDER (ranks then tie by index). */
+   PARTITION; equal seq values raise ORDER (ranks then tie by index).
+   Partitions without launches share the empty sequence: one class. part_id
+   is required when k->n > 0. */
 int oref_dedup_classes(const oref_kernels *k, const oref_dims *d, int32_t *part_rep,
                        oref_diag *diag);
 
