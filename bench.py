@@ -133,6 +133,95 @@ def cpu_baseline(tr, reps=2):
                       f"{med:.2f} s, single-threaded C oracle"}
 
 
+def _events(n):
+    import torch
+
+    row = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+    for e in row:
+        e.record()  # materialise the HIP event before handing it over
+    return row
+
+
+def measure_next_rows(dt, tr, flags, steps, warmup, out, ws):
+    """The rows beyond the core hot path that this library also runs, timed on
+    the same trace after the headline measurement: the attribution with the
+    kind-aware walk of Alg. 2 (outermost ranges as boundaries, a fifth of the
+    others skipped), and layer class discovery (Sec. 3.7)."""
+    import torch
+
+    from paper_2609_11938_amd import opattr, tracegen
+
+    T, R = tr["seq"].size, tr["r_start"].size
+    NP = tr.get("n_parts", 0) or 0
+    rows = {}
+
+    kinds = tracegen.with_range_kinds(tr)["r_kind"]
+    dtk = dict(dt, r_kind=torch.from_numpy(kinds).to(dt["seq"].device))
+
+    def walk_step():
+        opattr.opattr_attribute(dtk, flags=flags, outputs=out, ws=ws, raise_strict=False)
+
+    for _ in range(warmup):
+        walk_step()
+    torch.cuda.synchronize()
+    diag = opattr.read_diag(out["diag"])
+    if diag["status"] != 0:
+        raise SystemExit(f"attribution with range kinds reported {diag}")
+    pm = opattr.PROBES.index("main_pass")
+    ev = [_events(2) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        only = [None] * (2 * len(opattr.PROBES))
+        only[2 * pm], only[2 * pm + 1] = ev[k]
+        opattr.set_probe_events(only)
+        walk_step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    opattr.set_probe_events(None)
+    ms = (t1 - t0) * 1e3 / steps
+    enc_ms = statistics.mean(a.elapsed_time(b) for a, b in ev)
+    # k_enclose with kinds: stream, query point in, range id out; range
+    # starts, ends, parents and kinds
+    enc_bytes = T * (2 + 8 + 4) + R * (8 + 8 + 4 + 1)
+    enc_gbps = enc_bytes / (enc_ms * 1e-3) / 1e9
+    rows["enclose_walk"] = {
+        "call": "opattr_attribute, ranges with kinds", "ms_per_step": ms,
+        "records_per_s": T / (ms * 1e-3), "boundaries": int((kinds == 1).sum()),
+        "skipped": int((kinds == 2).sum()), "kernel": "k_enclose", "kernel_ms": enc_ms,
+        "kernel_algorithmic_bytes": enc_bytes, "kernel_GBps": enc_gbps,
+        "kernel_frac": enc_gbps / HBM_PEAK_GBPS}
+
+    if NP:
+        cflags = flags & (opattr.SEQ_DENSE | opattr.VALIDATE)
+        res = None
+        for _ in range(warmup):
+            res = opattr.opattr_dedup_classes(dt, flags=cflags, ws=ws)
+        torch.cuda.synchronize()
+        diag = opattr.read_diag(res["diag"])
+        if diag["status"] != 0:
+            raise SystemExit(f"class discovery reported {diag}")
+        n_classes = int(torch.unique(res["part_rep"]).numel())
+        ev = [_events(2) for _ in range(steps)]
+        torch.cuda.synchronize()
+        for k in range(steps):
+            ev[k][0].record()
+            opattr.opattr_dedup_classes(dt, flags=cflags, ws=ws)
+            ev[k][1].record()
+        torch.cuda.synchronize()
+        cls_ms = statistics.mean(a.elapsed_time(b) for a, b in ev)
+        # every launch's seq, name, stream and partition read once; the class
+        # map written once
+        cls_bytes = T * (4 + 4 + 2 + 4) + 4 * NP
+        gbps = cls_bytes / (cls_ms * 1e-3) / 1e9
+        rows["dedup_classes"] = {
+            "call": "opattr_dedup_classes", "ms_per_call": cls_ms,
+            "records_per_s": T / (cls_ms * 1e-3), "partitions": int(NP),
+            "classes": n_classes, "algorithmic_bytes": cls_bytes, "achieved_GBps": gbps,
+            "frac": gbps / HBM_PEAK_GBPS}
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -143,6 +232,8 @@ def main():
                     choices=["stream_major", "seq", "shuffled"])
     ap.add_argument("--validate", action="store_true", help="also check the layout hints")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-next-rows", action="store_true",
+                    help="skip timing the walk with range kinds and class discovery")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -203,13 +294,7 @@ def main():
     nprobe = len(opattr.PROBES)
     total_bytes, kbytes = algorithmic_bytes(tr)
 
-    def new_events(n):
-        row = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
-        for e in row:
-            e.record()  # materialise the HIP event before handing it over
-        return row
-
-    ev_all = [new_events(2 * nprobe) for _ in range(args.steps)]
+    ev_all = [_events(2 * nprobe) for _ in range(args.steps)]
     torch.cuda.synchronize()
     for k in range(args.steps):
         opattr.set_probe_events(ev_all[k])
@@ -223,7 +308,7 @@ def main():
     dominant = max(kbytes, key=lambda n: probe_ms[n])
     pdom = opattr.PROBES.index(dominant)
 
-    ev_dom = [new_events(2) for _ in range(args.steps)]
+    ev_dom = [_events(2) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for k in range(args.steps):
@@ -268,6 +353,8 @@ def main():
                      "frac_of_hbm_peak": pipe_gbps / HBM_PEAK_GBPS,
                      "probe_ms_untimed_pass": probe_ms},
     }
+    if not args.no_next_rows:
+        line["next_rows"] = measure_next_rows(dt, tr, flags, args.steps, args.warmup, out, ws)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(tr)
     print(json.dumps(line), flush=True)

@@ -128,11 +128,9 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.part = b.take((size_t)pl.max_chunks * 200);
   // class discovery: per partition, and the key table
   const size_t NPc = d->n_parts, TS = (size_t)class_table_slots(d->n_parts);
-  pl.c_cnt = b.take(NPc * 4);
-  pl.c_lo = b.take(NPc * 4);
-  pl.c_hi = b.take(NPc * 4);
-  pl.c_cc = b.take(NPc * 4);
-  pl.c_off = b.take(NPc * 4);
+  pl.c_first = b.take(NPc * 4);
+  pl.c_last = b.take(NPc * 4);
+  pl.c_runs = b.take(NPc * 4);
   pl.c_key = b.take(NPc * 8);
   pl.c_cand = b.take(NPc * 4);
   pl.c_fail = b.take(NPc * 4);
@@ -392,10 +390,9 @@ int opattr_dedup_classes(const opattr_kernels *k, const opattr_dims *d, int32_t 
   hipStream_t s = (hipStream_t)stream;
   check_kernel_layout(k, d, diag, s);
   if (d->n_parts > 0) {
-    // launch-order ranks: sorted when seq is not promised dense; a dense seq
-    // is checked only under OPATTR_VALIDATE
-    const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
-    if (!pl.seq_dense || validate) build_seq_view(k, d, ws, pl, diag, validate, s);
+    // the launch-order view: sorted when seq is not promised dense; a dense
+    // seq is checked only under OPATTR_VALIDATE
+    build_seq_view(k, d, ws, pl, diag, (d->flags & OPATTR_VALIDATE) != 0, s);
     run_classes(k, d, part_rep, diag, ws, pl, s);
   }
   launch_finish(diag, nullptr, 0, s);

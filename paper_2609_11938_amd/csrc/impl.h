@@ -46,7 +46,7 @@ struct Plan {
   int64_t cap_items, cap_rows, max_chunks;
   size_t wi, wr, hmb, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, coff, cmap, sit, part;
   // dedup class discovery
-  size_t c_cnt, c_lo, c_hi, c_cc, c_off, c_key, c_cand, c_fail, c_list, c_tkey, c_tmin;
+  size_t c_first, c_last, c_runs, c_key, c_cand, c_fail, c_list, c_tkey, c_tmin;
   size_t misc;  // small device scalars
 };
 
@@ -162,7 +162,7 @@ inline thread_local int g_class_key_bits = 64;
 // slots of the key table for NP partitions (a power of two >= 2 NP)
 int64_t class_table_slots(uint32_t NP);
 // part_rep[NP] from the partitions' (name, stream) sequences in launch order;
-// needs the launch-order ranks (build_seq_view) unless seq is dense
+// needs the launch-order view (build_seq_view)
 void run_classes(const opattr_kernels *k, const opattr_dims *d, int32_t *part_rep,
                  opattr_diag *diag, void *ws, const Plan &pl, hipStream_t s);
 

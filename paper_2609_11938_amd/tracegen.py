@@ -549,3 +549,28 @@ def summary(tr) -> dict:
     return dict(T=int(tr["seq"].size), P=int(tr["pf_name"].size), R=int(tr["r_start"].size),
                 n_names=tr["n_names"], n_streams=tr["n_streams"], n_ops=tr["n_ops"],
                 n_parts=tr["n_parts"])
+
+
+def with_range_kinds(tr, seed=5, p_skip=0.2):
+    """A copy of ``tr`` whose ranges carry enclosure-walk kinds (r_kind u8):
+    every outermost range of its stream (contained in no other, like a
+    profiler step) is a boundary (1); of the others a fraction ``p_skip`` is
+    skipped (2, namespaces the walk passes over) and the rest are operators
+    (0)."""
+    rng = _rng(seed)
+    R = tr["r_start"].size
+    kind = np.where(rng.random(R) < p_skip, 2, 0).astype(np.uint8)
+    if R:
+        rs, re, st = tr["r_start"], tr["r_end"], tr["r_stream"]
+        order = np.lexsort((np.arange(R), -re.astype(np.int64), rs, st))
+        st_o, re_o = st[order], re[order].astype(np.int64)
+        cuts = np.flatnonzero(np.diff(st_o.astype(np.int64))) + 1
+        root = np.zeros(R, dtype=bool)
+        for a, b in zip(np.r_[0, cuts], np.r_[cuts, R]):
+            seg = re_o[a:b]
+            prev = np.maximum.accumulate(np.r_[np.int64(-1), seg[:-1]])
+            root[a:b] = seg > prev  # ends beyond every earlier range of the stream
+        kind[order[root]] = 1
+    out = dict(tr)
+    out["r_kind"] = kind
+    return out
