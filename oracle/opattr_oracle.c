@@ -541,15 +541,11 @@ static const uint8_t DEFAULT_KIND[OREF_NC] = {
     OREF_DWMEAN, OREF_DWMEAN, OREF_DWMEAN, OREF_SUM, OREF_DWMEAN, OREF_DWMEAN,
     OREF_DWMEAN, OREF_SUM, OREF_DWMEAN, OREF_DWMEAN, OREF_MAX, OREF_SUM, OREF_MAX};
 
-int oref_aggregate(const oref_kernels *k, const oref_profiled *p,
-                   const int32_t *match, const int32_t *range_id,
-                   const oref_ranges *r, const oref_dims *d, const uint8_t *agg_kind,
-                   oref_row *table, oref_summary *sum, oref_diag *diag) {
-  if (!k || !p || !match || !range_id || !r || !d || !table || !sum || !diag) return OREF_ERR_ARG;
-  if (k->n < 0 || (k->n > 0 && !k->dur_ns)) return OREF_ERR_ARG;
-  const uint8_t *kind = agg_kind ? agg_kind : DEFAULT_KIND;
-  for (int c = 0; c < OREF_NC; ++c)
-    if (kind[c] > OREF_MAX) return OREF_ERR_ARG;
+/* Eq. 1 per operator row: row_of[i] is the row of kernel i (n_ops =
+   UNATTRIBUTED) */
+static int aggregate_rows(const oref_kernels *k, const oref_profiled *p, const int32_t *match,
+                          const uint32_t *row_of, const oref_dims *d, const uint8_t *kind,
+                          oref_row *table, oref_summary *sum, oref_diag *diag) {
   const int64_t T = k->n;
   const uint32_t G = d->n_ops + 1; /* row n_ops is UNATTRIBUTED */
   nsum *acc = xcalloc((size_t)G * OREF_NC, sizeof(nsum));
@@ -558,11 +554,7 @@ int oref_aggregate(const oref_kernels *k, const oref_profiled *p,
   memset(table, 0, sizeof(oref_row) * G);
 
   for (int64_t i = 0; i < T; ++i) {
-    int32_t rid = range_id[i];
-    uint32_t g = d->n_ops;
-    if (rid >= 0 && rid < r->n && r->op_id[rid] < d->n_ops) g = r->op_id[rid];
-    else if (rid < -1 || rid >= r->n || (rid >= 0 && r->op_id[rid] >= d->n_ops))
-      diag->bad_records++;
+    const uint32_t g = row_of[i];
     oref_row *row = &table[g];
     uint64_t dur = k->dur_ns[i];
     row->kernel_count++;
@@ -603,6 +595,128 @@ int oref_aggregate(const oref_kernels *k, const oref_profiled *p,
   sum->attributed_fraction =
       sum->total_ns ? (double)sum->attributed_ns / (double)sum->total_ns : NAN;
   free(acc); free(mx);
+  return 0;
+}
+
+static const uint8_t *agg_kinds(const uint8_t *agg_kind) {
+  const uint8_t *kind = agg_kind ? agg_kind : DEFAULT_KIND;
+  for (int c = 0; c < OREF_NC; ++c)
+    if (kind[c] > OREF_MAX) return NULL;
+  return kind;
+}
+
+int oref_aggregate(const oref_kernels *k, const oref_profiled *p,
+                   const int32_t *match, const int32_t *range_id,
+                   const oref_ranges *r, const oref_dims *d, const uint8_t *agg_kind,
+                   oref_row *table, oref_summary *sum, oref_diag *diag) {
+  if (!k || !p || !match || !range_id || !r || !d || !table || !sum || !diag) return OREF_ERR_ARG;
+  if (k->n < 0 || (k->n > 0 && !k->dur_ns)) return OREF_ERR_ARG;
+  const uint8_t *kind = agg_kinds(agg_kind);
+  if (!kind) return OREF_ERR_ARG;
+  /* the operator row of a kernel: the op of its range (Alg. 2 output) */
+  uint32_t *row_of = xcalloc((size_t)k->n, sizeof(uint32_t));
+  for (int64_t i = 0; i < k->n; ++i) {
+    const int32_t rid = range_id[i];
+    row_of[i] = d->n_ops;
+    if (rid >= 0 && rid < r->n && r->op_id[rid] < d->n_ops) row_of[i] = r->op_id[rid];
+    else if (rid < -1 || rid >= r->n || (rid >= 0 && r->op_id[rid] >= d->n_ops))
+      diag->bad_records++;
+  }
+  const int rc = aggregate_rows(k, p, match, row_of, d, kind, table, sum, diag);
+  free(row_of);
+  return rc;
+}
+
+int oref_aggregate_ops(const oref_kernels *k, const oref_profiled *p, const int32_t *match,
+                       const int32_t *op, const oref_dims *d, const uint8_t *agg_kind,
+                       oref_row *table, oref_summary *sum, oref_diag *diag) {
+  if (!k || !p || !match || !op || !d || !table || !sum || !diag) return OREF_ERR_ARG;
+  if (k->n < 0 || (k->n > 0 && !k->dur_ns)) return OREF_ERR_ARG;
+  const uint8_t *kind = agg_kinds(agg_kind);
+  if (!kind) return OREF_ERR_ARG;
+  uint32_t *row_of = xcalloc((size_t)k->n, sizeof(uint32_t));
+  for (int64_t i = 0; i < k->n; ++i) {
+    const int32_t o = op[i];
+    row_of[i] = (o >= 0 && (uint32_t)o < d->n_ops) ? (uint32_t)o : d->n_ops;
+    if (o < -1 || (o >= 0 && (uint32_t)o >= d->n_ops)) diag->bad_records++;
+  }
+  const int rc = aggregate_rows(k, p, match, row_of, d, kind, table, sum, diag);
+  free(row_of);
+  return rc;
+}
+
+/* ----------------------------------------------------------------------- */
+/* Tiered attribution (Table "tiers", decision-tree figure, Sec. 3.4-3.6)    */
+/* ----------------------------------------------------------------------- */
+
+int oref_tiers(const oref_kernels *k, const oref_corr *corr, const oref_fusion *fm,
+               const oref_ranges *r, const oref_dims *d, int corr_policy,
+               const int32_t *range_id, const uint8_t *walk_fused, uint8_t *tier, int32_t *op,
+               uint8_t *fused, oref_coverage *cov, oref_diag *diag) {
+  if (!k || !r || !d || !diag || !cov || k->n < 0 || corr_policy < 0 || corr_policy > 2)
+    return OREF_ERR_ARG;
+  const int64_t T = k->n;
+  if (T > 0 && (!k->name_id || !k->dur_ns || !range_id || !tier || !op || !fused))
+    return OREF_ERR_ARG;
+  if (corr && (corr->n < 0 || (corr->n > 0 && (!corr->name_id || !corr->op_id)))) return OREF_ERR_ARG;
+  if (corr && T > 0 && !k->seq) return OREF_ERR_ARG;
+  if (fm && (!fm->off || !fm->op_id)) return OREF_ERR_ARG;
+  const uint32_t NN = d->n_names, NOPS = d->n_ops;
+
+  /* HIGH: the correlation map gives, per kernel name, the operator of each
+     invocation index; a kernel's index is its rank among all launches of its
+     name in launch order, every launch counting (the correlation pass runs
+     the whole model, so layer dedup does not apply). This is Alg. 1 with
+     the map's entries in place of the profiled rows. */
+  int32_t *entry = xcalloc((size_t)T, sizeof(int32_t));
+  for (int64_t i = 0; i < T; ++i) entry[i] = -1;
+  if (corr) {
+    oref_kernels kk = *k;
+    kk.part_id = NULL;
+    oref_dims dd = *d;
+    dd.part_rep = NULL;
+    dd.n_parts = 0;
+    oref_profiled pc = {corr->n, corr->name_id, NULL, 0, 0, 0};
+    const int rc = oref_match(&kk, &pc, &dd, corr_policy, entry, NULL, diag);
+    if (rc) { free(entry); return rc; }
+    for (int64_t j = 0; j < corr->n; ++j)
+      if (corr->op_id[j] < -1 || (corr->op_id[j] >= 0 && (uint32_t)corr->op_id[j] >= NOPS))
+        diag->bad_records++;
+  }
+
+  memset(cov, 0, sizeof(*cov));
+  for (int64_t i = 0; i < T; ++i) {
+    const uint32_t nm = k->name_id[i];
+    int t = OREF_TIER_UNATTRIBUTED;
+    int32_t o = -1;
+    const int32_t e = entry[i];
+    const int32_t rid = range_id[i];
+    if (rid < -1 || rid >= r->n) diag->bad_records++;
+    int64_t nf = 0; /* operators the fusion map lists for this kernel name */
+    if (fm && nm < NN && fm->off[nm + 1] > fm->off[nm]) nf = (int64_t)fm->off[nm + 1] - fm->off[nm];
+    if (e >= 0 && corr->op_id[e] >= 0 && (uint32_t)corr->op_id[e] < NOPS) {
+      t = OREF_TIER_HIGH; /* pre-empts the enclosure and the fusion map */
+      o = corr->op_id[e];
+    } else if (rid >= 0 && rid < r->n) {
+      t = OREF_TIER_NVTX; /* the enclosure walk's operator range */
+      o = (int32_t)r->op_id[rid];
+    } else if (nf > 0 && fm->op_id[fm->off[nm]] >= 0 && (uint32_t)fm->op_id[fm->off[nm]] < NOPS) {
+      t = OREF_TIER_FUSION; /* no enclosing op range: the fused kernel's first operator */
+      o = fm->op_id[fm->off[nm]];
+    }
+    tier[i] = (uint8_t)t;
+    op[i] = o;
+    /* the fusion map augments every tier: more than one listed operator
+       marks the kernel fused, as does more than one enclosing op range */
+    fused[i] = (uint8_t)(((walk_fused && walk_fused[i]) || nf > 1) ? 1 : 0);
+    cov->count[t]++;
+    cov->ns[t] += k->dur_ns[i];
+  }
+  uint64_t total = 0;
+  for (int t = 0; t < 4; ++t) total += cov->ns[t];
+  for (int t = 0; t < 4; ++t) cov->frac[t] = total ? (double)cov->ns[t] / (double)total : NAN;
+  if (diag->bad_records) diag->flags |= OREF_F_DATA;
+  free(entry);
   return 0;
 }
 

@@ -129,6 +129,56 @@ int oref_aggregate(const oref_kernels *k, const oref_profiled *p,
                    const int32_t *match, const int32_t *range_id,
                    const oref_ranges *r, const oref_dims *d, const uint8_t *agg_kind,
                    oref_row *table, oref_summary *sum, oref_diag *diag);
+/* Eq. 1 with the operator row of each kernel given (op[i] in [0, n_ops), -1
+   = UNATTRIBUTED; other values are bad records and go to UNATTRIBUTED). */
+int oref_aggregate_ops(const oref_kernels *k, const oref_profiled *p, const int32_t *match,
+                       const int32_t *op, const oref_dims *d, const uint8_t *agg_kind,
+                       oref_row *table, oref_summary *sum, oref_diag *diag);
+
+/* Correlation map of the torch.profiler pass (Sec. 3.4): entry j says that
+   one invocation of kernel name name_id[j] was launched by operator op_id[j]
+   (-1: none recorded); the entries of a name are its invocation indices 0,
+   1, ... in array order. */
+typedef struct {
+  int64_t n;
+  const uint32_t *name_id;
+  const int32_t *op_id;
+} oref_corr;
+
+/* Inductor fusion map (Sec. 3.6): for kernel name n, the operators fused
+   into it are op_id[off[n] .. off[n+1]), the first one primary. off has
+   n_names + 1 entries; a decreasing pair reads as an empty list. */
+typedef struct {
+  const uint32_t *off;
+  const int32_t *op_id;
+} oref_fusion;
+
+/* Attribution tiers (Table "tiers", decision-tree figure). */
+enum { OREF_TIER_UNATTRIBUTED = 0, OREF_TIER_HIGH = 1, OREF_TIER_NVTX = 2, OREF_TIER_FUSION = 3 };
+
+/* kernels and nanoseconds per tier; frac = share of all kernel runtime (NaN
+   when there is none) */
+typedef struct {
+  uint64_t count[4], ns[4];
+  double frac[4];
+} oref_coverage;
+
+/* Tiered attribution. Per kernel, in order: HIGH when the correlation map
+   has an entry with a valid operator for (name, invocation index), the index
+   being the kernel's rank among all launches of its name in launch order
+   (Alg. 1 over the map's entries under corr_policy; partitions play no
+   part); NVTX when the enclosure walk found an op range (range_id, from
+   oref_enclose_walk); FUSION when the fusion map lists operators for its
+   name and the first is valid; else UNATTRIBUTED. op = the operator chosen
+   (-1 for UNATTRIBUTED). fused = walk_fused (optional) or more than one
+   operator listed for the name. corr and fm may be NULL. Map entries with
+   an operator outside [-1, n_ops) and range ids outside [-1, r->n) are bad
+   records. */
+int oref_tiers(const oref_kernels *k, const oref_corr *corr, const oref_fusion *fm,
+               const oref_ranges *r, const oref_dims *d, int corr_policy,
+               const int32_t *range_id, const uint8_t *walk_fused, uint8_t *tier, int32_t *op,
+               uint8_t *fused, oref_coverage *cov, oref_diag *diag);
+
 /* Dedup class discovery (Sec. 3.7): partitions whose launches form the same
    sequence of (name, stream) in launch order are structural duplicates; each
    gets as representative the lowest-numbered partition of its class

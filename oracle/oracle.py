@@ -87,6 +87,21 @@ class Summary(C.Structure):
                 ("attributed_fraction", C.c_double)]
 
 
+class Corr(C.Structure):
+    _fields_ = [("n", C.c_int64), ("name_id", C.c_void_p), ("op_id", C.c_void_p)]
+
+
+class Fusion(C.Structure):
+    _fields_ = [("off", C.c_void_p), ("op_id", C.c_void_p)]
+
+
+class Coverage(C.Structure):
+    _fields_ = [("count", C.c_uint64 * 4), ("ns", C.c_uint64 * 4), ("frac", C.c_double * 4)]
+
+
+# attribution tiers (Table "tiers")
+TIER_UNATTRIBUTED, TIER_HIGH, TIER_NVTX, TIER_FUSION = 0, 1, 2, 3
+
 ROW_DTYPE = np.dtype([("kernel_count", "<u8"), ("total_ns", "<u8"),
                       ("matched_count", "<u8"), ("matched_ns", "<u8"),
                       ("value", "<f8", (NC,))])
@@ -110,9 +125,14 @@ def load(path: str):
     L.oref_enclose_walk.argtypes = [P(Kernels), P(Ranges), P(Dims), C.c_void_p, C.c_void_p,
                                     C.c_void_p, C.c_void_p, C.c_void_p, P(Diag)]
     L.oref_dedup_classes.argtypes = [P(Kernels), P(Dims), C.c_void_p, P(Diag)]
+    L.oref_aggregate_ops.argtypes = [P(Kernels), P(Profiled), C.c_void_p, C.c_void_p, P(Dims),
+                                     C.c_void_p, C.c_void_p, P(Summary), P(Diag)]
+    L.oref_tiers.argtypes = [P(Kernels), P(Corr), P(Fusion), P(Ranges), P(Dims), C.c_int,
+                             C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                             P(Coverage), P(Diag)]
     L.oref_diag_finish.argtypes = [P(Diag), C.c_int]
     for f in ("oref_match", "oref_dedup", "oref_enclose", "oref_enclose_walk", "oref_aggregate",
-              "oref_dedup_classes"):
+              "oref_dedup_classes", "oref_aggregate_ops", "oref_tiers"):
         getattr(L, f).restype = C.c_int
     return L
 
@@ -272,3 +292,75 @@ def dedup_classes(tr, library=None):
         raise ValueError(f"oref_dedup_classes: {rc}")
     L.oref_diag_finish(C.byref(dg), PREFIX)
     return {"part_rep": rep, "diag": diag_dict(dg)}
+
+
+def _maps(tr):
+    """ctypes views of the correlation map (corr_name, corr_op) and the
+    fusion map (fmap_off, fmap_op) of a trace dict; absent maps give NULL."""
+    keep = []
+    corr = None
+    if tr.get("corr_name") is not None:
+        cn, co = _c(tr["corr_name"], np.uint32), _c(tr["corr_op"], np.int32)
+        keep += [cn, co]
+        corr = Corr(cn.size, _ptr(cn), _ptr(co))
+    fm = None
+    if tr.get("fmap_off") is not None:
+        fo, fop = _c(tr["fmap_off"], np.uint32), _c(tr["fmap_op"], np.int32)
+        if fop.size == 0:
+            fop = np.zeros(1, np.int32)  # a valid pointer for an empty list
+        keep += [fo, fop]
+        fm = Fusion(_ptr(fo), _ptr(fop))
+    return corr, fm, keep
+
+
+def _coverage_dict(cv: Coverage) -> dict:
+    return {"count": np.array(cv.count[:], dtype=np.uint64),
+            "ns": np.array(cv.ns[:], dtype=np.uint64),
+            "frac": np.array(cv.frac[:], dtype=np.float64)}
+
+
+def tiers(tr, corr_policy=SKIP_NAME, library=None):
+    """Tiered attribution (Table "tiers", decision-tree figure): the
+    enclosure walk of Alg. 2, then per kernel the tier (HIGH from the
+    correlation map, NVTX from the walk, FUSION from the fusion map,
+    UNATTRIBUTED), its operator, the fused flag, and per-tier coverage."""
+    L = library if library is not None else lib()
+    walk = enclose_walk(tr, library=L)
+    x = _Inputs(tr)
+    T = x.seq.size
+    corr, fm, keep = _maps(tr)
+    tier = np.empty(T, dtype=np.uint8)
+    op = np.empty(T, dtype=np.int32)
+    fused = np.empty(T, dtype=np.uint8)
+    cv = Coverage()
+    dg = Diag()
+    rc = L.oref_tiers(C.byref(x.k), C.byref(corr) if corr is not None else None,
+                      C.byref(fm) if fm is not None else None, C.byref(x.r), C.byref(x.d),
+                      corr_policy, _ptr(walk["range_id"]), _ptr(walk["fused"]), _ptr(tier),
+                      _ptr(op), _ptr(fused), C.byref(cv), C.byref(dg))
+    del keep
+    if rc:
+        raise ValueError(f"oref_tiers: {rc}")
+    L.oref_diag_finish(C.byref(dg), corr_policy)
+    return {"range_id": walk["range_id"], "walk_fused": walk["fused"], "tier": tier, "op": op,
+            "fused": fused, "coverage": _coverage_dict(cv), "diag": diag_dict(dg)}
+
+
+def aggregate_ops(tr, match, op, agg_kind=None, absent_mask=0, library=None):
+    """Eq. 1 with the operator of every kernel given (``op``, -1 =
+    UNATTRIBUTED)."""
+    L = library if library is not None else lib()
+    x = _Inputs(tr, absent_mask)
+    match = np.ascontiguousarray(match, dtype=np.int32)
+    op = np.ascontiguousarray(op, dtype=np.int32)
+    table = np.zeros(tr["n_ops"] + 1, dtype=ROW_DTYPE)
+    sm = Summary()
+    dg = Diag()
+    kind = None if agg_kind is None else np.ascontiguousarray(agg_kind, dtype=np.uint8)
+    rc = L.oref_aggregate_ops(C.byref(x.k), C.byref(x.p), _ptr(match), _ptr(op), C.byref(x.d),
+                              _ptr(kind), _ptr(table), C.byref(sm), C.byref(dg))
+    if rc:
+        raise ValueError(f"oref_aggregate_ops: {rc}")
+    L.oref_diag_finish(C.byref(dg), PREFIX)
+    return {"table": table, "summary": {f: getattr(sm, f) for f, _ in Summary._fields_},
+            "diag": diag_dict(dg)}

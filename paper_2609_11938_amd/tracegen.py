@@ -574,3 +574,67 @@ def with_range_kinds(tr, seed=5, p_skip=0.2):
     out = dict(tr)
     out["r_kind"] = kind
     return out
+
+
+def with_attribution_maps(tr, seed=7, p_corr=0.4, p_mismatch=0.1, p_none=0.02, p_fmap=0.3,
+                          max_fused=3, p_bad=0.0, shuffle=False):
+    """A copy of ``tr`` with the two maps of the tiered attribution:
+
+    * a correlation map (``corr_name`` u32, ``corr_op`` i32), as the
+      torch.profiler pass would record it: for a fraction ``p_corr`` of the
+      kernel names, one entry per launch in launch order, whose operator is
+      the op of the launch's planted range (a random op where there is none);
+      a fraction ``p_none`` of the entries record no operator (-1); for a
+      fraction ``p_mismatch`` of those names the last entry is missing (a
+      count mismatch); ``shuffle`` interleaves the names at random while
+      keeping each name's entries in order;
+    * a fusion map (``fmap_off`` u32[n_names + 1], ``fmap_op`` i32): for a
+      fraction ``p_fmap`` of the names, 1..``max_fused`` random operators.
+
+    ``p_bad`` of the map entries get an operator id out of range."""
+    rng = _rng(seed)
+    NN, NOPS = int(tr["n_names"]), int(tr["n_ops"])
+    T = tr["seq"].size
+    name = np.asarray(tr["name_id"])
+    order = np.lexsort((np.arange(T), tr["seq"]))
+    order = order[name[order] < NN]
+    nm = name[order].astype(np.int64)
+    op = rng.integers(0, max(NOPS, 1), size=order.size).astype(np.int64)
+    pl = tr.get("planted_range")
+    if pl is not None and order.size:
+        pr = np.asarray(pl)[order]
+        op = np.where(pr >= 0, np.asarray(tr["r_op"], dtype=np.int64)[np.maximum(pr, 0)], op)
+    covered = rng.random(NN) < p_corr
+    keep = covered[nm]
+    cn, co = nm[keep], op[keep]
+    co = np.where(rng.random(co.size) < p_none, -1, co)
+    mism = covered & (rng.random(NN) < p_mismatch)
+    last = np.full(NN, -1, dtype=np.int64)
+    if cn.size:
+        np.maximum.at(last, cn, np.arange(cn.size))
+    drop = last[mism]
+    sel = np.ones(cn.size, dtype=bool)
+    sel[drop[drop >= 0]] = False
+    cn, co = cn[sel], co[sel]
+    if shuffle and cn.size:
+        # a random order of the names, each name's entries still in order
+        names_new = cn[rng.permutation(cn.size)]
+        by_name = np.argsort(cn, kind="stable")
+        start = np.searchsorted(cn[by_name], names_new)
+        pos_new = np.argsort(names_new, kind="stable")
+        occ = np.empty(cn.size, dtype=np.int64)
+        occ[pos_new] = np.arange(cn.size) - np.searchsorted(names_new[pos_new], names_new[pos_new])
+        co = co[by_name][start + occ]
+        cn = names_new
+    if p_bad:
+        co = np.where(rng.random(co.size) < p_bad, NOPS + 3, co)
+    nf = np.where(rng.random(NN) < p_fmap, rng.integers(1, max_fused + 1, size=NN), 0)
+    off = np.zeros(NN + 1, dtype=np.uint32)
+    off[1:] = np.cumsum(nf)
+    fop = rng.integers(0, max(NOPS, 1), size=int(off[-1])).astype(np.int64)
+    if p_bad:
+        fop = np.where(rng.random(fop.size) < p_bad, -5, fop)
+    out = dict(tr)
+    out.update(corr_name=cn.astype(np.uint32), corr_op=co.astype(np.int32), fmap_off=off,
+               fmap_op=fop.astype(np.int32))
+    return out

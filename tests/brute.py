@@ -274,3 +274,54 @@ def aggregate(tr, match, range_id, agg_kind=None, absent_mask=0):
         row["value"] = vals
         rows.append(row)
     return rows
+
+
+def tiers(tr, policy=1):
+    """The decision tree per kernel, from the definitions: the invocation
+    index of a launch is its rank among all launches of its (valid) name by
+    (seq, index); entry k of a name in the correlation map is its index k;
+    under policy 1 (SKIP_NAME) a name whose entry count differs from its
+    launch count has no entries. Then HIGH (entry with a valid operator), NVTX
+    (the walk's range), FUSION (first listed operator valid), UNATTRIBUTED.
+    Returns tier, op, fused and per-tier (count, ns)."""
+    T, NN, NOPS = tr["seq"].size, tr["n_names"], tr["n_ops"]
+    name = [int(v) for v in tr["name_id"]]
+    order = sorted(range(T), key=lambda i: (int(tr["seq"][i]), i))
+    index, launches = {}, {}
+    for i in order:
+        n = name[i]
+        if n < NN:
+            index[i] = launches.get(n, 0)
+            launches[n] = index[i] + 1
+    entries = {}
+    cn = tr.get("corr_name")
+    if cn is not None:
+        for j in range(cn.size):
+            if int(cn[j]) < NN:
+                entries.setdefault(int(cn[j]), []).append(int(tr["corr_op"][j]))
+    fo, fop = tr.get("fmap_off"), tr.get("fmap_op")
+    rid, wfused, _, _ = enclose_walk(tr)
+    tier = np.zeros(T, dtype=np.int64)
+    op = np.full(T, -1, dtype=np.int64)
+    fused = np.zeros(T, dtype=np.int64)
+    cnt, ns = [0] * 4, [0] * 4
+    for i in range(T):
+        n = name[i]
+        ent = None
+        if cn is not None and n < NN:
+            lst = entries.get(n, [])
+            if (policy != 1 or len(lst) == launches.get(n, 0)) and index[i] < len(lst):
+                ent = lst[index[i]]
+        fl = []
+        if fo is not None and n < NN and int(fo[n + 1]) > int(fo[n]):
+            fl = [int(v) for v in fop[int(fo[n]):int(fo[n + 1])]]
+        if ent is not None and 0 <= ent < NOPS:
+            tier[i], op[i] = 1, ent
+        elif rid[i] >= 0:
+            tier[i], op[i] = 2, int(tr["r_op"][rid[i]])
+        elif fl and 0 <= fl[0] < NOPS:
+            tier[i], op[i] = 3, fl[0]
+        fused[i] = 1 if (wfused[i] or len(fl) > 1) else 0
+        cnt[tier[i]] += 1
+        ns[tier[i]] += int(tr["dur_ns"][i])
+    return tier, op, fused, cnt, ns

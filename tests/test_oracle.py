@@ -615,3 +615,126 @@ def test_emission_orders_agree():
         np.testing.assert_array_equal(res[0], base[0])
         np.testing.assert_array_equal(res[1], base[1])
         _assert_rows(_table_dicts(res[2]), _table_dicts(base[2]), 1e-14)
+
+
+def _tier_trace(seed, T=120, dedup=False, shuffle=False, p_bad=0.0):
+    tr = cases.random_trace(500 + seed, T=T, R=40, S=2, t_max=80, max_depth=4, dedup=dedup)
+    tr = cases.with_kinds(tr, seed)
+    return tg.with_attribution_maps(tr, seed=seed, p_corr=0.6, p_mismatch=0.3, p_none=0.1,
+                                    p_fmap=0.5, p_bad=p_bad, shuffle=shuffle)
+
+
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("policy", [0, 1, 2])
+def test_tiers_match_brute_force(seed, policy):
+    """The decision tree written out per kernel (brute.tiers) against the
+    oracle: random traces with range kinds, partitions (which the
+    correlation index ignores), maps with missing entries, count mismatches,
+    interleaved names and bad operator ids."""
+    tr = _tier_trace(seed, dedup=seed % 2 == 0, shuffle=seed % 3 == 1,
+                     p_bad=0.05 if seed % 4 == 3 else 0.0)
+    out = O.tiers(tr, corr_policy=policy)
+    tier, op, fused, cnt, ns = brute.tiers(tr, 1 if policy == 1 else 0)
+    np.testing.assert_array_equal(out["tier"], tier)
+    np.testing.assert_array_equal(out["op"], op)
+    np.testing.assert_array_equal(out["fused"], fused)
+    assert list(out["coverage"]["count"]) == cnt and list(out["coverage"]["ns"]) == ns
+    assert out["coverage"]["ns"].sum() == tr["dur_ns"].astype(np.int64).sum()
+    assert math.isclose(out["coverage"]["frac"].sum(), 1.0, rel_tol=1e-12)
+    co = tr["corr_op"].astype(np.int64)
+    bad = int(((co < -1) | (co >= tr["n_ops"])).sum())
+    assert out["diag"]["bad_records"] == bad and bool(out["diag"]["flags"] & 1) == (bad > 0)
+    if policy == 2 and out["diag"]["flags"] & 64 and not bad:
+        assert out["diag"]["status"] == -4
+
+
+def test_tiers_decision_tree_example():
+    """One kernel per branch of the decision-tree figure, on one stream with
+    one op range around launches 0, 1 and 5:
+      0  name 0, invocation 0: map entry op 3 -> HIGH 3 (pre-empts the range);
+         the fusion map lists two ops for name 0 -> fused
+      1  name 1 (no map entries) inside the range -> NVTX, the range's op 1
+      2  name 2 outside the range, fusion map [4] -> FUSION 4, not fused
+      3  name 3 outside, nothing -> UNATTRIBUTED
+      4  name 2 again -> FUSION 4
+      5  name 0, invocation 1: the entry records no operator -> the range, NVTX 1
+    """
+    tr = cases.random_trace(0, T=6, S=1, n_names=4, R=1)
+    tr.update(seq=np.arange(6, dtype=np.uint32),
+              start_ns=np.array([10, 20, 50, 60, 70, 30], np.uint64),
+              dur_ns=np.array([1, 2, 4, 8, 16, 32], np.uint32),
+              stream_id=np.zeros(6, np.uint16), name_id=np.array([0, 1, 2, 3, 2, 0], np.uint32),
+              part_id=None, part_rep=None, query_ns=None,
+              r_start=np.array([5], np.uint64), r_end=np.array([40], np.uint64),
+              r_stream=np.zeros(1, np.uint16), r_op=np.array([1], np.uint32), r_kind=None,
+              n_ops=8, n_names=4, n_streams=1,
+              corr_name=np.array([0, 0], np.uint32), corr_op=np.array([3, -1], np.int32),
+              fmap_off=np.array([0, 2, 2, 3, 3], np.uint32), fmap_op=np.array([5, 6, 4], np.int32))
+    out = O.tiers(tr)
+    np.testing.assert_array_equal(out["tier"], [1, 2, 3, 0, 3, 2])
+    np.testing.assert_array_equal(out["op"], [3, 1, 4, -1, 4, 1])
+    np.testing.assert_array_equal(out["fused"], [1, 0, 0, 0, 0, 1])
+    np.testing.assert_array_equal(out["coverage"]["count"], [1, 1, 2, 2])
+    np.testing.assert_array_equal(out["coverage"]["ns"], [8, 1, 34, 20])
+    np.testing.assert_allclose(out["coverage"]["frac"], np.array([8, 1, 34, 20]) / 63)
+
+
+def test_tiers_full_correlation_map_is_all_high():
+    """A correlation map recorded from the same run for every name (no gaps,
+    no mismatches): every launch with a valid name is HIGH, with the op of
+    its planted innermost range where it has one."""
+    tr = tg.with_attribution_maps(tg.generate("tiny"), seed=3, p_corr=1.0, p_mismatch=0.0,
+                                  p_none=0.0, p_fmap=0.0)
+    out = O.tiers(tr)
+    assert np.all(out["tier"] == 1)
+    enc = tr["planted_range"] >= 0
+    np.testing.assert_array_equal(out["op"][enc], tr["r_op"][tr["planted_range"][enc]])
+    assert out["coverage"]["frac"][1] == 1.0 and out["diag"]["status"] == 0
+
+
+def test_tiers_without_maps_reduce_to_the_walk():
+    tr = cases.with_kinds(tg.generate("tiny"), 2)
+    out = O.tiers(tr)
+    walk = O.enclose_walk(tr)
+    rid = walk["range_id"]
+    np.testing.assert_array_equal(out["tier"], np.where(rid >= 0, 2, 0))
+    r_op = tr["r_op"].astype(np.int64)
+    np.testing.assert_array_equal(out["op"], np.where(rid >= 0, r_op[np.maximum(rid, 0)], -1))
+    np.testing.assert_array_equal(out["fused"], walk["fused"])
+
+
+def test_tiers_count_policies():
+    """Name 0 has 5 launches and 4 entries: PREFIX gives HIGH to its first
+    four invocations, SKIP_NAME to none of them, STRICT like PREFIX with
+    status COUNT_MISMATCH."""
+    tr = cases.random_trace(1, T=10, S=1, n_names=2, R=0)
+    tr.update(seq=np.arange(10, dtype=np.uint32), name_id=np.array([0, 1] * 5, np.uint32),
+              part_id=None, part_rep=None, n_ops=9,
+              corr_name=np.array([0, 0, 1, 0, 1, 1, 0, 1, 1], np.uint32),
+              corr_op=np.array([0, 1, 5, 2, 6, 7, 3, 8, 8], np.int32))
+    pre = O.tiers(tr, corr_policy=0)
+    np.testing.assert_array_equal(pre["tier"], [1, 1, 1, 1, 1, 1, 1, 1, 0, 1])
+    np.testing.assert_array_equal(pre["op"], [0, 5, 1, 6, 2, 7, 3, 8, -1, 8])
+    skip = O.tiers(tr, corr_policy=1)
+    np.testing.assert_array_equal(skip["tier"], [0, 1] * 5)
+    strict = O.tiers(tr, corr_policy=2)
+    np.testing.assert_array_equal(strict["tier"], pre["tier"])
+    assert pre["diag"]["status"] == 0 and strict["diag"]["status"] == -4
+    assert pre["diag"]["names_mismatched"] == 1
+
+
+def test_aggregate_ops_equals_range_aggregation():
+    """Given each kernel's op as the op of its range, the aggregation by op
+    is the aggregation by range (Eq. 1 pinned elsewhere)."""
+    tr = tg.generate("tiny")
+    full = O.attribute(tr)
+    rid = full["range_id"]
+    op = np.where(rid >= 0, tr["r_op"].astype(np.int64)[np.maximum(rid, 0)], -1).astype(np.int32)
+    out = O.aggregate_ops(tr, full["match"], op)
+    for f in ("kernel_count", "total_ns", "matched_count", "matched_ns"):
+        np.testing.assert_array_equal(out["table"][f], full["table"][f])
+    np.testing.assert_array_equal(out["table"]["value"], full["table"]["value"])
+    bad = op.copy()
+    bad[:3] = [tr["n_ops"], -2, 0]
+    out = O.aggregate_ops(tr, full["match"], bad)
+    assert out["diag"]["bad_records"] == 2 and out["diag"]["status"] == -9

@@ -60,6 +60,16 @@ MUTANTS = {
     "ranks_order_unchecked": ("if (all[x].a == all[x - 1].a) { diag->flags |= OREF_F_ORDER; break; }",
                               "if (0) break;"),
     "classes_never_grouped": ("part_rep[q] = (int32_t)head;", "part_rep[q] = (int32_t)q;"),
+    "tiers_nvtx_before_high": ("if (e >= 0 && corr->op_id[e] >= 0 && (uint32_t)corr->op_id[e] < NOPS) {",
+                               "if (rid < 0 && e >= 0 && corr->op_id[e] >= 0 && (uint32_t)corr->op_id[e] < NOPS) {"),
+    "tiers_fusion_overrides_nvtx": ("} else if (rid >= 0 && rid < r->n) {",
+                                    "} else if (rid >= 0 && rid < r->n && nf == 0) {"),
+    "tiers_fused_not_augmented": ("fused[i] = (uint8_t)(((walk_fused && walk_fused[i]) || nf > 1) ? 1 : 0);",
+                                  "fused[i] = (uint8_t)((walk_fused && walk_fused[i]) ? 1 : 0);"),
+    "tiers_index_with_dedup": ("kk.part_id = NULL;\n    oref_dims dd = *d;\n    dd.part_rep = NULL;\n    dd.n_parts = 0;",
+                               "oref_dims dd = *d;"),
+    "tiers_fusion_last_op": ("o = fm->op_id[fm->off[nm]];", "o = fm->op_id[fm->off[nm + 1] - 1];"),
+    "coverage_counts_kernels": ("cov->ns[t] += k->dur_ns[i];", "cov->ns[t] += 1;"),
     "parent_is_root": ("if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[top - 1] : -1;",
                        "if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[0] : -1;"),
 }
@@ -151,6 +161,16 @@ def battery(L) -> bool:
             return False
         if bool(out["diag"]["flags"] & 2) != (np.unique(tr["seq"]).size < tr["seq"].size):
             return False
+    for seed in range(6):
+        tr = test_oracle._tier_trace(seed, T=80, dedup=seed % 2 == 0, shuffle=seed % 3 == 1)
+        for pol in (0, 1):
+            out = O.tiers(tr, corr_policy=pol, library=L)
+            tier, op, fused, cnt, ns = brute.tiers(tr, pol)
+            if not (np.array_equal(out["tier"], tier) and np.array_equal(out["op"], op)
+                    and np.array_equal(out["fused"], fused)
+                    and list(out["coverage"]["count"]) == cnt
+                    and list(out["coverage"]["ns"]) == ns):
+                return False
     tr = _edge_trace()
     out = O.attribute(tr, library=L)
     if not np.array_equal(out["range_id"], brute.enclose(tr)):
