@@ -10,6 +10,8 @@
  *                          representative of a layer class (Sec. 3.7)
  *   opattr_dedup_classes   discovery of those classes from the timeline alone
  *                          (Sec. 3.7)
+ *   opattr_tiers           tiered attribution: correlation map, enclosure,
+ *                          fusion map (attribution-methods table)
  *   opattr_enclose         innermost operator range enclosing each launch on its
  *                          own stream (Sec. 3.5, Alg. 2)
  *   opattr_aggregate       per-operator SUM / duration-weighted mean (Eq. 1) / MAX
@@ -132,6 +134,41 @@ typedef struct {
   double attributed_fraction; /* attributed_ns / total_ns, NaN if total is 0 */
 } opattr_summary;
 
+/* Correlation map of the torch.profiler pass (Sec. 3.4; device arrays):
+   entry j records that one invocation of kernel name name_id[j] was launched
+   by operator op_id[j] (-1: no operator recorded). The entries of a name, in
+   array order, are its invocation indices 0, 1, 2, ...; names may
+   interleave. */
+typedef struct {
+  int64_t n;
+  const uint32_t *name_id;
+  const int32_t *op_id;
+} opattr_corr_map;
+
+/* Inductor fusion map (Sec. 3.6; device arrays): the operators fused into
+   kernel name n are op_id[off[n] .. off[n+1]), the first one primary. off has
+   n_names + 1 non-decreasing entries (a decreasing pair reads as an empty
+   list) and op_id holds off[n_names] entries. */
+typedef struct {
+  const uint32_t *off;
+  const int32_t *op_id;
+} opattr_fusion_map;
+
+/* Attribution tiers (the attribution-methods table): HIGH from the
+   correlation map, MEDIUM from the enclosure (NVTX) or from the fusion map
+   (FUSION), else UNATTRIBUTED. */
+enum { OPATTR_TIER_UNATTRIBUTED = 0, OPATTR_TIER_HIGH = 1, OPATTR_TIER_NVTX = 2,
+       OPATTR_TIER_FUSION = 3 };
+
+/* Coverage by tier (the attribution-coverage figure): kernels and kernel
+   nanoseconds per tier, and each tier's share of all kernel runtime (NaN
+   when there is none). Indexed by OPATTR_TIER_*. */
+typedef struct {
+  uint64_t count[4];
+  uint64_t ns[4];
+  double frac[4];
+} opattr_coverage; /* 96 bytes */
+
 /* Error classes (bits of opattr_diag.flags) and status codes. */
 #define OPATTR_F_DATA 1u        /* an id out of range / a range with start > end */
 #define OPATTR_F_ORDER 2u       /* duplicate seq, or a promised layout is false   */
@@ -213,6 +250,46 @@ int opattr_match(const opattr_kernels *k, const opattr_profiled *p, const opattr
 int opattr_dedup_broadcast(const opattr_kernels *k, const opattr_dims *d, int32_t *match,
                            opattr_diag *diag, void *ws, size_t ws_bytes, void *stream);
 
+/* Tiered attribution (the attribution-methods table and the decision-tree
+   figure). For each launch, the first tier that applies:
+     HIGH    corr has an entry for (name_id, invocation index) whose operator
+             is valid; the invocation index is the launch's rank among all
+             launches of its name in launch order (seq, ties by input index),
+             partitions playing no part: the lookup is Alg. 1 with corr's
+             entries as the rows, under corr_policy (OPATTR_MISMATCH_*;
+             SKIP_NAME = HIGH only for names whose launch and entry counts
+             agree, the table's trigger condition);
+     NVTX    range_id[i] >= 0 (the enclosure walk's op range, from
+             opattr_enclose_walk): operator r->op_id[range_id[i]];
+     FUSION  fmap lists operators for the name and the first one is valid;
+     UNATTRIBUTED otherwise (op -1).
+   fused[i] = walk_fused[i] (optional, from opattr_enclose_walk) or more than
+   one operator listed in fmap for the name: the fusion map augments every
+   tier without overriding it. corr and fmap may be NULL.
+   In: k->seq (with corr), name_id, dur_ns; r->n and r->op_id (the ranges
+   range_id refers to). Out (device): tier[k->n] (OPATTR_TIER_*), op[k->n],
+   fused[k->n], cov (one opattr_coverage). Correlation entries with an
+   operator outside [-1, n_ops) and range ids outside [-1, r->n) are bad
+   records; the matching's count diagnostics describe corr. Workspace:
+   opattr_tiers_workspace_bytes. */
+size_t opattr_tiers_workspace_bytes(const opattr_kernels *k, const opattr_corr_map *corr,
+                                    const opattr_ranges *r, const opattr_dims *d);
+int opattr_tiers(const opattr_kernels *k, const opattr_corr_map *corr,
+                 const opattr_fusion_map *fmap, const opattr_ranges *r, const opattr_dims *d,
+                 int corr_policy, const int32_t *range_id, const uint8_t *walk_fused,
+                 uint8_t *tier, int32_t *op, uint8_t *fused, opattr_coverage *cov,
+                 opattr_diag *diag, void *ws, size_t ws_bytes, void *stream);
+
+/* Aggregation (Eq. 1) by a given operator per launch: row op[i] when
+   op[i] in [0, n_ops), row n_ops (UNATTRIBUTED) when op[i] == -1; other
+   values are bad records and go to UNATTRIBUTED. Otherwise as
+   opattr_aggregate (e.g. op from opattr_tiers). Workspace:
+   opattr_workspace_bytes(k, p, NULL, d). */
+int opattr_aggregate_ops(const opattr_kernels *k, const opattr_profiled *p, const int32_t *match,
+                         const int32_t *op, const opattr_dims *d, const uint8_t *agg_kind,
+                         opattr_op_row *table, opattr_summary *sum, opattr_diag *diag,
+                         void *ws, size_t ws_bytes, void *stream);
+
 /* Layer class discovery (Sec. 3.7: structurally identical layers share one
    profiled representative). Two partitions are one class when the launches
    of each (valid name_id and part_id) form the same sequence of (name_id,
@@ -250,8 +327,10 @@ int opattr_enclose(const opattr_kernels *k, const opattr_ranges *r, const opattr
    innermost enclosing range of any kind, or -1; range_parent[r] = the
    innermost range that contains range r (the nearest earlier range of its
    stream in nesting order whose end is not before end_r), or -1 for a root
-   or a bad range. range_any and range_parent together give every range
-   enclosing a kernel, innermost first. fused, range_any, range_parent and
+   or a bad range. The ranges enclosing a kernel are range_any and its
+   parent chain, plus, when range_any starts exactly at the query point,
+   ranges that end there (touching it rather than nesting it), which the walk
+   visits in nesting order. fused, range_any, range_parent and
    range_depth may be NULL. Defined for properly nested ranges (crossing
    ranges are reported as NOT_NESTED). */
 int opattr_enclose_walk(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,

@@ -137,6 +137,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.c_list = b.take(NPc * 4);
   pl.c_tkey = b.take(TS * 8);
   pl.c_tmin = b.take(TS * 4);
+  pl.ident = b.take((size_t)d->n_ops * 4);
   pl.misc = b.take(256);
   pl.total = b.off;
   return pl;
@@ -533,6 +534,98 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   if (ss) note(hipStreamWaitEvent(s, ss->join3, 0));
   reduce_items(e, s);
   launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s, table, sum, pl.G, d->n_ops);
+  return launch_status();
+}
+
+// the matching's view of a tiers call: the correlation entries as profiled
+// rows, no partitions
+struct TiersView {
+  opattr_kernels k;
+  opattr_profiled p;
+  opattr_dims d;
+  TiersView(const opattr_kernels *k0, const opattr_corr_map *corr, const opattr_dims *d0)
+      : k(*k0), p{}, d(*d0) {
+    k.part_id = nullptr;
+    d.part_rep = nullptr;
+    d.n_parts = 0;
+    p.n = corr ? corr->n : 0;
+    p.name_id = corr ? corr->name_id : nullptr;
+  }
+};
+
+size_t opattr_tiers_workspace_bytes(const opattr_kernels *k, const opattr_corr_map *corr,
+                                    const opattr_ranges *r, const opattr_dims *d) {
+  if (!k || !d) return 0;
+  const TiersView v(k, corr, d);
+  return make_plan(&v.k, &v.p, r, &v.d).total;
+}
+
+int opattr_tiers(const opattr_kernels *k, const opattr_corr_map *corr,
+                 const opattr_fusion_map *fmap, const opattr_ranges *r, const opattr_dims *d,
+                 int corr_policy, const int32_t *range_id, const uint8_t *walk_fused,
+                 uint8_t *tier, int32_t *op, uint8_t *fused, opattr_coverage *cov,
+                 opattr_diag *diag, void *ws, size_t ws_bytes, void *stream) {
+  if (!check_dims(d) || !k || !ok_n(k->n) || !r || !ok_n(r->n) || !diag || !cov ||
+      corr_policy < 0 || corr_policy > 2)
+    return OPATTR_ERR_INVALID_ARG;
+  if (k->n > 0 && (!k->name_id || !k->dur_ns || !range_id || !tier || !op || !fused ||
+                   (r->n > 0 && !r->op_id)))
+    return OPATTR_ERR_INVALID_ARG;
+  if (corr && (!ok_n(corr->n) || (corr->n > 0 && (!corr->name_id || !corr->op_id)) ||
+               (k->n > 0 && !k->seq)))
+    return OPATTR_ERR_INVALID_ARG;
+  if (fmap && (!fmap->off || !fmap->op_id)) return OPATTR_ERR_INVALID_ARG;
+  const TiersView v(k, corr, d);
+  const Plan pl = make_plan(&v.k, &v.p, r, &v.d);
+  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
+  int32_t *entry = nullptr;
+  if (corr) {
+    // HIGH: Alg. 1 with the correlation entries as the rows
+    check_kernel_layout(&v.k, &v.d, diag, s);
+    entry = at<int32_t>(ws, pl.ia);
+    build_seq_view(&v.k, &v.d, ws, pl, diag, validate, s);
+    IomArgs a{&v.k, &v.p, &v.d, corr_policy, entry, nullptr, diag, ws, &pl, false, validate};
+    run_match(a, s);
+  }
+  TierIn x{k, corr, fmap, r, d, entry, range_id, walk_fused, tier, op, fused, cov, diag, ws, &pl};
+  run_tiers(x, s);
+  launch_finish(diag, nullptr, 0, s);
+  return launch_status();
+}
+
+int opattr_aggregate_ops(const opattr_kernels *k, const opattr_profiled *p, const int32_t *match,
+                         const int32_t *op, const opattr_dims *d, const uint8_t *agg_kind,
+                         opattr_op_row *table, opattr_summary *sum, opattr_diag *diag,
+                         void *ws, size_t ws_bytes, void *stream) {
+  if (!check_dims(d) || !check_kernels(k, false, false, true) || !check_profiled(p, false, true) ||
+      !diag || !table || !sum || !kinds_ok(agg_kind) || (k->n > 0 && (!match || !op)))
+    return OPATTR_ERR_INVALID_ARG;
+  const Plan pl = make_plan(k, p, nullptr, d);
+  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  // the operators stand in for range ids over the identity op table
+  uint32_t *ident = at<uint32_t>(ws, pl.ident);
+  launch_iota(ident, d->n_ops, s);
+  opattr_ranges ops{};
+  ops.n = d->n_ops;
+  ops.op_id = ident;
+  EncArgs e{};
+  e.k = k;
+  e.p = p;
+  e.match = match;
+  e.r = &ops;
+  e.d = d;
+  e.range_id = const_cast<int32_t *>(op);
+  e.agg_kind = agg_kind ? agg_kind : kDefaultKind;
+  e.table = table;
+  e.sum = sum;
+  e.diag = diag;
+  e.ws = ws;
+  e.pl = &pl;
+  run_aggregate_all(e, s);
+  launch_finish(diag, nullptr, 0, s, table, sum, pl.G, d->n_ops);
   return launch_status();
 }
 

@@ -255,11 +255,14 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
     int32_t rlast = -1, olast = -1, alast = -1;
     uint32_t glast = 0;
     uint8_t flast = 0;
+    bool tlast = false;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
       int32_t rid = -1;
+      int64_t slo = 0;  // first range of the launch's stream
       if (k < nv && st[k] < a.NS && q[k] < (1ull << 63)) {
         const int64_t lo = a.rblk[st[k]], hi = a.rblk[st[k] + 1];
+        slo = lo;
         const bool win = staged && st[k] == s0;  // the staged starts belong to this stream
         int64_t j, ej = 0;
         int steps = 0;
@@ -318,8 +321,24 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
         if (k < nv && st[k] >= a.NS) bad++;
         have = false;
       }
-      if (rid >= 0 && rid != rlast) {
+      // A range that starts at the query point may be preceded, among the
+      // ranges containing the point, by ranges that end there without
+      // containing it (touching, not nested); any other enclosing range is
+      // an ancestor. So the walk depends on the query point only through
+      // "the innermost range starts at it", which keys the cache with rid.
+      const bool touch = rid >= 0 && (uint64_t)a.cr.s[rid] == q[k];
+      if (rid >= 0 && (rid != rlast || touch != tlast)) {
         rlast = rid;
+        tlast = touch;
+        // the next range outward that contains the query point: the parent,
+        // or from a range starting at the point the nearest earlier range in
+        // nesting order that ends at or after it
+        auto next_out = [&](int64_t j) -> int64_t {
+          if (!touch || (uint64_t)a.cr.s[j] != q[k]) return a.npg[j];
+          int64_t c = j - 1;
+          for (int h = 0; c >= slo && a.ree[c] < (int64_t)q[k] && h < kMaxWalk; ++h) c = a.npg[c];
+          return c >= slo ? c : -1;
+        };
         // Alg. 2's walk outward from the innermost range: ops collected,
         // skipped kinds passed over, a boundary ends it
         int32_t first = rid;
@@ -327,16 +346,16 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
         if (a.cr.kind) {
           first = -1;
           int nops = 0, hops = 0;
-          for (int32_t j = rid; j >= 0 && hops < kMaxWalk; j = a.npg[j], ++hops) {
+          for (int64_t j = rid; j >= 0 && hops < kMaxWalk; j = next_out(j), ++hops) {
             const uint8_t kd = a.cr.kind[j];
             if (kd == OPATTR_KIND_BOUNDARY) break;
             if (kd != OPATTR_KIND_OP) continue;
-            if (first < 0) first = j;
+            if (first < 0) first = (int32_t)j;
             ++nops;
           }
           flast = nops > 1 ? 1 : 0;
         } else if (a.fused) {
-          flast = a.npg[rid] >= 0 ? 1 : 0;  // every enclosing range is an op
+          flast = next_out(rid) >= 0 ? 1 : 0;  // every enclosing range is an op
         }
         olast = first >= 0 ? (a.cr.perm ? a.cr.perm[first] : first) : -1;
         glast = first >= 0 ? a.cr.op[first] : a.NOPS;

@@ -47,7 +47,8 @@ struct Plan {
   size_t wi, wr, hmb, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, coff, cmap, sit, part;
   // dedup class discovery
   size_t c_first, c_last, c_runs, c_key, c_cand, c_fail, c_list, c_tkey, c_tmin;
-  size_t misc;  // small device scalars
+  size_t ident;  // 0 .. n_ops - 1 (aggregation by a given operator)
+  size_t misc;   // small device scalars
 };
 
 Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_ranges *r,
@@ -165,6 +166,26 @@ int64_t class_table_slots(uint32_t NP);
 // needs the launch-order view (build_seq_view)
 void run_classes(const opattr_kernels *k, const opattr_dims *d, int32_t *part_rep,
                  opattr_diag *diag, void *ws, const Plan &pl, hipStream_t s);
+
+// ---- tiered attribution (tiers.hip) ---------------------------------------------
+struct TierIn {
+  const opattr_kernels *k;
+  const opattr_corr_map *corr;
+  const opattr_fusion_map *fmap;
+  const opattr_ranges *r;
+  const opattr_dims *d;
+  const int32_t *entry;  // correlation entry per launch (from the matching), or NULL
+  const int32_t *range_id;
+  const uint8_t *walk_fused;
+  uint8_t *tier;
+  int32_t *op;
+  uint8_t *fused;
+  opattr_coverage *cov;
+  opattr_diag *diag;
+  void *ws;
+  const Plan *pl;
+};
+void run_tiers(const TierIn &x, hipStream_t s);
 
 // ---- ranges and enclosure (ranges.hip, enclose.hip) ----------------------------
 CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws, const Plan &pl,

@@ -52,6 +52,21 @@ class opattr_dims(C.Structure):
                 ("n_parts", C.c_uint32), ("part_rep", C.c_void_p), ("flags", C.c_uint32)]
 
 
+class opattr_corr_map(C.Structure):
+    _fields_ = [("n", C.c_int64), ("name_id", C.c_void_p), ("op_id", C.c_void_p)]
+
+
+class opattr_fusion_map(C.Structure):
+    _fields_ = [("off", C.c_void_p), ("op_id", C.c_void_p)]
+
+
+class opattr_coverage(C.Structure):
+    _fields_ = [("count", C.c_uint64 * 4), ("ns", C.c_uint64 * 4), ("frac", C.c_double * 4)]
+
+
+TIER_UNATTRIBUTED, TIER_HIGH, TIER_NVTX, TIER_FUSION = 0, 1, 2, 3
+
+
 class opattr_diag(C.Structure):
     _fields_ = [("status", C.c_int32), ("flags", C.c_uint32), ("names_mismatched", C.c_uint32),
                 ("nesting_errors", C.c_uint32), ("tl_unmatched", C.c_uint64),
@@ -70,7 +85,8 @@ assert OP_ROW_DTYPE.itemsize == 192 and SUMMARY_DTYPE.itemsize == 40
 assert C.sizeof(opattr_diag) == 64
 
 EXPORTS = ("opattr_workspace_bytes", "opattr_diag_clear", "opattr_read_diag", "opattr_match",
-           "opattr_dedup_broadcast", "opattr_dedup_classes", "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate",
+           "opattr_dedup_broadcast", "opattr_dedup_classes", "opattr_tiers_workspace_bytes",
+           "opattr_tiers", "opattr_aggregate_ops", "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate",
            "opattr_attribute", "opattr_set_probe_events", "opattr_set_class_key_bits",
            "opattr_strerror")
 PROBES = ("seq_view", "tl_hist", "pf_hist", "col_scan", "pf_slot", "tl_match", "dedup",
@@ -112,6 +128,16 @@ def library(path: str | None = None):
     for f in ("opattr_diag_clear", "opattr_read_diag", "opattr_match", "opattr_dedup_broadcast",
               "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate", "opattr_attribute"):
         getattr(L, f).restype = C.c_int
+    L.opattr_tiers_workspace_bytes.argtypes = [P(opattr_kernels), P(opattr_corr_map),
+                                               P(opattr_ranges), P(opattr_dims)]
+    L.opattr_tiers_workspace_bytes.restype = sz
+    L.opattr_tiers.argtypes = [P(opattr_kernels), P(opattr_corr_map), P(opattr_fusion_map),
+                               P(opattr_ranges), P(opattr_dims), i, vp, vp, vp, vp, vp, vp, vp,
+                               vp, sz, vp]
+    L.opattr_tiers.restype = C.c_int
+    L.opattr_aggregate_ops.argtypes = [P(opattr_kernels), P(opattr_profiled), vp, vp,
+                                       P(opattr_dims), vp, vp, vp, vp, vp, sz, vp]
+    L.opattr_aggregate_ops.restype = C.c_int
     L.opattr_set_class_key_bits.argtypes = [i]
     L.opattr_set_class_key_bits.restype = C.c_int
     L.opattr_set_probe_events.argtypes = [vp, i]
@@ -147,6 +173,8 @@ def strerror(status: int) -> str:
 _KERNEL_FIELDS = {"seq": np.uint32, "start_ns": np.uint64, "dur_ns": np.uint32,
                   "stream_id": np.uint16, "name_id": np.uint32, "part_id": np.int32,
                   "query_ns": np.uint64}
+_MAP_FIELDS = {"corr_name": np.uint32, "corr_op": np.int32, "fmap_off": np.uint32,
+               "fmap_op": np.int32}
 _RANGE_FIELDS = {"r_start": np.uint64, "r_end": np.uint64, "r_stream": np.uint16,
                  "r_op": np.uint32, "r_kind": np.uint8}
 
@@ -157,7 +185,7 @@ def to_device(tr: dict, device="cuda:0") -> dict:
     import torch
 
     out = {}
-    for k, dt in {**_KERNEL_FIELDS, **_RANGE_FIELDS, "pf_name": np.uint32,
+    for k, dt in {**_KERNEL_FIELDS, **_RANGE_FIELDS, **_MAP_FIELDS, "pf_name": np.uint32,
                   "part_rep": np.int32}.items():
         a = tr.get(k)
         out[k] = None if a is None else torch.from_numpy(
@@ -261,6 +289,12 @@ class Outputs(dict):
     def table_host(self):
         return self["table"].cpu().numpy().view(OP_ROW_DTYPE).reshape(-1)
 
+    def coverage_host(self):
+        c = opattr_coverage.from_buffer_copy(self["coverage"].cpu().numpy().tobytes())
+        return {"count": np.array(c.count[:], dtype=np.uint64),
+                "ns": np.array(c.ns[:], dtype=np.uint64),
+                "frac": np.array(c.frac[:], dtype=np.float64)}
+
     def summary_host(self):
         a = self["summary"].cpu().numpy().view(SUMMARY_DTYPE)[0]
         return {f: (float(a[f]) if f == "attributed_fraction" else int(a[f]))
@@ -360,6 +394,98 @@ def opattr_dedup_classes(dt: dict, flags=0, ws: Workspace | None = None,
                                   _p(out["diag"]), _p(buf), C.c_size_t(buf.numel()),
                                   _stream_handle(stream)), "opattr_dedup_classes")
     return out
+
+
+def _maps(dt: dict):
+    """ctypes views of a device trace's correlation and fusion maps (None
+    when absent); keeps a placeholder for an empty fusion list alive."""
+    import torch
+
+    corr = fm = None
+    keep = []
+    if dt.get("corr_name") is not None:
+        corr = opattr_corr_map(int(dt["corr_name"].numel()), _p(dt["corr_name"]),
+                               _p(dt["corr_op"]))
+    if dt.get("fmap_off") is not None:
+        fop = dt["fmap_op"]
+        if fop.numel() == 0:
+            fop = torch.zeros(1, dtype=torch.int32, device=dt["fmap_off"].device)
+            keep.append(fop)
+        fm = opattr_fusion_map(_p(dt["fmap_off"]), _p(fop))
+    return corr, fm, keep
+
+
+def opattr_tiers(dt: dict, range_id, walk_fused=None, corr_policy=MISMATCH_SKIP_NAME, flags=0,
+                 ws: Workspace | None = None, stream=None) -> Outputs:
+    """Tiered attribution (see opattr_tiers in include/opattr.h): tier, op
+    and fused per launch, and the coverage record, from the enclosure walk's
+    range_id / fused and the maps in ``dt`` (corr_name/corr_op,
+    fmap_off/fmap_op)."""
+    import torch
+
+    L = library()
+    m = _Marshal(dt, flags)
+    corr, fm, keep = _maps(dt)
+    dev = dt["seq"].device
+    out = Outputs(tier=torch.empty(m.T, dtype=torch.uint8, device=dev),
+                  op=torch.empty(m.T, dtype=torch.int32, device=dev),
+                  fused=torch.empty(m.T, dtype=torch.uint8, device=dev),
+                  coverage=torch.empty(C.sizeof(opattr_coverage), dtype=torch.uint8, device=dev),
+                  diag=_new_diag(dev, stream))
+    cp = C.byref(corr) if corr is not None else None
+    fp = C.byref(fm) if fm is not None else None
+    ws = ws or Workspace(dev)
+    buf = ws.get(L.opattr_tiers_workspace_bytes(C.byref(m.k), cp, C.byref(m.r), C.byref(m.d)))
+    rc = L.opattr_tiers(C.byref(m.k), cp, fp, C.byref(m.r), C.byref(m.d), corr_policy,
+                        _p(range_id), _p(walk_fused), _p(out["tier"]), _p(out["op"]),
+                        _p(out["fused"]), _p(out["coverage"]), _p(out["diag"]), _p(buf),
+                        C.c_size_t(buf.numel()), _stream_handle(stream))
+    del keep
+    _check(rc, "opattr_tiers")
+    return out
+
+
+def opattr_aggregate_ops(dt: dict, match, op, agg_kind=None, flags=0, absent_mask=0,
+                         ws: Workspace | None = None, stream=None) -> Outputs:
+    """Eq. 1 by a given operator per launch (see opattr_aggregate_ops)."""
+    import torch
+
+    L = library()
+    m = _Marshal(dt, flags, absent_mask)
+    dev = dt["counters"].device
+    out = Outputs(table=torch.empty((dt["n_ops"] + 1) * 192, dtype=torch.uint8, device=dev),
+                  summary=torch.empty(40, dtype=torch.uint8, device=dev),
+                  diag=_new_diag(dev, stream))
+    ws = ws or Workspace(dev)
+    buf = ws.get(L.opattr_workspace_bytes(C.byref(m.k), C.byref(m.p), None, C.byref(m.d)))
+    k_keep, kp = _kinds(agg_kind)
+    rc = L.opattr_aggregate_ops(C.byref(m.k), C.byref(m.p), _p(match), _p(op), C.byref(m.d), kp,
+                                _p(out["table"]), _p(out["summary"]), _p(out["diag"]), _p(buf),
+                                C.c_size_t(buf.numel()), _stream_handle(stream))
+    del k_keep
+    _check(rc, "opattr_aggregate_ops")
+    return out
+
+
+def attribute_tiered(dt: dict, policy=MISMATCH_PREFIX, corr_policy=MISMATCH_SKIP_NAME,
+                     agg_kind=None, flags=0, ws: Workspace | None = None,
+                     stream=None) -> dict:
+    """The tiered pipeline as a sequence of library calls on one stream:
+    matching (with the dedup broadcast when a class map is given), the
+    enclosure walk, the tiers, and the operator table by tier operator.
+    Returns each call's outputs."""
+    ws = ws or Workspace(dt["seq"].device)
+    m = opattr_match(dt, policy=policy, flags=flags, ws=ws, stream=stream)
+    res = {"match": m}
+    if dt.get("part_rep") is not None and dt.get("part_id") is not None:
+        res["dedup"] = opattr_dedup_broadcast(dt, m["match"], flags=flags, ws=ws, stream=stream)
+    w = opattr_enclose_walk(dt, flags=flags, ws=ws, stream=stream)
+    t = opattr_tiers(dt, w["range_id"], w["fused"], corr_policy=corr_policy, flags=flags, ws=ws,
+                     stream=stream)
+    a = opattr_aggregate_ops(dt, m["match"], t["op"], agg_kind=agg_kind, flags=flags, ws=ws,
+                             stream=stream)
+    res.update(walk=w, tiers=t, aggregate=a)
+    return res
 
 
 def set_class_key_bits(bits: int = 64):

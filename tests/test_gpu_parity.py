@@ -339,6 +339,28 @@ def test_enclose_walk_parity(seed):
     _assert_walk(out, want, diag)
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_enclose_walk_touching_ranges(seed):
+    """Coarse timestamps: many ranges end exactly where the next one starts
+    and many launches sit on those points, where a range that only touches
+    the innermost one still contains the launch (closed intervals): the walk
+    must visit it (fused, the op chosen) as the oracle's stack does."""
+    print(f"case walk touching seed={seed}", flush=True)
+    tr = cases.random_trace(950 + seed, T=500, R=150, S=1 + seed % 2, t_max=60, max_depth=6)
+    tr = cases.with_kinds(tr, seed, p_boundary=0.1 * (seed % 2), p_skip=0.3)
+    flags = 0
+    if seed % 3 == 0:
+        tr = cases.stream_major(tr)[0]
+        flags = opattr.KERNELS_STREAM_MAJOR | opattr.RANGES_NESTED
+    want = O.enclose_walk(tr)
+    out, diag = _walk_gpu(tr, flags)
+    _assert_walk(out, want, diag)
+    no_kinds = dict(tr, r_kind=None)
+    want = O.enclose_walk(no_kinds)
+    out, diag = _walk_gpu(no_kinds, flags)
+    _assert_walk(out, want, diag)
+
+
 def test_enclose_walk_large_with_kinds():
     """The 10M-launch trace with profiler-step roots (boundaries) and skipped
     namespaces: the walk outputs, and the whole attribution following the

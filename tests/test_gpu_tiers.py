@@ -1,0 +1,156 @@
+"""Tiered attribution on the GPU against the oracle, through the C ABI: the
+tier, operator and fused flag of every launch, the coverage record and the
+diagnostics, on random traces (range kinds, partitions, correlation maps
+with gaps, count mismatches, interleaved names and bad operator ids, fusion
+maps), the generated workloads in every emission order, the 10M-launch
+trace, and the operator table by tier operator (Eq. 1)."""
+import numpy as np
+import pytest
+
+import cases
+import parity
+from oracle import oracle as O
+from paper_2609_11938_amd import opattr, tracegen as tg
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+HINTS = opattr.KERNELS_STREAM_MAJOR | opattr.SEQ_DENSE | opattr.RANGES_NESTED
+DIAG = ("status", "flags", "bad_records", "names_mismatched", "tl_unmatched", "pf_unmatched")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _setup():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    opattr.library()
+    O.build(force=False)
+
+
+def _gpu_tiers(tr, policy=1, flags=0, walk_from_oracle=None):
+    import torch
+
+    dt = opattr.to_device(tr, DEV)
+    if walk_from_oracle is None:
+        w = opattr.opattr_enclose_walk(dt, flags=flags)
+        rid, wf = w["range_id"], w["fused"]
+    else:
+        rid = torch.from_numpy(walk_from_oracle["range_id"]).to(DEV)
+        wf = torch.from_numpy(walk_from_oracle["walk_fused"]).to(DEV)
+    out = opattr.opattr_tiers(dt, rid, wf, corr_policy=policy, flags=flags)
+    torch.cuda.synchronize()
+    return out, opattr.read_diag(out["diag"])
+
+
+def _assert_tiers(out, diag, want):
+    for f in ("tier", "op", "fused"):
+        np.testing.assert_array_equal(parity.host(out[f]), want[f], err_msg=f)
+    cov = out.coverage_host()
+    np.testing.assert_array_equal(cov["count"], want["coverage"]["count"])
+    np.testing.assert_array_equal(cov["ns"], want["coverage"]["ns"])
+    np.testing.assert_array_equal(cov["frac"], want["coverage"]["frac"])
+    for f in DIAG:
+        assert diag[f] == want["diag"][f], (f, diag, want["diag"])
+
+
+def _tier_trace(seed, T=400, dedup=False, shuffle=False, p_bad=0.0):
+    tr = cases.random_trace(600 + seed, T=T, R=120, S=1 + seed % 4, t_max=300, max_depth=6,
+                            dedup=dedup)
+    tr = cases.with_kinds(tr, seed)
+    return tg.with_attribution_maps(tr, seed=seed, p_corr=0.6, p_mismatch=0.3, p_none=0.1,
+                                    p_fmap=0.5, p_bad=p_bad, shuffle=shuffle)
+
+
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("policy", [0, 1, 2])
+def test_tiers_parity(seed, policy):
+    print(f"case tiers seed={seed} policy={policy}", flush=True)
+    tr = _tier_trace(seed, dedup=seed % 2 == 0, shuffle=seed % 3 == 1,
+                     p_bad=0.05 if seed % 4 == 3 else 0.0)
+    want = O.tiers(tr, corr_policy=policy)
+    out, diag = _gpu_tiers(tr, policy)
+    _assert_tiers(out, diag, want)
+
+
+@pytest.mark.parametrize("cfg", ["tiny", "gpt2", "sdpa", "lstm"])
+@pytest.mark.parametrize("emission", ["stream_major", "seq", "shuffled"])
+def test_tiers_generated(cfg, emission):
+    """The generated workloads with range kinds and maps; layout hints where
+    the emission keeps them."""
+    print(f"case tiers {cfg}/{emission}", flush=True)
+    tr = cases.with_kinds(parity.trace(cfg, emission), 4, p_boundary=0.0, p_skip=0.2,
+                          roots_boundary=True)
+    tr = tg.with_attribution_maps(tr, seed=11, shuffle=emission == "shuffled")
+    flags = {"stream_major": HINTS, "seq": opattr.SEQ_DENSE, "shuffled": 0}[emission]
+    want = O.tiers(tr)
+    out, diag = _gpu_tiers(tr, flags=flags, walk_from_oracle=want)
+    _assert_tiers(out, diag, want)
+
+
+def test_tiers_large():
+    """The 10M-launch trace with profiler-step boundaries, skipped ranges, a
+    correlation map for 40% of the names and a fusion map; the whole GPU
+    chain (walk, then tiers)."""
+    print("case tiers large", flush=True)
+    tr = tg.with_attribution_maps(tg.with_range_kinds(parity.trace("large", "stream_major")))
+    want = O.tiers(tr)
+    out, diag = _gpu_tiers(tr, flags=HINTS)
+    _assert_tiers(out, diag, want)
+    assert want["coverage"]["frac"][opattr.TIER_HIGH] > 0.2
+
+
+def test_tiers_without_maps_and_empty():
+    print("case tiers no maps", flush=True)
+    tr = cases.with_kinds(parity.trace("tiny", "stream_major"), 2)
+    want = O.tiers(tr)
+    out, diag = _gpu_tiers(tr, flags=HINTS)
+    _assert_tiers(out, diag, want)
+    # maps present but empty: no entries, every fusion list empty
+    tr = dict(tr, corr_name=np.zeros(0, np.uint32), corr_op=np.zeros(0, np.int32),
+              fmap_off=np.zeros(tr["n_names"] + 1, np.uint32), fmap_op=np.zeros(0, np.int32))
+    want = O.tiers(tr, corr_policy=0)
+    out, diag = _gpu_tiers(tr, policy=0, flags=HINTS)
+    _assert_tiers(out, diag, want)
+
+
+@pytest.mark.parametrize("cfg", ["tiny", "gpt2"])
+def test_aggregate_ops_parity(cfg):
+    """Eq. 1 by tier operator: the oracle's table given the oracle's match
+    and ops, on the GPU; a few operators out of range are bad records."""
+    import torch
+
+    print(f"case aggregate_ops {cfg}", flush=True)
+    tr = tg.with_attribution_maps(cases.with_kinds(parity.trace(cfg, "stream_major"), 1))
+    match = O.attribute(tr, stages=["match", "dedup"])["match"]
+    op = O.tiers(tr)["op"].copy()
+    op[:2] = [tr["n_ops"] + 4, -3]
+    want = O.aggregate_ops(tr, match, op)
+    dt = opattr.to_device(tr, DEV)
+    out = opattr.opattr_aggregate_ops(dt, torch.from_numpy(match).to(DEV),
+                                      torch.from_numpy(op).to(DEV))
+    torch.cuda.synchronize()
+    diag = opattr.read_diag(out["diag"])
+    parity.assert_table(out.table_host(), want["table"])
+    assert diag["bad_records"] == want["diag"]["bad_records"] == 2
+    assert diag["status"] == want["diag"]["status"]
+
+
+def test_attribute_tiered_pipeline():
+    """The tiered pipeline as library calls (match + dedup broadcast, walk,
+    tiers, table by tier operator) against the oracle's stages on GPT-2
+    (layer dedup on)."""
+    import torch
+
+    print("case tiered pipeline gpt2", flush=True)
+    tr = tg.with_attribution_maps(cases.with_kinds(parity.trace("gpt2", "stream_major"), 3,
+                                                   p_boundary=0.0, roots_boundary=True))
+    match = O.attribute(tr, stages=["match", "dedup"])["match"]
+    wt = O.tiers(tr)
+    want = O.aggregate_ops(tr, match, wt["op"])
+    dt = opattr.to_device(tr, DEV)
+    res = opattr.attribute_tiered(dt, flags=HINTS)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(parity.host(res["match"]["match"]), match)
+    _assert_tiers(res["tiers"], opattr.read_diag(res["tiers"]["diag"]), wt)
+    parity.assert_table(res["aggregate"].table_host(), want["table"])
