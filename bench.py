@@ -146,7 +146,8 @@ def measure_next_rows(dt, tr, flags, steps, warmup, out, ws):
     """The rows beyond the core hot path that this library also runs, timed on
     the same trace after the headline measurement: the attribution with the
     kind-aware walk of Alg. 2 (outermost ranges as boundaries, a fifth of the
-    others skipped), and layer class discovery (Sec. 3.7)."""
+    others skipped), tiered attribution (correlation map, enclosure, fusion
+    map) and layer class discovery (Sec. 3.7)."""
     import torch
 
     from paper_2609_11938_amd import opattr, tracegen
@@ -191,6 +192,48 @@ def measure_next_rows(dt, tr, flags, steps, warmup, out, ws):
         "skipped": int((kinds == 2).sum()), "kernel": "k_enclose", "kernel_ms": enc_ms,
         "kernel_algorithmic_bytes": enc_bytes, "kernel_GBps": enc_gbps,
         "kernel_frac": enc_gbps / HBM_PEAK_GBPS}
+
+    # tiered attribution: the pipeline of library calls (matching with the
+    # dedup broadcast, the walk, the tiers, the table by tier operator) with
+    # a correlation map for 40% of the names and a fusion map for 30%
+    maps = tracegen.with_attribution_maps(dict(tr, r_kind=kinds))
+    dtm = dict(dtk)
+    for f in ("corr_name", "corr_op", "fmap_off", "fmap_op"):
+        dtm[f] = torch.from_numpy(maps[f]).to(dt["seq"].device)
+    res = None
+    for _ in range(warmup):
+        res = opattr.attribute_tiered(dtm, flags=flags, ws=ws)
+    torch.cuda.synchronize()
+    diag = opattr.read_diag(res["tiers"]["diag"])
+    if diag["status"] not in (0, -4):
+        raise SystemExit(f"tiered attribution reported {diag}")
+    cov = res["tiers"].coverage_host()
+    ev = [_events(4) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for k in range(steps):
+        ev[k][0].record()
+        r = opattr.attribute_tiered(dtm, flags=flags, ws=ws)
+        ev[k][1].record()
+        opattr.opattr_tiers(dtm, r["walk"]["range_id"], r["walk"]["fused"], flags=flags, ws=ws)
+        ev[k][2].record()
+    torch.cuda.synchronize()
+    pipe_ms = statistics.mean(e[0].elapsed_time(e[1]) for e in ev)
+    tiers_ms = statistics.mean(e[1].elapsed_time(e[2]) for e in ev)
+    C_ = maps["corr_name"].size
+    # opattr_tiers alone: the correlation join (seq, name per launch; name
+    # per entry) and the tier pass (name, dur, range id, walk fused in;
+    # tier, op, fused out; entry op gathered once per launch at most)
+    tier_bytes = T * (4 + 4) + C_ * (4 + 4) + T * (4 + 4 + 4 + 1 + 1 + 4 + 1)
+    gbps = tier_bytes / (tiers_ms * 1e-3) / 1e9
+    rows["tiered"] = {
+        "call": "match + dedup broadcast + enclose_walk + tiers + aggregate_ops",
+        "ms_per_step": pipe_ms, "records_per_s": T / (pipe_ms * 1e-3),
+        "correlation_entries": int(C_),
+        "coverage_frac": {"high": float(cov["frac"][1]), "nvtx": float(cov["frac"][2]),
+                          "fusion": float(cov["frac"][3]),
+                          "unattributed": float(cov["frac"][0])},
+        "tiers_call_ms": tiers_ms, "tiers_algorithmic_bytes": tier_bytes,
+        "tiers_GBps": gbps, "tiers_frac": gbps / HBM_PEAK_GBPS}
 
     if NP:
         cflags = flags & (opattr.SEQ_DENSE | opattr.VALIDATE)

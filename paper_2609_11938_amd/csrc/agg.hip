@@ -6,22 +6,26 @@
 //   1. counting-sorted by row (per-tile row histograms scanned down the
 //      columns; stable, so each row keeps its items in launch order); this
 //      needs only the rows, so it runs beside the matching,
-//   2. cut into chunks of at most 64 items of one row, each reduced by one
-//      wave (a lane loads a partial row or accumulates its referenced
-//      launches, then a butterfly reduction),
-//   3. finalised (duration-weighted means divided by the matched duration,
-//      NaN for absent counters and rows without matched launches): a row of
-//      one chunk by the wave that reduced it, a row of several chunks by one
-//      wave that combines them in chunk order in a second pass. The summary
-//      over the table is taken by the finishing kernel.
-// Every sum is taken in a fixed order, so results are reproducible.
+//   2. reduced in windows of 64 consecutive sorted items, one wave each: a
+//      lane loads a partial row or accumulates its referenced launches, then
+//      a segmented scan over the lanes by row; a row whose items all lie in
+//      the window is finalised there (duration-weighted means divided by the
+//      matched duration, NaN for absent counters and rows without matched
+//      launches), a row crossing the window's edge leaves a partial for it,
+//   3. rows without items, and rows spread over several windows, finalised in
+//      a second pass: one wave per row, or a whole block for a row spread
+//      over many windows (one operator holding most of the launches, e.g.
+//      the UNATTRIBUTED row of a workload that is mostly not enclosed).
+// The summary over the table is taken by the finishing kernel. Every sum is
+// taken in a fixed order, so results are reproducible.
 #include "accum.h"
 #include "common.h"
 #include "impl.h"
 
 namespace opa {
 
-constexpr int kChunkItems = 64;
+constexpr int kWinItems = 64;     // sorted items per window (one wave)
+constexpr uint32_t kHeavy = 256;  // partials above which a row takes a whole block
 
 EmitOut emit_out(void *ws, const Plan &pl) {
   EmitOut e;
@@ -59,10 +63,11 @@ struct AggWork {
   AggIn in;
   const uint32_t *ig, *ia, *ib;
   const PartRow *rows;
-  int64_t *meta;  // [0] items, [1] partial rows, [2] item tiles, [3] chunks
-  uint32_t *ith, *gcnt, *goff, *coff, *cmap;
+  int64_t *meta;  // [0] items, [1] partial rows, [2] item tiles, [3] heavy rows
+  uint32_t *ith, *gcnt, *goff;
+  uint32_t *heavy;          // rows spread over more than kHeavy windows
   unsigned long long *sit;  // sorted items: partial-row index or first launch | length << 32
-  PartRow *part;
+  PartRow *part;            // [windows][2]: a continuing row's partial per window
   opattr_op_row *table;
   opattr_summary *sum;
 };
@@ -129,33 +134,24 @@ __global__ void __launch_bounds__(256) k_item_hist_r(AggWork w) {
   }
 }
 
-// 1b. row offsets of the sorted items and chunk offsets (one block; each
-// thread scans a contiguous run of rows)
+// 1b. row offsets of the sorted items (one block; each thread scans a
+// contiguous run of rows)
 __global__ void __launch_bounds__(1024) k_row_offsets(AggWork w) {
   __shared__ uint32_t sh[16];
   const uint32_t ch = (w.G + blockDim.x - 1) / blockDim.x;
   const uint32_t lo = threadIdx.x * ch;
   const uint32_t hi = lo + ch < w.G ? lo + ch : w.G;
-  uint32_t c = 0, cc = 0;
-  for (uint32_t g = lo; g < hi; ++g) {
-    const uint32_t n = w.gcnt[g];
-    c += n;
-    cc += (n + kChunkItems - 1) / kChunkItems;
-  }
-  uint32_t tot, ctot;
+  uint32_t c = 0;
+  for (uint32_t g = lo; g < hi; ++g) c += w.gcnt[g];
+  uint32_t tot;
   uint32_t run = block_excl_scan_add<uint32_t>(c, sh, &tot);
-  uint32_t crun = block_excl_scan_add<uint32_t>(cc, sh, &ctot);
   for (uint32_t g = lo; g < hi; ++g) {
-    const uint32_t n = w.gcnt[g];
     w.goff[g] = run;
-    w.coff[g] = crun;
-    run += n;
-    crun += (n + kChunkItems - 1) / kChunkItems;
+    run += w.gcnt[g];
   }
   if (threadIdx.x == 0) {
     w.goff[w.G] = tot;
-    w.coff[w.G] = ctot;
-    w.meta[3] = ctot;
+    w.meta[3] = 0;
   }
 }
 
@@ -222,14 +218,6 @@ __global__ void __launch_bounds__(256) k_item_scatter_r(AggWork w) {
   }
 }
 
-// 1d. chunk -> row map
-__global__ void k_chunk_map(AggWork w) {
-  const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= w.G) return;
-  const uint32_t c0 = w.coff[g], c1 = w.coff[g + 1];  // read once: cmap may alias
-  for (uint32_t c = c0; c < c1; ++c) w.cmap[c] = g;
-}
-
 // the row's table entry from its combined partial (lane c writes counter c)
 __device__ __forceinline__ void write_row(const AggWork &w, uint32_t g, const Acc &acc,
                                           uint32_t mx, uint32_t dw) {
@@ -258,20 +246,52 @@ __device__ __forceinline__ void write_row(const AggWork &w, uint32_t g, const Ac
   }
 }
 
-// 2. one wave per chunk of at most 64 items of one row; a row's only chunk
-// is finalised right away
+// the row's table entry from one lane's accumulator
+__device__ __forceinline__ void write_row_lane(const AggWork &w, uint32_t g, const Acc &acc,
+                                               uint32_t mx, uint32_t dw) {
+  opattr_op_row *row = w.table + g;
+  row->kernel_count = acc.kc;
+  row->total_ns = acc.tns;
+  row->matched_count = acc.mc;
+  row->matched_ns = acc.mns;
+  const double qnan = __longlong_as_double(0x7FF8000000000000ll);
+#pragma unroll
+  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
+    double v;
+    if (((w.absent >> c) & 1u) || acc.mc == 0) v = qnan;
+    else if ((mx >> c) & 1u) v = ((acc.nan >> c) & 1u) ? qnan : (double)key2f((uint32_t)acc.v[c]);
+    else if ((dw >> c) & 1u) v = acc.mns ? bits2d(acc.v[c]) / (double)acc.mns : qnan;
+    else v = bits2d(acc.v[c]);
+    row->value[c] = v;
+  }
+}
+
+// the row holding sorted item p: the last g with goff[g] <= p
+__device__ __forceinline__ uint32_t row_of_item(const uint32_t *goff, uint32_t G, uint32_t p) {
+  uint32_t lo = 0, hi = G - 1;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi + 1) >> 1;
+    if (goff[mid] <= p) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+// 2. one wave per window of 64 sorted items
 template <bool DEF>
-__global__ void __launch_bounds__(256) k_chunk_reduce(AggWork w) {
+__global__ void __launch_bounds__(256) k_window_reduce(AggWork w) {
   const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
-  const int64_t nch = w.meta[3];
+  const int64_t n = w.meta[0];
+  const int64_t nwin = (n + kWinItems - 1) / kWinItems;
   const int ln = lane_id();
-  for (int64_t ch = (int64_t)blockIdx.x * 4 + wave_id(); ch < nch; ch += (int64_t)gridDim.x * 4) {
-    const uint32_t g = w.cmap[ch];
-    const uint32_t c0 = w.coff[g];
-    const uint32_t p = w.goff[g] + (uint32_t)(ch - c0) * kChunkItems + (uint32_t)ln;
+  for (int64_t win = (int64_t)blockIdx.x * 4 + wave_id(); win < nwin;
+       win += (int64_t)gridDim.x * 4) {
+    const int64_t p = win * kWinItems + ln;
+    uint32_t g = 0xFFFFFFFFu;
     Acc acc;
     acc_zero(acc);
-    if (p < w.goff[g + 1]) {
+    if (p < n) {
+      g = row_of_item(w.goff, w.G, (uint32_t)p);
       const unsigned long long it = w.sit[p];
       const uint32_t a = (uint32_t)it, b = (uint32_t)(it >> 32);
       if (b == 0) {
@@ -281,30 +301,94 @@ __global__ void __launch_bounds__(256) k_chunk_reduce(AggWork w) {
           acc_launch(acc, w.in, w.in.match[a + k], w.in.dur[a + k], mx, dw);
       }
     }
-    acc_wave_reduce(acc, mx);
-    if (w.coff[g + 1] - c0 == 1) write_row(w, g, acc, mx, dw);
-    else if (ln == 0) acc_store(w.part + ch, acc);
+    // segmented scan by row (rows are contiguous in the window)
+    const uint32_t gp = __shfl_up(g, 1, OPA_WAVE), gn = __shfl_down(g, 1, OPA_WAVE);
+    const uint64_t heads = __ballot(ln == 0 || gp != g);
+    const uint64_t upto = ln == OPA_WAVE - 1 ? heads : heads & ((2ull << ln) - 1);
+    const int sl = 63 - __clzll((long long)upto);
+    acc_seg_scan(acc, sl, mx);
+    const bool tail = ln == OPA_WAVE - 1 || gn != g;
+    if (tail && g != 0xFFFFFFFFu) {
+      const uint32_t lo = w.goff[g], hi = w.goff[g + 1];
+      const int64_t wlo = win * kWinItems, whi = wlo + kWinItems;
+      if ((int64_t)lo >= wlo && (int64_t)hi <= whi) write_row_lane(w, g, acc, mx, dw);
+      else if ((int64_t)lo < wlo) acc_store(w.part + 2 * win, acc);  // continued from before
+      else acc_store(w.part + 2 * win + 1, acc);                      // continues after
+    }
   }
 }
 
-// 3. one wave per operator row with no or several chunks
+// partial j of a row whose items span windows w0 .. w1: the part of w0 it
+// continues into, then each later window's continued part
+__device__ __forceinline__ const PartRow *row_part(const AggWork &w, int64_t w0, int64_t j) {
+  return j == 0 ? w.part + 2 * w0 + 1 : w.part + 2 * (w0 + j);
+}
+
+// 3. one wave per operator row without items or spread over several
+// windows; rows over more than kHeavy windows are left to a block each
 template <bool DEF>
 __global__ void __launch_bounds__(256) k_combine(AggWork w) {
   const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
   const uint32_t g = blockIdx.x * 4 + wave_id();
   if (g >= w.G) return;
   const int ln = lane_id();
-  const uint32_t c0 = w.coff[g], c1 = w.coff[g + 1];
-  if (c1 - c0 == 1) return;  // finalised with its chunk
+  const uint32_t lo = w.goff[g], hi = w.goff[g + 1];
   Acc acc;
   acc_zero(acc);
-  for (uint32_t c = c0 + ln; c < c1; c += OPA_WAVE) {
-    Acc b;
-    acc_load(b, w.part + c);
-    acc_merge(acc, b, mx);
+  if (hi > lo) {
+    const int64_t w0 = lo / kWinItems, w1 = (hi - 1) / kWinItems;
+    if (w0 == w1) return;  // finalised in its window
+    const uint32_t m = (uint32_t)(w1 - w0 + 1);
+    if (m > kHeavy) {
+      if (ln == 0) w.heavy[atomicAdd((unsigned long long *)&w.meta[3], 1ull)] = g;
+      return;
+    }
+    for (uint32_t j = ln; j < m; j += OPA_WAVE) {
+      Acc b;
+      acc_load(b, row_part(w, w0, j));
+      acc_merge(acc, b, mx);
+    }
   }
   acc_wave_reduce(acc, mx);
   write_row(w, g, acc, mx, dw);
+}
+
+// 3b. rows spread over many windows: a block each (the few heavy rows)
+constexpr int kHeavyThreads = 1024;
+
+template <bool DEF>
+__global__ void __launch_bounds__(kHeavyThreads) k_combine_heavy(AggWork w) {
+  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
+  constexpr int kWaves = kHeavyThreads / OPA_WAVE;
+  __shared__ PartRow red[kWaves];
+  const int64_t nh = w.meta[3];
+  for (int64_t h = blockIdx.x; h < nh; h += gridDim.x) {
+    const uint32_t g = w.heavy[h];
+    const uint32_t lo = w.goff[g], hi = w.goff[g + 1];
+    const int64_t w0 = lo / kWinItems, w1 = (hi - 1) / kWinItems;
+    const int64_t m = w1 - w0 + 1;
+    Acc acc;
+    acc_zero(acc);
+    for (int64_t j = threadIdx.x; j < m; j += blockDim.x) {
+      Acc b;
+      acc_load(b, row_part(w, w0, j));
+      acc_merge(acc, b, mx);
+    }
+    acc_wave_reduce(acc, mx);
+    __syncthreads();  // red is free (previous row done)
+    if (lane_id() == 0) acc_store(red + wave_id(), acc);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      Acc t;
+      acc_load(t, red);
+      for (int k = 1; k < kWaves; ++k) {
+        Acc b;
+        acc_load(b, red + k);
+        acc_merge(t, b, mx);
+      }
+      write_row_lane(w, g, t, mx, dw);
+    }
+  }
 }
 
 static AggWork agg_work(const EncArgs &x) {
@@ -323,8 +407,7 @@ static AggWork agg_work(const EncArgs &x) {
   w.ith = at<uint32_t>(x.ws, pl.ith);
   w.gcnt = at<uint32_t>(x.ws, pl.gcnt);
   w.goff = at<uint32_t>(x.ws, pl.goff);
-  w.coff = at<uint32_t>(x.ws, pl.coff);
-  w.cmap = at<uint32_t>(x.ws, pl.cmap);
+  w.heavy = at<uint32_t>(x.ws, pl.heavy);
   w.sit = at<unsigned long long>(x.ws, pl.sit);
   w.part = at<PartRow>(x.ws, pl.part);
   w.table = x.table;
@@ -350,7 +433,6 @@ void plan_items(const EncArgs &x, hipStream_t s) {
   if (pl.T > 0) {
     if (fast) k_item_scatter_w<<<tgrid, 256, lds, s>>>(w);
     else k_item_scatter_r<<<tgrid, 256, 0, s>>>(w);
-    k_chunk_map<<<(pl.G + 255) / 256, 256, 0, s>>>(w);
   }
   probe_end(OPATTR_PROBE_ITEM_SORT, s);
 }
@@ -361,13 +443,18 @@ void reduce_items(const EncArgs &x, hipStream_t s) {
   const bool def = w.in.maxmask == kDefMaxMask && w.in.dwmask == kDefDwMask;
   probe_begin(OPATTR_PROBE_AGGREGATE, s);
   if (pl.T > 0) {
-    const int64_t want = (pl.max_chunks + 3) / 4;
+    const int64_t want = (pl.max_windows + 3) / 4;
     const unsigned cgrid = (unsigned)(want < 2048 ? want : 2048);
-    if (def) k_chunk_reduce<true><<<cgrid, 256, 0, s>>>(w);
-    else k_chunk_reduce<false><<<cgrid, 256, 0, s>>>(w);
+    if (def) k_window_reduce<true><<<cgrid, 256, 0, s>>>(w);
+    else k_window_reduce<false><<<cgrid, 256, 0, s>>>(w);
   }
-  if (def) k_combine<true><<<(pl.G + 3) / 4, 256, 0, s>>>(w);
-  else k_combine<false><<<(pl.G + 3) / 4, 256, 0, s>>>(w);
+  if (def) {
+    k_combine<true><<<(pl.G + 3) / 4, 256, 0, s>>>(w);
+    k_combine_heavy<true><<<64, kHeavyThreads, 0, s>>>(w);
+  } else {
+    k_combine<false><<<(pl.G + 3) / 4, 256, 0, s>>>(w);
+    k_combine_heavy<false><<<64, kHeavyThreads, 0, s>>>(w);
+  }
   probe_end(OPATTR_PROBE_AGGREGATE, s);
 }
 

@@ -106,10 +106,10 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.tlast = b.take(ntr * 4);
   pl.sflag = b.take(pl.NS);
   // aggregation: items (at most one per launch), partial rows (at most
-  // kEncRowsPerWave per 64 * 8 launches), chunks of 64 items per row
+  // kEncRowsPerWave per 64 * 8 launches), windows of 64 sorted items
   pl.cap_items = pl.T;
   pl.cap_rows = pl.nencb * (kEncThreads / OPA_WAVE) * kEncRowsPerWave;
-  pl.max_chunks = pl.T / 64 + pl.G + 1;
+  pl.max_windows = pl.cap_items / 64 + 1;
   pl.wi = b.take((size_t)pl.nencb * (kEncThreads / OPA_WAVE) * 4);
   pl.wr = b.take((size_t)pl.nencb * (kEncThreads / OPA_WAVE) * 4);
   pl.hmb = b.take((size_t)pl.nencb * kEncThreads);
@@ -122,10 +122,9 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.itch = b.take((size_t)pl.nchr * pl.G * 4);
   pl.gcnt = b.take((size_t)pl.G * 4);
   pl.goff = b.take(((size_t)pl.G + 1) * 4);
-  pl.coff = b.take(((size_t)pl.G + 1) * 4);
-  pl.cmap = b.take((size_t)pl.max_chunks * 4);
+  pl.heavy = b.take((size_t)pl.G * 4);
   pl.sit = b.take((size_t)pl.cap_items * 8);
-  pl.part = b.take((size_t)pl.max_chunks * 200);
+  pl.part = b.take((size_t)pl.max_windows * 2 * 200);
   // class discovery: per partition, and the key table
   const size_t NPc = d->n_parts, TS = (size_t)class_table_slots(d->n_parts);
   pl.c_first = b.take(NPc * 4);

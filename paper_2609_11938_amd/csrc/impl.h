@@ -43,8 +43,8 @@ struct Plan {
   size_t rperm, rs_c, re_c, rst_c, rop_c, rkd_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
   // aggregation
-  int64_t cap_items, cap_rows, max_chunks;
-  size_t wi, wr, hmb, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, coff, cmap, sit, part;
+  int64_t cap_items, cap_rows, max_windows;
+  size_t wi, wr, hmb, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, heavy, sit, part;
   // dedup class discovery
   size_t c_first, c_last, c_runs, c_key, c_cand, c_fail, c_list, c_tkey, c_tmin;
   size_t ident;  // 0 .. n_ops - 1 (aggregation by a given operator)

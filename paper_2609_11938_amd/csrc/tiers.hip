@@ -8,8 +8,10 @@
 // (the enclosure walk's op range), FUSION (the first operator the fusion map
 // lists for the kernel name), else UNATTRIBUTED -- marks the kernel fused
 // when the walk collected several op ranges or the fusion map lists several
-// operators, and sums kernels and nanoseconds per tier: wave reductions,
-// one LDS atomic per wave and tier, one global atomic per block and tier.
+// operators, and sums kernels and nanoseconds per tier: a fixed grid
+// strides over the launches with the sums in registers, each block writes
+// its eight partial sums, and one block adds them up (atomics on eight hot
+// addresses would serialise at a few ns each).
 #include "common.h"
 #include "impl.h"
 
@@ -32,9 +34,11 @@ struct TierArgs {
   uint8_t *tier;
   int32_t *op;
   uint8_t *fused;
-  unsigned long long *acc;  // [8]: kernels per tier, then ns per tier
+  unsigned long long *part;  // [blocks][8]: kernels per tier, then ns per tier
   opattr_diag *diag;
 };
+
+constexpr int kTierBlocks = 1024;  // grid of the tier pass (4 blocks per CU)
 
 // correlation entries with an operator outside [-1, n_ops) are bad records
 __global__ void k_corr_bad(const int32_t *__restrict__ corr_op, int64_t C, uint32_t NOPS,
@@ -50,73 +54,98 @@ __global__ void k_corr_bad(const int32_t *__restrict__ corr_op, int64_t C, uint3
     atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)__popcll(m));
 }
 
-__global__ void __launch_bounds__(256) k_tiers(TierArgs a) {
-  __shared__ unsigned long long sacc[8];
-  if (threadIdx.x < 8) sacc[threadIdx.x] = 0;
-  __syncthreads();
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const bool live = i < a.T;
+// tier, operator and fused of launch i; returns the tier
+__device__ __forceinline__ int tier_of(const TierArgs &a, int64_t i, uint32_t &bad) {
+  const uint32_t nm = a.name[i];
+  const int32_t e = a.entry ? a.entry[i] : -1;
+  const int32_t rid = a.range_id[i];
+  if (rid < -1 || (int64_t)rid >= a.R) bad++;
+  uint32_t f0 = 0, nf = 0;  // the kernel name's fusion list
+  if (a.f_off && nm < a.NN) {
+    const uint32_t lo = a.f_off[nm], hi = a.f_off[nm + 1];
+    if (hi > lo) {
+      f0 = lo;
+      nf = hi - lo;
+    }
+  }
+  const int32_t co = (e >= 0 && e < a.C) ? a.corr_op[e] : -1;
   int t = OPATTR_TIER_UNATTRIBUTED;
-  uint64_t d = 0;
-  bool bad = false;
-  if (live) {
-    const uint32_t nm = a.name[i];
-    d = a.dur[i];
-    const int32_t e = a.entry ? a.entry[i] : -1;
-    const int32_t rid = a.range_id[i];
-    bad = rid < -1 || (int64_t)rid >= a.R;
-    uint32_t f0 = 0, nf = 0;  // the kernel name's fusion list
-    if (a.f_off && nm < a.NN) {
-      const uint32_t lo = a.f_off[nm], hi = a.f_off[nm + 1];
-      if (hi > lo) {
-        f0 = lo;
-        nf = hi - lo;
-      }
-    }
-    const int32_t co = (e >= 0 && e < a.C) ? a.corr_op[e] : -1;
-    int32_t o = -1;
-    if (co >= 0 && (uint32_t)co < a.NOPS) {
-      t = OPATTR_TIER_HIGH;
-      o = co;
-    } else if (rid >= 0 && (int64_t)rid < a.R) {
-      t = OPATTR_TIER_NVTX;
-      o = (int32_t)a.r_op[rid];
-    } else if (nf > 0) {
-      const int32_t fo = a.f_op[f0];
-      if (fo >= 0 && (uint32_t)fo < a.NOPS) {
-        t = OPATTR_TIER_FUSION;
-        o = fo;
-      }
-    }
-    a.tier[i] = (uint8_t)t;
-    a.op[i] = o;
-    a.fused[i] = (uint8_t)(((a.walk_fused && a.walk_fused[i]) || nf > 1) ? 1 : 0);
-  }
-  const uint64_t mb = __ballot(bad);
-  if (mb && lane_id() == __ffsll((unsigned long long)mb) - 1)
-    atomicAdd((unsigned long long *)&a.diag->bad_records, (unsigned long long)__popcll(mb));
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const bool in = live && t == q;
-    const uint64_t c = (uint64_t)__popcll(__ballot(in));
-    const uint64_t ns = wave_reduce_add<uint64_t>(in ? d : 0);
-    if (lane_id() == 0 && c) {
-      atomicAdd(&sacc[q], (unsigned long long)c);
-      atomicAdd(&sacc[4 + q], (unsigned long long)ns);
+  int32_t o = -1;
+  if (co >= 0 && (uint32_t)co < a.NOPS) {
+    t = OPATTR_TIER_HIGH;
+    o = co;
+  } else if (rid >= 0 && (int64_t)rid < a.R) {
+    t = OPATTR_TIER_NVTX;
+    o = (int32_t)a.r_op[rid];
+  } else if (nf > 0) {
+    const int32_t fo = a.f_op[f0];
+    if (fo >= 0 && (uint32_t)fo < a.NOPS) {
+      t = OPATTR_TIER_FUSION;
+      o = fo;
     }
   }
-  __syncthreads();
-  if (threadIdx.x < 8 && sacc[threadIdx.x]) atomicAdd(&a.acc[threadIdx.x], sacc[threadIdx.x]);
+  a.tier[i] = (uint8_t)t;
+  a.op[i] = o;
+  a.fused[i] = (uint8_t)(((a.walk_fused && a.walk_fused[i]) || nf > 1) ? 1 : 0);
+  return t;
 }
 
-__global__ void k_cov_finish(const unsigned long long *acc, opattr_coverage *cov) {
+__global__ void __launch_bounds__(256) k_tiers(TierArgs a) {
+  __shared__ unsigned long long red[4][8];
+  uint32_t cnt[4] = {0, 0, 0, 0}, bad = 0;
+  unsigned long long ns[4] = {0, 0, 0, 0};
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < a.T; i += stride) {
+    const int t = tier_of(a, i, bad);
+    const uint32_t d = a.dur[i];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      cnt[q] += t == q ? 1u : 0u;
+      ns[q] += t == q ? d : 0u;
+    }
+  }
+  const uint32_t bw = wave_reduce_add(bad);
+  if (lane_id() == 0 && bw)
+    atomicAdd((unsigned long long *)&a.diag->bad_records, (unsigned long long)bw);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const unsigned long long c = wave_reduce_add<unsigned long long>(cnt[q]);
+    const unsigned long long n = wave_reduce_add(ns[q]);
+    if (lane_id() == 0) {
+      red[wave_id()][q] = c;
+      red[wave_id()][4 + q] = n;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < 8) {
+    unsigned long long v = 0;
+    for (int w = 0; w < 4; ++w) v += red[w][threadIdx.x];
+    a.part[(int64_t)blockIdx.x * 8 + threadIdx.x] = v;
+  }
+}
+
+// the per-block sums added up (one block), and the coverage record
+__global__ void __launch_bounds__(256) k_cov_finish(const unsigned long long *part, int nblocks,
+                                                    opattr_coverage *cov) {
+  __shared__ unsigned long long red[4][8];
+  unsigned long long v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int b = threadIdx.x; b < nblocks; b += blockDim.x)
+#pragma unroll
+    for (int f = 0; f < 8; ++f) v[f] += part[(int64_t)b * 8 + f];
+#pragma unroll
+  for (int f = 0; f < 8; ++f) {
+    const unsigned long long r = wave_reduce_add(v[f]);
+    if (lane_id() == 0) red[wave_id()][f] = r;
+  }
+  __syncthreads();
   if (threadIdx.x != 0) return;
   opattr_coverage c;
   uint64_t total = 0;
+  for (int f = 0; f < 8; ++f) v[f] = red[0][f] + red[1][f] + red[2][f] + red[3][f];
   for (int q = 0; q < 4; ++q) {
-    c.count[q] = acc[q];
-    c.ns[q] = acc[4 + q];
-    total += acc[4 + q];
+    c.count[q] = v[q];
+    c.ns[q] = v[4 + q];
+    total += v[4 + q];
   }
   for (int q = 0; q < 4; ++q)
     c.frac[q] = total ? (double)c.ns[q] / (double)total
@@ -126,8 +155,12 @@ __global__ void k_cov_finish(const unsigned long long *acc, opattr_coverage *cov
 
 void run_tiers(const TierIn &x, hipStream_t s) {
   const Plan &pl = *x.pl;
-  unsigned long long *acc = at<unsigned long long>(x.ws, pl.misc);
-  fill_u32(reinterpret_cast<uint32_t *>(acc), 0u, 16, s);
+  const int64_t want = (pl.T + 255) / 256;
+  const int nb = want < 1 ? 1 : (want < kTierBlocks ? (int)want : kTierBlocks);
+  // partial sums: the aggregation's item rows (T 4-byte entries) hold them
+  // when T >= 2 * 8 * nb, else the small scalars
+  unsigned long long *part = pl.T >= 16 * (int64_t)nb ? at<unsigned long long>(x.ws, pl.ib)
+                                                       : at<unsigned long long>(x.ws, pl.misc);
   if (x.corr && x.corr->n > 0)
     k_corr_bad<<<(unsigned)((x.corr->n + 255) / 256), 256, 0, s>>>(x.corr->op_id, x.corr->n,
                                                                    x.d->n_ops, x.diag);
@@ -149,10 +182,10 @@ void run_tiers(const TierIn &x, hipStream_t s) {
   a.tier = x.tier;
   a.op = x.op;
   a.fused = x.fused;
-  a.acc = acc;
+  a.part = part;
   a.diag = x.diag;
-  if (pl.T > 0) k_tiers<<<(unsigned)((pl.T + 255) / 256), 256, 0, s>>>(a);
-  k_cov_finish<<<1, 64, 0, s>>>(acc, x.cov);
+  k_tiers<<<nb, 256, 0, s>>>(a);
+  k_cov_finish<<<1, 256, 0, s>>>(part, nb, x.cov);
 }
 
 }  // namespace opa
