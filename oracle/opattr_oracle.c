@@ -645,6 +645,39 @@ int oref_aggregate_ops(const oref_kernels *k, const oref_profiled *p, const int3
   return rc;
 }
 
+int oref_aggregate_dispatch(const oref_kernels *k, const oref_profiled *p, const int32_t *match,
+                            const int32_t *range_id, const int32_t *op, const oref_ranges *r,
+                            const oref_dims *d, const uint8_t *agg_kind, oref_row *table,
+                            oref_summary *sum, oref_diag *diag) {
+  if (!k || !p || !match || !range_id || !r || !d || !table || !sum || !diag) return OREF_ERR_ARG;
+  if (k->n < 0 || (k->n > 0 && !k->dur_ns) || r->n < 0 || (r->n > 0 && !r->op_id))
+    return OREF_ERR_ARG;
+  const uint8_t *kind = agg_kinds(agg_kind);
+  if (!kind) return OREF_ERR_ARG;
+  const int64_t R = r->n;
+  const uint32_t NOPS = d->n_ops;
+  /* a dispatch is an operator range (its op's call); a kernel attributed to
+     an operator outside any range of that operator is grouped per operator */
+  uint32_t *row_of = xcalloc((size_t)k->n, sizeof(uint32_t));
+  for (int64_t i = 0; i < k->n; ++i) {
+    const int32_t rid = range_id[i];
+    const int32_t o = op ? op[i] : (rid >= 0 && rid < R ? (int32_t)r->op_id[rid] : -1);
+    if (rid < -1 || rid >= R) diag->bad_records++;
+    if (op && (o < -1 || (o >= 0 && (uint32_t)o >= NOPS))) diag->bad_records++;
+    if (rid >= 0 && rid < R && o >= 0 && (uint32_t)o == r->op_id[rid] && (uint32_t)o < NOPS)
+      row_of[i] = (uint32_t)rid;
+    else if (o >= 0 && (uint32_t)o < NOPS)
+      row_of[i] = (uint32_t)(R + o);
+    else
+      row_of[i] = (uint32_t)(R + NOPS);
+  }
+  oref_dims dd = *d;
+  dd.n_ops = (uint32_t)(R + NOPS);
+  const int rc = aggregate_rows(k, p, match, row_of, &dd, kind, table, sum, diag);
+  free(row_of);
+  return rc;
+}
+
 /* ----------------------------------------------------------------------- */
 /* Tiered attribution (Table "tiers", decision-tree figure, Sec. 3.4-3.6)    */
 /* ----------------------------------------------------------------------- */

@@ -135,6 +135,18 @@ int oref_aggregate_ops(const oref_kernels *k, const oref_profiled *p, const int3
                        const int32_t *op, const oref_dims *d, const uint8_t *agg_kind,
                        oref_row *table, oref_summary *sum, oref_diag *diag);
 
+/* Per-dispatch table (the operators[] of profile.json, App. A.4): Eq. 1 by
+   operator dispatch. Row rid (< r->n) collects the kernels of range rid
+   whose operator (op[i], or the range's own op when op is NULL) is the
+   range's op; row r->n + o the kernels attributed to operator o otherwise
+   (no range, or a range of another operator); row r->n + n_ops the
+   unattributed ones. table has r->n + n_ops + 1 rows; the summary counts
+   the last row as unattributed. */
+int oref_aggregate_dispatch(const oref_kernels *k, const oref_profiled *p, const int32_t *match,
+                            const int32_t *range_id, const int32_t *op, const oref_ranges *r,
+                            const oref_dims *d, const uint8_t *agg_kind, oref_row *table,
+                            oref_summary *sum, oref_diag *diag);
+
 /* Correlation map of the torch.profiler pass (Sec. 3.4): entry j says that
    one invocation of kernel name name_id[j] was launched by operator op_id[j]
    (-1: none recorded); the entries of a name are its invocation indices 0,

@@ -127,12 +127,16 @@ def load(path: str):
     L.oref_dedup_classes.argtypes = [P(Kernels), P(Dims), C.c_void_p, P(Diag)]
     L.oref_aggregate_ops.argtypes = [P(Kernels), P(Profiled), C.c_void_p, C.c_void_p, P(Dims),
                                      C.c_void_p, C.c_void_p, P(Summary), P(Diag)]
+    L.oref_aggregate_dispatch.argtypes = [P(Kernels), P(Profiled), C.c_void_p, C.c_void_p,
+                                          C.c_void_p, P(Ranges), P(Dims), C.c_void_p,
+                                          C.c_void_p, P(Summary), P(Diag)]
     L.oref_tiers.argtypes = [P(Kernels), P(Corr), P(Fusion), P(Ranges), P(Dims), C.c_int,
                              C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                              P(Coverage), P(Diag)]
     L.oref_diag_finish.argtypes = [P(Diag), C.c_int]
     for f in ("oref_match", "oref_dedup", "oref_enclose", "oref_enclose_walk", "oref_aggregate",
-              "oref_dedup_classes", "oref_aggregate_ops", "oref_tiers"):
+              "oref_dedup_classes", "oref_aggregate_ops", "oref_tiers",
+              "oref_aggregate_dispatch"):
         getattr(L, f).restype = C.c_int
     return L
 
@@ -361,6 +365,30 @@ def aggregate_ops(tr, match, op, agg_kind=None, absent_mask=0, library=None):
                               _ptr(kind), _ptr(table), C.byref(sm), C.byref(dg))
     if rc:
         raise ValueError(f"oref_aggregate_ops: {rc}")
+    L.oref_diag_finish(C.byref(dg), PREFIX)
+    return {"table": table, "summary": {f: getattr(sm, f) for f, _ in Summary._fields_},
+            "diag": diag_dict(dg)}
+
+
+def aggregate_dispatch(tr, match, range_id, op=None, agg_kind=None, absent_mask=0,
+                       library=None):
+    """Eq. 1 per operator dispatch: rows 0..R-1 the ranges, R + o the kernels
+    of operator o outside a range of o, R + n_ops the unattributed ones."""
+    L = library if library is not None else lib()
+    x = _Inputs(tr, absent_mask)
+    match = np.ascontiguousarray(match, dtype=np.int32)
+    rid = np.ascontiguousarray(range_id, dtype=np.int32)
+    opa = None if op is None else np.ascontiguousarray(op, dtype=np.int32)
+    G = x.r_start.size + tr["n_ops"] + 1
+    table = np.zeros(G, dtype=ROW_DTYPE)
+    sm = Summary()
+    dg = Diag()
+    kind = None if agg_kind is None else np.ascontiguousarray(agg_kind, dtype=np.uint8)
+    rc = L.oref_aggregate_dispatch(C.byref(x.k), C.byref(x.p), _ptr(match), _ptr(rid), _ptr(opa),
+                                   C.byref(x.r), C.byref(x.d), _ptr(kind), _ptr(table),
+                                   C.byref(sm), C.byref(dg))
+    if rc:
+        raise ValueError(f"oref_aggregate_dispatch: {rc}")
     L.oref_diag_finish(C.byref(dg), PREFIX)
     return {"table": table, "summary": {f: getattr(sm, f) for f, _ in Summary._fields_},
             "diag": diag_dict(dg)}

@@ -242,14 +242,37 @@ def aggregate(tr, match, range_id, agg_kind=None, absent_mask=0):
     """Per operator: counts and ns sums, and per counter the correctly rounded
     (math.fsum) SUM, duration-weighted mean (Eq. 1) or MAX over matched
     kernels."""
+    T = tr["seq"].size
+    group = [int(tr["r_op"][int(range_id[i])]) if int(range_id[i]) >= 0 else tr["n_ops"]
+             for i in range(T)]
+    return aggregate_groups(tr, match, group, tr["n_ops"] + 1, agg_kind, absent_mask)
+
+
+def dispatch_keys(tr, range_id, op=None):
+    """Per kernel, its row of the per-dispatch table: its range when the
+    kernel's operator is the range's operator, else R + its operator, else
+    (unattributed) R + n_ops."""
+    R, NOPS = tr["r_start"].size, tr["n_ops"]
+    keys = []
+    for i in range(tr["seq"].size):
+        r = int(range_id[i])
+        o = int(op[i]) if op is not None else (int(tr["r_op"][r]) if r >= 0 else -1)
+        if r >= 0 and 0 <= o < NOPS and o == int(tr["r_op"][r]):
+            keys.append(r)
+        elif 0 <= o < NOPS:
+            keys.append(R + o)
+        else:
+            keys.append(R + NOPS)
+    return keys
+
+
+def aggregate_groups(tr, match, group, G, agg_kind=None, absent_mask=0):
+    """The same reduction over given groups (group[i] in [0, G))."""
     kind = DEFAULT_KIND if agg_kind is None else list(agg_kind)
-    G = tr["n_ops"] + 1
     T = tr["seq"].size
     groups = [[] for _ in range(G)]
     for i in range(T):
-        r = int(range_id[i])
-        g = int(tr["r_op"][r]) if r >= 0 else tr["n_ops"]
-        groups[g].append(i)
+        groups[group[i]].append(i)
     rows = []
     dur = tr["dur_ns"]
     cnt = tr["counters"]

@@ -738,3 +738,66 @@ def test_aggregate_ops_equals_range_aggregation():
     bad[:3] = [tr["n_ops"], -2, 0]
     out = O.aggregate_ops(tr, full["match"], bad)
     assert out["diag"]["bad_records"] == 2 and out["diag"]["status"] == -9
+
+
+def _dispatch_case(seed):
+    tr = _tier_trace(seed, T=150, dedup=seed % 2 == 0)
+    match = O.attribute(tr, stages=["match", "dedup"])["match"]
+    t = O.tiers(tr)
+    return tr, match, t
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_dispatch_table_matches_brute_force(seed):
+    """Per-dispatch rows (a range when the kernel's tier operator is the
+    range's, else per operator, else unattributed) against the fsum
+    reduction over the same groups written out."""
+    tr, match, t = _dispatch_case(seed)
+    op = t["op"] if seed % 3 else None
+    out = O.aggregate_dispatch(tr, match, t["range_id"], op)
+    R = tr["r_start"].size
+    keys = brute.dispatch_keys(tr, t["range_id"], op)
+    want = brute.aggregate_groups(tr, match, keys, R + tr["n_ops"] + 1)
+    for a, b in zip(out["table"], want):
+        for f in ("kernel_count", "total_ns", "matched_count", "matched_ns"):
+            assert int(a[f]) == b[f]
+        for x, y in zip(a["value"], b["value"]):
+            assert (math.isnan(x) and math.isnan(y)) or math.isclose(x, y, rel_tol=1e-12)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_dispatch_rows_add_up_to_operator_rows(seed):
+    """Every kernel of operator o lies in a dispatch of o or in o's own row
+    R + o, so the per-dispatch rows of o add up to o's row of the operator
+    table: counts and ns exactly, SUM by addition, MAX by max, the
+    duration-weighted mean as the matched-ns weighted mean of the rows."""
+    tr, match, t = _dispatch_case(10 + seed)
+    disp = O.aggregate_dispatch(tr, match, t["range_id"], t["op"])["table"]
+    ops = O.aggregate_ops(tr, match, t["op"])["table"]
+    R, NOPS = tr["r_start"].size, tr["n_ops"]
+    owner = np.concatenate([tr["r_op"].astype(np.int64), np.arange(NOPS), [NOPS]])
+    kinds = O.DEFAULT_KIND
+    for o in range(NOPS + 1):
+        rows = disp[owner == o]
+        for f in ("kernel_count", "total_ns", "matched_count", "matched_ns"):
+            assert rows[f].sum() == ops[o][f]
+        mk = rows[rows["matched_count"] > 0]
+        for c in range(O.NC):
+            want = ops[o]["value"][c]
+            if not len(mk):
+                assert math.isnan(want)
+                continue
+            v = mk["value"][:, c]
+            if kinds[c] == O.SUM:
+                got = math.fsum(v)
+            elif kinds[c] == O.MAX:
+                got = v.max()
+            else:
+                w = mk["matched_ns"].astype(np.float64)
+                got = math.fsum(v * w) / w.sum()
+            assert math.isclose(got, want, rel_tol=1e-9), (o, c, got, want)
+    # without tier operators every kernel sits in its range's row
+    plain = O.aggregate_dispatch(tr, match, t["range_id"])["table"]
+    cnt = np.bincount(t["range_id"][t["range_id"] >= 0], minlength=R)
+    np.testing.assert_array_equal(plain["kernel_count"][:R], cnt)
+    assert plain["kernel_count"][R:R + NOPS].sum() == 0

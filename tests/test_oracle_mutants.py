@@ -70,6 +70,9 @@ MUTANTS = {
                                "oref_dims dd = *d;"),
     "tiers_fusion_last_op": ("o = fm->op_id[fm->off[nm]];", "o = fm->op_id[fm->off[nm + 1] - 1];"),
     "coverage_counts_kernels": ("cov->ns[t] += k->dur_ns[i];", "cov->ns[t] += 1;"),
+    "dispatch_ignores_operator": ("if (rid >= 0 && rid < R && o >= 0 && (uint32_t)o == r->op_id[rid] && (uint32_t)o < NOPS)",
+                                  "if (rid >= 0 && rid < R && o >= 0 && (uint32_t)o < NOPS)"),
+    "dispatch_op_row_shifted": ("row_of[i] = (uint32_t)(R + o);", "row_of[i] = (uint32_t)(R + o - (o > 0));"),
     "parent_is_root": ("if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[top - 1] : -1;",
                        "if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[0] : -1;"),
 }
@@ -171,6 +174,13 @@ def battery(L) -> bool:
                     and list(out["coverage"]["count"]) == cnt
                     and list(out["coverage"]["ns"]) == ns):
                 return False
+    for seed in range(4):
+        tr, match, t = test_oracle._dispatch_case(seed)
+        out = O.aggregate_dispatch(tr, match, t["range_id"], t["op"], library=L)
+        keys = brute.dispatch_keys(tr, t["range_id"], t["op"])
+        want = brute.aggregate_groups(tr, match, keys, tr["r_start"].size + tr["n_ops"] + 1)
+        if not _rows_close(out, want):
+            return False
     tr = _edge_trace()
     out = O.attribute(tr, library=L)
     if not np.array_equal(out["range_id"], brute.enclose(tr)):
