@@ -12,6 +12,7 @@
  *                          (Sec. 3.7)
  *   opattr_tiers           tiered attribution: correlation map, enclosure,
  *                          fusion map (attribution-methods table)
+ *   opattr_aggregate_dispatch  the operator table per dispatch (App. A.4)
  *   opattr_enclose         innermost operator range enclosing each launch on its
  *                          own stream (Sec. 3.5, Alg. 2)
  *   opattr_aggregate       per-operator SUM / duration-weighted mean (Eq. 1) / MAX
@@ -289,6 +290,24 @@ int opattr_aggregate_ops(const opattr_kernels *k, const opattr_profiled *p, cons
                          const int32_t *op, const opattr_dims *d, const uint8_t *agg_kind,
                          opattr_op_row *table, opattr_summary *sum, opattr_diag *diag,
                          void *ws, size_t ws_bytes, void *stream);
+
+/* Per-dispatch operator table (the operators[] of profile.json, App. A.4:
+   one entry per operator call, operator_id = name + call index). A dispatch
+   is an operator range. Row rid (< r->n) collects the launches with
+   range_id[i] == rid whose operator is the range's (op[i] from
+   opattr_tiers, or the range's own op when op is NULL); row r->n + o the
+   launches attributed to operator o otherwise (no range, or a range of
+   another operator); row r->n + n_ops the unattributed ones. Per row as
+   opattr_aggregate (Eq. 1). Out: table[r->n + n_ops + 1], sum (device; the
+   last row counts as unattributed). Needs r->n + n_ops <= 2^20 - 2.
+   Workspace: opattr_dispatch_workspace_bytes. */
+size_t opattr_dispatch_workspace_bytes(const opattr_kernels *k, const opattr_profiled *p,
+                                       const opattr_ranges *r, const opattr_dims *d);
+int opattr_aggregate_dispatch(const opattr_kernels *k, const opattr_profiled *p,
+                              const int32_t *match, const int32_t *range_id, const int32_t *op,
+                              const opattr_ranges *r, const opattr_dims *d,
+                              const uint8_t *agg_kind, opattr_op_row *table, opattr_summary *sum,
+                              opattr_diag *diag, void *ws, size_t ws_bytes, void *stream);
 
 /* Layer class discovery (Sec. 3.7: structurally identical layers share one
    profiled representative). Two partitions are one class when the launches

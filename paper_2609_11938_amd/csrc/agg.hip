@@ -115,25 +115,6 @@ __global__ void __launch_bounds__(256) k_item_hist_w(AggWork w) {
   else item_hist<16>(w, n, cnt);
 }
 
-// 1a'. the same with an LDS radix sort per tile, for many rows
-__global__ void __launch_bounds__(256) k_item_hist_r(AggWork w) {
-  __shared__ TileSmem sm;
-  const int64_t n = w.meta[0];
-  const int64_t ntiles = (n + OPA_TILE - 1) / OPA_TILE;
-  if (blockIdx.x == 0 && threadIdx.x == 0) w.meta[2] = ntiles;
-  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-    __syncthreads();
-    for (int l = threadIdx.x; l < OPA_TILE; l += 256) {
-      const int64_t x = tile * OPA_TILE + l;
-      const uint32_t g = x < n ? w.ig[x] : w.G;
-      sm.A[l] = (g << OPA_SLOT_BITS) | (uint32_t)l;
-    }
-    __syncthreads();
-    tile_radix_sort(sm.A, sm.B, sm.srt, OPA_SLOT_BITS, bits_for(w.G));
-    write_hist_row(sm.A, w.G, w.ith + tile * w.G);
-  }
-}
-
 // 1b. row offsets of the sorted items (one block; each thread scans a
 // contiguous run of rows)
 __global__ void __launch_bounds__(1024) k_row_offsets(AggWork w) {
@@ -192,30 +173,37 @@ __global__ void __launch_bounds__(256) k_item_scatter_w(AggWork w) {
   else item_scatter<16>(w, n, cnt);
 }
 
-__global__ void __launch_bounds__(256) k_item_scatter_r(AggWork w) {
-  __shared__ TileSmem sm;
+// 1'. many rows: one stable radix sort of (row, item) over all items; keys
+// of the padding past the item count sort last
+__global__ void k_item_keys(AggWork w, unsigned long long *k0, uint32_t *v0, int64_t cap) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= cap) return;
   const int64_t n = w.meta[0];
-  const int64_t ntiles = (n + OPA_TILE - 1) / OPA_TILE;
-  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-    __syncthreads();
-    for (int l = threadIdx.x; l < OPA_TILE; l += 256) {
-      const int64_t x = tile * OPA_TILE + l;
-      const uint32_t g = x < n ? w.ig[x] : w.G;
-      sm.A[l] = (g << OPA_SLOT_BITS) | (uint32_t)l;
-    }
-    __syncthreads();
-    tile_radix_sort(sm.A, sm.B, sm.srt, OPA_SLOT_BITS, bits_for(w.G));
-    const uint32_t *row = w.ith + tile * w.G;
-    for (int p = threadIdx.x; p < OPA_TILE; p += 256) {
-      const uint32_t key = sm.A[p];
-      const uint32_t g = key >> OPA_SLOT_BITS;
-      if (g >= w.G) continue;
-      const int lo = lds_lower_bound(sm.A, OPA_TILE, g << OPA_SLOT_BITS);
-      const int64_t x = tile * OPA_TILE + (key & (OPA_TILE - 1));
-      w.sit[w.goff[g] + row[g] + (uint32_t)(p - lo)] =
-          w.ia[x] | ((unsigned long long)w.ib[x] << 32);
-    }
+  k0[x] = x < n ? w.ig[x] : w.G;
+  v0[x] = (uint32_t)x;
+}
+
+// sorted items in place
+__global__ void k_item_place(AggWork w, const uint32_t *val, int64_t cap) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= cap || p >= w.meta[0]) return;
+  const uint32_t x = val[p];
+  w.sit[p] = w.ia[x] | ((unsigned long long)w.ib[x] << 32);
+}
+
+// row offsets: goff[g] = the first sorted item of row g or later (the
+// padding keys equal G, so goff[G] is the item count)
+__global__ void k_row_bounds(AggWork w, const unsigned long long *key, int64_t cap) {
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g > (int64_t)w.G) return;
+  int64_t lo = 0, hi = cap;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if ((int64_t)key[mid] < g) lo = mid + 1;
+    else hi = mid;
   }
+  w.goff[g] = (uint32_t)lo;
+  if (g == 0) w.meta[3] = 0;
 }
 
 // the row's table entry from its combined partial (lane c writes counter c)
@@ -418,21 +406,33 @@ static AggWork agg_work(const EncArgs &x) {
 void plan_items(const EncArgs &x, hipStream_t s) {
   const Plan &pl = *x.pl;
   AggWork w = agg_work(x);
-  const bool fast = pl.G <= kFastKeys;
-  const size_t lds = (size_t)4 * pl.G * sizeof(uint16_t);
-  const unsigned tgrid = (unsigned)(pl.ntrt < 1024 ? (pl.ntrt > 0 ? pl.ntrt : 1) : 1024);
-  // gcnt (and meta when there are no launches) were cleared with the
-  // look-back states
   probe_begin(OPATTR_PROBE_ITEM_SORT, s);
-  if (pl.T > 0) {
-    if (fast) k_item_hist_w<<<tgrid, 256, lds, s>>>(w);
-    else k_item_hist_r<<<tgrid, 256, 0, s>>>(w);
-    column_scan(w.ith, pl.ntrt, pl.G, at<uint32_t>(x.ws, pl.itch), w.gcnt, s, w.meta + 2);
-  }
-  k_row_offsets<<<1, 1024, 0, s>>>(w);
-  if (pl.T > 0) {
-    if (fast) k_item_scatter_w<<<tgrid, 256, lds, s>>>(w);
-    else k_item_scatter_r<<<tgrid, 256, 0, s>>>(w);
+  if (pl.G <= kFastKeys) {
+    const size_t lds = (size_t)4 * pl.G * sizeof(uint16_t);
+    const unsigned tgrid = (unsigned)(pl.ntrt < 1024 ? (pl.ntrt > 0 ? pl.ntrt : 1) : 1024);
+    // gcnt (and meta when there are no launches) were cleared with the
+    // look-back states
+    if (pl.T > 0) {
+      k_item_hist_w<<<tgrid, 256, lds, s>>>(w);
+      column_scan(w.ith, pl.ntrt, pl.G, at<uint32_t>(x.ws, pl.itch), w.gcnt, s, w.meta + 2);
+    }
+    k_row_offsets<<<1, 1024, 0, s>>>(w);
+    if (pl.T > 0) k_item_scatter_w<<<tgrid, 256, lds, s>>>(w);
+  } else {
+    const int64_t cap = pl.cap_items;
+    unsigned long long *k0 = at<unsigned long long>(x.ws, pl.isort_k0);
+    unsigned long long *k1 = at<unsigned long long>(x.ws, pl.isort_k1);
+    uint32_t *v0 = at<uint32_t>(x.ws, pl.isort_v0), *v1 = at<uint32_t>(x.ws, pl.isort_v1);
+    bool in1 = false;
+    if (cap > 0) {
+      k_item_keys<<<(unsigned)((cap + 255) / 256), 256, 0, s>>>(w, k0, v0, cap);
+      const int bits = (bits_for_host(pl.G) + 7) & ~7;
+      in1 = radix_sort_pairs(reinterpret_cast<uint64_t *>(k0), v0,
+                             reinterpret_cast<uint64_t *>(k1), v1, cap, 0, bits,
+                             at<uint32_t>(x.ws, pl.isort_hist), s);
+    }
+    if (cap > 0) k_item_place<<<(unsigned)((cap + 255) / 256), 256, 0, s>>>(w, in1 ? v1 : v0, cap);
+    k_row_bounds<<<(pl.G + 1 + 255) / 256, 256, 0, s>>>(w, in1 ? k1 : k0, cap);
   }
   probe_end(OPATTR_PROBE_ITEM_SORT, s);
 }

@@ -118,8 +118,16 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.ib = b.take((size_t)pl.cap_items * 4);
   pl.rows = b.take((size_t)pl.cap_rows * 200);
   pl.meta = b.take(8 * 8);
-  pl.ith = b.take((size_t)pl.ntrt * pl.G * 4);
-  pl.itch = b.take((size_t)pl.nchr * pl.G * 4);
+  // item sort: per-tile row histograms for few rows, else one radix sort
+  const bool few_rows = pl.G <= kFastKeys;
+  pl.ith = b.take(few_rows ? (size_t)pl.ntrt * pl.G * 4 : 0);
+  pl.itch = b.take(few_rows ? (size_t)pl.nchr * pl.G * 4 : 0);
+  const size_t ni = few_rows ? 0 : (size_t)pl.cap_items;
+  pl.isort_k0 = b.take(ni * 8);
+  pl.isort_k1 = b.take(ni * 8);
+  pl.isort_v0 = b.take(ni * 4);
+  pl.isort_v1 = b.take(ni * 4);
+  pl.isort_hist = b.take(few_rows ? 0 : radix_hist_entries((int64_t)ni) * 4);
   pl.gcnt = b.take((size_t)pl.G * 4);
   pl.goff = b.take(((size_t)pl.G + 1) * 4);
   pl.heavy = b.take((size_t)pl.G * 4);
@@ -625,6 +633,61 @@ int opattr_aggregate_ops(const opattr_kernels *k, const opattr_profiled *p, cons
   e.pl = &pl;
   run_aggregate_all(e, s);
   launch_finish(diag, nullptr, 0, s, table, sum, pl.G, d->n_ops);
+  return launch_status();
+}
+
+// the aggregation's view of a per-dispatch call: R + n_ops operator rows
+static opattr_dims dispatch_dims(const opattr_ranges *r, const opattr_dims *d) {
+  opattr_dims dd = *d;
+  dd.n_ops = (uint32_t)(r->n + d->n_ops);
+  return dd;
+}
+
+size_t opattr_dispatch_workspace_bytes(const opattr_kernels *k, const opattr_profiled *p,
+                                       const opattr_ranges *r, const opattr_dims *d) {
+  if (!d || !r || r->n < 0 || r->n + (int64_t)d->n_ops > (int64_t)kMaxOps) return 0;
+  const opattr_dims dd = dispatch_dims(r, d);
+  return make_plan(k, p, nullptr, &dd).total;
+}
+
+int opattr_aggregate_dispatch(const opattr_kernels *k, const opattr_profiled *p,
+                              const int32_t *match, const int32_t *range_id, const int32_t *op,
+                              const opattr_ranges *r, const opattr_dims *d,
+                              const uint8_t *agg_kind, opattr_op_row *table, opattr_summary *sum,
+                              opattr_diag *diag, void *ws, size_t ws_bytes, void *stream) {
+  if (!check_dims(d) || !check_kernels(k, false, false, true) || !check_profiled(p, false, true) ||
+      !r || !ok_n(r->n) || r->n + (int64_t)d->n_ops > (int64_t)kMaxOps || !diag || !table ||
+      !sum || !kinds_ok(agg_kind) || (k->n > 0 && (!match || !range_id)) ||
+      (r->n > 0 && !r->op_id))
+    return OPATTR_ERR_INVALID_ARG;
+  const opattr_dims dd = dispatch_dims(r, d);
+  const Plan pl = make_plan(k, p, nullptr, &dd);
+  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  // per-launch rows in the launch-order view's space (unused here), then
+  // the aggregation by those rows over an identity op table
+  int32_t *key = at<int32_t>(ws, pl.sv);
+  launch_dispatch_keys(range_id, op, r, d->n_ops, pl.T, key, diag, s);
+  uint32_t *ident = at<uint32_t>(ws, pl.ident);
+  launch_iota(ident, dd.n_ops, s);
+  opattr_ranges rows{};
+  rows.n = dd.n_ops;
+  rows.op_id = ident;
+  EncArgs e{};
+  e.k = k;
+  e.p = p;
+  e.match = match;
+  e.r = &rows;
+  e.d = &dd;
+  e.range_id = key;
+  e.agg_kind = agg_kind ? agg_kind : kDefaultKind;
+  e.table = table;
+  e.sum = sum;
+  e.diag = diag;
+  e.ws = ws;
+  e.pl = &pl;
+  run_aggregate_all(e, s);
+  launch_finish(diag, nullptr, 0, s, table, sum, pl.G, dd.n_ops);
   return launch_status();
 }
 

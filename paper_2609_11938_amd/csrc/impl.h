@@ -45,6 +45,7 @@ struct Plan {
   // aggregation
   int64_t cap_items, cap_rows, max_windows;
   size_t wi, wr, hmb, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, heavy, sit, part;
+  size_t isort_k0, isort_k1, isort_v0, isort_v1, isort_hist;  // item sort, many rows
   // dedup class discovery
   size_t c_first, c_last, c_runs, c_key, c_cand, c_fail, c_list, c_tkey, c_tmin;
   size_t ident;  // 0 .. n_ops - 1 (aggregation by a given operator)
@@ -102,6 +103,12 @@ void launch_scan_excl(const uint32_t *in, uint32_t *out, int64_t n, int64_t *tot
 // totals in totals; rows_dev (optional) holds the actual row count on device.
 void column_scan(uint32_t *tab, int64_t rows, uint32_t cols, uint32_t *chs, uint32_t *totals,
                  hipStream_t s, const int64_t *rows_dev);
+// bits to hold the values 0..v (host)
+inline int bits_for_host(uint32_t v) {
+  int b = 1;
+  while (b < 32 && (v >> b) != 0) ++b;
+  return b;
+}
 bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, int64_t n,
                       int begin_bit, int end_bit, uint32_t *hist, hipStream_t s);
 size_t radix_hist_entries(int64_t n);
@@ -186,6 +193,10 @@ struct TierIn {
   const Plan *pl;
 };
 void run_tiers(const TierIn &x, hipStream_t s);
+// per-dispatch row of every launch (see opattr_aggregate_dispatch)
+void launch_dispatch_keys(const int32_t *range_id, const int32_t *op, const opattr_ranges *r,
+                          uint32_t NOPS, int64_t T, int32_t *key, opattr_diag *diag,
+                          hipStream_t s);
 
 // ---- ranges and enclosure (ranges.hip, enclose.hip) ----------------------------
 CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws, const Plan &pl,

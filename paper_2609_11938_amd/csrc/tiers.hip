@@ -153,6 +153,39 @@ __global__ void __launch_bounds__(256) k_cov_finish(const unsigned long long *pa
   *cov = c;
 }
 
+// Per-dispatch key of each launch: its range when its operator (op[i], or
+// the range's own op when op is NULL) is the range's operator, else R + its
+// operator, else -1 (the last row, unattributed). Bad range ids and
+// operators are counted.
+__global__ void k_dispatch_keys(const int32_t *__restrict__ range_id, const int32_t *__restrict__ op,
+                                const uint32_t *__restrict__ r_op, int64_t R, uint32_t NOPS,
+                                int64_t T, int32_t *key, opattr_diag *diag) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  uint32_t bad = 0;
+  if (i < T) {
+    const int32_t rid = range_id[i];
+    const bool rok = rid >= 0 && (int64_t)rid < R;
+    const int32_t o = op ? op[i] : (rok ? (int32_t)r_op[rid] : -1);
+    if (rid < -1 || (int64_t)rid >= R) bad++;
+    if (op && (o < -1 || (o >= 0 && (uint32_t)o >= NOPS))) bad++;
+    const bool ook = o >= 0 && (uint32_t)o < NOPS;
+    int64_t k = -1;  // the last row, as an unattributed operator
+    if (rok && ook && (uint32_t)o == r_op[rid]) k = rid;
+    else if (ook) k = R + o;
+    key[i] = (int32_t)k;
+  }
+  const uint32_t b = wave_reduce_add(bad);
+  if (lane_id() == 0 && b) atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)b);
+}
+
+void launch_dispatch_keys(const int32_t *range_id, const int32_t *op, const opattr_ranges *r,
+                          uint32_t NOPS, int64_t T, int32_t *key, opattr_diag *diag,
+                          hipStream_t s) {
+  if (T > 0)
+    k_dispatch_keys<<<(unsigned)((T + 255) / 256), 256, 0, s>>>(range_id, op, r->op_id, r->n, NOPS,
+                                                                T, key, diag);
+}
+
 void run_tiers(const TierIn &x, hipStream_t s) {
   const Plan &pl = *x.pl;
   const int64_t want = (pl.T + 255) / 256;

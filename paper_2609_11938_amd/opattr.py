@@ -86,7 +86,8 @@ assert C.sizeof(opattr_diag) == 64
 
 EXPORTS = ("opattr_workspace_bytes", "opattr_diag_clear", "opattr_read_diag", "opattr_match",
            "opattr_dedup_broadcast", "opattr_dedup_classes", "opattr_tiers_workspace_bytes",
-           "opattr_tiers", "opattr_aggregate_ops", "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate",
+           "opattr_tiers", "opattr_aggregate_ops", "opattr_dispatch_workspace_bytes",
+           "opattr_aggregate_dispatch", "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate",
            "opattr_attribute", "opattr_set_probe_events", "opattr_set_class_key_bits",
            "opattr_strerror")
 PROBES = ("seq_view", "tl_hist", "pf_hist", "col_scan", "pf_slot", "tl_match", "dedup",
@@ -138,6 +139,13 @@ def library(path: str | None = None):
     L.opattr_aggregate_ops.argtypes = [P(opattr_kernels), P(opattr_profiled), vp, vp,
                                        P(opattr_dims), vp, vp, vp, vp, vp, sz, vp]
     L.opattr_aggregate_ops.restype = C.c_int
+    L.opattr_dispatch_workspace_bytes.argtypes = [P(opattr_kernels), P(opattr_profiled),
+                                                  P(opattr_ranges), P(opattr_dims)]
+    L.opattr_dispatch_workspace_bytes.restype = sz
+    L.opattr_aggregate_dispatch.argtypes = [P(opattr_kernels), P(opattr_profiled), vp, vp, vp,
+                                            P(opattr_ranges), P(opattr_dims), vp, vp, vp, vp, vp,
+                                            sz, vp]
+    L.opattr_aggregate_dispatch.restype = C.c_int
     L.opattr_set_class_key_bits.argtypes = [i]
     L.opattr_set_class_key_bits.restype = C.c_int
     L.opattr_set_probe_events.argtypes = [vp, i]
@@ -467,13 +475,44 @@ def opattr_aggregate_ops(dt: dict, match, op, agg_kind=None, flags=0, absent_mas
     return out
 
 
+def opattr_aggregate_dispatch(dt: dict, match, range_id, op=None, agg_kind=None, flags=0,
+                              absent_mask=0, ws: Workspace | None = None,
+                              stream=None) -> Outputs:
+    """Eq. 1 per operator dispatch (see opattr_aggregate_dispatch): R range
+    rows, then n_ops per-operator rows, then the unattributed row."""
+    import torch
+
+    L = library()
+    m = _Marshal(dt, flags, absent_mask)
+    dev = dt["counters"].device
+    G = m.R + dt["n_ops"] + 1
+    out = Outputs(table=torch.empty(G * 192, dtype=torch.uint8, device=dev),
+                  summary=torch.empty(40, dtype=torch.uint8, device=dev),
+                  diag=_new_diag(dev, stream))
+    ws = ws or Workspace(dev)
+    nbytes = L.opattr_dispatch_workspace_bytes(C.byref(m.k), C.byref(m.p), C.byref(m.r),
+                                               C.byref(m.d))
+    if nbytes == 0:
+        raise RuntimeError("opattr_aggregate_dispatch: too many ranges and operators")
+    buf = ws.get(nbytes)
+    k_keep, kp = _kinds(agg_kind)
+    rc = L.opattr_aggregate_dispatch(C.byref(m.k), C.byref(m.p), _p(match), _p(range_id), _p(op),
+                                     C.byref(m.r), C.byref(m.d), kp, _p(out["table"]),
+                                     _p(out["summary"]), _p(out["diag"]), _p(buf),
+                                     C.c_size_t(buf.numel()), _stream_handle(stream))
+    del k_keep
+    _check(rc, "opattr_aggregate_dispatch")
+    return out
+
+
 def attribute_tiered(dt: dict, policy=MISMATCH_PREFIX, corr_policy=MISMATCH_SKIP_NAME,
-                     agg_kind=None, flags=0, ws: Workspace | None = None,
+                     agg_kind=None, flags=0, dispatch=False, ws: Workspace | None = None,
                      stream=None) -> dict:
     """The tiered pipeline as a sequence of library calls on one stream:
     matching (with the dedup broadcast when a class map is given), the
-    enclosure walk, the tiers, and the operator table by tier operator.
-    Returns each call's outputs."""
+    enclosure walk, the tiers, the operator table by tier operator and,
+    with ``dispatch``, the per-dispatch table. Returns each call's
+    outputs."""
     ws = ws or Workspace(dt["seq"].device)
     m = opattr_match(dt, policy=policy, flags=flags, ws=ws, stream=stream)
     res = {"match": m}
@@ -485,6 +524,10 @@ def attribute_tiered(dt: dict, policy=MISMATCH_PREFIX, corr_policy=MISMATCH_SKIP
     a = opattr_aggregate_ops(dt, m["match"], t["op"], agg_kind=agg_kind, flags=flags, ws=ws,
                              stream=stream)
     res.update(walk=w, tiers=t, aggregate=a)
+    if dispatch:
+        res["dispatch"] = opattr_aggregate_dispatch(dt, m["match"], w["range_id"], t["op"],
+                                                    agg_kind=agg_kind, flags=flags, ws=ws,
+                                                    stream=stream)
     return res
 
 

@@ -154,3 +154,54 @@ def test_attribute_tiered_pipeline():
     np.testing.assert_array_equal(parity.host(res["match"]["match"]), match)
     _assert_tiers(res["tiers"], opattr.read_diag(res["tiers"]["diag"]), wt)
     parity.assert_table(res["aggregate"].table_host(), want["table"])
+
+
+def _gpu_dispatch(tr, match, range_id, op, flags=0):
+    import torch
+
+    dt = opattr.to_device(tr, DEV)
+    out = opattr.opattr_aggregate_dispatch(
+        dt, torch.from_numpy(np.ascontiguousarray(match, np.int32)).to(DEV),
+        torch.from_numpy(np.ascontiguousarray(range_id, np.int32)).to(DEV),
+        None if op is None else torch.from_numpy(np.ascontiguousarray(op, np.int32)).to(DEV),
+        flags=flags)
+    torch.cuda.synchronize()
+    return out, opattr.read_diag(out["diag"])
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_dispatch_parity(seed):
+    """The per-dispatch table (ranges, then per-operator rows, then the
+    unattributed row) against the oracle, with tier operators and without;
+    a few bad range ids and operators."""
+    print(f"case dispatch seed={seed}", flush=True)
+    tr = _tier_trace(seed, dedup=seed % 2 == 0)
+    match = O.attribute(tr, stages=["match", "dedup"])["match"]
+    t = O.tiers(tr)
+    rid, op = t["range_id"].copy(), t["op"].copy()
+    if seed % 3 == 2:
+        rid[:2] = [tr["r_start"].size + 1, -4]
+        op[2:4] = [tr["n_ops"], -2]
+    for o in (op, None):
+        want = O.aggregate_dispatch(tr, match, rid, o)
+        out, diag = _gpu_dispatch(tr, match, rid, o)
+        parity.assert_table(out.table_host(), want["table"])
+        assert diag["bad_records"] == want["diag"]["bad_records"]
+        assert diag["status"] == want["diag"]["status"]
+        parity.assert_summary(out.summary_host(), want["summary"])
+
+
+@pytest.mark.parametrize("cfg", ["gpt2", "sdpa", "large"])
+def test_dispatch_generated(cfg):
+    """Tens of thousands to half a million dispatch rows (one radix sort of
+    the items by row): the tiered pipeline's dispatch table against the
+    oracle's."""
+    print(f"case dispatch {cfg}", flush=True)
+    tr = tg.with_attribution_maps(tg.with_range_kinds(parity.trace(cfg, "stream_major")))
+    match = O.attribute(tr, stages=["match", "dedup"])["match"]
+    t = O.tiers(tr)
+    want = O.aggregate_dispatch(tr, match, t["range_id"], t["op"])
+    out, diag = _gpu_dispatch(tr, match, t["range_id"], t["op"], flags=HINTS)
+    parity.assert_table(out.table_host(), want["table"])
+    parity.assert_summary(out.summary_host(), want["summary"])
+    assert diag["status"] == want["diag"]["status"] == 0
