@@ -299,15 +299,17 @@ int opattr_aggregate_ops(const opattr_kernels *k, const opattr_profiled *p, cons
    launches attributed to operator o otherwise (no range, or a range of
    another operator); row r->n + n_ops the unattributed ones. Per row as
    opattr_aggregate (Eq. 1). Out: table[r->n + n_ops + 1], sum (device; the
-   last row counts as unattributed). Needs r->n + n_ops <= 2^20 - 2.
-   Workspace: opattr_dispatch_workspace_bytes. */
+   last row counts as unattributed), and row[k->n] (or NULL), the table row
+   of each launch. Needs r->n + n_ops <= 2^20 - 2. Workspace:
+   opattr_dispatch_workspace_bytes. */
 size_t opattr_dispatch_workspace_bytes(const opattr_kernels *k, const opattr_profiled *p,
                                        const opattr_ranges *r, const opattr_dims *d);
 int opattr_aggregate_dispatch(const opattr_kernels *k, const opattr_profiled *p,
                               const int32_t *match, const int32_t *range_id, const int32_t *op,
                               const opattr_ranges *r, const opattr_dims *d,
                               const uint8_t *agg_kind, opattr_op_row *table, opattr_summary *sum,
-                              opattr_diag *diag, void *ws, size_t ws_bytes, void *stream);
+                              int32_t *row, opattr_diag *diag, void *ws, size_t ws_bytes,
+                              void *stream);
 
 /* Layer class discovery (Sec. 3.7: structurally identical layers share one
    profiled representative). Two partitions are one class when the launches

@@ -654,7 +654,8 @@ int opattr_aggregate_dispatch(const opattr_kernels *k, const opattr_profiled *p,
                               const int32_t *match, const int32_t *range_id, const int32_t *op,
                               const opattr_ranges *r, const opattr_dims *d,
                               const uint8_t *agg_kind, opattr_op_row *table, opattr_summary *sum,
-                              opattr_diag *diag, void *ws, size_t ws_bytes, void *stream) {
+                              int32_t *row, opattr_diag *diag, void *ws, size_t ws_bytes,
+                              void *stream) {
   if (!check_dims(d) || !check_kernels(k, false, false, true) || !check_profiled(p, false, true) ||
       !r || !ok_n(r->n) || r->n + (int64_t)d->n_ops > (int64_t)kMaxOps || !diag || !table ||
       !sum || !kinds_ok(agg_kind) || (k->n > 0 && (!match || !range_id)) ||
@@ -667,7 +668,7 @@ int opattr_aggregate_dispatch(const opattr_kernels *k, const opattr_profiled *p,
   // per-launch rows in the launch-order view's space (unused here), then
   // the aggregation by those rows over an identity op table
   int32_t *key = at<int32_t>(ws, pl.sv);
-  launch_dispatch_keys(range_id, op, r, d->n_ops, pl.T, key, diag, s);
+  launch_dispatch_keys(range_id, op, r, d->n_ops, pl.T, key, row, diag, s);
   uint32_t *ident = at<uint32_t>(ws, pl.ident);
   launch_iota(ident, dd.n_ops, s);
   opattr_ranges rows{};

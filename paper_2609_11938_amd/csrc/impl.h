@@ -195,8 +195,8 @@ struct TierIn {
 void run_tiers(const TierIn &x, hipStream_t s);
 // per-dispatch row of every launch (see opattr_aggregate_dispatch)
 void launch_dispatch_keys(const int32_t *range_id, const int32_t *op, const opattr_ranges *r,
-                          uint32_t NOPS, int64_t T, int32_t *key, opattr_diag *diag,
-                          hipStream_t s);
+                          uint32_t NOPS, int64_t T, int32_t *key, int32_t *row,
+                          opattr_diag *diag, hipStream_t s);
 
 // ---- ranges and enclosure (ranges.hip, enclose.hip) ----------------------------
 CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws, const Plan &pl,

@@ -159,7 +159,7 @@ __global__ void __launch_bounds__(256) k_cov_finish(const unsigned long long *pa
 // operators are counted.
 __global__ void k_dispatch_keys(const int32_t *__restrict__ range_id, const int32_t *__restrict__ op,
                                 const uint32_t *__restrict__ r_op, int64_t R, uint32_t NOPS,
-                                int64_t T, int32_t *key, opattr_diag *diag) {
+                                int64_t T, int32_t *key, int32_t *row, opattr_diag *diag) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   uint32_t bad = 0;
   if (i < T) {
@@ -173,17 +173,18 @@ __global__ void k_dispatch_keys(const int32_t *__restrict__ range_id, const int3
     if (rok && ook && (uint32_t)o == r_op[rid]) k = rid;
     else if (ook) k = R + o;
     key[i] = (int32_t)k;
+    if (row) row[i] = (int32_t)(k >= 0 ? k : R + NOPS);
   }
   const uint32_t b = wave_reduce_add(bad);
   if (lane_id() == 0 && b) atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)b);
 }
 
 void launch_dispatch_keys(const int32_t *range_id, const int32_t *op, const opattr_ranges *r,
-                          uint32_t NOPS, int64_t T, int32_t *key, opattr_diag *diag,
-                          hipStream_t s) {
+                          uint32_t NOPS, int64_t T, int32_t *key, int32_t *row,
+                          opattr_diag *diag, hipStream_t s) {
   if (T > 0)
     k_dispatch_keys<<<(unsigned)((T + 255) / 256), 256, 0, s>>>(range_id, op, r->op_id, r->n, NOPS,
-                                                                T, key, diag);
+                                                                T, key, row, diag);
 }
 
 void run_tiers(const TierIn &x, hipStream_t s) {

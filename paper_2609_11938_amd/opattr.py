@@ -144,7 +144,7 @@ def library(path: str | None = None):
     L.opattr_dispatch_workspace_bytes.restype = sz
     L.opattr_aggregate_dispatch.argtypes = [P(opattr_kernels), P(opattr_profiled), vp, vp, vp,
                                             P(opattr_ranges), P(opattr_dims), vp, vp, vp, vp, vp,
-                                            sz, vp]
+                                            vp, sz, vp]
     L.opattr_aggregate_dispatch.restype = C.c_int
     L.opattr_set_class_key_bits.argtypes = [i]
     L.opattr_set_class_key_bits.restype = C.c_int
@@ -488,6 +488,7 @@ def opattr_aggregate_dispatch(dt: dict, match, range_id, op=None, agg_kind=None,
     G = m.R + dt["n_ops"] + 1
     out = Outputs(table=torch.empty(G * 192, dtype=torch.uint8, device=dev),
                   summary=torch.empty(40, dtype=torch.uint8, device=dev),
+                  row=torch.empty(m.T, dtype=torch.int32, device=dev),
                   diag=_new_diag(dev, stream))
     ws = ws or Workspace(dev)
     nbytes = L.opattr_dispatch_workspace_bytes(C.byref(m.k), C.byref(m.p), C.byref(m.r),
@@ -498,7 +499,7 @@ def opattr_aggregate_dispatch(dt: dict, match, range_id, op=None, agg_kind=None,
     k_keep, kp = _kinds(agg_kind)
     rc = L.opattr_aggregate_dispatch(C.byref(m.k), C.byref(m.p), _p(match), _p(range_id), _p(op),
                                      C.byref(m.r), C.byref(m.d), kp, _p(out["table"]),
-                                     _p(out["summary"]), _p(out["diag"]), _p(buf),
+                                     _p(out["summary"]), _p(out["row"]), _p(out["diag"]), _p(buf),
                                      C.c_size_t(buf.numel()), _stream_handle(stream))
     del k_keep
     _check(rc, "opattr_aggregate_dispatch")

@@ -205,3 +205,50 @@ def test_dispatch_generated(cfg):
     parity.assert_table(out.table_host(), want["table"])
     parity.assert_summary(out.summary_host(), want["summary"])
     assert diag["status"] == want["diag"]["status"] == 0
+
+
+def _same_doc(a, b, path="doc"):
+    """Equal JSON-like values, floats within the aggregation tolerance."""
+    if isinstance(a, dict):
+        assert isinstance(b, dict) and a.keys() == b.keys(), path
+        for k in a:
+            _same_doc(a[k], b[k], f"{path}.{k}")
+    elif isinstance(a, list):
+        assert isinstance(b, list) and len(a) == len(b), path
+        for i, (x, y) in enumerate(zip(a, b)):
+            _same_doc(x, y, f"{path}[{i}]")
+    elif isinstance(a, float) and isinstance(b, float):
+        assert abs(a - b) <= parity.RTOL * max(abs(a), abs(b)), (path, a, b)
+    else:
+        assert a == b, (path, a, b)
+
+
+def test_profile_from_gpu_outputs():
+    """profile.json built from the GPU pipeline's outputs (tiers, the walk's
+    range links, the per-dispatch rows and table) equals the one built from
+    the oracle's, GPT-2 with range kinds and both maps."""
+    import torch
+
+    from paper_2609_11938_amd import profile
+
+    print("case profile.json gpt2", flush=True)
+    tr = tg.with_attribution_maps(cases.with_kinds(parity.trace("gpt2", "stream_major"), 2,
+                                                   p_boundary=0.0, roots_boundary=True))
+    dt = opattr.to_device(tr, DEV)
+    res = opattr.attribute_tiered(dt, flags=HINTS, dispatch=True)
+    torch.cuda.synchronize()
+    h = parity.host
+    got = profile.build(tr, h(res["match"]["match"]), h(res["tiers"]["tier"]),
+                        h(res["tiers"]["op"]), h(res["tiers"]["fused"]), h(res["dispatch"]["row"]),
+                        res["dispatch"].table_host(), range_any=h(res["walk"]["range_any"]),
+                        range_parent=h(res["walk"]["range_parent"]))
+    match = O.attribute(tr, stages=["match", "dedup"])["match"]
+    t = O.tiers(tr)
+    walk = O.enclose_walk(tr)
+    disp = O.aggregate_dispatch(tr, match, t["range_id"], t["op"])
+    import brute
+    row = np.array(brute.dispatch_keys(tr, t["range_id"], t["op"]))
+    np.testing.assert_array_equal(h(res["dispatch"]["row"]), row)
+    want = profile.build(tr, match, t["tier"], t["op"], t["fused"], row, disp["table"],
+                         range_any=walk["range_any"], range_parent=walk["range_parent"])
+    _same_doc(got, want)
