@@ -216,9 +216,13 @@ def measure_next_rows(dt, tr, flags, steps, warmup, out, ws):
         ev[k][1].record()
         opattr.opattr_tiers(dtm, r["walk"]["range_id"], r["walk"]["fused"], flags=flags, ws=ws)
         ev[k][2].record()
+        opattr.opattr_aggregate_dispatch(dtm, r["match"]["match"], r["walk"]["range_id"],
+                                         r["tiers"]["op"], flags=flags, ws=ws)
+        ev[k][3].record()
     torch.cuda.synchronize()
     pipe_ms = statistics.mean(e[0].elapsed_time(e[1]) for e in ev)
     tiers_ms = statistics.mean(e[1].elapsed_time(e[2]) for e in ev)
+    disp_ms = statistics.mean(e[2].elapsed_time(e[3]) for e in ev)
     C_ = maps["corr_name"].size
     # opattr_tiers alone: the correlation join (seq, name per launch; name
     # per entry) and the tier pass (name, dur, range id, walk fused in;
@@ -234,6 +238,15 @@ def measure_next_rows(dt, tr, flags, steps, warmup, out, ws):
                           "unattributed": float(cov["frac"][0])},
         "tiers_call_ms": tiers_ms, "tiers_algorithmic_bytes": tier_bytes,
         "tiers_GBps": gbps, "tiers_frac": gbps / HBM_PEAK_GBPS}
+    # the per-dispatch table: range id, tier op, match, duration per launch,
+    # the op of each range, each counter row once; one row per dispatch out
+    G_disp = R + tr["n_ops"] + 1
+    disp_bytes = T * (4 + 4 + 4 + 4 + 4) + R * 4 + tr["pf_name"].size * 80 + G_disp * 192
+    dgbps = disp_bytes / (disp_ms * 1e-3) / 1e9
+    rows["dispatch_table"] = {
+        "call": "opattr_aggregate_dispatch", "rows": int(G_disp), "ms_per_call": disp_ms,
+        "records_per_s": T / (disp_ms * 1e-3), "algorithmic_bytes": disp_bytes,
+        "achieved_GBps": dgbps, "frac": dgbps / HBM_PEAK_GBPS}
 
     if NP:
         cflags = flags & (opattr.SEQ_DENSE | opattr.VALIDATE)

@@ -25,6 +25,14 @@
 namespace opa {
 
 constexpr int kWinItems = 64;     // sorted items per window (one wave)
+
+// A sorted item in 64 bits: partial-row index or first launch (31 bits, <
+// 2^31), reference length (5 bits, 0 for a partial row, else <= 16), and
+// its operator row (20 bits, < 2^20).
+static_assert(kMaxOps + 1 < (1u << 20), "operator rows fit the item's 20 row bits");
+__device__ __forceinline__ unsigned long long item_pack(uint32_t a, uint32_t b, uint32_t g) {
+  return (unsigned long long)a | ((unsigned long long)b << 31) | ((unsigned long long)g << 36);
+}
 constexpr uint32_t kHeavy = 256;  // partials above which a row takes a whole block
 
 EmitOut emit_out(void *ws, const Plan &pl) {
@@ -63,10 +71,11 @@ struct AggWork {
   AggIn in;
   const uint32_t *ig, *ia, *ib;
   const PartRow *rows;
-  int64_t *meta;  // [0] items, [1] partial rows, [2] item tiles, [3] heavy rows
+  int64_t *meta;  // [0] items, [1] partial rows, [2] item tiles, [3] heavy rows, [4] spread rows
   uint32_t *ith, *gcnt, *goff;
+  uint32_t *multi;          // rows spread over several windows
   uint32_t *heavy;          // rows spread over more than kHeavy windows
-  unsigned long long *sit;  // sorted items: partial-row index or first launch | length << 32
+  unsigned long long *sit;  // sorted items (item_pack)
   PartRow *part;            // [windows][2]: a continuing row's partial per window
   opattr_op_row *table;
   opattr_summary *sum;
@@ -133,6 +142,7 @@ __global__ void __launch_bounds__(1024) k_row_offsets(AggWork w) {
   if (threadIdx.x == 0) {
     w.goff[w.G] = tot;
     w.meta[3] = 0;
+    w.meta[4] = 0;
   }
 }
 
@@ -160,7 +170,7 @@ __device__ inline void item_scatter(const AggWork &w, int64_t n, uint16_t *cnt) 
       const uint32_t g = key[c];
       if (g >= w.G) continue;
       const int64_t x = item_x<PER>(tile, c);
-      w.sit[w.goff[g] + row[g] + wb[g] + rank[c]] = w.ia[x] | ((unsigned long long)w.ib[x] << 32);
+      w.sit[w.goff[g] + row[g] + wb[g] + rank[c]] = item_pack(w.ia[x], w.ib[x], g);
     }
   }
 }
@@ -184,11 +194,12 @@ __global__ void k_item_keys(AggWork w, unsigned long long *k0, uint32_t *v0, int
 }
 
 // sorted items in place
-__global__ void k_item_place(AggWork w, const uint32_t *val, int64_t cap) {
+__global__ void k_item_place(AggWork w, const unsigned long long *key, const uint32_t *val,
+                             int64_t cap) {
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= cap || p >= w.meta[0]) return;
   const uint32_t x = val[p];
-  w.sit[p] = w.ia[x] | ((unsigned long long)w.ib[x] << 32);
+  w.sit[p] = item_pack(w.ia[x], w.ib[x], (uint32_t)key[p]);
 }
 
 // row offsets: goff[g] = the first sorted item of row g or later (the
@@ -203,7 +214,10 @@ __global__ void k_row_bounds(AggWork w, const unsigned long long *key, int64_t c
     else hi = mid;
   }
   w.goff[g] = (uint32_t)lo;
-  if (g == 0) w.meta[3] = 0;
+  if (g == 0) {
+    w.meta[3] = 0;
+    w.meta[4] = 0;
+  }
 }
 
 // the row's table entry from its combined partial (lane c writes counter c)
@@ -254,17 +268,6 @@ __device__ __forceinline__ void write_row_lane(const AggWork &w, uint32_t g, con
   }
 }
 
-// the row holding sorted item p: the last g with goff[g] <= p
-__device__ __forceinline__ uint32_t row_of_item(const uint32_t *goff, uint32_t G, uint32_t p) {
-  uint32_t lo = 0, hi = G - 1;
-  while (lo < hi) {
-    const uint32_t mid = (lo + hi + 1) >> 1;
-    if (goff[mid] <= p) lo = mid;
-    else hi = mid - 1;
-  }
-  return lo;
-}
-
 // 2. one wave per window of 64 sorted items
 template <bool DEF>
 __global__ void __launch_bounds__(256) k_window_reduce(AggWork w) {
@@ -279,9 +282,9 @@ __global__ void __launch_bounds__(256) k_window_reduce(AggWork w) {
     Acc acc;
     acc_zero(acc);
     if (p < n) {
-      g = row_of_item(w.goff, w.G, (uint32_t)p);
       const unsigned long long it = w.sit[p];
-      const uint32_t a = (uint32_t)it, b = (uint32_t)(it >> 32);
+      const uint32_t a = (uint32_t)(it & 0x7FFFFFFFu), b = (uint32_t)(it >> 31) & 31u;
+      g = (uint32_t)(it >> 36);
       if (b == 0) {
         acc_load(acc, w.rows + a);
       } else {
@@ -312,36 +315,51 @@ __device__ __forceinline__ const PartRow *row_part(const AggWork &w, int64_t w0,
   return j == 0 ? w.part + 2 * w0 + 1 : w.part + 2 * (w0 + j);
 }
 
-// 3. one wave per operator row without items or spread over several
-// windows; rows over more than kHeavy windows are left to a block each
+// 3a. one thread per operator row: a row without items is written empty, a
+// row inside one window is done, a row spread over several windows is listed
+template <bool DEF>
+__global__ void __launch_bounds__(256) k_row_triage(AggWork w) {
+  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
+  const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= w.G) return;
+  const uint32_t lo = w.goff[g], hi = w.goff[g + 1];
+  if (hi == lo) {
+    Acc acc;
+    acc_zero(acc);
+    write_row_lane(w, g, acc, mx, dw);
+  } else if (lo / kWinItems != (hi - 1) / kWinItems) {
+    w.multi[atomicAdd((unsigned long long *)&w.meta[4], 1ull)] = g;
+  }
+}
+
+// 3b. one wave per listed row; rows over more than kHeavy windows are left
+// to a block each
 template <bool DEF>
 __global__ void __launch_bounds__(256) k_combine(AggWork w) {
   const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
-  const uint32_t g = blockIdx.x * 4 + wave_id();
-  if (g >= w.G) return;
+  const int64_t nm = w.meta[4];
   const int ln = lane_id();
-  const uint32_t lo = w.goff[g], hi = w.goff[g + 1];
-  Acc acc;
-  acc_zero(acc);
-  if (hi > lo) {
+  for (int64_t k = (int64_t)blockIdx.x * 4 + wave_id(); k < nm; k += (int64_t)gridDim.x * 4) {
+    const uint32_t g = w.multi[k];
+    const uint32_t lo = w.goff[g], hi = w.goff[g + 1];
     const int64_t w0 = lo / kWinItems, w1 = (hi - 1) / kWinItems;
-    if (w0 == w1) return;  // finalised in its window
     const uint32_t m = (uint32_t)(w1 - w0 + 1);
     if (m > kHeavy) {
       if (ln == 0) w.heavy[atomicAdd((unsigned long long *)&w.meta[3], 1ull)] = g;
-      return;
+      continue;
     }
+    Acc acc;
+    acc_zero(acc);
     for (uint32_t j = ln; j < m; j += OPA_WAVE) {
       Acc b;
       acc_load(b, row_part(w, w0, j));
       acc_merge(acc, b, mx);
     }
+    acc_wave_reduce(acc, mx);
+    write_row(w, g, acc, mx, dw);
   }
-  acc_wave_reduce(acc, mx);
-  write_row(w, g, acc, mx, dw);
 }
 
-// 3b. rows spread over many windows: a block each (the few heavy rows)
 constexpr int kHeavyThreads = 1024;
 
 template <bool DEF>
@@ -396,6 +414,7 @@ static AggWork agg_work(const EncArgs &x) {
   w.gcnt = at<uint32_t>(x.ws, pl.gcnt);
   w.goff = at<uint32_t>(x.ws, pl.goff);
   w.heavy = at<uint32_t>(x.ws, pl.heavy);
+  w.multi = at<uint32_t>(x.ws, pl.multi);
   w.sit = at<unsigned long long>(x.ws, pl.sit);
   w.part = at<PartRow>(x.ws, pl.part);
   w.table = x.table;
@@ -431,7 +450,9 @@ void plan_items(const EncArgs &x, hipStream_t s) {
                              reinterpret_cast<uint64_t *>(k1), v1, cap, 0, bits,
                              at<uint32_t>(x.ws, pl.isort_hist), s);
     }
-    if (cap > 0) k_item_place<<<(unsigned)((cap + 255) / 256), 256, 0, s>>>(w, in1 ? v1 : v0, cap);
+    if (cap > 0)
+      k_item_place<<<(unsigned)((cap + 255) / 256), 256, 0, s>>>(w, in1 ? k1 : k0, in1 ? v1 : v0,
+                                                                 cap);
     k_row_bounds<<<(pl.G + 1 + 255) / 256, 256, 0, s>>>(w, in1 ? k1 : k0, cap);
   }
   probe_end(OPATTR_PROBE_ITEM_SORT, s);
@@ -448,11 +469,15 @@ void reduce_items(const EncArgs &x, hipStream_t s) {
     if (def) k_window_reduce<true><<<cgrid, 256, 0, s>>>(w);
     else k_window_reduce<false><<<cgrid, 256, 0, s>>>(w);
   }
+  const unsigned tg = (pl.G + 255) / 256;
+  const unsigned cg = (unsigned)((pl.G + 3) / 4 < 1024 ? (pl.G + 3) / 4 : 1024);
   if (def) {
-    k_combine<true><<<(pl.G + 3) / 4, 256, 0, s>>>(w);
+    k_row_triage<true><<<tg, 256, 0, s>>>(w);
+    k_combine<true><<<cg, 256, 0, s>>>(w);
     k_combine_heavy<true><<<64, kHeavyThreads, 0, s>>>(w);
   } else {
-    k_combine<false><<<(pl.G + 3) / 4, 256, 0, s>>>(w);
+    k_row_triage<false><<<tg, 256, 0, s>>>(w);
+    k_combine<false><<<cg, 256, 0, s>>>(w);
     k_combine_heavy<false><<<64, kHeavyThreads, 0, s>>>(w);
   }
   probe_end(OPATTR_PROBE_AGGREGATE, s);

@@ -131,6 +131,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.gcnt = b.take((size_t)pl.G * 4);
   pl.goff = b.take(((size_t)pl.G + 1) * 4);
   pl.heavy = b.take((size_t)pl.G * 4);
+  pl.multi = b.take((size_t)pl.G * 4);
   pl.sit = b.take((size_t)pl.cap_items * 8);
   pl.part = b.take((size_t)pl.max_windows * 2 * 200);
   // class discovery: per partition, and the key table
@@ -145,6 +146,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.c_tkey = b.take(TS * 8);
   pl.c_tmin = b.take(TS * 4);
   pl.ident = b.take((size_t)d->n_ops * 4);
+  pl.sumpart = b.take((size_t)kSumBlocks * 4 * 8);
   pl.misc = b.take(256);
   pl.total = b.off;
   return pl;
@@ -155,14 +157,40 @@ static bool ws_ok(const void *ws, size_t ws_bytes, const Plan &pl) {
   return ws && (reinterpret_cast<uintptr_t>(ws) & 255) == 0 && ws_bytes >= pl.total;
 }
 
+// the summary's four sums over a stretch of table rows, per block
+__global__ void __launch_bounds__(256) k_summary_part(const opattr_op_row *table, uint32_t G,
+                                                      uint32_t NOPS, unsigned long long *part) {
+  __shared__ unsigned long long red[4][4];
+  unsigned long long at_ = 0, un = 0, tot = 0, mt = 0;
+  for (uint32_t g = blockIdx.x * blockDim.x + threadIdx.x; g < G; g += gridDim.x * blockDim.x) {
+    const unsigned long long t = table[g].total_ns;
+    tot += t;
+    mt += table[g].matched_ns;
+    if (g < NOPS) at_ += t;
+    else un += t;
+  }
+  at_ = wave_reduce_add(at_);
+  un = wave_reduce_add(un);
+  tot = wave_reduce_add(tot);
+  mt = wave_reduce_add(mt);
+  if (lane_id() == 0) {
+    red[0][wave_id()] = at_;
+    red[1][wave_id()] = un;
+    red[2][wave_id()] = tot;
+    red[3][wave_id()] = mt;
+  }
+  __syncthreads();
+  if (threadIdx.x < 4)
+    part[blockIdx.x * 4 + threadIdx.x] =
+        red[threadIdx.x][0] + red[threadIdx.x][1] + red[threadIdx.x][2] + red[threadIdx.x][3];
+}
+
 // nesting_errors from the per-stream crossing flags; status from the flags;
-// with a table, the summary over its rows (one block)
+// with a table, the summary from the per-block sums (one block)
 __global__ void __launch_bounds__(1024) k_finish(opattr_diag *diag, const uint8_t *sflag,
-                                                 uint32_t ns, const opattr_op_row *table,
-                                                 opattr_summary *sum, uint32_t G,
-                                                 uint32_t NOPS) {
+                                                 uint32_t ns, const unsigned long long *part,
+                                                 int nparts, opattr_summary *sum) {
   __shared__ uint32_t cnt;
-  __shared__ unsigned long long red[4][16];
   if (threadIdx.x == 0) cnt = 0;
   __syncthreads();
   if (sflag) {
@@ -170,34 +198,14 @@ __global__ void __launch_bounds__(1024) k_finish(opattr_diag *diag, const uint8_
     for (uint32_t s = threadIdx.x; s < ns; s += blockDim.x) c += sflag[s] ? 1u : 0u;
     if (c) atomicAdd(&cnt, c);
   }
-  if (table) {
-    unsigned long long at_ = 0, un = 0, tot = 0, mt = 0;
-    for (uint32_t g = threadIdx.x; g < G; g += blockDim.x) {
-      const unsigned long long t = table[g].total_ns;
-      tot += t;
-      mt += table[g].matched_ns;
-      if (g < NOPS) at_ += t;
-      else un += t;
-    }
-    at_ = wave_reduce_add(at_);
-    un = wave_reduce_add(un);
-    tot = wave_reduce_add(tot);
-    mt = wave_reduce_add(mt);
-    if (lane_id() == 0) {
-      red[0][wave_id()] = at_;
-      red[1][wave_id()] = un;
-      red[2][wave_id()] = tot;
-      red[3][wave_id()] = mt;
-    }
-  }
   __syncthreads();
-  if (threadIdx.x == 0 && table) {
+  if (threadIdx.x == 0 && part) {
     opattr_summary s{};
-    for (uint32_t k = 0; k < blockDim.x / OPA_WAVE; ++k) {
-      s.attributed_ns += red[0][k];
-      s.unattributed_ns += red[1][k];
-      s.total_ns += red[2][k];
-      s.matched_ns += red[3][k];
+    for (int b = 0; b < nparts; ++b) {
+      s.attributed_ns += part[b * 4 + 0];
+      s.unattributed_ns += part[b * 4 + 1];
+      s.total_ns += part[b * 4 + 2];
+      s.matched_ns += part[b * 4 + 3];
     }
     s.attributed_fraction = s.total_ns ? (double)s.attributed_ns / (double)s.total_ns
                                        : __longlong_as_double(0x7FF8000000000000ll);
@@ -223,9 +231,16 @@ __global__ void __launch_bounds__(1024) k_finish(opattr_diag *diag, const uint8_
 }
 
 void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s,
-                   const opattr_op_row *table, opattr_summary *sum, uint32_t G, uint32_t NOPS) {
+                   const opattr_op_row *table, opattr_summary *sum, uint32_t G, uint32_t NOPS,
+                   unsigned long long *part) {
   probe_begin(OPATTR_PROBE_FINALIZE, s);
-  k_finish<<<1, 1024, 0, s>>>(diag, sflag, ns, table, sum, G, NOPS);
+  int nb = 0;
+  if (table) {
+    const uint32_t want = (G + 255) / 256;
+    nb = (int)(want < (uint32_t)kSumBlocks ? (want > 0 ? want : 1) : kSumBlocks);
+    k_summary_part<<<nb, 256, 0, s>>>(table, G, NOPS, part);
+  }
+  k_finish<<<1, 1024, 0, s>>>(diag, sflag, ns, table ? part : nullptr, nb, sum);
   probe_end(OPATTR_PROBE_FINALIZE, s);
 }
 
@@ -477,7 +492,8 @@ int opattr_aggregate(const opattr_kernels *k, const opattr_profiled *p, const in
   e.ws = ws;
   e.pl = &pl;
   run_aggregate_all(e, s);
-  launch_finish(diag, nullptr, 0, s, table, sum, pl.G, d->n_ops);
+  launch_finish(diag, nullptr, 0, s, table, sum, pl.G, d->n_ops,
+                at<unsigned long long>(ws, pl.sumpart));
   return launch_status();
 }
 
@@ -540,7 +556,8 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   reduce_runs(e, s);
   if (ss) note(hipStreamWaitEvent(s, ss->join3, 0));
   reduce_items(e, s);
-  launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s, table, sum, pl.G, d->n_ops);
+  launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s, table, sum, pl.G, d->n_ops,
+                at<unsigned long long>(ws, pl.sumpart));
   return launch_status();
 }
 
@@ -632,7 +649,8 @@ int opattr_aggregate_ops(const opattr_kernels *k, const opattr_profiled *p, cons
   e.ws = ws;
   e.pl = &pl;
   run_aggregate_all(e, s);
-  launch_finish(diag, nullptr, 0, s, table, sum, pl.G, d->n_ops);
+  launch_finish(diag, nullptr, 0, s, table, sum, pl.G, d->n_ops,
+                at<unsigned long long>(ws, pl.sumpart));
   return launch_status();
 }
 
@@ -688,7 +706,8 @@ int opattr_aggregate_dispatch(const opattr_kernels *k, const opattr_profiled *p,
   e.ws = ws;
   e.pl = &pl;
   run_aggregate_all(e, s);
-  launch_finish(diag, nullptr, 0, s, table, sum, pl.G, dd.n_ops);
+  launch_finish(diag, nullptr, 0, s, table, sum, pl.G, dd.n_ops,
+                at<unsigned long long>(ws, pl.sumpart));
   return launch_status();
 }
 

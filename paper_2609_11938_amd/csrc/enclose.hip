@@ -326,7 +326,12 @@ __global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
       // containing it (touching, not nested); any other enclosing range is
       // an ancestor. So the walk depends on the query point only through
       // "the innermost range starts at it", which keys the cache with rid.
-      const bool touch = rid >= 0 && (uint64_t)a.cr.s[rid] == q[k];
+      bool touch = false;
+      if (rid >= 0 && (a.cr.kind || a.fused)) {
+        const int64_t x = rid - wlo;
+        const uint64_t sr = (staged && st[k] == s0 && x >= 0 && x < wn) ? sS[x] : a.cr.s[rid];
+        touch = sr == q[k];
+      }
       if (rid >= 0 && (rid != rlast || touch != tlast)) {
         rlast = rid;
         tlast = touch;

@@ -26,6 +26,7 @@ constexpr uint32_t kFastNames = 4096;
 constexpr int kMaxWalk = 300;       // bound on parent-chain walks (depth <= 255)
 constexpr uint32_t kMaxNames = (1u << 20) - 1;  // names and rows are packed above a 12-bit slot
 constexpr uint32_t kMaxOps = (1u << 20) - 2;    // rows = n_ops + 1
+constexpr int kSumBlocks = 256;  // blocks of the summary's first pass over the table
 
 // Byte offsets of every scratch array inside the caller's workspace.
 struct Plan {
@@ -44,11 +45,12 @@ struct Plan {
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
   // aggregation
   int64_t cap_items, cap_rows, max_windows;
-  size_t wi, wr, hmb, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, heavy, sit, part;
+  size_t wi, wr, hmb, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, heavy, multi, sit, part;
   size_t isort_k0, isort_k1, isort_v0, isort_v1, isort_hist;  // item sort, many rows
   // dedup class discovery
   size_t c_first, c_last, c_runs, c_key, c_cand, c_fail, c_list, c_tkey, c_tmin;
-  size_t ident;  // 0 .. n_ops - 1 (aggregation by a given operator)
+  size_t ident;    // 0 .. n_ops - 1 (aggregation by a given operator)
+  size_t sumpart;  // per-block sums of the summary
   size_t misc;   // small device scalars
 };
 
@@ -258,6 +260,6 @@ void reduce_items(const EncArgs &a, hipStream_t s);
 // (rows below NOPS attributed)
 void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s,
                    const opattr_op_row *table = nullptr, opattr_summary *sum = nullptr,
-                   uint32_t G = 0, uint32_t NOPS = 0);
+                   uint32_t G = 0, uint32_t NOPS = 0, unsigned long long *part = nullptr);
 
 }  // namespace opa

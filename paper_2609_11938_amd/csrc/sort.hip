@@ -77,6 +77,62 @@ __global__ void __launch_bounds__(1024) k_scan_excl_oop(const uint32_t *__restri
   if (threadIdx.x == 0 && total_out) *total_out = carry;
 }
 
+// Exclusive scan of a long array in three passes: the sum of every
+// 4096-element chunk (one block each), a one-block scan of the chunk sums,
+// and each chunk scanned from its base.
+constexpr int kScanChunk = 4096;
+
+__global__ void __launch_bounds__(256) k_chunk_sums(const uint32_t *__restrict__ a, int64_t n,
+                                                    uint32_t *__restrict__ sums) {
+  __shared__ uint32_t sh[4];
+  const int64_t base = (int64_t)blockIdx.x * kScanChunk;
+  uint32_t v = 0;
+  for (int k = threadIdx.x; k < kScanChunk; k += 256) {
+    const int64_t x = base + k;
+    if (x < n) v += a[x];
+  }
+  uint32_t tot;
+  block_excl_scan_add<uint32_t>(v, sh, &tot);
+  if (threadIdx.x == 0) sums[blockIdx.x] = tot;
+}
+
+__global__ void __launch_bounds__(256) k_chunk_scan(uint32_t *__restrict__ a, int64_t n,
+                                                    const uint32_t *__restrict__ sums) {
+  __shared__ uint32_t sh[4];
+  constexpr int kPerThread = kScanChunk / 256;
+  const int64_t base = (int64_t)blockIdx.x * kScanChunk + (int64_t)threadIdx.x * kPerThread;
+  uint32_t v[kPerThread];
+  uint32_t t = 0;
+#pragma unroll
+  for (int k = 0; k < kPerThread; ++k) {
+    const int64_t x = base + k;
+    v[k] = x < n ? a[x] : 0u;
+    t += v[k];
+  }
+  uint32_t run = sums[blockIdx.x] + block_excl_scan_add<uint32_t>(t, sh, nullptr);
+#pragma unroll
+  for (int k = 0; k < kPerThread; ++k) {
+    const int64_t x = base + k;
+    if (x < n) a[x] = run;
+    run += v[k];
+  }
+}
+
+size_t scan_scratch_entries(int64_t n) { return (size_t)((n + kScanChunk - 1) / kScanChunk) + 1; }
+
+// in place; scratch holds scan_scratch_entries(n) entries
+void scan_excl_inplace(uint32_t *a, int64_t n, uint32_t *scratch, hipStream_t s) {
+  if (n <= 0) return;
+  if (n <= 16 * kScanChunk) {
+    k_scan_excl_u32<<<1, 1024, 0, s>>>(a, n);
+    return;
+  }
+  const int64_t nb = (n + kScanChunk - 1) / kScanChunk;
+  k_chunk_sums<<<(unsigned)nb, 256, 0, s>>>(a, n, scratch);
+  k_scan_excl_u32<<<1, 1024, 0, s>>>(scratch, nb);
+  k_chunk_scan<<<(unsigned)nb, 256, 0, s>>>(a, n, scratch);
+}
+
 void launch_scan_excl(const uint32_t *in, uint32_t *out, int64_t n, int64_t *total_out,
                       hipStream_t s) {
   k_scan_excl_oop<<<1, 1024, 0, s>>>(in, out, n, total_out);
@@ -127,9 +183,11 @@ __global__ void __launch_bounds__(256) k_rs_scatter(const uint64_t *__restrict__
   }
 }
 
+// the digit histograms of every tile, then the scan's chunk sums
 size_t radix_hist_entries(int64_t n) {
   const int64_t nt = (n + OPA_TILE - 1) / OPA_TILE;
-  return (size_t)(nt > 0 ? nt : 1) * 256;
+  const int64_t h = (nt > 0 ? nt : 1) * 256;
+  return (size_t)h + scan_scratch_entries(h);
 }
 
 bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, int64_t n,
@@ -141,7 +199,7 @@ bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, in
     uint64_t *ki = in1 ? k1 : k0, *ko = in1 ? k0 : k1;
     uint32_t *vi = in1 ? v1 : v0, *vo = in1 ? v0 : v1;
     k_rs_hist<<<(unsigned)nt, 256, 0, s>>>(ki, n, sh, hist, nt);
-    k_scan_excl_u32<<<1, 1024, 0, s>>>(hist, nt * 256);
+    scan_excl_inplace(hist, nt * 256, hist + nt * 256, s);
     k_rs_scatter<<<(unsigned)nt, 256, 0, s>>>(ki, vi, ko, vo, n, sh, hist, nt);
     in1 = !in1;
   }
