@@ -396,6 +396,51 @@ static int range_ok(const oref_ranges *r, const oref_dims *d, int64_t x) {
          (!r->kind || r->kind[x] <= OREF_KIND_SKIP);
 }
 
+/* valid ranges in nesting order per stream: (stream, start asc, end desc,
+   index asc); an identical interval with a lower index is the outer one */
+static key3 *nesting_order(const oref_ranges *r, const oref_dims *d, int64_t *nr_out) {
+  key3 *rs = xcalloc((size_t)r->n, sizeof(key3));
+  int64_t nr = 0;
+  for (int64_t x = 0; x < r->n; ++x) {
+    if (!range_ok(r, d, x)) continue;
+    rs[nr].a = r->stream_id[x];
+    rs[nr].b = r->start_ns[x];
+    rs[nr].c = UINT64_MAX - r->end_ns[x];
+    rs[nr].idx = x;
+    nr++;
+  }
+  qsort(rs, (size_t)nr, sizeof(key3), cmp_key3);
+  *nr_out = nr;
+  return rs;
+}
+
+/* kernels on a valid stream, per stream by query point */
+static key3 *kernels_by_query(const oref_kernels *k, const oref_dims *d, const uint64_t *q,
+                              int64_t *nk_out) {
+  key3 *ks = xcalloc((size_t)k->n, sizeof(key3));
+  int64_t nk = 0;
+  for (int64_t i = 0; i < k->n; ++i) {
+    if (k->stream_id[i] >= d->n_streams) continue;
+    ks[nk].a = k->stream_id[i];
+    ks[nk].b = q[i];
+    ks[nk].c = 0;
+    ks[nk].idx = i;
+    nk++;
+  }
+  qsort(ks, (size_t)nk, sizeof(key3), cmp_key3);
+  *nk_out = nk;
+  return ks;
+}
+
+/* the sweep's stack at query point t: every range of the stream that has
+   started (s <= t) pushed in nesting order, then the finished ones (e < t)
+   dropped from the top (closed intervals) */
+static void stack_advance(const key3 *rs, int64_t a_end, int64_t *x, int64_t *stack,
+                          int64_t *top, const oref_ranges *r, uint64_t t) {
+  while (*x < a_end && rs[*x].b <= t) stack[(*top)++] = rs[(*x)++].idx;
+  while (*top > 0 && r->end_ns[stack[*top - 1]] < t) (*top)--;
+}
+
 int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,
                  int32_t *range_id, uint8_t *range_depth, oref_diag *diag) {
   return oref_enclose_walk(k, r, d, range_id, NULL, NULL, NULL, range_depth, diag);
@@ -420,34 +465,14 @@ int oref_enclose_walk(const oref_kernels *k, const oref_ranges *r, const oref_di
   if (range_parent)
     for (int64_t x = 0; x < R; ++x) range_parent[x] = -1;
 
-  /* ranges in nesting order per stream: (stream, start asc, end desc, index
-     asc); an identical interval with a lower index is the outer one */
-  key3 *rs = xcalloc((size_t)R, sizeof(key3));
-  int64_t nr = 0;
-  for (int64_t x = 0; x < R; ++x) {
-    if (!range_ok(r, d, x)) continue;
-    rs[nr].a = r->stream_id[x];
-    rs[nr].b = r->start_ns[x];
-    rs[nr].c = UINT64_MAX - r->end_ns[x];
-    rs[nr].idx = x;
-    nr++;
-  }
-  qsort(rs, (size_t)nr, sizeof(key3), cmp_key3);
-  /* kernels per stream by query point */
-  key3 *ks = xcalloc((size_t)T, sizeof(key3));
-  int64_t nk = 0;
   for (int64_t i = 0; i < T; ++i) {
     range_id[i] = -1;
     if (fused) fused[i] = 0;
     if (range_any) range_any[i] = -1;
-    if (k->stream_id[i] >= NS) continue;
-    ks[nk].a = k->stream_id[i];
-    ks[nk].b = q[i];
-    ks[nk].c = 0;
-    ks[nk].idx = i;
-    nk++;
   }
-  qsort(ks, (size_t)nk, sizeof(key3), cmp_key3);
+  int64_t nr, nk;
+  key3 *rs = nesting_order(r, d, &nr);
+  key3 *ks = kernels_by_query(k, d, q, &nk);
 
   int64_t *stack = xcalloc((size_t)nr + 1, sizeof(int64_t));
   uint32_t *depth = xcalloc((size_t)R, sizeof(uint32_t));
@@ -495,9 +520,8 @@ int oref_enclose_walk(const oref_kernels *k, const oref_ranges *r, const oref_di
     top = 0;
     int64_t x = a;
     for (int64_t y = b; y < b_end; ++y) {
-      uint64_t t = ks[y].b;
-      while (x < a_end && rs[x].b <= t) stack[top++] = rs[x++].idx;
-      while (top > 0 && r->end_ns[stack[top - 1]] < t) top--;
+      const uint64_t t = ks[y].b;
+      stack_advance(rs, a_end, &x, stack, &top, r, t);
       const int64_t i = ks[y].idx;
       if (range_any) range_any[i] = top > 0 ? (int32_t)stack[top - 1] : -1;
       int32_t first = -1;
@@ -518,6 +542,66 @@ int oref_enclose_walk(const oref_kernels *k, const oref_ranges *r, const oref_di
     b = b_end;
   }
   free(rs); free(ks); free(stack); free(depth);
+  return 0;
+}
+
+/* All enclosing ranges (the all_enclosing output of Alg. 2) as CSR lists:
+   for each kernel, every valid range of its stream containing its query
+   point, innermost first. The same sweep as the walk: at a kernel's point
+   the stack holds, bottom to top in nesting order, the ranges that have
+   started; those not ended before the point are the enclosing ones. */
+int oref_enclose_all(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,
+                     int64_t *off, int32_t *ids, int64_t cap, oref_diag *diag) {
+  if (!k || !r || !d || !off || !diag || k->n < 0 || r->n < 0 || cap < 0) return OREF_ERR_ARG;
+  if (cap > 0 && !ids) return OREF_ERR_ARG;
+  if (k->n > 0 && (!k->stream_id || !(k->query_ns || k->start_ns))) return OREF_ERR_ARG;
+  const int64_t T = k->n, R = r->n;
+  const uint32_t NS = d->n_streams;
+  const uint64_t *q = k->query_ns ? k->query_ns : k->start_ns;
+  for (int64_t x = 0; x < R; ++x)
+    if (!range_ok(r, d, x)) diag->bad_records++;
+  for (int64_t i = 0; i < T; ++i)
+    if (k->stream_id[i] >= NS) diag->bad_records++;
+  if (diag->bad_records) diag->flags |= OREF_F_DATA;
+
+  int64_t nr, nk;
+  key3 *rs = nesting_order(r, d, &nr);
+  key3 *ks = kernels_by_query(k, d, q, &nk);
+
+  /* first pass: the count per kernel; second pass: the lists */
+  int64_t *cnt = xcalloc((size_t)T + 1, sizeof(int64_t));
+  int64_t *stack = xcalloc((size_t)nr + 1, sizeof(int64_t));
+  for (int pass = 0; pass < 2; ++pass) {
+    int64_t a = 0, b = 0;
+    while (a < nr || b < nk) {
+      uint64_t st = a < nr ? rs[a].a : UINT64_MAX;
+      if (b < nk && ks[b].a < st) st = ks[b].a;
+      int64_t a_end = a, b_end = b;
+      while (a_end < nr && rs[a_end].a == st) a_end++;
+      while (b_end < nk && ks[b_end].a == st) b_end++;
+      int64_t top = 0, x = a;
+      for (int64_t y = b; y < b_end; ++y) {
+        const uint64_t t = ks[y].b;
+        stack_advance(rs, a_end, &x, stack, &top, r, t);
+        const int64_t i = ks[y].idx;
+        int64_t c = 0;
+        for (int64_t u = top - 1; u >= 0; --u) {
+          const int64_t id = stack[u];
+          if (r->end_ns[id] < t) continue; /* ended before the point */
+          if (pass == 1 && off[i + 1] <= cap) ids[off[i] + c] = (int32_t)id;
+          c++;
+        }
+        if (pass == 0) cnt[i] = c;
+      }
+      a = a_end;
+      b = b_end;
+    }
+    if (pass == 0) {
+      off[0] = 0;
+      for (int64_t i = 0; i < T; ++i) off[i + 1] = off[i] + cnt[i];
+    }
+  }
+  free(rs); free(ks); free(stack); free(cnt);
   return 0;
 }
 

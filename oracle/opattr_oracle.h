@@ -125,6 +125,13 @@ int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d
 int oref_enclose_walk(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,
                       int32_t *range_id, uint8_t *fused, int32_t *range_any,
                       int32_t *range_parent, uint8_t *range_depth, oref_diag *diag);
+/* All enclosing ranges per kernel as CSR lists (Alg. 2's all_enclosing):
+   ids[off[i] .. off[i+1]) = every valid range of the kernel's stream whose
+   closed interval holds its query point, innermost first (reverse nesting
+   order; kinds are not consulted). off has k->n + 1 entries and is always
+   written; ids (capacity cap) receives the lists that end within cap. */
+int oref_enclose_all(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,
+                     int64_t *off, int32_t *ids, int64_t cap, oref_diag *diag);
 int oref_aggregate(const oref_kernels *k, const oref_profiled *p,
                    const int32_t *match, const int32_t *range_id,
                    const oref_ranges *r, const oref_dims *d, const uint8_t *agg_kind,

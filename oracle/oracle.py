@@ -127,6 +127,8 @@ def load(path: str):
     L.oref_dedup_classes.argtypes = [P(Kernels), P(Dims), C.c_void_p, P(Diag)]
     L.oref_aggregate_ops.argtypes = [P(Kernels), P(Profiled), C.c_void_p, C.c_void_p, P(Dims),
                                      C.c_void_p, C.c_void_p, P(Summary), P(Diag)]
+    L.oref_enclose_all.argtypes = [P(Kernels), P(Ranges), P(Dims), C.c_void_p, C.c_void_p,
+                                   C.c_int64, P(Diag)]
     L.oref_aggregate_dispatch.argtypes = [P(Kernels), P(Profiled), C.c_void_p, C.c_void_p,
                                           C.c_void_p, P(Ranges), P(Dims), C.c_void_p,
                                           C.c_void_p, P(Summary), P(Diag)]
@@ -136,7 +138,7 @@ def load(path: str):
     L.oref_diag_finish.argtypes = [P(Diag), C.c_int]
     for f in ("oref_match", "oref_dedup", "oref_enclose", "oref_enclose_walk", "oref_aggregate",
               "oref_dedup_classes", "oref_aggregate_ops", "oref_tiers",
-              "oref_aggregate_dispatch"):
+              "oref_aggregate_dispatch", "oref_enclose_all"):
         getattr(L, f).restype = C.c_int
     return L
 
@@ -392,3 +394,25 @@ def aggregate_dispatch(tr, match, range_id, op=None, agg_kind=None, absent_mask=
     L.oref_diag_finish(C.byref(dg), PREFIX)
     return {"table": table, "summary": {f: getattr(sm, f) for f, _ in Summary._fields_},
             "diag": diag_dict(dg)}
+
+
+def enclose_all(tr, library=None):
+    """All enclosing ranges of every kernel (Alg. 2's all_enclosing) as CSR:
+    ``off`` (T + 1) and ``ids``, innermost first."""
+    L = library if library is not None else lib()
+    x = _Inputs(tr)
+    T = x.seq.size
+    off = np.empty(T + 1, dtype=np.int64)
+    dg = Diag()
+    rc = L.oref_enclose_all(C.byref(x.k), C.byref(x.r), C.byref(x.d), _ptr(off), None, 0,
+                            C.byref(dg))
+    if rc:
+        raise ValueError(f"oref_enclose_all: {rc}")
+    ids = np.empty(max(int(off[-1]), 1), dtype=np.int32)
+    dg = Diag()
+    rc = L.oref_enclose_all(C.byref(x.k), C.byref(x.r), C.byref(x.d), _ptr(off), _ptr(ids),
+                            int(off[-1]), C.byref(dg))
+    if rc:
+        raise ValueError(f"oref_enclose_all: {rc}")
+    L.oref_diag_finish(C.byref(dg), PREFIX)
+    return {"off": off, "ids": ids[:int(off[-1])], "diag": diag_dict(dg)}

@@ -135,6 +135,22 @@ def _range_valid(tr, r):
             and (kind is None or int(kind[r]) <= 2))
 
 
+def enclosing_lists(tr):
+    """Per kernel: every valid range of its stream whose closed interval holds
+    its query point, innermost first (reverse nesting order)."""
+    T, R = tr["seq"].size, tr["r_start"].size
+    q = tr.get("query_ns")
+    q = tr["start_ns"] if q is None else q
+    rs, re, rst = tr["r_start"], tr["r_end"], tr["r_stream"]
+    out = []
+    for i in range(T):
+        enc = [r for r in range(R) if _range_valid(tr, r) and rst[r] == tr["stream_id"][i]
+               and tr["stream_id"][i] < tr["n_streams"] and int(rs[r]) <= int(q[i]) <= int(re[r])]
+        enc.sort(key=lambda r: (int(rs[r]), -int(re[r]), r))
+        out.append(enc[::-1])
+    return out
+
+
 def enclose_walk(tr):
     """Alg. 2 written out per kernel: the valid ranges of its stream that
     contain its query point, outermost first in nesting order, are walked

@@ -801,3 +801,54 @@ def test_dispatch_rows_add_up_to_operator_rows(seed):
     cnt = np.bincount(t["range_id"][t["range_id"] >= 0], minlength=R)
     np.testing.assert_array_equal(plain["kernel_count"][:R], cnt)
     assert plain["kernel_count"][R:R + NOPS].sum() == 0
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_enclose_all_matches_brute_force(seed):
+    """Every enclosing range of every kernel, innermost first, against the
+    containment test written out per kernel; coarse timestamps put many
+    launches on range edges (closed intervals: a range ending at the point
+    contains it). The walk's outputs are read off the same lists: range_any
+    is the first entry, range_id the first op before a boundary, fused more
+    than one op before it."""
+    tr = cases.random_trace(960 + seed, T=120, R=60, S=1 + seed % 3, t_max=40 + 20 * (seed % 3),
+                            max_depth=5)
+    tr = cases.with_kinds(tr, seed, p_bad=0.05 if seed % 4 == 3 else 0.0)
+    out = O.enclose_all(tr)
+    want = brute.enclosing_lists(tr)
+    off, ids = out["off"], out["ids"]
+    assert off[0] == 0 and off[-1] == sum(len(w) for w in want)
+    for i, w in enumerate(want):
+        assert list(ids[off[i]:off[i + 1]]) == w, i
+    walk = O.enclose_walk(tr)
+    kind = tr["r_kind"]
+    for i, w in enumerate(want):
+        assert walk["range_any"][i] == (w[0] if w else -1)
+        ops = []
+        for r in w:
+            if kind[r] == 1:
+                break
+            if kind[r] == 0:
+                ops.append(r)
+        assert walk["range_id"][i] == (ops[0] if ops else -1)
+        assert walk["fused"][i] == (1 if len(ops) > 1 else 0)
+
+
+def test_enclose_all_capacity():
+    """With a smaller capacity the offsets are still complete and exactly the
+    lists that end within it are written."""
+    tr = cases.random_trace(7, T=80, R=40, S=2, t_max=60, max_depth=4)
+    full = O.enclose_all(tr)
+    off = full["off"]
+    cap = int(off[-1]) // 2
+    import ctypes as C
+    x = O._Inputs(tr)
+    o2 = np.empty_like(off)
+    ids = np.full(max(cap, 1), -7, np.int32)
+    dg = O.Diag()
+    assert O.lib().oref_enclose_all(C.byref(x.k), C.byref(x.r), C.byref(x.d), O._ptr(o2),
+                                    O._ptr(ids), cap, C.byref(dg)) == 0
+    np.testing.assert_array_equal(o2, off)
+    last = np.searchsorted(off, cap, side="right") - 1  # lists 0..last-1 end within cap
+    np.testing.assert_array_equal(ids[:off[last]], full["ids"][:off[last]])
+    assert np.all(ids[off[last]:cap] == -7)

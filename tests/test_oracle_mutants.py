@@ -29,10 +29,10 @@ MUTANTS = {
     "dedup_no_name_check": ("ok = k->name_id[src] == k->name_id[i];", "ok = 1;"),
     "enclose_end_ascending": ("rs[nr].c = UINT64_MAX - r->end_ns[x];",
                               "rs[nr].c = r->end_ns[x];"),
-    "enclose_open_at_start_excluded": ("while (x < a_end && rs[x].b <= t)",
-                                       "while (x < a_end && rs[x].b < t)"),
-    "enclose_closed_at_end_excluded": ("while (top > 0 && r->end_ns[stack[top - 1]] < t) top--;",
-                                       "while (top > 0 && r->end_ns[stack[top - 1]] <= t) top--;"),
+    "enclose_open_at_start_excluded": ("while (*x < a_end && rs[*x].b <= t)",
+                                       "while (*x < a_end && rs[*x].b < t)"),
+    "enclose_closed_at_end_excluded": ("while (*top > 0 && r->end_ns[stack[*top - 1]] < t) (*top)--;",
+                                       "while (*top > 0 && r->end_ns[stack[*top - 1]] <= t) (*top)--;"),
     "depth_root_zero": ("depth[id] = top > 0 ? depth[stack[top - 1]] + 1 : 1;",
                         "depth[id] = top > 0 ? depth[stack[top - 1]] + 1 : 0;"),
     "nesting_touch_is_cross": ("while (top > 0 && r->end_ns[stack[top - 1]] <= r->start_ns[id]) top--;",
@@ -73,6 +73,10 @@ MUTANTS = {
     "dispatch_ignores_operator": ("if (rid >= 0 && rid < R && o >= 0 && (uint32_t)o == r->op_id[rid] && (uint32_t)o < NOPS)",
                                   "if (rid >= 0 && rid < R && o >= 0 && (uint32_t)o < NOPS)"),
     "dispatch_op_row_shifted": ("row_of[i] = (uint32_t)(R + o);", "row_of[i] = (uint32_t)(R + o - (o > 0));"),
+    "all_outermost_first": ("for (int64_t u = top - 1; u >= 0; --u) {\n          const int64_t id = stack[u];\n          if (r->end_ns[id] < t) continue; /* ended before the point */",
+                            "for (int64_t u = 0; u < top; ++u) {\n          const int64_t id = stack[u];\n          if (r->end_ns[id] < t) continue; /* ended before the point */"),
+    "all_touching_excluded": ("if (r->end_ns[id] < t) continue; /* ended before the point */",
+                              "if (r->end_ns[id] <= t) continue; /* ended before the point */"),
     "parent_is_root": ("if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[top - 1] : -1;",
                        "if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[0] : -1;"),
 }
@@ -181,6 +185,15 @@ def battery(L) -> bool:
         want = brute.aggregate_groups(tr, match, keys, tr["r_start"].size + tr["n_ops"] + 1)
         if not _rows_close(out, want):
             return False
+    for seed in range(4):
+        tr = cases.random_trace(960 + seed, T=60, R=30, S=2, t_max=40, max_depth=4)
+        out = O.enclose_all(tr, library=L)
+        want = brute.enclosing_lists(tr)
+        if int(out["off"][-1]) != sum(len(w) for w in want):
+            return False
+        for i, w in enumerate(want):
+            if list(out["ids"][out["off"][i]:out["off"][i + 1]]) != w:
+                return False
     tr = _edge_trace()
     out = O.attribute(tr, library=L)
     if not np.array_equal(out["range_id"], brute.enclose(tr)):
