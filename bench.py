@@ -193,6 +193,30 @@ def measure_next_rows(dt, tr, flags, steps, warmup, out, ws):
         "kernel_algorithmic_bytes": enc_bytes, "kernel_GBps": enc_gbps,
         "kernel_frac": enc_gbps / HBM_PEAK_GBPS}
 
+    # all enclosing ranges of every launch as CSR lists (one call into a
+    # buffer sized by a first call)
+    first = opattr.opattr_enclose_all(dtk, flags=flags, ws=ws)
+    total = int(first["ids"].numel())
+    ids = torch.empty(max(total, 1), dtype=torch.int32, device=dt["seq"].device)
+    for _ in range(warmup):
+        opattr.opattr_enclose_all(dtk, flags=flags, ids=ids, ws=ws)
+    ev = [_events(2) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for k in range(steps):
+        ev[k][0].record()
+        opattr.opattr_enclose_all(dtk, flags=flags, ids=ids, ws=ws)
+        ev[k][1].record()
+    torch.cuda.synchronize()
+    all_ms = statistics.mean(a.elapsed_time(b) for a, b in ev)
+    # stream and query point per launch, the lists and offsets out, range
+    # starts, ends, parents once
+    all_bytes = T * (2 + 8 + 8) + total * 4 + R * (8 + 8 + 4)
+    agbps = all_bytes / (all_ms * 1e-3) / 1e9
+    rows["enclose_all"] = {
+        "call": "opattr_enclose_all (CSR lists, innermost first)", "entries": total,
+        "ms_per_call": all_ms, "records_per_s": T / (all_ms * 1e-3),
+        "algorithmic_bytes": all_bytes, "achieved_GBps": agbps, "frac": agbps / HBM_PEAK_GBPS}
+
     # tiered attribution: the pipeline of library calls (matching with the
     # dedup broadcast, the walk, the tiers, the table by tier operator) with
     # a correlation map for 40% of the names and a fusion map for 30%

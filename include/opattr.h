@@ -359,6 +359,17 @@ int opattr_enclose_walk(const opattr_kernels *k, const opattr_ranges *r, const o
                         int32_t *range_parent, uint8_t *range_depth, opattr_diag *diag,
                         void *ws, size_t ws_bytes, void *stream);
 
+/* All enclosing ranges (Alg. 2 keeps all_enclosing_ranges for fused kernels)
+   as CSR lists: ids[off[i] .. off[i+1]) are the valid ranges of the launch's
+   stream whose closed interval holds its query point, innermost first
+   (reverse nesting order; kinds are not consulted). Out (device): off[k->n +
+   1] (int64, always written; off[k->n] is the total), ids (capacity cap
+   entries) receives the lists that end within cap: call once with cap = 0
+   to learn the total. Workspace: opattr_workspace_bytes(k, NULL, r, d). */
+int opattr_enclose_all(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,
+                       int64_t *off, int32_t *ids, int64_t cap, opattr_diag *diag, void *ws,
+                       size_t ws_bytes, void *stream);
+
 /* Aggregation (Eq. 1). Row g = op_id[range_id[i]] (or n_ops when range_id is
    -1) collects kernel_count and total_ns of every launch, and over launches
    with match >= 0: matched_count, matched_ns and, per counter c with

@@ -452,6 +452,23 @@ int opattr_enclose_walk(const opattr_kernels *k, const opattr_ranges *r, const o
   return launch_status();
 }
 
+int opattr_enclose_all(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,
+                       int64_t *off, int32_t *ids, int64_t cap, opattr_diag *diag, void *ws,
+                       size_t ws_bytes, void *stream) {
+  if (!check_dims(d) || !check_kernels(k, false, true, false) || !check_ranges(r) || !diag ||
+      !off || cap < 0 || (cap > 0 && !ids))
+    return OPATTR_ERR_INVALID_ARG;
+  const Plan pl = make_plan(k, nullptr, r, d);
+  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  check_kernel_layout(k, d, diag, s);
+  const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, (d->flags & OPATTR_VALIDATE) != 0, s);
+  resolve_ranges(cr, d, ws, pl, nullptr, diag, s);
+  run_enclose_all(cr, k, d, ws, pl, off, ids, cap, diag, s);
+  launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s);
+  return launch_status();
+}
+
 int opattr_enclose(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,
                    int32_t *range_id, uint8_t *range_depth, opattr_diag *diag, void *ws,
                    size_t ws_bytes, void *stream) {

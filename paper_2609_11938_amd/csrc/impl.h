@@ -111,6 +111,8 @@ inline int bits_for_host(uint32_t v) {
   while (b < 32 && (v >> b) != 0) ++b;
   return b;
 }
+// inclusive scan of n int64 values in place; scratch holds n / 4096 + 1 values
+void scan_incl_i64_inplace(int64_t *a, int64_t n, int64_t *scratch, hipStream_t s);
 bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, int64_t n,
                       int begin_bit, int end_bit, uint32_t *hist, hipStream_t s);
 size_t radix_hist_entries(int64_t n);
@@ -205,6 +207,10 @@ CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws
                           opattr_diag *diag, bool validate, hipStream_t s);
 void resolve_ranges(const CoreRanges &cr, const opattr_dims *d, void *ws, const Plan &pl,
                     uint8_t *range_depth, opattr_diag *diag, hipStream_t s);
+// all enclosing ranges per launch as CSR (off[T + 1] always, ids within cap)
+void run_enclose_all(const CoreRanges &cr, const opattr_kernels *k, const opattr_dims *d, void *ws,
+                     const Plan &pl, int64_t *off, int32_t *ids, int64_t cap, opattr_diag *diag,
+                     hipStream_t s);
 // range_parent[input index] = input index of the range's parent, -1 root / bad
 void write_range_parents(const CoreRanges &cr, void *ws, const Plan &pl, int32_t *range_parent,
                          hipStream_t s);

@@ -118,6 +118,65 @@ __global__ void __launch_bounds__(256) k_chunk_scan(uint32_t *__restrict__ a, in
   }
 }
 
+// the same three passes for an inclusive scan of int64 values
+__global__ void __launch_bounds__(256) k_chunk_sums64(const int64_t *__restrict__ a, int64_t n,
+                                                      int64_t *__restrict__ sums) {
+  __shared__ int64_t sh[4];
+  const int64_t base = (int64_t)blockIdx.x * kScanChunk;
+  int64_t v = 0;
+  for (int k = threadIdx.x; k < kScanChunk; k += 256) {
+    const int64_t x = base + k;
+    if (x < n) v += a[x];
+  }
+  int64_t tot;
+  block_excl_scan_add<int64_t>(v, sh, &tot);
+  if (threadIdx.x == 0) sums[blockIdx.x] = tot;
+}
+
+// exclusive scan of the chunk sums, one block, in place
+__global__ void __launch_bounds__(256) k_scan_sums64(int64_t *a, int64_t n) {
+  __shared__ int64_t sh[4];
+  int64_t carry = 0;
+  for (int64_t base = 0; base < n; base += 256) {
+    const int64_t x = base + threadIdx.x;
+    const int64_t v = x < n ? a[x] : 0;
+    int64_t tot;
+    const int64_t pre = block_excl_scan_add<int64_t>(v, sh, &tot);
+    if (x < n) a[x] = carry + pre;
+    carry += tot;
+  }
+}
+
+__global__ void __launch_bounds__(256) k_chunk_scan64(int64_t *__restrict__ a, int64_t n,
+                                                      const int64_t *__restrict__ sums) {
+  __shared__ int64_t sh[4];
+  constexpr int kPerThread = kScanChunk / 256;
+  const int64_t base = (int64_t)blockIdx.x * kScanChunk + (int64_t)threadIdx.x * kPerThread;
+  int64_t v[kPerThread];
+  int64_t t = 0;
+#pragma unroll
+  for (int k = 0; k < kPerThread; ++k) {
+    const int64_t x = base + k;
+    v[k] = x < n ? a[x] : 0;
+    t += v[k];
+  }
+  int64_t run = sums[blockIdx.x] + block_excl_scan_add<int64_t>(t, sh, nullptr);
+#pragma unroll
+  for (int k = 0; k < kPerThread; ++k) {
+    const int64_t x = base + k;
+    run += v[k];
+    if (x < n) a[x] = run;
+  }
+}
+
+void scan_incl_i64_inplace(int64_t *a, int64_t n, int64_t *scratch, hipStream_t s) {
+  if (n <= 0) return;
+  const int64_t nb = (n + kScanChunk - 1) / kScanChunk;
+  k_chunk_sums64<<<(unsigned)nb, 256, 0, s>>>(a, n, scratch);
+  k_scan_sums64<<<1, 256, 0, s>>>(scratch, nb);
+  k_chunk_scan64<<<(unsigned)nb, 256, 0, s>>>(a, n, scratch);
+}
+
 size_t scan_scratch_entries(int64_t n) { return (size_t)((n + kScanChunk - 1) / kScanChunk) + 1; }
 
 // in place; scratch holds scan_scratch_entries(n) entries

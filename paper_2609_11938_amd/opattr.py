@@ -87,7 +87,7 @@ assert C.sizeof(opattr_diag) == 64
 EXPORTS = ("opattr_workspace_bytes", "opattr_diag_clear", "opattr_read_diag", "opattr_match",
            "opattr_dedup_broadcast", "opattr_dedup_classes", "opattr_tiers_workspace_bytes",
            "opattr_tiers", "opattr_aggregate_ops", "opattr_dispatch_workspace_bytes",
-           "opattr_aggregate_dispatch", "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate",
+           "opattr_aggregate_dispatch", "opattr_enclose_all", "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate",
            "opattr_attribute", "opattr_set_probe_events", "opattr_set_class_key_bits",
            "opattr_strerror")
 PROBES = ("seq_view", "tl_hist", "pf_hist", "col_scan", "pf_slot", "tl_match", "dedup",
@@ -146,6 +146,9 @@ def library(path: str | None = None):
                                             P(opattr_ranges), P(opattr_dims), vp, vp, vp, vp, vp,
                                             vp, sz, vp]
     L.opattr_aggregate_dispatch.restype = C.c_int
+    L.opattr_enclose_all.argtypes = [P(opattr_kernels), P(opattr_ranges), P(opattr_dims), vp, vp,
+                                     C.c_int64, vp, vp, sz, vp]
+    L.opattr_enclose_all.restype = C.c_int
     L.opattr_set_class_key_bits.argtypes = [i]
     L.opattr_set_class_key_bits.restype = C.c_int
     L.opattr_set_probe_events.argtypes = [vp, i]
@@ -579,6 +582,41 @@ def opattr_enclose_walk(dt: dict, flags=0, ws: Workspace | None = None, stream=N
                                  _p(out["range_depth"]), _p(out["diag"]), _p(buf),
                                  C.c_size_t(buf.numel()), _stream_handle(stream)),
            "opattr_enclose_walk")
+    return out
+
+
+def opattr_enclose_all(dt: dict, flags=0, ids=None, ws: Workspace | None = None,
+                       stream=None) -> Outputs:
+    """Every enclosing range of every launch as CSR lists (see
+    opattr_enclose_all): one call for the offsets, one for the lists; with
+    ``ids`` given (an int32 device tensor), one call filling it up to its
+    size."""
+    import torch
+
+    L = library()
+    m = _Marshal(dt, flags)
+    dev = dt["counters"].device
+    out = Outputs(off=torch.empty(m.T + 1, dtype=torch.int64, device=dev),
+                  diag=_new_diag(dev, stream))
+    ws = ws or Workspace(dev)
+    buf = ws.get(L.opattr_workspace_bytes(C.byref(m.k), None, C.byref(m.r), C.byref(m.d)))
+
+    def call(ids, cap):
+        _check(L.opattr_enclose_all(C.byref(m.k), C.byref(m.r), C.byref(m.d), _p(out["off"]),
+                                    _p(ids), C.c_int64(cap), _p(out["diag"]), _p(buf),
+                                    C.c_size_t(buf.numel()), _stream_handle(stream)),
+               "opattr_enclose_all")
+
+    if ids is not None:
+        out["ids"] = ids
+        call(ids, int(ids.numel()))
+        return out
+    call(None, 0)
+    total = int(out["off"][-1].item())
+    out["ids"] = torch.empty(max(total, 1), dtype=torch.int32, device=dev)
+    out["diag"] = _new_diag(dev, stream)
+    call(out["ids"], total)
+    out["ids"] = out["ids"][:total]
     return out
 
 

@@ -412,3 +412,42 @@ def test_empty_inputs():
     want = O.attribute(tr)
     out, diag = _run(tr)
     parity.assert_attribute(out, want, diag)
+
+
+def _assert_all(out, want):
+    import torch
+
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(parity.host(out["off"]), want["off"])
+    np.testing.assert_array_equal(parity.host(out["ids"]), want["ids"])
+    diag = opattr.read_diag(out["diag"])
+    for f in ("status", "bad_records", "nesting_errors"):
+        assert diag[f] == want["diag"][f], (f, diag, want["diag"])
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_enclose_all_parity(seed):
+    """Every enclosing range of every launch (CSR, innermost first) against
+    the oracle's stack sweep, coarse timestamps (launches on range edges),
+    some ranges with bad ids, each emission order."""
+    print(f"case enclose_all seed={seed}", flush=True)
+    tr = cases.random_trace(970 + seed, T=600, R=200, S=1 + seed % 3, t_max=80 + 200 * (seed % 2),
+                            max_depth=6)
+    tr = cases.with_kinds(tr, seed, p_bad=0.05 if seed % 3 == 2 else 0.0)
+    flags = 0
+    if seed % 2 == 0:
+        tr = cases.stream_major(tr)[0]
+        flags = opattr.KERNELS_STREAM_MAJOR | opattr.RANGES_NESTED
+    want = O.enclose_all(tr)
+    out = opattr.opattr_enclose_all(opattr.to_device(tr, DEV), flags=flags)
+    _assert_all(out, want)
+
+
+@pytest.mark.parametrize("cfg", ["sdpa", "large"])
+def test_enclose_all_generated(cfg):
+    """The generated workloads: one list per launch over up to 8 levels."""
+    print(f"case enclose_all {cfg}", flush=True)
+    tr = parity.trace(cfg, "stream_major")
+    want = O.enclose_all(tr)
+    out = opattr.opattr_enclose_all(opattr.to_device(tr, DEV), flags=HINTS)
+    _assert_all(out, want)
