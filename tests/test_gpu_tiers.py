@@ -252,3 +252,46 @@ def test_profile_from_gpu_outputs():
     want = profile.build(tr, match, t["tier"], t["op"], t["fused"], row, disp["table"],
                          range_any=walk["range_any"], range_parent=walk["range_parent"])
     _same_doc(got, want)
+
+
+def _empty_trace(T, R):
+    tr = cases.random_trace(31, T=max(T, 1), R=max(R, 1), S=2, n_names=3)
+    if T == 0:
+        for f in ("seq", "start_ns", "dur_ns", "stream_id", "name_id", "part_id", "query_ns"):
+            if tr.get(f) is not None:
+                tr[f] = tr[f][:0]
+    if R == 0:
+        for f in ("r_start", "r_end", "r_stream", "r_op", "r_kind"):
+            if tr.get(f) is not None:
+                tr[f] = tr[f][:0]
+    return tr
+
+
+@pytest.mark.parametrize("T,R", [(0, 5), (7, 0), (0, 0)])
+def test_next_rows_on_empty_inputs(T, R):
+    """No launches and/or no ranges: tiers (with an empty correlation map and
+    an empty fusion map), the table by operator, the per-dispatch table and
+    the CSR lists all equal the oracle's."""
+    import torch
+
+    print(f"case next rows empty T={T} R={R}", flush=True)
+    tr = _empty_trace(T, R)
+    tr.update(corr_name=np.zeros(0, np.uint32), corr_op=np.zeros(0, np.int32),
+              fmap_off=np.zeros(tr["n_names"] + 1, np.uint32), fmap_op=np.zeros(0, np.int32))
+    want = O.tiers(tr, corr_policy=0)
+    out, diag = _gpu_tiers(tr, policy=0)
+    _assert_tiers(out, diag, want)
+    match = np.full(T, -1, np.int32)
+    dt = opattr.to_device(tr, DEV)
+    agg = opattr.opattr_aggregate_ops(dt, torch.from_numpy(match).to(DEV), out["op"])
+    torch.cuda.synchronize()
+    parity.assert_table(agg.table_host(), O.aggregate_ops(tr, match, want["op"])["table"])
+    dout, ddiag = _gpu_dispatch(tr, match, want["range_id"], want["op"])
+    dwant = O.aggregate_dispatch(tr, match, want["range_id"], want["op"])
+    parity.assert_table(dout.table_host(), dwant["table"])
+    assert ddiag["status"] == dwant["diag"]["status"]
+    aw = O.enclose_all(tr)
+    ao = opattr.opattr_enclose_all(dt)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(parity.host(ao["off"]), aw["off"])
+    assert int(ao["ids"].numel()) == 0
