@@ -175,8 +175,11 @@ __device__ __forceinline__ void wave_counts(uint32_t hm, uint32_t hp, uint32_t &
 
 // MODE 1: range ids; MODE 3: range ids and the per-wave item and row counts;
 // MODE 2: the counts from a given range_id array.
+// six waves per SIMD: the kernel waits on chains of dependent loads, and
+// 80 registers (one fewer than it would take) buy a sixth wave without spills
 template <int MODE>
-__global__ void __launch_bounds__(kEncThreads) k_enclose(EncParams a) {
+__global__ void __launch_bounds__(kEncThreads) __attribute__((amdgpu_waves_per_eu(6)))
+k_enclose(EncParams a) {
   __shared__ uint64_t sS[(MODE & 1) ? kEncWindow : 1];
   __shared__ uint64_t red[2][kEncThreads / OPA_WAVE];
   __shared__ int64_t win[2];
