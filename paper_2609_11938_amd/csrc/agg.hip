@@ -183,13 +183,12 @@ __global__ void __launch_bounds__(256) k_item_scatter_w(AggWork w) {
   else item_scatter<16>(w, n, cnt);
 }
 
-// 1'. many rows: one stable radix sort of (row, item) over all items; keys
-// of the padding past the item count sort last
+// 1'. many rows: one stable radix sort of (row, item) over the items (the
+// sort reads the item count on the device)
 __global__ void k_item_keys(AggWork w, unsigned long long *k0, uint32_t *v0, int64_t cap) {
   const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (x >= cap) return;
-  const int64_t n = w.meta[0];
-  k0[x] = x < n ? w.ig[x] : w.G;
+  if (x >= cap || x >= w.meta[0]) return;
+  k0[x] = w.ig[x];
   v0[x] = (uint32_t)x;
 }
 
@@ -203,11 +202,12 @@ __global__ void k_item_place(AggWork w, const unsigned long long *key, const uin
 }
 
 // row offsets: goff[g] = the first sorted item of row g or later (the
-// padding keys equal G, so goff[G] is the item count)
+// item count for g = G)
 __global__ void k_row_bounds(AggWork w, const unsigned long long *key, int64_t cap) {
   const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (g > (int64_t)w.G) return;
-  int64_t lo = 0, hi = cap;
+  const int64_t n = w.meta[0] < cap ? w.meta[0] : cap;
+  int64_t lo = 0, hi = n;
   while (lo < hi) {
     const int64_t mid = (lo + hi) >> 1;
     if ((int64_t)key[mid] < g) lo = mid + 1;
@@ -448,7 +448,7 @@ void plan_items(const EncArgs &x, hipStream_t s) {
       const int bits = (bits_for_host(pl.G) + 7) & ~7;
       in1 = radix_sort_pairs(reinterpret_cast<uint64_t *>(k0), v0,
                              reinterpret_cast<uint64_t *>(k1), v1, cap, 0, bits,
-                             at<uint32_t>(x.ws, pl.isort_hist), s);
+                             at<uint32_t>(x.ws, pl.isort_hist), s, w.meta);
     }
     if (cap > 0)
       k_item_place<<<(unsigned)((cap + 255) / 256), 256, 0, s>>>(w, in1 ? k1 : k0, in1 ? v1 : v0,

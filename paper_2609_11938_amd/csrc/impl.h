@@ -113,8 +113,11 @@ inline int bits_for_host(uint32_t v) {
 }
 // inclusive scan of n int64 values in place; scratch holds n / 4096 + 1 values
 void scan_incl_i64_inplace(int64_t *a, int64_t n, int64_t *scratch, hipStream_t s);
+// n_dev (optional): the element count on the device (<= n); only that many
+// are sorted
 bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, int64_t n,
-                      int begin_bit, int end_bit, uint32_t *hist, hipStream_t s);
+                      int begin_bit, int end_bit, uint32_t *hist, hipStream_t s,
+                      const int64_t *n_dev = nullptr);
 size_t radix_hist_entries(int64_t n);
 // Several 32-bit fills in one launch (up to 8 arrays).
 struct FillJobs {

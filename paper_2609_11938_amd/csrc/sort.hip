@@ -7,12 +7,21 @@
 
 namespace opa {
 
-__global__ void __launch_bounds__(256) k_rs_hist(const uint64_t *__restrict__ keys, int64_t n,
-                                                 int shift, uint32_t *__restrict__ hist,
-                                                 int64_t ntiles) {
+// n_dev (optional): the element count on the device, at most n; tiles past it
+// count nothing and move nothing
+__device__ __forceinline__ int64_t sort_count(int64_t n, const int64_t *n_dev) {
+  if (!n_dev) return n;
+  const int64_t m = *n_dev;
+  return m < n ? (m > 0 ? m : 0) : n;
+}
+
+__global__ void __launch_bounds__(256) k_rs_hist(const uint64_t *__restrict__ keys, int64_t n_cap,
+                                                 const int64_t *n_dev, int shift,
+                                                 uint32_t *__restrict__ hist, int64_t ntiles) {
   __shared__ uint32_t c[256];
   c[threadIdx.x] = 0;
   __syncthreads();
+  const int64_t n = sort_count(n_cap, n_dev);
   const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
   for (int i = threadIdx.x; i < OPA_TILE; i += 256) {
     const int64_t x = base + i;
@@ -200,12 +209,15 @@ void launch_scan_excl(const uint32_t *in, uint32_t *out, int64_t n, int64_t *tot
 __global__ void __launch_bounds__(256) k_rs_scatter(const uint64_t *__restrict__ kin,
                                                     const uint32_t *__restrict__ vin,
                                                     uint64_t *__restrict__ kout,
-                                                    uint32_t *__restrict__ vout, int64_t n,
-                                                    int shift, const uint32_t *__restrict__ offs,
+                                                    uint32_t *__restrict__ vout, int64_t n_cap,
+                                                    const int64_t *n_dev, int shift,
+                                                    const uint32_t *__restrict__ offs,
                                                     int64_t ntiles) {
   __shared__ uint16_t cnt[OPA_TILE_CHUNKS][4][256];
   const int tid = threadIdx.x, w = wave_id();
+  const int64_t n = sort_count(n_cap, n_dev);
   const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
+  if (base >= n) return;  // uniform over the block
   for (int i = tid; i < OPA_TILE_CHUNKS * 4 * 256; i += 256) (&cnt[0][0][0])[i] = 0;
   __syncthreads();
   uint32_t dig[OPA_TILE_CHUNKS], lr[OPA_TILE_CHUNKS];
@@ -250,16 +262,17 @@ size_t radix_hist_entries(int64_t n) {
 }
 
 bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, int64_t n,
-                      int begin_bit, int end_bit, uint32_t *hist, hipStream_t s) {
+                      int begin_bit, int end_bit, uint32_t *hist, hipStream_t s,
+                      const int64_t *n_dev) {
   if (n <= 0) return false;
   const int64_t nt = (n + OPA_TILE - 1) / OPA_TILE;
   bool in1 = false;
   for (int sh = begin_bit; sh < end_bit; sh += 8) {
     uint64_t *ki = in1 ? k1 : k0, *ko = in1 ? k0 : k1;
     uint32_t *vi = in1 ? v1 : v0, *vo = in1 ? v0 : v1;
-    k_rs_hist<<<(unsigned)nt, 256, 0, s>>>(ki, n, sh, hist, nt);
+    k_rs_hist<<<(unsigned)nt, 256, 0, s>>>(ki, n, n_dev, sh, hist, nt);
     scan_excl_inplace(hist, nt * 256, hist + nt * 256, s);
-    k_rs_scatter<<<(unsigned)nt, 256, 0, s>>>(ki, vi, ko, vo, n, sh, hist, nt);
+    k_rs_scatter<<<(unsigned)nt, 256, 0, s>>>(ki, vi, ko, vo, n, n_dev, sh, hist, nt);
     in1 = !in1;
   }
   return in1;
