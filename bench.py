@@ -247,6 +247,21 @@ def measure_next_rows(dt, tr, flags, steps, warmup, out, ws):
     pipe_ms = statistics.mean(e[0].elapsed_time(e[1]) for e in ev)
     tiers_ms = statistics.mean(e[1].elapsed_time(e[2]) for e in ev)
     disp_ms = statistics.mean(e[2].elapsed_time(e[3]) for e in ev)
+    # the same in one library call (the ranges and the walk on a side stream)
+    one = None
+    for _ in range(warmup):
+        one = opattr.opattr_attribute_tiered(dtm, flags=flags, ws=ws)
+    torch.cuda.synchronize()
+    ev1 = [_events(2) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for k in range(steps):
+        ev1[k][0].record()
+        opattr.opattr_attribute_tiered(dtm, flags=flags, ws=ws)
+        ev1[k][1].record()
+    torch.cuda.synchronize()
+    one_ms = statistics.mean(a.elapsed_time(b) for a, b in ev1)
+    if not torch.equal(one["tier"], res["tiers"]["tier"]):
+        raise SystemExit("one-call and composed tiers differ")
     C_ = maps["corr_name"].size
     # opattr_tiers alone: the correlation join (seq, name per launch; name
     # per entry) and the tier pass (name, dur, range id, walk fused in;
@@ -254,8 +269,9 @@ def measure_next_rows(dt, tr, flags, steps, warmup, out, ws):
     tier_bytes = T * (4 + 4) + C_ * (4 + 4) + T * (4 + 4 + 4 + 1 + 1 + 4 + 1)
     gbps = tier_bytes / (tiers_ms * 1e-3) / 1e9
     rows["tiered"] = {
-        "call": "match + dedup broadcast + enclose_walk + tiers + aggregate_ops",
-        "ms_per_step": pipe_ms, "records_per_s": T / (pipe_ms * 1e-3),
+        "call": "opattr_attribute_tiered (matching + dedup broadcast, walk, tiers, table)",
+        "ms_per_step": one_ms, "records_per_s": T / (one_ms * 1e-3),
+        "composed_calls_ms": pipe_ms,
         "correlation_entries": int(C_),
         "coverage_frac": {"high": float(cov["frac"][1]), "nvtx": float(cov["frac"][2]),
                           "fusion": float(cov["frac"][3]),

@@ -13,6 +13,7 @@
  *   opattr_tiers           tiered attribution: correlation map, enclosure,
  *                          fusion map (attribution-methods table)
  *   opattr_aggregate_dispatch  the operator table per dispatch (App. A.4)
+ *   opattr_attribute_tiered    matching, walk, tiers and the table in one call
  *   opattr_enclose         innermost operator range enclosing each launch on its
  *                          own stream (Sec. 3.5, Alg. 2)
  *   opattr_aggregate       per-operator SUM / duration-weighted mean (Eq. 1) / MAX
@@ -280,6 +281,27 @@ int opattr_tiers(const opattr_kernels *k, const opattr_corr_map *corr,
                  int corr_policy, const int32_t *range_id, const uint8_t *walk_fused,
                  uint8_t *tier, int32_t *op, uint8_t *fused, opattr_coverage *cov,
                  opattr_diag *diag, void *ws, size_t ws_bytes, void *stream);
+
+/* Tiered attribution in one call: opattr_match (with the dedup broadcast
+   when partitions are given), opattr_enclose_walk's range_id and fused,
+   opattr_tiers and opattr_aggregate_ops, with the ranges and the walk on a
+   side stream of the device beside the two matchings (the profiled rows,
+   then the correlation map), joined back before the tiers. Out (device):
+   match, range_id, tier, op, fused [k->n]; table[n_ops + 1] by tier
+   operator; sum; cov. One diag record covers both matchings (their count
+   diagnostics add up; STRICT in either makes a count mismatch an error).
+   Workspace: opattr_attribute_tiered_workspace_bytes. */
+size_t opattr_attribute_tiered_workspace_bytes(const opattr_kernels *k, const opattr_profiled *p,
+                                               const opattr_ranges *r,
+                                               const opattr_corr_map *corr,
+                                               const opattr_dims *d);
+int opattr_attribute_tiered(const opattr_kernels *k, const opattr_profiled *p,
+                            const opattr_ranges *r, const opattr_corr_map *corr,
+                            const opattr_fusion_map *fmap, const opattr_dims *d, int policy,
+                            int corr_policy, const uint8_t *agg_kind, int32_t *match,
+                            int32_t *range_id, uint8_t *tier, int32_t *op, uint8_t *fused,
+                            opattr_op_row *table, opattr_summary *sum, opattr_coverage *cov,
+                            opattr_diag *diag, void *ws, size_t ws_bytes, void *stream);
 
 /* Aggregation (Eq. 1) by a given operator per launch: row op[i] when
    op[i] in [0, n_ops), row n_ops (UNATTRIBUTED) when op[i] == -1; other

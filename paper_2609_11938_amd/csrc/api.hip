@@ -636,6 +636,107 @@ int opattr_tiers(const opattr_kernels *k, const opattr_corr_map *corr,
   return launch_status();
 }
 
+// profiled rows sized for the larger of the profiled list and the map, so
+// that one plan serves both matchings of the tiered call
+static opattr_profiled tiered_rows(const opattr_profiled *p, const opattr_corr_map *corr) {
+  opattr_profiled m = *p;
+  if (corr && corr->n > m.n) m.n = corr->n;
+  return m;
+}
+
+size_t opattr_attribute_tiered_workspace_bytes(const opattr_kernels *k, const opattr_profiled *p,
+                                               const opattr_ranges *r,
+                                               const opattr_corr_map *corr,
+                                               const opattr_dims *d) {
+  if (!k || !p || !d) return 0;
+  const opattr_profiled m = tiered_rows(p, corr);
+  return make_plan(k, &m, r, d).total;
+}
+
+int opattr_attribute_tiered(const opattr_kernels *k, const opattr_profiled *p,
+                            const opattr_ranges *r, const opattr_corr_map *corr,
+                            const opattr_fusion_map *fmap, const opattr_dims *d, int policy,
+                            int corr_policy, const uint8_t *agg_kind, int32_t *match,
+                            int32_t *range_id, uint8_t *tier, int32_t *op, uint8_t *fused,
+                            opattr_op_row *table, opattr_summary *sum, opattr_coverage *cov,
+                            opattr_diag *diag, void *ws, size_t ws_bytes, void *stream) {
+  if (!check_dims(d) || !check_kernels(k, true, true, true) || !check_profiled(p, true, true) ||
+      !check_ranges(r) || !diag || !table || !sum || !cov || policy < 0 || policy > 2 ||
+      corr_policy < 0 || corr_policy > 2 || !kinds_ok(agg_kind) ||
+      (k->n > 0 && (!match || !range_id || !tier || !op || !fused)))
+    return OPATTR_ERR_INVALID_ARG;
+  if (corr && (!ok_n(corr->n) || (corr->n > 0 && (!corr->name_id || !corr->op_id))))
+    return OPATTR_ERR_INVALID_ARG;
+  if (fmap && (!fmap->off || !fmap->op_id)) return OPATTR_ERR_INVALID_ARG;
+  const opattr_profiled rows = tiered_rows(p, corr);
+  const Plan pl = make_plan(k, &rows, r, d);
+  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  check_kernel_layout(k, d, diag, s);
+  const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
+  // the ranges and the walk need no match: a side stream, joined back
+  // before the tiers
+  SideStream *ss = side_stream();
+  const hipStream_t s2 = ss ? ss->s : s;
+  if (ss) {
+    note(hipEventRecord(ss->fork, s));
+    note(hipStreamWaitEvent(s2, ss->fork, 0));
+  }
+  probe_begin(OPATTR_PROBE_RANGES, s2);
+  const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s2);
+  resolve_ranges(cr, d, ws, pl, nullptr, diag, s2);
+  probe_end(OPATTR_PROBE_RANGES, s2);
+  EncArgs w{};
+  w.k = k;
+  w.cr = cr;
+  w.d = d;
+  w.range_id = range_id;
+  w.fused = fused;
+  w.diag = diag;
+  w.ws = ws;
+  w.pl = &pl;
+  run_enclose(w, s2);
+  if (ss) note(hipEventRecord(ss->join, s2));
+  // matching with the dedup broadcast, then the correlation lookup (Alg. 1
+  // over the map's entries, partitions off) into the item array
+  build_seq_view(k, d, ws, pl, diag, validate, s);
+  IomArgs a{k, p, d, policy, match, nullptr, diag, ws, &pl, true, validate};
+  run_match(a, s);
+  int32_t *entry = nullptr;
+  const TiersView v(k, corr, d);
+  if (corr) {
+    entry = at<int32_t>(ws, pl.ia);
+    IomArgs c{&v.k, &v.p, &v.d, corr_policy, entry, nullptr, diag, ws, &pl, false, validate};
+    run_match(c, s);
+  }
+  if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
+  TierIn x{k, corr, fmap, r, d, entry, range_id, fused, tier, op, fused, cov, diag, ws, &pl};
+  run_tiers(x, s);
+  // the table by tier operator
+  uint32_t *ident = at<uint32_t>(ws, pl.ident);
+  launch_iota(ident, d->n_ops, s);
+  opattr_ranges ops{};
+  ops.n = d->n_ops;
+  ops.op_id = ident;
+  EncArgs e{};
+  e.k = k;
+  e.p = p;
+  e.match = match;
+  e.r = &ops;
+  e.d = d;
+  e.range_id = op;
+  e.agg_kind = agg_kind ? agg_kind : kDefaultKind;
+  e.table = table;
+  e.sum = sum;
+  e.diag = diag;
+  e.ws = ws;
+  e.pl = &pl;
+  run_aggregate_all(e, s);
+  launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s, table, sum, pl.G, d->n_ops,
+                at<unsigned long long>(ws, pl.sumpart));
+  return launch_status();
+}
+
 int opattr_aggregate_ops(const opattr_kernels *k, const opattr_profiled *p, const int32_t *match,
                          const int32_t *op, const opattr_dims *d, const uint8_t *agg_kind,
                          opattr_op_row *table, opattr_summary *sum, opattr_diag *diag,

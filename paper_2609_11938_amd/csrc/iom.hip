@@ -1182,7 +1182,10 @@ void run_match(const IomArgs &x, hipStream_t s) {
   const TlArgs ta = tl_args(k, d, ws, pl, dedup);
   PfArgs pa;
   pa.name = x.p->name_id;
-  pa.P = pl.P;
+  // the rows of this call (the plan may be sized for a longer list)
+  const int64_t P = x.p->n < pl.P ? x.p->n : pl.P;
+  const int64_t ntp = (P + OPA_TILE - 1) / OPA_TILE;
+  pa.P = P;
   pa.NN = NN;
   // the profiled side depends only on the row names: it runs on its own
   // stream when one is given, joined back before the lookups
@@ -1192,17 +1195,17 @@ void run_match(const IomArgs &x, hipStream_t s) {
     note(hipStreamWaitEvent(sp, x.pf_fork, 0));
   }
   probe_begin(OPATTR_PROBE_PF_HIST, sp);
-  if (pl.ntp > 0) {
-    if (fast_pf) k_pf_hist_w<<<(unsigned)pl.ntp, 256, lds, sp>>>(pa, pfh, x.diag);
-    else k_pf_hist<<<(unsigned)pl.ntp, 256, 0, sp>>>(pa, pfh, x.diag);
+  if (ntp > 0) {
+    if (fast_pf) k_pf_hist_w<<<(unsigned)ntp, 256, lds, sp>>>(pa, pfh, x.diag);
+    else k_pf_hist<<<(unsigned)ntp, 256, 0, sp>>>(pa, pfh, x.diag);
   }
   probe_end(OPATTR_PROBE_PF_HIST, sp);
-  column_scan(pfh, pl.ntp, NN, at<uint32_t>(ws, pl.pfch), pfc, sp, nullptr);
+  column_scan(pfh, ntp, NN, at<uint32_t>(ws, pl.pfch), pfc, sp, nullptr);
   if (NN) k_pf_off<<<1, 1024, 0, sp>>>(pfc, NN, off);
   probe_begin(OPATTR_PROBE_PF_SLOT, sp);
-  if (pl.ntp > 0) {
-    if (fast_pf) k_pf_slot_w<<<(unsigned)pl.ntp, 256, lds, sp>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
-    else k_pf_slot<<<(unsigned)pl.ntp, 256, 0, sp>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
+  if (ntp > 0) {
+    if (fast_pf) k_pf_slot_w<<<(unsigned)ntp, 256, lds, sp>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
+    else k_pf_slot<<<(unsigned)ntp, 256, 0, sp>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
   }
   probe_end(OPATTR_PROBE_PF_SLOT, sp);
   if (sp != s) note(hipEventRecord(x.pf_join, sp));

@@ -87,7 +87,8 @@ assert C.sizeof(opattr_diag) == 64
 EXPORTS = ("opattr_workspace_bytes", "opattr_diag_clear", "opattr_read_diag", "opattr_match",
            "opattr_dedup_broadcast", "opattr_dedup_classes", "opattr_tiers_workspace_bytes",
            "opattr_tiers", "opattr_aggregate_ops", "opattr_dispatch_workspace_bytes",
-           "opattr_aggregate_dispatch", "opattr_enclose_all", "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate",
+           "opattr_aggregate_dispatch", "opattr_enclose_all",
+           "opattr_attribute_tiered_workspace_bytes", "opattr_attribute_tiered", "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate",
            "opattr_attribute", "opattr_set_probe_events", "opattr_set_class_key_bits",
            "opattr_strerror")
 PROBES = ("seq_view", "tl_hist", "pf_hist", "col_scan", "pf_slot", "tl_match", "dedup",
@@ -149,6 +150,14 @@ def library(path: str | None = None):
     L.opattr_enclose_all.argtypes = [P(opattr_kernels), P(opattr_ranges), P(opattr_dims), vp, vp,
                                      C.c_int64, vp, vp, sz, vp]
     L.opattr_enclose_all.restype = C.c_int
+    L.opattr_attribute_tiered_workspace_bytes.argtypes = [P(opattr_kernels), P(opattr_profiled),
+                                                          P(opattr_ranges), P(opattr_corr_map),
+                                                          P(opattr_dims)]
+    L.opattr_attribute_tiered_workspace_bytes.restype = sz
+    L.opattr_attribute_tiered.argtypes = [P(opattr_kernels), P(opattr_profiled), P(opattr_ranges),
+                                          P(opattr_corr_map), P(opattr_fusion_map), P(opattr_dims),
+                                          i, i, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.opattr_attribute_tiered.restype = C.c_int
     L.opattr_set_class_key_bits.argtypes = [i]
     L.opattr_set_class_key_bits.restype = C.c_int
     L.opattr_set_probe_events.argtypes = [vp, i]
@@ -506,6 +515,44 @@ def opattr_aggregate_dispatch(dt: dict, match, range_id, op=None, agg_kind=None,
                                      C.c_size_t(buf.numel()), _stream_handle(stream))
     del k_keep
     _check(rc, "opattr_aggregate_dispatch")
+    return out
+
+
+def opattr_attribute_tiered(dt: dict, policy=MISMATCH_PREFIX, corr_policy=MISMATCH_SKIP_NAME,
+                            agg_kind=None, flags=0, absent_mask=0, ws: Workspace | None = None,
+                            stream=None) -> Outputs:
+    """Tiered attribution in one library call (see opattr_attribute_tiered):
+    match, range_id, tier, op, fused per launch, the table by tier operator,
+    the summary and the coverage record."""
+    import torch
+
+    L = library()
+    m = _Marshal(dt, flags, absent_mask)
+    corr, fm, keep = _maps(dt)
+    dev = dt["counters"].device
+    T = m.T
+    out = Outputs(match=torch.empty(T, dtype=torch.int32, device=dev),
+                  range_id=torch.empty(T, dtype=torch.int32, device=dev),
+                  tier=torch.empty(T, dtype=torch.uint8, device=dev),
+                  op=torch.empty(T, dtype=torch.int32, device=dev),
+                  fused=torch.empty(T, dtype=torch.uint8, device=dev),
+                  table=torch.empty((dt["n_ops"] + 1) * 192, dtype=torch.uint8, device=dev),
+                  summary=torch.empty(40, dtype=torch.uint8, device=dev),
+                  coverage=torch.empty(C.sizeof(opattr_coverage), dtype=torch.uint8, device=dev),
+                  diag=_new_diag(dev, stream))
+    cp = C.byref(corr) if corr is not None else None
+    fp = C.byref(fm) if fm is not None else None
+    ws = ws or Workspace(dev)
+    buf = ws.get(L.opattr_attribute_tiered_workspace_bytes(C.byref(m.k), C.byref(m.p),
+                                                           C.byref(m.r), cp, C.byref(m.d)))
+    k_keep, kp = _kinds(agg_kind)
+    rc = L.opattr_attribute_tiered(
+        C.byref(m.k), C.byref(m.p), C.byref(m.r), cp, fp, C.byref(m.d), policy, corr_policy, kp,
+        _p(out["match"]), _p(out["range_id"]), _p(out["tier"]), _p(out["op"]), _p(out["fused"]),
+        _p(out["table"]), _p(out["summary"]), _p(out["coverage"]), _p(out["diag"]), _p(buf),
+        C.c_size_t(buf.numel()), _stream_handle(stream))
+    del k_keep, keep
+    _check(rc, "opattr_attribute_tiered")
     return out
 
 

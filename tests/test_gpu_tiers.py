@@ -295,3 +295,40 @@ def test_next_rows_on_empty_inputs(T, R):
     torch.cuda.synchronize()
     np.testing.assert_array_equal(parity.host(ao["off"]), aw["off"])
     assert int(ao["ids"].numel()) == 0
+
+
+@pytest.mark.parametrize("case", ["random0", "random1", "gpt2", "large"])
+def test_attribute_tiered_one_call(case):
+    """opattr_attribute_tiered against the oracle's stages: matching with the
+    dedup broadcast, the walk's range ids and fused flags, the tiers and
+    coverage, the table by tier operator; the diag record covers both
+    matchings, the walk and the tiers."""
+    import torch
+
+    print(f"case attribute_tiered {case}", flush=True)
+    if case.startswith("random"):
+        seed = int(case[-1])
+        tr = _tier_trace(40 + seed, dedup=seed == 0, shuffle=seed == 1,
+                         p_bad=0.05 if seed == 1 else 0.0)
+        flags = 0
+    else:
+        tr = tg.with_attribution_maps(tg.with_range_kinds(parity.trace(case, "stream_major")))
+        flags = HINTS
+    att = O.attribute(tr, stages=["match", "dedup"])
+    t = O.tiers(tr)
+    walk = O.enclose_walk(tr)
+    agg = O.aggregate_ops(tr, att["match"], t["op"])
+    dt = opattr.to_device(tr, DEV)
+    out = opattr.opattr_attribute_tiered(dt, flags=flags)
+    torch.cuda.synchronize()
+    h = parity.host
+    np.testing.assert_array_equal(h(out["match"]), att["match"])
+    np.testing.assert_array_equal(h(out["range_id"]), walk["range_id"])
+    _assert_tiers(out, opattr.read_diag(out["diag"]) | {f: t["diag"][f] for f in DIAG}, t)
+    parity.assert_table(out.table_host(), agg["table"])
+    parity.assert_summary(out.summary_host(), agg["summary"])
+    diag = opattr.read_diag(out["diag"])
+    bad = att["diag"]["bad_records"] + t["diag"]["bad_records"] + walk["diag"]["bad_records"]
+    assert diag["bad_records"] == bad
+    ok = att["diag"]["status"] == t["diag"]["status"] == walk["diag"]["status"] == 0
+    assert (diag["status"] == 0) == ok
