@@ -92,7 +92,7 @@ def test_random_traces_with_ties(seed):
         parity.assert_attribute(out2, want2, diag2)
 
 
-@pytest.mark.parametrize("n_names,n_ops", [(5000, 50), (7000, 7000)])
+@pytest.mark.parametrize("n_names,n_ops", [(5000, 50), (7000, 7000), (4096, 6143), (4097, 6144)])
 def test_many_names_and_rows(n_names, n_ops):
     """Name and operator-row counts past the LDS-counter limits take the
     tile radix sort instead; both must agree with the oracle."""

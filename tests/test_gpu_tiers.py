@@ -332,3 +332,25 @@ def test_attribute_tiered_one_call(case):
     assert diag["bad_records"] == bad
     ok = att["diag"]["status"] == t["diag"]["status"] == walk["diag"]["status"] == 0
     assert (diag["status"] == 0) == ok
+
+
+@pytest.mark.parametrize("n_names,n_ops", [(4096, 6143), (4097, 6144)])
+def test_attribute_tiered_at_path_boundaries(n_names, n_ops):
+    """Either side of the LDS-ranking limit on names (4096) and of the
+    per-tile item histograms on operator rows (6144): the one-call tiered
+    attribution still equals the oracle's stages."""
+    import torch
+
+    print(f"case tiered names={n_names} ops={n_ops}", flush=True)
+    tr = cases.random_trace(77, T=30_000, S=3, n_names=n_names, R=5_000, n_ops=n_ops,
+                            t_max=300_000, max_depth=5, dedup=True)
+    tr = tg.with_attribution_maps(cases.with_kinds(tr, 3), seed=5)
+    att = O.attribute(tr, stages=["match", "dedup"])
+    t = O.tiers(tr)
+    agg = O.aggregate_ops(tr, att["match"], t["op"])
+    out = opattr.opattr_attribute_tiered(opattr.to_device(tr, DEV))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(parity.host(out["match"]), att["match"])
+    for f in ("tier", "op", "fused"):
+        np.testing.assert_array_equal(parity.host(out[f]), t[f], err_msg=f)
+    parity.assert_table(out.table_host(), agg["table"])
