@@ -576,6 +576,27 @@ def with_range_kinds(tr, seed=5, p_skip=0.2):
     return out
 
 
+def _range_parents(tr):
+    """Per range: the innermost range of its stream that contains it (the
+    nearest earlier range in nesting order whose end is not before its own),
+    -1 for a root."""
+    R = tr["r_start"].size
+    rs, re, st = tr["r_start"], tr["r_end"], tr["r_stream"]
+    order = np.lexsort((np.arange(R), -re.astype(np.int64), rs, st))
+    parent = np.full(R, -1, dtype=np.int64)
+    stack = []
+    cur = None
+    for x in order:
+        if st[x] != cur:
+            stack, cur = [], st[x]
+        while stack and re[stack[-1]] < re[x]:
+            stack.pop()
+        if stack:
+            parent[x] = stack[-1]
+        stack.append(x)
+    return parent
+
+
 def with_attribution_maps(tr, seed=7, p_corr=0.4, p_mismatch=0.1, p_none=0.02, p_fmap=0.3,
                           max_fused=3, p_bad=0.0, shuffle=False):
     """A copy of ``tr`` with the two maps of the tiered attribution:
@@ -583,7 +604,10 @@ def with_attribution_maps(tr, seed=7, p_corr=0.4, p_mismatch=0.1, p_none=0.02, p
     * a correlation map (``corr_name`` u32, ``corr_op`` i32), as the
       torch.profiler pass would record it: for a fraction ``p_corr`` of the
       kernel names, one entry per launch in launch order, whose operator is
-      the op of the launch's planted range (a random op where there is none);
+      the one that dispatched the launch: the op of its planted innermost
+      range, or with range kinds the first op range outward from it (past
+      skipped ranges; none past a boundary), and for a launch no op range
+      covers a fixed random op of its kernel name;
       a fraction ``p_none`` of the entries record no operator (-1); for a
       fraction ``p_mismatch`` of those names the last entry is missing (a
       count mismatch); ``shuffle`` interleaves the names at random while
@@ -599,10 +623,20 @@ def with_attribution_maps(tr, seed=7, p_corr=0.4, p_mismatch=0.1, p_none=0.02, p
     order = np.lexsort((np.arange(T), tr["seq"]))
     order = order[name[order] < NN]
     nm = name[order].astype(np.int64)
-    op = rng.integers(0, max(NOPS, 1), size=order.size).astype(np.int64)
+    op = rng.integers(0, max(NOPS, 1), size=NN).astype(np.int64)[nm]
     pl = tr.get("planted_range")
     if pl is not None and order.size:
-        pr = np.asarray(pl)[order]
+        pr = np.asarray(pl)[order].astype(np.int64)
+        kinds = tr.get("r_kind")
+        if kinds is not None and pr.size:
+            kinds = np.asarray(kinds)
+            parent = _range_parents(tr)
+            for _ in range(256):  # outward past skipped ranges
+                up = (pr >= 0) & (kinds[np.maximum(pr, 0)] == 2)
+                if not up.any():
+                    break
+                pr = np.where(up, parent[np.maximum(pr, 0)], pr)
+            pr = np.where((pr >= 0) & (kinds[np.maximum(pr, 0)] == 1), -1, pr)
         op = np.where(pr >= 0, np.asarray(tr["r_op"], dtype=np.int64)[np.maximum(pr, 0)], op)
     covered = rng.random(NN) < p_corr
     keep = covered[nm]
