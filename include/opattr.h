@@ -387,7 +387,10 @@ int opattr_enclose_walk(const opattr_kernels *k, const opattr_ranges *r, const o
    (reverse nesting order; kinds are not consulted). Out (device): off[k->n +
    1] (int64, always written; off[k->n] is the total), ids (capacity cap
    entries) receives the lists that end within cap: call once with cap = 0
-   to learn the total. Workspace: opattr_workspace_bytes(k, NULL, r, d). */
+   to learn the total. Defined for properly nested ranges: crossing ranges
+   are reported as NOT_NESTED (nesting_errors counts the streams that have
+   them) and the lists are then unspecified. Workspace:
+   opattr_workspace_bytes(k, NULL, r, d). */
 int opattr_enclose_all(const opattr_kernels *k, const opattr_ranges *r, const opattr_dims *d,
                        int64_t *off, int32_t *ids, int64_t cap, opattr_diag *diag, void *ws,
                        size_t ws_bytes, void *stream);

@@ -441,6 +441,38 @@ static void stack_advance(const key3 *rs, int64_t a_end, int64_t *x, int64_t *st
   while (*top > 0 && r->end_ns[stack[*top - 1]] < t) (*top)--;
 }
 
+/* Depth, parents and the nesting check of one stream's ranges (rs[a ..
+   a_end) in nesting order). */
+static void stream_structure(const key3 *rs, int64_t a, int64_t a_end, const oref_ranges *r,
+                             int64_t *stack, uint32_t *depth, int32_t *range_parent,
+                             uint8_t *range_depth, oref_diag *diag) {
+  /* depth: 1 + depth of the nearest earlier range (nesting order) whose end
+     is not before this one's end -- that range contains it */
+  int64_t top = 0;
+  for (int64_t x = a; x < a_end; ++x) {
+    int64_t id = rs[x].idx;
+    while (top > 0 && r->end_ns[stack[top - 1]] < r->end_ns[id]) top--;
+    depth[id] = top > 0 ? depth[stack[top - 1]] + 1 : 1;
+    if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[top - 1] : -1;
+    if (depth[id] > 255) diag->flags |= OREF_F_LIMIT;
+    if (range_depth) range_depth[id] = (uint8_t)(depth[id] > 255 ? 255 : depth[id]);
+    stack[top++] = id;
+  }
+  /* proper nesting: no two ranges with s_A < s_B < e_A < e_B. Walking in
+     nesting order, after dropping ranges that end at or before s_B the top
+     has the smallest end of those still open at s_B; B crosses one of them
+     exactly when it crosses the top. */
+  top = 0;
+  int crossed = 0;
+  for (int64_t x = a; x < a_end; ++x) {
+    int64_t id = rs[x].idx;
+    while (top > 0 && r->end_ns[stack[top - 1]] <= r->start_ns[id]) top--;
+    if (top > 0 && r->end_ns[stack[top - 1]] < r->end_ns[id]) crossed = 1;
+    stack[top++] = id;
+  }
+  if (crossed) { diag->nesting_errors++; diag->flags |= OREF_F_NOT_NESTED; }
+}
+
 int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,
                  int32_t *range_id, uint8_t *range_depth, oref_diag *diag) {
   return oref_enclose_walk(k, r, d, range_id, NULL, NULL, NULL, range_depth, diag);
@@ -484,31 +516,8 @@ int oref_enclose_walk(const oref_kernels *k, const oref_ranges *r, const oref_di
     while (a_end < nr && rs[a_end].a == s) a_end++;
     while (b_end < nk && ks[b_end].a == s) b_end++;
 
-    /* depth: 1 + depth of the nearest earlier range (nesting order) whose end
-       is not before this one's end -- that range contains it */
+    stream_structure(rs, a, a_end, r, stack, depth, range_parent, range_depth, diag);
     int64_t top = 0;
-    for (int64_t x = a; x < a_end; ++x) {
-      int64_t id = rs[x].idx;
-      while (top > 0 && r->end_ns[stack[top - 1]] < r->end_ns[id]) top--;
-      depth[id] = top > 0 ? depth[stack[top - 1]] + 1 : 1;
-      if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[top - 1] : -1;
-      if (depth[id] > 255) diag->flags |= OREF_F_LIMIT;
-      if (range_depth) range_depth[id] = (uint8_t)(depth[id] > 255 ? 255 : depth[id]);
-      stack[top++] = id;
-    }
-    /* proper nesting: no two ranges with s_A < s_B < e_A < e_B. Walking in
-       nesting order, after dropping ranges that end at or before s_B the top
-       has the smallest end of those still open at s_B; B crosses one of them
-       exactly when it crosses the top. */
-    top = 0;
-    int crossed = 0;
-    for (int64_t x = a; x < a_end; ++x) {
-      int64_t id = rs[x].idx;
-      while (top > 0 && r->end_ns[stack[top - 1]] <= r->start_ns[id]) top--;
-      if (top > 0 && r->end_ns[stack[top - 1]] < r->end_ns[id]) crossed = 1;
-      stack[top++] = id;
-    }
-    if (crossed) { diag->nesting_errors++; diag->flags |= OREF_F_NOT_NESTED; }
 
     /* sweep: for each kernel in query order, push every range that has
        started (s <= T), drop finished ones from the top (e < T); the top is
@@ -571,6 +580,7 @@ int oref_enclose_all(const oref_kernels *k, const oref_ranges *r, const oref_dim
   /* first pass: the count per kernel; second pass: the lists */
   int64_t *cnt = xcalloc((size_t)T + 1, sizeof(int64_t));
   int64_t *stack = xcalloc((size_t)nr + 1, sizeof(int64_t));
+  uint32_t *depth = xcalloc((size_t)R, sizeof(uint32_t));
   for (int pass = 0; pass < 2; ++pass) {
     int64_t a = 0, b = 0;
     while (a < nr || b < nk) {
@@ -579,6 +589,7 @@ int oref_enclose_all(const oref_kernels *k, const oref_ranges *r, const oref_dim
       int64_t a_end = a, b_end = b;
       while (a_end < nr && rs[a_end].a == st) a_end++;
       while (b_end < nk && ks[b_end].a == st) b_end++;
+      if (pass == 0) stream_structure(rs, a, a_end, r, stack, depth, NULL, NULL, diag);
       int64_t top = 0, x = a;
       for (int64_t y = b; y < b_end; ++y) {
         const uint64_t t = ks[y].b;
@@ -601,7 +612,7 @@ int oref_enclose_all(const oref_kernels *k, const oref_ranges *r, const oref_dim
       for (int64_t i = 0; i < T; ++i) off[i + 1] = off[i] + cnt[i];
     }
   }
-  free(rs); free(ks); free(stack); free(cnt);
+  free(rs); free(ks); free(stack); free(cnt); free(depth);
   return 0;
 }
 

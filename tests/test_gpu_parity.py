@@ -443,6 +443,25 @@ def test_enclose_all_parity(seed):
     _assert_all(out, want)
 
 
+def test_enclose_all_crossing_ranges_reported():
+    """Crossing ranges: the list call reports them as the oracle does (count
+    of streams with a crossing, NOT_NESTED status); the lists are then
+    unspecified and only their offsets' consistency is checked."""
+    import torch
+
+    for seed in range(3):
+        print(f"case enclose_all crossing seed={seed}", flush=True)
+        tr = cases.random_trace(990 + seed, T=60, R=30, S=1 + seed % 3, t_max=40, nested=False)
+        want = O.enclose_all(tr)
+        out = opattr.opattr_enclose_all(opattr.to_device(tr, DEV))
+        torch.cuda.synchronize()
+        diag = opattr.read_diag(out["diag"])
+        for f in ("status", "bad_records", "nesting_errors"):
+            assert diag[f] == want["diag"][f], (f, diag, want["diag"])
+        off = parity.host(out["off"])
+        assert off[0] == 0 and np.all(np.diff(off) >= 0)
+
+
 @pytest.mark.parametrize("cfg", ["sdpa", "large"])
 def test_enclose_all_generated(cfg):
     """The generated workloads: one list per launch over up to 8 levels."""

@@ -834,6 +834,18 @@ def test_enclose_all_matches_brute_force(seed):
         assert walk["fused"][i] == (1 if len(ops) > 1 else 0)
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_enclose_all_reports_crossing_ranges(seed):
+    """Crossing ranges (Alg. 2 assumes proper nesting): the list call counts
+    the streams that have them, as the walk does, and the status says so."""
+    tr = cases.random_trace(990 + seed, T=60, R=30, S=1 + seed % 3, t_max=40, nested=False)
+    out = O.enclose_all(tr)
+    n = len(brute.crossing_streams(tr))
+    assert out["diag"]["nesting_errors"] == n
+    assert out["diag"]["nesting_errors"] == O.enclose_walk(tr)["diag"]["nesting_errors"]
+    assert (out["diag"]["status"] == -5) == (n > 0)
+
+
 def test_enclose_all_capacity():
     """With a smaller capacity the offsets are still complete and exactly the
     lists that end within it are written."""
