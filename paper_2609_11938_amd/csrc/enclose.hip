@@ -241,140 +241,161 @@ k_enclose(EncParams a) {
       for (int k = tid; k < wn; k += kEncThreads) sS[k] = a.cr.s[wlo + k];
     __syncthreads();
 
+    // Phase 1, the last range starting at or before each query point.
     // Consecutive launches of one stream with non-decreasing query points
-    // (the common case) continue from the previous launch: the last range
-    // starting at or before the query only moves forward, and while it stays
-    // the same, the parent walk resumes where the previous one stopped (the
-    // ranges it skipped end before the earlier query point, hence before this
-    // one too), with the same step budget.
-    int32_t rout[kPer];
+    // (the common case) continue from the previous launch: that range only
+    // moves forward. Only the staged starts (LDS) are read here when the
+    // window holds the stream.
+    int32_t pk[kPer], lok[kPer];
     bool have = false;  // the previous launch was searched
     uint16_t sprev = 0;
     uint64_t qprev = 0;
-    int64_t pprev = 0, jprev = -1, eprev = 0;  // eprev = ree[jprev] when jprev is a range
-    int sprevsteps = 0;
-    // the last innermost range found, and what the walk made of it: the op
-    // range (output id and row), the innermost range's output id, fused
-    int32_t rlast = -1, olast = -1, alast = -1;
-    uint32_t glast = 0;
-    uint8_t flast = 0;
-    bool tlast = false;
+    int32_t pprev = 0;
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
-      int32_t rid = -1;
-      int64_t slo = 0;  // first range of the launch's stream
+      pk[k] = -1;
+      lok[k] = 0;
       if (k < nv && st[k] < a.NS && q[k] < (1ull << 63)) {
-        const int64_t lo = a.rblk[st[k]], hi = a.rblk[st[k] + 1];
-        slo = lo;
+        const int32_t lo = (int32_t)a.rblk[st[k]], hi = (int32_t)a.rblk[st[k] + 1];
+        lok[k] = lo;
         const bool win = staged && st[k] == s0;  // the staged starts belong to this stream
-        int64_t j, ej = 0;
-        int steps = 0;
-        bool fresh = true;
+        int32_t p;
         if (have && st[k] == sprev && q[k] >= qprev) {
-          int64_t p = pprev;
+          p = pprev;
           while (p + 1 < hi) {
-            const int64_t x = p + 1 - wlo;
+            const int64_t x = (int64_t)p + 1 - wlo;
             const uint64_t sx = (win && x >= 0 && x < wn) ? sS[x] : a.cr.s[p + 1];
             if (sx > q[k]) break;
             ++p;
           }
-          if (p == pprev) {
-            j = jprev;
-            steps = sprevsteps;
-            ej = eprev;
-            fresh = false;
-          } else {
-            j = p;
+        } else if (st[k] == s0 && wn == 0) {
+          p = lo - 1;  // no range of the stream starts at or before the block's queries
+        } else if (win) {
+          int l2 = 0, h2 = (int)wn;
+          while (l2 < h2) {
+            const int mid = (l2 + h2) >> 1;
+            if (sS[mid] <= q[k]) l2 = mid + 1;
+            else h2 = mid;
           }
-          pprev = p;
+          p = (int32_t)(wlo + l2 - 1);
+          if (p < lo) p = lo - 1;
         } else {
-          const bool in0 = st[k] == s0;
-          int64_t p;
-          if (in0 && wn == 0) {
-            p = lo - 1;  // no range of the stream starts at or before the block's queries
-          } else if (win) {
-            int l2 = 0, h2 = (int)wn;
-            while (l2 < h2) {
-              const int mid = (l2 + h2) >> 1;
-              if (sS[mid] <= q[k]) l2 = mid + 1;
-              else h2 = mid;
-            }
-            p = wlo + l2 - 1;
-            if (p < lo) p = lo - 1;
-          } else {
-            p = thread_upper_bound(a.cr.s, lo, hi, q[k]) - 1;
-          }
-          j = p;
-          pprev = p;
+          p = (int32_t)thread_upper_bound(a.cr.s, lo, hi, q[k]) - 1;
         }
-        if (fresh && j >= lo) ej = a.ree[j];
-        while (j >= lo && ej < (int64_t)q[k] && steps < kMaxWalk) {
-          j = a.npg[j];
-          ++steps;
-          if (j >= lo) ej = a.ree[j];
-        }
-        if (j >= lo && ej >= (int64_t)q[k]) rid = (int32_t)j;
+        pk[k] = p;
+        pprev = p;
         have = true;
         sprev = st[k];
         qprev = q[k];
-        jprev = j;
-        eprev = ej;
-        sprevsteps = steps;
       } else {
         if (k < nv && st[k] >= a.NS) bad++;
         have = false;
       }
-      // A range that starts at the query point may be preceded, among the
-      // ranges containing the point, by ranges that end there without
-      // containing it (touching, not nested); any other enclosing range is
-      // an ancestor. So the walk depends on the query point only through
-      // "the innermost range starts at it", which keys the cache with rid.
-      bool touch = false;
-      if (rid >= 0 && (a.cr.kind || a.fused)) {
-        const int64_t x = rid - wlo;
-        const uint64_t sr = (staged && st[k] == s0 && x >= 0 && x < wn) ? sS[x] : a.cr.s[rid];
-        touch = sr == q[k];
-      }
-      if (rid >= 0 && (rid != rlast || touch != tlast)) {
-        rlast = rid;
-        tlast = touch;
-        // the next range outward that contains the query point: the parent,
-        // or from a range starting at the point the nearest earlier range in
-        // nesting order that ends at or after it
-        auto next_out = [&](int64_t j) -> int64_t {
-          if (!touch || (uint64_t)a.cr.s[j] != q[k]) return a.npg[j];
-          int64_t c = j - 1;
-          for (int h = 0; c >= slo && a.ree[c] < (int64_t)q[k] && h < kMaxWalk; ++h) c = a.npg[c];
-          return c >= slo ? c : -1;
-        };
-        // Alg. 2's walk outward from the innermost range: ops collected,
-        // skipped kinds passed over, a boundary ends it
-        int32_t first = rid;
-        flast = 0;
-        if (a.cr.kind) {
-          first = -1;
-          int nops = 0, hops = 0;
-          for (int64_t j = rid; j >= 0 && hops < kMaxWalk; j = next_out(j), ++hops) {
-            const uint8_t kd = a.cr.kind[j];
-            if (kd == OPATTR_KIND_BOUNDARY) break;
-            if (kd != OPATTR_KIND_OP) continue;
-            if (first < 0) first = (int32_t)j;
-            ++nops;
-          }
-          flast = nops > 1 ? 1 : 0;
-        } else if (a.fused) {
-          flast = next_out(rid) >= 0 ? 1 : 0;  // every enclosing range is an op
-        }
-        olast = first >= 0 ? (a.cr.perm ? a.cr.perm[first] : first) : -1;
-        glast = first >= 0 ? a.cr.op[first] : a.NOPS;
-        alast = a.cr.perm ? a.cr.perm[rid] : rid;
-      }
-      rout[k] = rid >= 0 ? olast : -1;
-      g[k] = k < nv ? (rid >= 0 ? glast : a.NOPS) : 0xFFFFFFFFu;
-      if (k < nv && a.range_any) a.range_any[ib + k] = rid >= 0 ? alast : -1;
-      if (k < nv && a.fused) a.fused[ib + k] = rid >= 0 ? flast : 0;
     }
-    store_run(a.range_id, ib, nv, rout);
+    // Phase 2, the walk up the parent chain while the range ends before the
+    // query point, all of the thread's launches in lock step so that their
+    // loads (ends, then parents) are in flight together.
+    int64_t ek[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) ek[k] = pk[k] >= lok[k] ? a.ree[pk[k]] : 0;
+    for (int step = 0; step < kMaxWalk; ++step) {
+      bool act[kPer], any = false;
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        act[k] = pk[k] >= lok[k] && ek[k] < (int64_t)q[k];
+        any |= act[k];
+      }
+      if (!any) break;
+#pragma unroll
+      for (int k = 0; k < kPer; ++k)
+        if (act[k]) pk[k] = a.npg[pk[k]];
+#pragma unroll
+      for (int k = 0; k < kPer; ++k)
+        if (act[k] && pk[k] >= lok[k]) ek[k] = a.ree[pk[k]];
+    }
+    int32_t ridk[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k)
+      ridk[k] = (pk[k] >= lok[k] && ek[k] >= (int64_t)q[k]) ? pk[k] : -1;
+
+    int32_t rout[kPer];
+    if (!a.cr.kind && !a.fused) {
+      // Phase 3 without kinds: the innermost range is the op range; its row
+      // and output id for every launch, loads in flight together
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        const int32_t rid = ridk[k];
+        g[k] = k < nv ? (rid >= 0 ? a.cr.op[rid] : a.NOPS) : 0xFFFFFFFFu;
+        rout[k] = rid >= 0 ? (a.cr.perm ? a.cr.perm[rid] : rid) : -1;
+      }
+      if (a.range_any)
+#pragma unroll
+        for (int k = 0; k < kPer; ++k)
+          if (k < nv) a.range_any[ib + k] = rout[k];
+      store_run(a.range_id, ib, nv, rout);
+    } else {
+      // Phase 3 with kinds or fused wanted: Alg. 2's walk outward from the
+      // innermost range, once per change of (innermost range, touching)
+      int32_t rlast = -1, olast = -1, alast = -1;
+      uint32_t glast = 0;
+      uint8_t flast = 0;
+      bool tlast = false;
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        const int32_t rid = ridk[k];
+        const int64_t slo = lok[k];  // first range of the launch's stream
+        // A range that starts at the query point may be preceded, among the
+        // ranges containing the point, by ranges that end there without
+        // containing it (touching, not nested); any other enclosing range is
+        // an ancestor. So the walk depends on the query point only through
+        // "the innermost range starts at it", which keys the cache with rid.
+        bool touch = false;
+        if (rid >= 0 && (a.cr.kind || a.fused)) {
+          const int64_t x = rid - wlo;
+          const uint64_t sr = (staged && st[k] == s0 && x >= 0 && x < wn) ? sS[x] : a.cr.s[rid];
+          touch = sr == q[k];
+        }
+        if (rid >= 0 && (rid != rlast || touch != tlast)) {
+          rlast = rid;
+          tlast = touch;
+          // the next range outward that contains the query point: the parent,
+          // or from a range starting at the point the nearest earlier range in
+          // nesting order that ends at or after it
+          auto next_out = [&](int64_t j) -> int64_t {
+            if (!touch || (uint64_t)a.cr.s[j] != q[k]) return a.npg[j];
+            int64_t c = j - 1;
+            for (int h = 0; c >= slo && a.ree[c] < (int64_t)q[k] && h < kMaxWalk; ++h) c = a.npg[c];
+            return c >= slo ? c : -1;
+          };
+          // Alg. 2's walk outward from the innermost range: ops collected,
+          // skipped kinds passed over, a boundary ends it
+          int32_t first = rid;
+          flast = 0;
+          if (a.cr.kind) {
+            first = -1;
+            int nops = 0, hops = 0;
+            for (int64_t j = rid; j >= 0 && hops < kMaxWalk; j = next_out(j), ++hops) {
+              const uint8_t kd = a.cr.kind[j];
+              if (kd == OPATTR_KIND_BOUNDARY) break;
+              if (kd != OPATTR_KIND_OP) continue;
+              if (first < 0) first = (int32_t)j;
+              ++nops;
+            }
+            flast = nops > 1 ? 1 : 0;
+          } else if (a.fused) {
+            flast = next_out(rid) >= 0 ? 1 : 0;  // every enclosing range is an op
+          }
+          olast = first >= 0 ? (a.cr.perm ? a.cr.perm[first] : first) : -1;
+          glast = first >= 0 ? a.cr.op[first] : a.NOPS;
+          alast = a.cr.perm ? a.cr.perm[rid] : rid;
+        }
+        rout[k] = rid >= 0 ? olast : -1;
+        g[k] = k < nv ? (rid >= 0 ? glast : a.NOPS) : 0xFFFFFFFFu;
+        if (k < nv && a.range_any) a.range_any[ib + k] = rid >= 0 ? alast : -1;
+        if (k < nv && a.fused) a.fused[ib + k] = rid >= 0 ? flast : 0;
+      }
+      store_run(a.range_id, ib, nv, rout);
+    }
   } else {
     bad += rows_from_ids(a, ib, nv, g);
   }
