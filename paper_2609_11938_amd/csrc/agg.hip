@@ -33,7 +33,8 @@ static_assert(kMaxOps + 1 < (1u << 20), "operator rows fit the item's 20 row bit
 __device__ __forceinline__ unsigned long long item_pack(uint32_t a, uint32_t b, uint32_t g) {
   return (unsigned long long)a | ((unsigned long long)b << 31) | ((unsigned long long)g << 36);
 }
-constexpr uint32_t kHeavy = 256;  // partials above which a row takes a whole block
+constexpr uint32_t kHeavy = 256;  // partials above which a row is reduced in chunks
+constexpr int kChunk = 256;       // partials per chunk of a heavy row (one per thread)
 
 EmitOut emit_out(void *ws, const Plan &pl) {
   EmitOut e;
@@ -71,10 +72,15 @@ struct AggWork {
   AggIn in;
   const uint32_t *ig, *ia, *ib;
   const PartRow *rows;
-  int64_t *meta;  // [0] items, [1] partial rows, [2] item tiles, [3] heavy rows, [4] spread rows
+  // [0] items, [1] partial rows, [2] item tiles, [3] heavy-row chunks,
+  // [4] spread rows, [5] heavy rows
+  int64_t *meta;
   uint32_t *ith, *gcnt, *goff;
   uint32_t *multi;          // rows spread over several windows
-  uint32_t *heavy;          // rows spread over more than kHeavy windows
+  uint32_t *heavy;          // rows over more than kHeavy windows: (row, first chunk) pairs
+  unsigned long long *hch;  // chunk slots of the heavy rows: row << 32 | chunk
+  PartRow *hpart;           // one partial per chunk slot
+  int64_t hcap;             // chunk slots available
   unsigned long long *sit;  // sorted items (item_pack)
   PartRow *part;            // [windows][2]: a continuing row's partial per window
   opattr_op_row *table;
@@ -143,6 +149,7 @@ __global__ void __launch_bounds__(1024) k_row_offsets(AggWork w) {
     w.goff[w.G] = tot;
     w.meta[3] = 0;
     w.meta[4] = 0;
+    w.meta[5] = 0;
   }
 }
 
@@ -217,6 +224,7 @@ __global__ void k_row_bounds(AggWork w, const unsigned long long *key, int64_t c
   if (g == 0) {
     w.meta[3] = 0;
     w.meta[4] = 0;
+    w.meta[5] = 0;
   }
 }
 
@@ -332,8 +340,9 @@ __global__ void __launch_bounds__(256) k_row_triage(AggWork w) {
   }
 }
 
-// 3b. one wave per listed row; rows over more than kHeavy windows are left
-// to a block each
+// 3b. one wave per listed row. A row over more than kHeavy windows is
+// reduced in chunks of kChunk partials instead: it reserves consecutive chunk
+// slots, fills them (row, chunk) and lists itself with the first of them.
 template <bool DEF>
 __global__ void __launch_bounds__(256) k_combine(AggWork w) {
   const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
@@ -345,7 +354,17 @@ __global__ void __launch_bounds__(256) k_combine(AggWork w) {
     const int64_t w0 = lo / kWinItems, w1 = (hi - 1) / kWinItems;
     const uint32_t m = (uint32_t)(w1 - w0 + 1);
     if (m > kHeavy) {
-      if (ln == 0) w.heavy[atomicAdd((unsigned long long *)&w.meta[3], 1ull)] = g;
+      const uint32_t nch = (m + kChunk - 1) / kChunk;
+      uint32_t base = 0;
+      if (ln == 0) {
+        base = (uint32_t)atomicAdd((unsigned long long *)&w.meta[3], (unsigned long long)nch);
+        const uint64_t h = atomicAdd((unsigned long long *)&w.meta[5], 1ull);
+        w.heavy[2 * h] = g;
+        w.heavy[2 * h + 1] = base;
+      }
+      base = __shfl(base, 0, OPA_WAVE);
+      for (uint32_t c = ln; c < nch; c += OPA_WAVE)
+        if ((int64_t)base + c < w.hcap) w.hch[base + c] = ((unsigned long long)g << 32) | c;
       continue;
     }
     Acc acc;
@@ -360,40 +379,59 @@ __global__ void __launch_bounds__(256) k_combine(AggWork w) {
   }
 }
 
-constexpr int kHeavyThreads = 1024;
-
-template <bool DEF>
-__global__ void __launch_bounds__(kHeavyThreads) k_combine_heavy(AggWork w) {
-  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
-  constexpr int kWaves = kHeavyThreads / OPA_WAVE;
-  __shared__ PartRow red[kWaves];
-  const int64_t nh = w.meta[3];
-  for (int64_t h = blockIdx.x; h < nh; h += gridDim.x) {
-    const uint32_t g = w.heavy[h];
+// 3c. one block per chunk slot: its kChunk partials, one per thread, merged
+// in order (lanes, then waves) into the slot's partial
+__global__ void __launch_bounds__(kChunk) k_heavy_chunks(AggWork w) {
+  const uint32_t mx = w.in.maxmask;
+  __shared__ PartRow red[kChunk / OPA_WAVE];
+  const int64_t ns = w.meta[3] < w.hcap ? w.meta[3] : w.hcap;
+  for (int64_t sl = blockIdx.x; sl < ns; sl += gridDim.x) {
+    const unsigned long long e = w.hch[sl];
+    const uint32_t g = (uint32_t)(e >> 32), c = (uint32_t)e;
     const uint32_t lo = w.goff[g], hi = w.goff[g + 1];
     const int64_t w0 = lo / kWinItems, w1 = (hi - 1) / kWinItems;
-    const int64_t m = w1 - w0 + 1;
+    const int64_t j = (int64_t)c * kChunk + threadIdx.x;
     Acc acc;
     acc_zero(acc);
-    for (int64_t j = threadIdx.x; j < m; j += blockDim.x) {
-      Acc b;
-      acc_load(b, row_part(w, w0, j));
-      acc_merge(acc, b, mx);
-    }
+    if (j < w1 - w0 + 1) acc_load(acc, row_part(w, w0, j));
     acc_wave_reduce(acc, mx);
-    __syncthreads();  // red is free (previous row done)
+    __syncthreads();  // red is free (previous slot done)
     if (lane_id() == 0) acc_store(red + wave_id(), acc);
     __syncthreads();
     if (threadIdx.x == 0) {
       Acc t;
       acc_load(t, red);
-      for (int k = 1; k < kWaves; ++k) {
+      for (int k = 1; k < kChunk / OPA_WAVE; ++k) {
         Acc b;
         acc_load(b, red + k);
         acc_merge(t, b, mx);
       }
-      write_row_lane(w, g, t, mx, dw);
+      acc_store(w.hpart + sl, t);
     }
+  }
+}
+
+// 3d. one wave per heavy row: its chunk partials in order, and the row
+template <bool DEF>
+__global__ void __launch_bounds__(256) k_heavy_rows(AggWork w) {
+  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
+  const int64_t nh = w.meta[5];
+  const int ln = lane_id();
+  for (int64_t h = (int64_t)blockIdx.x * 4 + wave_id(); h < nh; h += (int64_t)gridDim.x * 4) {
+    const uint32_t g = w.heavy[2 * h], base = w.heavy[2 * h + 1];
+    const uint32_t lo = w.goff[g], hi = w.goff[g + 1];
+    const uint32_t m = (uint32_t)((hi - 1) / kWinItems - lo / kWinItems + 1);
+    const uint32_t nch = (m + kChunk - 1) / kChunk;
+    Acc acc;
+    acc_zero(acc);
+    for (uint32_t c = ln; c < nch; c += OPA_WAVE) {
+      if ((int64_t)base + c >= w.hcap) break;
+      Acc b;
+      acc_load(b, w.hpart + base + c);
+      acc_merge(acc, b, mx);
+    }
+    acc_wave_reduce(acc, mx);
+    write_row(w, g, acc, mx, dw);
   }
 }
 
@@ -414,6 +452,9 @@ static AggWork agg_work(const EncArgs &x) {
   w.gcnt = at<uint32_t>(x.ws, pl.gcnt);
   w.goff = at<uint32_t>(x.ws, pl.goff);
   w.heavy = at<uint32_t>(x.ws, pl.heavy);
+  w.hch = at<unsigned long long>(x.ws, pl.hch);
+  w.hpart = at<PartRow>(x.ws, pl.hpart);
+  w.hcap = pl.hcap;
   w.multi = at<uint32_t>(x.ws, pl.multi);
   w.sit = at<unsigned long long>(x.ws, pl.sit);
   w.part = at<PartRow>(x.ws, pl.part);
@@ -471,15 +512,17 @@ void reduce_items(const EncArgs &x, hipStream_t s) {
   }
   const unsigned tg = (pl.G + 255) / 256;
   const unsigned cg = (unsigned)((pl.G + 3) / 4 < 1024 ? (pl.G + 3) / 4 : 1024);
+  const unsigned hg = (unsigned)(pl.hcap < 2048 ? pl.hcap : 2048);
   if (def) {
     k_row_triage<true><<<tg, 256, 0, s>>>(w);
     k_combine<true><<<cg, 256, 0, s>>>(w);
-    k_combine_heavy<true><<<64, kHeavyThreads, 0, s>>>(w);
   } else {
     k_row_triage<false><<<tg, 256, 0, s>>>(w);
     k_combine<false><<<cg, 256, 0, s>>>(w);
-    k_combine_heavy<false><<<64, kHeavyThreads, 0, s>>>(w);
   }
+  k_heavy_chunks<<<hg, kChunk, 0, s>>>(w);
+  if (def) k_heavy_rows<true><<<64, 256, 0, s>>>(w);
+  else k_heavy_rows<false><<<64, 256, 0, s>>>(w);
   probe_end(OPATTR_PROBE_AGGREGATE, s);
 }
 

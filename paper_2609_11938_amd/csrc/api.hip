@@ -130,7 +130,13 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.isort_hist = b.take(few_rows ? 0 : radix_hist_entries((int64_t)ni) * 4);
   pl.gcnt = b.take((size_t)pl.G * 4);
   pl.goff = b.take(((size_t)pl.G + 1) * 4);
-  pl.heavy = b.take((size_t)pl.G * 4);
+  // heavy rows (over 256 windows of 64 items, so at most items / 16320 of
+  // them) as (row, first chunk) pairs, and their chunks of 256 windows: at
+  // most about items / 8000, below max_windows / 64
+  pl.heavy = b.take((size_t)pl.G * 8);
+  pl.hcap = pl.max_windows / 64 + 64;
+  pl.hch = b.take((size_t)pl.hcap * 8);
+  pl.hpart = b.take((size_t)pl.hcap * 200);
   pl.multi = b.take((size_t)pl.G * 4);
   pl.sit = b.take((size_t)pl.cap_items * 8);
   pl.part = b.take((size_t)pl.max_windows * 2 * 200);

@@ -44,8 +44,9 @@ struct Plan {
   size_t rperm, rs_c, re_c, rst_c, rop_c, rkd_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
   // aggregation
-  int64_t cap_items, cap_rows, max_windows;
+  int64_t cap_items, cap_rows, max_windows, hcap;
   size_t wi, wr, hmb, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, heavy, multi, sit, part;
+  size_t hch, hpart;
   size_t isort_k0, isort_k1, isort_v0, isort_v1, isort_hist;  // item sort, many rows
   // dedup class discovery
   size_t c_first, c_last, c_runs, c_key, c_cand, c_fail, c_list, c_tkey, c_tmin;

@@ -136,6 +136,35 @@ def test_aggregate_ops_parity(cfg):
     assert diag["status"] == want["diag"]["status"]
 
 
+@pytest.mark.parametrize("T", [2_000_000, 9_000_000])
+def test_aggregate_ops_heavy_rows(T):
+    """Rows whose items span hundreds of thousands of windows: every launch
+    alternates between the UNATTRIBUTED row and operator 0 (one item each),
+    so both rows are reduced in chunks of 256 windows; at 9M launches each
+    row has more than 256 chunks. Random matches, some unmatched."""
+    import torch
+
+    print(f"case aggregate_ops heavy rows T={T}", flush=True)
+    rng = np.random.default_rng(T)
+    tr = cases.random_trace(5, T=64, R=8, n_ops=3)
+    P = 200_000
+    tr.update(seq=np.arange(T, dtype=np.uint32), start_ns=np.arange(T, dtype=np.uint64) * 10,
+              dur_ns=rng.integers(1, 5000, size=T).astype(np.uint32),
+              stream_id=np.zeros(T, np.uint16), name_id=np.zeros(T, np.uint32), part_id=None,
+              pf_name=np.zeros(P, np.uint32),
+              counters=rng.random((P, 20), dtype=np.float32), part_rep=None, n_parts=0)
+    match = rng.integers(-1, P, size=T).astype(np.int32)
+    op = np.where(np.arange(T) % 2 == 0, -1, 0).astype(np.int32)
+    want = O.aggregate_ops(tr, match, op)
+    dt = opattr.to_device(tr, DEV)
+    out = opattr.opattr_aggregate_ops(dt, torch.from_numpy(match).to(DEV),
+                                      torch.from_numpy(op).to(DEV))
+    torch.cuda.synchronize()
+    diag = opattr.read_diag(out["diag"])
+    parity.assert_table(out.table_host(), want["table"])
+    assert diag["status"] == want["diag"]["status"] == 0
+
+
 def test_attribute_tiered_pipeline():
     """The tiered pipeline as library calls (match + dedup broadcast, walk,
     tiers, table by tier operator) against the oracle's stages on GPT-2
