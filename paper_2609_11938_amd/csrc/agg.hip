@@ -73,10 +73,10 @@ struct AggWork {
   const uint32_t *ig, *ia, *ib;
   const PartRow *rows;
   // [0] items, [1] partial rows, [2] item tiles, [3] heavy-row chunks,
-  // [4] spread rows, [5] heavy rows
+  // [4] listed spread rows, [5] heavy rows
   int64_t *meta;
   uint32_t *ith, *gcnt, *goff;
-  uint32_t *multi;          // rows spread over several windows
+  uint32_t *multi;          // spread rows, when found by row
   uint32_t *heavy;          // rows over more than kHeavy windows: (row, first chunk) pairs
   unsigned long long *hch;  // chunk slots of the heavy rows: row << 32 | chunk
   PartRow *hpart;           // one partial per chunk slot
@@ -323,59 +323,112 @@ __device__ __forceinline__ const PartRow *row_part(const AggWork &w, int64_t w0,
   return j == 0 ? w.part + 2 * w0 + 1 : w.part + 2 * (w0 + j);
 }
 
-// 3a. one thread per operator row: a row without items is written empty, a
-// row inside one window is done, a row spread over several windows is listed
+// Spread rows (items over several windows) are found by row when there are
+// fewer rows than windows (3a lists them), else by window (3b checks each).
+__device__ __forceinline__ bool spread_by_row(const AggWork &w) {
+  return (int64_t)w.G < (w.meta[0] + kWinItems - 1) / kWinItems;
+}
+
+// 3a. rows without items: zero counts and no values, written by each wave
+// over its 64 consecutive rows with coalesced 8-byte stores. A row inside
+// one window was written by its window. When spread rows are found by row,
+// they are listed here, with one atomic per block (atomics on one address
+// serialise across the chip).
 template <bool DEF>
 __global__ void __launch_bounds__(256) k_row_triage(AggWork w) {
-  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
+  __shared__ uint32_t wcnt[4];
+  __shared__ unsigned long long bbase;
   const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= w.G) return;
-  const uint32_t lo = w.goff[g], hi = w.goff[g + 1];
-  if (hi == lo) {
-    Acc acc;
-    acc_zero(acc);
-    write_row_lane(w, g, acc, mx, dw);
-  } else if (lo / kWinItems != (hi - 1) / kWinItems) {
-    w.multi[atomicAdd((unsigned long long *)&w.meta[4], 1ull)] = g;
+  const int ln = lane_id();
+  bool empty = false, spread = false;
+  if (g < w.G) {
+    const uint32_t lo = w.goff[g], hi = w.goff[g + 1];
+    empty = hi == lo;
+    spread = !empty && lo / kWinItems != (hi - 1) / kWinItems;
+  }
+  if (spread_by_row(w)) {  // uniform over the grid
+    const unsigned long long sm = __ballot(spread);
+    if (ln == 0) wcnt[wave_id()] = (uint32_t)__popcll(sm);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      const uint32_t n = wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
+      bbase = n ? atomicAdd((unsigned long long *)&w.meta[4], (unsigned long long)n) : 0ull;
+    }
+    __syncthreads();
+    if (spread) {
+      unsigned long long pos = bbase;
+      for (int k = 0; k < wave_id(); ++k) pos += wcnt[k];
+      w.multi[pos + __popcll(sm & ((1ull << ln) - 1ull))] = g;
+    }
+  }
+  const unsigned long long em = __ballot(empty);
+  if (em) {
+    constexpr int kWords = (int)(sizeof(opattr_op_row) / 8);
+    static_assert(kWords == 24, "row layout: four counts, then the counter values");
+    unsigned long long *dst = reinterpret_cast<unsigned long long *>(w.table + (g - ln));
+    for (int x = ln; x < OPA_WAVE * kWords; x += OPA_WAVE) {
+      const int r = x / kWords, c = x % kWords;
+      if ((em >> r) & 1ull) dst[x] = c < 4 ? 0ull : 0x7FF8000000000000ull;
+    }
   }
 }
 
-// 3b. one wave per listed row. A row over more than kHeavy windows is
-// reduced in chunks of kChunk partials instead: it reserves consecutive chunk
-// slots, fills them (row, chunk) and lists itself with the first of them.
+// The spread row g over windows w0 .. w1, by one wave. A row over more than
+// kHeavy windows is reduced in chunks of kChunk partials instead: it reserves
+// consecutive chunk slots, fills them (row, chunk) and lists itself with the
+// first of them.
+template <bool DEF>
+__device__ __forceinline__ void combine_row(const AggWork &w, uint32_t g, int64_t w0, int64_t w1) {
+  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
+  const int ln = lane_id();
+  const uint32_t m = (uint32_t)(w1 - w0 + 1);
+  if (m > kHeavy) {
+    const uint32_t nch = (m + kChunk - 1) / kChunk;
+    uint32_t base = 0;
+    if (ln == 0) {
+      base = (uint32_t)atomicAdd((unsigned long long *)&w.meta[3], (unsigned long long)nch);
+      const uint64_t h = atomicAdd((unsigned long long *)&w.meta[5], 1ull);
+      w.heavy[2 * h] = g;
+      w.heavy[2 * h + 1] = base;
+    }
+    base = __shfl(base, 0, OPA_WAVE);
+    for (uint32_t c = ln; c < nch; c += OPA_WAVE)
+      if ((int64_t)base + c < w.hcap) w.hch[base + c] = ((unsigned long long)g << 32) | c;
+    return;
+  }
+  Acc acc;
+  acc_zero(acc);
+  for (uint32_t j = ln; j < m; j += OPA_WAVE) {
+    Acc b;
+    acc_load(b, row_part(w, w0, j));
+    acc_merge(acc, b, mx);
+  }
+  acc_wave_reduce(acc, mx);
+  write_row(w, g, acc, mx, dw);
+}
+
+// 3b. the spread rows, one wave each: from the list of 3a, or else one wave
+// per window: the window whose first item's row began in an earlier window
+// and ends in it combines that row (every spread row has exactly one such
+// window)
 template <bool DEF>
 __global__ void __launch_bounds__(256) k_combine(AggWork w) {
-  const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
-  const int64_t nm = w.meta[4];
-  const int ln = lane_id();
-  for (int64_t k = (int64_t)blockIdx.x * 4 + wave_id(); k < nm; k += (int64_t)gridDim.x * 4) {
-    const uint32_t g = w.multi[k];
+  const int64_t nwin = (w.meta[0] + kWinItems - 1) / kWinItems;
+  const int64_t wave = (int64_t)blockIdx.x * 4 + wave_id(), nwaves = (int64_t)gridDim.x * 4;
+  if (spread_by_row(w)) {
+    const int64_t nm = w.meta[4];
+    for (int64_t k = wave; k < nm; k += nwaves) {
+      const uint32_t g = w.multi[k];
+      const uint32_t lo = w.goff[g], hi = w.goff[g + 1];
+      combine_row<DEF>(w, g, lo / kWinItems, (hi - 1) / kWinItems);
+    }
+    return;
+  }
+  for (int64_t win = wave; win < nwin; win += nwaves) {
+    const uint32_t g = (uint32_t)(w.sit[win * kWinItems] >> 36);
     const uint32_t lo = w.goff[g], hi = w.goff[g + 1];
-    const int64_t w0 = lo / kWinItems, w1 = (hi - 1) / kWinItems;
-    const uint32_t m = (uint32_t)(w1 - w0 + 1);
-    if (m > kHeavy) {
-      const uint32_t nch = (m + kChunk - 1) / kChunk;
-      uint32_t base = 0;
-      if (ln == 0) {
-        base = (uint32_t)atomicAdd((unsigned long long *)&w.meta[3], (unsigned long long)nch);
-        const uint64_t h = atomicAdd((unsigned long long *)&w.meta[5], 1ull);
-        w.heavy[2 * h] = g;
-        w.heavy[2 * h + 1] = base;
-      }
-      base = __shfl(base, 0, OPA_WAVE);
-      for (uint32_t c = ln; c < nch; c += OPA_WAVE)
-        if ((int64_t)base + c < w.hcap) w.hch[base + c] = ((unsigned long long)g << 32) | c;
-      continue;
-    }
-    Acc acc;
-    acc_zero(acc);
-    for (uint32_t j = ln; j < m; j += OPA_WAVE) {
-      Acc b;
-      acc_load(b, row_part(w, w0, j));
-      acc_merge(acc, b, mx);
-    }
-    acc_wave_reduce(acc, mx);
-    write_row(w, g, acc, mx, dw);
+    if ((int64_t)lo >= win * kWinItems || (int64_t)(hi - 1) / kWinItems != win) continue;
+    combine_row<DEF>(w, g, lo / kWinItems, win);
   }
 }
 
@@ -452,10 +505,10 @@ static AggWork agg_work(const EncArgs &x) {
   w.gcnt = at<uint32_t>(x.ws, pl.gcnt);
   w.goff = at<uint32_t>(x.ws, pl.goff);
   w.heavy = at<uint32_t>(x.ws, pl.heavy);
+  w.multi = at<uint32_t>(x.ws, pl.multi);
   w.hch = at<unsigned long long>(x.ws, pl.hch);
   w.hpart = at<PartRow>(x.ws, pl.hpart);
   w.hcap = pl.hcap;
-  w.multi = at<uint32_t>(x.ws, pl.multi);
   w.sit = at<unsigned long long>(x.ws, pl.sit);
   w.part = at<PartRow>(x.ws, pl.part);
   w.table = x.table;
@@ -511,7 +564,8 @@ void reduce_items(const EncArgs &x, hipStream_t s) {
     else k_window_reduce<false><<<cgrid, 256, 0, s>>>(w);
   }
   const unsigned tg = (pl.G + 255) / 256;
-  const unsigned cg = (unsigned)((pl.G + 3) / 4 < 1024 ? (pl.G + 3) / 4 : 1024);
+  const int64_t cw = (pl.max_windows + 3) / 4;
+  const unsigned cg = (unsigned)(cw < 1024 ? (cw > 0 ? cw : 1) : 1024);
   const unsigned hg = (unsigned)(pl.hcap < 2048 ? pl.hcap : 2048);
   if (def) {
     k_row_triage<true><<<tg, 256, 0, s>>>(w);

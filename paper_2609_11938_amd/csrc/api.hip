@@ -197,6 +197,8 @@ __global__ void __launch_bounds__(1024) k_finish(opattr_diag *diag, const uint8_
                                                  uint32_t ns, const unsigned long long *part,
                                                  int nparts, opattr_summary *sum) {
   __shared__ uint32_t cnt;
+  __shared__ unsigned long long tot[4];
+  if (threadIdx.x < 4) tot[threadIdx.x] = 0;
   if (threadIdx.x == 0) cnt = 0;
   __syncthreads();
   if (sflag) {
@@ -204,15 +206,26 @@ __global__ void __launch_bounds__(1024) k_finish(opattr_diag *diag, const uint8_
     for (uint32_t s = threadIdx.x; s < ns; s += blockDim.x) c += sflag[s] ? 1u : 0u;
     if (c) atomicAdd(&cnt, c);
   }
+  // the per-block sums, one block's four per thread (integer sums: exact in
+  // any order)
+  if (part) {
+    unsigned long long v[4] = {0, 0, 0, 0};
+    for (int b = threadIdx.x; b < nparts; b += blockDim.x)
+#pragma unroll
+      for (int f = 0; f < 4; ++f) v[f] += part[b * 4 + f];
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+      const unsigned long long x = wave_reduce_add(v[f]);
+      if (lane_id() == 0 && x) atomicAdd(&tot[f], x);
+    }
+  }
   __syncthreads();
   if (threadIdx.x == 0 && part) {
     opattr_summary s{};
-    for (int b = 0; b < nparts; ++b) {
-      s.attributed_ns += part[b * 4 + 0];
-      s.unattributed_ns += part[b * 4 + 1];
-      s.total_ns += part[b * 4 + 2];
-      s.matched_ns += part[b * 4 + 3];
-    }
+    s.attributed_ns = tot[0];
+    s.unattributed_ns = tot[1];
+    s.total_ns = tot[2];
+    s.matched_ns = tot[3];
     s.attributed_fraction = s.total_ns ? (double)s.attributed_ns / (double)s.total_ns
                                        : __longlong_as_double(0x7FF8000000000000ll);
     *sum = s;

@@ -157,23 +157,63 @@ __global__ void __launch_bounds__(256) k_cov_finish(const unsigned long long *pa
 // the range's own op when op is NULL) is the range's operator, else R + its
 // operator, else -1 (the last row, unattributed). Bad range ids and
 // operators are counted.
+// four consecutive int32 from p + i (one 16-byte load when aligned); nv of them valid
+__device__ __forceinline__ void load4(const int32_t *p, int64_t i, int nv, int32_t (&o)[4]) {
+  if (nv == 4 && (reinterpret_cast<uintptr_t>(p + i) & 15) == 0) {
+    const int4 v = *reinterpret_cast<const int4 *>(p + i);
+    o[0] = v.x;
+    o[1] = v.y;
+    o[2] = v.z;
+    o[3] = v.w;
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) o[k] = k < nv ? p[i + k] : -1;
+  }
+}
+
+__device__ __forceinline__ void store4(int32_t *p, int64_t i, int nv, const int32_t (&v)[4]) {
+  if (nv == 4 && (reinterpret_cast<uintptr_t>(p + i) & 15) == 0) {
+    *reinterpret_cast<int4 *>(p + i) = make_int4(v[0], v[1], v[2], v[3]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (k < nv) p[i + k] = v[k];
+  }
+}
+
+// four launches per thread
 __global__ void k_dispatch_keys(const int32_t *__restrict__ range_id, const int32_t *__restrict__ op,
                                 const uint32_t *__restrict__ r_op, int64_t R, uint32_t NOPS,
                                 int64_t T, int32_t *key, int32_t *row, opattr_diag *diag) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   uint32_t bad = 0;
   if (i < T) {
-    const int32_t rid = range_id[i];
-    const bool rok = rid >= 0 && (int64_t)rid < R;
-    const int32_t o = op ? op[i] : (rok ? (int32_t)r_op[rid] : -1);
-    if (rid < -1 || (int64_t)rid >= R) bad++;
-    if (op && (o < -1 || (o >= 0 && (uint32_t)o >= NOPS))) bad++;
-    const bool ook = o >= 0 && (uint32_t)o < NOPS;
-    int64_t k = -1;  // the last row, as an unattributed operator
-    if (rok && ook && (uint32_t)o == r_op[rid]) k = rid;
-    else if (ook) k = R + o;
-    key[i] = (int32_t)k;
-    if (row) row[i] = (int32_t)(k >= 0 ? k : R + NOPS);
+    const int nv = T - i < 4 ? (int)(T - i) : 4;
+    int32_t rid[4], o[4], ky[4], rw[4];
+    load4(range_id, i, nv, rid);
+    if (op) load4(op, i, nv, o);
+    uint32_t ro[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const bool rok = k < nv && rid[k] >= 0 && (int64_t)rid[k] < R;
+      ro[k] = rok ? r_op[rid[k]] : 0xFFFFFFFFu;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (k >= nv) continue;
+      const bool rok = rid[k] >= 0 && (int64_t)rid[k] < R;
+      const int32_t ok_ = op ? o[k] : (rok ? (int32_t)ro[k] : -1);
+      if (rid[k] < -1 || (int64_t)rid[k] >= R) bad++;
+      if (op && (ok_ < -1 || (ok_ >= 0 && (uint32_t)ok_ >= NOPS))) bad++;
+      const bool ook = ok_ >= 0 && (uint32_t)ok_ < NOPS;
+      int64_t kk = -1;  // the last row, as an unattributed operator
+      if (rok && ook && (uint32_t)ok_ == ro[k]) kk = rid[k];
+      else if (ook) kk = R + ok_;
+      ky[k] = (int32_t)kk;
+      rw[k] = (int32_t)(kk >= 0 ? kk : R + NOPS);
+    }
+    store4(key, i, nv, ky);
+    if (row) store4(row, i, nv, rw);
   }
   const uint32_t b = wave_reduce_add(bad);
   if (lane_id() == 0 && b) atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)b);
@@ -183,8 +223,8 @@ void launch_dispatch_keys(const int32_t *range_id, const int32_t *op, const opat
                           uint32_t NOPS, int64_t T, int32_t *key, int32_t *row,
                           opattr_diag *diag, hipStream_t s) {
   if (T > 0)
-    k_dispatch_keys<<<(unsigned)((T + 255) / 256), 256, 0, s>>>(range_id, op, r->op_id, r->n, NOPS,
-                                                                T, key, row, diag);
+    k_dispatch_keys<<<(unsigned)((T + 1023) / 1024), 256, 0, s>>>(range_id, op, r->op_id, r->n,
+                                                                  NOPS, T, key, row, diag);
 }
 
 void run_tiers(const TierIn &x, hipStream_t s) {
