@@ -278,28 +278,60 @@ __device__ __forceinline__ void write_row_lane(const AggWork &w, uint32_t g, con
 
 // 2. one wave per window of 64 sorted items
 template <bool DEF>
-__global__ void __launch_bounds__(256) k_window_reduce(AggWork w) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
+k_window_reduce(AggWork w) {
+  constexpr int kPiece = 16;  // launches of a reference (at most)
+  // the matches and durations of the window's references, staged per wave
+  __shared__ int32_t s_m[4][kWinItems * kPiece];
+  __shared__ uint32_t s_d[4][kWinItems * kPiece];
   const uint32_t mx = DEF ? kDefMaxMask : w.in.maxmask, dw = DEF ? kDefDwMask : w.in.dwmask;
   const int64_t n = w.meta[0];
   const int64_t nwin = (n + kWinItems - 1) / kWinItems;
   const int ln = lane_id();
+  int32_t *lm = s_m[wave_id()];
+  uint32_t *ld = s_d[wave_id()];
   for (int64_t win = (int64_t)blockIdx.x * 4 + wave_id(); win < nwin;
        win += (int64_t)gridDim.x * 4) {
     const int64_t p = win * kWinItems + ln;
-    uint32_t g = 0xFFFFFFFFu;
+    uint32_t g = 0xFFFFFFFFu, a = 0, b = 0;
+    if (p < n) {
+      const unsigned long long it = w.sit[p];
+      a = (uint32_t)(it & 0x7FFFFFFFu);
+      b = (uint32_t)(it >> 31) & 31u;
+      g = (uint32_t)(it >> 36);
+    }
+    // A reference's launches are consecutive: the wave stages them four
+    // references at a time, sixteen lanes each, so that its loads of
+    // matches and durations are contiguous rather than one line per lane.
+    const uint32_t bs = b <= (uint32_t)kPiece ? b : (uint32_t)kPiece;  // staged launches
+    const uint32_t incl = wave_incl_scan_add(bs), pre = incl - bs;
+    if (__shfl(incl, OPA_WAVE - 1, OPA_WAVE) > 0) {
+#pragma unroll 2
+      for (int r = 0; r < kWinItems / 4; ++r) {
+        const int j = 4 * r + (ln >> 4), k = ln & 15;
+        const uint32_t aj = __shfl(a, j, OPA_WAVE), bj = __shfl(bs, j, OPA_WAVE);
+        const uint32_t pj = __shfl(pre, j, OPA_WAVE);
+        if ((uint32_t)k < bj) {
+          lm[pj + k] = w.in.match[aj + k];
+          ld[pj + k] = w.in.dur[aj + k];
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
     Acc acc;
     acc_zero(acc);
     if (p < n) {
-      const unsigned long long it = w.sit[p];
-      const uint32_t a = (uint32_t)(it & 0x7FFFFFFFu), b = (uint32_t)(it >> 31) & 31u;
-      g = (uint32_t)(it >> 36);
       if (b == 0) {
         acc_load(acc, w.rows + a);
       } else {
-        for (uint32_t k = 0; k < b; ++k)
-          acc_launch(acc, w.in, w.in.match[a + k], w.in.dur[a + k], mx, dw);
+        for (uint32_t k = 0; k < b; ++k) {
+          const bool st = k < bs;  // always, for references of at most kPiece launches
+          acc_launch(acc, w.in, st ? lm[pre + k] : w.in.match[a + k],
+                     st ? ld[pre + k] : w.in.dur[a + k], mx, dw);
+        }
       }
     }
+    __builtin_amdgcn_wave_barrier();  // the staged entries are read before the next window's
     // segmented scan by row (rows are contiguous in the window)
     const uint32_t gp = __shfl_up(g, 1, OPA_WAVE), gn = __shfl_down(g, 1, OPA_WAVE);
     const uint64_t heads = __ballot(ln == 0 || gp != g);
