@@ -48,6 +48,7 @@ struct EncParams {
   int32_t *range_id;
   uint8_t *fused;      // optional walk outputs
   int32_t *range_any;
+  int32_t *core_id;    // set: the innermost range's core position instead (no kinds)
   AggIn ag;
   EmitOut em;
   opattr_diag *diag;
@@ -319,7 +320,9 @@ k_enclose(EncParams a) {
       ridk[k] = (pk[k] >= lok[k] && ek[k] >= (int64_t)q[k]) ? pk[k] : -1;
 
     int32_t rout[kPer];
-    if (!a.cr.kind && !a.fused) {
+    if (a.core_id) {
+      store_run(a.core_id, ib, nv, ridk);
+    } else if (!a.cr.kind && !a.fused) {
       // Phase 3 without kinds: the innermost range is the op range; its row
       // and output id for every launch, loads in flight together
 #pragma unroll
@@ -662,6 +665,24 @@ void plan_emit(const EncArgs &x, hipStream_t s) {
   const EncParams a = enc_params(x);
   if (pl.T > 0) k_emit<<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
   plan_items(x, s);
+}
+
+void launch_innermost(const CoreRanges &cr, const opattr_kernels *k, const opattr_dims *d,
+                      void *ws, const Plan &pl, int32_t *core, opattr_diag *diag, hipStream_t s) {
+  EncParams a{};
+  a.T = pl.T;
+  a.q = k->query_ns ? k->query_ns : k->start_ns;
+  a.stream = k->stream_id;
+  a.NS = d->n_streams;
+  a.NOPS = d->n_ops;
+  a.cr = cr;
+  a.cr.kind = nullptr;  // the innermost range whatever its kind
+  a.rblk = at<int64_t>(ws, pl.rblk);
+  a.ree = at<int64_t>(ws, pl.ree);
+  a.npg = at<int32_t>(ws, pl.npg);
+  a.core_id = core;
+  a.diag = diag;
+  if (pl.T > 0) k_enclose<1><<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
 }
 
 void run_enclose(const EncArgs &x, hipStream_t s) {

@@ -251,6 +251,10 @@ struct EncArgs {
 AggIn agg_inputs(const EncArgs &x);
 // range_id of every launch (Alg. 2)
 void run_enclose(const EncArgs &a, hipStream_t s);
+// the innermost range of every launch (core position, -1 for none), kinds
+// not consulted; counts launches with bad stream ids
+void launch_innermost(const CoreRanges &cr, const opattr_kernels *k, const opattr_dims *d,
+                      void *ws, const Plan &pl, int32_t *core, opattr_diag *diag, hipStream_t s);
 // The aggregation in four parts. Plan (no matches needed): per-wave item and
 // row counts and their scan (with the enclosure when enclose is set), then
 // the items and their sort by operator row. Reduction: the runs in place
