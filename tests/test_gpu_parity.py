@@ -443,6 +443,36 @@ def test_enclose_all_parity(seed):
     _assert_all(out, want)
 
 
+def test_enclose_all_bad_streams_and_capacity():
+    """Launches on stream ids past n_streams get empty lists and count as
+    bad records; a capacity below the total writes exactly the lists that
+    end within it (the offsets stay complete)."""
+    import torch
+
+    print("case enclose_all bad streams", flush=True)
+    tr = cases.random_trace(995, T=300, R=80, S=3, t_max=60, max_depth=5)
+    tr["stream_id"] = tr["stream_id"].copy()
+    tr["stream_id"][[3, 77, 150]] = 7
+    want = O.enclose_all(tr)
+    dt = opattr.to_device(tr, DEV)
+    out = opattr.opattr_enclose_all(dt)
+    torch.cuda.synchronize()
+    off = parity.host(out["off"])
+    np.testing.assert_array_equal(off, want["off"])
+    np.testing.assert_array_equal(parity.host(out["ids"]), want["ids"])
+    diag = opattr.read_diag(out["diag"])
+    assert diag["bad_records"] == want["diag"]["bad_records"] == 3
+    assert all(off[i + 1] == off[i] for i in (3, 77, 150))
+    cap = int(off[-1]) // 2
+    part = opattr.opattr_enclose_all(dt, ids=torch.full((max(cap, 1),), -7, dtype=torch.int32,
+                                                          device=DEV))
+    torch.cuda.synchronize()
+    got = parity.host(part["ids"])
+    last = np.searchsorted(off, cap, side="right") - 1
+    np.testing.assert_array_equal(got[:off[last]], want["ids"][:off[last]])
+    assert np.all(got[off[last]:cap] == -7)
+
+
 def test_enclose_all_crossing_ranges_reported():
     """Crossing ranges: the list call reports them as the oracle does (count
     of streams with a crossing, NOT_NESTED status); the lists are then
