@@ -174,7 +174,8 @@ typedef struct {
 /* Error classes (bits of opattr_diag.flags) and status codes. */
 #define OPATTR_F_DATA 1u        /* an id out of range / a range with start > end */
 #define OPATTR_F_ORDER 2u       /* duplicate seq, or a promised layout is false   */
-#define OPATTR_F_LIMIT 4u       /* range nesting deeper than 255                  */
+#define OPATTR_F_LIMIT 4u       /* range nesting deeper than 255, or an internal
+                                   capacity exceeded (sized not to be)          */
 #define OPATTR_F_NOT_NESTED 8u  /* two ranges of one stream cross                 */
 #define OPATTR_F_PARTITION 16u  /* a partition is not one contiguous seq run      */
 #define OPATTR_F_DEDUP 32u      /* positional inheritance failed for a duplicate  */

@@ -85,6 +85,7 @@ struct AggWork {
   PartRow *part;            // [windows][2]: a continuing row's partial per window
   opattr_op_row *table;
   opattr_summary *sum;
+  opattr_diag *diag;
 };
 
 // Item tiles hold 1024 items (4 per thread) when the items fit the
@@ -470,6 +471,10 @@ __global__ void __launch_bounds__(kChunk) k_heavy_chunks(AggWork w) {
   const uint32_t mx = w.in.maxmask;
   __shared__ PartRow red[kChunk / OPA_WAVE];
   const int64_t ns = w.meta[3] < w.hcap ? w.meta[3] : w.hcap;
+  // the slots are sized so that this cannot happen; if it did, rows would
+  // lose partials, so it is reported rather than left silent
+  if (blockIdx.x == 0 && threadIdx.x == 0 && w.meta[3] > w.hcap)
+    atomicOr(&w.diag->flags, OPATTR_F_LIMIT);
   for (int64_t sl = blockIdx.x; sl < ns; sl += gridDim.x) {
     const unsigned long long e = w.hch[sl];
     const uint32_t g = (uint32_t)(e >> 32), c = (uint32_t)e;
@@ -545,6 +550,7 @@ static AggWork agg_work(const EncArgs &x) {
   w.part = at<PartRow>(x.ws, pl.part);
   w.table = x.table;
   w.sum = x.sum;
+  w.diag = x.diag;
   return w;
 }
 

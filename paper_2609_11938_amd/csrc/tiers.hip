@@ -54,40 +54,68 @@ __global__ void k_corr_bad(const int32_t *__restrict__ corr_op, int64_t C, uint3
     atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)__popcll(m));
 }
 
-// tier, operator and fused of launch i; returns the tier
-__device__ __forceinline__ int tier_of(const TierArgs &a, int64_t i, uint32_t &bad) {
-  const uint32_t nm = a.name[i];
-  const int32_t e = a.entry ? a.entry[i] : -1;
-  const int32_t rid = a.range_id[i];
-  if (rid < -1 || (int64_t)rid >= a.R) bad++;
-  uint32_t f0 = 0, nf = 0;  // the kernel name's fusion list
-  if (a.f_off && nm < a.NN) {
-    const uint32_t lo = a.f_off[nm], hi = a.f_off[nm + 1];
-    if (hi > lo) {
-      f0 = lo;
-      nf = hi - lo;
-    }
+constexpr int kTierPer = 4;  // launches per thread per step, their loads in flight together
+
+// Tier, operator and fused of kTierPer launches (x[k] < 0: none): every load
+// of one level for all of them before the next level (coalesced fields;
+// the fusion list bounds, the entry's and the range's operators; the first
+// fused operator), then the stores. Returns the tiers (-1: none).
+__device__ __forceinline__ void tiers_of(const TierArgs &a, const int64_t (&x)[kTierPer],
+                                         int (&t)[kTierPer], uint32_t (&d)[kTierPer],
+                                         uint32_t &bad) {
+  uint32_t nm[kTierPer];
+  int32_t e[kTierPer], rid[kTierPer];
+  uint8_t wf[kTierPer];
+#pragma unroll
+  for (int k = 0; k < kTierPer; ++k) {
+    const bool v = x[k] >= 0;
+    nm[k] = v ? a.name[x[k]] : 0xFFFFFFFFu;
+    e[k] = (v && a.entry) ? a.entry[x[k]] : -1;
+    rid[k] = v ? a.range_id[x[k]] : -1;
+    d[k] = v ? a.dur[x[k]] : 0u;
+    wf[k] = (v && a.walk_fused) ? a.walk_fused[x[k]] : 0;
   }
-  const int32_t co = (e >= 0 && e < a.C) ? a.corr_op[e] : -1;
-  int t = OPATTR_TIER_UNATTRIBUTED;
-  int32_t o = -1;
-  if (co >= 0 && (uint32_t)co < a.NOPS) {
-    t = OPATTR_TIER_HIGH;
-    o = co;
-  } else if (rid >= 0 && (int64_t)rid < a.R) {
-    t = OPATTR_TIER_NVTX;
-    o = (int32_t)a.r_op[rid];
-  } else if (nf > 0) {
-    const int32_t fo = a.f_op[f0];
-    if (fo >= 0 && (uint32_t)fo < a.NOPS) {
-      t = OPATTR_TIER_FUSION;
-      o = fo;
+  uint32_t f0[kTierPer], nf[kTierPer];
+  int32_t co[kTierPer], ro[kTierPer];
+#pragma unroll
+  for (int k = 0; k < kTierPer; ++k) {
+    f0[k] = 0;
+    nf[k] = 0;
+    if (a.f_off && nm[k] < a.NN) {
+      const uint32_t lo = a.f_off[nm[k]], hi = a.f_off[nm[k] + 1];
+      if (hi > lo) {
+        f0[k] = lo;
+        nf[k] = hi - lo;
+      }
     }
+    co[k] = (e[k] >= 0 && e[k] < a.C) ? a.corr_op[e[k]] : -1;
+    ro[k] = (rid[k] >= 0 && (int64_t)rid[k] < a.R) ? (int32_t)a.r_op[rid[k]] : -1;
   }
-  a.tier[i] = (uint8_t)t;
-  a.op[i] = o;
-  a.fused[i] = (uint8_t)(((a.walk_fused && a.walk_fused[i]) || nf > 1) ? 1 : 0);
-  return t;
+  int32_t fo[kTierPer];
+#pragma unroll
+  for (int k = 0; k < kTierPer; ++k) fo[k] = nf[k] > 0 ? a.f_op[f0[k]] : -1;
+#pragma unroll
+  for (int k = 0; k < kTierPer; ++k) {
+    t[k] = -1;
+    if (x[k] < 0) continue;
+    if (rid[k] < -1 || (int64_t)rid[k] >= a.R) bad++;
+    int tk = OPATTR_TIER_UNATTRIBUTED;
+    int32_t o = -1;
+    if (co[k] >= 0 && (uint32_t)co[k] < a.NOPS) {
+      tk = OPATTR_TIER_HIGH;
+      o = co[k];
+    } else if (rid[k] >= 0 && (int64_t)rid[k] < a.R) {
+      tk = OPATTR_TIER_NVTX;
+      o = ro[k];
+    } else if (nf[k] > 0 && fo[k] >= 0 && (uint32_t)fo[k] < a.NOPS) {
+      tk = OPATTR_TIER_FUSION;
+      o = fo[k];
+    }
+    a.tier[x[k]] = (uint8_t)tk;
+    a.op[x[k]] = o;
+    a.fused[x[k]] = (uint8_t)((wf[k] || nf[k] > 1) ? 1 : 0);
+    t[k] = tk;
+  }
 }
 
 __global__ void __launch_bounds__(256) k_tiers(TierArgs a) {
@@ -95,14 +123,21 @@ __global__ void __launch_bounds__(256) k_tiers(TierArgs a) {
   uint32_t cnt[4] = {0, 0, 0, 0}, bad = 0;
   unsigned long long ns[4] = {0, 0, 0, 0};
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < a.T; i += stride) {
-    const int t = tier_of(a, i, bad);
-    const uint32_t d = a.dur[i];
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < a.T;
+       i += stride * kTierPer) {
+    int64_t x[kTierPer];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      cnt[q] += t == q ? 1u : 0u;
-      ns[q] += t == q ? d : 0u;
-    }
+    for (int k = 0; k < kTierPer; ++k) x[k] = i + k * stride < a.T ? i + k * stride : -1;
+    int t[kTierPer];
+    uint32_t d[kTierPer];
+    tiers_of(a, x, t, d, bad);
+#pragma unroll
+    for (int k = 0; k < kTierPer; ++k)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        cnt[q] += t[k] == q ? 1u : 0u;
+        ns[q] += t[k] == q ? d[k] : 0u;
+      }
   }
   const uint32_t bw = wave_reduce_add(bad);
   if (lane_id() == 0 && bw)
