@@ -94,6 +94,8 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.ree = b.take(R * 8);
   pl.npg = b.take(R * 4);
   pl.mxv = b.take(R * 8);
+  pl.wfirst = b.take(R * 4);
+  pl.wfused = b.take(R);
   pl.rblk = b.take(((size_t)pl.NS + 1) * 8);
   pl.tbase = b.take(((size_t)pl.NS + 1) * 4);
   const size_t ntr = (size_t)pl.ntr_max;

@@ -49,6 +49,8 @@ struct EncParams {
   uint8_t *fused;      // optional walk outputs
   int32_t *range_any;
   int32_t *core_id;    // set: the innermost range's core position instead (no kinds)
+  const int32_t *wfirst;  // with kinds: each range's walk (first op range, fused)
+  const uint8_t *wfused;
   AggIn ag;
   EmitOut em;
   opattr_diag *diag;
@@ -343,6 +345,8 @@ k_enclose(EncParams a) {
       uint32_t glast = 0;
       uint8_t flast = 0;
       bool tlast = false;
+      int32_t aout[kPer];
+      uint8_t fout[kPer];
 #pragma unroll
       for (int k = 0; k < kPer; ++k) {
         const int32_t rid = ridk[k];
@@ -374,7 +378,10 @@ k_enclose(EncParams a) {
           // skipped kinds passed over, a boundary ends it
           int32_t first = rid;
           flast = 0;
-          if (a.cr.kind) {
+          if (a.cr.kind && !touch) {
+            first = a.wfirst[rid];  // the walk from rid, done once per range
+            flast = a.wfused[rid];
+          } else if (a.cr.kind) {
             first = -1;
             int nops = 0, hops = 0;
             for (int64_t j = rid; j >= 0 && hops < kMaxWalk; j = next_out(j), ++hops) {
@@ -394,10 +401,17 @@ k_enclose(EncParams a) {
         }
         rout[k] = rid >= 0 ? olast : -1;
         g[k] = k < nv ? (rid >= 0 ? glast : a.NOPS) : 0xFFFFFFFFu;
-        if (k < nv && a.range_any) a.range_any[ib + k] = rid >= 0 ? alast : -1;
-        if (k < nv && a.fused) a.fused[ib + k] = rid >= 0 ? flast : 0;
+        aout[k] = rid >= 0 ? alast : -1;
+        fout[k] = rid >= 0 ? flast : 0;
       }
+      // stored after the walks, so that no store sits between the loads of
+      // consecutive launches
       store_run(a.range_id, ib, nv, rout);
+      if (a.range_any) store_run(a.range_any, ib, nv, aout);
+      if (a.fused)
+#pragma unroll
+        for (int k = 0; k < kPer; ++k)
+          if (k < nv) a.fused[ib + k] = fout[k];
     }
   } else {
     bad += rows_from_ids(a, ib, nv, g);
@@ -638,6 +652,8 @@ static EncParams enc_params(const EncArgs &x) {
   a.R_in = x.r ? x.r->n : 0;
   a.op_in = x.r ? x.r->op_id : nullptr;
   a.em = emit_out(x.ws, pl);
+  a.wfirst = at<int32_t>(x.ws, pl.wfirst);
+  a.wfused = at<uint8_t>(x.ws, pl.wfused);
   return a;
 }
 

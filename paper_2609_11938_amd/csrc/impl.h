@@ -43,6 +43,7 @@ struct Plan {
   // ranges
   size_t rperm, rs_c, re_c, rst_c, rop_c, rkd_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
+  size_t wfirst, wfused;  // per range with kinds: the walk's first op range and fused
   // aggregation
   int64_t cap_items, cap_rows, max_windows, hcap;
   size_t wi, wr, hmb, ig, ia, ib, rows, meta, ith, itch, gcnt, goff, heavy, multi, sit, part;

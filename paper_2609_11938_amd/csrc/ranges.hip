@@ -409,6 +409,29 @@ CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws
   return cr;
 }
 
+// With range kinds: Alg. 2's walk from every range as the innermost one
+// (outward through the parents; a boundary ends it, skipped kinds are passed
+// over): the first op range (core position, -1 none) and whether more than
+// one op range is reached. A launch whose innermost range does not start at
+// its query point walks exactly this way, so the enclosure pass looks the
+// result up instead of walking.
+__global__ void k_range_walk(CoreRanges cr, const int32_t *npg, int32_t *wfirst,
+                             uint8_t *wfused) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= cr.n) return;
+  int32_t first = -1;
+  int nops = 0, hops = 0;
+  for (int64_t j = x; j >= 0 && hops < kMaxWalk; j = npg[j], ++hops) {
+    const uint8_t kd = cr.kind[j];
+    if (kd == OPATTR_KIND_BOUNDARY) break;
+    if (kd != OPATTR_KIND_OP) continue;
+    if (first < 0) first = (int32_t)j;
+    if (++nops > 1) break;  // fused: the rest of the walk changes nothing
+  }
+  wfirst[x] = first;
+  wfused[x] = nops > 1 ? 1 : 0;
+}
+
 void resolve_ranges(const CoreRanges &cr, const opattr_dims *d, void *ws, const Plan &pl,
                     uint8_t *range_depth, opattr_diag *diag, hipStream_t s) {
   const uint32_t NS = d->n_streams;
@@ -424,6 +447,9 @@ void resolve_ranges(const CoreRanges &cr, const opattr_dims *d, void *ws, const 
   const unsigned nb = (unsigned)((pl.R + 255) / 256);
   k_rresolve<<<nb, 256, 0, s>>>(w);
   k_rdepth<<<nb, 256, 0, s>>>(w, range_depth);
+  if (cr.kind)
+    k_range_walk<<<nb, 256, 0, s>>>(cr, at<int32_t>(ws, pl.npg), at<int32_t>(ws, pl.wfirst),
+                                   at<uint8_t>(ws, pl.wfused));
 }
 
 }  // namespace opa
