@@ -144,12 +144,6 @@ __device__ __forceinline__ uint32_t piece_heads(uint32_t hm, int nv) {
   return hm | ((nv > 0 && (lane_id() & 1) == 0) ? 1u : 0u);
 }
 
-// The operator row of launch x (an item's row) from its input range id.
-__device__ __forceinline__ uint32_t row_of_launch(const EncParams &a, int64_t x) {
-  const int32_t r = a.range_id[x];
-  return (r >= 0 && r < a.R_in && a.op_in[r] < a.NOPS) ? a.op_in[r] : a.NOPS;
-}
-
 // Run starts of a thread's launches inside its wave (bit k: launch k starts
 // a run; the wave's first launch always does), and the references' piece
 // starts (runs cut at every 16th launch as well).
@@ -510,6 +504,18 @@ __global__ void __launch_bounds__(kEncThreads) k_emit(EncParams a) {
   const uint32_t hpb = wave_incl_scan_add(nhp) - nhp;
   const uint32_t nr_w = __shfl(hb + nh, OPA_WAVE - 1, OPA_WAVE);
   const uint32_t ibase = a.em.wi[wave];
+  // the operator rows of the thread's run and piece starts (hp holds hm),
+  // all loaded before any item is stored
+  int32_t rin[kPer];
+  load_run(a.range_id, ib, nv, rin);
+  uint32_t gk[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int32_t r = rin[k];
+    const bool head = k < nv && ((hp >> k) & 1u);
+    gk[k] = (head && r >= 0 && r < a.R_in) ? a.op_in[r] : a.NOPS;
+    if (gk[k] >= a.NOPS) gk[k] = a.NOPS;
+  }
   if (nr_w <= (uint32_t)kRowCap) {
     // one item per run, written by the launch that starts it
     const uint32_t rbase = a.em.wr[wave];
@@ -517,7 +523,7 @@ __global__ void __launch_bounds__(kEncThreads) k_emit(EncParams a) {
     for (int k = 0; k < kPer; ++k) {
       if (!((hm >> k) & 1u)) continue;
       const uint32_t idx = hb + __popc(hm & ((1u << k) - 1u));
-      a.em.ig[ibase + idx] = row_of_launch(a, ib + k);
+      a.em.ig[ibase + idx] = gk[k];
       a.em.ia[ibase + idx] = rbase + idx;
       a.em.ib[ibase + idx] = 0;
     }
@@ -532,7 +538,7 @@ __global__ void __launch_bounds__(kEncThreads) k_emit(EncParams a) {
       const uint32_t rest = hp >> (k + 1);
       const uint32_t len = rest ? (uint32_t)__ffs(rest) : (uint32_t)(nv - k) + spill;
       const uint32_t idx = hpb + __popc(hp & ((1u << k) - 1u));
-      a.em.ig[ibase + idx] = row_of_launch(a, ib + k);
+      a.em.ig[ibase + idx] = gk[k];
       a.em.ia[ibase + idx] = (uint32_t)(ib + k);
       a.em.ib[ibase + idx] = len;
     }
