@@ -107,45 +107,52 @@ __device__ __forceinline__ void acc_merge(Acc &a, const Acc &b, uint32_t maxmask
 }
 
 // Lane shift of a 64-bit value by a DPP move of each half (register to
-// register, no LDS round trip); lanes without a source get 0.
+// register, no LDS round trip). Lanes without a source (bound_ctrl: 0) or in
+// rows the row mask leaves out (not written) hold no shifted value: the scan
+// steps use the result only in lanes that take it, which always have a
+// source. The move needs no old value, hence no extra register move.
 template <int CTRL, int ROWMASK, int BANKMASK>
 __device__ __forceinline__ unsigned long long dpp64(unsigned long long v) {
   const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
-  const uint32_t l2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)lo, CTRL, ROWMASK, BANKMASK, false);
-  const uint32_t h2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)hi, CTRL, ROWMASK, BANKMASK, false);
+  const uint32_t l2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)lo, CTRL, ROWMASK, BANKMASK, true);
+  const uint32_t h2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)hi, CTRL, ROWMASK, BANKMASK, true);
   return ((unsigned long long)h2 << 32) | l2;
 }
 
-// One step of the segmented scan, field by field so that no second
-// accumulator is held: a += the shifted value if take.
+// One step of the segmented scan: a += the shifted value in the lanes that
+// take it. Fields go in groups of four: the group's moves, then its adds
+// under one branch, so that no second accumulator is held and the adds need
+// no per-field select.
 template <int CTRL, int ROWMASK, int BANKMASK>
 __device__ __forceinline__ void acc_scan_dpp(Acc &a, bool take, uint32_t maxmask) {
   {
-    const unsigned long long y = dpp64<CTRL, ROWMASK, BANKMASK>(a.kc);
-    if (take) a.kc += y;
-  }
-  {
-    const unsigned long long y = dpp64<CTRL, ROWMASK, BANKMASK>(a.tns);
-    if (take) a.tns += y;
-  }
-  {
-    const unsigned long long y = dpp64<CTRL, ROWMASK, BANKMASK>(a.mc);
-    if (take) a.mc += y;
-  }
-  {
-    const unsigned long long y = dpp64<CTRL, ROWMASK, BANKMASK>(a.mns);
-    if (take) a.mns += y;
-  }
-#pragma unroll
-  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-    const unsigned long long y = dpp64<CTRL, ROWMASK, BANKMASK>(a.v[c]);
+    const unsigned long long y0 = dpp64<CTRL, ROWMASK, BANKMASK>(a.kc);
+    const unsigned long long y1 = dpp64<CTRL, ROWMASK, BANKMASK>(a.tns);
+    const unsigned long long y2 = dpp64<CTRL, ROWMASK, BANKMASK>(a.mc);
+    const unsigned long long y3 = dpp64<CTRL, ROWMASK, BANKMASK>(a.mns);
+    const uint32_t yn = (uint32_t)__builtin_amdgcn_mov_dpp((int)a.nan, CTRL, ROWMASK, BANKMASK, true);
     if (take) {
-      if ((maxmask >> c) & 1u) a.v[c] = y > a.v[c] ? y : a.v[c];
-      else a.v[c] = d2bits(bits2d(a.v[c]) + bits2d(y));
+      a.kc += y0;
+      a.tns += y1;
+      a.mc += y2;
+      a.mns += y3;
+      a.nan |= yn;
     }
   }
-  const uint32_t yn = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)a.nan, CTRL, ROWMASK, BANKMASK, false);
-  if (take) a.nan |= yn;
+#pragma unroll
+  for (int g = 0; g < OPATTR_NUM_COUNTERS; g += 4) {
+    unsigned long long y[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) y[j] = dpp64<CTRL, ROWMASK, BANKMASK>(a.v[g + j]);
+    if (take) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int c = g + j;
+        if ((maxmask >> c) & 1u) a.v[c] = y[j] > a.v[c] ? y[j] : a.v[c];
+        else a.v[c] = d2bits(bits2d(a.v[c]) + bits2d(y[j]));
+      }
+    }
+  }
 }
 
 // Segmented inclusive scan over the wave (segment of lane l starts at lane
