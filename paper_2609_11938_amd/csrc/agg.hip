@@ -13,9 +13,11 @@
 //      matched duration, NaN for absent counters and rows without matched
 //      launches), a row crossing the window's edge leaves a partial for it,
 //   3. rows without items, and rows spread over several windows, finalised in
-//      a second pass: one wave per row, or a whole block for a row spread
-//      over many windows (one operator holding most of the launches, e.g.
-//      the UNATTRIBUTED row of a workload that is mostly not enclosed).
+//      a second pass: one wave per spread row, or, for a row spread over
+//      many windows (one operator holding most of the launches, e.g. the
+//      UNATTRIBUTED row of a workload that is mostly not enclosed), chunks
+//      of 256 window partials reduced by a block each and then merged in
+//      order by one wave.
 // The summary over the table is taken by the finishing kernel. Every sum is
 // taken in a fixed order, so results are reproducible.
 #include "accum.h"
