@@ -23,7 +23,7 @@ static bool has_dedup(const opattr_kernels *k, const opattr_dims *d) {
 }
 
 Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_ranges *r,
-               const opattr_dims *d) {
+               const opattr_dims *d, bool second_match) {
   Plan pl{};
   pl.T = k ? k->n : 0;
   pl.P = p ? p->n : 0;
@@ -156,6 +156,22 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.ident = b.take((size_t)d->n_ops * 4);
   pl.sumpart = b.take((size_t)kSumBlocks * 4 * 8);
   pl.misc = b.take(256);
+  // a second set of the segment path's matching arrays, so that a second
+  // matching (the tiered call's correlation lookup) can run beside the first
+  pl.m2 = second_match && pl.seg;
+  if (pl.m2) {
+    pl.kblk2 = b.take(((size_t)pl.NS + 2) * 8);
+    pl.tbnd2 = b.take(((size_t)pl.nt + 1) * pl.NS * 4);
+    pl.tlh2 = b.take((size_t)pl.nt * NN * 4);
+    pl.pfh2 = b.take((size_t)pl.ntp * NN * 4);
+    pl.tlch2 = b.take((size_t)pl.ncht * NN * 4);
+    pl.pfch2 = b.take((size_t)pl.nchp * NN * 4);
+    pl.tlc2 = b.take(NN * 4);
+    pl.pfc2 = b.take(NN * 4);
+    pl.off2 = b.take(NN * 4);
+    pl.slot2 = b.take(P * 4);
+    pl.nbs2 = b.take(T * 4);
+  }
   pl.total = b.off;
   return pl;
 }
@@ -671,7 +687,25 @@ size_t opattr_attribute_tiered_workspace_bytes(const opattr_kernels *k, const op
                                                const opattr_dims *d) {
   if (!k || !p || !d) return 0;
   const opattr_profiled m = tiered_rows(p, corr);
-  return make_plan(k, &m, r, d).total;
+  return make_plan(k, &m, r, d, true).total;
+}
+
+// The plan with the segment path's matching arrays swapped for the second set.
+static Plan second_match_plan(const Plan &pl) {
+  Plan q = pl;
+  if (!pl.m2) return q;
+  q.kblk = pl.kblk2;
+  q.tbnd = pl.tbnd2;
+  q.tlh = pl.tlh2;
+  q.pfh = pl.pfh2;
+  q.tlch = pl.tlch2;
+  q.pfch = pl.pfch2;
+  q.tlc = pl.tlc2;
+  q.pfc = pl.pfc2;
+  q.off = pl.off2;
+  q.slot = pl.slot2;
+  q.nbs = pl.nbs2;
+  return q;
 }
 
 int opattr_attribute_tiered(const opattr_kernels *k, const opattr_profiled *p,
@@ -690,7 +724,7 @@ int opattr_attribute_tiered(const opattr_kernels *k, const opattr_profiled *p,
     return OPATTR_ERR_INVALID_ARG;
   if (fmap && (!fmap->off || !fmap->op_id)) return OPATTR_ERR_INVALID_ARG;
   const opattr_profiled rows = tiered_rows(p, corr);
-  const Plan pl = make_plan(k, &rows, r, d);
+  const Plan pl = make_plan(k, &rows, r, d, true);
   if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   check_kernel_layout(k, d, diag, s);
@@ -721,15 +755,30 @@ int opattr_attribute_tiered(const opattr_kernels *k, const opattr_profiled *p,
   // matching with the dedup broadcast, then the correlation lookup (Alg. 1
   // over the map's entries, partitions off) into the item array
   build_seq_view(k, d, ws, pl, diag, validate, s);
-  IomArgs a{k, p, d, policy, match, nullptr, diag, ws, &pl, true, validate};
-  run_match(a, s);
+  // the correlation lookup needs only the launches and the map: on the
+  // segment path it runs on the second side stream with its own arrays,
+  // beside the matching of the profiled rows
   int32_t *entry = nullptr;
   const TiersView v(k, corr, d);
+  const Plan pl2 = second_match_plan(pl);
+  const bool beside = corr && ss && pl.m2;
   if (corr) {
     entry = at<int32_t>(ws, pl.ia);
+    if (beside) {
+      note(hipEventRecord(ss->fork2, s));
+      note(hipStreamWaitEvent(ss->s2, ss->fork2, 0));
+      IomArgs c{&v.k, &v.p, &v.d, corr_policy, entry, nullptr, diag, ws, &pl2, false, validate};
+      run_match(c, ss->s2);
+      note(hipEventRecord(ss->join2, ss->s2));
+    }
+  }
+  IomArgs a{k, p, d, policy, match, nullptr, diag, ws, &pl, true, validate};
+  run_match(a, s);
+  if (corr && !beside) {
     IomArgs c{&v.k, &v.p, &v.d, corr_policy, entry, nullptr, diag, ws, &pl, false, validate};
     run_match(c, s);
   }
+  if (beside) note(hipStreamWaitEvent(s, ss->join2, 0));
   if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
   TierIn x{k, corr, fmap, r, d, entry, range_id, fused, tier, op, fused, cov, diag, ws, &pl};
   run_tiers(x, s);

@@ -40,6 +40,8 @@ struct Plan {
   size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist, rs_hist_r, kblk, tbnd;
   size_t tlh, pfh, tlch, pfch, tlc, pfc, off, slot;
   size_t pfirst, plast, pheads, prec, mbs, nbs;
+  bool m2;  // the second set below exists
+  size_t kblk2, tbnd2, tlh2, pfh2, tlch2, pfch2, tlc2, pfc2, off2, slot2, nbs2;
   // ranges
   size_t rperm, rs_c, re_c, rst_c, rop_c, rkd_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
@@ -56,8 +58,9 @@ struct Plan {
   size_t misc;   // small device scalars
 };
 
+// second_match: also a second set of the segment path's matching arrays
 Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_ranges *r,
-               const opattr_dims *d);
+               const opattr_dims *d, bool second_match = false);
 
 // First HIP error of the calling host thread since the last reset; entry
 // points report it as OPATTR_ERR_HIP.
