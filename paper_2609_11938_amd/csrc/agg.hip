@@ -369,7 +369,7 @@ __device__ __forceinline__ bool spread_by_row(const AggWork &w) {
 // one window was written by its window. When spread rows are found by row,
 // they are listed here, with one atomic per block (atomics on one address
 // serialise across the chip).
-template <bool DEF>
+template <bool DEF>  // the kinds do not matter here; one instance is used
 __global__ void __launch_bounds__(256) k_row_triage(AggWork w) {
   __shared__ uint32_t wcnt[4];
   __shared__ unsigned long long bbase;
@@ -592,7 +592,15 @@ void plan_items(const EncArgs &x, hipStream_t s) {
   probe_end(OPATTR_PROBE_ITEM_SORT, s);
 }
 
-void reduce_items(const EncArgs &x, hipStream_t s) {
+// the rows without items and the listing of spread rows need only the
+// sorted items' row offsets, so they can run before the window reduction
+void triage_rows(const EncArgs &x, hipStream_t s) {
+  const Plan &pl = *x.pl;
+  const AggWork w = agg_work(x);
+  k_row_triage<true><<<(pl.G + 255) / 256, 256, 0, s>>>(w);
+}
+
+void reduce_items(const EncArgs &x, hipStream_t s, bool triaged) {
   const Plan &pl = *x.pl;
   AggWork w = agg_work(x);
   const bool def = w.in.maxmask == kDefMaxMask && w.in.dwmask == kDefDwMask;
@@ -607,13 +615,9 @@ void reduce_items(const EncArgs &x, hipStream_t s) {
   const int64_t cw = (pl.max_windows + 3) / 4;
   const unsigned cg = (unsigned)(cw < 1024 ? (cw > 0 ? cw : 1) : 1024);
   const unsigned hg = (unsigned)(pl.hcap < 2048 ? pl.hcap : 2048);
-  if (def) {
-    k_row_triage<true><<<tg, 256, 0, s>>>(w);
-    k_combine<true><<<cg, 256, 0, s>>>(w);
-  } else {
-    k_row_triage<false><<<tg, 256, 0, s>>>(w);
-    k_combine<false><<<cg, 256, 0, s>>>(w);
-  }
+  if (!triaged) k_row_triage<true><<<tg, 256, 0, s>>>(w);
+  if (def) k_combine<true><<<cg, 256, 0, s>>>(w);
+  else k_combine<false><<<cg, 256, 0, s>>>(w);
   k_heavy_chunks<<<hg, kChunk, 0, s>>>(w);
   if (def) k_heavy_rows<true><<<64, 256, 0, s>>>(w);
   else k_heavy_rows<false><<<64, 256, 0, s>>>(w);

@@ -597,6 +597,7 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   plan_counts(e, true, s2);
   if (ss) note(hipEventRecord(ss->join, s2));
   plan_emit(e, s2);
+  triage_rows(e, s2);  // empty rows and the spread-row list, off the caller's path
   if (ss) note(hipEventRecord(ss->join3, s2));
   build_seq_view(k, d, ws, pl, diag, validate, s);
   IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, validate};
@@ -609,7 +610,7 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
   reduce_runs(e, s);
   if (ss) note(hipStreamWaitEvent(s, ss->join3, 0));
-  reduce_items(e, s);
+  reduce_items(e, s, true);
   launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s, table, sum, pl.G, d->n_ops,
                 at<unsigned long long>(ws, pl.sumpart));
   return launch_status();

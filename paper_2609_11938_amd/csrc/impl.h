@@ -271,7 +271,9 @@ void reduce_runs(const EncArgs &a, hipStream_t s);
 void run_aggregate_all(const EncArgs &a, hipStream_t s);
 // item sort by row (agg.hip), and the per-row reduction of the sorted items
 void plan_items(const EncArgs &a, hipStream_t s);
-void reduce_items(const EncArgs &a, hipStream_t s);
+// triaged: triage_rows already ran (on a stream joined before this one)
+void reduce_items(const EncArgs &a, hipStream_t s, bool triaged = false);
+void triage_rows(const EncArgs &a, hipStream_t s);
 
 // ---- finish (api.hip) ---------------------------------------------------------
 // status of the diag record; with a table, also the summary over its G rows
