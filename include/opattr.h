@@ -286,8 +286,10 @@ int opattr_tiers(const opattr_kernels *k, const opattr_corr_map *corr,
 /* Tiered attribution in one call: opattr_match (with the dedup broadcast
    when partitions are given), opattr_enclose_walk's range_id and fused,
    opattr_tiers and opattr_aggregate_ops, with the ranges and the walk on a
-   side stream of the device beside the two matchings (the profiled rows,
-   then the correlation map), joined back before the tiers. Out (device):
+   side stream of the device beside the two matchings (the profiled rows;
+   the correlation map, on a second side stream with its own workspace
+   arrays when the kernels are stream-major with dense seq, else after the
+   profiled rows), all joined back on `stream` before the tiers. Out (device):
    match, range_id, tier, op, fused [k->n]; table[n_ops + 1] by tier
    operator; sum; cov. One diag record covers both matchings (their count
    diagnostics add up; STRICT in either makes a count mismatch an error).
