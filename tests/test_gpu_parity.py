@@ -63,12 +63,34 @@ def test_config_parity(cfg, emission):
     parity.assert_attribute(out, want, diag)
 
 
-def test_large_parity_full_size():
-    """The 10M-launch, 16-stream, dedup 48/3 trace in the benchmark's launch
-    configuration, every output compared."""
-    print("case config=large emission=stream_major", flush=True)
-    tr = _trace("large", "stream_major")
-    want = _oracle("large", "stream_major")
+@pytest.mark.parametrize("emission,flags", [
+    ("stream_major", HINTS),
+    ("seq", opattr.SEQ_DENSE),
+    ("shuffled", 0),
+    ("stream_major", HINTS | opattr.VALIDATE),
+], ids=["stream_major", "seq", "shuffled", "stream_major_validate"])
+def test_large_parity_full_size(emission, flags):
+    """The 10M-launch, 16-stream, dedup 48/3 trace, every output compared:
+    in the benchmark's launch configuration (stream-major with every layout
+    hint), in launch order (the launch-order view is a scatter), shuffled
+    (no hints: the seq sort, the kernel sort by stream and query point, the
+    500k-range nesting sort), and with the hints checked (VALIDATE)."""
+    print(f"case config=large emission={emission} flags={flags:#x}", flush=True)
+    tr = _trace("large", emission)
+    want = _oracle("large", emission)
+    out, diag = _run(tr, flags=flags)
+    parity.assert_attribute(out, want, diag)
+    assert diag["status"] == 0 and diag["order_violations"] == 0
+
+
+def test_many_names_full_size():
+    """More names than the LDS counters hold (5000) on the 10M-launch trace
+    with dedup 48/3: the tile radix sort ranks every tile and a separate pass
+    broadcasts to the duplicates."""
+    print("case config=large names=5000", flush=True)
+    tr = tg.generate("large", emission="stream_major", names=5000)
+    assert tr["n_names"] == 5000 and int(tr["name_id"].max()) >= 4096
+    want = O.attribute(tr)
     out, diag = _run(tr, flags=HINTS)
     parity.assert_attribute(out, want, diag)
     assert diag["status"] == 0
