@@ -92,6 +92,51 @@ __device__ __forceinline__ void acc_launch(Acc &a, const AggIn &in, int32_t m, u
   }
 }
 
+// The counter row m (fp32), or nothing when m is outside [0, P): the load
+// half of acc_launch, so that a caller can have the next row in flight.
+__device__ __forceinline__ void acc_load_row(const AggIn &in, int32_t m,
+                                             float (&v)[OPATTR_NUM_COUNTERS]) {
+  if (m < 0 || (int64_t)m >= in.P) return;
+  const float *row = in.counters + (int64_t)m * in.rs;
+  if (in.vec4) {
+    const float4 *r4 = reinterpret_cast<const float4 *>(row);
+#pragma unroll
+    for (int q = 0; q < OPATTR_NUM_COUNTERS / 4; ++q) {
+      const float4 t = r4[q];
+      v[4 * q] = t.x;
+      v[4 * q + 1] = t.y;
+      v[4 * q + 2] = t.z;
+      v[4 * q + 3] = t.w;
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) v[c] = row[(int64_t)c * in.cs];
+  }
+}
+
+// The accumulation half of acc_launch, with the row already loaded.
+__device__ __forceinline__ void acc_add_row(Acc &a, const AggIn &in, int32_t m, uint32_t d,
+                                            const float (&v)[OPATTR_NUM_COUNTERS], uint32_t mx,
+                                            uint32_t dw) {
+  a.kc += 1;
+  a.tns += d;
+  if (m < 0 || (int64_t)m >= in.P) return;
+  a.mc += 1;
+  a.mns += d;
+  const double dd = (double)d;
+#pragma unroll
+  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
+    if ((mx >> c) & 1u) {
+      const unsigned long long k = f2key(v[c]);
+      a.v[c] = k > a.v[c] ? k : a.v[c];
+      if (v[c] != v[c]) a.nan |= 1u << c;
+    } else {
+      const double x = ((dw >> c) & 1u) ? (double)v[c] * dd : (double)v[c];  // m_i * d_i
+      a.v[c] = d2bits(bits2d(a.v[c]) + x);
+    }
+  }
+}
+
 // a <- a (+) b, where b covers launches after a's
 __device__ __forceinline__ void acc_merge(Acc &a, const Acc &b, uint32_t maxmask) {
   a.kc += b.kc;

@@ -2,6 +2,7 @@
 // sequencing on the caller's stream.
 #include <string.h>
 
+#include "accum.h"
 #include "common.h"
 #include "impl.h"
 
@@ -78,8 +79,18 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.plast = b.take(dd ? (size_t)pl.NP * 4 : 0);
   pl.pheads = b.take(dd ? (size_t)pl.NP * 4 : 0);
   pl.prec = b.take(dd ? (size_t)pl.NP * 8 : 0);
-  pl.mbs = b.take(dd ? T * 4 : 0);
+  pl.mbs = b.take(dd || pl.seg ? T * 4 : 0);
   pl.nbs = b.take(T * 4);  // dedup source names, or the fast path's key and in-tile rank
+  pl.bcnt = b.take(pl.seg ? (size_t)pl.nt * 4 : 0);
+  // the fused attribution keeps one partial result per run of launches of
+  // one operator row; ranges at most one per 16 launches keep the runs long
+  // enough for its per-block capacity (the rest would go through atomics)
+  // (only opattr_attribute, which always has ranges, takes it: a plan
+  // without ranges must stay within the size of the plan with them)
+  pl.fused = pl.seg && r != nullptr && pl.G <= kFusedMaxRows && pl.R * 16 <= pl.T && pl.T > 0;
+  pl.acc = b.take(pl.fused ? (size_t)pl.G * 200 : 0);
+  pl.fbkt = b.take(pl.fused ? fused_bkt_bytes(pl.T) : 0);
+  pl.fsplit = b.take(pl.fused ? fused_split_bytes(pl.G) : 0);
   const bool rs = !pl.ranges_nested;
   pl.rperm = b.take(rs ? R * 4 : 0);
   pl.rs_c = b.take(rs ? R * 8 : 0);
@@ -119,6 +130,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.ia = b.take((size_t)pl.cap_items * 4);
   pl.ib = b.take((size_t)pl.cap_items * 4);
   pl.rows = b.take((size_t)pl.cap_rows * 200);
+  pl.fparts = pl.rows;  // the fused attribution's kept partials (never both in one call)
   pl.meta = b.take(8 * 8);
   // item sort: per-tile row histograms for few rows, else one radix sort
   const bool few_rows = pl.G <= kFastKeys;
@@ -269,10 +281,10 @@ __global__ void __launch_bounds__(1024) k_finish(opattr_diag *diag, const uint8_
 
 void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s,
                    const opattr_op_row *table, opattr_summary *sum, uint32_t G, uint32_t NOPS,
-                   unsigned long long *part) {
+                   unsigned long long *part, int prepart) {
   probe_begin(OPATTR_PROBE_FINALIZE, s);
-  int nb = 0;
-  if (table) {
+  int nb = prepart;
+  if (table && prepart <= 0) {
     const uint32_t want = (G + 255) / 256;
     nb = (int)(want < (uint32_t)kSumBlocks ? (want > 0 ? want : 1) : kSumBlocks);
     k_summary_part<<<nb, 256, 0, s>>>(table, G, NOPS, part);
@@ -551,6 +563,74 @@ int opattr_aggregate(const opattr_kernels *k, const opattr_profiled *p, const in
   return launch_status();
 }
 
+// opattr_attribute on the fused path (kernels stream-major with dense seq,
+// ranges at most one per 16 launches): the ranges and the enclosure on a
+// side stream, the profiled slot table on a second one, the matching up to
+// the eligible launches' rows on the caller's stream; then one pass gives
+// every launch its match (dedup broadcast included) and one pass reduces the
+// runs of launches of one operator row.
+static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
+                           const opattr_ranges *r, const opattr_dims *d, int policy,
+                           const uint8_t *agg_kind, int32_t *match, int32_t *range_id,
+                           uint8_t *range_depth, uint32_t *name_counts, opattr_op_row *table,
+                           opattr_summary *sum, opattr_diag *diag, void *ws, const Plan &pl,
+                           hipStream_t s) {
+  SideStream *ss = side_stream();
+  const hipStream_t s2 = ss ? ss->s : s;
+  if (ss) {
+    note(hipEventRecord(ss->fork, s));
+    note(hipStreamWaitEvent(s2, ss->fork, 0));
+  }
+  clear_fused_acc(ws, pl, s2);
+  probe_begin(OPATTR_PROBE_RANGES, s2);
+  const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, false, s2);
+  resolve_ranges(cr, d, ws, pl, range_depth, diag, s2);
+  probe_end(OPATTR_PROBE_RANGES, s2);
+  EncArgs e{};
+  e.k = k;
+  e.p = p;
+  e.match = match;
+  e.r = r;
+  e.cr = cr;
+  e.d = d;
+  e.range_id = range_id;
+  e.agg_kind = agg_kind ? agg_kind : kDefaultKind;
+  e.table = table;
+  e.sum = sum;
+  e.diag = diag;
+  e.ws = ws;
+  e.pl = &pl;
+  run_enclose(e, s2);
+  if (ss) note(hipEventRecord(ss->join, s2));
+  IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, false};
+  a.buckets = true;
+  if (ss) {
+    a.pf_stream = ss->s2;
+    a.pf_fork = ss->fork2;
+    a.pf_join = ss->join2;
+  }
+  run_match(a, s);
+  if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
+  const AggIn in = agg_inputs(e);
+  FusedIn f{};
+  f.k = k;
+  f.r = r;
+  f.d = d;
+  f.range_id = range_id;
+  f.match = match;
+  f.in = &in;
+  f.absent = p->absent_mask;
+  f.table = table;
+  f.diag = diag;
+  f.ws = ws;
+  f.pl = &pl;
+  run_fused_match(f, s);
+  run_fused_agg(f, s);
+  launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s, table, sum, pl.G, d->n_ops,
+                at<unsigned long long>(ws, pl.sumpart), fused_sum_blocks(pl));
+  return launch_status();
+}
+
 int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const opattr_ranges *r,
                      const opattr_dims *d, int policy, const uint8_t *agg_kind, int32_t *match,
                      int32_t *range_id, uint8_t *range_depth, uint32_t *name_counts,
@@ -565,6 +645,8 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   hipStream_t s = (hipStream_t)stream;
   check_kernel_layout(k, d, diag, s);
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
+  if (pl.fused) return attribute_fused(k, p, r, d, policy, agg_kind, match, range_id,
+                                       range_depth, name_counts, table, sum, diag, ws, pl, s);
   // the ranges, the enclosure and the aggregation plan do not depend on the
   // matching: they run on a side stream of this device, joined back before
   // the run reduction (counts) and the per-row reduction (items)

@@ -40,6 +40,12 @@ struct Plan {
   size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist, rs_hist_r, kblk, tbnd;
   size_t tlh, pfh, tlch, pfch, tlc, pfc, off, slot;
   size_t pfirst, plast, pheads, prec, mbs, nbs;
+  size_t bcnt;  // bucket path: bucket size of every seq tile
+  // fused attribution (segment path, sparse ranges, few rows): row
+  // accumulators, kept partials (aliasing the partial rows of the other
+  // aggregation), their bucket entries, and the per-bucket shares
+  bool fused;
+  size_t acc, fparts, fbkt, fsplit;
   bool m2;  // the second set below exists
   size_t kblk2, tbnd2, tlh2, pfh2, tlch2, pfch2, tlc2, pfc2, off2, slot2, nbs2;
   // ranges
@@ -145,6 +151,20 @@ void launch_gather_key_u32(const uint32_t *src, const uint32_t *perm, uint64_t *
                            hipStream_t s);
 
 // ---- IOM (iom.hip) -----------------------------------------------------------
+// Per partition p, how its launches find their row:
+//   hi == kRecEligible  p is its own class representative: its launches rank
+//                       themselves;
+//   hi == kRecNone      p has no valid representative: no row, no dedup error;
+//   otherwise           a duplicate: the launch at seq rank x takes the row of
+//                       the launch at x + delta when x < hi (the representative
+//                       partition is shorter otherwise), else a dedup error;
+//                       hi == 0 when either partition is not one run.
+struct PartRec {
+  int32_t delta;
+  uint32_t hi;
+};
+constexpr uint32_t kRecEligible = 0xFFFFFFFFu, kRecNone = 0xFFFFFFFEu;
+
 struct IomArgs {
   const opattr_kernels *k;
   const opattr_profiled *p;
@@ -157,6 +177,9 @@ struct IomArgs {
   const Plan *pl;
   bool want_dedup;  // also broadcast to duplicate partitions
   bool validate;
+  // bucket path (segment plans only): stop at the eligible launches' rows
+  // by seq rank (mbs, nbs); match is left to run_fused_agg
+  bool buckets = false;
   // optional second stream for the profiled side, with the events that fork
   // it from and join it back to the main stream
   hipStream_t pf_stream = nullptr;
@@ -275,11 +298,41 @@ void plan_items(const EncArgs &a, hipStream_t s);
 void reduce_items(const EncArgs &a, hipStream_t s, bool triaged = false);
 void triage_rows(const EncArgs &a, hipStream_t s);
 
+// ---- fused dedup broadcast and aggregation (fused.hip) ---------------------------
+struct FusedIn {
+  const opattr_kernels *k;
+  const opattr_ranges *r;
+  const opattr_dims *d;
+  const int32_t *range_id;  // from the enclosure
+  int32_t *match;           // out
+  const AggIn *in;
+  uint32_t absent;
+  opattr_op_row *table;
+  opattr_diag *diag;
+  void *ws;
+  const Plan *pl;
+};
+// match of every launch from the bucket path's mbs / nbs (and the dedup
+// errors)
+void run_fused_match(const FusedIn &x, hipStream_t s);
+// the operator table from match and range_id, with the summary's per-block
+// sums in sumpart (the row accumulators must be zero: clear_fused_acc)
+void run_fused_agg(const FusedIn &x, hipStream_t s);
+void clear_fused_acc(void *ws, const Plan &pl, hipStream_t s);
+int fused_sum_blocks(const Plan &pl);
+// workspace sizes of the fused aggregation
+size_t fused_parts_bytes(int64_t T);
+size_t fused_bkt_bytes(int64_t T);
+size_t fused_split_bytes(uint32_t G);
+constexpr uint32_t kFusedMaxRows = 16384;  // rows the per-bucket LDS tables hold
+
 // ---- finish (api.hip) ---------------------------------------------------------
 // status of the diag record; with a table, also the summary over its G rows
 // (rows below NOPS attributed)
+// (with prepart > 0, part already holds that many blocks' summary sums)
 void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s,
                    const opattr_op_row *table = nullptr, opattr_summary *sum = nullptr,
-                   uint32_t G = 0, uint32_t NOPS = 0, unsigned long long *part = nullptr);
+                   uint32_t G = 0, uint32_t NOPS = 0, unsigned long long *part = nullptr,
+                   int prepart = 0);
 
 }  // namespace opa

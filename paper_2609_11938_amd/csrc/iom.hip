@@ -392,20 +392,8 @@ __global__ void __launch_bounds__(256) k_part_edges(TlArgs a, uint32_t *pfirst, 
   part_edges(sm.lp, base, sm.sg.edge[0], sm.sg.edge[1], pfirst, plast, pheads);
 }
 
-// Per partition p, how its launches find their row (fast path lookup):
-//   hi == kRecEligible  p is its own class representative: its launches rank
-//                       themselves;
-//   hi == kRecNone      p has no valid representative: no row, no dedup error;
-//   otherwise           a duplicate: the launch at seq rank x takes the rank of
-//                       the launch at x + delta when x < hi (the representative
-//                       partition is shorter otherwise), else a dedup error;
-//                       hi == 0 when either partition is not one run.
-// Also raises PARTITION for every partition seen in more than one run.
-struct PartRec {
-  int32_t delta;
-  uint32_t hi;
-};
-constexpr uint32_t kRecEligible = 0xFFFFFFFFu, kRecNone = 0xFFFFFFFEu;
+// The record of every partition (PartRec, see impl.h); also raises
+// PARTITION for every partition seen in more than one run.
 
 __global__ void k_part_prep(const int32_t *__restrict__ part_rep, uint32_t NP,
                             const uint32_t *__restrict__ pfirst, const uint32_t *__restrict__ plast,
@@ -603,6 +591,110 @@ k_tl_look(TlArgs a, LookArgs m) {
   if (lane_id() == 0 && e) atomicAdd(&serr, e);
   __syncthreads();
   if (tid == 0 && serr) atomicAdd((unsigned long long *)&m.diag->dedup_errors, serr);
+}
+
+// ---------------------------------------------------------------------------
+// Bucket path (segment tiles, the fused attribution): the matching stops at
+// the eligible launches. Per seq tile, a first pass counts the eligible
+// launches of each name (the tile histogram) and writes them, in seq order,
+// to the tile's bucket as (name, position). After the column scan a second
+// pass ranks the buckets only -- a small fraction of the launches when most
+// of them are layer duplicates -- and leaves, by seq rank, each eligible
+// launch's row (mbs) and name (nbs). Every launch then finds its match in
+// the fused aggregation pass over storage order: its own entry, or, for a
+// duplicate, the entry of the representative's launch at its position.
+// ---------------------------------------------------------------------------
+struct BucketOut {
+  uint32_t *tlh;                      // [tiles][NN] eligible launches per name
+  uint32_t *rec;                      // [tiles][4096] name << 12 | position, in seq order
+  uint32_t *cnt;                      // [tiles] bucket sizes
+  uint32_t *pfirst, *plast, *pheads;  // pheads NULL: no partitions
+  opattr_diag *diag;
+};
+
+__global__ void __launch_bounds__(256) k_f_pass1(TlArgs a, BucketOut o) {
+  OPA_DYN_LDS(uint32_t, cnt);
+  __shared__ TileData sm;
+  __shared__ uint32_t sh[4];
+  const int tid = threadIdx.x;
+  const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
+  const uint32_t NN = a.NN;
+  for (uint32_t i = tid; i < NN; i += OPA_TILE_THREADS) cnt[i] = 0;
+  if (tid == 0) sm.bad = 0;
+  const uint32_t bad = seg_tile(a, tile, sm);
+  // this thread's 16 consecutive positions: counts, then the bucket in order
+  constexpr int kPos = OPA_TILE / OPA_TILE_THREADS;
+  const int e0 = tid * kPos;
+  uint32_t key[kPos];
+  uint32_t ne = 0;
+#pragma unroll
+  for (int k = 0; k < kPos; ++k) {
+    key[k] = sm.key[e0 + k];
+    if (key[k] < NN) {
+      ne++;
+      atomicAdd(&cnt[key[k]], 1u);
+    }
+  }
+  uint32_t tot;
+  uint32_t j = block_excl_scan_add<uint32_t>(ne, sh, &tot);
+  uint32_t *rec = o.rec + base;
+#pragma unroll
+  for (int k = 0; k < kPos; ++k)
+    if (key[k] < NN) rec[j++] = (key[k] << OPA_SLOT_BITS) | (uint32_t)(e0 + k);
+  if (tid == 0) o.cnt[tile] = tot;
+  __syncthreads();
+  for (uint32_t n = tid; n < NN; n += OPA_TILE_THREADS) o.tlh[tile * NN + n] = cnt[n];
+  if (o.pheads) part_edges(sm.lp, base, sm.sg.edge[0], sm.sg.edge[1], o.pfirst, o.plast, o.pheads);
+  if (bad) atomicAdd(&sm.bad, bad);
+  __syncthreads();
+  if (tid == 0 && sm.bad)
+    atomicAdd((unsigned long long *)&o.diag->bad_records, (unsigned long long)sm.bad);
+}
+
+struct RankArgs {
+  const uint32_t *rec, *cnt;  // the buckets
+  const uint32_t *tlh;        // exclusive prefix of each name down the tiles
+  const uint32_t *tlc, *pfc, *off;
+  const int32_t *slot;
+  int32_t *mbs;   // by seq rank: the row of each eligible launch (-1 none)
+  uint32_t *nbs;  // by seq rank: its name
+  uint32_t NN;
+  int skip_name;
+};
+
+// rank = (eligible launches of the name in earlier tiles) + (rank in the
+// bucket, which is in seq order); row = slot[off[name] + rank] while the
+// name has rows left (Alg. 1)
+__global__ void __launch_bounds__(256) k_f_pass2(RankArgs m) {
+  OPA_DYN_LDS(uint16_t, cnt);
+  const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
+  const uint32_t NN = m.NN;
+  const uint32_t n = m.cnt[tile];
+  if (n == 0) return;
+  for (uint32_t i = threadIdx.x; i < 4 * NN; i += OPA_TILE_THREADS) cnt[i] = 0;
+  __syncthreads();
+  uint32_t key[kWaveChunks], pos[kWaveChunks], rank[kWaveChunks];
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const int e = tile_elem(c);
+    const uint32_t r = (uint32_t)e < n ? m.rec[base + e] : (NN << OPA_SLOT_BITS);
+    key[c] = r >> OPA_SLOT_BITS;
+    pos[c] = r & (OPA_TILE - 1);
+  }
+  wave_rank<kWaveChunks>(key, NN, bits_for(NN), cnt + wave_id() * NN, rank);
+  block_rank_bases(cnt, NN, nullptr);
+  const uint16_t *wb = cnt + wave_id() * NN;
+  const uint32_t *pre = m.tlh + tile * NN;
+#pragma unroll
+  for (int c = 0; c < kWaveChunks; ++c) {
+    const uint32_t k = key[c];
+    if (k >= NN) continue;
+    const uint32_t r = pre[k] + wb[k] + rank[c];
+    uint32_t rows = m.pfc[k];
+    if (m.skip_name && m.tlc[k] != rows) rows = 0;  // the name is left out
+    m.mbs[base + pos[c]] = r < rows ? m.slot[m.off[k] + r] : -1;
+    m.nbs[base + pos[c]] = k;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1166,6 +1258,7 @@ void run_match(const IomArgs &x, hipStream_t s) {
   const bool dedup = has_dedup(k, d);
   const bool parts = dedup && x.want_dedup;
   const bool seg = pl.seg;  // implies the fast path
+  const bool buckets = seg && x.buckets;
   const bool fast = NN <= kFastNames, fast_pf = NN <= kFastKeys;
   const size_t lds = (size_t)4 * NN * sizeof(uint16_t);
   uint32_t *tlh = at<uint32_t>(ws, pl.tlh), *pfh = at<uint32_t>(ws, pl.pfh);
@@ -1224,9 +1317,19 @@ void run_match(const IomArgs &x, hipStream_t s) {
   ho.plast = plast;
   ho.pheads = parts ? pheads : nullptr;
   ho.diag = x.diag;
+  BucketOut bo;
+  bo.tlh = tlh;
+  bo.rec = at<uint32_t>(ws, pl.sv);  // the launch-order view is unused on the segment path
+  bo.cnt = at<uint32_t>(ws, pl.bcnt);
+  bo.pfirst = pfirst;
+  bo.plast = plast;
+  bo.pheads = parts ? pheads : nullptr;
+  bo.diag = x.diag;
   probe_begin(OPATTR_PROBE_TL_HIST, s);
   if (pl.nt > 0) {
-    if (seg) {
+    if (buckets) {
+      k_f_pass1<<<(unsigned)pl.nt, 256, (size_t)NN * 4, s>>>(ta, bo);
+    } else if (seg) {
       k_tl_hist_w<true><<<(unsigned)pl.nt, 256, lds, s>>>(ta, ho);
     } else if (fast) {
       k_tl_hist_w<false><<<(unsigned)pl.nt, 256, lds, s>>>(ta, ho);
@@ -1248,7 +1351,21 @@ void run_match(const IomArgs &x, hipStream_t s) {
     k_names<<<1, 1024, 0, s>>>(tlc, pfc, NN, x.name_counts, x.diag,
                                x.policy == OPATTR_MISMATCH_STRICT ? 1 : 0);
   probe_begin(OPATTR_PROBE_TL_MATCH, s);
-  if (pl.nt > 0) {
+  if (pl.nt > 0 && buckets) {
+    RankArgs m;
+    m.rec = bo.rec;
+    m.cnt = bo.cnt;
+    m.tlh = tlh;
+    m.tlc = tlc;
+    m.pfc = pfc;
+    m.off = off;
+    m.slot = at<int32_t>(ws, pl.slot);
+    m.mbs = at<int32_t>(ws, pl.mbs);
+    m.nbs = at<uint32_t>(ws, pl.nbs);
+    m.NN = NN;
+    m.skip_name = x.policy == OPATTR_MISMATCH_SKIP_NAME ? 1 : 0;
+    k_f_pass2<<<(unsigned)pl.nt, 256, lds, s>>>(m);
+  } else if (pl.nt > 0) {
     if (fast) {
       LookArgs m;
       m.tlh = tlh;
