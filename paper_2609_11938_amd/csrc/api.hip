@@ -88,7 +88,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   // (only opattr_attribute, which always has ranges, takes it: a plan
   // without ranges must stay within the size of the plan with them)
   pl.fused = pl.seg && r != nullptr && pl.G <= kFusedMaxRows && pl.R * 16 <= pl.T && pl.T > 0;
-  pl.acc = b.take(pl.fused ? (size_t)pl.G * 200 : 0);
+  pl.acc = b.take(pl.fused ? fused_acc_bytes(pl.G) : 0);
   pl.fbkt = b.take(pl.fused ? fused_bkt_bytes(pl.T) : 0);
   pl.fsplit = b.take(pl.fused ? fused_split_bytes(pl.G) : 0);
   const bool rs = !pl.ranges_nested;

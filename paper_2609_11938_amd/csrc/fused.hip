@@ -7,7 +7,7 @@
 //    takes the entry of the representative's launch at the same position
 //    (the partition record gives the seq offset) when the names agree (else
 //    -1 and a dedup error).
-// 2. k_f_agg: each lane takes sixteen consecutive launches and adds their
+// 2. k_f_agg: each lane takes eight consecutive launches and adds their
 //    durations and counter rows (m or m * d, or the fp32 maximum as an
 //    order-preserving key) into a register accumulator. Consecutive launches
 //    of one operator row form a run: a run that ends inside a lane is staged
@@ -18,8 +18,9 @@
 //    to a row accumulator with device-scope atomics.
 // 3. k_f_comb: one wave per (bucket, share of the blocks) adds the bucket's
 //    partial results of those blocks in LDS and writes one partial per row.
-// 4. k_f_rows: every table row from its shares and its accumulator
-//    (DW-mean = sum / matched ns, NaN rules), and the summary's block sums.
+// 4. k_f_rows: one block per bucket adds every share and the row
+//    accumulators and writes the bucket's table rows (DW-mean = sum /
+//    matched ns, NaN rules) and summary sums.
 // Integer fields are exact in any order; fp64 sums are added in an order
 // that depends on scheduling (well inside the 1e-9 tolerance); maxima are
 // exact.
@@ -30,18 +31,19 @@
 namespace opa {
 
 constexpr int kMPer = 8;                       // launches per thread (matching)
-constexpr int kAPer = 16;                      // launches per lane (aggregation)
+constexpr int kAPer = 8;                      // launches per lane (aggregation)
 constexpr int kAHalf = 8;                      // of them in registers at a time
 constexpr int kAThreads = 256;                 // threads per block
 constexpr int kASpan = kAPer * kAThreads;      // launches per block
-constexpr int kASlots = 48;                    // partial results a wave keeps
+constexpr int kASlots = 32;                    // partial results a wave keeps
 constexpr int kABlockCap = kASlots * (kAThreads / OPA_WAVE);  // and a block
 constexpr int kFFields = 25;                   // kc, tns, mc, mns, 20 counters, NaN bits
 constexpr int kBuckets = 256;                  // buckets of operator rows
 constexpr int kSplits = 16;                    // shares of the blocks per bucket
 constexpr uint32_t kNoSrc = 0xFFFFFFFFu;
+constexpr uint32_t kHash = 256;                // LDS table of a block's rows (> 2 x kept)
 
-static_assert(kAPer == 2 * kAHalf, "two halves per lane");
+
 static_assert(kABlockCap <= 255, "bucket offsets fit in a byte");
 
 // kN consecutive 32-bit elements from p[i..), 16-byte vector loads when aligned
@@ -255,6 +257,7 @@ k_f_agg(AggParams a) {
   __shared__ Slot slots[kAThreads / OPA_WAVE][kASlots];
   __shared__ int nslot[kAThreads / OPA_WAVE];
   __shared__ uint32_t hist[kBuckets], spos[kABlockCap];
+  __shared__ uint32_t hkey[kHash], hown[kHash];
   __shared__ uint32_t sh[4];
   const int tid = threadIdx.x, ln = lane_id(), w = wave_id();
   const AggIn &in = a.in;
@@ -273,7 +276,7 @@ k_f_agg(AggParams a) {
   if (ln > 0 && nv > 0) gprev = row_of(a, a.range_id[ib - 1]);
   uint32_t gcur = 0xFFFFFFFFu;
 #pragma unroll 1
-  for (int h = 0; h < 2; ++h) {
+  for (int h = 0; h < kAPer / kAHalf; ++h) {
     const int64_t i0 = ib + h * kAHalf;
     const int nh = nv - h * kAHalf < 0 ? 0 : (nv - h * kAHalf < kAHalf ? nv - h * kAHalf : kAHalf);
     int32_t mt[kAHalf], rid[kAHalf];
@@ -281,18 +284,6 @@ k_f_agg(AggParams a) {
     load_n<kAHalf>(a.match, i0, nh, mt);
     load_n<kAHalf>(in.dur, i0, nh, du);
     load_n<kAHalf>(a.range_id, i0, nh, rid);
-    // the counter rows of these launches are touched first (two words per
-    // row), so that the accumulation below finds them in cache instead of
-    // waiting for one row after another
-    uint32_t touch = 0;
-#pragma unroll
-    for (int k = 0; k < kAHalf; ++k)
-      if (k < nh && mt[k] >= 0 && (int64_t)mt[k] < in.P) {
-        const float *row = in.counters + (int64_t)mt[k] * in.rs;
-        touch ^= __float_as_uint(row[0]) ^
-                 __float_as_uint(row[(int64_t)(OPATTR_NUM_COUNTERS - 1) * in.cs]);
-      }
-    if (touch == 0x9E3779B9u && a.T < 0) a.bkt[0] = 0;  // never true: keeps the loads
 #pragma unroll
     for (int k = 0; k < kAHalf; ++k) g[k] = k < nh ? row_of(a, rid[k]) : 0xFFFFFFFFu;
 #pragma unroll
@@ -351,18 +342,58 @@ k_f_agg(AggParams a) {
             mx);
   if (ln == 0) nslot[w] = nst;
   for (int q = tid; q < kBuckets; q += kAThreads) hist[q] = 0;
+  for (int q = tid; q < kHash; q += kAThreads) {
+    hkey[q] = 0u;
+    hown[q] = 0xFFFFFFFFu;
+  }
   __syncthreads();
 
-  // the block's kept partials, counted by bucket, then written in bucket
-  // order
-  uint32_t bq = 0xFFFFFFFFu, rk = 0;
+  // the block's kept partials of one row are added into the first of them
+  // (a busy row, such as the unattributed one, would otherwise reach the
+  // combine once per run), then counted by bucket and written in bucket order
+  // (an open-addressing table of rows in LDS: the lowest slot of a row owns it)
+  bool own = false;
+  int hs = -1;
+  const Slot *qs = nullptr;
   if (tid < kABlockCap) {
     const int sw = tid / kASlots, sj = tid % kASlots;
-    const Slot *q = &slots[sw][sj];
-    if (sj < nslot[sw] && q->live) {
-      bq = q->g / a.rb;
-      rk = atomicAdd(&hist[bq], 1u);
+    qs = &slots[sw][sj];
+    if (sj < nslot[sw] && qs->live) {
+      const uint32_t key = qs->g + 1u;
+      uint32_t h = (qs->g * 2654435761u) >> 24;
+      for (;;) {
+        const uint32_t old = atomicCAS(&hkey[h], 0u, key);
+        if (old == 0u || old == key) break;
+        h = (h + 1u) & (kHash - 1u);
+      }
+      atomicMin(&hown[h], (uint32_t)tid);
+      hs = (int)h;
     }
+  }
+  __syncthreads();
+  if (hs >= 0) {
+    const uint32_t first = hown[hs];
+    own = first == (uint32_t)tid;
+    if (!own) {
+      Slot *o = &slots[first / kASlots][first % kASlots];
+      atomicAdd(&o->f[0], qs->f[0]);
+      atomicAdd(&o->f[1], qs->f[1]);
+      atomicAdd(&o->f[2], qs->f[2]);
+      atomicAdd(&o->f[3], qs->f[3]);
+#pragma unroll
+      for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
+        if ((mx >> c) & 1u) atomicMax(&o->f[4 + c], qs->f[4 + c]);
+        else unsafeAtomicAdd(reinterpret_cast<double *>(&o->f[4 + c]), bits2d(qs->f[4 + c]));
+      }
+      if ((uint32_t)qs->f[24])
+        atomicOr(reinterpret_cast<unsigned int *>(&o->f[24]), (uint32_t)qs->f[24]);
+    }
+  }
+  __syncthreads();
+  uint32_t bq = 0xFFFFFFFFu, rk = 0;
+  if (own) {
+    bq = slots[tid / kASlots][tid % kASlots].g / a.rb;
+    rk = atomicAdd(&hist[bq], 1u);
   }
   __syncthreads();
   uint32_t cnt = 0, tot;
@@ -393,125 +424,162 @@ k_f_agg(AggParams a) {
 // ---------------------------------------------------------------------------
 struct CombParams {
   int64_t nblocks;
-  uint32_t rb;
+  uint32_t rb, G, NOPS;
+  uint32_t mx, dw, absent;
   const PartRow *parts;
   const uint16_t *bkt;
-  PartRow *split;  // [kBuckets][kSplits][rb]
+  PartRow *split;              // [kBuckets][kSplits][rb]
+  const PartRow *acc;          // [G] row accumulators (the blocks' overflow)
+  opattr_op_row *table;
+  unsigned long long *part;    // [kBuckets][4] summary sums per bucket
 };
 
+__device__ __forceinline__ unsigned long long merge_field(int f, unsigned long long x,
+                                                          unsigned long long y, uint32_t mx) {
+  if (f < 4) return x + y;
+  if (f < 24) return ((mx >> (f - 4)) & 1u) ? (x > y ? x : y) : d2bits(bits2d(x) + bits2d(y));
+  return x | y;
+}
+
+// t (an LDS row) += the partial v
+__device__ __forceinline__ void tab_add(unsigned long long *t,
+                                        const unsigned long long (&v)[kFFields], uint32_t mx) {
+  atomicAdd(t + 0, v[0]);
+  atomicAdd(t + 1, v[1]);
+  if (v[2] == 0) return;  // no matched launch: counter fields are zero
+  atomicAdd(t + 2, v[2]);
+  atomicAdd(t + 3, v[3]);
+#pragma unroll
+  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
+    if ((mx >> c) & 1u) atomicMax(t + 4 + c, v[4 + c]);
+    else unsafeAtomicAdd(reinterpret_cast<double *>(t + 4 + c), bits2d(v[4 + c]));
+  }
+  if ((uint32_t)v[24]) atomicOr(reinterpret_cast<unsigned int *>(t + 24), (uint32_t)v[24]);
+}
+
 // Each lane takes its own blocks (a contiguous share of them per wave) and
-// adds their partials of the bucket one after another, so that the loads of
-// all lanes are in flight together; rows accumulate in LDS.
+// their partials of the bucket one after another, the next one's loads in
+// flight while the current one is added; consecutive partials of one row are
+// added in registers (a busy row would serialise the LDS atomics of the
+// wave), rows accumulate in LDS.
 template <bool DEF>
-__global__ void __launch_bounds__(64) k_f_comb(CombParams a, uint32_t maxmask) {
+__global__ void __launch_bounds__(64) k_f_comb(CombParams a) {
   extern __shared__ __align__(16) unsigned char comb_raw[];
   unsigned long long *tab = reinterpret_cast<unsigned long long *>(comb_raw);  // [rb][kFFields]
-  const uint32_t mx = DEF ? kDefMaxMask : maxmask;
+  const uint32_t mx = DEF ? kDefMaxMask : a.mx;
   const int ln = lane_id();
   const uint32_t q = blockIdx.x / kSplits, s = blockIdx.x % kSplits;
-  const uint32_t rb = a.rb;
-  for (uint32_t x = ln; x < rb * kFFields; x += OPA_WAVE) tab[x] = 0;
+  const uint32_t rb = a.rb, ne = rb * kFFields;
+  for (uint32_t x = ln; x < ne; x += OPA_WAVE) tab[x] = 0;
   wave_sync_lds();
   const int64_t per = (a.nblocks + kSplits - 1) / kSplits;
   const int64_t b_lo = (int64_t)s * per, b_hi = b_lo + per < a.nblocks ? b_lo + per : a.nblocks;
-  for (int64_t b0 = b_lo; b0 < b_hi; b0 += 4 * OPA_WAVE) {
-    // this lane's blocks of the round (their bucket entries loaded together)
-    uint32_t e[4];
+  unsigned long long racc[kFFields];
+  uint32_t rg = 0xFFFFFFFFu;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t b = b0 + j * OPA_WAVE + ln;
-      e[j] = b < b_hi ? a.bkt[b * kBuckets + q] : 0u;
-    }
+  for (int f = 0; f < kFFields; ++f) racc[f] = 0;
+  for (int64_t b = b_lo + ln; b < b_hi; b += OPA_WAVE) {
+    const uint32_t e = a.bkt[b * kBuckets + q];
+    const uint32_t c = e & 0xFFu, o = e >> 8;
+    const unsigned long long *pr =
+        reinterpret_cast<const unsigned long long *>(a.parts + b * kABlockCap + o);
 #pragma unroll 1
-    for (int j = 0; j < 4; ++j) {
-      const int64_t b = b0 + j * OPA_WAVE + ln;
-      const uint32_t c = e[j] & 0xFFu, o = e[j] >> 8;
-      const unsigned long long *pr =
-          reinterpret_cast<const unsigned long long *>(a.parts + b * kABlockCap + o);
-#pragma unroll 1
-      for (uint32_t p = 0; p < c; ++p, pr += sizeof(PartRow) / 8) {
-        unsigned long long v[kFFields];
+    for (uint32_t p = 0; p < c; ++p, pr += sizeof(PartRow) / 8) {
+      unsigned long long v[kFFields];
 #pragma unroll
-        for (int f = 0; f < kFFields; ++f) v[f] = pr[f];
-        unsigned long long *t = tab + (size_t)((uint32_t)(v[24] >> 32) % rb) * kFFields;
-        atomicAdd(t + 0, v[0]);
-        atomicAdd(t + 1, v[1]);
-        if (v[2] == 0) continue;  // no matched launch: counter fields are zero
-        atomicAdd(t + 2, v[2]);
-        atomicAdd(t + 3, v[3]);
+      for (int f = 0; f < kFFields; ++f) v[f] = pr[f];
+      const uint32_t g = (uint32_t)(v[24] >> 32);
+      v[24] &= 0xFFFFFFFFull;
+      if (g != rg) {
+        if (rg != 0xFFFFFFFFu) tab_add(tab + (size_t)(rg % rb) * kFFields, racc, mx);
+        rg = g;
 #pragma unroll
-        for (int c2 = 0; c2 < OPATTR_NUM_COUNTERS; ++c2) {
-          if ((mx >> c2) & 1u) atomicMax(t + 4 + c2, v[4 + c2]);
-          else unsafeAtomicAdd(reinterpret_cast<double *>(t + 4 + c2), bits2d(v[4 + c2]));
-        }
-        if ((uint32_t)v[24]) atomicOr(reinterpret_cast<unsigned int *>(t + 24), (uint32_t)v[24]);
+        for (int f = 0; f < kFFields; ++f) racc[f] = v[f];
+      } else {
+#pragma unroll
+        for (int f = 0; f < kFFields; ++f) racc[f] = merge_field(f, racc[f], v[f], mx);
       }
     }
   }
+  if (rg != 0xFFFFFFFFu) tab_add(tab + (size_t)(rg % rb) * kFFields, racc, mx);
   wave_sync_lds();
   unsigned long long *out =
       reinterpret_cast<unsigned long long *>(a.split + ((size_t)q * kSplits + s) * rb);
-  for (uint32_t x = ln; x < rb * kFFields; x += OPA_WAVE) {
-    const uint32_t r = x / kFFields, ff = x % kFFields;
-    out[r * (sizeof(PartRow) / 8) + ff] = tab[x];
+  for (uint32_t x = ln; x < ne; x += OPA_WAVE) {
+    const uint32_t rr = x / kFFields, ff = x % kFFields;
+    out[rr * (sizeof(PartRow) / 8) + ff] = tab[x];
   }
 }
 
 // ---------------------------------------------------------------------------
-// 4. table rows and the summary's block sums (attributed, unattributed,
-// total, matched ns)
+// 4. per bucket (one block): the row accumulators plus every share, then the
+// bucket's table rows (DW-mean = sum / matched ns, NaN rules) and its summary
+// sums (attributed, unattributed, total, matched ns)
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) k_f_rows(const PartRow *__restrict__ acc,
-                                                const PartRow *__restrict__ split, uint32_t rb,
-                                                uint32_t G, uint32_t NOPS, uint32_t mx,
-                                                uint32_t dw, uint32_t absent,
-                                                opattr_op_row *table, unsigned long long *part) {
+template <bool DEF>
+__global__ void __launch_bounds__(256) k_f_rows(CombParams a) {
+  extern __shared__ __align__(16) unsigned char rows_raw[];
+  unsigned long long *tab = reinterpret_cast<unsigned long long *>(rows_raw);  // [rb][kFFields]
   __shared__ unsigned long long red[4][4];
+  const uint32_t mx = DEF ? kDefMaxMask : a.mx, dw = DEF ? kDefDwMask : a.dw;
+  const int tid = threadIdx.x, ln = lane_id();
+  const uint32_t q = blockIdx.x, rb = a.rb, ne = rb * kFFields;
+  // element x = row * 25 + field: its accumulator and all its shares at once
+  for (uint32_t x = tid; x < ne; x += blockDim.x) {
+    const uint32_t rr = x / kFFields, ff = x % kFFields;
+    const uint32_t g = q * rb + rr;
+    const unsigned long long *sp =
+        reinterpret_cast<const unsigned long long *>(a.split + (size_t)q * kSplits * rb) +
+        (size_t)rr * (sizeof(PartRow) / 8) + ff;
+    unsigned long long y[kSplits + 1];
+    y[kSplits] = g < a.G ? reinterpret_cast<const unsigned long long *>(a.acc + g)[ff] : 0ull;
+#pragma unroll
+    for (int k = 0; k < kSplits; ++k) y[k] = sp[(size_t)k * rb * (sizeof(PartRow) / 8)];
+    unsigned long long v = y[kSplits];
+#pragma unroll
+    for (int k = 0; k < kSplits; ++k) v = merge_field((int)ff, v, y[k], mx);
+    tab[x] = v;
+  }
+  __syncthreads();
   unsigned long long at_ = 0, un = 0, tot = 0, mt = 0;
-  for (uint32_t g = blockIdx.x * blockDim.x + threadIdx.x; g < G; g += gridDim.x * blockDim.x) {
-    Acc x;
-    acc_load(x, acc + g);
-    const uint32_t q = g / rb, r = g % rb;
-#pragma unroll 1
-    for (int s = 0; s < kSplits; ++s) {
-      Acc y;
-      acc_load(y, split + ((size_t)q * kSplits + s) * rb + r);
-      acc_merge(x, y, mx);
-    }
-    opattr_op_row *row = table + g;
-    row->kernel_count = x.kc;
-    row->total_ns = x.tns;
-    row->matched_count = x.mc;
-    row->matched_ns = x.mns;
+  for (uint32_t rr = tid; rr < rb; rr += blockDim.x) {
+    const uint32_t g = q * rb + rr;
+    if (g >= a.G) break;
+    const unsigned long long *f = tab + (size_t)rr * kFFields;
+    opattr_op_row *row = a.table + g;
+    const unsigned long long kc = f[0], tns = f[1], mc = f[2], mns = f[3];
+    const uint32_t nan = (uint32_t)f[24];
+    row->kernel_count = kc;
+    row->total_ns = tns;
+    row->matched_count = mc;
+    row->matched_ns = mns;
     const double qnan = __longlong_as_double(0x7FF8000000000000ll);
 #pragma unroll
     for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
       double v;
-      if (((absent >> c) & 1u) || x.mc == 0) v = qnan;
-      else if ((mx >> c) & 1u) v = ((x.nan >> c) & 1u) ? qnan : (double)key2f((uint32_t)x.v[c]);
-      else if ((dw >> c) & 1u) v = x.mns ? bits2d(x.v[c]) / (double)x.mns : qnan;
-      else v = bits2d(x.v[c]);
+      if (((a.absent >> c) & 1u) || mc == 0) v = qnan;
+      else if ((mx >> c) & 1u) v = ((nan >> c) & 1u) ? qnan : (double)key2f((uint32_t)f[4 + c]);
+      else if ((dw >> c) & 1u) v = mns ? bits2d(f[4 + c]) / (double)mns : qnan;
+      else v = bits2d(f[4 + c]);
       row->value[c] = v;
     }
-    tot += x.tns;
-    mt += x.mns;
-    if (g < NOPS) at_ += x.tns;
-    else un += x.tns;
+    tot += tns;
+    mt += mns;
+    if (g < a.NOPS) at_ += tns;
+    else un += tns;
   }
   at_ = wave_reduce_add(at_);
   un = wave_reduce_add(un);
   tot = wave_reduce_add(tot);
   mt = wave_reduce_add(mt);
-  if (lane_id() == 0) {
+  if (ln == 0) {
     red[0][wave_id()] = at_;
     red[1][wave_id()] = un;
     red[2][wave_id()] = tot;
     red[3][wave_id()] = mt;
   }
   __syncthreads();
-  if (threadIdx.x < 4)
-    part[blockIdx.x * 4 + threadIdx.x] =
-        red[threadIdx.x][0] + red[threadIdx.x][1] + red[threadIdx.x][2] + red[threadIdx.x][3];
+  if (tid < 4) a.part[q * 4 + tid] = red[tid][0] + red[tid][1] + red[tid][2] + red[tid][3];
 }
 
 // ---------------------------------------------------------------------------
@@ -531,14 +599,14 @@ size_t fused_split_bytes(uint32_t G) {
   return (size_t)kBuckets * kSplits * fused_rows_per_bucket(G) * sizeof(PartRow);
 }
 
-int fused_sum_blocks(const Plan &pl) {
-  const int64_t want = ((int64_t)pl.G + 255) / 256;
-  return (int)(want < kSumBlocks ? (want > 0 ? want : 1) : kSumBlocks);
-}
+int fused_sum_blocks(const Plan &) { return kBuckets; }
 
+// the row accumulators
 void clear_fused_acc(void *ws, const Plan &pl, hipStream_t s) {
   fill_u32(at<uint32_t>(ws, pl.acc), 0u, (int64_t)pl.G * (sizeof(PartRow) / 4), s);
 }
+
+size_t fused_acc_bytes(uint32_t G) { return (size_t)G * sizeof(PartRow); }
 
 void run_fused_match(const FusedIn &x, hipStream_t s) {
   const Plan &pl = *x.pl;
@@ -589,15 +657,25 @@ void run_fused_agg(const FusedIn &x, hipStream_t s) {
   CombParams c{};
   c.nblocks = nb;
   c.rb = rb;
+  c.G = pl.G;
+  c.NOPS = x.d->n_ops;
+  c.mx = a.in.maxmask;
+  c.dw = a.in.dwmask;
+  c.absent = x.absent;
   c.parts = a.parts;
   c.bkt = a.bkt;
   c.split = at<PartRow>(x.ws, pl.fsplit);
+  c.acc = a.acc;
+  c.table = x.table;
+  c.part = at<unsigned long long>(x.ws, pl.sumpart);
   const size_t lds = (size_t)rb * kFFields * 8;
-  if (def) k_f_comb<true><<<kBuckets * kSplits, 64, lds, s>>>(c, a.in.maxmask);
-  else k_f_comb<false><<<kBuckets * kSplits, 64, lds, s>>>(c, a.in.maxmask);
-  k_f_rows<<<fused_sum_blocks(pl), 256, 0, s>>>(a.acc, c.split, rb, pl.G, x.d->n_ops, a.in.maxmask,
-                                                 a.in.dwmask, x.absent, x.table,
-                                                 at<unsigned long long>(x.ws, pl.sumpart));
+  if (def) {
+    k_f_comb<true><<<kBuckets * kSplits, 64, lds, s>>>(c);
+    k_f_rows<true><<<kBuckets, 256, lds, s>>>(c);
+  } else {
+    k_f_comb<false><<<kBuckets * kSplits, 64, lds, s>>>(c);
+    k_f_rows<false><<<kBuckets, 256, lds, s>>>(c);
+  }
   probe_end(OPATTR_PROBE_AGGREGATE, s);
 }
 

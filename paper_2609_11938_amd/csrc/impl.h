@@ -324,6 +324,7 @@ int fused_sum_blocks(const Plan &pl);
 size_t fused_parts_bytes(int64_t T);
 size_t fused_bkt_bytes(int64_t T);
 size_t fused_split_bytes(uint32_t G);
+size_t fused_acc_bytes(uint32_t G);
 constexpr uint32_t kFusedMaxRows = 16384;  // rows the per-bucket LDS tables hold
 
 // ---- finish (api.hip) ---------------------------------------------------------
