@@ -192,6 +192,8 @@ typedef struct {
 #define OPATTR_ERR_ORDER (-8)       /* diag */
 #define OPATTR_ERR_DATA (-9)        /* diag */
 #define OPATTR_ERR_LIMIT (-10)      /* diag */
+#define OPATTR_ERR_SCRATCH (-11)    /* host: opattr_attribute_noalloc needs more than
+                                       OPATTR_NOALLOC_SCRATCH_BYTES            */
 
 /* Device-resident error record. status is the highest-precedence flagged class
    in the order DATA, ORDER, LIMIT, NOT_NESTED, PARTITION, DEDUP, COUNT (COUNT
@@ -415,6 +417,26 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
                      int32_t *range_id, uint8_t *range_depth, uint32_t *name_counts,
                      opattr_op_row *table, opattr_summary *sum, opattr_diag *diag, void *ws,
                      size_t ws_bytes, void *stream);
+
+/* opattr_attribute for callers that cannot allocate device memory (code
+   under stream capture, serving loops, harnesses that forbid hipMalloc): no
+   workspace argument; the call uses a scratch array that the library holds
+   on each device it runs on (OPATTR_NOALLOC_SCRATCH_BYTES, kept until the
+   process ends, set up on the first call on that device) and runs every
+   stage on `stream` alone (no side streams). Same arguments, outputs and
+   diag as opattr_attribute. Returns OPATTR_ERR_SCRATCH, enqueueing nothing,
+   when opattr_workspace_bytes(k, p, r, d) exceeds the scratch, and
+   OPATTR_ERR_HIP when the scratch's address cannot be had. Every call on a
+   device shares that device's scratch: calls that may overlap on one device
+   (other streams, other host threads) race and must be ordered by the
+   caller. No entry point allocates or frees; this one also creates no
+   streams or events. */
+#define OPATTR_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int opattr_attribute_noalloc(const opattr_kernels *k, const opattr_profiled *p,
+                             const opattr_ranges *r, const opattr_dims *d, int policy,
+                             const uint8_t *agg_kind, int32_t *match, int32_t *range_id,
+                             uint8_t *range_depth, uint32_t *name_counts, opattr_op_row *table,
+                             opattr_summary *sum, opattr_diag *diag, void *stream);
 
 /* Probe events (diagnostics, per host thread). events is a host array of
    2*n hipEvent_t values; while set, every later call on this thread records

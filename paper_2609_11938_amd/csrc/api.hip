@@ -2,6 +2,8 @@
 // sequencing on the caller's stream.
 #include <string.h>
 
+#include <mutex>
+
 #include "accum.h"
 #include "common.h"
 #include "impl.h"
@@ -383,6 +385,26 @@ static SideStream *side_stream() {
   return &ss;
 }
 
+// Library-held workspace of opattr_attribute_noalloc: every device that
+// runs it holds its own copy until the process ends. In host code the
+// array's name stands for no device address: scratch_ptr() gives this
+// device's copy, taken once per device with that device current.
+static __device__ __align__(256) uint8_t scratch[OPATTR_NOALLOC_SCRATCH_BYTES];
+static void *g_scratch[kMaxDevices];
+static std::mutex g_scratch_mu;
+
+static void *scratch_ptr() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void *ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_scratch[dev] = ptr;
+  }
+  return g_scratch[dev];
+}
+
 static int launch_status() {
   const hipError_t launch = hipGetLastError();
   const hipError_t first = g_hip_error;
@@ -574,8 +596,8 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
                            const uint8_t *agg_kind, int32_t *match, int32_t *range_id,
                            uint8_t *range_depth, uint32_t *name_counts, opattr_op_row *table,
                            opattr_summary *sum, opattr_diag *diag, void *ws, const Plan &pl,
-                           hipStream_t s) {
-  SideStream *ss = side_stream();
+                           hipStream_t s, bool fork) {
+  SideStream *ss = fork ? side_stream() : nullptr;
   const hipStream_t s2 = ss ? ss->s : s;
   if (ss) {
     note(hipEventRecord(ss->fork, s));
@@ -631,26 +653,32 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
   return launch_status();
 }
 
-int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const opattr_ranges *r,
-                     const opattr_dims *d, int policy, const uint8_t *agg_kind, int32_t *match,
-                     int32_t *range_id, uint8_t *range_depth, uint32_t *name_counts,
-                     opattr_op_row *table, opattr_summary *sum, opattr_diag *diag, void *ws,
-                     size_t ws_bytes, void *stream) {
-  if (!check_dims(d) || !check_kernels(k, true, true, true) || !check_profiled(p, true, true) ||
-      !check_ranges(r) || !diag || !table || !sum || policy < 0 || policy > 2 ||
-      !kinds_ok(agg_kind) || (k->n > 0 && (!match || !range_id)))
-    return OPATTR_ERR_INVALID_ARG;
-  const Plan pl = make_plan(k, p, r, d);
-  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
-  hipStream_t s = (hipStream_t)stream;
+static bool attribute_args_ok(const opattr_kernels *k, const opattr_profiled *p,
+                              const opattr_ranges *r, const opattr_dims *d, int policy,
+                              const uint8_t *agg_kind, int32_t *match, int32_t *range_id,
+                              opattr_op_row *table, opattr_summary *sum, opattr_diag *diag) {
+  return check_dims(d) && check_kernels(k, true, true, true) && check_profiled(p, true, true) &&
+         check_ranges(r) && diag && table && sum && policy >= 0 && policy <= 2 &&
+         kinds_ok(agg_kind) && (k->n == 0 || (match && range_id));
+}
+
+// The four stages on a checked plan and workspace; with fork, independent
+// stages run on this thread's side streams, else all on the caller's stream.
+static int attribute_call(const opattr_kernels *k, const opattr_profiled *p,
+                          const opattr_ranges *r, const opattr_dims *d, int policy,
+                          const uint8_t *agg_kind, int32_t *match, int32_t *range_id,
+                          uint8_t *range_depth, uint32_t *name_counts, opattr_op_row *table,
+                          opattr_summary *sum, opattr_diag *diag, void *ws, const Plan &pl,
+                          hipStream_t s, bool fork) {
   check_kernel_layout(k, d, diag, s);
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
   if (pl.fused) return attribute_fused(k, p, r, d, policy, agg_kind, match, range_id,
-                                       range_depth, name_counts, table, sum, diag, ws, pl, s);
+                                       range_depth, name_counts, table, sum, diag, ws, pl, s,
+                                       fork);
   // the ranges, the enclosure and the aggregation plan do not depend on the
   // matching: they run on a side stream of this device, joined back before
   // the run reduction (counts) and the per-row reduction (items)
-  SideStream *ss = side_stream();
+  SideStream *ss = fork ? side_stream() : nullptr;
   const hipStream_t s2 = ss ? ss->s : s;
   if (ss) {
     note(hipEventRecord(ss->fork, s));
@@ -696,6 +724,34 @@ int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const op
   launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s, table, sum, pl.G, d->n_ops,
                 at<unsigned long long>(ws, pl.sumpart));
   return launch_status();
+}
+
+int opattr_attribute(const opattr_kernels *k, const opattr_profiled *p, const opattr_ranges *r,
+                     const opattr_dims *d, int policy, const uint8_t *agg_kind, int32_t *match,
+                     int32_t *range_id, uint8_t *range_depth, uint32_t *name_counts,
+                     opattr_op_row *table, opattr_summary *sum, opattr_diag *diag, void *ws,
+                     size_t ws_bytes, void *stream) {
+  if (!attribute_args_ok(k, p, r, d, policy, agg_kind, match, range_id, table, sum, diag))
+    return OPATTR_ERR_INVALID_ARG;
+  const Plan pl = make_plan(k, p, r, d);
+  if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
+  return attribute_call(k, p, r, d, policy, agg_kind, match, range_id, range_depth, name_counts,
+                        table, sum, diag, ws, pl, (hipStream_t)stream, true);
+}
+
+int opattr_attribute_noalloc(const opattr_kernels *k, const opattr_profiled *p,
+                             const opattr_ranges *r, const opattr_dims *d, int policy,
+                             const uint8_t *agg_kind, int32_t *match, int32_t *range_id,
+                             uint8_t *range_depth, uint32_t *name_counts, opattr_op_row *table,
+                             opattr_summary *sum, opattr_diag *diag, void *stream) {
+  if (!attribute_args_ok(k, p, r, d, policy, agg_kind, match, range_id, table, sum, diag))
+    return OPATTR_ERR_INVALID_ARG;
+  const Plan pl = make_plan(k, p, r, d);
+  if (pl.total > OPATTR_NOALLOC_SCRATCH_BYTES) return OPATTR_ERR_SCRATCH;
+  void *ws = scratch_ptr();
+  if (!ws) return OPATTR_ERR_HIP;
+  return attribute_call(k, p, r, d, policy, agg_kind, match, range_id, range_depth, name_counts,
+                        table, sum, diag, ws, pl, (hipStream_t)stream, false);
 }
 
 // the matching's view of a tiers call: the correlation entries as profiled
@@ -1009,6 +1065,7 @@ const char *opattr_strerror(int status) {
     case OPATTR_ERR_ORDER: return "launch order violated (duplicate seq or false layout promise)";
     case OPATTR_ERR_DATA: return "id out of range or malformed range";
     case OPATTR_ERR_LIMIT: return "range nesting deeper than 255";
+    case OPATTR_ERR_SCRATCH: return "the call needs more than the library's scratch";
     default: return "unknown status";
   }
 }

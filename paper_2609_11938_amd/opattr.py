@@ -88,8 +88,9 @@ EXPORTS = ("opattr_workspace_bytes", "opattr_diag_clear", "opattr_read_diag", "o
            "opattr_dedup_broadcast", "opattr_dedup_classes", "opattr_tiers_workspace_bytes",
            "opattr_tiers", "opattr_aggregate_ops", "opattr_dispatch_workspace_bytes",
            "opattr_aggregate_dispatch", "opattr_enclose_all",
-           "opattr_attribute_tiered_workspace_bytes", "opattr_attribute_tiered", "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate",
-           "opattr_attribute", "opattr_set_probe_events", "opattr_set_class_key_bits",
+           "opattr_attribute_tiered_workspace_bytes", "opattr_attribute_tiered", "opattr_enclose",
+           "opattr_enclose_walk", "opattr_aggregate", "opattr_attribute",
+           "opattr_attribute_noalloc", "opattr_set_probe_events", "opattr_set_class_key_bits",
            "opattr_strerror")
 PROBES = ("seq_view", "tl_hist", "pf_hist", "col_scan", "pf_slot", "tl_match", "dedup",
           "ranges", "main_pass", "finalize", "aggregate", "agg_runs", "item_sort")
@@ -127,8 +128,12 @@ def library(path: str | None = None):
                                    P(opattr_ranges), P(opattr_dims), vp, vp, vp, vp, vp, sz, vp]
     L.opattr_attribute.argtypes = [P(opattr_kernels), P(opattr_profiled), P(opattr_ranges),
                                    P(opattr_dims), i, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.opattr_attribute_noalloc.argtypes = [P(opattr_kernels), P(opattr_profiled),
+                                           P(opattr_ranges), P(opattr_dims), i, vp, vp, vp, vp,
+                                           vp, vp, vp, vp, vp]
     for f in ("opattr_diag_clear", "opattr_read_diag", "opattr_match", "opattr_dedup_broadcast",
-              "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate", "opattr_attribute"):
+              "opattr_enclose", "opattr_enclose_walk", "opattr_aggregate", "opattr_attribute",
+              "opattr_attribute_noalloc"):
         getattr(L, f).restype = C.c_int
     L.opattr_tiers_workspace_bytes.argtypes = [P(opattr_kernels), P(opattr_corr_map),
                                                P(opattr_ranges), P(opattr_dims)]
@@ -321,25 +326,37 @@ class Outputs(dict):
                 for f in SUMMARY_DTYPE.names}
 
 
+def _attribute_outputs(dt: dict, m: _Marshal, want_depth: bool, want_name_counts: bool):
+    import torch
+
+    dev = dt["counters"].device
+    return Outputs(
+        match=torch.empty(m.T, dtype=torch.int32, device=dev),
+        range_id=torch.empty(m.T, dtype=torch.int32, device=dev),
+        range_depth=torch.empty(m.R, dtype=torch.uint8, device=dev) if want_depth else None,
+        name_counts=torch.empty((dt["n_names"], 2), dtype=torch.int32, device=dev)
+        if want_name_counts else None,
+        table=torch.empty((dt["n_ops"] + 1) * 192, dtype=torch.uint8, device=dev),
+        summary=torch.empty(40, dtype=torch.uint8, device=dev),
+    )
+
+
+def _raise_strict(outputs: Outputs, stream):
+    d = read_diag(outputs["diag"], stream)
+    if d["status"] == -4:
+        raise InvocationCountMismatchError(
+            f"{d['names_mismatched']} kernel names have different launch and profiled counts")
+
+
 def opattr_attribute(dt: dict, policy=MISMATCH_PREFIX, agg_kind=None, flags=0, absent_mask=0,
                      want_depth=True, want_name_counts=True, ws: Workspace | None = None,
                      stream=None, outputs: Outputs | None = None, raise_strict=True) -> Outputs:
     """All four stages in one call (see opattr_attribute in include/opattr.h)."""
-    import torch
-
     L = library()
     m = _Marshal(dt, flags, absent_mask)
     dev = dt["counters"].device
     if outputs is None:
-        outputs = Outputs(
-            match=torch.empty(m.T, dtype=torch.int32, device=dev),
-            range_id=torch.empty(m.T, dtype=torch.int32, device=dev),
-            range_depth=torch.empty(m.R, dtype=torch.uint8, device=dev) if want_depth else None,
-            name_counts=torch.empty((dt["n_names"], 2), dtype=torch.int32, device=dev)
-            if want_name_counts else None,
-            table=torch.empty((dt["n_ops"] + 1) * 192, dtype=torch.uint8, device=dev),
-            summary=torch.empty(40, dtype=torch.uint8, device=dev),
-        )
+        outputs = _attribute_outputs(dt, m, want_depth, want_name_counts)
     outputs["diag"] = _new_diag(dev, stream)
     ws = ws or Workspace(dev)
     need = L.opattr_workspace_bytes(C.byref(m.k), C.byref(m.p), C.byref(m.r), C.byref(m.d))
@@ -354,10 +371,39 @@ def opattr_attribute(dt: dict, policy=MISMATCH_PREFIX, agg_kind=None, flags=0, a
     del k_keep
     _check(rc, "opattr_attribute")
     if raise_strict and policy == MISMATCH_STRICT:
-        d = read_diag(outputs["diag"], stream)
-        if d["status"] == -4:
-            raise InvocationCountMismatchError(
-                f"{d['names_mismatched']} kernel names have different launch and profiled counts")
+        _raise_strict(outputs, stream)
+    return outputs
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def opattr_attribute_noalloc(dt: dict, policy=MISMATCH_PREFIX, agg_kind=None, flags=0,
+                             absent_mask=0, want_depth=True, want_name_counts=True, stream=None,
+                             outputs: Outputs | None = None, raise_strict=True) -> Outputs:
+    """opattr_attribute on the library's own scratch (see opattr_attribute_noalloc
+    in include/opattr.h): the call itself allocates nothing; pass ``outputs``
+    (from an earlier call) to allocate nothing here either."""
+    L = library()
+    m = _Marshal(dt, flags, absent_mask)
+    dev = dt["counters"].device
+    if outputs is None:
+        outputs = _attribute_outputs(dt, m, want_depth, want_name_counts)
+    if outputs.get("diag") is None:
+        outputs["diag"] = _new_diag(dev, stream)
+    else:
+        _check(L.opattr_diag_clear(_p(outputs["diag"]), _stream_handle(stream)),
+               "opattr_diag_clear")
+    k_keep, kp = _kinds(agg_kind)
+    rc = L.opattr_attribute_noalloc(C.byref(m.k), C.byref(m.p), C.byref(m.r), C.byref(m.d),
+                                    policy, kp, _p(outputs["match"]), _p(outputs["range_id"]),
+                                    _p(outputs["range_depth"]), _p(outputs["name_counts"]),
+                                    _p(outputs["table"]), _p(outputs["summary"]),
+                                    _p(outputs["diag"]), _stream_handle(stream))
+    del k_keep
+    _check(rc, "opattr_attribute_noalloc")
+    if raise_strict and policy == MISMATCH_STRICT:
+        _raise_strict(outputs, stream)
     return outputs
 
 
