@@ -277,6 +277,20 @@ int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
   return 0;
 }
 
+int oref_counters_out(const oref_profiled *p, const int32_t *match, int64_t n, float *out) {
+  if (!p || n < 0 || (n > 0 && (!match || !out))) return OREF_ERR_ARG;
+  for (int64_t i = 0; i < n; ++i) {
+    const int32_t m = match[i];
+    for (int c = 0; c < OREF_NC; ++c) {
+      float v = NAN; /* no row, or the counter was not captured */
+      if (m >= 0 && m < p->n && !((p->absent_mask >> c) & 1u))
+        v = p->counters[(int64_t)m * p->row_stride + (int64_t)c * p->col_stride];
+      out[i * OREF_NC + c] = v;
+    }
+  }
+  return 0;
+}
+
 /* ----------------------------------------------------------------------- */
 /* Dedup class discovery (Sec. 3.7)                                         */
 /* ----------------------------------------------------------------------- */

@@ -111,6 +111,11 @@ int oref_match(const oref_kernels *k, const oref_profiled *p, const oref_dims *d
                int policy, int32_t *match, uint32_t *name_counts, oref_diag *diag);
 int oref_dedup(const oref_kernels *k, const oref_dims *d, int32_t *match,
                oref_diag *diag);
+/* Counters inherited by position (Sec. 3.7): once the broadcast has given
+   every duplicate its representative's match, each launch carries the counter
+   row of the profiled row it is matched to. out[i*20 + c] = counter c of row
+   match[i]; NaN when match[i] is outside [0, p->n) or counter c is absent. */
+int oref_counters_out(const oref_profiled *p, const int32_t *match, int64_t n, float *out);
 int oref_enclose(const oref_kernels *k, const oref_ranges *r, const oref_dims *d,
                  int32_t *range_id, uint8_t *range_depth, oref_diag *diag);
 /* The full walk of Alg. 2. For each kernel, the ranges of its stream that

@@ -117,6 +117,7 @@ def load(path: str):
     L.oref_match.argtypes = [P(Kernels), P(Profiled), P(Dims), C.c_int, C.c_void_p,
                              C.c_void_p, P(Diag)]
     L.oref_dedup.argtypes = [P(Kernels), P(Dims), C.c_void_p, P(Diag)]
+    L.oref_counters_out.argtypes = [P(Profiled), C.c_void_p, C.c_int64, C.c_void_p]
     L.oref_enclose.argtypes = [P(Kernels), P(Ranges), P(Dims), C.c_void_p, C.c_void_p,
                                P(Diag)]
     L.oref_aggregate.argtypes = [P(Kernels), P(Profiled), C.c_void_p, C.c_void_p,
@@ -136,7 +137,7 @@ def load(path: str):
                              C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                              P(Coverage), P(Diag)]
     L.oref_diag_finish.argtypes = [P(Diag), C.c_int]
-    for f in ("oref_match", "oref_dedup", "oref_enclose", "oref_enclose_walk", "oref_aggregate",
+    for f in ("oref_match", "oref_dedup", "oref_counters_out", "oref_enclose", "oref_enclose_walk", "oref_aggregate",
               "oref_dedup_classes", "oref_aggregate_ops", "oref_tiers",
               "oref_aggregate_dispatch", "oref_enclose_all"):
         getattr(L, f).restype = C.c_int
@@ -254,6 +255,20 @@ def attribute(tr, policy=PREFIX, agg_kind=None, absent_mask=0, stages=None, libr
         out["summary"] = {f: getattr(sm, f) for f, _ in Summary._fields_}
     L.oref_diag_finish(C.byref(dg), policy)
     out["diag"] = diag_dict(dg)
+    return out
+
+
+def counters_out(tr, match, absent_mask=0, library=None):
+    """Each launch's inherited counter row (Sec. 3.7): ``out[i, c]`` = counter c
+    of profiled row ``match[i]``, NaN when unmatched or absent. ``tr`` gives
+    the profiled rows (``counters``, ``pf_name``)."""
+    L = library if library is not None else lib()
+    x = _Inputs(tr, absent_mask)
+    m = np.ascontiguousarray(match, dtype=np.int32)
+    out = np.empty((m.size, NC), dtype=np.float32)
+    rc = L.oref_counters_out(C.byref(x.p), _ptr(m), m.size, _ptr(out))
+    if rc:
+        raise ValueError(f"oref_counters_out: {rc}")
     return out
 
 

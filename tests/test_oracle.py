@@ -234,6 +234,65 @@ def test_dedup_error_cases():
     np.testing.assert_array_equal(out["match"][3:], [-1] * 6)
 
 
+def test_counters_out_inherited_by_position():
+    """Sec. 3.7: a duplicate layer's launches carry the counters of the
+    representative's launch at the same position. Planted: row j of the
+    profile holds 1000 * j + c, and the representative's launches are rows
+    0, 1, 2 in launch order."""
+    tr = _dedup_case()
+    tr["counters"] = (1000 * np.arange(3)[:, None] + np.arange(20)[None, :]).astype(np.float32)
+    rows = tr["counters"]
+    out = O.attribute(tr, stages=["match", "dedup"])
+    got = O.counters_out(tr, out["match"])
+    np.testing.assert_array_equal(got, rows[[0, 1, 2] * 3])
+    # counters absent from the capture are NaN for every launch
+    got = O.counters_out(tr, out["match"], absent_mask=(1 << 3) | (1 << 19))
+    assert np.isnan(got[:, [3, 19]]).all()
+    keep = [c for c in range(20) if c not in (3, 19)]
+    np.testing.assert_array_equal(got[:, keep], rows[[0, 1, 2] * 3][:, keep])
+    # a duplicate whose name differs at its position inherits nothing
+    t2 = dict(tr, name_id=tr["name_id"].copy())
+    t2["name_id"][4] = 0
+    got = O.counters_out(t2, O.attribute(t2, stages=["match", "dedup"])["match"])
+    assert np.isnan(got[4]).all()
+    np.testing.assert_array_equal(got[[3, 5]], rows[[0, 2]])
+    # rows out of range and unmatched launches are NaN; strides are honoured
+    m = np.array([2, -1, 3, 0], np.int32)
+    t3 = dict(tr, counters=np.asfortranarray(rows))
+    got = O.counters_out(t3, m)
+    np.testing.assert_array_equal(got[[0, 3]], rows[[2, 0]])
+    assert np.isnan(got[[1, 2]]).all()
+
+
+def test_counters_out_gpt2_layers_equal_by_position():
+    """The GPT-2-shaped trace (12 identical layers, one profiled): every
+    launch of a duplicate layer carries the same counters as the launch at
+    its position in its class representative, with positions taken from the
+    partition tags in launch order."""
+    tr = tg.generate("gpt2")
+    out = O.attribute(tr, stages=["match", "dedup"])
+    assert out["diag"]["dedup_errors"] == 0
+    got = O.counters_out(tr, out["match"])
+    order = np.argsort(tr["seq"], kind="stable")
+    part = tr["part_id"][order]
+    members = {q: order[part == q] for q in np.unique(part[part >= 0])}
+    checked = 0
+    for q, idx in members.items():
+        r = int(tr["part_rep"][q])
+        if r == q:
+            continue
+        src = members[r]
+        assert src.size == idx.size
+        np.testing.assert_array_equal(got[idx], got[src])
+        checked += idx.size
+    assert checked > 0.9 * tr["seq"].size * 11 / 12 * 0.9
+    # the representative's launches carry rows of their own name
+    reps = np.concatenate([members[q] for q in members if tr["part_rep"][q] == q])
+    m = out["match"][reps]
+    assert (m >= 0).all() and (tr["pf_name"][m] == tr["name_id"][reps]).all()
+    np.testing.assert_array_equal(got[reps], tr["counters"][m])
+
+
 def test_dedup_contiguity_is_in_launch_order():
     """A partition is a window of launches (Sec. 3.7): with gaps between the
     launch ordinals it is still contiguous when no other launch falls inside."""

@@ -77,6 +77,13 @@ MUTANTS = {
                             "for (int64_t u = 0; u < top; ++u) {\n          const int64_t id = stack[u];\n          if (r->end_ns[id] < t) continue; /* ended before the point */"),
     "all_touching_excluded": ("if (r->end_ns[id] < t) continue; /* ended before the point */",
                               "if (r->end_ns[id] <= t) continue; /* ended before the point */"),
+    "counters_out_absent_ignored": ("if (m >= 0 && m < p->n && !((p->absent_mask >> c) & 1u))",
+                                    "if (m >= 0 && m < p->n)"),
+    "counters_out_strides_swapped": (
+        "v = p->counters[(int64_t)m * p->row_stride + (int64_t)c * p->col_stride];",
+        "v = p->counters[(int64_t)m * p->col_stride + (int64_t)c * p->row_stride];"),
+    "counters_out_no_upper_bound": ("if (m >= 0 && m < p->n && !((p->absent_mask >> c) & 1u))",
+                                    "if (m >= 0 && !((p->absent_mask >> c) & 1u))"),
     "parent_is_root": ("if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[top - 1] : -1;",
                        "if (range_parent) range_parent[id] = top > 0 ? (int32_t)stack[0] : -1;"),
 }
@@ -199,6 +206,22 @@ def battery(L) -> bool:
     if not np.array_equal(out["range_id"], brute.enclose(tr)):
         return False
     if not _rows_close(out, brute.aggregate(tr, out["match"], out["range_id"])):
+        return False
+    import test_oracle
+    tr = test_oracle._dedup_case()
+    # three rows of a larger block, so that a mistaken stride stays in bounds
+    big = (1000 * np.arange(20)[:, None] + np.arange(20)[None, :]).astype(np.float32)
+    rows = big[:3]
+    tr["counters"] = rows
+    m = O.attribute(tr, stages=["match", "dedup"], library=L)["match"]
+    got = O.counters_out(tr, m, absent_mask=1 << 7, library=L)
+    want = rows[[0, 1, 2] * 3].copy()
+    want[:, 7] = np.nan
+    if not np.array_equal(got, want, equal_nan=True):
+        return False
+    got = O.counters_out(dict(tr, counters=np.asfortranarray(rows)),
+                         np.array([2, -1, 3], np.int32), library=L)
+    if not (np.array_equal(got[0], rows[2]) and np.isnan(got[1:]).all()):
         return False
     for seed in range(6):
         tr = cases.random_trace(400 + seed, T=80, R=20, drop=0.3)
