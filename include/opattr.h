@@ -26,11 +26,13 @@
  *    on the current HIP device, unless marked (host).
  *  - Every call enqueues its work on `stream` (a hipStream_t; NULL = the null
  *    stream) and returns without synchronising, except opattr_read_diag.
- *    opattr_attribute forks independent stages onto an internal stream of the
- *    current device (one per calling host thread, created on first use, default
- *    priority) with events recorded on `stream`, and joins it back on `stream`
- *    before its last kernels: completion is observed on `stream` alone, and a
- *    capture of `stream` records both branches.
+ *    opattr_attribute and opattr_attribute_tiered fork independent stages onto
+ *    two side streams of the current device (one pair per calling host thread,
+ *    created on its first such call, default priority, kept until the process
+ *    ends) with events recorded on `stream`, and join them back on `stream`
+ *    before their last kernels: completion is observed on `stream` alone, and
+ *    a capture of `stream` records every branch. Calls from one host thread on
+ *    several caller streams share that pair, so their side work is ordered.
  *  - The caller owns every buffer: inputs, outputs, the diag record and the
  *    workspace. No entry point allocates or frees device memory. Calls are
  *    stateless and reentrant on distinct workspaces. The workspace starts on a
@@ -251,9 +253,17 @@ int opattr_match(const opattr_kernels *k, const opattr_profiled *p, const opattr
    q) at launch-order position x of q takes match[] of the launch at position x
    of partition part_rep[q]; if that launch does not exist or has another name,
    or either partition is not one contiguous seq run, it gets -1 and counts as a
-   dedup error. In/out: match[k->n]. */
+   dedup error. In/out: match[k->n].
+   counters_out (device, or NULL): every launch's counters after the
+   broadcast, so that a duplicate carries its representative's metrics by
+   position: counters_out[i * 20 + c] (float32, [k->n][20], row-major, written
+   by the call) = counter c of profiled row match[i] of p, NaN when match[i]
+   is outside [0, p->n) or bit c of p->absent_mask is set. p (with counters)
+   is required with counters_out and not read without it (may be NULL).
+   Workspace: opattr_workspace_bytes(k, NULL, NULL, d). */
 int opattr_dedup_broadcast(const opattr_kernels *k, const opattr_dims *d, int32_t *match,
-                           opattr_diag *diag, void *ws, size_t ws_bytes, void *stream);
+                           const opattr_profiled *p, float *counters_out, opattr_diag *diag,
+                           void *ws, size_t ws_bytes, void *stream);
 
 /* Tiered attribution (the attribution-methods table and the decision-tree
    figure). For each launch, the first tier that applies:

@@ -458,9 +458,10 @@ int opattr_match(const opattr_kernels *k, const opattr_profiled *p, const opattr
 }
 
 int opattr_dedup_broadcast(const opattr_kernels *k, const opattr_dims *d, int32_t *match,
-                           opattr_diag *diag, void *ws, size_t ws_bytes, void *stream) {
+                           const opattr_profiled *p, float *counters_out, opattr_diag *diag,
+                           void *ws, size_t ws_bytes, void *stream) {
   if (!check_dims(d) || !check_kernels(k, true, false, false) || !diag ||
-      (k->n > 0 && !match))
+      (k->n > 0 && !match) || (counters_out && !check_profiled(p, false, true)))
     return OPATTR_ERR_INVALID_ARG;
   const Plan pl = make_plan(k, nullptr, nullptr, d);
   if (!ws_ok(ws, ws_bytes, pl)) return OPATTR_ERR_WORKSPACE;
@@ -470,6 +471,7 @@ int opattr_dedup_broadcast(const opattr_kernels *k, const opattr_dims *d, int32_
     build_seq_view(k, d, ws, pl, diag, (d->flags & OPATTR_VALIDATE) != 0, s);
     run_dedup(k, d, match, diag, ws, pl, s);
   }
+  if (counters_out) run_counters_out(p, match, k->n, counters_out, s);
   launch_finish(diag, nullptr, 0, s);
   return launch_status();
 }

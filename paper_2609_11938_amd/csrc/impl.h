@@ -198,6 +198,10 @@ void launch_stream_blocks(const uint16_t *st, int64_t n, uint32_t NS, int64_t *b
 // broadcasts when IomArgs::want_dedup is set).
 void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, opattr_diag *diag,
                void *ws, const Plan &pl, hipStream_t s);
+// every launch's counter row by its (broadcast) match: out[i][20], NaN for
+// no row or an absent counter
+void run_counters_out(const opattr_profiled *p, const int32_t *match, int64_t T, float *out,
+                      hipStream_t s);
 
 // ---- dedup class discovery (classes.hip) -----------------------------------------
 // bits of the class key kept by the calling host thread (opattr_set_class_key_bits)

@@ -1426,4 +1426,36 @@ void run_dedup(const opattr_kernels *k, const opattr_dims *d, int32_t *match, op
   probe_end(OPATTR_PROBE_DEDUP, s);
 }
 
+// out[i * 20 + c] = counter c of row match[i]. A block writes 64 whole
+// rows (1280 consecutive floats): thread t takes elements t, t + 256, ...,
+// so every store is coalesced and the lanes of one row read its counters
+// side by side (contiguous when the counters are row-major).
+constexpr int kCoRows = 64;
+__global__ void __launch_bounds__(256) k_counters_out(const float *__restrict__ cnt, int64_t rs,
+                                                      int64_t cs, int64_t P, uint32_t absent,
+                                                      const int32_t *__restrict__ match,
+                                                      int64_t T, float *__restrict__ out) {
+  const int64_t i0 = (int64_t)blockIdx.x * kCoRows;
+  const int64_t nr = T - i0 < kCoRows ? T - i0 : kCoRows;
+  const int ne = (int)nr * OPATTR_NUM_COUNTERS;
+#pragma unroll
+  for (int k = 0; k < kCoRows * OPATTR_NUM_COUNTERS / 256; ++k) {
+    const int e = k * 256 + (int)threadIdx.x;
+    if (e >= ne) break;
+    const int r = e / OPATTR_NUM_COUNTERS, c = e - r * OPATTR_NUM_COUNTERS;
+    const int32_t m = match[i0 + r];
+    float v = __builtin_nanf("");
+    if (m >= 0 && m < P && !((absent >> c) & 1u)) v = cnt[(int64_t)m * rs + (int64_t)c * cs];
+    out[i0 * OPATTR_NUM_COUNTERS + e] = v;
+  }
+}
+
+void run_counters_out(const opattr_profiled *p, const int32_t *match, int64_t T, float *out,
+                      hipStream_t s) {
+  if (T <= 0) return;
+  const unsigned nb = (unsigned)((T + kCoRows - 1) / kCoRows);
+  k_counters_out<<<nb, 256, 0, s>>>(p->counters, p->row_stride, p->col_stride, p->n,
+                                    p->absent_mask, match, T, out);
+}
+
 }  // namespace opa

@@ -118,7 +118,8 @@ def library(path: str | None = None):
     L.opattr_read_diag.argtypes = [vp, P(opattr_diag), vp]
     L.opattr_match.argtypes = [P(opattr_kernels), P(opattr_profiled), P(opattr_dims), i, vp, vp,
                                vp, vp, sz, vp]
-    L.opattr_dedup_broadcast.argtypes = [P(opattr_kernels), P(opattr_dims), vp, vp, vp, sz, vp]
+    L.opattr_dedup_broadcast.argtypes = [P(opattr_kernels), P(opattr_dims), vp,
+                                         P(opattr_profiled), vp, vp, vp, sz, vp]
     L.opattr_dedup_classes.argtypes = [P(opattr_kernels), P(opattr_dims), vp, vp, vp, sz, vp]
     L.opattr_enclose.argtypes = [P(opattr_kernels), P(opattr_ranges), P(opattr_dims), vp, vp,
                                  vp, vp, sz, vp]
@@ -426,15 +427,28 @@ def opattr_match(dt: dict, policy=MISMATCH_PREFIX, flags=0, ws: Workspace | None
 
 
 def opattr_dedup_broadcast(dt: dict, match, flags=0, ws: Workspace | None = None,
-                           stream=None) -> Outputs:
+                           stream=None, counters_out=None, absent_mask=0) -> Outputs:
+    """Dedup broadcast of ``match`` in place; with ``counters_out`` (True for a
+    new [T, 20] float32 tensor, or such a tensor) also every launch's
+    inherited counter row."""
+    import torch
+
     L = library()
-    m = _Marshal(dt, flags)
+    m = _Marshal(dt, flags, absent_mask)
     dev = dt["counters"].device
-    out = Outputs(match=match, diag=_new_diag(dev, stream))
+    if counters_out is True:
+        counters_out = torch.empty((m.T, NUM_COUNTERS), dtype=torch.float32, device=dev)
+    if counters_out is not None and (counters_out.shape != (m.T, NUM_COUNTERS)
+                                     or counters_out.dtype != torch.float32
+                                     or not counters_out.is_contiguous()):
+        raise ValueError("counters_out must be a contiguous [T, 20] float32 tensor")
+    out = Outputs(match=match, diag=_new_diag(dev, stream), counters_out=counters_out)
     ws = ws or Workspace(dev)
-    buf = ws.get(L.opattr_workspace_bytes(C.byref(m.k), C.byref(m.p), C.byref(m.r), C.byref(m.d)))
-    _check(L.opattr_dedup_broadcast(C.byref(m.k), C.byref(m.d), _p(match), _p(out["diag"]),
-                                    _p(buf), C.c_size_t(buf.numel()), _stream_handle(stream)),
+    buf = ws.get(L.opattr_workspace_bytes(C.byref(m.k), None, None, C.byref(m.d)))
+    _check(L.opattr_dedup_broadcast(C.byref(m.k), C.byref(m.d), _p(match),
+                                    C.byref(m.p) if counters_out is not None else None,
+                                    _p(counters_out), _p(out["diag"]), _p(buf),
+                                    C.c_size_t(buf.numel()), _stream_handle(stream)),
            "opattr_dedup_broadcast")
     return out
 

@@ -218,10 +218,12 @@ def test_stages_one_by_one():
     np.testing.assert_array_equal(parity.host(m["match"]), want["match_iom"])
     np.testing.assert_array_equal(parity.host(m["name_counts"]).view(np.uint32),
                                   want["name_counts"])
-    dd = opattr.opattr_dedup_broadcast(dt, m["match"])
+    dd = opattr.opattr_dedup_broadcast(dt, m["match"], counters_out=True)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(parity.host(m["match"]), want["match"])
     assert opattr.read_diag(dd["diag"])["dedup_errors"] == 0
+    np.testing.assert_array_equal(parity.host(dd["counters_out"]),
+                                  O.counters_out(tr, want["match"]))
     e = opattr.opattr_enclose(dt)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(parity.host(e["range_id"]), want["range_id"])
@@ -240,9 +242,22 @@ def test_stage_dedup_and_aggregate_on_given_inputs():
     want = _oracle("large", "stream_major")
     dt = opattr.to_device(tr, DEV)
     mt = torch.from_numpy(want["match_iom"].copy()).to(DEV)
-    opattr.opattr_dedup_broadcast(dt, mt, flags=opattr.SEQ_DENSE)
+    absent = 1 << 9
+    dd = opattr.opattr_dedup_broadcast(dt, mt, flags=opattr.SEQ_DENSE, counters_out=True,
+                                       absent_mask=absent)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(parity.host(mt), want["match"])
+    # the 10M x 20 inherited counters: every launch of a sample, one by one
+    rng = np.random.default_rng(11)
+    idx = np.sort(rng.choice(tr["seq"].size, 200_000, replace=False))
+    got = parity.host(dd["counters_out"][torch.from_numpy(idx).to(DEV)])
+    ref = O.counters_out(tr, want["match"][idx], absent_mask=absent)
+    np.testing.assert_array_equal(got, ref)
+    co = dd["counters_out"]
+    assert int(torch.isnan(co[:, 9]).sum()) == tr["seq"].size
+    unmatched = torch.from_numpy(want["match"] < 0).to(DEV)
+    assert int(torch.isnan(co[unmatched]).logical_not().sum()) == 0
+    del dd, co
     a = opattr.opattr_aggregate(dt, torch.from_numpy(want["match"]).to(DEV),
                                 torch.from_numpy(want["range_id"]).to(DEV))
     torch.cuda.synchronize()
