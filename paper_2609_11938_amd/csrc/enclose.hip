@@ -258,13 +258,37 @@ k_enclose(EncParams a) {
         const bool win = staged && st[k] == s0;  // the staged starts belong to this stream
         int32_t p;
         if (have && st[k] == sprev && q[k] >= qprev) {
-          p = pprev;
-          while (p + 1 < hi) {
-            const int64_t x = (int64_t)p + 1 - wlo;
-            const uint64_t sx = (win && x >= 0 && x < wn) ? sS[x] : a.cr.s[p + 1];
-            if (sx > q[k]) break;
-            ++p;
+          // forward from the previous launch's range: single steps first
+          // (launches close in time), then steps of 2, 4, 8, ... and a
+          // bisection of the last one (launches far apart in storage order)
+          auto start_of = [&](int64_t j) -> uint64_t {
+            const int64_t x = j - wlo;
+            return (win && x >= 0 && x < wn) ? sS[x] : a.cr.s[j];
+          };
+          int64_t lo2 = pprev, hi2 = hi;  // start_of(lo2) <= q (or lo2 = lo - 1)
+          int n1 = 0;
+          for (; n1 < 4 && lo2 + 1 < hi; ++n1) {
+            if (start_of(lo2 + 1) > q[k]) {
+              hi2 = lo2 + 1;
+              break;
+            }
+            ++lo2;
           }
+          if (n1 == 4) {
+            for (int64_t stp = 2; lo2 + stp < hi; stp <<= 1) {
+              if (start_of(lo2 + stp) > q[k]) {
+                hi2 = lo2 + stp;
+                break;
+              }
+              lo2 += stp;
+            }
+            while (hi2 - lo2 > 1) {  // every start in [hi2, hi) is past q
+              const int64_t mid = lo2 + ((hi2 - lo2) >> 1);
+              if (start_of(mid) <= q[k]) lo2 = mid;
+              else hi2 = mid;
+            }
+          }
+          p = (int32_t)lo2;
         } else if (st[k] == s0 && wn == 0) {
           p = lo - 1;  // no range of the stream starts at or before the block's queries
         } else if (win) {
