@@ -6,9 +6,12 @@ broadcast, enclosure, aggregation) over the large synthetic trace: 10M kernel
 launches on 16 streams, 500k nested ranges (depth <= 8), 1000 kernel names
 Zipf(1.1), layer dedup 48 layers / 3 classes, 1M profiled rows of 20 fp32
 counters. Inputs are resident in HBM before the timed region. Prints one JSON
-line: records/s, the dominant kernel against the HBM roofline (HIP probe events
-recorded by the library around its launches), and the oracle's rate on the
-host cores as a reported CPU baseline.
+line: records/s (wall clock over the timed steps, no probe events inside
+them), per-step spread and graph-replayed step time, the dominant kernel
+against the HBM roofline (HIP probe events recorded by the library around its
+launch, on its stream), a per-kernel table, a device copy's rate in the same
+run, rows for the other workloads and launch orders, and the oracle's rate on
+one host core as a reported CPU baseline.
 """
 import argparse
 import json
@@ -26,9 +29,9 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
 
 
 def algorithmic_bytes(tr):
-    """Compulsory bytes: every input read once, every output written once, at
-    the ABI widths (duplicate counter rows reused by dedup count once).
-    Returns the step total and, per single-kernel probe, that kernel's bytes."""
+    """Compulsory bytes of one step: every input read once, every output
+    written once, at the ABI widths (duplicate counter rows reused by dedup
+    count once)."""
     T, P, R = tr["seq"].size, tr["pf_name"].size, tr["r_start"].size
     part = 4 if tr.get("part_id") is not None else 0
     G = tr["n_ops"] + 1
@@ -38,35 +41,52 @@ def algorithmic_bytes(tr):
     ranges = R * (8 + 8 + 2 + 4)                    # start, end, stream, op
     outputs = T * (4 + 4)                           # match, range_id
     table = G * 192 + 4 * NP                        # op rows + class map
-    per_kernel = {
-        # k_seqview_dense: seq in, launch-order view out
-        "seq_view": T * (4 + 4),
-        # k_tl_hist_w: view, name, partition in
-        "tl_hist": T * (4 + 4 + part),
-        # k_pf_hist_w: row names in
-        "pf_hist": P * 4,
-        # k_pf_slot_w: row names in, slot table out
-        "pf_slot": P * (4 + 4),
-        # k_tl_look (per-tile rank, join and dedup lookup): seq, name,
-        # partition in; match out
-        "tl_match": T * (4 + 4 + part + 4),
-        # k_dedup: partition, name, seq in; match out
-        "dedup": T * (4 + 4 + 4 + 4),
-        # k_enclose: stream, query point in, range id out; range starts, ends
-        # and parents
-        "main_pass": T * (2 + 8 + 4) + R * (8 + 8 + 4),
-        # k_agg_rows: range id, match, duration of every launch, each range's
-        # op id and each profiled counter row once
-        "agg_runs": T * (4 + 4 + 4) + R * 4 + P * 80,
-    }
-    return timeline + profiled + ranges + outputs + table, per_kernel
+    return timeline + profiled + ranges + outputs + table
 
 
-# kernel behind each single-kernel probe (for the rocprofv3 cross-check)
-PROBE_KERNEL = {"seq_view": "k_seqview_dense", "tl_hist": "k_tl_hist_w",
-                "pf_hist": "k_pf_hist_w", "pf_slot": "k_pf_slot_w",
-                "tl_match": "k_tl_look", "dedup": "k_dedup",
-                "main_pass": "k_enclose", "agg_runs": "k_agg_rows"}
+def eligible_launches(tr):
+    """Launches that rank themselves (not a layer duplicate, valid name)."""
+    import numpy as np
+
+    ok = tr["name_id"] < tr["n_names"]
+    part = tr.get("part_id")
+    if part is None or tr.get("part_rep") is None:
+        return int(ok.sum())
+    rep = tr["part_rep"]
+    p = part.astype(np.int64)
+    own = (p < 0) | (rep[np.clip(p, 0, rep.size - 1)] == p)
+    return int((ok & own).sum())
+
+
+def fused_kernels(tr):
+    """The kernels of one opattr_attribute step on the fused path (kernels
+    stream-major with dense seq, sparse ranges), each with the probe that
+    brackets it, the stream it runs on and its algorithmic bytes per launch
+    of the kernel: what it must read and write for its own function."""
+    T, P, R = tr["seq"].size, tr["pf_name"].size, tr["r_start"].size
+    part = 4 if tr.get("part_id") is not None else 0
+    E = eligible_launches(tr)
+    return [
+        # seq tiles: seq, name and partition of every launch
+        dict(kernel="k_f_pass1", probe="tl_hist", stream="caller", bytes=T * (4 + 4 + part)),
+        # ranks of the eligible launches: their bucket records in, row and
+        # name by seq rank out
+        dict(kernel="k_f_pass2", probe="tl_match", stream="caller", bytes=E * (4 + 4 + 4)),
+        # every launch's match with the dedup broadcast: seq, name,
+        # partition in, match out
+        dict(kernel="k_f_match", probe="dedup", stream="caller", bytes=T * (4 + 4 + part + 4)),
+        # run reduction: range id, match and duration of every launch, the
+        # op of each range and each profiled counter row once
+        dict(kernel="k_f_agg", probe="agg_runs", stream="caller",
+             bytes=T * (4 + 4 + 4) + R * 4 + P * 80),
+        # enclosure: stream and query point of every launch in, range id
+        # out; range starts, ends and parents
+        dict(kernel="k_enclose", probe="main_pass", stream="side 1",
+             bytes=T * (2 + 8 + 4) + R * (8 + 8 + 4)),
+        # profiled rows: names in (histograms), names in and slots out
+        dict(kernel="k_pf_hist_w", probe="pf_hist", stream="side 2", bytes=P * 4),
+        dict(kernel="k_pf_slot_w", probe="pf_slot", stream="side 2", bytes=P * (4 + 4)),
+    ]
 
 
 def source_hash():
@@ -118,19 +138,105 @@ def copy_calibration(mb, reps):
     print(json.dumps({"copy_bytes": n * 4, "reps": reps}), flush=True)
 
 
-def cpu_baseline(tr, reps=2):
+def stored_kernel_ms(kernel, config, emission):
+    """Average duration (ms) of `kernel` in the committed rocprofv3 kernel
+    statistics of this workload (profiles/attribute_<config>_<emission>_kernel_stats.txt),
+    or None when absent or taken on other sources."""
+    path = os.path.join(ROOT, "profiles", f"attribute_{config}_{emission}_kernel_stats.txt")
+    if not os.path.exists(path):
+        return None
+    ok, ms = False, None
+    with open(path) as fh:
+        for line in fh:
+            if line.startswith("# source_hash:"):
+                ok = line.split(":", 1)[1].strip() == source_hash()
+            f = line.split()
+            if len(f) >= 3 and not line.startswith("#") and \
+                    (f[0] == kernel or f[0].startswith(kernel + "<")):
+                try:
+                    ms = float(f[2]) / 1e3
+                except ValueError:
+                    pass
+    return ms if ok else None
+
+
+def copy_bandwidth(mib=1024, reps=10):
+    """Device-to-device copy rate (read + write bytes per second) in the same
+    run: the practical HBM ceiling next to the 8 TB/s peak."""
+    import torch
+
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.int32, device="cuda:0")
+    b = torch.empty_like(a)
+    for _ in range(2):
+        b.copy_(a)
+    ev = [_events(2) for _ in range(reps)]
+    for e0, e1 in ev:
+        e0.record()
+        b.copy_(a)
+        e1.record()
+    torch.cuda.synchronize()
+    ms = statistics.median(e0.elapsed_time(e1) for e0, e1 in ev)
+    del a, b
+    return {"bytes": 2 * n * 4, "median_ms": ms, "GBps": 2 * n * 4 / (ms * 1e-3) / 1e9}
+
+
+def clocks():
+    """Current SCLK / MCLK as rocm-smi reports them (None when unavailable)."""
+    import subprocess
+
+    try:
+        r = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True,
+                           text=True, timeout=30)
+        data = json.loads(r.stdout)
+    except Exception:  # noqa: BLE001 - the record is optional
+        return None
+    card = next(iter(data.values()), {}) if isinstance(data, dict) else {}
+    out = {}
+    for k, v in card.items():
+        kl = k.lower()
+        if "sclk" in kl or "mclk" in kl:
+            out[k] = v
+    return out or None
+
+
+def cpu_info():
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, os.cpu_count()
+
+
+def cpu_baseline(tr, reps=3):
+    """The oracle on one host core (the process pinned to core 0, as taskset -c 0
+    would): one warm-up run, then `reps` timed runs of the full workload."""
     from oracle import oracle as O
 
     O.build(force=False)
-    times = []
-    for _ in range(reps):
-        t0 = time.perf_counter()
+    prev = os.sched_getaffinity(0)
+    os.sched_setaffinity(0, {0})
+    try:
         O.attribute(tr)
-        times.append(time.perf_counter() - t0)
+        times = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            O.attribute(tr)
+            times.append(time.perf_counter() - t0)
+    finally:
+        os.sched_setaffinity(0, prev)
     med = statistics.median(times)
+    model, ncpu = cpu_info()
     return {"value": tr["seq"].size / med, "unit": "records/s", "cores": 1, "kind": "oracle",
-            "sample": f"the full workload ({tr['seq'].size} launches), {reps} runs, median "
-                      f"{med:.2f} s, single-threaded C oracle"}
+            "sample": f"the full workload ({tr['seq'].size} launches): 1 warm-up + {reps} "
+                      f"runs pinned to core 0, median {med:.2f} s (min {min(times):.2f}, "
+                      f"max {max(times):.2f}), single-threaded C oracle",
+            "cpu_model": model, "nproc": ncpu}
 
 
 def _events(n):
@@ -318,6 +424,131 @@ def measure_next_rows(dt, tr, flags, steps, warmup, out, ws):
     return rows
 
 
+FLAGS = {"stream_major": 1 | 2 | 4, "seq": 2, "shuffled": 0}  # layout hints per emission
+
+
+def new_outputs(tr, dev):
+    import torch
+
+    from paper_2609_11938_amd import opattr
+
+    T = tr["seq"].size
+    return opattr.Outputs(
+        match=torch.empty(T, dtype=torch.int32, device=dev),
+        range_id=torch.empty(T, dtype=torch.int32, device=dev),
+        range_depth=None, name_counts=None,
+        table=torch.empty((tr["n_ops"] + 1) * 192, dtype=torch.uint8, device=dev),
+        summary=torch.empty(40, dtype=torch.uint8, device=dev))
+
+
+def timed_steps(step, steps, warmup, flush=None):
+    """`warmup` untimed steps, then exactly `steps` timed ones bracketed by
+    synchronisations: the wall clock over all of them, and each step's span
+    from HIP events recorded on the caller's stream between steps (a flush,
+    when given, runs before each step, outside its span)."""
+    import torch
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [_events(2) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for e0, e1 in ev:
+        if flush is not None:
+            flush()
+        e0.record()
+        step()
+        e1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    per = [e0.elapsed_time(e1) for e0, e1 in ev]
+    return (t1 - t0) * 1e3 / steps, per
+
+
+def graph_step_ms(step, steps):
+    """One step captured in a HIP graph (both side-stream branches) and
+    replayed `steps` times: ms per replay, median over the replays."""
+    import torch
+
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        step()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=cap):
+        step()
+    g.replay()
+    torch.cuda.synchronize()
+    ev = [_events(2) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for e0, e1 in ev:
+        e0.record()
+        g.replay()
+        e1.record()
+    torch.cuda.synchronize()
+    per = [e0.elapsed_time(e1) for e0, e1 in ev]
+    del g
+    return statistics.median(per), min(per), max(per)
+
+
+def spread(per):
+    return {"median": statistics.median(per), "min": min(per), "max": max(per)}
+
+
+def config_row(name, emission, validate, steps, warmup, dev, graph, flush_mib):
+    """records/s of one opattr_attribute step on another workload (inputs
+    resident; optional graph replay; optional flush of the caches by writing
+    a `flush_mib` MiB buffer before each timed step)."""
+    import torch
+
+    from paper_2609_11938_amd import opattr, tracegen
+
+    tr = tracegen.generate(name, emission=emission)
+    dt = opattr.to_device(tr, dev)
+    flags = FLAGS[emission] | (opattr.VALIDATE if validate else 0)
+    ws = opattr.Workspace(dev)
+    out = new_outputs(tr, dev)
+    T = tr["seq"].size
+
+    def step():
+        opattr.opattr_attribute(dt, flags=flags, outputs=out, ws=ws, raise_strict=False)
+
+    step()
+    torch.cuda.synchronize()
+    diag = opattr.read_diag(out["diag"])
+    if diag["status"] not in (0, -4):
+        raise SystemExit(f"{name}/{emission} reported {diag}")
+    flush = None
+    if flush_mib:
+        buf = torch.empty(flush_mib << 18, dtype=torch.int32, device=dev)
+
+        def flush():
+            buf.fill_(1)
+    ms, per = timed_steps(step, steps, warmup, flush)
+    nbytes = algorithmic_bytes(tr)
+    med = statistics.median(per)
+    row = {"workload": f"{name}: {T} launches, {tr['n_streams']} streams, "
+                       f"{tr['r_start'].size} ranges, {tr['n_names']} names, "
+                       f"{tr['pf_name'].size} profiled rows, {tr['n_ops']} ops, "
+                       f"emission {emission}" + (", validated" if validate else ""),
+           "records_per_s": T / (med * 1e-3), "step_ms": spread(per),
+           "algorithmic_bytes": nbytes, "frac_of_hbm_peak": nbytes / (med * 1e-3) / 1e9 /
+           HBM_PEAK_GBPS}
+    if flush_mib:
+        row["flush_mib_before_each_step"] = flush_mib
+    else:
+        row["ms_per_step_back_to_back"] = ms
+    if graph:
+        gmed, gmin, gmax = graph_step_ms(step, steps)
+        row["graph_step_ms"] = {"median": gmed, "min": gmin, "max": gmax}
+        row["graph_records_per_s"] = T / (gmed * 1e-3)
+    del dt, out, ws
+    torch.cuda.empty_cache()
+    return row
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -330,6 +561,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-next-rows", action="store_true",
                     help="skip timing the walk with range kinds and class discovery")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the rows of the other workloads and orders")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -360,36 +593,26 @@ def main():
     print(f"generated {args.config}/{args.emission}: {tracegen.summary(tr)} in {gen_s:.1f}s",
           file=sys.stderr, flush=True)
     dt = opattr.to_device(tr, dev)
-    flags = {"stream_major": opattr.KERNELS_STREAM_MAJOR | opattr.SEQ_DENSE |
-             opattr.RANGES_NESTED, "seq": opattr.SEQ_DENSE, "shuffled": 0}[args.emission]
-    if args.validate:
-        flags |= opattr.VALIDATE
+    flags = FLAGS[args.emission] | (opattr.VALIDATE if args.validate else 0)
     ws = opattr.Workspace(dev)
     T = tr["seq"].size
-    out = opattr.Outputs(
-        match=torch.empty(T, dtype=torch.int32, device=dev),
-        range_id=torch.empty(T, dtype=torch.int32, device=dev),
-        range_depth=None, name_counts=None,
-        table=torch.empty((tr["n_ops"] + 1) * 192, dtype=torch.uint8, device=dev),
-        summary=torch.empty(40, dtype=torch.uint8, device=dev))
+    out = new_outputs(tr, dev)
 
     def step():
         opattr.opattr_attribute(dt, flags=flags, outputs=out, ws=ws, raise_strict=False)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    # 1. the headline: K steps, no probe events inside them
+    ms_per_step, per = timed_steps(step, args.steps, args.warmup)
     diag = opattr.read_diag(out["diag"])
     if diag["status"] != 0:
         raise SystemExit(f"attribution reported status {diag['status']}: {diag}")
+    value = T / (ms_per_step * 1e-3)
+    total_bytes = algorithmic_bytes(tr)
+    print(f"timed {args.steps} steps: {ms_per_step:.4f} ms/step", file=sys.stderr, flush=True)
 
-    # probe events: one start/stop pair per instrumented launch group per step.
-    # Every probe is recorded once in an untimed pass (to find the dominant
-    # kernel); the timed pass records only the dominant kernel's pair, since
-    # each recorded event adds a stream barrier.
+    # 2. every probe recorded once per step (each recorded event is a stream
+    # barrier inside the step: per-kernel spans, not the step time)
     nprobe = len(opattr.PROBES)
-    total_bytes, kbytes = algorithmic_bytes(tr)
-
     ev_all = [_events(2 * nprobe) for _ in range(args.steps)]
     torch.cuda.synchronize()
     for k in range(args.steps):
@@ -400,33 +623,57 @@ def main():
     probe_ms = {}
     for p, name in enumerate(opattr.PROBES):
         d = [ev_all[k][2 * p].elapsed_time(ev_all[k][2 * p + 1]) for k in range(args.steps)]
-        probe_ms[name] = statistics.mean(d)
-    dominant = max(kbytes, key=lambda n: probe_ms[n])
-    pdom = opattr.PROBES.index(dominant)
-
-    ev_dom = [_events(2) for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for k in range(args.steps):
-        only = [None] * (2 * nprobe)
-        only[2 * pdom], only[2 * pdom + 1] = ev_dom[k]
-        opattr.set_probe_events(only)
-        step()
-    torch.cuda.synchronize()
-    t_end = time.perf_counter()
-    opattr.set_probe_events(None)
-
-    ms_per_step = (t_end - t_start) * 1e3 / args.steps
-    value = T / (ms_per_step * 1e-3)
-    # the dominant single-kernel probe sets the roofline line, timed live
-    dom_ms = statistics.mean(e0.elapsed_time(e1) for e0, e1 in ev_dom)
-    achieved = kbytes[dominant] / (dom_ms * 1e-3) / 1e9
-    pipe_gbps = total_bytes / (ms_per_step * 1e-3) / 1e9
-    per_launch = stored_traffic(PROBE_KERNEL[dominant], args.config, args.emission)
-    traffic = per_launch * T if per_launch is not None else None
+        probe_ms[name] = statistics.median(d)
     print("probe ms/step: " + ", ".join(f"{n}={v:.4f}" for n, v in probe_ms.items()),
           file=sys.stderr, flush=True)
 
+    fused = args.emission == "stream_major" and T >= 16 * tr["r_start"].size
+    table = []
+    if fused:
+        for kk in fused_kernels(tr):
+            ms = probe_ms[kk["probe"]]
+            rp = stored_kernel_ms(kk["kernel"], args.config, args.emission)
+            per_launch = stored_traffic(kk["kernel"], args.config, args.emission)
+            row = dict(kk, probe_ms=ms, GBps=kk["bytes"] / (ms * 1e-3) / 1e9,
+                       rocprof_ms=rp,
+                       rocprof_frac=(kk["bytes"] / (rp * 1e-3) / 1e9 / HBM_PEAK_GBPS
+                                     if rp else None),
+                       measured_bytes=per_launch * T if per_launch is not None else None)
+            row["frac"] = row["GBps"] / HBM_PEAK_GBPS
+            row["traffic_ratio"] = (row["measured_bytes"] / kk["bytes"]
+                                    if row["measured_bytes"] else None)
+            table.append(row)
+        dom = max(table, key=lambda r: r["probe_ms"])
+    else:
+        dom = None
+
+    # 3. the dominant kernel timed live: K steps with only its probe pair,
+    # recorded on the stream it runs on
+    roofline = None
+    if dom is not None:
+        pdom = opattr.PROBES.index(dom["probe"])
+        ev_dom = [_events(2) for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        t_a = time.perf_counter()
+        for k in range(args.steps):
+            only = [None] * (2 * nprobe)
+            only[2 * pdom], only[2 * pdom + 1] = ev_dom[k]
+            opattr.set_probe_events(only)
+            step()
+        torch.cuda.synchronize()
+        t_b = time.perf_counter()
+        opattr.set_probe_events(None)
+        dom_ms = statistics.mean(e0.elapsed_time(e1) for e0, e1 in ev_dom)
+        achieved = dom["bytes"] / (dom_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "kernel": dom["kernel"], "achieved": achieved,
+                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                    "traffic": dom["measured_bytes"], "algorithmic_bytes": dom["bytes"],
+                    "avg_ms": dom_ms, "rocprof_avg_ms": dom["rocprof_ms"],
+                    "rocprof_frac": dom["rocprof_frac"],
+                    "ms_per_step_with_probe": (t_b - t_a) * 1e3 / args.steps}
+
+    copy = copy_bandwidth()
+    gmed, gmin, gmax = graph_step_ms(step, args.steps)
     line = {
         "metric": METRIC, "value": value, "unit": "records/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
@@ -441,16 +688,38 @@ def main():
                    "profiled_rows": int(tr["pf_name"].size), "ops": tr["n_ops"],
                    "partitions": tr["n_parts"], "emission": args.emission,
                    "validate": bool(args.validate)},
-        "roofline": {"bound": "hbm", "kernel": PROBE_KERNEL[dominant], "achieved": achieved,
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": traffic, "algorithmic_bytes": kbytes[dominant],
-                     "avg_ms": dom_ms},
-        "pipeline": {"algorithmic_bytes": total_bytes, "achieved_GBps": pipe_gbps,
-                     "frac_of_hbm_peak": pipe_gbps / HBM_PEAK_GBPS,
-                     "probe_ms_untimed_pass": probe_ms},
+        "step_ms": spread(per),
+        "graph_step_ms": {"median": gmed, "min": gmin, "max": gmax},
+        "roofline": roofline,
+        "pipeline": {"algorithmic_bytes": total_bytes,
+                     "achieved_GBps": total_bytes / (ms_per_step * 1e-3) / 1e9,
+                     "frac_of_hbm_peak": total_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                     "graph_frac_of_hbm_peak": total_bytes / (gmed * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                     "copy_GBps": copy["GBps"], "copy_bytes": copy["bytes"]},
+        "kernels": table,
+        "probe_ms_median": probe_ms,
+        "clocks": clocks(),
     }
     if not args.no_next_rows:
         line["next_rows"] = measure_next_rows(dt, tr, flags, args.steps, args.warmup, out, ws)
+    if not args.no_other_configs:
+        del dt, out, ws
+        torch.cuda.empty_cache()
+        rows = {}
+        for name, emission, validate, graph, flush in (
+                ("tiny", "stream_major", False, True, 0),
+                ("gpt2", "stream_major", False, True, 0),
+                ("sdpa", "stream_major", False, False, 512),
+                ("lstm", "stream_major", False, False, 512),
+                ("large", "seq", False, False, 0),
+                ("large", "shuffled", False, False, 0),
+                ("large", "stream_major", True, False, 0)):
+            key = f"{name}_{emission}" + ("_validate" if validate else "")
+            rows[key] = config_row(name, emission, validate, args.steps, args.warmup, dev,
+                                   graph, flush)
+            print(f"row {key}: {rows[key]['records_per_s']:.4g} records/s", file=sys.stderr,
+                  flush=True)
+        line["other_configs"] = rows
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(tr)
     print(json.dumps(line), flush=True)

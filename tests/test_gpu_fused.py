@@ -101,3 +101,43 @@ def test_fused_dedup_errors():
     out2, diag2 = _run(t2)
     assert want2["diag"]["status"] == diag2["status"] != 0
     parity.assert_attribute(out2, want2, diag2)
+
+
+def test_fused_graph_replay():
+    """The fused path captured in a HIP graph (caller stream and both side
+    streams) replays to the oracle's outputs, replay after replay, with the
+    outputs poisoned and eager work in between."""
+    import torch
+
+    T = 60_000
+    tr = cases.random_trace(808, T=T, S=4, n_names=31, R=T // 25, n_ops=300, t_max=4 * T,
+                            max_depth=5, dedup=True)
+    tr, _, _ = cases.stream_major(tr)
+    want = O.attribute(tr)
+    dt = opattr.to_device(tr, DEV)
+    ws = opattr.Workspace(DEV)
+    R = tr["r_start"].size
+    o = opattr.Outputs(
+        match=torch.empty(T, dtype=torch.int32, device=DEV),
+        range_id=torch.empty(T, dtype=torch.int32, device=DEV),
+        range_depth=torch.empty(R, dtype=torch.uint8, device=DEV),
+        name_counts=torch.empty((tr["n_names"], 2), dtype=torch.int32, device=DEV),
+        table=torch.empty((tr["n_ops"] + 1) * 192, dtype=torch.uint8, device=DEV),
+        summary=torch.empty(40, dtype=torch.uint8, device=DEV))
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        opattr.opattr_attribute(dt, flags=HINTS, ws=ws, outputs=o, raise_strict=False)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        opattr.opattr_attribute(dt, flags=HINTS, ws=ws, outputs=o, raise_strict=False)
+    for rep in range(4):
+        for k in ("match", "range_id", "table", "summary", "range_depth", "name_counts"):
+            o[k].fill_(0x5A if o[k].dtype == torch.uint8 else -7)
+        # eager work on the same workspace between replays
+        opattr.opattr_attribute(dt, flags=HINTS, ws=ws, raise_strict=False)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        print(f"case fused graph replay {rep}", flush=True)
+        parity.assert_attribute(o, want, opattr.read_diag(o["diag"]))
