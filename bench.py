@@ -72,13 +72,12 @@ def fused_kernels(tr):
         # ranks of the eligible launches: their bucket records in, row and
         # name by seq rank out
         dict(kernel="k_f_pass2", probe="tl_match", stream="caller", bytes=E * (4 + 4 + 4)),
-        # every launch's match with the dedup broadcast: seq, name,
-        # partition in, match out
-        dict(kernel="k_f_match", probe="dedup", stream="caller", bytes=T * (4 + 4 + part + 4)),
-        # run reduction: range id, match and duration of every launch, the
-        # op of each range and each profiled counter row once
+        # every launch's match with the dedup broadcast (seq, name,
+        # partition in, match out) and the run reduction (range id and
+        # duration of every launch, the op of each range and each profiled
+        # counter row once)
         dict(kernel="k_f_agg", probe="agg_runs", stream="caller",
-             bytes=T * (4 + 4 + 4) + R * 4 + P * 80),
+             bytes=T * (4 + 4 + part + 4 + 4 + 4) + R * 4 + P * 80),
         # enclosure: stream and query point of every launch in, range id
         # out; range starts, ends and parents
         dict(kernel="k_enclose", probe="main_pass", stream="side 1",

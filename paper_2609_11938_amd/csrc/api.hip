@@ -591,8 +591,8 @@ int opattr_aggregate(const opattr_kernels *k, const opattr_profiled *p, const in
 // ranges at most one per 16 launches): the ranges and the enclosure on a
 // side stream, the profiled slot table on a second one, the matching up to
 // the eligible launches' rows on the caller's stream; then one pass gives
-// every launch its match (dedup broadcast included) and one pass reduces the
-// runs of launches of one operator row.
+// every launch its match (dedup broadcast included) and reduces the runs of
+// launches of one operator row.
 static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
                            const opattr_ranges *r, const opattr_dims *d, int policy,
                            const uint8_t *agg_kind, int32_t *match, int32_t *range_id,
@@ -634,7 +634,6 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
     a.pf_join = ss->join2;
   }
   run_match(a, s);
-  if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
   const AggIn in = agg_inputs(e);
   FusedIn f{};
   f.k = k;
@@ -648,7 +647,7 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
   f.diag = diag;
   f.ws = ws;
   f.pl = &pl;
-  run_fused_match(f, s);
+  if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
   run_fused_agg(f, s);
   launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s, table, sum, pl.G, d->n_ops,
                 at<unsigned long long>(ws, pl.sumpart), fused_sum_blocks(pl));

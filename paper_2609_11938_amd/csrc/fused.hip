@@ -2,23 +2,23 @@
 // layer-dedup broadcast (Sec. 3.7) and aggregation (Eq. 1, Sec. 3.8.1) over
 // the launches in storage order.
 //
-// 1. k_f_match: the matching leaves, by seq rank, the row and name of every
-//    eligible launch (mbs, nbs). Each launch takes its own entry; a duplicate
-//    takes the entry of the representative's launch at the same position
-//    (the partition record gives the seq offset) when the names agree (else
-//    -1 and a dedup error).
-// 2. k_f_agg: each lane takes eight consecutive launches and adds their
+// 1. k_f_agg: each lane takes eight consecutive launches. Their matches come
+//    first: the matching leaves, by seq rank, the row and name of every
+//    eligible launch (mbs, nbs); each launch takes its own entry, and a
+//    duplicate the entry of the representative's launch at the same
+//    position (the partition record gives the seq offset) when the names
+//    agree (else -1 and a dedup error). The lane then adds the launches'
 //    durations and counter rows (m or m * d, or the fp32 maximum as an
-//    order-preserving key) into a register accumulator. Consecutive launches
-//    of one operator row form a run: a run that ends inside a lane is staged
-//    in LDS; the piece a lane ends with is carried across the wave by a
-//    segmented lane scan. A block keeps up to 128 partial results, sorts them
-//    by bucket of operator rows (256 buckets) and writes them to its own
-//    region with a (count, offset) entry per bucket; anything past that goes
-//    to a row accumulator with device-scope atomics.
-// 3. k_f_comb: one wave per (bucket, share of the blocks) adds the bucket's
+//    order-preserving key) into a register accumulator. Consecutive
+//    launches of one operator row form a run: a run that ends inside a lane
+//    is staged in LDS; the piece a lane ends with is carried across the
+//    wave by a segmented lane scan. A block keeps up to 128 partial results,
+//    sorts them by bucket of operator rows (256 buckets) and writes them to
+//    its own region with a (count, offset) entry per bucket; anything past
+//    that goes to a row accumulator with device-scope atomics.
+// 2. k_f_comb: one wave per (bucket, share of the blocks) adds the bucket's
 //    partial results of those blocks in LDS and writes one partial per row.
-// 4. k_f_rows: one block per bucket adds every share and the row
+// 3. k_f_rows: one block per bucket adds every share and the row
 //    accumulators and writes the bucket's table rows (DW-mean = sum /
 //    matched ns, NaN rules) and summary sums.
 // Integer fields are exact in any order; fp64 sums are added in an order
@@ -30,7 +30,6 @@
 
 namespace opa {
 
-constexpr int kMPer = 8;                       // launches per thread (matching)
 constexpr int kAPer = 8;                      // launches per lane (aggregation)
 constexpr int kAHalf = 8;                      // of them in registers at a time
 constexpr int kAThreads = 256;                 // threads per block
@@ -81,7 +80,7 @@ __device__ __forceinline__ void store_n(T *p, int64_t i, int nv, const T (&o)[kN
 }
 
 // ---------------------------------------------------------------------------
-// 1. matches
+// matches
 // ---------------------------------------------------------------------------
 struct MatchParams {
   int64_t T;
@@ -95,28 +94,30 @@ struct MatchParams {
   opattr_diag *diag;
 };
 
-__global__ void __launch_bounds__(256) k_f_match(MatchParams a) {
-  const int64_t ib = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kMPer;
-  const int nv = (int)(a.T - ib < 0 ? 0 : (a.T - ib < kMPer ? a.T - ib : kMPer));
-  uint32_t sq[kMPer], nm[kMPer];
-  int32_t pt[kMPer];
-  load_n<kMPer>(a.seq, ib, nv, sq);
-  load_n<kMPer>(a.name, ib, nv, nm);
-  if (a.part) load_n<kMPer>(a.part, ib, nv, pt);
+// The matches of kN consecutive launches from i (nv of them exist), stored to
+// a.match; dedup errors are added to err.
+template <int kN>
+__device__ __forceinline__ void match_of(const MatchParams &a, int64_t i, int nv,
+                                         int32_t (&mt)[kN], uint32_t &err) {
+  uint32_t sq[kN], nm[kN];
+  int32_t pt[kN];
+  load_n<kN>(a.seq, i, nv, sq);
+  load_n<kN>(a.name, i, nv, nm);
+  if (a.part) load_n<kN>(a.part, i, nv, pt);
   else
 #pragma unroll
-    for (int k = 0; k < kMPer; ++k) pt[k] = -1;
-  PartRec rc[kMPer];
+    for (int k = 0; k < kN; ++k) pt[k] = -1;
+  PartRec rc[kN];
 #pragma unroll
-  for (int k = 0; k < kMPer; ++k) {
+  for (int k = 0; k < kN; ++k) {
     const bool ok = k < nv && nm[k] < a.NN && (int64_t)sq[k] < a.T && pt[k] >= -1 &&
                     (pt[k] < 0 || (uint32_t)pt[k] < a.NP);
     rc[k] = PartRec{0, ok ? kRecEligible : kRecNone};
     if (ok && pt[k] >= 0) rc[k] = a.prec[pt[k]];
   }
-  uint32_t src[kMPer], dup = 0, err = 0;
+  uint32_t src[kN], dup = 0;
 #pragma unroll
-  for (int k = 0; k < kMPer; ++k) {
+  for (int k = 0; k < kN; ++k) {
     const uint32_t hi = rc[k].hi;
     src[k] = kNoSrc;
     if (hi == kRecEligible) {
@@ -131,30 +132,27 @@ __global__ void __launch_bounds__(256) k_f_match(MatchParams a) {
       }
     }
   }
-  int32_t mt[kMPer];
-  uint32_t sn[kMPer];
+  uint32_t sn[kN];
 #pragma unroll
-  for (int k = 0; k < kMPer; ++k) {
+  for (int k = 0; k < kN; ++k) {
     mt[k] = src[k] != kNoSrc ? a.mbs[src[k]] : -1;
     sn[k] = ((dup >> k) & 1u) ? a.nbs[src[k]] : 0u;
   }
 #pragma unroll
-  for (int k = 0; k < kMPer; ++k)
+  for (int k = 0; k < kN; ++k)
     if (((dup >> k) & 1u) && sn[k] != nm[k]) {
       mt[k] = -1;
       err++;
     }
-  store_n<kMPer>(a.match, ib, nv, mt);
-  const unsigned long long e = wave_reduce_add((unsigned long long)err);
-  if (lane_id() == 0 && e) atomicAdd((unsigned long long *)&a.diag->dedup_errors, e);
+  store_n<kN>(a.match, i, nv, mt);
 }
 
 // ---------------------------------------------------------------------------
-// 2. runs
+// 1. runs
 // ---------------------------------------------------------------------------
 struct AggParams {
   int64_t T;
-  const int32_t *match;
+  MatchParams m;            // the matching's inputs; m.match is written here
   const int32_t *range_id;  // innermost (or walked) range, input index, or -1
   const uint32_t *op_in;    // op id of each input range
   int64_t R_in;
@@ -251,6 +249,27 @@ __device__ __forceinline__ uint32_t row_of(const AggParams &a, int32_t rid) {
   return g;
 }
 
+// The operator rows of kN launches: every gather is issued before the first
+// is used (an out-of-range id reads entry 0 and is replaced afterwards), so
+// their latencies overlap instead of adding up.
+template <int kN>
+__device__ __forceinline__ void rows_of(const AggParams &a, const int32_t (&rid)[kN], int nh,
+                                        uint32_t (&g)[kN]) {
+  if (a.R_in > 0) {
+    uint32_t o[kN];
+#pragma unroll
+    for (int k = 0; k < kN; ++k) o[k] = a.op_in[(rid[k] >= 0 && rid[k] < a.R_in) ? rid[k] : 0];
+#pragma unroll
+    for (int k = 0; k < kN; ++k) {
+      const bool ok = rid[k] >= 0 && rid[k] < a.R_in && o[k] < a.NOPS;
+      g[k] = k < nh ? (ok ? o[k] : a.NOPS) : 0xFFFFFFFFu;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < kN; ++k) g[k] = k < nh ? a.NOPS : 0xFFFFFFFFu;
+  }
+}
+
 template <bool DEF>  // DEF: the default aggregation kinds
 __global__ void __launch_bounds__(kAThreads) __attribute__((amdgpu_waves_per_eu(3)))
 k_f_agg(AggParams a) {
@@ -275,17 +294,17 @@ k_f_agg(AggParams a) {
   uint32_t gprev = 0xFFFFFFFFu;
   if (ln > 0 && nv > 0) gprev = row_of(a, a.range_id[ib - 1]);
   uint32_t gcur = 0xFFFFFFFFu;
+  uint32_t err = 0;  // dedup errors of the lane's launches
 #pragma unroll 1
   for (int h = 0; h < kAPer / kAHalf; ++h) {
     const int64_t i0 = ib + h * kAHalf;
     const int nh = nv - h * kAHalf < 0 ? 0 : (nv - h * kAHalf < kAHalf ? nv - h * kAHalf : kAHalf);
     int32_t mt[kAHalf], rid[kAHalf];
     uint32_t du[kAHalf], g[kAHalf];
-    load_n<kAHalf>(a.match, i0, nh, mt);
+    match_of<kAHalf>(a.m, i0, nh, mt, err);
     load_n<kAHalf>(in.dur, i0, nh, du);
     load_n<kAHalf>(a.range_id, i0, nh, rid);
-#pragma unroll
-    for (int k = 0; k < kAHalf; ++k) g[k] = k < nh ? row_of(a, rid[k]) : 0xFFFFFFFFu;
+    rows_of<kAHalf>(a, rid, nh, g);
 #pragma unroll
     for (int k = 0; k < kAHalf; ++k) {
       const int kk = h * kAHalf + k;
@@ -341,6 +360,10 @@ k_f_agg(AggParams a) {
   stage_put(nv > 0 && (ln == OPA_WAVE - 1 || nvn == 0 || hmn != 0), gcur, inc, wslot, nst, a.acc,
             mx);
   if (ln == 0) nslot[w] = nst;
+  {
+    const unsigned long long e = wave_reduce_add((unsigned long long)err);
+    if (ln == 0 && e) atomicAdd((unsigned long long *)&a.m.diag->dedup_errors, e);
+  }
   for (int q = tid; q < kBuckets; q += kAThreads) hist[q] = 0;
   for (int q = tid; q < kHash; q += kAThreads) {
     hkey[q] = 0u;
@@ -420,7 +443,7 @@ k_f_agg(AggParams a) {
 }
 
 // ---------------------------------------------------------------------------
-// 3. per bucket: the kept partials of a share of the blocks, added in LDS
+// 2. per bucket: the kept partials of a share of the blocks, added in LDS
 // ---------------------------------------------------------------------------
 struct CombParams {
   int64_t nblocks;
@@ -608,10 +631,12 @@ void clear_fused_acc(void *ws, const Plan &pl, hipStream_t s) {
 
 size_t fused_acc_bytes(uint32_t G) { return (size_t)G * sizeof(PartRow); }
 
-void run_fused_match(const FusedIn &x, hipStream_t s) {
+void run_fused_agg(const FusedIn &x, hipStream_t s) {
   const Plan &pl = *x.pl;
-  if (pl.T <= 0) return;
-  MatchParams m{};
+  const uint32_t rb = fused_rows_per_bucket(pl.G);
+  AggParams a{};
+  a.T = pl.T;
+  MatchParams &m = a.m;
   m.T = pl.T;
   m.seq = x.k->seq;
   m.name = x.k->name_id;
@@ -624,18 +649,6 @@ void run_fused_match(const FusedIn &x, hipStream_t s) {
   m.nbs = at<uint32_t>(x.ws, pl.nbs);
   m.match = x.match;
   m.diag = x.diag;
-  probe_begin(OPATTR_PROBE_DEDUP, s);
-  const int64_t threads = (pl.T + kMPer - 1) / kMPer;
-  k_f_match<<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(m);
-  probe_end(OPATTR_PROBE_DEDUP, s);
-}
-
-void run_fused_agg(const FusedIn &x, hipStream_t s) {
-  const Plan &pl = *x.pl;
-  const uint32_t rb = fused_rows_per_bucket(pl.G);
-  AggParams a{};
-  a.T = pl.T;
-  a.match = x.match;
   a.range_id = x.range_id;
   a.op_in = x.r->op_id;
   a.R_in = x.r->n;

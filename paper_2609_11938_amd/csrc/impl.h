@@ -316,11 +316,10 @@ struct FusedIn {
   void *ws;
   const Plan *pl;
 };
-// match of every launch from the bucket path's mbs / nbs (and the dedup
-// errors)
-void run_fused_match(const FusedIn &x, hipStream_t s);
-// the operator table from match and range_id, with the summary's per-block
-// sums in sumpart (the row accumulators must be zero: clear_fused_acc)
+// every launch's match (from the bucket path's mbs / nbs, with the dedup
+// broadcast and its errors) and the operator table from it and range_id,
+// with the summary's per-bucket sums in sumpart (the row accumulators must
+// be zero: clear_fused_acc)
 void run_fused_agg(const FusedIn &x, hipStream_t s);
 void clear_fused_acc(void *ws, const Plan &pl, hipStream_t s);
 int fused_sum_blocks(const Plan &pl);
