@@ -275,19 +275,23 @@ __device__ __forceinline__ int64_t edge_candidate(const TlArgs &a, int64_t t) {
   return c;
 }
 
-// Input index of the launch at position e of tile t's segment order (or -1).
-__device__ __forceinline__ int32_t seg_elem(const SegTable &sm, uint32_t e, int64_t T) {
+// Input index of each of the thread's elements c * 256 + tid of tile t's
+// segment order (or -1). They ascend by 256, so their segment only moves
+// forward: a step per segment boundary passed instead of a search for each.
+template <int kN>
+__device__ __forceinline__ void seg_elems(const SegTable &sm, int64_t T, int32_t (&ii)[kN]) {
   const uint32_t total = sm.pre[OPA_WAVE] < OPA_TILE ? sm.pre[OPA_WAVE] : OPA_TILE;
-  if (e >= total) return -1;
-  int lo = 0, hi = OPA_WAVE;  // last segment with pre <= e
+  int sgi = 0;  // last segment with pre <= e
 #pragma unroll
-  for (int st = 0; st < 6; ++st) {
-    const int mid = (lo + hi) >> 1;
-    if (sm.pre[mid] <= e) lo = mid;
-    else hi = mid;
+  for (int c = 0; c < kN; ++c) {
+    const uint32_t e = (uint32_t)(c * OPA_TILE_THREADS + threadIdx.x);
+    ii[c] = -1;
+    if (e < total) {
+      while (sgi < OPA_WAVE - 1 && sm.pre[sgi + 1] <= e) ++sgi;
+      const int64_t i = (int64_t)sm.lo[sgi] + (e - sm.pre[sgi]);
+      ii[c] = i < T ? (int32_t)i : -1;
+    }
   }
-  const int64_t i = (int64_t)sm.lo[lo] + (e - sm.pre[lo]);
-  return i < T ? (int32_t)i : -1;
 }
 
 // Fill TileData for seq tile t from its segments. Ends with a barrier. The
@@ -306,9 +310,7 @@ __device__ inline uint32_t seg_tile(const TlArgs &a, int64_t t, TileData &sm) {
   int32_t ii[kWaveChunks];
   uint32_t sq[kWaveChunks], nm[kWaveChunks];
   int32_t pt[kWaveChunks];
-#pragma unroll
-  for (int c = 0; c < kWaveChunks; ++c)
-    ii[c] = seg_elem(sm.sg, (uint32_t)(c * OPA_TILE_THREADS + tid), a.T);
+  seg_elems<kWaveChunks>(sm.sg, a.T, ii);
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
     sq[c] = ii[c] >= 0 ? a.seq[ii[c]] : 0u;
@@ -515,11 +517,14 @@ k_tl_look(TlArgs a, LookArgs m) {
   int32_t ii[kWaveChunks];
   uint32_t xs[kWaveChunks], nm[kWaveChunks];
   int32_t pt[kWaveChunks];
+  if (SEG) {
+    seg_elems<kWaveChunks>(sm, a.T, ii);
+  } else {
 #pragma unroll
-  for (int c = 0; c < kWaveChunks; ++c) {
-    const uint32_t e = (uint32_t)(c * OPA_TILE_THREADS + tid);
-    if (SEG) ii[c] = seg_elem(sm, e, a.T);
-    else ii[c] = base + e < a.T ? a.sv[base + e] : -1;
+    for (int c = 0; c < kWaveChunks; ++c) {
+      const uint32_t e = (uint32_t)(c * OPA_TILE_THREADS + tid);
+      ii[c] = base + e < a.T ? a.sv[base + e] : -1;
+    }
   }
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
