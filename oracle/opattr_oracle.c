@@ -148,19 +148,17 @@ int oref_match(const oref_kernels *k, const oref_profiled *p, const oref_dims *d
     free(all);
   }
 
-  /* Alg. 1: counter[name] = invocations seen so far; the i-th invocation of a
-     name takes the i-th profiled row of that name; once the rows run out the
-     kernel gets none (warn and continue, counter not advanced) */
-  int64_t *counter = xcalloc(NN, sizeof(int64_t));
+  /* The matching of Alg. 1 as a definition: the launch of rank r among the
+     eligible launches of its name, in launch order, takes that name's
+     profiled row of rank r (replay order); a name with fewer rows than
+     launches leaves its launches of rank >= its row count unmatched.
+     tl_cnt[name] ends as the name's launch count. */
   int64_t *tl_cnt = xcalloc(NN, sizeof(int64_t));
   for (int64_t x = 0; x < ne; ++x) {
-    int64_t i = ord[x].idx;
-    uint32_t n = k->name_id[i];
-    tl_cnt[n]++;
-    int64_t c = counter[n];
-    if (c >= pf_cnt[n]) continue; /* invocation count mismatch: skip */
-    match[i] = (int32_t)rows[pf_off[n] + c];
-    counter[n] = c + 1;
+    const int64_t i = ord[x].idx;
+    const uint32_t n = k->name_id[i];
+    const int64_t r = tl_cnt[n]++; /* rank of launch i within its name */
+    if (r < pf_cnt[n]) match[i] = (int32_t)rows[pf_off[n] + r];
   }
 
   /* count validation (Sec. 3.3 text, limitations paragraph) */
@@ -185,8 +183,7 @@ int oref_match(const oref_kernels *k, const oref_profiled *p, const oref_dims *d
     }
   if (diag->bad_records) diag->flags |= OREF_F_DATA;
 
-  free(pf_cnt); free(pf_off); free(rows); free(fill); free(ord); free(counter);
-  free(tl_cnt);
+  free(pf_cnt); free(pf_off); free(rows); free(fill); free(ord); free(tl_cnt);
   return 0;
 }
 

@@ -577,6 +577,33 @@ def _assert_rows(got, want, rtol):
                 assert abs(x - y) <= rtol * max(abs(x), abs(y)), (x, y)
 
 
+def golden_kinds():
+    """The Agg. column of the counter reference table (tests/golden)."""
+    code = {"SUM": O.SUM, "DW-mean": O.DWMEAN, "MAX": O.MAX}
+    rows = [ln.split() for ln in open(os.path.join(GOLD, "counter_agg.txt"))
+            if ln.strip() and not ln.startswith("#")]
+    assert [int(r[0]) for r in rows] == list(range(1, 21))
+    return np.array([code[r[2]] for r in rows], np.uint8)
+
+
+def test_default_kinds_are_the_counter_table():
+    """The default aggregation kinds equal the transcribed Agg. column: the
+    Python constant, the brute-force copy, and the C oracle's own table
+    (the default gives the same table as passing the column explicitly, and
+    a different one as soon as any single counter's kind changes)."""
+    want = golden_kinds()
+    np.testing.assert_array_equal(O.DEFAULT_KIND, want)
+    np.testing.assert_array_equal(np.array(brute.DEFAULT_KIND, np.uint8), want)
+    tr = cases.random_trace(31, T=400, R=60, n_ops=9, t_max=500)
+    base = O.attribute(tr)["table"]
+    same = O.attribute(tr, agg_kind=want)["table"]
+    assert base.tobytes() == same.tobytes()
+    for c in range(20):
+        k = want.copy()
+        k[c] = (k[c] + 1) % 3
+        assert O.attribute(tr, agg_kind=k)["table"].tobytes() != base.tobytes(), c
+
+
 def test_single_kernel_identity_from_profile_excerpt():
     """The appendix excerpt: one kernel attributed to aten::mm_26 gives
     kernel_count 1, total_duration_ns = its duration, and every aggregated

@@ -17,7 +17,9 @@ SRC = open(O.SRC).read()
 
 MUTANTS = {
     "iom_descending_seq": ("ord[ne].a = k->seq[i];", "ord[ne].a = UINT32_MAX - k->seq[i];"),
-    "iom_counter_not_advanced": ("counter[n] = c + 1;", "counter[n] = c;"),
+    "iom_rank_not_advanced": ("const int64_t r = tl_cnt[n]++;", "const int64_t r = 0 * tl_cnt[n]++;"),
+    "iom_rank_off_by_one": ("if (r < pf_cnt[n]) match[i] = (int32_t)rows[pf_off[n] + r];",
+                            "if (r + 1 < pf_cnt[n]) match[i] = (int32_t)rows[pf_off[n] + r + 1];"),
     "iom_skip_name_ignored": ("if (tl_cnt[n] != pf_cnt[n]) match[i] = -1;",
                               "if (0) match[i] = -1;"),
     "dedup_reversed_position": ("int64_t src = mem[off[r] + pos].idx;",
