@@ -537,3 +537,18 @@ def test_enclose_all_generated(cfg):
     want = O.enclose_all(tr)
     out = opattr.opattr_enclose_all(opattr.to_device(tr, DEV), flags=HINTS)
     _assert_all(out, want)
+
+
+@pytest.mark.parametrize("emission", ["stream_major", "seq"])
+def test_default_kinds_are_the_counter_table(emission):
+    """The library's default aggregation kinds equal the transcribed Agg.
+    column of the counter reference table: passing the column explicitly
+    gives the default's table (stream_major: the fused path; seq: the
+    general one)."""
+    import test_oracle
+
+    tr = tg.generate("lstm" if emission == "stream_major" else "gpt2", emission=emission)
+    flags = HINTS if emission == "stream_major" else opattr.SEQ_DENSE
+    a, _ = _run(tr, flags=flags)
+    b, _ = _run(tr, flags=flags, agg_kind=test_oracle.golden_kinds())
+    parity.assert_table(a.table_host(), b.table_host(), rtol=1e-12)

@@ -383,3 +383,39 @@ def test_attribute_tiered_at_path_boundaries(n_names, n_ops):
     for f in ("tier", "op", "fused"):
         np.testing.assert_array_equal(parity.host(out[f]), t[f], err_msg=f)
     parity.assert_table(out.table_host(), agg["table"])
+
+
+@pytest.mark.parametrize("side", ["profiled", "corr"])
+@pytest.mark.parametrize("policy,corr_policy", [(0, 2), (2, 1), (2, 2), (1, 0)])
+def test_attribute_tiered_policy_mix(side, policy, corr_policy):
+    """The two matchings of the one-call tiered attribution under different
+    count policies, with a count mismatch in the correlation map (entries
+    missing at the end of some names) and, or not, in the profiled rows
+    (missing rows): outputs
+    as the oracle's stages, the count diagnostics of both matchings added up,
+    and COUNT_MISMATCH exactly when either policy is STRICT and either side
+    has a mismatch."""
+    import torch
+
+    print(f"case tiered policy mix side={side} policy={policy} corr={corr_policy}", flush=True)
+    tr = cases.random_trace(901, T=3000, S=2, n_names=12, R=400, n_ops=30, t_max=6000,
+                            max_depth=4, drop=0.1 if side == "profiled" else 0.0)
+    tr = tg.with_attribution_maps(cases.with_kinds(tr, 1), seed=3, p_corr=0.6,
+                                  p_mismatch=0.4 if side == "corr" else 0.0, p_none=0.1,
+                                  p_fmap=0.4)
+    att = O.attribute(tr, policy=policy, stages=["match", "dedup"])
+    t = O.tiers(tr, corr_policy=corr_policy)
+    assert bool(att["diag"]["flags"] & O.F_COUNT) == (side == "profiled")
+    assert bool(t["diag"]["flags"] & O.F_COUNT)
+    out = opattr.opattr_attribute_tiered(opattr.to_device(tr, DEV), policy=policy,
+                                         corr_policy=corr_policy)
+    torch.cuda.synchronize()
+    diag = opattr.read_diag(out["diag"])
+    np.testing.assert_array_equal(parity.host(out["match"]), att["match"])
+    for f in ("tier", "op", "fused"):
+        np.testing.assert_array_equal(parity.host(out[f]), t[f], err_msg=f)
+    for f in ("names_mismatched", "tl_unmatched", "pf_unmatched"):
+        assert diag[f] == att["diag"][f] + t["diag"][f], f
+    strict = opattr.MISMATCH_STRICT in (policy, corr_policy)
+    assert (diag["status"] == -4) == strict, diag
+    assert bool(diag["flags"] & O.F_COUNT)
