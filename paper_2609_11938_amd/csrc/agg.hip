@@ -563,8 +563,8 @@ void plan_items(const EncArgs &x, hipStream_t s) {
   if (pl.G <= kFastKeys) {
     const size_t lds = (size_t)4 * pl.G * sizeof(uint16_t);
     const unsigned tgrid = (unsigned)(pl.ntrt < 1024 ? (pl.ntrt > 0 ? pl.ntrt : 1) : 1024);
-    // gcnt (and meta when there are no launches) were cleared with the
-    // look-back states
+    // gcnt (and meta when there are no launches) were cleared before the
+    // enclosure pass counted the items
     if (pl.T > 0) {
       k_item_hist_w<<<tgrid, 256, lds, s>>>(w);
       column_scan(w.ith, pl.ntrt, pl.G, at<uint32_t>(x.ws, pl.itch), w.gcnt, s, w.meta + 2);
