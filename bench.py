@@ -181,22 +181,24 @@ def copy_bandwidth(mib=1024, reps=10):
 
 
 def clocks():
-    """Current SCLK / MCLK as rocm-smi reports them (None when unavailable)."""
-    import subprocess
+    """Current SCLK / MCLK levels as the driver lists them in sysfs (the line
+    marked '*' of pp_dpm_sclk / pp_dpm_mclk), or None when unavailable. Read
+    from files: no child process is started from this GPU process."""
+    import glob
 
-    try:
-        r = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True,
-                           text=True, timeout=30)
-        data = json.loads(r.stdout)
-    except Exception:  # noqa: BLE001 - the record is optional
-        return None
-    card = next(iter(data.values()), {}) if isinstance(data, dict) else {}
     out = {}
-    for k, v in card.items():
-        kl = k.lower()
-        if "sclk" in kl or "mclk" in kl:
-            out[k] = v
-    return out or None
+    for dev in sorted(glob.glob("/sys/class/drm/card*/device")):
+        for clk in ("sclk", "mclk"):
+            try:
+                with open(os.path.join(dev, f"pp_dpm_{clk}")) as fh:
+                    cur = [ln.strip() for ln in fh if ln.strip().endswith("*")]
+            except OSError:
+                continue
+            if cur:
+                out[clk] = cur[0].rstrip("*").strip()
+        if out:
+            return out
+    return None
 
 
 def cpu_info():
