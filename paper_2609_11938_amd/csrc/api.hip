@@ -119,7 +119,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.tmx2 = b.take(ntr * 8);
   pl.tfirst = b.take(ntr * 4);
   pl.tlast = b.take(ntr * 4);
-  pl.sflag = b.take(pl.NS);
+  pl.sflag = b.take((size_t)sflag_words(pl.NS) * 4);
   // aggregation: items (at most one per launch), partial rows (at most
   // kEncRowsPerWave per 64 * 8 launches), windows of 64 sorted items
   pl.cap_items = pl.T;
@@ -223,62 +223,11 @@ __global__ void __launch_bounds__(256) k_summary_part(const opattr_op_row *table
         red[threadIdx.x][0] + red[threadIdx.x][1] + red[threadIdx.x][2] + red[threadIdx.x][3];
 }
 
-// nesting_errors from the per-stream crossing flags; status from the flags;
-// with a table, the summary from the per-block sums (one block)
+// the finalisation by one block (body in common.h)
 __global__ void __launch_bounds__(1024) k_finish(opattr_diag *diag, const uint8_t *sflag,
                                                  uint32_t ns, const unsigned long long *part,
                                                  int nparts, opattr_summary *sum) {
-  __shared__ uint32_t cnt;
-  __shared__ unsigned long long tot[4];
-  if (threadIdx.x < 4) tot[threadIdx.x] = 0;
-  if (threadIdx.x == 0) cnt = 0;
-  __syncthreads();
-  if (sflag) {
-    uint32_t c = 0;
-    for (uint32_t s = threadIdx.x; s < ns; s += blockDim.x) c += sflag[s] ? 1u : 0u;
-    if (c) atomicAdd(&cnt, c);
-  }
-  // the per-block sums, one block's four per thread (integer sums: exact in
-  // any order)
-  if (part) {
-    unsigned long long v[4] = {0, 0, 0, 0};
-    for (int b = threadIdx.x; b < nparts; b += blockDim.x)
-#pragma unroll
-      for (int f = 0; f < 4; ++f) v[f] += part[b * 4 + f];
-#pragma unroll
-    for (int f = 0; f < 4; ++f) {
-      const unsigned long long x = wave_reduce_add(v[f]);
-      if (lane_id() == 0 && x) atomicAdd(&tot[f], x);
-    }
-  }
-  __syncthreads();
-  if (threadIdx.x == 0 && part) {
-    opattr_summary s{};
-    s.attributed_ns = tot[0];
-    s.unattributed_ns = tot[1];
-    s.total_ns = tot[2];
-    s.matched_ns = tot[3];
-    s.attributed_fraction = s.total_ns ? (double)s.attributed_ns / (double)s.total_ns
-                                       : __longlong_as_double(0x7FF8000000000000ll);
-    *sum = s;
-  }
-  if (threadIdx.x == 0) {
-    if (sflag) diag->nesting_errors = cnt;
-    uint32_t f = diag->flags;
-    if (diag->nesting_errors) f |= OPATTR_F_NOT_NESTED;
-    if (diag->bad_records) f |= OPATTR_F_DATA;
-    if (diag->dedup_errors) f |= OPATTR_F_DEDUP;
-    diag->flags = f;
-    int32_t st = 0;
-    if (f & OPATTR_F_DATA) st = OPATTR_ERR_DATA;
-    else if (f & OPATTR_F_ORDER) st = OPATTR_ERR_ORDER;
-    else if (f & OPATTR_F_LIMIT) st = OPATTR_ERR_LIMIT;
-    else if (f & OPATTR_F_NOT_NESTED) st = OPATTR_ERR_NOT_NESTED;
-    else if (f & OPATTR_F_PARTITION) st = OPATTR_ERR_PARTITION;
-    else if (f & OPATTR_F_DEDUP) st = OPATTR_ERR_DEDUP;
-    else if ((f & OPATTR_F_COUNT) && diag->strict) st = OPATTR_ERR_COUNT_MISMATCH;
-    diag->status = st;
-  }
+  finish_block(diag, sflag, ns, part, nparts, sum);
 }
 
 void launch_finish(opattr_diag *diag, const uint8_t *sflag, uint32_t ns, hipStream_t s,
@@ -508,7 +457,7 @@ int opattr_enclose_walk(const opattr_kernels *k, const opattr_ranges *r, const o
   check_kernel_layout(k, d, diag, s);
   const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
   const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s);
-  resolve_ranges(cr, d, ws, pl, range_depth, diag, s);
+  resolve_ranges(cr, d, ws, pl, range_depth, diag, s, true);
   write_range_parents(cr, ws, pl, range_parent, s);
   EncArgs e{};
   e.k = k;
@@ -520,6 +469,8 @@ int opattr_enclose_walk(const opattr_kernels *k, const opattr_ranges *r, const o
   e.diag = diag;
   e.ws = ws;
   e.pl = &pl;
+  e.depth = true;
+  e.range_depth = range_depth;
   run_enclose(e, s);
   launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s);
   return launch_status();
@@ -605,10 +556,11 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
     note(hipEventRecord(ss->fork, s));
     note(hipStreamWaitEvent(s2, ss->fork, 0));
   }
-  clear_fused_acc(ws, pl, s2);
+  FillJobs acc;  // the fused aggregation's accumulators, cleared with the ranges' state
+  fused_acc_clear(acc, ws, pl);
   probe_begin(OPATTR_PROBE_RANGES, s2);
-  const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, false, s2);
-  resolve_ranges(cr, d, ws, pl, range_depth, diag, s2);
+  const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, false, s2, &acc);
+  resolve_ranges(cr, d, ws, pl, range_depth, diag, s2, true);
   probe_end(OPATTR_PROBE_RANGES, s2);
   EncArgs e{};
   e.k = k;
@@ -624,6 +576,8 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
   e.diag = diag;
   e.ws = ws;
   e.pl = &pl;
+  e.depth = true;
+  e.range_depth = range_depth;
   run_enclose(e, s2);
   if (ss) note(hipEventRecord(ss->join, s2));
   IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, false};
@@ -648,9 +602,8 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
   f.ws = ws;
   f.pl = &pl;
   if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
-  run_fused_agg(f, s);
-  launch_finish(diag, at<uint8_t>(ws, pl.sflag), d->n_streams, s, table, sum, pl.G, d->n_ops,
-                at<unsigned long long>(ws, pl.sumpart), fused_sum_blocks(pl));
+  f.sum = sum;
+  run_fused_agg(f, s);  // ends with the finalisation
   return launch_status();
 }
 
@@ -879,7 +832,7 @@ int opattr_attribute_tiered(const opattr_kernels *k, const opattr_profiled *p,
   }
   probe_begin(OPATTR_PROBE_RANGES, s2);
   const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s2);
-  resolve_ranges(cr, d, ws, pl, nullptr, diag, s2);
+  resolve_ranges(cr, d, ws, pl, nullptr, diag, s2, true);
   probe_end(OPATTR_PROBE_RANGES, s2);
   EncArgs w{};
   w.k = k;
@@ -890,6 +843,7 @@ int opattr_attribute_tiered(const opattr_kernels *k, const opattr_profiled *p,
   w.diag = diag;
   w.ws = ws;
   w.pl = &pl;
+  w.depth = true;
   run_enclose(w, s2);
   if (ss) note(hipEventRecord(ss->join, s2));
   // matching with the dedup broadcast, then the correlation lookup (Alg. 1

@@ -270,4 +270,119 @@ __device__ __forceinline__ void diag_add(unsigned long long *p, unsigned long lo
   if (v) atomicAdd(p, v);
 }
 
+
+// blk[s] = first position with stream >= s in st[0..n) (sorted by stream);
+// called by one whole wave: each round, the 64 lanes probe 64 evenly spaced
+// positions and the range shrinks to the gap where the answer lies.
+__device__ inline void stream_block_wave(const uint16_t *st, int64_t n, uint32_t s, int64_t *blk) {
+  const int ln = lane_id();
+  int64_t lo = 0, hi = n;  // answer in [lo, hi]
+  while (hi - lo > OPA_WAVE) {
+    const int64_t step = (hi - lo + OPA_WAVE - 1) / OPA_WAVE;
+    int64_t p = lo + (int64_t)(ln + 1) * step - 1;
+    if (p > hi - 1) p = hi - 1;
+    const uint64_t m = __ballot(st[p] >= s);
+    if (m == 0) {
+      lo = hi;
+      break;
+    }
+    const int f = __ffsll((unsigned long long)m) - 1;  // first probe at or past s
+    int64_t pf = lo + (int64_t)(f + 1) * step - 1;
+    if (pf > hi - 1) pf = hi - 1;
+    lo = f == 0 ? lo : lo + (int64_t)f * step;
+    hi = pf;  // st[pf] >= s
+  }
+  if (hi - lo <= OPA_WAVE && lo < hi) {
+    const int64_t p = lo + ln;
+    const uint64_t m = __ballot(p < hi && st[p] >= s);
+    lo = m ? lo + __ffsll((unsigned long long)m) - 1 : hi;
+  }
+  if (ln == 0) blk[s] = lo;
+}
+
+// The finalisation, by one block of any size: nesting_errors from the
+// per-stream crossing flags; with part, the summary from the per-block sums;
+// then the flags and the status from every stage's diagnostics
+__device__ inline void finish_block(opattr_diag *diag, const uint8_t *sflag, uint32_t ns,
+                                    const unsigned long long *part, int nparts,
+                                    opattr_summary *sum) {
+  __shared__ uint32_t cnt;
+  __shared__ unsigned long long tot[4];
+  if (threadIdx.x < 4) tot[threadIdx.x] = 0;
+  if (threadIdx.x == 0) cnt = 0;
+  __syncthreads();
+  if (sflag) {
+    uint32_t c = 0;
+    for (uint32_t s = threadIdx.x; s < ns; s += blockDim.x) c += sflag[s] ? 1u : 0u;
+    if (c) atomicAdd(&cnt, c);
+  }
+  // the per-block sums, one block's four per thread (integer sums: exact in
+  // any order)
+  if (part) {
+    unsigned long long v[4] = {0, 0, 0, 0};
+    for (int b = threadIdx.x; b < nparts; b += blockDim.x)
+#pragma unroll
+      for (int f = 0; f < 4; ++f) v[f] += part[b * 4 + f];
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+      const unsigned long long x = wave_reduce_add(v[f]);
+      if (lane_id() == 0 && x) atomicAdd(&tot[f], x);
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0 && part) {
+    opattr_summary s{};
+    s.attributed_ns = tot[0];
+    s.unattributed_ns = tot[1];
+    s.total_ns = tot[2];
+    s.matched_ns = tot[3];
+    s.attributed_fraction = s.total_ns ? (double)s.attributed_ns / (double)s.total_ns
+                                       : __longlong_as_double(0x7FF8000000000000ll);
+    *sum = s;
+  }
+  if (threadIdx.x == 0) {
+    if (sflag) diag->nesting_errors = cnt;
+    uint32_t f = diag->flags;
+    if (diag->nesting_errors) f |= OPATTR_F_NOT_NESTED;
+    if (diag->bad_records) f |= OPATTR_F_DATA;
+    if (diag->dedup_errors) f |= OPATTR_F_DEDUP;
+    diag->flags = f;
+    int32_t st = 0;
+    if (f & OPATTR_F_DATA) st = OPATTR_ERR_DATA;
+    else if (f & OPATTR_F_ORDER) st = OPATTR_ERR_ORDER;
+    else if (f & OPATTR_F_LIMIT) st = OPATTR_ERR_LIMIT;
+    else if (f & OPATTR_F_NOT_NESTED) st = OPATTR_ERR_NOT_NESTED;
+    else if (f & OPATTR_F_PARTITION) st = OPATTR_ERR_PARTITION;
+    else if (f & OPATTR_F_DEDUP) st = OPATTR_ERR_DEDUP;
+    else if ((f & OPATTR_F_COUNT) && diag->strict) st = OPATTR_ERR_COUNT_MISMATCH;
+    diag->status = st;
+  }
+}
+
+// Depth of range x in nesting order (length of its parent chain: 1 for a
+// root, 0 for a bad range, ree < 0) into range_depth by input position (perm,
+// or x without one); a chain longer than 255 sets the LIMIT flag. Called by
+// whole waves.
+__device__ inline void range_depth_one(const int32_t *npg, const int64_t *ree, const uint16_t *st,
+                                       const int32_t *perm, int64_t n, uint32_t NS, int64_t x,
+                                       uint8_t *range_depth, opattr_diag *diag) {
+  bool lim = false;
+  if (x < n) {
+    int d = 0;
+    int32_t y = (int32_t)x;
+    while (y >= 0 && d <= 255) {
+      ++d;
+      y = npg[y];
+    }
+    lim = y >= 0;
+    const bool ok = ree[x] >= 0 && st[x] < NS;
+    if (range_depth) {
+      const int64_t o = perm ? perm[x] : x;
+      range_depth[o] = ok ? (uint8_t)(d > 255 ? 255 : d) : 0;
+    }
+    lim = lim && ok;
+  }
+  if (__ballot(lim) && lane_id() == 0) atomicOr(&diag->flags, OPATTR_F_LIMIT);
+}
+
 }  // namespace opa

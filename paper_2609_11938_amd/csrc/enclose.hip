@@ -54,6 +54,9 @@ struct EncParams {
   AggIn ag;
   EmitOut em;
   opattr_diag *diag;
+  // blocks [nenc, grid) write the range depths instead, 256 ranges a block
+  int64_t nenc;
+  uint8_t *range_depth;
 };
 
 // first index in [lo, hi) with a[idx] > x (or hi); called by a whole wave
@@ -181,6 +184,11 @@ k_enclose(EncParams a) {
   __shared__ uint64_t red[2][kEncThreads / OPA_WAVE];
   __shared__ int64_t win[2];
   __shared__ uint32_t sbad;
+  if ((int64_t)blockIdx.x >= a.nenc) {
+    const int64_t x = ((int64_t)blockIdx.x - a.nenc) * kEncThreads + threadIdx.x;
+    range_depth_one(a.npg, a.ree, a.cr.st, a.cr.perm, a.cr.n, a.NS, x, a.range_depth, a.diag);
+    return;
+  }
   const int tid = threadIdx.x, w = wave_id(), ln = lane_id();
   if (tid == 0) sbad = 0;
   if (MODE == 2) __syncthreads();
@@ -684,6 +692,7 @@ static EncParams enc_params(const EncArgs &x) {
   a.em = emit_out(x.ws, pl);
   a.wfirst = at<int32_t>(x.ws, pl.wfirst);
   a.wfused = at<uint8_t>(x.ws, pl.wfused);
+  a.nenc = pl.nencb;
   return a;
 }
 
@@ -728,14 +737,19 @@ void launch_innermost(const CoreRanges &cr, const opattr_kernels *k, const opatt
   a.npg = at<int32_t>(ws, pl.npg);
   a.core_id = core;
   a.diag = diag;
+  a.nenc = pl.nencb;
   if (pl.T > 0) k_enclose<1><<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
 }
 
 void run_enclose(const EncArgs &x, hipStream_t s) {
   const Plan &pl = *x.pl;
-  const EncParams a = enc_params(x);
+  EncParams a = enc_params(x);
+  a.nenc = pl.T > 0 ? pl.nencb : 0;
+  // the range depths (deferred by resolve_ranges) in blocks of their own
+  const int64_t nd = x.depth && pl.R > 0 && x.d->n_streams > 0 ? (pl.R + kEncThreads - 1) / kEncThreads : 0;
+  a.range_depth = x.range_depth;
   probe_begin(OPATTR_PROBE_MAIN_PASS, s);
-  if (pl.T > 0) k_enclose<1><<<(unsigned)pl.nencb, kEncThreads, 0, s>>>(a);
+  if (a.nenc + nd > 0) k_enclose<1><<<(unsigned)(a.nenc + nd), kEncThreads, 0, s>>>(a);
   probe_end(OPATTR_PROBE_MAIN_PASS, s);
 }
 

@@ -44,6 +44,7 @@ constexpr uint32_t kHash = 256;                // LDS table of a block's rows (>
 
 
 static_assert(kABlockCap <= 255, "bucket offsets fit in a byte");
+static_assert(kBuckets <= kSumBlocks, "one summary partial per bucket fits the summary workspace");
 
 // kN consecutive 32-bit elements from p[i..), 16-byte vector loads when aligned
 template <int kN, typename T>
@@ -455,6 +456,12 @@ struct CombParams {
   const PartRow *acc;          // [G] row accumulators (the blocks' overflow)
   opattr_op_row *table;
   unsigned long long *part;    // [kBuckets][4] summary sums per bucket
+  // the finalisation, by the last block of the per-row reduction to finish
+  uint32_t *done;              // blocks finished (zero at launch)
+  opattr_diag *diag;
+  const uint8_t *sflag;        // [ns] per-stream crossing flags
+  uint32_t ns;
+  opattr_summary *sum;
 };
 
 __device__ __forceinline__ unsigned long long merge_field(int f, unsigned long long x,
@@ -603,6 +610,21 @@ __global__ void __launch_bounds__(256) k_f_rows(CombParams a) {
   }
   __syncthreads();
   if (tid < 4) a.part[q * 4 + tid] = red[tid][0] + red[tid][1] + red[tid][2] + red[tid][3];
+  // the last block to finish reads every block's sums: the wave that wrote
+  // them makes them visible device-wide before it counts the block done, and
+  // in the last block that wave orders the block's reads after the count
+  __shared__ uint32_t last;
+  if (tid < OPA_WAVE) {
+    __threadfence();
+    uint32_t l = 0;
+    if (tid == 0) l = atomicAdd(a.done, 1u) == gridDim.x - 1 ? 1u : 0u;
+    l = __shfl(l, 0);
+    if (l) __threadfence();
+    if (tid == 0) last = l;
+  }
+  __syncthreads();
+  if (!last) return;
+  finish_block(a.diag, a.sflag, a.ns, a.part, (int)gridDim.x, a.sum);
 }
 
 // ---------------------------------------------------------------------------
@@ -622,14 +644,13 @@ size_t fused_split_bytes(uint32_t G) {
   return (size_t)kBuckets * kSplits * fused_rows_per_bucket(G) * sizeof(PartRow);
 }
 
-int fused_sum_blocks(const Plan &) { return kBuckets; }
 
-// the row accumulators
-void clear_fused_acc(void *ws, const Plan &pl, hipStream_t s) {
-  fill_u32(at<uint32_t>(ws, pl.acc), 0u, (int64_t)pl.G * (sizeof(PartRow) / 4), s);
+// the row accumulators, then the per-row reduction's count of finished blocks
+size_t fused_acc_bytes(uint32_t G) { return (size_t)G * sizeof(PartRow) + 256; }
+
+void fused_acc_clear(FillJobs &j, void *ws, const Plan &pl) {
+  j.add(at<uint32_t>(ws, pl.acc), 0u, (int64_t)(fused_acc_bytes(pl.G) / 4));
 }
-
-size_t fused_acc_bytes(uint32_t G) { return (size_t)G * sizeof(PartRow); }
 
 void run_fused_agg(const FusedIn &x, hipStream_t s) {
   const Plan &pl = *x.pl;
@@ -681,6 +702,12 @@ void run_fused_agg(const FusedIn &x, hipStream_t s) {
   c.acc = a.acc;
   c.table = x.table;
   c.part = at<unsigned long long>(x.ws, pl.sumpart);
+  c.done = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(x.ws) + pl.acc +
+                                        (size_t)pl.G * sizeof(PartRow));
+  c.diag = x.diag;
+  c.sflag = at<uint8_t>(x.ws, pl.sflag);
+  c.ns = x.d->n_streams;
+  c.sum = x.sum;
   const size_t lds = (size_t)rb * kFFields * 8;
   if (def) {
     k_f_comb<true><<<kBuckets * kSplits, 64, lds, s>>>(c);

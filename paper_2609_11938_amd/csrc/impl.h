@@ -132,9 +132,10 @@ bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, in
 size_t radix_hist_entries(int64_t n);
 // Several 32-bit fills in one launch (up to 8 arrays).
 struct FillJobs {
-  uint32_t *p[8];
-  uint32_t v[8];
-  int64_t n[8];
+  static constexpr int kMaxJobs = 8;
+  uint32_t *p[kMaxJobs];
+  uint32_t v[kMaxJobs];
+  int64_t n[kMaxJobs];
   int count = 0;
   void add(void *ptr, uint32_t value, int64_t words);
 };
@@ -238,10 +239,18 @@ void launch_dispatch_keys(const int32_t *range_id, const int32_t *op, const opat
                           opattr_diag *diag, hipStream_t s);
 
 // ---- ranges and enclosure (ranges.hip, enclose.hip) ----------------------------
+// nesting order, validity, effective ends and stream blocks of the ranges,
+// with the range stage's clears and the caller's extra clears (extra)
 CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws, const Plan &pl,
-                          opattr_diag *diag, bool validate, hipStream_t s);
+                          opattr_diag *diag, bool validate, hipStream_t s,
+                          const FillJobs *extra = nullptr);
+// parents, crossing flags and depths (defer_depth: the enclosure pass writes
+// the depths, EncArgs::depth)
 void resolve_ranges(const CoreRanges &cr, const opattr_dims *d, void *ws, const Plan &pl,
-                    uint8_t *range_depth, opattr_diag *diag, hipStream_t s);
+                    uint8_t *range_depth, opattr_diag *diag, hipStream_t s,
+                    bool defer_depth = false);
+// words of the per-stream crossing flags (one byte per stream, whole words)
+inline int64_t sflag_words(uint32_t NS) { return (int64_t)NS / 4 + 1; }
 // all enclosing ranges per launch as CSR (off[T + 1] always, ids within cap)
 void run_enclose_all(const CoreRanges &cr, const opattr_kernels *k, const opattr_dims *d, void *ws,
                      const Plan &pl, int64_t *off, int32_t *ids, int64_t cap, opattr_diag *diag,
@@ -278,6 +287,8 @@ struct EncArgs {
   opattr_diag *diag;
   void *ws;
   const Plan *pl;
+  bool depth = false;            // run_enclose also writes the range depths
+  uint8_t *range_depth = nullptr;
 };
 AggIn agg_inputs(const EncArgs &x);
 // range_id of every launch (Alg. 2)
@@ -312,17 +323,18 @@ struct FusedIn {
   const AggIn *in;
   uint32_t absent;
   opattr_op_row *table;
+  opattr_summary *sum;
   opattr_diag *diag;
   void *ws;
   const Plan *pl;
 };
 // every launch's match (from the bucket path's mbs / nbs, with the dedup
-// broadcast and its errors) and the operator table from it and range_id,
-// with the summary's per-bucket sums in sumpart (the row accumulators must
-// be zero: clear_fused_acc)
+// broadcast and its errors), the operator table from it and range_id, the
+// summary and the final status (the row accumulators and the done count must
+// be zero: fused_acc_clear)
 void run_fused_agg(const FusedIn &x, hipStream_t s);
-void clear_fused_acc(void *ws, const Plan &pl, hipStream_t s);
-int fused_sum_blocks(const Plan &pl);
+// the clear of the row accumulators and the done count, as a fill job
+void fused_acc_clear(FillJobs &j, void *ws, const Plan &pl);
 // workspace sizes of the fused aggregation
 size_t fused_parts_bytes(int64_t T);
 size_t fused_bkt_bytes(int64_t T);

@@ -434,6 +434,41 @@ __global__ void k_rep_check(const int32_t *__restrict__ part_rep, uint32_t NP, o
     atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)__popcll(m));
 }
 
+// The matching's first launch on the segment path, three jobs in one grid
+// by block ranges: [0, nf) the clears (fill jobs), [nf, nf + nr) the class
+// map's range check, then one wave per stream s = 0..NS for the storage
+// block of the stream (kblk).
+struct ProArgs {
+  FillJobs fill;
+  int nf, nr;
+  const int32_t *part_rep;  // the class map (nr = 0: none)
+  uint32_t NP;
+  opattr_diag *diag;
+  const uint16_t *st;
+  int64_t T;
+  uint32_t NS;
+  int64_t *kblk;
+};
+
+__global__ void __launch_bounds__(256) k_seg_prologue(ProArgs a) {
+  const int b = blockIdx.x;
+  if (b < a.nf) {
+    const int64_t stride = (int64_t)a.nf * blockDim.x;
+    for (int q = 0; q < a.fill.count; ++q)
+      for (int64_t i = (int64_t)b * blockDim.x + threadIdx.x; i < a.fill.n[q]; i += stride)
+        a.fill.p[q][i] = a.fill.v[q];
+  } else if (b < a.nf + a.nr) {
+    const uint32_t q = (uint32_t)(b - a.nf) * blockDim.x + threadIdx.x;
+    const bool bad = q < a.NP && (a.part_rep[q] < 0 || (uint32_t)a.part_rep[q] >= a.NP);
+    const uint64_t m = __ballot(bad);
+    if (m && lane_id() == __ffsll((unsigned long long)m) - 1)
+      atomicAdd((unsigned long long *)&a.diag->bad_records, (unsigned long long)__popcll(m));
+  } else {
+    const uint32_t sw = (uint32_t)(b - a.nf - a.nr) * (blockDim.x / OPA_WAVE) + wave_id();
+    if (sw <= a.NS) stream_block_wave(a.st, a.T, sw, a.kblk);
+  }
+}
+
 #define OPA_DYN_LDS(T, name) extern __shared__ __align__(16) unsigned char name##_raw[]; \
   T *name = reinterpret_cast<T *>(name##_raw)
 
@@ -656,6 +691,57 @@ __global__ void __launch_bounds__(256) k_f_pass1(TlArgs a, BucketOut o) {
     atomicAdd((unsigned long long *)&o.diag->bad_records, (unsigned long long)sm.bad);
 }
 
+// count validation (Sec. 3.3): per name, eligible launches against rows;
+// run by one block of up to 1024 threads
+__device__ void names_check(const uint32_t *__restrict__ tlc, const uint32_t *__restrict__ pfc,
+                            uint32_t NN, uint32_t *name_counts, opattr_diag *diag, int strict) {
+  __shared__ unsigned long long red[3][16];
+  unsigned long long mism = 0, tlu = 0, pfu = 0;
+  for (uint32_t n = threadIdx.x; n < NN; n += blockDim.x) {
+    const uint32_t tl = tlc[n], pf = pfc[n];
+    if (name_counts) {
+      name_counts[2 * (size_t)n] = tl;
+      name_counts[2 * (size_t)n + 1] = pf;
+    }
+    if (tl != pf) {
+      mism++;
+      if (tl > pf) tlu += tl - pf;
+      else pfu += pf - tl;
+    }
+  }
+  mism = wave_reduce_add(mism);
+  tlu = wave_reduce_add(tlu);
+  pfu = wave_reduce_add(pfu);
+  if (lane_id() == 0) {
+    red[0][wave_id()] = mism;
+    red[1][wave_id()] = tlu;
+    red[2][wave_id()] = pfu;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long a = 0, b = 0, c = 0;
+    for (uint32_t i = 0; i < blockDim.x / OPA_WAVE; ++i) {
+      a += red[0][i];
+      b += red[1][i];
+      c += red[2][i];
+    }
+    if (a) {
+      atomicAdd(&diag->names_mismatched, (uint32_t)a);
+      atomicOr(&diag->flags, OPATTR_F_COUNT);
+    }
+    if (b) atomicAdd((unsigned long long *)&diag->tl_unmatched, b);
+    if (c) atomicAdd((unsigned long long *)&diag->pf_unmatched, c);
+    if (strict) diag->strict = 1u;
+  }
+}
+
+__global__ void __launch_bounds__(1024) k_names(const uint32_t *__restrict__ tlc,
+                                                const uint32_t *__restrict__ pfc, uint32_t NN,
+                                                uint32_t *name_counts, opattr_diag *diag,
+                                                int strict) {
+  names_check(tlc, pfc, NN, name_counts, diag, strict);
+}
+
 struct RankArgs {
   const uint32_t *rec, *cnt;  // the buckets
   const uint32_t *tlh;        // exclusive prefix of each name down the tiles
@@ -665,6 +751,11 @@ struct RankArgs {
   uint32_t *nbs;  // by seq rank: its name
   uint32_t NN;
   int skip_name;
+  // the count validation, by the block after the last tile (NN > 0)
+  int64_t ntiles;
+  uint32_t *name_counts;
+  opattr_diag *diag;
+  int strict;
 };
 
 // rank = (eligible launches of the name in earlier tiles) + (rank in the
@@ -674,6 +765,10 @@ __global__ void __launch_bounds__(256) k_f_pass2(RankArgs m) {
   OPA_DYN_LDS(uint16_t, cnt);
   const int64_t tile = blockIdx.x, base = tile * OPA_TILE;
   const uint32_t NN = m.NN;
+  if (tile >= m.ntiles) {
+    names_check(m.tlc, m.pfc, NN, m.name_counts, m.diag, m.strict);
+    return;
+  }
   const uint32_t n = m.cnt[tile];
   if (n == 0) return;
   for (uint32_t i = threadIdx.x; i < 4 * NN; i += OPA_TILE_THREADS) cnt[i] = 0;
@@ -1055,50 +1150,6 @@ __global__ void __launch_bounds__(1024) k_pf_off(const uint32_t *__restrict__ pf
   }
 }
 
-// count validation (Sec. 3.3): per name, eligible launches against rows
-__global__ void __launch_bounds__(1024) k_names(const uint32_t *__restrict__ tlc,
-                                                const uint32_t *__restrict__ pfc, uint32_t NN,
-                                                uint32_t *name_counts, opattr_diag *diag,
-                                                int strict) {
-  __shared__ unsigned long long red[3][16];
-  unsigned long long mism = 0, tlu = 0, pfu = 0;
-  for (uint32_t n = threadIdx.x; n < NN; n += 1024) {
-    const uint32_t tl = tlc[n], pf = pfc[n];
-    if (name_counts) {
-      name_counts[2 * (size_t)n] = tl;
-      name_counts[2 * (size_t)n + 1] = pf;
-    }
-    if (tl != pf) {
-      mism++;
-      if (tl > pf) tlu += tl - pf;
-      else pfu += pf - tl;
-    }
-  }
-  mism = wave_reduce_add(mism);
-  tlu = wave_reduce_add(tlu);
-  pfu = wave_reduce_add(pfu);
-  if (lane_id() == 0) {
-    red[0][wave_id()] = mism;
-    red[1][wave_id()] = tlu;
-    red[2][wave_id()] = pfu;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    unsigned long long a = 0, b = 0, c = 0;
-    for (int i = 0; i < 16; ++i) {
-      a += red[0][i];
-      b += red[1][i];
-      c += red[2][i];
-    }
-    if (a) {
-      atomicAdd(&diag->names_mismatched, (uint32_t)a);
-      atomicOr(&diag->flags, OPATTR_F_COUNT);
-    }
-    if (b) atomicAdd((unsigned long long *)&diag->tl_unmatched, b);
-    if (c) atomicAdd((unsigned long long *)&diag->pf_unmatched, c);
-    if (strict) diag->strict = 1u;
-  }
-}
 
 // Layout promise of the kernels (checked under OPATTR_VALIDATE): sorted by
 // (stream, seq) with seq unique, streams below n_streams, query points not
@@ -1275,8 +1326,27 @@ void run_match(const IomArgs &x, hipStream_t s) {
   clr.add(tlc, 0, NN);
   clr.add(pfc, 0, NN);
   if (parts) clear_partitions(clr, ws, pl);
-  fill_many(clr, s);
-  if (dedup) k_rep_check<<<(d->n_parts + 255) / 256, 256, 0, s>>>(d->part_rep, d->n_parts, x.diag);
+  const bool seg_pro = seg && pl.nt > 0;  // clears, class-map check and stream blocks in one launch
+  if (seg_pro) {
+    ProArgs pa{};
+    pa.fill = clr;
+    int64_t mx = 0;
+    for (int q = 0; q < clr.count; ++q) mx = clr.n[q] > mx ? clr.n[q] : mx;
+    pa.nf = (int)((mx + 255) / 256 < 1024 ? (mx + 255) / 256 : 1024);
+    pa.nr = dedup ? (int)((d->n_parts + 255) / 256) : 0;
+    pa.part_rep = d->part_rep;
+    pa.NP = d->n_parts;
+    pa.diag = x.diag;
+    pa.st = k->stream_id;
+    pa.T = pl.T;
+    pa.NS = pl.NS;
+    pa.kblk = at<int64_t>(ws, pl.kblk);
+    const int nw = (int)((pl.NS + 1 + 3) / 4);
+    k_seg_prologue<<<(unsigned)(pa.nf + pa.nr + nw), 256, 0, s>>>(pa);
+  } else {
+    fill_many(clr, s);
+    if (dedup) k_rep_check<<<(d->n_parts + 255) / 256, 256, 0, s>>>(d->part_rep, d->n_parts, x.diag);
+  }
   const TlArgs ta = tl_args(k, d, ws, pl, dedup);
   PfArgs pa;
   pa.name = x.p->name_id;
@@ -1310,7 +1380,7 @@ void run_match(const IomArgs &x, hipStream_t s) {
 
   // the timeline side
   if (seg && pl.nt > 0) {
-    launch_stream_blocks(k->stream_id, pl.T, pl.NS, at<int64_t>(ws, pl.kblk), s);
+    if (!seg_pro) launch_stream_blocks(k->stream_id, pl.T, pl.NS, at<int64_t>(ws, pl.kblk), s);
     const int64_t nb = (pl.nt + 1) * pl.NS;
     k_tile_bounds<<<(unsigned)((nb + 255) / 256), 256, 0, s>>>(k->seq, at<int64_t>(ws, pl.kblk),
                                                              pl.NS, pl.nt, at<uint32_t>(ws, pl.tbnd));
@@ -1352,9 +1422,9 @@ void run_match(const IomArgs &x, hipStream_t s) {
   column_scan(tlh, pl.nt, NN, at<uint32_t>(ws, pl.tlch), tlc, s, nullptr);
   probe_end(OPATTR_PROBE_COL_SCAN, s);
   if (sp != s) note(hipStreamWaitEvent(s, x.pf_join, 0));
-  if (NN)
-    k_names<<<1, 1024, 0, s>>>(tlc, pfc, NN, x.name_counts, x.diag,
-                               x.policy == OPATTR_MISMATCH_STRICT ? 1 : 0);
+  const int strict = x.policy == OPATTR_MISMATCH_STRICT ? 1 : 0;
+  const bool names_in_pass2 = pl.nt > 0 && buckets;  // an extra block of the ranking
+  if (NN && !names_in_pass2) k_names<<<1, 1024, 0, s>>>(tlc, pfc, NN, x.name_counts, x.diag, strict);
   probe_begin(OPATTR_PROBE_TL_MATCH, s);
   if (pl.nt > 0 && buckets) {
     RankArgs m;
@@ -1369,7 +1439,11 @@ void run_match(const IomArgs &x, hipStream_t s) {
     m.nbs = at<uint32_t>(ws, pl.nbs);
     m.NN = NN;
     m.skip_name = x.policy == OPATTR_MISMATCH_SKIP_NAME ? 1 : 0;
-    k_f_pass2<<<(unsigned)pl.nt, 256, lds, s>>>(m);
+    m.ntiles = pl.nt;
+    m.name_counts = x.name_counts;
+    m.diag = x.diag;
+    m.strict = strict;
+    k_f_pass2<<<(unsigned)(pl.nt + (NN ? 1 : 0)), 256, lds, s>>>(m);
   } else if (pl.nt > 0) {
     if (fast) {
       LookArgs m;

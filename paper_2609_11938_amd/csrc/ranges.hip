@@ -19,22 +19,58 @@ namespace opa {
 
 constexpr uint64_t kEndLimit = 1ull << 63;  // valid ends stay below 2^63
 
-// validity, effective ends and stream blocks
-__global__ void k_rprep(CoreRanges cr, uint32_t NS, uint32_t NOPS, int64_t *ree, int32_t *npg,
-                        opattr_diag *diag) {
-  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  bool bad = false;
-  if (x < cr.n) {
-    const uint64_t s = cr.s[x], e = cr.e[x];
-    const bool ok = cr.st[x] < NS && cr.op[x] < NOPS && s <= e && e < kEndLimit &&
-                    (!cr.kind || cr.kind[x] <= OPATTR_KIND_SKIP);
-    ree[x] = ok ? (int64_t)e : -1;
-    npg[x] = -1;
-    bad = !ok;
-  }
+// validity and effective end of range x (-1 marks a bad range); parents unknown
+__device__ __forceinline__ bool rprep_one(const CoreRanges &cr, uint32_t NS, uint32_t NOPS,
+                                          int64_t *ree, int32_t *npg, int64_t x) {
+  const uint64_t s = cr.s[x], e = cr.e[x];
+  const bool ok = cr.st[x] < NS && cr.op[x] < NOPS && s <= e && e < kEndLimit &&
+                  (!cr.kind || cr.kind[x] <= OPATTR_KIND_SKIP);
+  ree[x] = ok ? (int64_t)e : -1;
+  npg[x] = -1;
+  return !ok;
+}
+
+__device__ __forceinline__ void count_bad(bool bad, opattr_diag *diag) {
   const uint64_t m = __ballot(bad);
   if (m && lane_id() == __ffsll((unsigned long long)m) - 1)
     atomicAdd((unsigned long long *)&diag->bad_records, (unsigned long long)__popcll(m));
+}
+
+__global__ void k_rprep(CoreRanges cr, uint32_t NS, uint32_t NOPS, int64_t *ree, int32_t *npg,
+                        opattr_diag *diag) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  count_bad(x < cr.n && rprep_one(cr, NS, NOPS, ree, npg, x), diag);
+}
+
+// The range preparation in one launch, three jobs by block ranges: [0, na)
+// validity and effective ends, 256 ranges a block; [na, na + nb) the stream
+// blocks, one wave per stream s = 0..NS; then the clears (fill jobs).
+struct RangePro {
+  CoreRanges cr;
+  uint32_t NS, NOPS;
+  int64_t *ree;
+  int32_t *npg;
+  int64_t *rblk;
+  opattr_diag *diag;
+  int na, nb, nf;
+  FillJobs fill;
+};
+
+__global__ void __launch_bounds__(256) k_range_pro(RangePro a) {
+  const int b = blockIdx.x;
+  if (b < a.na) {
+    const int64_t x = (int64_t)b * blockDim.x + threadIdx.x;
+    count_bad(x < a.cr.n && rprep_one(a.cr, a.NS, a.NOPS, a.ree, a.npg, x), a.diag);
+  } else if (b < a.na + a.nb) {
+    const uint32_t sw = (uint32_t)(b - a.na) * (blockDim.x / OPA_WAVE) + wave_id();
+    if (sw <= a.NS) stream_block_wave(a.cr.st, a.cr.n, sw, a.rblk);
+  } else {
+    const int fb = b - a.na - a.nb;
+    const int64_t stride = (int64_t)a.nf * blockDim.x;
+    for (int q = 0; q < a.fill.count; ++q)
+      for (int64_t i = (int64_t)fb * blockDim.x + threadIdx.x; i < a.fill.n[q]; i += stride)
+        a.fill.p[q][i] = a.fill.v[q];
+  }
 }
 
 // promised nesting order: (stream, start asc, end desc) never decreases
@@ -53,36 +89,11 @@ __global__ void k_rcheck(CoreRanges cr, opattr_diag *diag) {
   }
 }
 
-// blk[s] = first position with stream >= s, s = 0..NS (the array is sorted
-// by stream). One wave per s: each round, the 64 lanes probe 64 evenly spaced
-// positions and the range shrinks to the gap where the answer lies.
+// blk[s] = first position with stream >= s, s = 0..NS (one wave per s)
 __global__ void __launch_bounds__(256) k_blocks16(const uint16_t *st, int64_t n, uint32_t NS,
                                                   int64_t *blk) {
   const uint32_t s = blockIdx.x * (blockDim.x / OPA_WAVE) + wave_id();
-  if (s > NS) return;
-  const int ln = lane_id();
-  int64_t lo = 0, hi = n;  // answer in [lo, hi]
-  while (hi - lo > OPA_WAVE) {
-    const int64_t step = (hi - lo + OPA_WAVE - 1) / OPA_WAVE;
-    int64_t p = lo + (int64_t)(ln + 1) * step - 1;
-    if (p > hi - 1) p = hi - 1;
-    const uint64_t m = __ballot(st[p] >= s);
-    if (m == 0) {
-      lo = hi;
-      break;
-    }
-    const int f = __ffsll((unsigned long long)m) - 1;  // first probe at or past s
-    int64_t pf = lo + (int64_t)(f + 1) * step - 1;
-    if (pf > hi - 1) pf = hi - 1;
-    lo = f == 0 ? lo : lo + (int64_t)f * step;
-    hi = pf;  // st[pf] >= s
-  }
-  if (hi - lo <= OPA_WAVE && lo < hi) {
-    const int64_t p = lo + ln;
-    const uint64_t m = __ballot(p < hi && st[p] >= s);
-    lo = m ? lo + __ffsll((unsigned long long)m) - 1 : hi;
-  }
-  if (ln == 0) blk[s] = lo;
+  if (s <= NS) stream_block_wave(st, n, s, blk);
 }
 
 void launch_stream_blocks(const uint16_t *st, int64_t n, uint32_t NS, int64_t *blk,
@@ -91,9 +102,9 @@ void launch_stream_blocks(const uint16_t *st, int64_t n, uint32_t NS, int64_t *b
   k_blocks16<<<(waves + 3) / 4, 256, 0, s>>>(st, n, NS, blk);
 }
 
-// tbase[s] = first tile of stream s (tiles never straddle streams)
-__global__ void __launch_bounds__(1024) k_rtile_base(const int64_t *rblk, uint32_t NS,
-                                                     int32_t *tbase) {
+// tbase[s] = first tile of stream s (tiles never straddle streams), by one
+// block of 1024 threads
+__device__ inline void tile_bases(const int64_t *rblk, uint32_t NS, int32_t *tbase) {
   __shared__ uint32_t sh[16];
   uint32_t carry = 0;
   for (uint32_t base = 0; base < NS; base += 1024) {
@@ -107,6 +118,13 @@ __global__ void __launch_bounds__(1024) k_rtile_base(const int64_t *rblk, uint32
   }
   if (threadIdx.x == 0) tbase[NS] = (int32_t)carry;
 }
+
+__global__ void __launch_bounds__(1024) k_rtile_base(const int64_t *rblk, uint32_t NS,
+                                                     int32_t *tbase) {
+  tile_bases(rblk, NS, tbase);
+}
+
+constexpr uint32_t kInlineBases = 1024;  // streams whose tile bases k_rlocal finds itself
 
 __device__ __forceinline__ uint32_t stream_of_tile(const int32_t *tbase, uint32_t NS, int32_t t) {
   uint32_t lo = 0, hi = NS;  // last s with tbase[s] <= t
@@ -122,7 +140,7 @@ struct RangeWork {
   CoreRanges cr;
   uint32_t NS;
   const int64_t *rblk;
-  const int32_t *tbase;
+  int32_t *tbase;  // written by k_rtile_base, or by k_rlocal with inline_bases
   int64_t *ree;
   int32_t *npg;
   int64_t *mxv;
@@ -132,6 +150,7 @@ struct RangeWork {
   int32_t *tstr, *tlast;
   uint8_t *sflag;
   opattr_diag *diag;
+  int inline_bases;  // k_rlocal finds the tile bases (NS <= kInlineBases)
 };
 
 // Local parents inside one tile by pointer jumping (Jacobi rounds): cand[i]
@@ -144,10 +163,20 @@ __global__ void __launch_bounds__(kRangeTile) k_rlocal(RangeWork w) {
   __shared__ int64_t mx[kRangeTile];
   __shared__ int32_t cand[kRangeTile];
   __shared__ int64_t red[kRangeTile / OPA_WAVE];
-  const int32_t t = blockIdx.x;
-  if (t >= w.tbase[w.NS]) return;
-  const uint32_t s = stream_of_tile(w.tbase, w.NS, t);
-  const int64_t x0 = w.rblk[s] + (int64_t)(t - w.tbase[s]) * kRangeTile;
+  __shared__ int32_t stb[kInlineBases + 1];
+  static_assert(kRangeTile == 1024, "one thread per range of a tile, 1024 for the bases");
+  const int32_t *tb = w.tbase;
+  if (w.inline_bases) {
+    tile_bases(w.rblk, w.NS, stb);
+    __syncthreads();
+    if (blockIdx.x == 0)
+      for (uint32_t k = threadIdx.x; k <= w.NS; k += blockDim.x) w.tbase[k] = stb[k];
+    tb = stb;
+  }
+  const int32_t t = blockIdx.x, ntr = tb[w.NS];
+  if (t >= ntr) return;
+  const uint32_t s = stream_of_tile(tb, w.NS, t);
+  const int64_t x0 = w.rblk[s] + (int64_t)(t - tb[s]) * kRangeTile;
   const int64_t x1 = min(x0 + kRangeTile, w.rblk[s + 1]);
   const int i = threadIdx.x;
   const bool valid = x0 + i < x1;
@@ -274,23 +303,7 @@ __global__ void k_rresolve(RangeWork w) {
 // depth = length of the parent chain (1 for a root, 0 for a bad range)
 __global__ void k_rdepth(RangeWork w, uint8_t *range_depth) {
   const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  bool lim = false;
-  if (x < w.cr.n) {
-    int d = 0;
-    int32_t y = (int32_t)x;
-    while (y >= 0 && d <= 255) {
-      ++d;
-      y = w.npg[y];
-    }
-    lim = y >= 0;
-    const bool ok = w.ree[x] >= 0 && w.cr.st[x] < w.NS;
-    if (range_depth) {
-      const int64_t o = w.cr.perm ? w.cr.perm[x] : x;
-      range_depth[o] = ok ? (uint8_t)(d > 255 ? 255 : d) : 0;
-    }
-    lim = lim && ok;
-  }
-  if (__ballot(lim) && lane_id() == 0) atomicOr(&w.diag->flags, OPATTR_F_LIMIT);
+  range_depth_one(w.npg, w.ree, w.cr.st, w.cr.perm, w.cr.n, w.NS, x, range_depth, w.diag);
 }
 
 static RangeWork range_work(const CoreRanges &cr, const opattr_dims *d, void *ws, const Plan &pl,
@@ -312,6 +325,7 @@ static RangeWork range_work(const CoreRanges &cr, const opattr_dims *d, void *ws
   w.tlast = at<int32_t>(ws, pl.tlast);
   w.sflag = at<uint8_t>(ws, pl.sflag);
   w.diag = diag;
+  w.inline_bases = d->n_streams <= kInlineBases ? 1 : 0;
   return w;
 }
 
@@ -352,7 +366,7 @@ void write_range_parents(const CoreRanges &cr, void *ws, const Plan &pl, int32_t
 }
 
 CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws, const Plan &pl,
-                          opattr_diag *diag, bool validate, hipStream_t s) {
+                          opattr_diag *diag, bool validate, hipStream_t s, const FillJobs *extra) {
   CoreRanges cr;
   cr.n = pl.R;
   const int64_t R = pl.R;
@@ -401,11 +415,29 @@ CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws
   }
   const uint32_t NS = d->n_streams;
   int64_t *rblk = at<int64_t>(ws, pl.rblk);
-  if (R > 0)
-    k_rprep<<<(unsigned)((R + 255) / 256), 256, 0, s>>>(cr, NS, d->n_ops, at<int64_t>(ws, pl.ree),
-                                                        at<int32_t>(ws, pl.npg), diag);
-  if (R > 0) launch_stream_blocks(cr.st, R, NS, rblk, s);
-  else fill_u32(reinterpret_cast<uint32_t *>(rblk), 0, 2 * ((int64_t)NS + 1), s);
+  // the clears: the caller's and the crossing flags
+  FillJobs clr = extra ? *extra : FillJobs{};
+  clr.add(at<uint8_t>(ws, pl.sflag), 0, sflag_words(NS));
+  if (R > 0) {
+    RangePro a{};
+    a.cr = cr;
+    a.NS = NS;
+    a.NOPS = d->n_ops;
+    a.ree = at<int64_t>(ws, pl.ree);
+    a.npg = at<int32_t>(ws, pl.npg);
+    a.rblk = rblk;
+    a.diag = diag;
+    a.na = (int)((R + 255) / 256);
+    a.nb = (int)((NS + 1 + 3) / 4);
+    int64_t mx = 0;
+    for (int q = 0; q < clr.count; ++q) mx = clr.n[q] > mx ? clr.n[q] : mx;
+    a.nf = (int)((mx + 255) / 256 < 1024 ? (mx + 255) / 256 : 1024);
+    a.fill = clr;
+    k_range_pro<<<(unsigned)(a.na + a.nb + a.nf), 256, 0, s>>>(a);
+  } else {
+    clr.add(rblk, 0, 2 * ((int64_t)NS + 1));
+    fill_many(clr, s);
+  }
   return cr;
 }
 
@@ -433,20 +465,19 @@ __global__ void k_range_walk(CoreRanges cr, const int32_t *npg, int32_t *wfirst,
 }
 
 void resolve_ranges(const CoreRanges &cr, const opattr_dims *d, void *ws, const Plan &pl,
-                    uint8_t *range_depth, opattr_diag *diag, hipStream_t s) {
+                    uint8_t *range_depth, opattr_diag *diag, hipStream_t s, bool defer_depth) {
   const uint32_t NS = d->n_streams;
-  fill_u8(at<uint8_t>(ws, pl.sflag), 0, NS ? NS : 1, s);
   if (pl.R <= 0 || NS == 0) {
     if (range_depth && pl.R > 0) fill_u8(range_depth, 0, pl.R, s);
     return;
   }
   RangeWork w = range_work(cr, d, ws, pl, diag);
-  k_rtile_base<<<1, 1024, 0, s>>>(w.rblk, NS, at<int32_t>(ws, pl.tbase));
+  if (!w.inline_bases) k_rtile_base<<<1, 1024, 0, s>>>(w.rblk, NS, at<int32_t>(ws, pl.tbase));
   k_rlocal<<<(unsigned)pl.ntr_max, kRangeTile, 0, s>>>(w);
   k_rtiles<<<1, 1024, 0, s>>>(w);
   const unsigned nb = (unsigned)((pl.R + 255) / 256);
   k_rresolve<<<nb, 256, 0, s>>>(w);
-  k_rdepth<<<nb, 256, 0, s>>>(w, range_depth);
+  if (!defer_depth) k_rdepth<<<nb, 256, 0, s>>>(w, range_depth);
   if (cr.kind)
     k_range_walk<<<nb, 256, 0, s>>>(cr, at<int32_t>(ws, pl.npg), at<int32_t>(ws, pl.wfirst),
                                    at<uint8_t>(ws, pl.wfused));

@@ -319,6 +319,10 @@ __global__ void k_fill_many(FillJobs j) {
 
 void FillJobs::add(void *ptr, uint32_t value, int64_t words) {
   if (words <= 0) return;
+  if (count >= kMaxJobs) {  // a caller bug: make the call fail
+    note(hipErrorInvalidValue);
+    return;
+  }
   p[count] = static_cast<uint32_t *>(ptr);
   v[count] = value;
   n[count] = words;
