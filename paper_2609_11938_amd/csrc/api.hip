@@ -92,6 +92,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.fused = pl.seg && r != nullptr && pl.G <= kFusedMaxRows && pl.R * 16 <= pl.T && pl.T > 0;
   pl.acc = b.take(pl.fused ? fused_acc_bytes(pl.G) : 0);
   pl.fbkt = b.take(pl.fused ? fused_bkt_bytes(pl.T) : 0);
+  pl.forder = b.take(pl.fused ? (size_t)fused_agg_blocks(pl.T) * 4 : 0);
   pl.fsplit = b.take(pl.fused ? fused_split_bytes(pl.G) : 0);
   const bool rs = !pl.ranges_nested;
   pl.rperm = b.take(rs ? R * 4 : 0);
@@ -582,6 +583,7 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
   if (ss) note(hipEventRecord(ss->join, s2));
   IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, false};
   a.buckets = true;
+  a.fused_order = ss != nullptr;  // only where the profiled side has a stream of its own
   if (ss) {
     a.pf_stream = ss->s2;
     a.pf_fork = ss->fork2;
@@ -603,6 +605,7 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
   f.pl = &pl;
   if (ss) note(hipStreamWaitEvent(s, ss->join, 0));
   f.sum = sum;
+  f.ordered = a.fused_order;
   run_fused_agg(f, s);  // ends with the finalisation
   return launch_status();
 }

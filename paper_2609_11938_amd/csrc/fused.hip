@@ -149,6 +149,55 @@ __device__ __forceinline__ void match_of(const MatchParams &a, int64_t i, int nv
 }
 
 // ---------------------------------------------------------------------------
+// 0. processing order of the run reduction's blocks. A block of 2048
+// launches in storage order holds one stream's launches over a window of
+// launch order; its duplicates read the matches (and the counter rows) of
+// the representatives of that window, which every stream's blocks over the
+// window read too. The blocks are ordered by the seq rank of their first
+// launch (a counting sort into kOrderBuckets windows), and each XCD takes a
+// contiguous part of that order, so that the blocks sharing those reads
+// run at about the same time on one L2. The order only moves work between
+// workgroups: every block still reduces its own launches.
+// ---------------------------------------------------------------------------
+constexpr int kOrderBuckets = 1024;
+constexpr uint32_t kXcds = 8;  // workgroups go round robin over the XCDs in dispatch order
+
+__global__ void __launch_bounds__(kOrderBuckets) k_f_order(const uint32_t *__restrict__ seq,
+                                                           int64_t T, int64_t nb,
+                                                           uint32_t *order) {
+  __shared__ uint32_t hist[kOrderBuckets];
+  __shared__ uint32_t sh[kOrderBuckets / OPA_WAVE];
+  const int tid = threadIdx.x;
+  hist[tid] = 0;
+  __syncthreads();
+  auto bucket = [&](int64_t b) -> uint32_t {
+    const uint64_t q = seq[b * kASpan];
+    const uint64_t c = q < (uint64_t)T ? q : (uint64_t)T - 1;  // a broken promise: any window
+    return (uint32_t)(c * kOrderBuckets / (uint64_t)T);
+  };
+  for (int64_t b = tid; b < nb; b += kOrderBuckets) atomicAdd(&hist[bucket(b)], 1u);
+  __syncthreads();
+  uint32_t tot;
+  const uint32_t base = block_excl_scan_add<uint32_t>(hist[tid], sh, &tot);
+  __syncthreads();
+  hist[tid] = base;
+  __syncthreads();
+  for (int64_t b = tid; b < nb; b += kOrderBuckets)
+    order[atomicAdd(&hist[bucket(b)], 1u)] = (uint32_t)b;
+}
+
+// The block workgroup i reduces: dispatch index i runs on XCD i % kXcds,
+// and XCD x takes the part of the order after the parts of XCDs 0 .. x-1
+// (without an order, block i).
+__device__ __forceinline__ int64_t order_slot(const uint32_t *order, uint32_t i, uint32_t n) {
+  if (!order) return i;
+  const uint32_t x = i % kXcds, t = i / kXcds;
+  uint32_t before = 0;
+  for (uint32_t y = 0; y < x; ++y) before += (n - y + kXcds - 1) / kXcds;
+  return order[before + t];
+}
+
+// ---------------------------------------------------------------------------
 // 1. runs
 // ---------------------------------------------------------------------------
 struct AggParams {
@@ -162,6 +211,7 @@ struct AggParams {
   PartRow *acc;             // [G] row accumulators for what blocks do not keep (zeroed)
   PartRow *parts;           // [blocks][kABlockCap] kept partials, by bucket (row in pad)
   uint16_t *bkt;            // [blocks][kBuckets] offset << 8 | count
+  const uint32_t *order;    // [blocks] processing order (k_f_order), or NULL
 };
 
 // A partial result staged in LDS: its 25 fields and its row (live 0: merged
@@ -282,7 +332,8 @@ k_f_agg(AggParams a) {
   const int tid = threadIdx.x, ln = lane_id(), w = wave_id();
   const AggIn &in = a.in;
   const uint32_t mx = DEF ? kDefMaxMask : in.maxmask, dw = DEF ? kDefDwMask : in.dwmask;
-  const int64_t ib = (int64_t)blockIdx.x * kASpan + (int64_t)tid * kAPer;
+  const int64_t blk = order_slot(a.order, blockIdx.x, gridDim.x);
+  const int64_t ib = blk * kASpan + (int64_t)tid * kAPer;
   const int nv = (int)(a.T - ib < 0 ? 0 : (a.T - ib < kAPer ? a.T - ib : kAPer));
   Slot *wslot = slots[w];
   int nst = 0;      // staged partials of the wave (uniform)
@@ -424,14 +475,14 @@ k_f_agg(AggParams a) {
   if (tid < kBuckets) cnt = hist[tid];
   const uint32_t off = block_excl_scan_add<uint32_t>(tid < kBuckets ? cnt : 0u, sh, &tot);
   if (tid < kBuckets)
-    a.bkt[(int64_t)blockIdx.x * kBuckets + tid] = (uint16_t)((off << 8) | cnt);
+    a.bkt[blk * kBuckets + tid] = (uint16_t)((off << 8) | cnt);
   __syncthreads();
   if (tid < kBuckets) hist[tid] = off;
   __syncthreads();
   if (tid < kABlockCap) spos[tid] = bq != 0xFFFFFFFFu ? hist[bq] + rk : 0xFFFFFFFFu;
   __syncthreads();
   // coalesced copy: consecutive threads take consecutive fields
-  PartRow *dst = a.parts + (int64_t)blockIdx.x * kABlockCap;
+  PartRow *dst = a.parts + blk * kABlockCap;
   for (int x = tid; x < kABlockCap * kFFields; x += kAThreads) {
     const int s = x / kFFields, f = x % kFFields;
     const uint32_t p = spos[s];
@@ -652,6 +703,11 @@ void fused_acc_clear(FillJobs &j, void *ws, const Plan &pl) {
   j.add(at<uint32_t>(ws, pl.acc), 0u, (int64_t)(fused_acc_bytes(pl.G) / 4));
 }
 
+void run_fused_order(const opattr_kernels *k, void *ws, const Plan &pl, hipStream_t s) {
+  const int64_t nb = fused_agg_blocks(pl.T);
+  if (nb > 0) k_f_order<<<1, kOrderBuckets, 0, s>>>(k->seq, pl.T, nb, at<uint32_t>(ws, pl.forder));
+}
+
 void run_fused_agg(const FusedIn &x, hipStream_t s) {
   const Plan &pl = *x.pl;
   const uint32_t rb = fused_rows_per_bucket(pl.G);
@@ -681,6 +737,7 @@ void run_fused_agg(const FusedIn &x, hipStream_t s) {
   a.bkt = at<uint16_t>(x.ws, pl.fbkt);
   const bool def = a.in.maxmask == kDefMaxMask && a.in.dwmask == kDefDwMask;
   const int64_t nb = fused_agg_blocks(pl.T);
+  a.order = x.ordered ? at<uint32_t>(x.ws, pl.forder) : nullptr;  // from run_fused_order
   probe_begin(OPATTR_PROBE_AGG_RUNS, s);
   if (nb > 0) {
     if (def) k_f_agg<true><<<(unsigned)nb, kAThreads, 0, s>>>(a);

@@ -45,7 +45,7 @@ struct Plan {
   // accumulators, kept partials (aliasing the partial rows of the other
   // aggregation), their bucket entries, and the per-bucket shares
   bool fused;
-  size_t acc, fparts, fbkt, fsplit;
+  size_t acc, fparts, fbkt, fsplit, forder;
   bool m2;  // the second set below exists
   size_t kblk2, tbnd2, tlh2, pfh2, tlch2, pfch2, tlc2, pfc2, off2, slot2, nbs2;
   // ranges
@@ -185,6 +185,8 @@ struct IomArgs {
   // it from and join it back to the main stream
   hipStream_t pf_stream = nullptr;
   hipEvent_t pf_fork = nullptr, pf_join = nullptr;
+  // fused path: the run reduction's block order, computed on the profiled side
+  bool fused_order = false;
 };
 void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, const Plan &pl,
                     opattr_diag *diag, bool validate, hipStream_t s);
@@ -327,12 +329,16 @@ struct FusedIn {
   opattr_diag *diag;
   void *ws;
   const Plan *pl;
+  bool ordered = false;  // run_fused_order filled the block order
 };
 // every launch's match (from the bucket path's mbs / nbs, with the dedup
 // broadcast and its errors), the operator table from it and range_id, the
 // summary and the final status (the row accumulators and the done count must
 // be zero: fused_acc_clear)
 void run_fused_agg(const FusedIn &x, hipStream_t s);
+// the processing order of the run reduction's blocks (reads only seq)
+void run_fused_order(const opattr_kernels *k, void *ws, const Plan &pl, hipStream_t s);
+int64_t fused_agg_blocks(int64_t T);  // blocks of the run reduction
 // the clear of the row accumulators and the done count, as a fill job
 void fused_acc_clear(FillJobs &j, void *ws, const Plan &pl);
 // workspace sizes of the fused aggregation

@@ -1376,6 +1376,7 @@ void run_match(const IomArgs &x, hipStream_t s) {
     else k_pf_slot<<<(unsigned)ntp, 256, 0, sp>>>(pa, pfh, off, at<int32_t>(ws, pl.slot));
   }
   probe_end(OPATTR_PROBE_PF_SLOT, sp);
+  if (x.fused_order && sp != s) run_fused_order(k, ws, pl, sp);
   if (sp != s) note(hipEventRecord(x.pf_join, sp));
 
   // the timeline side
