@@ -52,6 +52,25 @@ def _run(tr, flags=0, policy=0, agg_kind=None, absent_mask=0, **kw):
     return out, opattr.read_diag(out["diag"])
 
 
+@pytest.mark.parametrize("S,hinted", [(700, True), (1500, True), (1500, False)])
+def test_many_streams(S, hinted):
+    """More streams than the range stage's parent search finds tile bases for
+    in each tile (1024): the bases then come from a kernel of their own.
+    Nested ranges with depth on every stream, stream blocks for every
+    stream, the depths written by the enclosure's extra blocks; hinted
+    (stream-major, nesting order promised) and not (sorted on the device)."""
+    tr = cases.random_trace(7100 + S, T=40_000, S=S, n_names=11, R=6000, n_ops=40,
+                            t_max=200_000, max_depth=6, dedup=True)
+    flags = 0
+    if hinted:
+        tr, _, _ = cases.stream_major(tr)
+        flags = HINTS
+    print(f"case many streams S={S} hinted={hinted} R={tr['r_start'].size}", flush=True)
+    want = O.attribute(tr)
+    out, diag = _run(tr, flags=flags)
+    parity.assert_attribute(out, want, diag)
+
+
 @pytest.mark.parametrize("cfg", ["tiny", "gpt2", "sdpa", "lstm"])
 @pytest.mark.parametrize("emission", ["stream_major", "seq", "shuffled"])
 def test_config_parity(cfg, emission):
