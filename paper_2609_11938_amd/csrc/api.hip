@@ -94,6 +94,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.fbkt = b.take(pl.fused ? fused_bkt_bytes(pl.T) : 0);
   pl.forder = b.take(pl.fused ? (size_t)fused_agg_blocks(pl.T) * 4 : 0);
   pl.fsplit = b.take(pl.fused ? fused_split_bytes(pl.G) : 0);
+  pl.fhot = b.take(pl.fused ? fused_hot_bytes() : 0);
   const bool rs = !pl.ranges_nested;
   pl.rperm = b.take(rs ? R * 4 : 0);
   pl.rs_c = b.take(rs ? R * 8 : 0);

@@ -38,6 +38,11 @@ constexpr int kASlots = 32;                    // partial results a wave keeps
 constexpr int kABlockCap = kASlots * (kAThreads / OPA_WAVE);  // and a block
 constexpr int kFFields = 25;                   // kc, tns, mc, mns, 20 counters, NaN bits
 constexpr int kBuckets = 256;                  // buckets of operator rows
+// A block's bucket entries: the buckets, then the unattributed row (NOPS) on
+// its own: it has a partial in almost every block, which would make its
+// bucket's combine waves the last to finish by far.
+constexpr int kBktStride = kBuckets + 1;
+constexpr int kHot = 32;                       // combine waves of the unattributed row
 constexpr int kSplits = 16;                    // shares of the blocks per bucket
 constexpr uint32_t kNoSrc = 0xFFFFFFFFu;
 constexpr uint32_t kHash = 256;                // LDS table of a block's rows (> 2 x kept)
@@ -210,7 +215,7 @@ struct AggParams {
   AggIn in;
   PartRow *acc;             // [G] row accumulators for what blocks do not keep (zeroed)
   PartRow *parts;           // [blocks][kABlockCap] kept partials, by bucket (row in pad)
-  uint16_t *bkt;            // [blocks][kBuckets] offset << 8 | count
+  uint16_t *bkt;            // [blocks][kBktStride] offset << 8 | count
   const uint32_t *order;    // [blocks] processing order (k_f_order), or NULL
 };
 
@@ -326,7 +331,7 @@ __global__ void __launch_bounds__(kAThreads) __attribute__((amdgpu_waves_per_eu(
 k_f_agg(AggParams a) {
   __shared__ Slot slots[kAThreads / OPA_WAVE][kASlots];
   __shared__ int nslot[kAThreads / OPA_WAVE];
-  __shared__ uint32_t hist[kBuckets], spos[kABlockCap];
+  __shared__ uint32_t hist[kBktStride], spos[kABlockCap];
   __shared__ uint32_t hkey[kHash], hown[kHash];
   __shared__ uint32_t sh[4];
   const int tid = threadIdx.x, ln = lane_id(), w = wave_id();
@@ -416,7 +421,7 @@ k_f_agg(AggParams a) {
     const unsigned long long e = wave_reduce_add((unsigned long long)err);
     if (ln == 0 && e) atomicAdd((unsigned long long *)&a.m.diag->dedup_errors, e);
   }
-  for (int q = tid; q < kBuckets; q += kAThreads) hist[q] = 0;
+  for (int q = tid; q < kBktStride; q += kAThreads) hist[q] = 0;
   for (int q = tid; q < kHash; q += kAThreads) {
     hkey[q] = 0u;
     hown[q] = 0xFFFFFFFFu;
@@ -467,17 +472,21 @@ k_f_agg(AggParams a) {
   __syncthreads();
   uint32_t bq = 0xFFFFFFFFu, rk = 0;
   if (own) {
-    bq = slots[tid / kASlots][tid % kASlots].g / a.rb;
+    const uint32_t g = slots[tid / kASlots][tid % kASlots].g;
+    bq = g == a.NOPS ? (uint32_t)kBuckets : g / a.rb;
     rk = atomicAdd(&hist[bq], 1u);
   }
   __syncthreads();
   uint32_t cnt = 0, tot;
   if (tid < kBuckets) cnt = hist[tid];
   const uint32_t off = block_excl_scan_add<uint32_t>(tid < kBuckets ? cnt : 0u, sh, &tot);
+  const uint32_t hcnt = hist[kBuckets];  // the unattributed row's partial goes last
   if (tid < kBuckets)
-    a.bkt[blk * kBuckets + tid] = (uint16_t)((off << 8) | cnt);
+    a.bkt[blk * kBktStride + tid] = (uint16_t)((off << 8) | cnt);
+  if (tid == 0) a.bkt[blk * kBktStride + kBuckets] = (uint16_t)((tot << 8) | hcnt);
   __syncthreads();
   if (tid < kBuckets) hist[tid] = off;
+  if (tid == 0) hist[kBuckets] = tot;
   __syncthreads();
   if (tid < kABlockCap) spos[tid] = bq != 0xFFFFFFFFu ? hist[bq] + rk : 0xFFFFFFFFu;
   __syncthreads();
@@ -504,6 +513,7 @@ struct CombParams {
   const PartRow *parts;
   const uint16_t *bkt;
   PartRow *split;              // [kBuckets][kSplits][rb]
+  PartRow *hot;                // [kHot] the unattributed row's shares
   const PartRow *acc;          // [G] row accumulators (the blocks' overflow)
   opattr_op_row *table;
   unsigned long long *part;    // [kBuckets][4] summary sums per bucket
@@ -549,6 +559,39 @@ __global__ void __launch_bounds__(64) k_f_comb(CombParams a) {
   unsigned long long *tab = reinterpret_cast<unsigned long long *>(comb_raw);  // [rb][kFFields]
   const uint32_t mx = DEF ? kDefMaxMask : a.mx;
   const int ln = lane_id();
+  if (blockIdx.x >= (unsigned)(kBuckets * kSplits)) {
+    // the unattributed row: a share of the blocks, each lane adding its
+    // blocks' partials in registers, then the lanes across the wave
+    const int h = (int)blockIdx.x - kBuckets * kSplits;
+    const int64_t per = (a.nblocks + kHot - 1) / kHot;
+    const int64_t b_lo = (int64_t)h * per, b_hi = b_lo + per < a.nblocks ? b_lo + per : a.nblocks;
+    unsigned long long racc[kFFields];
+#pragma unroll
+    for (int f = 0; f < kFFields; ++f) racc[f] = 0;
+    for (int64_t b = b_lo + ln; b < b_hi; b += OPA_WAVE) {
+      const uint32_t e = a.bkt[b * kBktStride + kBuckets];
+      const uint32_t c = e & 0xFFu, o = e >> 8;
+      const unsigned long long *pr =
+          reinterpret_cast<const unsigned long long *>(a.parts + b * kABlockCap + o);
+#pragma unroll 1
+      for (uint32_t p = 0; p < c; ++p, pr += sizeof(PartRow) / 8)
+#pragma unroll
+        for (int f = 0; f < kFFields; ++f)
+          racc[f] = merge_field(f, racc[f], f < 24 ? pr[f] : (pr[f] & 0xFFFFFFFFull), mx);
+    }
+#pragma unroll
+    for (int o = OPA_WAVE / 2; o > 0; o >>= 1)
+#pragma unroll
+      for (int f = 0; f < kFFields; ++f)
+        racc[f] = merge_field(f, racc[f], __shfl_xor(racc[f], o, OPA_WAVE), mx);
+    if (ln < kFFields) {
+      unsigned long long v = racc[0];
+#pragma unroll
+      for (int f = 1; f < kFFields; ++f) v = ln == f ? racc[f] : v;
+      reinterpret_cast<unsigned long long *>(a.hot + h)[ln] = v;
+    }
+    return;
+  }
   const uint32_t q = blockIdx.x / kSplits, s = blockIdx.x % kSplits;
   const uint32_t rb = a.rb, ne = rb * kFFields;
   for (uint32_t x = ln; x < ne; x += OPA_WAVE) tab[x] = 0;
@@ -560,7 +603,7 @@ __global__ void __launch_bounds__(64) k_f_comb(CombParams a) {
 #pragma unroll
   for (int f = 0; f < kFFields; ++f) racc[f] = 0;
   for (int64_t b = b_lo + ln; b < b_hi; b += OPA_WAVE) {
-    const uint32_t e = a.bkt[b * kBuckets + q];
+    const uint32_t e = a.bkt[b * kBktStride + q];
     const uint32_t c = e & 0xFFu, o = e >> 8;
     const unsigned long long *pr =
         reinterpret_cast<const unsigned long long *>(a.parts + b * kABlockCap + o);
@@ -619,6 +662,13 @@ __global__ void __launch_bounds__(256) k_f_rows(CombParams a) {
     unsigned long long v = y[kSplits];
 #pragma unroll
     for (int k = 0; k < kSplits; ++k) v = merge_field((int)ff, v, y[k], mx);
+    if (g == a.NOPS) {  // the unattributed row's own shares, loads in flight together
+      unsigned long long hv[kHot];
+#pragma unroll
+      for (int h = 0; h < kHot; ++h) hv[h] = reinterpret_cast<const unsigned long long *>(a.hot + h)[ff];
+#pragma unroll
+      for (int h = 0; h < kHot; ++h) v = merge_field((int)ff, v, hv[h], mx);
+    }
     tab[x] = v;
   }
   __syncthreads();
@@ -689,7 +739,9 @@ size_t fused_parts_bytes(int64_t T) {
   return (size_t)fused_agg_blocks(T) * kABlockCap * sizeof(PartRow);
 }
 
-size_t fused_bkt_bytes(int64_t T) { return (size_t)fused_agg_blocks(T) * kBuckets * 2; }
+size_t fused_bkt_bytes(int64_t T) { return (size_t)fused_agg_blocks(T) * kBktStride * 2; }
+
+size_t fused_hot_bytes() { return (size_t)kHot * sizeof(PartRow); }
 
 size_t fused_split_bytes(uint32_t G) {
   return (size_t)kBuckets * kSplits * fused_rows_per_bucket(G) * sizeof(PartRow);
@@ -756,6 +808,7 @@ void run_fused_agg(const FusedIn &x, hipStream_t s) {
   c.parts = a.parts;
   c.bkt = a.bkt;
   c.split = at<PartRow>(x.ws, pl.fsplit);
+  c.hot = at<PartRow>(x.ws, pl.fhot);
   c.acc = a.acc;
   c.table = x.table;
   c.part = at<unsigned long long>(x.ws, pl.sumpart);
@@ -767,10 +820,10 @@ void run_fused_agg(const FusedIn &x, hipStream_t s) {
   c.sum = x.sum;
   const size_t lds = (size_t)rb * kFFields * 8;
   if (def) {
-    k_f_comb<true><<<kBuckets * kSplits, 64, lds, s>>>(c);
+    k_f_comb<true><<<kBuckets * kSplits + kHot, 64, lds, s>>>(c);
     k_f_rows<true><<<kBuckets, 256, lds, s>>>(c);
   } else {
-    k_f_comb<false><<<kBuckets * kSplits, 64, lds, s>>>(c);
+    k_f_comb<false><<<kBuckets * kSplits + kHot, 64, lds, s>>>(c);
     k_f_rows<false><<<kBuckets, 256, lds, s>>>(c);
   }
   probe_end(OPATTR_PROBE_AGGREGATE, s);

@@ -45,7 +45,7 @@ struct Plan {
   // accumulators, kept partials (aliasing the partial rows of the other
   // aggregation), their bucket entries, and the per-bucket shares
   bool fused;
-  size_t acc, fparts, fbkt, fsplit, forder;
+  size_t acc, fparts, fbkt, fsplit, forder, fhot;
   bool m2;  // the second set below exists
   size_t kblk2, tbnd2, tlh2, pfh2, tlch2, pfch2, tlc2, pfc2, off2, slot2, nbs2;
   // ranges
@@ -345,6 +345,7 @@ void fused_acc_clear(FillJobs &j, void *ws, const Plan &pl);
 size_t fused_parts_bytes(int64_t T);
 size_t fused_bkt_bytes(int64_t T);
 size_t fused_split_bytes(uint32_t G);
+size_t fused_hot_bytes();
 size_t fused_acc_bytes(uint32_t G);
 constexpr uint32_t kFusedMaxRows = 16384;  // rows the per-bucket LDS tables hold
 
