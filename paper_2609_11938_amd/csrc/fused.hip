@@ -44,6 +44,9 @@ constexpr int kBuckets = 256;                  // buckets of operator rows
 constexpr int kBktStride = kBuckets + 1;
 constexpr int kHot = 32;                       // combine waves of the unattributed row
 constexpr int kSplits = 16;                    // shares of the blocks per bucket
+constexpr int kPre = 8;                        // bucket entries a combine lane fetches at once
+constexpr int kList = 512;                     // partials a combine wave lists in LDS at once
+constexpr int kBatch = 8;                      // partial loads per lane in flight
 constexpr uint32_t kNoSrc = 0xFFFFFFFFu;
 constexpr uint32_t kHash = 256;                // LDS table of a block's rows (> 2 x kept)
 
@@ -532,27 +535,26 @@ __device__ __forceinline__ unsigned long long merge_field(int f, unsigned long l
   return x | y;
 }
 
-// t (an LDS row) += the partial v
-__device__ __forceinline__ void tab_add(unsigned long long *t,
-                                        const unsigned long long (&v)[kFFields], uint32_t mx) {
-  atomicAdd(t + 0, v[0]);
-  atomicAdd(t + 1, v[1]);
-  if (v[2] == 0) return;  // no matched launch: counter fields are zero
-  atomicAdd(t + 2, v[2]);
-  atomicAdd(t + 3, v[3]);
-#pragma unroll
-  for (int c = 0; c < OPATTR_NUM_COUNTERS; ++c) {
-    if ((mx >> c) & 1u) atomicMax(t + 4 + c, v[4 + c]);
-    else unsafeAtomicAdd(reinterpret_cast<double *>(t + 4 + c), bits2d(v[4 + c]));
+// t (one field f of an LDS row) += the field's value x
+__device__ __forceinline__ void field_add(unsigned long long *t, int f, unsigned long long x,
+                                          uint32_t mx) {
+  if (f < 4) {
+    atomicAdd(t, x);
+  } else if (f < 24) {
+    if ((mx >> (f - 4)) & 1u) atomicMax(t, x);
+    else unsafeAtomicAdd(reinterpret_cast<double *>(t), bits2d(x));
+  } else if ((uint32_t)x) {
+    atomicOr(reinterpret_cast<unsigned int *>(t), (uint32_t)x);
   }
-  if ((uint32_t)v[24]) atomicOr(reinterpret_cast<unsigned int *>(t + 24), (uint32_t)v[24]);
 }
 
-// Each lane takes its own blocks (a contiguous share of them per wave) and
-// their partials of the bucket one after another, the next one's loads in
-// flight while the current one is added; consecutive partials of one row are
-// added in registers (a busy row would serialise the LDS atomics of the
-// wave), rows accumulate in LDS.
+// A wave takes a share of the blocks for one bucket: its lanes fetch the
+// blocks' bucket entries eight at a time, list the partial results those
+// entries point to in LDS, and then read each partial with 25 lanes (one
+// field each, two partials per load instruction, eight loads in flight), so
+// that a partial costs two cache lines of requests instead of 25; the fields
+// are added into the wave's LDS table of the bucket's rows. The unattributed
+// row's waves add whole partials per lane in registers, then across the wave.
 template <bool DEF>
 __global__ void __launch_bounds__(64) k_f_comb(CombParams a) {
   extern __shared__ __align__(16) unsigned char comb_raw[];
@@ -598,35 +600,72 @@ __global__ void __launch_bounds__(64) k_f_comb(CombParams a) {
   wave_sync_lds();
   const int64_t per = (a.nblocks + kSplits - 1) / kSplits;
   const int64_t b_lo = (int64_t)s * per, b_hi = b_lo + per < a.nblocks ? b_lo + per : a.nblocks;
-  unsigned long long racc[kFFields];
-  uint32_t rg = 0xFFFFFFFFu;
+  uint32_t *list = reinterpret_cast<uint32_t *>(tab + ne);  // [kList] partial indices
+  const unsigned long long *parts64 = reinterpret_cast<const unsigned long long *>(a.parts);
+  const int half = ln >> 5, f = ln & 31;
+  for (int64_t b0 = b_lo; b0 < b_hi; b0 += (int64_t)OPA_WAVE * kPre) {
+    // the lane's next kPre blocks' entries for the bucket, loads in flight together
+    uint32_t ev[kPre], mine = 0;
 #pragma unroll
-  for (int f = 0; f < kFFields; ++f) racc[f] = 0;
-  for (int64_t b = b_lo + ln; b < b_hi; b += OPA_WAVE) {
-    const uint32_t e = a.bkt[b * kBktStride + q];
-    const uint32_t c = e & 0xFFu, o = e >> 8;
-    const unsigned long long *pr =
-        reinterpret_cast<const unsigned long long *>(a.parts + b * kABlockCap + o);
+    for (int k = 0; k < kPre; ++k) {
+      const int64_t b = b0 + ln + (int64_t)OPA_WAVE * k;
+      ev[k] = b < b_hi ? a.bkt[b * kBktStride + q] : 0u;
+      mine += ev[k] & 0xFFu;
+    }
+    const uint32_t incl = wave_incl_scan_add<uint32_t>(mine);
+    const uint32_t n = __shfl(incl, OPA_WAVE - 1, OPA_WAVE);
+    if (n == 0) continue;
+    if (n <= (uint32_t)kList) {
+      // the partials listed in LDS, then read by 25 lanes each (two
+      // partials per instruction, kBatch instructions in flight) and added
+      // field by field
+      uint32_t w = incl - mine;
+#pragma unroll
+      for (int k = 0; k < kPre; ++k) {
+        const uint32_t c = ev[k] & 0xFFu;
+        const uint32_t x0 = (uint32_t)((b0 + ln + (int64_t)OPA_WAVE * k) * kABlockCap) + (ev[k] >> 8);
+        for (uint32_t p = 0; p < c; ++p) list[w++] = x0 + p;
+      }
+      wave_sync_lds();
+      for (uint32_t i = 0; i < n; i += 2 * kBatch) {
+        unsigned long long v[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+          const uint32_t idx = i + 2 * j + half;
+          v[j] = (idx < n && f < kFFields)
+                     ? parts64[(size_t)list[idx] * (sizeof(PartRow) / 8) + f] : 0ull;
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+          const uint32_t g = (uint32_t)(__shfl(v[j], (ln & 32) + 24, OPA_WAVE) >> 32);
+          const uint32_t idx = i + 2 * j + half;
+          if (idx < n && f < kFFields) field_add(tab + (size_t)(g % rb) * kFFields + f, f, v[j], mx);
+        }
+      }
+    } else {
+      // more partials than the list holds (rare): one lane's entry at a
+      // time, its partials read two at a time by 25 lanes each
 #pragma unroll 1
-    for (uint32_t p = 0; p < c; ++p, pr += sizeof(PartRow) / 8) {
-      unsigned long long v[kFFields];
+      for (int k = 0; k < kPre; ++k) {
+        uint32_t e = 0;
 #pragma unroll
-      for (int f = 0; f < kFFields; ++f) v[f] = pr[f];
-      const uint32_t g = (uint32_t)(v[24] >> 32);
-      v[24] &= 0xFFFFFFFFull;
-      if (g != rg) {
-        if (rg != 0xFFFFFFFFu) tab_add(tab + (size_t)(rg % rb) * kFFields, racc, mx);
-        rg = g;
-#pragma unroll
-        for (int f = 0; f < kFFields; ++f) racc[f] = v[f];
-      } else {
-#pragma unroll
-        for (int f = 0; f < kFFields; ++f) racc[f] = merge_field(f, racc[f], v[f], mx);
+        for (int j = 0; j < kPre; ++j) e = k == j ? ev[j] : e;
+        for (uint64_t m = __ballot((e & 0xFFu) != 0); m; m &= m - 1) {
+          const int src = __ffsll((unsigned long long)m) - 1;
+          const uint32_t es = __shfl(e, src, OPA_WAVE), c = es & 0xFFu;
+          const uint64_t x0 = (uint64_t)((b0 + src + (int64_t)OPA_WAVE * k) * kABlockCap) + (es >> 8);
+          for (uint32_t p = 0; p < c; p += 2) {
+            const uint32_t pp = p + half;
+            const unsigned long long v = (pp < c && f < kFFields)
+                ? parts64[(x0 + pp) * (sizeof(PartRow) / 8) + f] : 0ull;
+            const uint32_t g = (uint32_t)(__shfl(v, (ln & 32) + 24, OPA_WAVE) >> 32);
+            if (pp < c && f < kFFields) field_add(tab + (size_t)(g % rb) * kFFields + f, f, v, mx);
+          }
+        }
       }
     }
+    wave_sync_lds();
   }
-  if (rg != 0xFFFFFFFFu) tab_add(tab + (size_t)(rg % rb) * kFFields, racc, mx);
-  wave_sync_lds();
   unsigned long long *out =
       reinterpret_cast<unsigned long long *>(a.split + ((size_t)q * kSplits + s) * rb);
   for (uint32_t x = ln; x < ne; x += OPA_WAVE) {
@@ -819,11 +858,12 @@ void run_fused_agg(const FusedIn &x, hipStream_t s) {
   c.ns = x.d->n_streams;
   c.sum = x.sum;
   const size_t lds = (size_t)rb * kFFields * 8;
+  const size_t lds_comb = lds + (size_t)kList * 4;  // the table, then the partials' list
   if (def) {
-    k_f_comb<true><<<kBuckets * kSplits + kHot, 64, lds, s>>>(c);
+    k_f_comb<true><<<kBuckets * kSplits + kHot, 64, lds_comb, s>>>(c);
     k_f_rows<true><<<kBuckets, 256, lds, s>>>(c);
   } else {
-    k_f_comb<false><<<kBuckets * kSplits + kHot, 64, lds, s>>>(c);
+    k_f_comb<false><<<kBuckets * kSplits + kHot, 64, lds_comb, s>>>(c);
     k_f_rows<false><<<kBuckets, 256, lds, s>>>(c);
   }
   probe_end(OPATTR_PROBE_AGGREGATE, s);
