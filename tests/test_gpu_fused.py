@@ -71,6 +71,49 @@ def test_fused_lstm_policies(policy):
     parity.assert_attribute(out, want, diag)
 
 
+def _regular_trace(T, run, n_ops, cycle, seed, with_ranges=True, NC=20):
+    """One stream, launches 10 ns apart (5 ns long); each range covers `run`
+    consecutive launches, the operators of consecutive ranges cycling over
+    0 .. cycle-1; every launch has a profiled row in launch order."""
+    rng = np.random.default_rng(seed)
+    seq = np.arange(T, dtype=np.uint32)
+    start = (np.arange(T, dtype=np.uint64) * 10).astype(np.uint64)
+    dur = np.full(T, 5, dtype=np.uint32)
+    name = (np.arange(T) % 7).astype(np.uint32)
+    R = T // run if with_ranges else 0
+    j = np.arange(R, dtype=np.uint64)
+    r_start = (j * run * 10).astype(np.uint64)
+    r_end = ((j * run + run - 1) * 10 + 5).astype(np.uint64)
+    return dict(seq=seq, start_ns=start, dur_ns=dur, stream_id=np.zeros(T, np.uint16),
+                name_id=name, part_id=None, pf_name=name.copy(),
+                counters=rng.random((T, NC), dtype=np.float32), r_start=r_start, r_end=r_end,
+                r_stream=np.zeros(R, np.uint16), r_op=(np.arange(R) % cycle).astype(np.uint32),
+                part_rep=None, n_names=7, n_streams=1, n_ops=n_ops, n_parts=0)
+
+
+def test_fused_combine_list_overflow():
+    """More partial results for one bucket of operator rows in a combine
+    wave's round than its LDS list holds: 64 operators of one bucket, each in
+    every block, over more blocks than one round lists (the per-entry path)."""
+    tr = _regular_trace(T=400_000, run=32, n_ops=16383, cycle=64, seed=91)
+    print(f"case combine overflow T={tr['seq'].size} R={tr['r_start'].size}", flush=True)
+    want = O.attribute(tr)
+    out, diag = _run(tr)
+    parity.assert_attribute(out, want, diag)
+
+
+@pytest.mark.parametrize("with_ranges", [False, True])
+def test_fused_unattributed(with_ranges):
+    """No ranges at all (every launch in the unattributed row, which has a
+    partial in every block and combine waves of its own), and ranges whose
+    operator rows all fall in the unattributed row's bucket."""
+    tr = _regular_trace(T=300_000, run=40, n_ops=3, cycle=3, seed=92, with_ranges=with_ranges)
+    print(f"case unattributed ranges={with_ranges}", flush=True)
+    want = O.attribute(tr)
+    out, diag = _run(tr)
+    parity.assert_attribute(out, want, diag)
+
+
 def test_fused_dedup_errors():
     """Duplicates whose representative is shorter or has another name at a
     position, and a partition split in two: the same dedup errors, statuses
