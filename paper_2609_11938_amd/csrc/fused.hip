@@ -13,14 +13,19 @@
 //    launches of one operator row form a run: a run that ends inside a lane
 //    is staged in LDS; the piece a lane ends with is carried across the
 //    wave by a segmented lane scan. A block keeps up to 128 partial results,
-//    sorts them by bucket of operator rows (256 buckets) and writes them to
-//    its own region with a (count, offset) entry per bucket; anything past
-//    that goes to a row accumulator with device-scope atomics.
+//    sorts them by bucket of operator rows (256 buckets, then the
+//    unattributed row on its own) and writes them to its own region with a
+//    (count, offset) entry per bucket; anything past that goes to a row
+//    accumulator with device-scope atomics. The blocks are taken per XCD in
+//    the order k_f_order gives (launch-order windows).
 // 2. k_f_comb: one wave per (bucket, share of the blocks) adds the bucket's
-//    partial results of those blocks in LDS and writes one partial per row.
+//    partial results of those blocks in LDS (each partial read field-wise
+//    by 25 lanes) and writes one partial per row; 32 more waves add the
+//    unattributed row's partials.
 // 3. k_f_rows: one block per bucket adds every share and the row
 //    accumulators and writes the bucket's table rows (DW-mean = sum /
-//    matched ns, NaN rules) and summary sums.
+//    matched ns, NaN rules) and summary sums; the last block to finish
+//    writes the summary and the status.
 // Integer fields are exact in any order; fp64 sums are added in an order
 // that depends on scheduling (well inside the 1e-9 tolerance); maxima are
 // exact.
