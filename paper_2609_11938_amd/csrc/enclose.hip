@@ -324,9 +324,21 @@ k_enclose(EncParams a) {
     // Phase 2, the walk up the parent chain while the range ends before the
     // query point, all of the thread's launches in lock step so that their
     // loads (ends, then parents) are in flight together.
+    // a launch whose range is the previous launch's takes its end instead of
+    // loading it again (a load whose 64 lanes hit 64 lines costs 64 L1
+    // requests; consecutive launches mostly share their range)
+    // (the previous launch's end was loaded: its range is valid for its own
+    // stream, which an index just before a stream's ranges is not)
     int64_t ek[kPer];
+    bool same[kPer];
 #pragma unroll
-    for (int k = 0; k < kPer; ++k) ek[k] = pk[k] >= lok[k] ? a.ree[pk[k]] : 0;
+    for (int k = 0; k < kPer; ++k) {
+      same[k] = k > 0 && pk[k] == pk[k - 1] && pk[k - 1] >= lok[k - 1];
+      ek[k] = (pk[k] >= lok[k] && !same[k]) ? a.ree[pk[k]] : 0;
+    }
+#pragma unroll
+    for (int k = 1; k < kPer; ++k)
+      if (pk[k] >= lok[k] && same[k]) ek[k] = ek[k - 1];
     for (int step = 0; step < kMaxWalk; ++step) {
       bool act[kPer], any = false;
 #pragma unroll
