@@ -570,7 +570,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
         print("bench.py runs on one GPU only: the attribution join of one trace is "
-              "measured on a single MI355X (see DESIGN.md for how it would shard).",
+              "measured on a single MI355X; several GPUs would each take a contiguous "
+              "share of the launches, aligned to iterations, and exchange per-name counts.",
               file=sys.stderr)
         sys.exit(2)
 
