@@ -31,58 +31,68 @@ __global__ void __launch_bounds__(256) k_rs_hist(const uint64_t *__restrict__ ke
   hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = c[threadIdx.x];
 }
 
-// Exclusive scan of a[0..n) in place by one block of 1024 threads.
-__global__ void __launch_bounds__(1024) k_scan_excl_u32(uint32_t *__restrict__ a, int64_t n) {
+// Exclusive scan of in[0..n) into out (in place when they are the same) by
+// one block of 1024 threads, 16 consecutive elements per thread per round
+// (loads of a round in flight together, 16-byte vectors when aligned);
+// returns the total to every thread.
+constexpr int kScanPer = 16;
+__device__ inline uint32_t block_scan_rounds(const uint32_t *in, uint32_t *out, int64_t n) {
   __shared__ uint32_t sh[16];
   uint32_t carry = 0;
-  for (int64_t base = 0; base < n; base += 4096) {
-    uint32_t v[4];
+  const bool vec = ((reinterpret_cast<uintptr_t>(in) | reinterpret_cast<uintptr_t>(out)) & 15) == 0;
+  for (int64_t base = 0; base < n; base += (int64_t)1024 * kScanPer) {
+    const int64_t x0 = base + (int64_t)threadIdx.x * kScanPer;
+    const bool whole = vec && x0 + kScanPer <= n;
+    uint32_t v[kScanPer];
+    if (whole) {
+      const uint4 *p = reinterpret_cast<const uint4 *>(in + x0);
+#pragma unroll
+      for (int q = 0; q < kScanPer / 4; ++q) {
+        const uint4 t = p[q];
+        v[4 * q] = t.x;
+        v[4 * q + 1] = t.y;
+        v[4 * q + 2] = t.z;
+        v[4 * q + 3] = t.w;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < kScanPer; ++j) v[j] = x0 + j < n ? in[x0 + j] : 0u;
+    }
     uint32_t s = 0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t x = base + threadIdx.x * 4 + j;
-      v[j] = x < n ? a[x] : 0u;
-      s += v[j];
-    }
+    for (int j = 0; j < kScanPer; ++j) s += v[j];
     uint32_t tot;
-    uint32_t pre = block_excl_scan_add<uint32_t>(s, sh, &tot);
-    uint32_t run = carry + pre;
+    uint32_t run = carry + block_excl_scan_add<uint32_t>(s, sh, &tot);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t x = base + threadIdx.x * 4 + j;
-      if (x < n) a[x] = run;
-      run += v[j];
+    for (int j = 0; j < kScanPer; ++j) {
+      const uint32_t t = v[j];
+      v[j] = run;
+      run += t;
+    }
+    if (whole) {
+      uint4 *p = reinterpret_cast<uint4 *>(out + x0);
+#pragma unroll
+      for (int q = 0; q < kScanPer / 4; ++q) p[q] = make_uint4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < kScanPer; ++j)
+        if (x0 + j < n) out[x0 + j] = v[j];
     }
     carry += tot;
   }
+  return carry;
+}
+
+// Exclusive scan of a[0..n) in place by one block of 1024 threads.
+__global__ void __launch_bounds__(1024) k_scan_excl_u32(uint32_t *__restrict__ a, int64_t n) {
+  block_scan_rounds(a, a, n);
 }
 
 // Exclusive scan of in[0..n) into out by one block of 1024 threads.
 __global__ void __launch_bounds__(1024) k_scan_excl_oop(const uint32_t *__restrict__ in,
                                                         uint32_t *__restrict__ out, int64_t n,
                                                         int64_t *total_out) {
-  __shared__ uint32_t sh[16];
-  uint32_t carry = 0;
-  for (int64_t base = 0; base < n; base += 4096) {
-    uint32_t v[4];
-    uint32_t s = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t x = base + threadIdx.x * 4 + j;
-      v[j] = x < n ? in[x] : 0u;
-      s += v[j];
-    }
-    uint32_t tot;
-    const uint32_t pre = block_excl_scan_add<uint32_t>(s, sh, &tot);
-    uint32_t run = carry + pre;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t x = base + threadIdx.x * 4 + j;
-      if (x < n) out[x] = run;
-      run += v[j];
-    }
-    carry += tot;
-  }
+  const uint32_t carry = block_scan_rounds(in, out, n);
   if (threadIdx.x == 0 && total_out) *total_out = carry;
 }
 
