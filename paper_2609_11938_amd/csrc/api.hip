@@ -65,10 +65,8 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.seqsort_k1 = b.take(pl.seq_dense ? 0 : T * 8);
   pl.seqsort_v0 = b.take(pl.seq_dense ? 0 : T * 4);
   pl.seqsort_v1 = b.take(pl.seq_dense ? 0 : T * 4);
-  // radix histograms: one for the seq sort, one for the range sort (the two
-  // run concurrently in opattr_attribute)
+  // radix histograms of the seq sort
   pl.rs_hist = b.take(radix_hist_entries(pl.seq_dense ? 0 : pl.T) * 4);
-  pl.rs_hist_r = b.take(radix_hist_entries(pl.ranges_nested ? 0 : pl.R) * 4);
   pl.tlh = b.take((size_t)pl.nt * NN * 4);
   pl.pfh = b.take((size_t)pl.ntp * NN * 4);
   pl.tlch = b.take((size_t)pl.ncht * NN * 4);
@@ -105,7 +103,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.rsort_k0 = b.take(rs ? R * 8 : 0);
   pl.rsort_k1 = b.take(rs ? R * 8 : 0);
   pl.rsort_v0 = b.take(rs ? R * 4 : 0);
-  pl.rsort_v1 = b.take(rs ? R * 4 : 0);
+  pl.rsort_st = b.take(rs ? R * 2 : 0);
   pl.ree = b.take(R * 8);
   pl.npg = b.take(R * 4);
   pl.mxv = b.take(R * 8);

@@ -37,7 +37,7 @@ struct Plan {
   bool seg;  // seq tiles read from per-stream segments (kernels stream-major, seq dense)
   size_t total;
   // IOM
-  size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist, rs_hist_r, kblk, tbnd;
+  size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist, kblk, tbnd;
   size_t tlh, pfh, tlch, pfch, tlc, pfc, off, slot;
   size_t pfirst, plast, pheads, prec, mbs, nbs;
   size_t bcnt;  // bucket path: bucket size of every seq tile
@@ -49,7 +49,7 @@ struct Plan {
   bool m2;  // the second set below exists
   size_t kblk2, tbnd2, tlh2, pfh2, tlch2, pfch2, tlc2, pfc2, off2, slot2, nbs2;
   // ranges
-  size_t rperm, rs_c, re_c, rst_c, rop_c, rkd_c, rsort_k0, rsort_k1, rsort_v0, rsort_v1;
+  size_t rperm, rs_c, re_c, rst_c, rop_c, rkd_c, rsort_k0, rsort_k1, rsort_v0, rsort_st;
   size_t ree, npg, mxv, rblk, tbase, tM, tnpg, tnpg2, tmx, tmx2, tfirst, tlast, sflag;
   size_t wfirst, wfused;  // per range with kinds: the walk's first op range and fused
   // aggregation
@@ -144,10 +144,6 @@ void fill_many(const FillJobs &j, hipStream_t s);
 void fill_u32(uint32_t *p, uint32_t v, int64_t n, hipStream_t s);
 void fill_u8(uint8_t *p, uint8_t v, int64_t n, hipStream_t s);
 void launch_iota(uint32_t *v, int64_t n, hipStream_t s);
-void launch_gather_key_u64(const uint64_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
-                           bool invert, hipStream_t s);
-void launch_gather_key_u16(const uint16_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
-                           hipStream_t s);
 void launch_gather_key_u32(const uint32_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
                            hipStream_t s);
 

@@ -329,23 +329,161 @@ static RangeWork range_work(const CoreRanges &cr, const opattr_dims *d, void *ws
   return w;
 }
 
-__global__ void k_gather_small(const uint16_t *st, const uint32_t *op, const uint8_t *kd,
-                               const uint32_t *perm, uint16_t *st_o, uint32_t *op_o,
-                               uint8_t *kd_o, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) {
-    const uint32_t p = perm[i];
-    st_o[i] = st[p];
-    op_o[i] = op[p];
-    if (kd) kd_o[i] = kd[p];
+// ---------------------------------------------------------------------------
+// Nesting order of ranges given in any order: a merge sort of the records
+// (stream, start, end, index) by stream asc, start asc, end desc, index asc.
+// Blocks first sort tiles of kRsTile records in LDS (bitonic network), then
+// each pass merges pairs of sorted runs; a block takes kRsTile outputs of one
+// pair, finds where they begin in each run along the merge path (a binary
+// search on the diagonal), stages the two slices in LDS and places every
+// record by its rank in the other slice. The index makes the order strict,
+// so no two records compare equal. The last pass writes the sorted start,
+// end, stream and index and gathers the operator and kind by the index.
+// ---------------------------------------------------------------------------
+constexpr int kRsTile = 2048, kRsThreads = 256;
+
+struct RSortBuf {
+  uint64_t *s, *e;
+  uint32_t *x;
+  uint16_t *st;
+};
+struct RSortOut {  // the last pass's extra outputs (op, kind gathered by index)
+  const uint32_t *op;
+  const uint8_t *kd;
+  uint32_t *op_o;
+  uint8_t *kd_o;
+};
+
+struct RRec {
+  uint64_t s, e;
+  uint32_t x, st;
+};
+__device__ __forceinline__ bool rrec_less(const RRec &a, const RRec &b) {
+  if (a.st != b.st) return a.st < b.st;
+  if (a.s != b.s) return a.s < b.s;
+  if (a.e != b.e) return a.e > b.e;
+  return a.x < b.x;
+}
+
+struct RsLds {
+  uint64_t s[kRsTile], e[kRsTile];
+  uint32_t x[kRsTile], st[kRsTile];
+  __device__ __forceinline__ RRec get(int k) const { return RRec{s[k], e[k], x[k], st[k]}; }
+  __device__ __forceinline__ void put(int k, const RRec &r) {
+    s[k] = r.s;
+    e[k] = r.e;
+    x[k] = r.x;
+    st[k] = r.st;
+  }
+};
+
+__device__ __forceinline__ RRec rrec_load(const RSortBuf &b, int64_t i) {
+  return RRec{b.s[i], b.e[i], b.x[i], b.st[i]};
+}
+__device__ __forceinline__ void rrec_store(const RSortBuf &b, const RSortOut &f, bool last,
+                                           int64_t i, const RRec &r) {
+  b.s[i] = r.s;
+  b.e[i] = r.e;
+  b.x[i] = r.x;
+  b.st[i] = (uint16_t)r.st;
+  if (last) {
+    f.op_o[i] = f.op[r.x];
+    if (f.kd) f.kd_o[i] = f.kd[r.x];
   }
 }
-void launch_gather_small(const uint16_t *st, const uint32_t *op, const uint8_t *kd,
-                         const uint32_t *perm, uint16_t *st_o, uint32_t *op_o, uint8_t *kd_o,
-                         int64_t n, hipStream_t s) {
-  if (n > 0)
-    k_gather_small<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(st, op, kd, perm, st_o, op_o, kd_o,
-                                                               n);
+
+__global__ void __launch_bounds__(kRsThreads) k_rsort_tile(const opattr_ranges r, int64_t R,
+                                                           RSortBuf out, RSortOut f, int last) {
+  __shared__ RsLds t;
+  const int tid = threadIdx.x;
+  const int64_t base = (int64_t)blockIdx.x * kRsTile;
+  for (int k = tid; k < kRsTile; k += kRsThreads) {
+    const int64_t i = base + k;
+    // records past R sort after every real one (streams are 16-bit)
+    t.put(k, i < R ? RRec{r.start_ns[i], r.end_ns[i], (uint32_t)i, r.stream_id[i]}
+                   : RRec{~0ull, 0ull, 0xFFFFFFFFu, 0xFFFFFFFFu});
+  }
+  __syncthreads();
+  for (int k = 2; k <= kRsTile; k <<= 1)
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int q = tid; q < kRsTile / 2; q += kRsThreads) {
+        const int i = 2 * q - (q & (j - 1)), p = i + j;
+        const RRec a = t.get(i), b = t.get(p);
+        if (rrec_less(b, a) == ((i & k) == 0)) {
+          t.put(i, b);
+          t.put(p, a);
+        }
+      }
+      __syncthreads();
+    }
+  const int n = (int)(R - base < kRsTile ? R - base : kRsTile);
+  for (int k = tid; k < n; k += kRsThreads) rrec_store(out, f, last != 0, base + k, t.get(k));
+}
+
+__global__ void __launch_bounds__(kRsThreads) k_rsort_merge(RSortBuf in, RSortBuf out, int64_t R,
+                                                            int64_t w, RSortOut f, int last) {
+  __shared__ RsLds t;
+  __shared__ int64_t split[2];
+  const int tid = threadIdx.x;
+  const int64_t o0 = (int64_t)blockIdx.x * kRsTile;  // first output of the block
+  const int64_t p0 = o0 / (2 * w) * (2 * w);          // first record of the pair of runs
+  const int64_t la = R - p0 < w ? R - p0 : w;
+  const int64_t rb = R - p0 - la, lb = rb < 0 ? 0 : (rb < w ? rb : w);
+  const int64_t d0 = o0 - p0, d1 = d0 + kRsTile < la + lb ? d0 + kRsTile : la + lb;
+  if (tid < 2) {
+    // records of run A among the first d outputs of the pair
+    const int64_t d = tid ? d1 : d0;
+    int64_t lo = d - lb > 0 ? d - lb : 0, hi = d < la ? d : la;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) >> 1;
+      if (rrec_less(rrec_load(in, p0 + mid), rrec_load(in, p0 + la + d - 1 - mid)))
+        lo = mid + 1;
+      else
+        hi = mid;
+    }
+    split[tid] = lo;
+  }
+  __syncthreads();
+  const int64_t i0 = split[0], i1 = split[1];
+  const int na = (int)(i1 - i0), nt = (int)(d1 - d0);
+  const int64_t b0 = p0 + la + (d0 - i0);
+  for (int k = tid; k < nt; k += kRsThreads)
+    t.put(k, rrec_load(in, k < na ? p0 + i0 + k : b0 + (k - na)));
+  __syncthreads();
+  for (int k = tid; k < nt; k += kRsThreads) {
+    const RRec v = t.get(k);
+    const bool inA = k < na;
+    // rank among the other slice: how many of its records precede v
+    int lo = inA ? na : 0, hi = inA ? nt : na;
+    const int first = lo;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (rrec_less(t.get(mid), v))
+        lo = mid + 1;
+      else
+        hi = mid;
+    }
+    const int pos = (inA ? k : k - na) + (lo - first);
+    rrec_store(out, f, last != 0, o0 + pos, v);
+  }
+}
+
+// Sorts ranges into nesting order; the result lands in `fin` (with op and
+// kind in f), `tmp` is the other buffer of the passes.
+static void sort_ranges(const opattr_ranges *r, int64_t R, const RSortBuf &fin,
+                        const RSortBuf &tmp, const RSortOut &f, hipStream_t s) {
+  int np = 0;
+  for (int64_t w = kRsTile; w < R; w *= 2) ++np;
+  const unsigned nb = (unsigned)((R + kRsTile - 1) / kRsTile);
+  // the passes alternate buffers; start so that the last one writes fin
+  const RSortBuf *cur = (np % 2 == 0) ? &fin : &tmp;
+  k_rsort_tile<<<nb, kRsThreads, 0, s>>>(*r, R, *cur, f, np == 0 ? 1 : 0);
+  int q = 0;
+  for (int64_t w = kRsTile; w < R; w *= 2, ++q) {
+    const RSortBuf *nxt = cur == &fin ? &tmp : &fin;
+    k_rsort_merge<<<nb, kRsThreads, 0, s>>>(*cur, *nxt, R, w, f, q == np - 1 ? 1 : 0);
+    cur = nxt;
+  }
 }
 
 // range_parent[perm(x)] = perm(parent of x) for valid ranges, else -1
@@ -379,27 +517,13 @@ CoreRanges prepare_ranges(const opattr_ranges *r, const opattr_dims *d, void *ws
     cr.perm = nullptr;
     if (validate && R > 1) k_rcheck<<<(unsigned)((R + 255) / 256), 256, 0, s>>>(cr, diag);
   } else if (R > 0) {
-    // nesting order by three stable LSD sorts: end desc, then start asc, then
-    // stream; equal keys keep input order, so identical intervals nest by index
-    uint64_t *K[2] = {at<uint64_t>(ws, pl.rsort_k0), at<uint64_t>(ws, pl.rsort_k1)};
-    uint32_t *V[2] = {at<uint32_t>(ws, pl.rsort_v0), at<uint32_t>(ws, pl.rsort_v1)};
-    uint32_t *hist = at<uint32_t>(ws, pl.rs_hist_r);
-    int cur = 0;
-    launch_iota(V[0], R, s);
-    launch_gather_key_u64(r->end_ns, V[cur], K[cur], R, true, s);
-    cur ^= radix_sort_pairs(K[cur], V[cur], K[cur ^ 1], V[cur ^ 1], R, 0, 64, hist, s) ? 1 : 0;
-    launch_gather_key_u64(r->start_ns, V[cur], K[cur], R, false, s);
-    cur ^= radix_sort_pairs(K[cur], V[cur], K[cur ^ 1], V[cur ^ 1], R, 0, 64, hist, s) ? 1 : 0;
-    launch_gather_key_u16(r->stream_id, V[cur], K[cur], R, s);
-    cur ^= radix_sort_pairs(K[cur], V[cur], K[cur ^ 1], V[cur ^ 1], R, 0, 16, hist, s) ? 1 : 0;
-    const uint32_t *perm = V[cur];
-    uint64_t *sc = at<uint64_t>(ws, pl.rs_c), *ec = at<uint64_t>(ws, pl.re_c);
-    launch_gather_key_u64(r->start_ns, perm, sc, R, false, s);
-    launch_gather_key_u64(r->end_ns, perm, ec, R, false, s);
-    note(hipMemcpyAsync(at<uint32_t>(ws, pl.rperm), perm, (size_t)R * 4, hipMemcpyDeviceToDevice, s));
-    launch_gather_small(r->stream_id, r->op_id, r->kind, at<uint32_t>(ws, pl.rperm),
-                        at<uint16_t>(ws, pl.rst_c), at<uint32_t>(ws, pl.rop_c),
-                        at<uint8_t>(ws, pl.rkd_c), R, s);
+    RSortBuf fin{at<uint64_t>(ws, pl.rs_c), at<uint64_t>(ws, pl.re_c), at<uint32_t>(ws, pl.rperm),
+                 at<uint16_t>(ws, pl.rst_c)};
+    RSortBuf tmp{at<uint64_t>(ws, pl.rsort_k0), at<uint64_t>(ws, pl.rsort_k1),
+                 at<uint32_t>(ws, pl.rsort_v0), at<uint16_t>(ws, pl.rsort_st)};
+    RSortOut f{r->op_id, r->kind, at<uint32_t>(ws, pl.rop_c), at<uint8_t>(ws, pl.rkd_c)};
+    sort_ranges(r, R, fin, tmp, f, s);
+    const uint64_t *sc = fin.s, *ec = fin.e;
     cr.s = sc;
     cr.e = ec;
     cr.st = at<uint16_t>(ws, pl.rst_c);

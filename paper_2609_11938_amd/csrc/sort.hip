@@ -292,18 +292,6 @@ __global__ void k_iota(uint32_t *v, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) v[i] = (uint32_t)i;
 }
-__global__ void k_gather_u64(const uint64_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
-                             bool invert) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) {
-    const uint64_t v = src[perm[i]];
-    dst[i] = invert ? ~v : v;
-  }
-}
-__global__ void k_gather_u16(const uint16_t *src, const uint32_t *perm, uint64_t *dst, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) dst[i] = src[perm[i]];
-}
 __global__ void k_gather_u32(const uint32_t *src, const uint32_t *perm, uint64_t *dst, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) dst[i] = src[perm[i]];
@@ -356,14 +344,6 @@ void fill_u8(uint8_t *p, uint8_t v, int64_t n, hipStream_t s) {
 }
 void launch_iota(uint32_t *v, int64_t n, hipStream_t s) {
   if (n > 0) k_iota<<<blocks_for(n, 256), 256, 0, s>>>(v, n);
-}
-void launch_gather_key_u64(const uint64_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
-                           bool invert, hipStream_t s) {
-  if (n > 0) k_gather_u64<<<blocks_for(n, 256), 256, 0, s>>>(src, perm, dst, n, invert);
-}
-void launch_gather_key_u16(const uint16_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
-                           hipStream_t s) {
-  if (n > 0) k_gather_u16<<<blocks_for(n, 256), 256, 0, s>>>(src, perm, dst, n);
 }
 void launch_gather_key_u32(const uint32_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
                            hipStream_t s) {

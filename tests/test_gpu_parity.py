@@ -133,6 +133,24 @@ def test_random_traces_with_ties(seed):
         parity.assert_attribute(out2, want2, diag2)
 
 
+@pytest.mark.parametrize("R,S,t_max,nested,min_r", [(2049, 1, 300, True, 2049),
+                                                    (6143, 3, 200, False, 6143),
+                                                    (9001, 2, 40, False, 9001),
+                                                    (20000, 5, 3000, True, 16000)])
+def test_unordered_ranges_past_one_sort_tile(R, S, t_max, nested, min_r):
+    """Ranges in random order, more of them than one sorting tile holds
+    (2048): the merge passes of the nesting-order sort, a ragged last run,
+    and (with a short time span) many identical intervals, which nest by
+    index. Checked through the innermost ranges against the oracle."""
+    tr = cases.random_trace(7100 + R, T=30_000, S=S, n_names=40, R=R, n_ops=31, t_max=t_max,
+                            max_depth=6, nested=nested)
+    print(f"case unordered ranges R={tr['r_start'].size} S={S} t_max={t_max}", flush=True)
+    assert tr["r_start"].size >= min_r
+    want = O.attribute(tr)
+    out, diag = _run(tr)
+    parity.assert_attribute(out, want, diag)
+
+
 @pytest.mark.parametrize("n_names,n_ops", [(5000, 50), (7000, 7000), (4096, 6143), (4097, 6144)])
 def test_many_names_and_rows(n_names, n_ops):
     """Name and operator-row counts past the LDS-counter limits take the
