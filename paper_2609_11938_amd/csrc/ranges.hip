@@ -334,13 +334,15 @@ static RangeWork range_work(const CoreRanges &cr, const opattr_dims *d, void *ws
 // (stream, start, end, index) by stream asc, start asc, end desc, index asc.
 // Blocks first sort tiles of kRsTile records in LDS (bitonic network), then
 // each pass merges pairs of sorted runs; a block takes kRsTile outputs of one
-// pair, finds where they begin in each run along the merge path (a binary
-// search on the diagonal), stages the two slices in LDS and places every
-// record by its rank in the other slice. The index makes the order strict,
+// pair, finds where they begin in each run along the merge path (a search on
+// the diagonal, 64 probes per step across a wave), stages the two slices in
+// LDS and places every record by its rank in the other slice (binary
+// searches, a thread's records searched together). The index makes the order strict,
 // so no two records compare equal. The last pass writes the sorted start,
 // end, stream and index and gathers the operator and kind by the index.
 // ---------------------------------------------------------------------------
-constexpr int kRsTile = 2048, kRsThreads = 256;
+constexpr int kRsTile = 1024, kRsThreads = 256, kRsPer = kRsTile / kRsThreads;
+constexpr int kRsSteps = 11;  // binary search steps over at most kRsTile records
 
 struct RSortBuf {
   uint64_t *s, *e;
@@ -420,28 +422,38 @@ __global__ void __launch_bounds__(kRsThreads) k_rsort_tile(const opattr_ranges r
   for (int k = tid; k < n; k += kRsThreads) rrec_store(out, f, last != 0, base + k, t.get(k));
 }
 
+// Records of run A among the first d outputs of merging A = in[pa, pa + la)
+// with B = in[pb, pb + lb): the first m where A[m] does not precede
+// B[d - 1 - m]. One wave; each step probes 64 evenly spaced candidates.
+__device__ int64_t merge_split(const RSortBuf &in, int64_t pa, int64_t la, int64_t pb,
+                               int64_t lb, int64_t d) {
+  int64_t lo = d - lb > 0 ? d - lb : 0, hi = d < la ? d : la;
+  const int ln = lane_id();
+  while (lo < hi) {  // uniform over the wave
+    const int64_t step = (hi - lo + OPA_WAVE - 1) / OPA_WAVE, m = lo + ln * step;
+    const bool p = m < hi && rrec_less(rrec_load(in, pa + m), rrec_load(in, pb + d - 1 - m));
+    const int c = __popcll(__ballot(p));  // the predicate holds on a prefix of the probes
+    if (c == 0) break;
+    const int64_t ff = lo + (int64_t)c * step;  // first probe where it fails (or past hi)
+    lo = lo + (int64_t)(c - 1) * step + 1;
+    hi = ff < hi ? ff : hi;
+  }
+  return lo;
+}
+
 __global__ void __launch_bounds__(kRsThreads) k_rsort_merge(RSortBuf in, RSortBuf out, int64_t R,
                                                             int64_t w, RSortOut f, int last) {
   __shared__ RsLds t;
   __shared__ int64_t split[2];
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, wv = wave_id();
   const int64_t o0 = (int64_t)blockIdx.x * kRsTile;  // first output of the block
   const int64_t p0 = o0 / (2 * w) * (2 * w);          // first record of the pair of runs
   const int64_t la = R - p0 < w ? R - p0 : w;
   const int64_t rb = R - p0 - la, lb = rb < 0 ? 0 : (rb < w ? rb : w);
   const int64_t d0 = o0 - p0, d1 = d0 + kRsTile < la + lb ? d0 + kRsTile : la + lb;
-  if (tid < 2) {
-    // records of run A among the first d outputs of the pair
-    const int64_t d = tid ? d1 : d0;
-    int64_t lo = d - lb > 0 ? d - lb : 0, hi = d < la ? d : la;
-    while (lo < hi) {
-      const int64_t mid = (lo + hi) >> 1;
-      if (rrec_less(rrec_load(in, p0 + mid), rrec_load(in, p0 + la + d - 1 - mid)))
-        lo = mid + 1;
-      else
-        hi = mid;
-    }
-    split[tid] = lo;
+  if (wv < 2) {
+    const int64_t sp = merge_split(in, p0, la, p0 + la, lb, wv ? d1 : d0);
+    if (lane_id() == 0) split[wv] = sp;
   }
   __syncthreads();
   const int64_t i0 = split[0], i1 = split[1];
@@ -450,21 +462,36 @@ __global__ void __launch_bounds__(kRsThreads) k_rsort_merge(RSortBuf in, RSortBu
   for (int k = tid; k < nt; k += kRsThreads)
     t.put(k, rrec_load(in, k < na ? p0 + i0 + k : b0 + (k - na)));
   __syncthreads();
-  for (int k = tid; k < nt; k += kRsThreads) {
-    const RRec v = t.get(k);
+  // rank of each record among the other slice: how many of its records precede it
+  RRec v[kRsPer];
+  int lo[kRsPer], hi[kRsPer], first[kRsPer];
+#pragma unroll
+  for (int u = 0; u < kRsPer; ++u) {
+    const int k = tid + u * kRsThreads;
     const bool inA = k < na;
-    // rank among the other slice: how many of its records precede v
-    int lo = inA ? na : 0, hi = inA ? nt : na;
-    const int first = lo;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (rrec_less(t.get(mid), v))
-        lo = mid + 1;
-      else
-        hi = mid;
+    v[u] = t.get(k < nt ? k : 0);
+    lo[u] = k >= nt ? 0 : (inA ? na : 0);
+    hi[u] = k >= nt ? 0 : (inA ? nt : na);
+    first[u] = lo[u];
+  }
+#pragma unroll
+  for (int q = 0; q < kRsSteps; ++q)
+#pragma unroll
+    for (int u = 0; u < kRsPer; ++u)
+      if (lo[u] < hi[u]) {
+        const int mid = (lo[u] + hi[u]) >> 1;
+        if (rrec_less(t.get(mid), v[u]))
+          lo[u] = mid + 1;
+        else
+          hi[u] = mid;
+      }
+#pragma unroll
+  for (int u = 0; u < kRsPer; ++u) {
+    const int k = tid + u * kRsThreads;
+    if (k < nt) {
+      const int pos = (k < na ? k : k - na) + (lo[u] - first[u]);
+      rrec_store(out, f, last != 0, o0 + pos, v[u]);
     }
-    const int pos = (inA ? k : k - na) + (lo - first);
-    rrec_store(out, f, last != 0, o0 + pos, v);
   }
 }
 
