@@ -195,7 +195,7 @@ __global__ void __launch_bounds__(256) k_item_scatter_w(AggWork w) {
 
 // 1'. many rows: one stable radix sort of (row, item) over the items (the
 // sort reads the item count on the device)
-__global__ void k_item_keys(AggWork w, unsigned long long *k0, uint32_t *v0, int64_t cap) {
+__global__ void k_item_keys(AggWork w, uint32_t *k0, uint32_t *v0, int64_t cap) {
   const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (x >= cap || x >= w.meta[0]) return;
   k0[x] = w.ig[x];
@@ -203,7 +203,7 @@ __global__ void k_item_keys(AggWork w, unsigned long long *k0, uint32_t *v0, int
 }
 
 // sorted items in place
-__global__ void k_item_place(AggWork w, const unsigned long long *key, const uint32_t *val,
+__global__ void k_item_place(AggWork w, const uint32_t *key, const uint32_t *val,
                              int64_t cap) {
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= cap || p >= w.meta[0]) return;
@@ -213,7 +213,7 @@ __global__ void k_item_place(AggWork w, const unsigned long long *key, const uin
 
 // row offsets: goff[g] = the first sorted item of row g or later (the
 // item count for g = G)
-__global__ void k_row_bounds(AggWork w, const unsigned long long *key, int64_t cap) {
+__global__ void k_row_bounds(AggWork w, const uint32_t *key, int64_t cap) {
   const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (g > (int64_t)w.G) return;
   const int64_t n = w.meta[0] < cap ? w.meta[0] : cap;
@@ -573,15 +573,13 @@ void plan_items(const EncArgs &x, hipStream_t s) {
     if (pl.T > 0) k_item_scatter_w<<<tgrid, 256, lds, s>>>(w);
   } else {
     const int64_t cap = pl.cap_items;
-    unsigned long long *k0 = at<unsigned long long>(x.ws, pl.isort_k0);
-    unsigned long long *k1 = at<unsigned long long>(x.ws, pl.isort_k1);
+    uint32_t *k0 = at<uint32_t>(x.ws, pl.isort_k0), *k1 = at<uint32_t>(x.ws, pl.isort_k1);
     uint32_t *v0 = at<uint32_t>(x.ws, pl.isort_v0), *v1 = at<uint32_t>(x.ws, pl.isort_v1);
     bool in1 = false;
     if (cap > 0) {
       k_item_keys<<<(unsigned)((cap + 255) / 256), 256, 0, s>>>(w, k0, v0, cap);
       const int bits = (bits_for_host(pl.G) + 7) & ~7;
-      in1 = radix_sort_pairs(reinterpret_cast<uint64_t *>(k0), v0,
-                             reinterpret_cast<uint64_t *>(k1), v1, cap, 0, bits,
+      in1 = radix_sort_pairs(k0, v0, k1, v1, cap, 0, bits,
                              at<uint32_t>(x.ws, pl.isort_hist), s, w.meta);
     }
     if (cap > 0)

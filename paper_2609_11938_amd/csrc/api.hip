@@ -61,8 +61,8 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.kblk = b.take(pl.seg ? ((size_t)pl.NS + 2) * 8 : 0);
   pl.tbnd = b.take(pl.seg ? ((size_t)pl.nt + 1) * pl.NS * 4 : 0);
   pl.rk = b.take(pl.seq_dense ? 0 : T * 4);
-  pl.seqsort_k0 = b.take(pl.seq_dense ? 0 : T * 8);
-  pl.seqsort_k1 = b.take(pl.seq_dense ? 0 : T * 8);
+  pl.seqsort_k0 = b.take(pl.seq_dense ? 0 : T * 4);
+  pl.seqsort_k1 = b.take(pl.seq_dense ? 0 : T * 4);
   pl.seqsort_v0 = b.take(pl.seq_dense ? 0 : T * 4);
   pl.seqsort_v1 = b.take(pl.seq_dense ? 0 : T * 4);
   // radix histograms of the seq sort
@@ -139,8 +139,8 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.ith = b.take(few_rows ? (size_t)pl.ntrt * pl.G * 4 : 0);
   pl.itch = b.take(few_rows ? (size_t)pl.nchr * pl.G * 4 : 0);
   const size_t ni = few_rows ? 0 : (size_t)pl.cap_items;
-  pl.isort_k0 = b.take(ni * 8);
-  pl.isort_k1 = b.take(ni * 8);
+  pl.isort_k0 = b.take(ni * 4);
+  pl.isort_k1 = b.take(ni * 4);
   pl.isort_v0 = b.take(ni * 4);
   pl.isort_v1 = b.take(ni * 4);
   pl.isort_hist = b.take(few_rows ? 0 : radix_hist_entries((int64_t)ni) * 4);

@@ -124,9 +124,11 @@ inline int bits_for_host(uint32_t v) {
 }
 // inclusive scan of n int64 values in place; scratch holds n / 4096 + 1 values
 void scan_incl_i64_inplace(int64_t *a, int64_t n, int64_t *scratch, hipStream_t s);
-// n_dev (optional): the element count on the device (<= n); only that many
-// are sorted
-bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, int64_t n,
+// Stable LSD sort of (32-bit key, value) pairs by key bits [begin_bit,
+// end_bit), 8 bits a pass; true when the result is in (k1, v1). n_dev
+// (optional): the element count on the device (<= n); only that many are
+// sorted
+bool radix_sort_pairs(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n,
                       int begin_bit, int end_bit, uint32_t *hist, hipStream_t s,
                       const int64_t *n_dev = nullptr);
 size_t radix_hist_entries(int64_t n);
@@ -144,8 +146,8 @@ void fill_many(const FillJobs &j, hipStream_t s);
 void fill_u32(uint32_t *p, uint32_t v, int64_t n, hipStream_t s);
 void fill_u8(uint8_t *p, uint8_t v, int64_t n, hipStream_t s);
 void launch_iota(uint32_t *v, int64_t n, hipStream_t s);
-void launch_gather_key_u32(const uint32_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
-                           hipStream_t s);
+// k[i] = src[i], v[i] = i
+void launch_key_pairs(const uint32_t *src, uint32_t *k, uint32_t *v, int64_t n, hipStream_t s);
 
 // ---- IOM (iom.hip) -----------------------------------------------------------
 // Per partition p, how its launches find their row:

@@ -49,7 +49,7 @@ __global__ void k_seqview_dense(const uint32_t *__restrict__ seq, int64_t T, int
   }
 }
 
-__global__ void k_seqview_sorted(const uint64_t *__restrict__ keys, const uint32_t *__restrict__ vals,
+__global__ void k_seqview_sorted(const uint32_t *__restrict__ keys, const uint32_t *__restrict__ vals,
                                  int64_t T, int32_t *sv, int32_t *rk, opattr_diag *diag) {
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= T) return;
@@ -73,10 +73,9 @@ void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, con
     return;
   }
   probe_begin(OPATTR_PROBE_SEQ_VIEW, s);
-  uint64_t *k0 = at<uint64_t>(ws, pl.seqsort_k0), *k1 = at<uint64_t>(ws, pl.seqsort_k1);
+  uint32_t *k0 = at<uint32_t>(ws, pl.seqsort_k0), *k1 = at<uint32_t>(ws, pl.seqsort_k1);
   uint32_t *v0 = at<uint32_t>(ws, pl.seqsort_v0), *v1 = at<uint32_t>(ws, pl.seqsort_v1);
-  launch_iota(v0, T, s);
-  launch_gather_key_u32(k->seq, v0, k0, T, s);
+  launch_key_pairs(k->seq, k0, v0, T, s);
   const bool in1 = radix_sort_pairs(k0, v0, k1, v1, T, 0, 32, at<uint32_t>(ws, pl.rs_hist), s);
   k_seqview_sorted<<<nb, 256, 0, s>>>(in1 ? k1 : k0, in1 ? v1 : v0, T, sv,
                                        at<int32_t>(ws, pl.rk), diag);

@@ -15,7 +15,7 @@ __device__ __forceinline__ int64_t sort_count(int64_t n, const int64_t *n_dev) {
   return m < n ? (m > 0 ? m : 0) : n;
 }
 
-__global__ void __launch_bounds__(256) k_rs_hist(const uint64_t *__restrict__ keys, int64_t n_cap,
+__global__ void __launch_bounds__(256) k_rs_hist(const uint32_t *__restrict__ keys, int64_t n_cap,
                                                  const int64_t *n_dev, int shift,
                                                  uint32_t *__restrict__ hist, int64_t ntiles) {
   __shared__ uint32_t c[256];
@@ -216,51 +216,68 @@ void launch_scan_excl(const uint32_t *in, uint32_t *out, int64_t n, int64_t *tot
   k_scan_excl_oop<<<1, 1024, 0, s>>>(in, out, n, total_out);
 }
 
-__global__ void __launch_bounds__(256) k_rs_scatter(const uint64_t *__restrict__ kin,
+// One pass of the stable LSD sort over a tile of OPA_TILE pairs: the rank of
+// each pair among the tile's pairs of its digit (wave match of the digit,
+// then the counts scanned over chunks and waves), the pairs placed in digit
+// order in LDS, then written out in that order so that each digit's run goes
+// to consecutive addresses.
+__global__ void __launch_bounds__(256) k_rs_scatter(const uint32_t *__restrict__ kin,
                                                     const uint32_t *__restrict__ vin,
-                                                    uint64_t *__restrict__ kout,
+                                                    uint32_t *__restrict__ kout,
                                                     uint32_t *__restrict__ vout, int64_t n_cap,
                                                     const int64_t *n_dev, int shift,
                                                     const uint32_t *__restrict__ offs,
                                                     int64_t ntiles) {
   __shared__ uint16_t cnt[OPA_TILE_CHUNKS][4][256];
+  __shared__ uint32_t lk[OPA_TILE], lv[OPA_TILE];
+  __shared__ uint32_t dbase[256], gbase[256], sh[4];
   const int tid = threadIdx.x, w = wave_id();
   const int64_t n = sort_count(n_cap, n_dev);
   const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
   if (base >= n) return;  // uniform over the block
   for (int i = tid; i < OPA_TILE_CHUNKS * 4 * 256; i += 256) (&cnt[0][0][0])[i] = 0;
   __syncthreads();
-  uint32_t dig[OPA_TILE_CHUNKS], lr[OPA_TILE_CHUNKS];
+  uint32_t key[OPA_TILE_CHUNKS], val[OPA_TILE_CHUNKS], lr[OPA_TILE_CHUNKS];
 #pragma unroll
   for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
     const int64_t x = base + c * 256 + tid;
-    // elements past n sit after every valid one, so they never precede one
-    const uint32_t d = x < n ? (uint32_t)((kin[x] >> shift) & 255u) : 0u;
-    const uint64_t pm = peers8(d);
-    dig[c] = d;
+    const bool ok = x < n;  // pairs past n are the wave's last lanes
+    key[c] = ok ? kin[x] : 0u;
+    val[c] = ok ? vin[x] : 0u;
+    const uint32_t d = (key[c] >> shift) & 255u;
+    const uint64_t pm = peers8(d) & __ballot(ok);
     lr[c] = (uint32_t)__popcll(pm & lanemask_lt());
-    if ((pm & lanemask_lt()) == 0) cnt[c][w][d] = (uint16_t)__popcll(pm);
+    if (ok && (pm & lanemask_lt()) == 0) cnt[c][w][d] = (uint16_t)__popcll(pm);
   }
   __syncthreads();
-  {
-    uint32_t run = 0;
-    for (int c = 0; c < OPA_TILE_CHUNKS; ++c)
-      for (int ww = 0; ww < 4; ++ww) {
-        const uint32_t v = cnt[c][ww][tid];
-        cnt[c][ww][tid] = (uint16_t)run;
-        run += v;
-      }
-  }
+  uint32_t tot = 0;  // thread d: the tile's pairs of digit d
+  for (int c = 0; c < OPA_TILE_CHUNKS; ++c)
+    for (int ww = 0; ww < 4; ++ww) {
+      const uint32_t v = cnt[c][ww][tid];
+      cnt[c][ww][tid] = (uint16_t)tot;
+      tot += v;
+    }
+  const uint32_t db = block_excl_scan_add<uint32_t>(tot, sh, nullptr);
+  dbase[tid] = db;
+  gbase[tid] = offs[(int64_t)tid * ntiles + blockIdx.x];
   __syncthreads();
 #pragma unroll
   for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
     const int64_t x = base + c * 256 + tid;
     if (x < n) {
-      const uint32_t d = dig[c];
-      const uint32_t dst = offs[(int64_t)d * ntiles + blockIdx.x] + cnt[c][w][d] + lr[c];
-      kout[dst] = kin[x];
-      vout[dst] = vin[x];
+      const uint32_t d = (key[c] >> shift) & 255u;
+      const uint32_t lp = dbase[d] + cnt[c][w][d] + lr[c];
+      lk[lp] = key[c];
+      lv[lp] = val[c];
     }
+  }
+  __syncthreads();
+  const int nl = (int)(n - base < OPA_TILE ? n - base : OPA_TILE);
+  for (int j = tid; j < nl; j += 256) {
+    const uint32_t k = lk[j], d = (k >> shift) & 255u;
+    const uint32_t dst = gbase[d] + ((uint32_t)j - dbase[d]);
+    kout[dst] = k;
+    vout[dst] = lv[j];
   }
 }
 
@@ -271,14 +288,14 @@ size_t radix_hist_entries(int64_t n) {
   return (size_t)h + scan_scratch_entries(h);
 }
 
-bool radix_sort_pairs(uint64_t *k0, uint32_t *v0, uint64_t *k1, uint32_t *v1, int64_t n,
+bool radix_sort_pairs(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n,
                       int begin_bit, int end_bit, uint32_t *hist, hipStream_t s,
                       const int64_t *n_dev) {
   if (n <= 0) return false;
   const int64_t nt = (n + OPA_TILE - 1) / OPA_TILE;
   bool in1 = false;
   for (int sh = begin_bit; sh < end_bit; sh += 8) {
-    uint64_t *ki = in1 ? k1 : k0, *ko = in1 ? k0 : k1;
+    uint32_t *ki = in1 ? k1 : k0, *ko = in1 ? k0 : k1;
     uint32_t *vi = in1 ? v1 : v0, *vo = in1 ? v0 : v1;
     k_rs_hist<<<(unsigned)nt, 256, 0, s>>>(ki, n, n_dev, sh, hist, nt);
     scan_excl_inplace(hist, nt * 256, hist + nt * 256, s);
@@ -292,9 +309,13 @@ __global__ void k_iota(uint32_t *v, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) v[i] = (uint32_t)i;
 }
-__global__ void k_gather_u32(const uint32_t *src, const uint32_t *perm, uint64_t *dst, int64_t n) {
+// pairs (src[i], i) for a sort of src
+__global__ void k_key_pairs(const uint32_t *src, uint32_t *k, uint32_t *v, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) dst[i] = src[perm[i]];
+  if (i < n) {
+    k[i] = src[i];
+    v[i] = (uint32_t)i;
+  }
 }
 
 __global__ void k_fill_u32(uint32_t *p, uint32_t v, int64_t n) {
@@ -345,9 +366,8 @@ void fill_u8(uint8_t *p, uint8_t v, int64_t n, hipStream_t s) {
 void launch_iota(uint32_t *v, int64_t n, hipStream_t s) {
   if (n > 0) k_iota<<<blocks_for(n, 256), 256, 0, s>>>(v, n);
 }
-void launch_gather_key_u32(const uint32_t *src, const uint32_t *perm, uint64_t *dst, int64_t n,
-                           hipStream_t s) {
-  if (n > 0) k_gather_u32<<<blocks_for(n, 256), 256, 0, s>>>(src, perm, dst, n);
+void launch_key_pairs(const uint32_t *src, uint32_t *k, uint32_t *v, int64_t n, hipStream_t s) {
+  if (n > 0) k_key_pairs<<<blocks_for(n, 256), 256, 0, s>>>(src, k, v, n);
 }
 
 }  // namespace opa
