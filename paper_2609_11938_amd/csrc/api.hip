@@ -38,11 +38,11 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   pl.seq_dense = (d->flags & OPATTR_SEQ_DENSE) != 0;
   pl.ranges_nested = (d->flags & OPATTR_RANGES_NESTED) != 0;
   // seq tiles straight from per-stream segments: needs both kernel promises,
-  // a matching stage (profiled rows given) and few streams and names; under
-  // OPATTR_VALIDATE the general path runs (it checks what it relies on)
-  pl.seg = (d->flags & OPATTR_KERNELS_STREAM_MAJOR) && pl.seq_dense &&
-           !(d->flags & OPATTR_VALIDATE) && p != nullptr && pl.NS >= 1 &&
-           pl.NS <= 64 && pl.NN <= kFastNames;
+  // a matching stage (profiled rows given) and few streams and names (under
+  // OPATTR_VALIDATE both promises are checked beside it: the layout by
+  // check_kernel_layout, the density by the launch-order view's scatter)
+  pl.seg = (d->flags & OPATTR_KERNELS_STREAM_MAJOR) && pl.seq_dense && p != nullptr &&
+           pl.NS >= 1 && pl.NS <= 64 && pl.NN <= kFastNames;
   pl.nt = (pl.T + OPA_TILE - 1) / OPA_TILE;
   pl.ntp = (pl.P + OPA_TILE - 1) / OPA_TILE;
   pl.ncht = (pl.nt + kColChunk - 1) / kColChunk;
@@ -556,10 +556,19 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
     note(hipEventRecord(ss->fork, s));
     note(hipStreamWaitEvent(s2, ss->fork, 0));
   }
+  const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
+  if (validate) {
+    // the layout check goes first on the profiled rows' stream, whose work
+    // ends before the other two streams' (the density of seq is checked in
+    // the matching's tiles)
+    const hipStream_t sc = ss ? ss->s2 : s;
+    if (ss) note(hipStreamWaitEvent(sc, ss->fork, 0));
+    check_kernel_layout(k, d, diag, sc);
+  }
   FillJobs acc;  // the fused aggregation's accumulators, cleared with the ranges' state
   fused_acc_clear(acc, ws, pl);
   probe_begin(OPATTR_PROBE_RANGES, s2);
-  const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, false, s2, &acc);
+  const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s2, &acc);
   resolve_ranges(cr, d, ws, pl, range_depth, diag, s2, true);
   probe_end(OPATTR_PROBE_RANGES, s2);
   EncArgs e{};
@@ -580,7 +589,7 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
   e.range_depth = range_depth;
   run_enclose(e, s2);
   if (ss) note(hipEventRecord(ss->join, s2));
-  IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, false};
+  IomArgs a{k, p, d, policy, match, name_counts, diag, ws, &pl, true, validate};
   a.buckets = true;
   a.fused_order = ss != nullptr;  // only where the profiled side has a stream of its own
   if (ss) {
@@ -626,11 +635,11 @@ static int attribute_call(const opattr_kernels *k, const opattr_profiled *p,
                           uint8_t *range_depth, uint32_t *name_counts, opattr_op_row *table,
                           opattr_summary *sum, opattr_diag *diag, void *ws, const Plan &pl,
                           hipStream_t s, bool fork) {
-  check_kernel_layout(k, d, diag, s);
-  const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
   if (pl.fused) return attribute_fused(k, p, r, d, policy, agg_kind, match, range_id,
                                        range_depth, name_counts, table, sum, diag, ws, pl, s,
                                        fork);
+  check_kernel_layout(k, d, diag, s);
+  const bool validate = (d->flags & OPATTR_VALIDATE) != 0;
   // the ranges, the enclosure and the aggregation plan do not depend on the
   // matching: they run on a side stream of this device, joined back before
   // the run reduction (counts) and the per-row reduction (items)

@@ -35,12 +35,25 @@ __global__ void k_seqview_dense(const uint32_t *__restrict__ seq, int64_t T, int
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= T) return;
   const uint32_t s = seq[i];
+  const bool bad = (int64_t)s >= T && validate;
+  if ((int64_t)s < T) sv[s] = (int32_t)i;
+  const uint64_t m = __ballot(bad);
+  if (m && lane_id() == __ffsll((unsigned long long)m) - 1) {
+    atomicAdd((unsigned long long *)&diag->order_violations, (unsigned long long)__popcll(m));
+    atomicOr(&diag->flags, OPATTR_F_ORDER);
+  }
+}
+
+// Under OPATTR_VALIDATE, after the scatter: a seq value that two launches
+// hold keeps only one of them in the view, and the other finds itself
+// missing there (no atomics: each launch reads its own slot back).
+__global__ void k_seqview_check(const uint32_t *__restrict__ seq, int64_t T,
+                                const int32_t *__restrict__ sv, opattr_diag *diag) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   bool bad = false;
-  if ((int64_t)s < T) {
-    if (validate) bad = atomicCAS(&sv[s], -1, (int32_t)i) != -1;
-    else sv[s] = (int32_t)i;
-  } else {
-    bad = validate != 0;
+  if (i < T) {
+    const uint32_t s = seq[i];
+    bad = (int64_t)s < T && sv[s] != (int32_t)i;
   }
   const uint64_t m = __ballot(bad);
   if (m && lane_id() == __ffsll((unsigned long long)m) - 1) {
@@ -62,13 +75,16 @@ __global__ void k_seqview_sorted(const uint32_t *__restrict__ keys, const uint32
 void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, const Plan &pl,
                     opattr_diag *diag, bool validate, hipStream_t s) {
   const int64_t T = pl.T;
-  if (T <= 0 || pl.seg) return;  // the segment path reads tiles without the view
+  // the segment path reads tiles without the view (and checks the density
+  // of seq in them)
+  if (T <= 0 || pl.seg) return;
   int32_t *sv = at<int32_t>(ws, pl.sv);
   const unsigned nb = (unsigned)((T + 255) / 256);
   if (pl.seq_dense) {
-    fill_u32(reinterpret_cast<uint32_t *>(sv), 0xFFFFFFFFu, T, s);
+    fill_u32(reinterpret_cast<uint32_t *>(sv), 0xFFFFFFFFu, T, s);  // positions no launch claims
     probe_begin(OPATTR_PROBE_SEQ_VIEW, s);
     k_seqview_dense<<<nb, 256, 0, s>>>(k->seq, T, sv, diag, validate ? 1 : 0);
+    if (validate) k_seqview_check<<<nb, 256, 0, s>>>(k->seq, T, sv, diag);
     probe_end(OPATTR_PROBE_SEQ_VIEW, s);
     return;
   }
@@ -97,6 +113,7 @@ struct TlArgs {
   const uint32_t *bnd;  // [tiles + 1][NS]
   const int64_t *kblk;  // [NS + 1]
   uint32_t NS;
+  opattr_diag *vdiag;   // under OPATTR_VALIDATE: the density check reports here (else NULL)
 };
 
 // Element e of a tile sits in wave e / 1024, chunk (e / 64) % 16, lane e % 64.
@@ -150,6 +167,8 @@ struct TileData {
   int32_t lp[OPA_TILE];    // partition (-1 none, -2 no launch or bad id)
   SegTable sg;
   uint32_t bad;
+  uint32_t occ[OPA_TILE / 32];  // density check: positions taken
+  uint32_t placed, twice;       // density check: launches placed, on a taken position
 };
 
 // Fill TileData for seq tile t through the view. Ends with a barrier;
@@ -303,6 +322,10 @@ __device__ inline uint32_t seg_tile(const TlArgs &a, int64_t t, TileData &sm) {
     sm.key[x] = (uint16_t)a.NN;
     sm.lp[x] = -2;
   }
+  if (a.vdiag) {
+    for (int x = tid; x < OPA_TILE / 32; x += OPA_TILE_THREADS) sm.occ[x] = 0;
+    if (tid == 0) sm.placed = sm.twice = 0;
+  }
   seg_table(a, t, sm.sg);
   const int64_t ec = edge_candidate(a, t);
   __syncthreads();
@@ -333,11 +356,17 @@ __device__ inline uint32_t seg_tile(const TlArgs &a, int64_t t, TileData &sm) {
     rp[c] = (ii[c] >= 0 && ok && pt[c] >= 0) ? a.part_rep[pt[c]] : -1;
   }
   const bool eok = enm < a.NN && ept >= -1 && (ept < 0 || (uint32_t)ept < a.NP);
+  uint32_t placed = 0, twice = 0;
 #pragma unroll
   for (int c = 0; c < kWaveChunks; ++c) {
     if (ii[c] < 0) continue;
     const int64_t x = (int64_t)sq[c] - base;
     if (x < 0 || x >= OPA_TILE || base + x >= a.T) continue;  // a broken promise: left out
+    if (a.vdiag) {
+      placed++;
+      const uint32_t bit = 1u << (x & 31);
+      if (atomicOr(&sm.occ[x >> 5], bit) & bit) twice++;
+    }
     const bool ok = nm[c] < a.NN && pt[c] >= -1 && (pt[c] < 0 || (uint32_t)pt[c] < a.NP);
     if (!ok) {
       bad++;
@@ -357,7 +386,28 @@ __device__ inline uint32_t seg_tile(const TlArgs &a, int64_t t, TileData &sm) {
     const int32_t got = __shfl(lp, src, OPA_WAVE);
     if (lane_id() == 0) sm.sg.edge[side] = m ? got : -2;
   }
+  if (a.vdiag) {
+    placed = (uint32_t)wave_reduce_add((unsigned long long)placed);
+    twice = (uint32_t)wave_reduce_add((unsigned long long)twice);
+    if (lane_id() == 0 && (placed || twice)) {
+      atomicAdd(&sm.placed, placed);
+      atomicAdd(&sm.twice, twice);
+    }
+  }
   __syncthreads();
+  // Density (under OPATTR_VALIDATE): with seq sorted on every stream (checked
+  // on its own), the tiles take each launch at most once, so seq is a
+  // permutation of [0, n) exactly when every tile's positions are each taken
+  // once. Counted: launches on a taken position, plus positions left free.
+  if (a.vdiag && tid == 0) {
+    const int64_t len = a.T - base < OPA_TILE ? a.T - base : OPA_TILE;
+    const int64_t fresh = (int64_t)sm.placed - sm.twice;
+    const uint64_t v = (uint64_t)sm.twice + (uint64_t)(len - fresh);
+    if (v) {
+      atomicAdd((unsigned long long *)&a.vdiag->order_violations, (unsigned long long)v);
+      atomicOr(&a.vdiag->flags, OPATTR_F_ORDER);
+    }
+  }
   return bad;
 }
 
@@ -1274,6 +1324,7 @@ static TlArgs tl_args(const opattr_kernels *k, const opattr_dims *d, void *ws, c
   a.bnd = at<uint32_t>(ws, pl.tbnd);
   a.kblk = at<int64_t>(ws, pl.kblk);
   a.NS = d->n_streams;
+  a.vdiag = nullptr;
   return a;
 }
 
@@ -1325,6 +1376,12 @@ void run_match(const IomArgs &x, hipStream_t s) {
   clr.add(tlc, 0, NN);
   clr.add(pfc, 0, NN);
   if (parts) clear_partitions(clr, ws, pl);
+  // The tiles reach only the launches that the layout promises put in them
+  // (the segment path), or that hold their seq slot in the view; under
+  // OPATTR_VALIDATE, where a false promise must come out as an order error,
+  // every launch's match starts unmatched so that none is read unwritten.
+  // (The bucket path writes every match in storage order.)
+  if (!buckets && x.validate && x.match) clr.add(x.match, 0xFFFFFFFFu, pl.T);
   const bool seg_pro = seg && pl.nt > 0;  // clears, class-map check and stream blocks in one launch
   if (seg_pro) {
     ProArgs pa{};
@@ -1346,7 +1403,8 @@ void run_match(const IomArgs &x, hipStream_t s) {
     fill_many(clr, s);
     if (dedup) k_rep_check<<<(d->n_parts + 255) / 256, 256, 0, s>>>(d->part_rep, d->n_parts, x.diag);
   }
-  const TlArgs ta = tl_args(k, d, ws, pl, dedup);
+  TlArgs ta = tl_args(k, d, ws, pl, dedup);
+  if (seg && x.validate) ta.vdiag = x.diag;  // the density of seq, checked in the tiles
   PfArgs pa;
   pa.name = x.p->name_id;
   // the rows of this call (the plan may be sized for a longer list)

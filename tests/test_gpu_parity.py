@@ -179,6 +179,35 @@ def test_layout_promises_validated():
     assert diag2["status"] == -8 and diag2["order_violations"] > 0
 
 
+@pytest.mark.parametrize("cfg,emission,hints", [("gpt2", "stream_major", "all"),
+                                                 ("lstm", "stream_major", "all"),
+                                                 ("gpt2", "seq", "dense")])
+@pytest.mark.parametrize("kind", ["past_n", "shared"])
+def test_broken_density_validated(cfg, emission, hints, kind):
+    """Launches whose seq is not a permutation of [0, n) (every other
+    promise kept): under VALIDATE the density check reports an order error
+    -- a seq past n, or one seq value on two launches of different streams
+    (their neighbours on each stream keep their order). Covers the segment
+    path (GPT-2 shape), the fused one (LSTM shape, few ranges) and, with
+    only SEQ_DENSE promised, the launch-order view."""
+    import numpy as np
+
+    tr = dict(_trace(cfg, emission))
+    seq = tr["seq"].astype(np.int64).copy()
+    st = tr["stream_id"]
+    if kind == "past_n":
+        seq[int(np.argmax(seq))] = seq.size + 5  # the largest seq: still last on its stream
+    else:
+        order = np.argsort(seq, kind="stable")
+        k = next(j for j in range(1, order.size) if st[order[j]] != st[order[j - 1]])
+        seq[order[k]] = seq[order[k - 1]]  # v + 1 on another stream becomes v
+    tr["seq"] = seq.astype(np.uint32)
+    flags = (HINTS if hints == "all" else opattr.SEQ_DENSE) | opattr.VALIDATE
+    print(f"case broken density cfg={cfg} emission={emission} kind={kind}", flush=True)
+    _, diag = _run(tr, flags=flags)
+    assert diag["status"] == -8 and diag["order_violations"] > 0
+
+
 def test_graph_replay_matches_eager():
     """A captured opattr_attribute (both stream branches) replays to the eager
     outputs bit for bit, replay after replay, with eager work in between."""
