@@ -337,9 +337,10 @@ static RangeWork range_work(const CoreRanges &cr, const opattr_dims *d, void *ws
 // pair, finds where they begin in each run along the merge path (a search on
 // the diagonal, 64 probes per step across a wave), stages the two slices in
 // LDS and places every record by its rank in the other slice (binary
-// searches, a thread's records searched together). The index makes the order strict,
-// so no two records compare equal. The last pass writes the sorted start,
-// end, stream and index and gathers the operator and kind by the index.
+// searches, a thread's records searched together). The index makes the
+// order strict, so no two records compare equal. The last pass writes the
+// sorted start, end, stream and index and gathers the operator and kind by
+// the index.
 // ---------------------------------------------------------------------------
 constexpr int kRsTile = 1024, kRsThreads = 256, kRsPer = kRsTile / kRsThreads;
 constexpr int kRsSteps = 11;  // binary search steps over at most kRsTile records

@@ -133,6 +133,23 @@ def test_random_traces_with_ties(seed):
         parity.assert_attribute(out2, want2, diag2)
 
 
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_fused_path_random_times(seed):
+    """The fused path (stream-major launches with dense seq, ranges at most
+    one per 16 launches) on launches whose start times jump back and forth
+    along each stream: the enclosure searches from each block's range window
+    whatever the order of the query points."""
+    tr = cases.random_trace(9100 + seed, T=40_000 + 997 * seed, S=2 + seed, n_names=30,
+                            R=2000 + 100 * seed, n_ops=50, t_max=400_000, max_depth=5,
+                            dedup=seed == 1)
+    sm, _, _ = cases.stream_major(tr)
+    T, R = sm["seq"].size, sm["r_start"].size
+    assert R * 16 <= T
+    print(f"case fused random times seed={seed} T={T} R={R}", flush=True)
+    out, diag = _run(sm, flags=HINTS)
+    parity.assert_attribute(out, O.attribute(sm), diag)
+
+
 @pytest.mark.parametrize("R,S,t_max,nested,min_r", [(2049, 1, 300, True, 2049),
                                                     (6143, 3, 200, False, 6143),
                                                     (9001, 2, 40, False, 9001),
