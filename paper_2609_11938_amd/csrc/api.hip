@@ -41,8 +41,15 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   // a matching stage (profiled rows given) and few streams and names (under
   // OPATTR_VALIDATE both promises are checked beside it: the layout by
   // check_kernel_layout, the density by the launch-order view's scatter)
-  pl.seg = (d->flags & OPATTR_KERNELS_STREAM_MAJOR) && pl.seq_dense && p != nullptr &&
-           pl.NS >= 1 && pl.NS <= 64 && pl.NN <= kFastNames;
+  const bool seg_ok = pl.seq_dense && p != nullptr && pl.NS >= 1 && pl.NS <= 64 &&
+                      pl.NN <= kFastNames;
+  const bool sm_hint = (d->flags & OPATTR_KERNELS_STREAM_MAJOR) != 0;
+  // dense seq in another order: opattr_attribute permutes the launches into
+  // stream-major order when the fused path would then take them (not under
+  // OPATTR_VALIDATE, which checks the caller's layout as given)
+  const bool remap_ok = !sm_hint && seg_ok && !(d->flags & OPATTR_VALIDATE) && !second_match &&
+                        r != nullptr && pl.G <= kFusedMaxRows && pl.R * 16 <= pl.T && pl.T > 0;
+  pl.seg = (sm_hint || remap_ok) && seg_ok;  // sizes; reset below for the remapped case
   pl.nt = (pl.T + OPA_TILE - 1) / OPA_TILE;
   pl.ntp = (pl.P + OPA_TILE - 1) / OPA_TILE;
   pl.ncht = (pl.nt + kColChunk - 1) / kColChunk;
@@ -186,6 +193,21 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
     pl.slot2 = b.take(P * 4);
     pl.nbs2 = b.take(T * 4);
   }
+  pl.remap = remap_ok && pl.fused;
+  if (pl.remap) {
+    pl.rm_hist = b.take(remap_hist_entries(pl) * 4);
+    pl.rm_perm = b.take(T * 4);
+    pl.rm_seq = b.take(T * 4);
+    pl.rm_name = b.take(T * 4);
+    pl.rm_dur = b.take(T * 4);
+    pl.rm_st = b.take(T * 2);
+    pl.rm_start = b.take(T * 8);
+    pl.rm_query = b.take(k->query_ns ? T * 8 : 0);
+    pl.rm_part = b.take(k->part_id ? T * 4 : 0);
+    pl.rm_match = b.take(T * 4);
+    pl.rm_rid = b.take(T * 4);
+  }
+  if (!sm_hint) pl.seg = pl.fused = false;  // the launches as given
   pl.total = b.off;
   return pl;
 }
@@ -627,6 +649,29 @@ static bool attribute_args_ok(const opattr_kernels *k, const opattr_profiled *p,
          kinds_ok(agg_kind) && (k->n == 0 || (match && range_id));
 }
 
+// opattr_attribute on dense seq given in another order: the launches
+// permuted into stream-major order (through the launch-order view), the
+// fused path on them, and the per-launch outputs permuted back.
+static int attribute_remapped(const opattr_kernels *k, const opattr_profiled *p,
+                              const opattr_ranges *r, const opattr_dims *d, int policy,
+                              const uint8_t *agg_kind, int32_t *match, int32_t *range_id,
+                              uint8_t *range_depth, uint32_t *name_counts, opattr_op_row *table,
+                              opattr_summary *sum, opattr_diag *diag, void *ws, const Plan &pl,
+                              hipStream_t s, bool fork) {
+  build_seq_view(k, d, ws, pl, diag, false, s);
+  opattr_kernels k2;
+  remap_launches(k, d, ws, pl, &k2, s);
+  opattr_dims d2 = *d;
+  d2.flags |= OPATTR_KERNELS_STREAM_MAJOR;
+  Plan pf = pl;
+  pf.seg = pf.fused = true;
+  attribute_fused(&k2, p, r, &d2, policy, agg_kind, at<int32_t>(ws, pl.rm_match),
+                  at<int32_t>(ws, pl.rm_rid), range_depth, name_counts, table, sum, diag, ws, pf,
+                  s, fork);
+  remap_back(ws, pl, match, range_id, s);
+  return launch_status();
+}
+
 // The four stages on a checked plan and workspace; with fork, independent
 // stages run on this thread's side streams, else all on the caller's stream.
 static int attribute_call(const opattr_kernels *k, const opattr_profiled *p,
@@ -635,6 +680,9 @@ static int attribute_call(const opattr_kernels *k, const opattr_profiled *p,
                           uint8_t *range_depth, uint32_t *name_counts, opattr_op_row *table,
                           opattr_summary *sum, opattr_diag *diag, void *ws, const Plan &pl,
                           hipStream_t s, bool fork) {
+  if (pl.remap) return attribute_remapped(k, p, r, d, policy, agg_kind, match, range_id,
+                                          range_depth, name_counts, table, sum, diag, ws, pl, s,
+                                          fork);
   if (pl.fused) return attribute_fused(k, p, r, d, policy, agg_kind, match, range_id,
                                        range_depth, name_counts, table, sum, diag, ws, pl, s,
                                        fork);

@@ -35,6 +35,13 @@ struct Plan {
   int64_t nt, ntp, ncht, nchp, ntr_max, nencb, ntrt, nchr;
   bool seq_dense, ranges_nested;
   bool seg;  // seq tiles read from per-stream segments (kernels stream-major, seq dense)
+  // opattr_attribute on dense seq in another order: the launches permuted
+  // into stream-major order first, then the fused path (the sizes below and
+  // the segment path's are taken; seg and fused stay false for the other
+  // entry points, which read the launches as given)
+  bool remap;
+  size_t rm_hist, rm_perm, rm_seq, rm_name, rm_dur, rm_st, rm_start, rm_query, rm_part, rm_match,
+      rm_rid;
   size_t total;
   // IOM
   size_t sv, rk, seqsort_k0, seqsort_k1, seqsort_v0, seqsort_v1, rs_hist, kblk, tbnd;
@@ -189,6 +196,17 @@ struct IomArgs {
 void build_seq_view(const opattr_kernels *k, const opattr_dims *d, void *ws, const Plan &pl,
                     opattr_diag *diag, bool validate, hipStream_t s);
 void run_match(const IomArgs &a, hipStream_t s);
+// the launches of a remapped call in stream-major order (the launch-order
+// view must be built): the permutation and the permuted arrays into the
+// plan's rm_* regions; *out gets the arrays
+void remap_launches(const opattr_kernels *k, const opattr_dims *d, void *ws, const Plan &pl,
+                    opattr_kernels *out, hipStream_t s);
+size_t remap_hist_entries(const Plan &pl);
+// exclusive scan of a[0, n) in place; scratch holds scan_scratch_entries(n)
+void scan_excl_inplace(uint32_t *a, int64_t n, uint32_t *scratch, hipStream_t s);
+size_t scan_scratch_entries(int64_t n);
+// match and range_id of the permuted launches back to the caller's order
+void remap_back(void *ws, const Plan &pl, int32_t *match, int32_t *range_id, hipStream_t s);
 // OPATTR_VALIDATE: check the kernels' stream-major promise (if given)
 void check_kernel_layout(const opattr_kernels *k, const opattr_dims *d, opattr_diag *diag,
                          hipStream_t s);

@@ -1200,6 +1200,181 @@ __global__ void __launch_bounds__(1024) k_pf_off(const uint32_t *__restrict__ pf
 }
 
 
+// ---------------------------------------------------------------------------
+// Stream-major order for launches with dense seq given in another order
+// (opattr_attribute): a stable counting sort by stream of the launch-order
+// view, one 4096-rank tile of it per block, that also gathers the launch
+// arrays into that order. Launches with a stream id past the last stream
+// sort after all others (the fused path counts them as bad records); seq
+// ranks no launch claims (a false density promise) leave slots at the end,
+// filled with records the fused path leaves out.
+// ---------------------------------------------------------------------------
+struct RemapArgs {
+  const int32_t *sv;
+  int64_t T, nt;
+  uint32_t NS, NN;
+  const uint32_t *seq, *name, *dur;
+  const uint16_t *st;
+  const uint64_t *start, *query;
+  const int32_t *part;
+  uint32_t *hist;  // [(NS + 1) * nt + 1], then its scan scratch
+  int32_t *perm;
+  uint32_t *seq2, *name2, *dur2;
+  uint16_t *st2;
+  uint64_t *start2, *query2;
+  int32_t *part2;
+};
+
+// the group of the launch at seq rank j: its stream, NS past the last
+// stream, -1 when no launch holds the rank
+__device__ __forceinline__ int remap_group(const RemapArgs &a, int64_t j, int32_t &i) {
+  i = j < a.T ? a.sv[j] : -1;
+  if (i < 0) return -1;
+  const uint32_t s = a.st[i];
+  return (int)(s < a.NS ? s : a.NS);
+}
+
+__global__ void __launch_bounds__(256) k_remap_hist(RemapArgs a) {
+  __shared__ uint32_t c[kMaxSegStreams + 1];
+  const int tid = threadIdx.x;
+  if (tid <= (int)a.NS) c[tid] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
+  for (int e = tid; e < OPA_TILE; e += 256) {
+    int32_t i;
+    const int g = remap_group(a, base + e, i);
+    if (g >= 0) atomicAdd(&c[g], 1u);
+  }
+  __syncthreads();
+  if (tid <= (int)a.NS) a.hist[(int64_t)tid * a.nt + blockIdx.x] = c[tid];
+  if (blockIdx.x == 0 && tid == 0) a.hist[(int64_t)(a.NS + 1) * a.nt] = 0;  // the total, after the scan
+}
+
+__global__ void __launch_bounds__(256) k_remap_scatter(RemapArgs a) {
+  __shared__ uint16_t cnt[OPA_TILE_CHUNKS][4][kMaxSegStreams + 1];
+  const int tid = threadIdx.x, w = wave_id();
+  const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
+  const int ng = (int)a.NS + 1;
+  for (int q = tid; q < OPA_TILE_CHUNKS * 4 * (kMaxSegStreams + 1); q += 256)
+    (&cnt[0][0][0])[q] = 0;
+  __syncthreads();
+  int32_t ii[OPA_TILE_CHUNKS];
+  uint32_t lr[OPA_TILE_CHUNKS];
+  int gg[OPA_TILE_CHUNKS];
+#pragma unroll
+  for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
+    const int g = remap_group(a, base + c * 256 + tid, ii[c]);
+    gg[c] = g;
+    const uint64_t pm = peers8((uint32_t)(g >= 0 ? g : 255)) & __ballot(g >= 0);
+    lr[c] = (uint32_t)__popcll(pm & lanemask_lt());
+    if (g >= 0 && (pm & lanemask_lt()) == 0) cnt[c][w][g] = (uint16_t)__popcll(pm);
+  }
+  __syncthreads();
+  if (tid < ng) {  // thread g: its group's counts over (chunk, wave), in rank order
+    uint32_t run = 0;
+    for (int c = 0; c < OPA_TILE_CHUNKS; ++c)
+      for (int ww = 0; ww < 4; ++ww) {
+        const uint32_t v = cnt[c][ww][tid];
+        cnt[c][ww][tid] = (uint16_t)run;
+        run += v;
+      }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
+    const int g = gg[c];
+    if (g < 0) continue;
+    const int32_t i = ii[c];
+    const int64_t dst = (int64_t)a.hist[(int64_t)g * a.nt + blockIdx.x] + cnt[c][w][g] + lr[c];
+    a.perm[dst] = i;
+    a.seq2[dst] = a.seq[i];
+    a.name2[dst] = a.name[i];
+    a.dur2[dst] = a.dur[i];
+    a.st2[dst] = a.st[i];
+    a.start2[dst] = a.start[i];
+    if (a.query2) a.query2[dst] = a.query[i];
+    if (a.part2) a.part2[dst] = a.part[i];
+  }
+}
+
+// slots past the placed launches: records the fused path leaves out (seq
+// past n, stream and name out of range)
+__global__ void k_remap_tail(RemapArgs a) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t placed = a.hist[(int64_t)(a.NS + 1) * a.nt];
+  if (x >= a.T || x < placed) return;
+  a.perm[x] = -1;
+  a.seq2[x] = (uint32_t)(a.T + (x - placed) < 0xFFFFFFFFll ? a.T + (x - placed) : 0xFFFFFFFFll);
+  a.name2[x] = a.NN;
+  a.dur2[x] = 0;
+  a.st2[x] = 0xFFFFu;
+  a.start2[x] = ~0ull;
+  if (a.query2) a.query2[x] = ~0ull;
+  if (a.part2) a.part2[x] = -1;
+}
+
+size_t remap_hist_entries(const Plan &pl) {
+  const int64_t h = ((int64_t)pl.NS + 1) * pl.nt + 1;
+  return (size_t)h + scan_scratch_entries(h);
+}
+
+void remap_launches(const opattr_kernels *k, const opattr_dims *d, void *ws, const Plan &pl,
+                    opattr_kernels *out, hipStream_t s) {
+  RemapArgs a{};
+  a.sv = at<int32_t>(ws, pl.sv);
+  a.T = pl.T;
+  a.nt = pl.nt;
+  a.NS = d->n_streams;
+  a.NN = d->n_names;
+  a.seq = k->seq;
+  a.name = k->name_id;
+  a.dur = k->dur_ns;
+  a.st = k->stream_id;
+  a.start = k->start_ns;
+  a.query = k->query_ns;
+  a.part = k->part_id;
+  a.hist = at<uint32_t>(ws, pl.rm_hist);
+  a.perm = at<int32_t>(ws, pl.rm_perm);
+  a.seq2 = at<uint32_t>(ws, pl.rm_seq);
+  a.name2 = at<uint32_t>(ws, pl.rm_name);
+  a.dur2 = at<uint32_t>(ws, pl.rm_dur);
+  a.st2 = at<uint16_t>(ws, pl.rm_st);
+  a.start2 = at<uint64_t>(ws, pl.rm_start);
+  a.query2 = k->query_ns ? at<uint64_t>(ws, pl.rm_query) : nullptr;
+  a.part2 = k->part_id ? at<int32_t>(ws, pl.rm_part) : nullptr;
+  *out = *k;
+  out->seq = a.seq2;
+  out->name_id = a.name2;
+  out->dur_ns = a.dur2;
+  out->stream_id = a.st2;
+  out->start_ns = a.start2;
+  out->query_ns = a.query2;
+  out->part_id = a.part2;
+  if (pl.T <= 0) return;
+  const int64_t h = ((int64_t)a.NS + 1) * a.nt + 1;
+  k_remap_hist<<<(unsigned)a.nt, 256, 0, s>>>(a);
+  scan_excl_inplace(a.hist, h, a.hist + h, s);
+  k_remap_scatter<<<(unsigned)a.nt, 256, 0, s>>>(a);
+  k_remap_tail<<<(unsigned)((a.T + 255) / 256), 256, 0, s>>>(a);
+}
+
+__global__ void k_remap_back(const int32_t *perm, const int32_t *m2, const int32_t *r2, int64_t T,
+                             int32_t *match, int32_t *range_id) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= T) return;
+  const int32_t i = perm[x];
+  if (i < 0) return;
+  match[i] = m2[x];
+  range_id[i] = r2[x];
+}
+
+void remap_back(void *ws, const Plan &pl, int32_t *match, int32_t *range_id, hipStream_t s) {
+  if (pl.T > 0)
+    k_remap_back<<<(unsigned)((pl.T + 255) / 256), 256, 0, s>>>(
+        at<int32_t>(ws, pl.rm_perm), at<int32_t>(ws, pl.rm_match), at<int32_t>(ws, pl.rm_rid), pl.T,
+        match, range_id);
+}
+
 // Layout promise of the kernels (checked under OPATTR_VALIDATE): sorted by
 // (stream, seq) with seq unique, streams below n_streams, query points not
 // decreasing along a stream.

@@ -85,12 +85,16 @@ def test_workspace_size_is_pure_and_monotone(lib):
         sizes.append(lib.opattr_workspace_bytes(C.byref(k), C.byref(p), C.byref(r), C.byref(d)))
     assert all(s > 0 for s in sizes)
     assert sizes == sorted(sizes)
-    # hints drop the reordering buffers
+    # all hints drop the reordering buffers; dense seq in another order adds
+    # the permuted launch arrays of opattr_attribute (about 34 B per launch)
     k, p, r, d = _structs(T=100_000, R=5_000)
     full = lib.opattr_workspace_bytes(C.byref(k), C.byref(p), C.byref(r), C.byref(d))
-    d.flags = opattr.SEQ_DENSE | opattr.RANGES_NESTED
+    d.flags = opattr.KERNELS_STREAM_MAJOR | opattr.SEQ_DENSE | opattr.RANGES_NESTED
     hinted = lib.opattr_workspace_bytes(C.byref(k), C.byref(p), C.byref(r), C.byref(d))
     assert hinted < full
+    d.flags = opattr.SEQ_DENSE | opattr.RANGES_NESTED
+    permuted = lib.opattr_workspace_bytes(C.byref(k), C.byref(p), C.byref(r), C.byref(d))
+    assert permuted >= hinted + 100_000 * 34
     assert lib.opattr_workspace_bytes(C.byref(k), C.byref(p), C.byref(r), None) == 0
 
 

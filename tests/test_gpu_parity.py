@@ -150,6 +150,47 @@ def test_fused_path_random_times(seed):
     parity.assert_attribute(out, O.attribute(sm), diag)
 
 
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_dense_seq_in_any_order(seed):
+    """Launches in random storage order with seq promised dense (and ranges
+    at most one per 16 launches): opattr_attribute permutes them into
+    stream-major order through the launch-order view, runs the fused path and
+    permutes match and range_id back."""
+    tr = cases.random_trace(9300 + seed, T=40_000 + 1013 * seed, S=2 + 2 * seed, n_names=40,
+                            R=2000 + 90 * seed, n_ops=60, t_max=400_000, max_depth=5,
+                            dedup=seed != 1, drop=0.1 if seed == 2 else 0.0)
+    T, R = tr["seq"].size, tr["r_start"].size
+    assert R * 16 <= T
+    print(f"case dense seq any order seed={seed} T={T} R={R}", flush=True)
+    out, diag = _run(tr, flags=opattr.SEQ_DENSE)
+    parity.assert_attribute(out, O.attribute(tr), diag)
+
+
+@pytest.mark.parametrize("kind", ["shared_seq", "bad_stream"])
+def test_dense_seq_any_order_broken(kind):
+    """The permuted path on a false density promise (one seq value on two
+    launches) stays within its buffers; a launch on a stream past the last
+    one is counted as a bad record, as on the other paths."""
+    import numpy as np
+
+    tr = dict(cases.random_trace(9400, T=30_000, S=3, n_names=20, R=1500, n_ops=30,
+                                 t_max=300_000, max_depth=4))
+    if kind == "shared_seq":
+        seq = tr["seq"].copy()
+        seq[int(np.argmax(seq == 7))] = 8
+        tr["seq"] = seq
+    else:
+        st = tr["stream_id"].copy()
+        st[123] = 3  # n_streams is 3
+        tr["stream_id"] = st
+    print(f"case dense seq any order broken kind={kind}", flush=True)
+    out, diag = _run(tr, flags=opattr.SEQ_DENSE)
+    if kind == "bad_stream":
+        assert diag["bad_records"] >= 1 and diag["status"] == -9
+    else:
+        assert diag["status"] <= 0  # any status: the outputs are unspecified
+
+
 @pytest.mark.parametrize("R,S,t_max,nested,min_r", [(2049, 1, 300, True, 2049),
                                                     (6143, 3, 200, False, 6143),
                                                     (9001, 2, 40, False, 9001),
