@@ -197,6 +197,7 @@ Plan make_plan(const opattr_kernels *k, const opattr_profiled *p, const opattr_r
   if (pl.remap) {
     pl.rm_hist = b.take(remap_hist_entries(pl) * 4);
     pl.rm_perm = b.take(T * 4);
+    pl.rm_inv = b.take(T * 4);
     pl.rm_seq = b.take(T * 4);
     pl.rm_name = b.take(T * 4);
     pl.rm_dur = b.take(T * 4);

@@ -40,7 +40,7 @@ struct Plan {
   // the segment path's are taken; seg and fused stay false for the other
   // entry points, which read the launches as given)
   bool remap;
-  size_t rm_hist, rm_perm, rm_seq, rm_name, rm_dur, rm_st, rm_start, rm_query, rm_part, rm_match,
+  size_t rm_hist, rm_perm, rm_inv, rm_seq, rm_name, rm_dur, rm_st, rm_start, rm_query, rm_part, rm_match,
       rm_rid;
   size_t total;
   // IOM

@@ -1218,7 +1218,8 @@ struct RemapArgs {
   const uint64_t *start, *query;
   const int32_t *part;
   uint32_t *hist;  // [(NS + 1) * nt + 1], then its scan scratch
-  int32_t *perm;
+  int32_t *perm;  // slot -> launch (-1 past the placed ones)
+  int32_t *inv;   // launch -> slot (-1 for a launch no seq rank holds)
   uint32_t *seq2, *name2, *dur2;
   uint16_t *st2;
   uint64_t *start2, *query2;
@@ -1252,6 +1253,9 @@ __global__ void __launch_bounds__(256) k_remap_hist(RemapArgs a) {
 
 __global__ void __launch_bounds__(256) k_remap_scatter(RemapArgs a) {
   __shared__ uint16_t cnt[OPA_TILE_CHUNKS][4][kMaxSegStreams + 1];
+  __shared__ int32_t lidx[OPA_TILE];  // the tile's launches in (group, rank) order
+  __shared__ uint8_t lgrp[OPA_TILE];
+  __shared__ uint32_t lbase[kMaxSegStreams + 1], sh[4];
   const int tid = threadIdx.x, w = wave_id();
   const int64_t base = (int64_t)blockIdx.x * OPA_TILE;
   const int ng = (int)a.NS + 1;
@@ -1270,22 +1274,34 @@ __global__ void __launch_bounds__(256) k_remap_scatter(RemapArgs a) {
     if (g >= 0 && (pm & lanemask_lt()) == 0) cnt[c][w][g] = (uint16_t)__popcll(pm);
   }
   __syncthreads();
-  if (tid < ng) {  // thread g: its group's counts over (chunk, wave), in rank order
-    uint32_t run = 0;
+  uint32_t tot = 0;  // thread g: its group's counts over (chunk, wave), in rank order
+  if (tid < ng)
     for (int c = 0; c < OPA_TILE_CHUNKS; ++c)
       for (int ww = 0; ww < 4; ++ww) {
         const uint32_t v = cnt[c][ww][tid];
-        cnt[c][ww][tid] = (uint16_t)run;
-        run += v;
+        cnt[c][ww][tid] = (uint16_t)tot;
+        tot += v;
       }
-  }
+  uint32_t nl;
+  const uint32_t lb = block_excl_scan_add<uint32_t>(tid < ng ? tot : 0u, sh, &nl);
+  if (tid < ng) lbase[tid] = lb;
   __syncthreads();
+  // each launch's place: in the tile's LDS order, and its final one (inv)
 #pragma unroll
   for (int c = 0; c < OPA_TILE_CHUNKS; ++c) {
     const int g = gg[c];
     if (g < 0) continue;
-    const int32_t i = ii[c];
-    const int64_t dst = (int64_t)a.hist[(int64_t)g * a.nt + blockIdx.x] + cnt[c][w][g] + lr[c];
+    const uint32_t r = cnt[c][w][g] + lr[c];
+    lidx[lbase[g] + r] = ii[c];
+    lgrp[lbase[g] + r] = (uint8_t)g;
+    a.inv[ii[c]] = (int32_t)(a.hist[(int64_t)g * a.nt + blockIdx.x] + r);
+  }
+  __syncthreads();
+  // written in that order: each group's launches go to consecutive slots
+  for (int j = tid; j < (int)nl; j += 256) {
+    const int32_t i = lidx[j];
+    const int g = lgrp[j];
+    const int64_t dst = (int64_t)a.hist[(int64_t)g * a.nt + blockIdx.x] + (j - (int)lbase[g]);
     a.perm[dst] = i;
     a.seq2[dst] = a.seq[i];
     a.name2[dst] = a.name[i];
@@ -1335,6 +1351,7 @@ void remap_launches(const opattr_kernels *k, const opattr_dims *d, void *ws, con
   a.part = k->part_id;
   a.hist = at<uint32_t>(ws, pl.rm_hist);
   a.perm = at<int32_t>(ws, pl.rm_perm);
+  a.inv = at<int32_t>(ws, pl.rm_inv);
   a.seq2 = at<uint32_t>(ws, pl.rm_seq);
   a.name2 = at<uint32_t>(ws, pl.rm_name);
   a.dur2 = at<uint32_t>(ws, pl.rm_dur);
@@ -1352,18 +1369,20 @@ void remap_launches(const opattr_kernels *k, const opattr_dims *d, void *ws, con
   out->part_id = a.part2;
   if (pl.T <= 0) return;
   const int64_t h = ((int64_t)a.NS + 1) * a.nt + 1;
+  fill_u32(reinterpret_cast<uint32_t *>(a.inv), 0xFFFFFFFFu, a.T, s);
   k_remap_hist<<<(unsigned)a.nt, 256, 0, s>>>(a);
   scan_excl_inplace(a.hist, h, a.hist + h, s);
   k_remap_scatter<<<(unsigned)a.nt, 256, 0, s>>>(a);
   k_remap_tail<<<(unsigned)((a.T + 255) / 256), 256, 0, s>>>(a);
 }
 
-__global__ void k_remap_back(const int32_t *perm, const int32_t *m2, const int32_t *r2, int64_t T,
+// by launch, so that the caller's arrays are written in order
+__global__ void k_remap_back(const int32_t *inv, const int32_t *m2, const int32_t *r2, int64_t T,
                              int32_t *match, int32_t *range_id) {
-  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (x >= T) return;
-  const int32_t i = perm[x];
-  if (i < 0) return;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= T) return;
+  const int32_t x = inv[i];
+  if (x < 0) return;  // no seq rank holds the launch (a false density promise)
   match[i] = m2[x];
   range_id[i] = r2[x];
 }
@@ -1371,7 +1390,7 @@ __global__ void k_remap_back(const int32_t *perm, const int32_t *m2, const int32
 void remap_back(void *ws, const Plan &pl, int32_t *match, int32_t *range_id, hipStream_t s) {
   if (pl.T > 0)
     k_remap_back<<<(unsigned)((pl.T + 255) / 256), 256, 0, s>>>(
-        at<int32_t>(ws, pl.rm_perm), at<int32_t>(ws, pl.rm_match), at<int32_t>(ws, pl.rm_rid), pl.T,
+        at<int32_t>(ws, pl.rm_inv), at<int32_t>(ws, pl.rm_match), at<int32_t>(ws, pl.rm_rid), pl.T,
         match, range_id);
 }
 
