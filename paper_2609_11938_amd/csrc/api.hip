@@ -572,7 +572,7 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
                            const uint8_t *agg_kind, int32_t *match, int32_t *range_id,
                            uint8_t *range_depth, uint32_t *name_counts, opattr_op_row *table,
                            opattr_summary *sum, opattr_diag *diag, void *ws, const Plan &pl,
-                           hipStream_t s, bool fork) {
+                           hipStream_t s, bool fork, const opattr_kernels *k_given = nullptr) {
   SideStream *ss = fork ? side_stream() : nullptr;
   const hipStream_t s2 = ss ? ss->s : s;
   if (ss) {
@@ -594,6 +594,18 @@ static int attribute_fused(const opattr_kernels *k, const opattr_profiled *p,
   const CoreRanges cr = prepare_ranges(r, d, ws, pl, diag, validate, s2, &acc);
   resolve_ranges(cr, d, ws, pl, range_depth, diag, s2, true);
   probe_end(OPATTR_PROBE_RANGES, s2);
+  if (k_given) {
+    // the launches given in another order: permuted (into k's arrays) on the
+    // caller's stream while the ranges are sorted; the enclosure waits
+    Plan pv = pl;
+    pv.seg = false;  // the view is built here (the segment path reads none)
+    build_seq_view(k_given, d, ws, pv, diag, false, s);
+    remap_launches(k_given, d, ws, pl, nullptr, s);
+    if (ss) {
+      note(hipEventRecord(ss->join3, s));
+      note(hipStreamWaitEvent(s2, ss->join3, 0));
+    }
+  }
   EncArgs e{};
   e.k = k;
   e.p = p;
@@ -659,16 +671,15 @@ static int attribute_remapped(const opattr_kernels *k, const opattr_profiled *p,
                               uint8_t *range_depth, uint32_t *name_counts, opattr_op_row *table,
                               opattr_summary *sum, opattr_diag *diag, void *ws, const Plan &pl,
                               hipStream_t s, bool fork) {
-  build_seq_view(k, d, ws, pl, diag, false, s);
   opattr_kernels k2;
-  remap_launches(k, d, ws, pl, &k2, s);
+  remap_view(k, ws, pl, &k2);
   opattr_dims d2 = *d;
   d2.flags |= OPATTR_KERNELS_STREAM_MAJOR;
   Plan pf = pl;
   pf.seg = pf.fused = true;
   attribute_fused(&k2, p, r, &d2, policy, agg_kind, at<int32_t>(ws, pl.rm_match),
                   at<int32_t>(ws, pl.rm_rid), range_depth, name_counts, table, sum, diag, ws, pf,
-                  s, fork);
+                  s, fork, k);
   remap_back(ws, pl, match, range_id, s);
   return launch_status();
 }

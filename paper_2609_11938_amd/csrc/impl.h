@@ -202,6 +202,8 @@ void run_match(const IomArgs &a, hipStream_t s);
 void remap_launches(const opattr_kernels *k, const opattr_dims *d, void *ws, const Plan &pl,
                     opattr_kernels *out, hipStream_t s);
 size_t remap_hist_entries(const Plan &pl);
+// the permuted launch arrays' addresses (host only)
+void remap_view(const opattr_kernels *k, void *ws, const Plan &pl, opattr_kernels *out);
 // exclusive scan of a[0, n) in place; scratch holds scan_scratch_entries(n)
 void scan_excl_inplace(uint32_t *a, int64_t n, uint32_t *scratch, hipStream_t s);
 size_t scan_scratch_entries(int64_t n);

@@ -1329,6 +1329,17 @@ __global__ void k_remap_tail(RemapArgs a) {
   if (a.part2) a.part2[x] = -1;
 }
 
+void remap_view(const opattr_kernels *k, void *ws, const Plan &pl, opattr_kernels *out) {
+  *out = *k;
+  out->seq = at<uint32_t>(ws, pl.rm_seq);
+  out->name_id = at<uint32_t>(ws, pl.rm_name);
+  out->dur_ns = at<uint32_t>(ws, pl.rm_dur);
+  out->stream_id = at<uint16_t>(ws, pl.rm_st);
+  out->start_ns = at<uint64_t>(ws, pl.rm_start);
+  out->query_ns = k->query_ns ? at<uint64_t>(ws, pl.rm_query) : nullptr;
+  out->part_id = k->part_id ? at<int32_t>(ws, pl.rm_part) : nullptr;
+}
+
 size_t remap_hist_entries(const Plan &pl) {
   const int64_t h = ((int64_t)pl.NS + 1) * pl.nt + 1;
   return (size_t)h + scan_scratch_entries(h);
@@ -1359,14 +1370,7 @@ void remap_launches(const opattr_kernels *k, const opattr_dims *d, void *ws, con
   a.start2 = at<uint64_t>(ws, pl.rm_start);
   a.query2 = k->query_ns ? at<uint64_t>(ws, pl.rm_query) : nullptr;
   a.part2 = k->part_id ? at<int32_t>(ws, pl.rm_part) : nullptr;
-  *out = *k;
-  out->seq = a.seq2;
-  out->name_id = a.name2;
-  out->dur_ns = a.dur2;
-  out->stream_id = a.st2;
-  out->start_ns = a.start2;
-  out->query_ns = a.query2;
-  out->part_id = a.part2;
+  if (out) remap_view(k, ws, pl, out);
   if (pl.T <= 0) return;
   const int64_t h = ((int64_t)a.NS + 1) * a.nt + 1;
   fill_u32(reinterpret_cast<uint32_t *>(a.inv), 0xFFFFFFFFu, a.T, s);
